@@ -1,0 +1,334 @@
+"""Plain, slow, float64 CPU oracle of the PQ-HSA decode-attention operator.
+
+TEST INFRASTRUCTURE ONLY. This module is the reference that the HIP path is
+checked against. Only the test suite, the package smoke check and the CPU
+baseline leg of the benchmark may import it; the product path never calls it
+and shares no code with it (no kernels, headers, tables or helpers).
+
+Everything is written from the paper's statement of the method:
+
+* Section 3 (opening paragraph), Eq. (1): dense decode attention and the
+  exact/background decomposition y = (N_E + N_B) / (Z_E + Z_B).
+* Section 3.1, Eq. (2): direction-norm residual IVF-PQ score of an indexed
+  key, computed from a per-query lookup table (LUT) over the M subspaces plus
+  the coarse term u_q . c_{a_i}.
+* Section 3.2, Eq. (3): partition into sink prefix S, local window L and
+  indexed region R; top-k selection T over R; E = S u L u T, B = R \\ T.
+* Section 3.2, Eq. (4): per-list background masses M_j over B n R_j and the
+  list value means; Eq. (5): the output.
+* Appendix A ("Budgets"): 4 sinks, a 128-token local window, k = ceil(rho |R|)
+  and the exact-set size rounded up to whole pages of 16 tokens.
+* Appendix B (variant definitions, Table "mechanism variants"): variants T
+  (no background), C (token-weighted global value mean) and Bx (mean of the
+  unselected members of each list).
+
+Readings where the paper is silent (all listed in the design doc):
+* the top-k tie-break is the smaller token id;
+* r_q = 0 gives a score of 0 for every indexed token;
+* an empty list, or a list whose members are all selected, contributes 0.
+
+Parity pins for every function live in tests/test_oracle_pins.py (brute force,
+closed forms, special cases). No function here is "parity unpinned".
+"""
+
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+
+import numpy as np
+
+__all__ = [
+    "budget_paper",
+    "split_positions",
+    "lut_ref",
+    "pq_scores_ref",
+    "topk_ref",
+    "dense_attention_ref",
+    "list_means_ref",
+    "pqhsa_row_ref",
+    "pqhsa_batch_ref",
+    "RowResult",
+]
+
+
+# ---------------------------------------------------------------------------
+# Budget rule (Appendix A, "Budgets"; Section 3.2 for k = ceil(rho |R|)).
+# ---------------------------------------------------------------------------
+def budget_paper(n_ctx: int, rho: float, n_sink: int = 4, n_local: int = 128,
+                 page: int = 16) -> tuple[int, int]:
+    """Return (k, exact-set size rounded up to whole pages).
+
+    |R| = n_ctx - n_sink - n_local, k = ceil(rho |R|) (Section 3.2), and the
+    exact set S u L u T has n_sink + n_local + k tokens, rounded up to a
+    multiple of `page` tokens (Appendix A).
+    """
+    n_r = n_ctx - n_sink - n_local
+    if n_r < 0:
+        raise ValueError("context shorter than sink + local window")
+    # ceil of a decimal fraction without binary round-up surprises
+    k = int(math.ceil(round(rho * n_r, 9)))
+    exact = n_sink + n_local + k
+    rounded = -(-exact // page) * page
+    return k, rounded
+
+
+def split_positions(n_seq: int, n_sink: int, n_local: int):
+    """Sink prefix S, local window L and indexed region R (Section 3.2).
+
+    S = [0, n_sink), L = [n_seq - n_local, n_seq), R = the positions between.
+    """
+    if n_seq < n_sink + n_local:
+        raise ValueError("n_seq must be at least n_sink + n_local")
+    S = np.arange(0, n_sink)
+    L = np.arange(n_seq - n_local, n_seq)
+    R = np.arange(n_sink, n_seq - n_local)
+    return S, L, R
+
+
+# ---------------------------------------------------------------------------
+# Eq. (2): LUT and approximate logits.
+# ---------------------------------------------------------------------------
+def lut_ref(q: np.ndarray, centroids: np.ndarray, codebooks: np.ndarray):
+    """Query norm, coarse table and fine LUT of Eq. (2).
+
+    q [d]; centroids [n_list, d]; codebooks [M, ksub, d/M].
+    Returns r_q = ||q||, coarse[j] = u_q . c_j and fine[m, z] = u_q^(m) . p_{m,z}
+    where u_q = q / r_q and u_q^(m) is the m-th contiguous sub-vector of u_q.
+    """
+    q = np.asarray(q, dtype=np.float64)
+    d = q.shape[0]
+    n_m, ksub, dsub = codebooks.shape
+    if n_m * dsub != d:
+        raise ValueError("codebook subspaces do not tile the head dimension")
+    r_q = float(np.sqrt(np.sum(q * q)))
+    if r_q == 0.0:
+        # reading: a zero query has no direction; every PQ score is 0
+        return 0.0, np.zeros(centroids.shape[0]), np.zeros((n_m, ksub))
+    u_q = q / r_q
+    coarse = np.asarray(centroids, np.float64) @ u_q
+    fine = np.empty((n_m, ksub))
+    for m in range(n_m):
+        sub = u_q[m * dsub:(m + 1) * dsub]
+        fine[m] = np.asarray(codebooks[m], np.float64) @ sub
+    return r_q, coarse, fine
+
+
+def pq_scores_ref(q, list_ids, codes, norms, centroids, codebooks, positions):
+    """Approximate logits of Eq. (2) for the given token positions.
+
+    l~_i = (r_q r_i / sqrt(d)) (u_q . c_{a_i} + sum_m u_q^(m) . p_{m, z_im}),
+    evaluated as one LUT lookup per subspace. list_ids [N] (a_i), codes [N, M]
+    (z_im), norms [N] (r_i).
+    """
+    d = np.asarray(q).shape[0]
+    r_q, coarse, fine = lut_ref(q, centroids, codebooks)
+    positions = np.asarray(positions, dtype=np.int64)
+    a = np.asarray(list_ids)[positions].astype(np.int64)
+    z = np.asarray(codes)[positions].astype(np.int64)          # [n, M]
+    r = np.asarray(norms, np.float64)[positions]
+    n_m = fine.shape[0]
+    total = coarse[a].copy()
+    for m in range(n_m):
+        total += fine[m, z[:, m]]
+    return (r_q * r / math.sqrt(d)) * total
+
+
+def topk_ref(scores: np.ndarray, token_ids: np.ndarray, k: int):
+    """T = TopK_k over R (Eq. 3); ties go to the smaller token id.
+
+    Returns (selected token ids sorted ascending, tau = k-th largest score or
+    None when k = 0).
+    """
+    scores = np.asarray(scores, np.float64)
+    token_ids = np.asarray(token_ids, np.int64)
+    if not 0 <= k <= scores.shape[0]:
+        raise ValueError("k out of range")
+    order = np.lexsort((token_ids, -scores))   # primary: score desc; then id asc
+    chosen = order[:k]
+    tau = float(scores[order[k - 1]]) if k > 0 else None
+    return np.sort(token_ids[chosen]), tau
+
+
+# ---------------------------------------------------------------------------
+# Dense attention (Section 3, opening paragraph).
+# ---------------------------------------------------------------------------
+def dense_attention_ref(q, K, V, n_seq: int | None = None):
+    """y = sum_i e_i v_i / sum_i e_i with e_i = exp(q . k_i / sqrt(d))."""
+    q = np.asarray(q, np.float64)
+    K = np.asarray(K, np.float64)
+    V = np.asarray(V, np.float64)
+    if n_seq is not None:
+        K, V = K[:n_seq], V[:n_seq]
+    d = q.shape[0]
+    logits = K @ q / math.sqrt(d)
+    m0 = logits.max()
+    e = np.exp(logits - m0)
+    return (e @ V) / e.sum()
+
+
+def list_means_ref(V, list_ids, n_list: int, R: np.ndarray):
+    """v_bar_j = mean of v_i over R_j = {i in R : a_i = j} (Eq. 4); 0 if empty."""
+    V = np.asarray(V, np.float64)
+    a = np.asarray(list_ids)[R].astype(np.int64)
+    sums = np.zeros((n_list, V.shape[1]))
+    np.add.at(sums, a, V[R])
+    cnt = np.bincount(a, minlength=n_list).astype(np.float64)
+    means = np.zeros_like(sums)
+    nz = cnt > 0
+    means[nz] = sums[nz] / cnt[nz, None]
+    return means
+
+
+# ---------------------------------------------------------------------------
+# The operator, one query row (Section 3.2, Eqs. 3-5).
+# ---------------------------------------------------------------------------
+@dataclass
+class RowResult:
+    y: np.ndarray                 # output [d]
+    T: np.ndarray                 # selected token ids (sorted)
+    tau: float | None             # k-th largest approximate logit
+    scores: np.ndarray            # approximate logits over R (aligned with R)
+    R: np.ndarray                 # indexed token ids
+    m0: float                     # common shift
+    Z_E: float
+    Z_B: float
+    list_size: np.ndarray         # |R_j|
+    unselected_per_list: np.ndarray  # |B n R_j|
+    extra: dict = field(default_factory=dict)
+
+
+def pqhsa_row_ref(q, K, V, list_ids, codes, norms, centroids, codebooks,
+                  list_means, n_seq: int, n_sink: int, n_local: int, k: int,
+                  variant: str = "B", force_T=None) -> RowResult:
+    """PQ-HSA output for one query head against its KV head.
+
+    q [d]; K, V [>= n_seq, d]; list_ids [>= n_seq]; codes [>= n_seq, M];
+    norms [>= n_seq]; centroids [n_list, d]; codebooks [M, ksub, d/M];
+    list_means [n_list, d]. Index entries outside R are ignored.
+
+    variant: "B" (PQ-HSA, Eq. 5), "T" (background dropped), "C" (background
+    values = token-weighted global value mean over R), "Bx" (background values
+    = mean of the unselected members of each list, Appendix B).
+    force_T: evaluate Eqs. 3-5 with this selected set instead of the top-k.
+    """
+    q = np.asarray(q, np.float64)
+    d = q.shape[0]
+    n_list = centroids.shape[0]
+    S, L, R = split_positions(n_seq, n_sink, n_local)
+
+    # Eq. (2): one approximate logit per indexed token
+    scores = pq_scores_ref(q, list_ids, codes, norms, centroids, codebooks, R)
+
+    # Eq. (3): selection over R only
+    if force_T is None:
+        T, tau = topk_ref(scores, R, k)
+    else:
+        T = np.sort(np.asarray(force_T, np.int64))
+        if T.shape[0] != k or not np.all(np.isin(T, R)):
+            raise ValueError("force_T must hold k distinct indexed positions")
+        tau = None
+    in_T = np.isin(R, T)
+    B_ids = R[~in_T]
+    B_scores = scores[~in_T]
+    E_ids = np.concatenate([S, L, T]).astype(np.int64)
+
+    # exact logits replace the approximate ones on E
+    Kf = np.asarray(K, np.float64)
+    Vf = np.asarray(V, np.float64)
+    exact = Kf[E_ids] @ q / math.sqrt(d)
+
+    a_all = np.asarray(list_ids).astype(np.int64)
+    a_B = a_all[B_ids]
+    list_size = np.bincount(a_all[R], minlength=n_list)
+    unsel = np.bincount(a_B, minlength=n_list)
+
+    use_background = variant != "T"
+    # common shift: maximum over exact (E) and approximate (B) logits
+    cands = [exact.max()] if exact.size else []
+    if use_background and B_scores.size:
+        cands.append(B_scores.max())
+    m0 = float(max(cands)) if cands else 0.0
+
+    e_E = np.exp(exact - m0)
+    Z_E = float(e_E.sum())
+    N_E = e_E @ Vf[E_ids] if E_ids.size else np.zeros(d)
+
+    if use_background and B_ids.size:
+        e_B = np.exp(B_scores - m0)
+        # Eq. (4): M_j = sum of e~_i over B n R_j (0 for an empty list)
+        M = np.zeros(n_list)
+        np.add.at(M, a_B, e_B)
+        if variant == "B":
+            vbar = np.asarray(list_means, np.float64)
+        elif variant == "C":
+            glob = Vf[R].mean(axis=0) if R.size else np.zeros(d)
+            vbar = np.broadcast_to(glob, (n_list, d))
+        elif variant == "Bx":
+            lm = np.asarray(list_means, np.float64)
+            sel_sum = np.zeros((n_list, d))
+            np.add.at(sel_sum, a_all[T], Vf[T])
+            vbar = np.zeros((n_list, d))
+            nz = unsel > 0
+            vbar[nz] = (list_size[nz, None] * lm[nz] - sel_sum[nz]) / unsel[nz, None]
+        else:
+            raise ValueError(f"unknown variant {variant!r}")
+        Z_B = float(M.sum())
+        N_B = M @ vbar
+    else:
+        Z_B = 0.0
+        N_B = np.zeros(d)
+
+    # Eq. (5)
+    y = (N_E + N_B) / (Z_E + Z_B)
+    return RowResult(y=y, T=T, tau=tau, scores=scores, R=R, m0=m0, Z_E=Z_E,
+                     Z_B=Z_B, list_size=list_size, unselected_per_list=unsel)
+
+
+def pqhsa_batch_ref(inp: dict, topk, rows=None, variant: str = "B"):
+    """Run the row oracle over (batch element, query head) pairs.
+
+    inp holds numpy-convertible arrays with the ABI's layouts:
+    q [B, Hq, d]; k_cache, v_cache [B, Hkv, Nmax, d]; list_ids [B, Hkv, Nmax];
+    codes [B, Hkv, Nmax, M]; norms [B, Hkv, Nmax]; centroids [B, Hkv, n_list, d];
+    codebooks [B, Hkv, M, ksub, d/M]; list_means [B, Hkv, n_list, d];
+    seq_lens [B]; n_sink, n_local (ints). topk: int per batch element.
+    Query head h reads KV head h // G with G = Hq / Hkv (Section 3.3).
+    rows: iterable of (b, h); default all. Returns {(b, h): RowResult}.
+    """
+    q = inp["q"]
+    B, Hq, _ = q.shape
+    Hkv = inp["k_cache"].shape[1]
+    G = Hq // Hkv
+    if rows is None:
+        rows = [(b, h) for b in range(B) for h in range(Hq)]
+    out = {}
+    cache = {}
+    for b, h in rows:
+        g = h // G
+        key = (b, g)
+        if key not in cache:
+            cache.clear()
+            n = int(inp["seq_lens"][b])
+            cache[key] = dict(
+                K=_f64(inp["k_cache"][b, g, :n]), V=_f64(inp["v_cache"][b, g, :n]),
+                list_ids=np.asarray(inp["list_ids"][b, g, :n]),
+                codes=np.asarray(inp["codes"][b, g, :n]),
+                norms=_f64(inp["norms"][b, g, :n]),
+                centroids=_f64(inp["centroids"][b, g]),
+                codebooks=_f64(inp["codebooks"][b, g]),
+                list_means=_f64(inp["list_means"][b, g]), n=n)
+        c = cache[key]
+        out[(b, h)] = pqhsa_row_ref(
+            _f64(q[b, h]), c["K"], c["V"], c["list_ids"], c["codes"], c["norms"],
+            c["centroids"], c["codebooks"], c["list_means"], c["n"],
+            int(inp["n_sink"]), int(inp["n_local"]), int(np.asarray(topk)[b]),
+            variant=variant)
+    return out
+
+
+def _f64(x):
+    """Exact upcast of a numpy array or a CPU torch tensor (bf16 included)."""
+    if hasattr(x, "detach"):
+        return x.detach().to("cpu").double().numpy()
+    return np.asarray(x, np.float64)

@@ -1,0 +1,391 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+Each test checks the oracle against something other than itself: a library
+attention routine, an explicit key reconstruction, brute-force ranking,
+closed forms that the method reduces to in special cases, invariances, and
+the budget numbers the paper prints. A plausible mistake in the oracle (a
+dropped coarse term, a wrong sub-vector index, a missing norm factor, a
+selection off by one, a wrong shift or normaliser, the background counting
+selected tokens) fails at least one of them.
+"""
+
+import itertools
+import json
+import math
+import os
+
+import mpmath
+import numpy as np
+import pytest
+import scipy.special
+import torch
+
+from oracle import pqhsa_ref as R
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+# ---------------------------------------------------------------------------
+# small float64 problem builder (independent of the product's generator)
+# ---------------------------------------------------------------------------
+def tiny_problem(seed=0, n=64, d=16, n_m=4, ksub=8, n_list=5, noise=0.0,
+                 norms="one", values="random", q_scale=1.0, empty_list=None):
+    rng = np.random.default_rng(seed)
+    dsub = d // n_m
+    cen = rng.standard_normal((n_list, d))
+    cb = 0.4 * rng.standard_normal((n_m, ksub, dsub))
+    a = rng.integers(0, n_list, size=n)
+    if empty_list is not None:
+        a[a == empty_list] = (empty_list + 1) % n_list
+    z = rng.integers(0, ksub, size=(n, n_m))
+    recon = cen[a] + np.concatenate([cb[m, z[:, m]] for m in range(n_m)], axis=1)
+    if norms == "one":
+        r = np.ones(n)
+    else:
+        r = np.exp(rng.uniform(np.log(0.5), np.log(2.0), size=n))
+    K = r[:, None] * (recon + noise * rng.standard_normal((n, d)))
+    off = rng.standard_normal((n_list, d))
+    if values == "list_constant":
+        V = 0.5 * off[a]
+    else:
+        V = rng.standard_normal((n, d)) + 0.5 * off[a]
+    q = q_scale * K[rng.integers(0, n)] + 0.3 * rng.standard_normal(d)
+    return dict(q=q, K=K, V=V, a=a, z=z.astype(np.uint8), r=r, cen=cen, cb=cb,
+                n_list=n_list)
+
+
+def run(p, n_sink, n_local, k, means=None, variant="B", force_T=None):
+    n = p["K"].shape[0]
+    _, _, Rr = R.split_positions(n, n_sink, n_local)
+    if means is None:
+        means = R.list_means_ref(p["V"], p["a"], p["n_list"], Rr)
+    return R.pqhsa_row_ref(p["q"], p["K"], p["V"], p["a"], p["z"], p["r"], p["cen"],
+                           p["cb"], means, n, n_sink, n_local, k, variant=variant,
+                           force_T=force_T)
+
+
+def sdpa(q, K, V):
+    """Dense attention by torch's library routine (float64, CPU)."""
+    qt = torch.from_numpy(np.asarray(q, np.float64))[None, None, None, :]
+    kt = torch.from_numpy(np.asarray(K, np.float64))[None, None]
+    vt = torch.from_numpy(np.asarray(V, np.float64))[None, None]
+    return torch.nn.functional.scaled_dot_product_attention(qt, kt, vt)[0, 0, 0].numpy()
+
+
+def reconstructed_logits(p, positions):
+    """q . k_hat_i / sqrt(d) with k_hat_i = r_i (c_{a_i} + concat_m p_{m, z_im})."""
+    d = p["q"].shape[0]
+    n_m = p["cb"].shape[0]
+    out = []
+    for i in positions:
+        k_hat = np.concatenate([p["cb"][m, p["z"][i, m]] for m in range(n_m)])
+        k_hat = p["r"][i] * (p["cen"][p["a"][i]] + k_hat)
+        out.append(float(np.dot(p["q"], k_hat)) / math.sqrt(d))
+    return np.array(out)
+
+
+def close(a, b, tol=1e-12):
+    a, b = np.asarray(a, np.float64), np.asarray(b, np.float64)
+    scale = max(np.max(np.abs(b)), 1e-300)
+    return np.max(np.abs(a - b)) / scale <= tol
+
+
+# ---------------------------------------------------------------------------
+# budget numbers printed in Appendix A
+# ---------------------------------------------------------------------------
+def test_budget_rule_reproduces_paper_numbers():
+    with open(os.path.join(GOLDEN, "budget_paper.json")) as f:
+        gold = json.load(f)
+    for case in gold["cases"]:
+        _, rounded = R.budget_paper(case["n_ctx"], case["rho"])
+        if "exact_tokens" in case:
+            assert rounded == case["exact_tokens"], case
+        else:
+            assert abs(rounded - case["exact_tokens_about"]) <= case["about_tolerance"]
+        assert rounded % 16 == 0
+
+
+# ---------------------------------------------------------------------------
+# Eq. (2): LUT score == inner product with the explicitly reconstructed key
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("norms", ["one", "random"])
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_scores_equal_reconstructed_key_logits(norms, seed):
+    p = tiny_problem(seed=seed, n=80, d=32, n_m=8, ksub=16, n_list=6, noise=0.1,
+                     norms=norms)
+    pos = np.arange(80)
+    s = R.pq_scores_ref(p["q"], p["a"], p["z"], p["r"], p["cen"], p["cb"], pos)
+    assert close(s, reconstructed_logits(p, pos), 1e-12)
+
+
+def test_scores_zero_query_are_zero():
+    p = tiny_problem()
+    s = R.pq_scores_ref(np.zeros(16), p["a"], p["z"], p["r"], p["cen"], p["cb"],
+                        np.arange(10))
+    assert np.all(s == 0.0)
+
+
+def test_scores_with_exact_reconstruction_equal_exact_logits():
+    p = tiny_problem(noise=0.0, norms="random")
+    pos = np.arange(p["K"].shape[0])
+    s = R.pq_scores_ref(p["q"], p["a"], p["z"], p["r"], p["cen"], p["cb"], pos)
+    exact = p["K"] @ p["q"] / math.sqrt(p["q"].shape[0])
+    assert close(s, exact, 1e-12)
+
+
+# ---------------------------------------------------------------------------
+# Eq. (3): top-k by brute force ranking, including exact ties
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("seed", range(5))
+def test_topk_matches_brute_force_rank(seed):
+    rng = np.random.default_rng(seed)
+    n = 30
+    scores = rng.integers(0, 6, size=n).astype(np.float64)   # many exact ties
+    ids = rng.permutation(1000)[:n]
+    for k in range(n + 1):
+        T, tau = R.topk_ref(scores, ids, k)
+        brute = []
+        for i in range(n):
+            rank = sum(1 for j in range(n)
+                       if scores[j] > scores[i] or (scores[j] == scores[i] and ids[j] < ids[i]))
+            if rank < k:
+                brute.append(ids[i])
+        assert list(T) == sorted(brute)
+        if k:
+            assert tau == sorted(scores, reverse=True)[k - 1]
+
+
+def test_topk_is_max_sum_subset_for_distinct_scores():
+    rng = np.random.default_rng(7)
+    scores = rng.standard_normal(10)
+    ids = np.arange(10)
+    for k in range(0, 11):
+        T, _ = R.topk_ref(scores, ids, k)
+        best = max(itertools.combinations(range(10), k), key=lambda c: sum(scores[list(c)]))
+        assert list(T) == sorted(best)
+
+
+def test_operator_selects_only_from_R_with_ties_to_smaller_id():
+    p = tiny_problem(seed=3, n=40)
+    # duplicate index entries -> identical approximate logits
+    p["a"][10:20] = p["a"][10]
+    p["z"][10:20] = p["z"][10]
+    res = run(p, n_sink=4, n_local=8, k=5)
+    assert np.all((res.T >= 4) & (res.T < 32))
+    # brute-force rank on the oracle's own logits (ties -> smaller id)
+    rank_sel = [i for i, s in zip(res.R, res.scores)
+                if sum(1 for j, t in zip(res.R, res.scores) if t > s or (t == s and j < i)) < 5]
+    assert list(res.T) == sorted(rank_sel)
+
+
+# ---------------------------------------------------------------------------
+# Eq. (5) special cases
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("n_sink,n_local", [(0, 0), (4, 8), (2, 0)])
+def test_rho_one_is_dense_attention(n_sink, n_local):
+    """Section 3.2: at rho = 1 the background is empty and Eq. 5 is dense."""
+    p = tiny_problem(seed=11, n=50, noise=0.2, norms="random")
+    n_r = 50 - n_sink - n_local
+    res = run(p, n_sink, n_local, n_r)
+    assert res.Z_B == 0.0
+    assert close(res.y, sdpa(p["q"], p["K"], p["V"]), 1e-12)
+
+
+@pytest.mark.parametrize("k", [0, 1, 7, 20, 42])
+def test_exact_reconstruction_and_list_constant_values_is_dense(k):
+    """l~ = l and v_i = v_bar_{a_i}: every background term is exact."""
+    p = tiny_problem(seed=5, n=50, noise=0.0, values="list_constant", norms="random")
+    res = run(p, 4, 4, k)
+    assert close(res.y, sdpa(p["q"], p["K"], p["V"]), 1e-12)
+
+
+@pytest.mark.parametrize("k", [0, 3, 15])
+def test_exact_reconstruction_closed_form(k):
+    """With l~ = l, Eq. 5 is dense attention whose background values are
+    replaced by their list means."""
+    p = tiny_problem(seed=9, n=60, noise=0.0, norms="random", q_scale=0.5)
+    n_sink, n_local = 3, 5
+    res = run(p, n_sink, n_local, k)
+    _, _, Rr = R.split_positions(60, n_sink, n_local)
+    means = R.list_means_ref(p["V"], p["a"], p["n_list"], Rr)
+    V2 = p["V"].copy()
+    for i in Rr:
+        if i not in set(res.T.tolist()):
+            V2[i] = means[p["a"][i]]
+    assert close(res.y, sdpa(p["q"], p["K"], V2), 1e-12)
+
+
+def test_pure_background_is_attention_over_list_pseudo_tokens():
+    """k = 0, S = L = empty: softmax over lists with logit log sum_{R_j} e^{l~}
+    and value v_bar_j (Eq. 4 with every token in B)."""
+    p = tiny_problem(seed=21, n=70, noise=0.3, norms="random", n_list=6)
+    res = run(p, 0, 0, 0)
+    logits = reconstructed_logits(p, range(70))
+    lse = np.array([scipy.special.logsumexp(logits[p["a"] == j]) if np.any(p["a"] == j)
+                    else -np.inf for j in range(6)])
+    w = scipy.special.softmax(lse)
+    means = R.list_means_ref(p["V"], p["a"], 6, np.arange(70))
+    assert close(res.y, w @ means, 1e-12)
+
+
+def test_variant_T_is_softmax_over_exact_set():
+    p = tiny_problem(seed=4, n=50, noise=0.2)
+    res = run(p, 4, 6, 9, variant="T")
+    E = np.concatenate([np.arange(4), np.arange(44, 50), res.T])
+    assert close(res.y, sdpa(p["q"], p["K"][E], p["V"][E]), 1e-12)
+
+
+def test_single_list_equals_global_mean_variant():
+    p = tiny_problem(seed=8, n=50, noise=0.2, n_list=1)
+    yb = run(p, 4, 6, 9).y
+    yc = run(p, 4, 6, 9, variant="C").y
+    assert close(yb, yc, 1e-12)
+
+
+def test_unselected_mean_variant_on_list_constant_values():
+    p = tiny_problem(seed=12, n=50, noise=0.2, values="list_constant")
+    assert close(run(p, 4, 6, 9, variant="Bx").y, run(p, 4, 6, 9).y, 1e-12)
+
+
+def test_unselected_mean_variant_brute_force():
+    p = tiny_problem(seed=13, n=50, noise=0.2)
+    res = run(p, 4, 6, 9, variant="Bx")
+    B = [i for i in range(4, 44) if i not in set(res.T.tolist())]
+    logits = {i: s for i, s in zip(res.R, res.scores)}
+    E = list(range(4)) + list(range(44, 50)) + list(res.T)
+    d = 16
+    num = np.zeros(d)
+    den = 0.0
+    for i in E:
+        e = math.exp(float(np.dot(p["q"], p["K"][i])) / 4.0)
+        num += e * p["V"][i]
+        den += e
+    for i in B:
+        members = [t for t in B if p["a"][t] == p["a"][i]]
+        e = math.exp(logits[i])
+        num += e * p["V"][members].mean(axis=0)
+        den += e
+    assert close(res.y, num / den, 1e-12)
+
+
+# ---------------------------------------------------------------------------
+# Eq. (4) boundary rules and per-token form
+# ---------------------------------------------------------------------------
+def test_background_per_token_form():
+    """Sum over B of e~_i v_bar_{a_i} equals the per-list form (Eq. 4)."""
+    p = tiny_problem(seed=31, n=64, noise=0.3, norms="random", q_scale=0.3)
+    res = run(p, 2, 4, 10)
+    Tset = set(res.T.tolist())
+    d = 16
+    means = R.list_means_ref(p["V"], p["a"], p["n_list"], np.arange(2, 60))
+    num = np.zeros(d)
+    den = 0.0
+    for i in list(range(2)) + list(range(60, 64)) + sorted(Tset):
+        e = math.exp(float(np.dot(p["q"], p["K"][i])) / 4.0)
+        num += e * p["V"][i]
+        den += e
+    for i, s in zip(res.R, res.scores):
+        if i not in Tset:
+            e = math.exp(s)
+            num += e * means[p["a"][i]]
+            den += e
+    assert close(res.y, num / den, 1e-12)
+    assert close(res.Z_B / (res.Z_E + res.Z_B),
+                 sum(math.exp(s) for i, s in zip(res.R, res.scores) if i not in Tset) / den,
+                 1e-12)
+
+
+def test_empty_list_contributes_nothing():
+    p = tiny_problem(seed=14, n=50, noise=0.2, empty_list=2)
+    _, _, Rr = R.split_positions(50, 4, 6)
+    means = R.list_means_ref(p["V"], p["a"], p["n_list"], Rr)
+    y0 = run(p, 4, 6, 7, means=means).y
+    means2 = means.copy()
+    means2[2] = 1e6
+    assert np.array_equal(run(p, 4, 6, 7, means=means2).y, y0)
+
+
+def test_fully_selected_list_contributes_nothing():
+    p = tiny_problem(seed=15, n=50, noise=0.05, n_list=5)
+    # aim the query at list 0's centroid so its members rank first
+    p["q"] = 6.0 * p["cen"][0]
+    _, _, Rr = R.split_positions(50, 4, 6)
+    members = [i for i in Rr if p["a"][i] == 0]
+    k = len(members) + 2
+    means = R.list_means_ref(p["V"], p["a"], p["n_list"], Rr)
+    res = run(p, 4, 6, k, means=means)
+    assert set(members) <= set(res.T.tolist())
+    assert res.unselected_per_list[0] == 0
+    means2 = means.copy()
+    means2[0] = -1e6
+    assert np.array_equal(run(p, 4, 6, k, means=means2).y, res.y)
+
+
+def test_value_shift_and_scale_equivariance():
+    p = tiny_problem(seed=16, n=50, noise=0.3, q_scale=0.4)
+    _, _, Rr = R.split_positions(50, 4, 6)
+    means = R.list_means_ref(p["V"], p["a"], p["n_list"], Rr)
+    y = run(p, 4, 6, 8, means=means).y
+    w = np.linspace(-2, 3, 16)
+    p2 = dict(p, V=p["V"] + w)
+    assert close(run(p2, 4, 6, 8, means=means + w).y, y + w, 1e-12)
+    p3 = dict(p, V=-2.5 * p["V"])
+    assert close(run(p3, 4, 6, 8, means=-2.5 * means).y, -2.5 * y, 1e-12)
+
+
+def test_permutation_of_indexed_tokens():
+    """Reordering the indexed region (with its index entries) leaves y alone."""
+    p = tiny_problem(seed=17, n=50, noise=0.3, norms="random")
+    y = run(p, 4, 6, 9).y
+    perm = np.arange(50)
+    rng = np.random.default_rng(0)
+    perm[4:44] = 4 + rng.permutation(40)
+    p2 = {k: (v[perm] if isinstance(v, np.ndarray) and v.shape[:1] == (50,) else v)
+          for k, v in p.items()}
+    assert close(run(p2, 4, 6, 9).y, y, 1e-12)
+
+
+def test_list_means_helper_brute_force():
+    p = tiny_problem(seed=18, n=40)
+    Rr = np.arange(3, 35)
+    means = R.list_means_ref(p["V"], p["a"], p["n_list"], Rr)
+    for j in range(p["n_list"]):
+        mem = [i for i in Rr if p["a"][i] == j]
+        ref = p["V"][mem].mean(axis=0) if mem else np.zeros(16)
+        assert np.allclose(means[j], ref, rtol=1e-14, atol=1e-14)
+
+
+# ---------------------------------------------------------------------------
+# precision: the float64 oracle against 50-digit arithmetic on tiny inputs
+# ---------------------------------------------------------------------------
+def test_float64_oracle_against_mpmath():
+    mpmath.mp.dps = 50
+    p = tiny_problem(seed=19, n=24, d=8, n_m=2, ksub=4, n_list=3, noise=0.2,
+                     norms="random", q_scale=2.0)
+    n_sink, n_local, k = 2, 3, 5
+    res = run(p, n_sink, n_local, k)
+    d = 8
+    q = [mpmath.mpf(float(x)) for x in p["q"]]
+    Rr = list(range(n_sink, 24 - n_local))
+    Tset = set(res.T.tolist())
+    means = R.list_means_ref(p["V"], p["a"], 3, np.array(Rr))
+    num = [mpmath.mpf(0)] * d
+    den = mpmath.mpf(0)
+    for i in range(24):
+        if i in Rr and i not in Tset:
+            kh = [mpmath.mpf(float(x)) for x in p["cen"][p["a"][i]]]
+            for m in range(2):
+                for t in range(4):
+                    kh[m * 4 + t] += mpmath.mpf(float(p["cb"][m, p["z"][i, m], t]))
+            kh = [mpmath.mpf(float(p["r"][i])) * x for x in kh]
+            logit = mpmath.fsum(a * b for a, b in zip(q, kh)) / mpmath.sqrt(d)
+            val = [mpmath.mpf(float(x)) for x in means[p["a"][i]]]
+        else:
+            kk = [mpmath.mpf(float(x)) for x in p["K"][i]]
+            logit = mpmath.fsum(a * b for a, b in zip(q, kk)) / mpmath.sqrt(d)
+            val = [mpmath.mpf(float(x)) for x in p["V"][i]]
+        e = mpmath.exp(logit)
+        den += e
+        num = [a + e * b for a, b in zip(num, val)]
+    ref = np.array([float(x / den) for x in num])
+    assert close(res.y, ref, 1e-13)
