@@ -1,0 +1,186 @@
+/*
+ * pqhsa.h - C ABI of the PQ-HSA decode-attention operator for MI355X (gfx950).
+ *
+ * PQ-HSA ("hybrid sparse-approximate attention", arXiv 2609.33746) computes,
+ * for each decode query, one approximate logit per indexed cached key from an
+ * IVF-PQ index over key directions (Section 3.1, Eq. 2), attends the top-k of
+ * those tokens plus a sink prefix and a local window exactly with their
+ * original keys and values (Section 3.2, Eq. 3), and lets every unselected
+ * indexed token enter the same softmax through its approximate logit, summed
+ * per inverted list and multiplied by that list's value mean (Eq. 4). The
+ * output is Eq. 5: y = (N_E + N_B) / (Z_E + Z_B).
+ *
+ * Conventions for every entry point
+ *   - All functions return a pqhsa_status; no exception crosses the ABI.
+ *     On failure pqhsa_last_error(ctx) holds a readable message.
+ *   - Tensor arguments are device pointers owned by the caller unless stated
+ *     otherwise; the caller keeps them alive until the work enqueued on
+ *     `stream` has completed. Layouts are row-major, innermost index last.
+ *   - B = batch, Hq / Hkv = query / KV heads, G = Hq / Hkv (the GQA group
+ *     size; query head h reads KV head h / G, Section 3.3), d = head_dim,
+ *     Nmax = max_seq, M = pq_m subspaces of d / M dimensions, K = pq_ksub
+ *     codewords, n_list inverted lists.
+ *   - Sequence b has N_b tokens. Its sink prefix is S = [0, n_sink), its local
+ *     window L = [N_b - n_local, N_b) and its indexed region
+ *     R_b = [n_sink, N_b - n_local) (Section 3.2). Index entries outside R_b
+ *     are ignored.
+ *   - One context serves one stream at a time: calls that overlap on
+ *     different streams with the same context race on its workspace.
+ */
+#ifndef PQHSA_H
+#define PQHSA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    PQHSA_OK = 0,
+    PQHSA_ERR_INVALID_ARGUMENT = 1, /* bad pointer, shape or value            */
+    PQHSA_ERR_UNSUPPORTED = 2,      /* valid but not implemented (see shape)  */
+    PQHSA_ERR_HIP = 3,              /* a HIP runtime call failed              */
+    PQHSA_ERR_OUT_OF_MEMORY = 4,    /* device or host allocation failed       */
+    PQHSA_ERR_NOT_PREPARED = 5      /* decode before pqhsa_index_prepare      */
+} pqhsa_status;
+
+typedef enum { PQHSA_F32 = 0, PQHSA_BF16 = 1 } pqhsa_dtype;
+
+/* Problem shape, fixed for the life of a context.
+ * Supported: head_dim = 128, pq_m = 16 (8-dimensional subspaces),
+ * pq_ksub = 256 (one uint8 code per subspace), 1 <= n_list <= 4096,
+ * G in {1, 2, 4, 8}, 1 <= batch <= 256, kv_dtype F32 or BF16 (the query has
+ * the same dtype as the cache), 0 <= max_topk <= max_seq. */
+typedef struct {
+    int32_t batch;
+    int32_t n_q_heads;
+    int32_t n_kv_heads;
+    int32_t head_dim;
+    int32_t max_seq;
+    int32_t n_list;
+    int32_t pq_m;
+    int32_t pq_ksub;
+    int32_t n_sink;   /* |S|, 4 in the paper's setting (Appendix A)   */
+    int32_t n_local;  /* |L|, 128 in the paper's setting (Appendix A) */
+    int32_t max_topk; /* largest k any decode call will ask for        */
+    int32_t kv_dtype; /* pqhsa_dtype                                   */
+} pqhsa_shape;
+
+typedef struct pqhsa_ctx pqhsa_ctx;
+
+/* Create a context: validates the shape and allocates, on the current HIP
+ * device, the prepared-index storage and the whole decode workspace, so that
+ * decode calls allocate nothing. *out receives the context (NULL on error).
+ * Shape errors are reported before any HIP call is made. */
+pqhsa_status pqhsa_create(const pqhsa_shape* shape, pqhsa_ctx** out);
+
+/* Release every resource of the context (NULL is accepted). */
+void pqhsa_destroy(pqhsa_ctx* ctx);
+
+/* Load one prompt's IVF-PQ index into the context (Section 3.1, 3.3).
+ *   seq_lens   HOST int32 [B]: N_b, with n_sink + n_local <= N_b <= max_seq.
+ *   list_ids   int32 [B, Hkv, Nmax]          a_i, 0 <= a_i < n_list on R_b
+ *   codes      uint8 [B, Hkv, Nmax, M]       z_im
+ *   norms      float [B, Hkv, Nmax]          r_i (the key norm kept outside
+ *                                             the quantizer)
+ *   centroids  float [B, Hkv, n_list, d]     c_j
+ *   codebooks  float [B, Hkv, M, K, d/M]     p_{m,z}
+ *   list_means float [B, Hkv, n_list, d]     v_bar_j, the mean value over
+ *                                             all of R_j (Eq. 4); 0 if empty
+ * The context copies everything it needs (reordered list-major), so the
+ * caller may free these arrays once the call returns: the call synchronises
+ * `stream` before returning. Returns INVALID_ARGUMENT for a list id out of
+ * range (checked on the host after a device-to-host copy). */
+pqhsa_status pqhsa_index_prepare(pqhsa_ctx* ctx, const int32_t* seq_lens,
+                                 const int32_t* list_ids, const uint8_t* codes,
+                                 const float* norms, const float* centroids,
+                                 const float* codebooks, const float* list_means,
+                                 hipStream_t stream);
+
+/* One PQ-HSA decode step (Eqs. 2-5) for every (batch element, query head).
+ *   q          [B, Hq, d] in kv_dtype, contiguous
+ *   k_cache    keys   [B, Hkv, >= N_b, d] in kv_dtype
+ *   v_cache    values, same layout and strides as k_cache
+ *   kv_strides HOST int64 [3]: element strides of (b, kv head, token); the
+ *              last dimension d must be contiguous
+ *   topk       HOST int32 [B]: k_b = |T| for sequence b, 0 <= k_b <= |R_b|
+ *              and k_b <= max_topk (k = ceil(rho |R|) in the paper)
+ *   out        float [B, Hq, d]: y of Eq. 5, fp32
+ * Asynchronous: enqueues kernels on `stream`, allocates nothing, never
+ * synchronises. Requires a prior pqhsa_index_prepare. Device data are not
+ * validated here. */
+pqhsa_status pqhsa_decode(pqhsa_ctx* ctx, const void* q, const void* k_cache,
+                          const void* v_cache, const int64_t* kv_strides,
+                          const int32_t* topk, float* out, hipStream_t stream);
+
+/* pqhsa_decode plus diagnostics for parity checks (synchronises `stream`).
+ *   selected            int32 [B, Hq, max_topk] or NULL: the token ids of T,
+ *                       ascending, padded with -1
+ *   unselected_per_list int32 [B, Hq, n_list] or NULL: |B n R_j| (Eq. 4)
+ *   scores              float [B, Hq, Nmax] or NULL: the approximate logit of
+ *                       Eq. 2 for every token of R_b by token id, NaN
+ *                       elsewhere (computed by the same device code as the
+ *                       scan) */
+pqhsa_status pqhsa_decode_debug(pqhsa_ctx* ctx, const void* q, const void* k_cache,
+                                const void* v_cache, const int64_t* kv_strides,
+                                const int32_t* topk, float* out, int32_t* selected,
+                                int32_t* unselected_per_list, float* scores,
+                                hipStream_t stream);
+
+/* Dense decode attention over the whole cache, y = sum_i e_i v_i / sum_i e_i
+ * with e_i = exp(q.k_i / sqrt(d)) (Section 3, first paragraph): the same-chip
+ * baseline. Arguments as in pqhsa_decode; seq_lens is a HOST int32 [B] with
+ * 1 <= N_b <= max_seq. Needs no prepared index. Asynchronous. */
+pqhsa_status pqhsa_dense_decode(pqhsa_ctx* ctx, const void* q, const void* k_cache,
+                                const void* v_cache, const int64_t* kv_strides,
+                                const int32_t* seq_lens, float* out,
+                                hipStream_t stream);
+
+/* Copy out the prepared list-major layout (synchronises `stream`):
+ *   perm    int32 [B, Hkv, Nmax]: token id at each list-major position of R_b
+ *           (lists in increasing id, tokens in increasing id within a list),
+ *           -1 past |R_b|
+ *   offsets int32 [B, Hkv, n_list + 1]: start of each list in that order */
+pqhsa_status pqhsa_index_export(pqhsa_ctx* ctx, int32_t* perm, int32_t* offsets,
+                                hipStream_t stream);
+
+/* Options (values are int64):
+ *   PQHSA_OPT_FORCE_FALLBACK  1: every row takes the exact re-scan path of the
+ *                             top-k stage (normally used only when the
+ *                             sampled threshold yields fewer than k
+ *                             candidates); for testing that path.
+ *   PQHSA_OPT_STAGE_TIMING    1: record HIP events between the stages of each
+ *                             decode call (read with pqhsa_stage_times).
+ *   PQHSA_OPT_THRESHOLD_BIAS  added (as value / 1000.0) to every sampled
+ *                             candidate threshold; a large value starves the
+ *                             candidate set and forces the fallback. */
+enum {
+    PQHSA_OPT_FORCE_FALLBACK = 1,
+    PQHSA_OPT_STAGE_TIMING = 2,
+    PQHSA_OPT_THRESHOLD_BIAS = 3
+};
+pqhsa_status pqhsa_set_option(pqhsa_ctx* ctx, int32_t option, int64_t value);
+
+/* Stage durations (ms) of the last decode call made with stage timing on, in
+ * launch order: [0] LUT build, [1] threshold sample, [2] code scan,
+ * [3] top-k select, [4] exact attention + background, [5] merge.
+ * `n` is the capacity of `ms`; *n_out receives the number of stages.
+ * Synchronises on the recorded events. */
+pqhsa_status pqhsa_stage_times(pqhsa_ctx* ctx, float* ms, int32_t n, int32_t* n_out);
+
+/* Static description of a status code. */
+const char* pqhsa_status_string(pqhsa_status status);
+
+/* Message of the last failed call on this context ("" if none; NULL ctx gives
+ * the message of the last failed pqhsa_create in this process). */
+const char* pqhsa_last_error(const pqhsa_ctx* ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PQHSA_H */

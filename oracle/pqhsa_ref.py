@@ -285,7 +285,7 @@ def pqhsa_row_ref(q, K, V, list_ids, codes, norms, centroids, codebooks,
                      Z_B=Z_B, list_size=list_size, unselected_per_list=unsel)
 
 
-def pqhsa_batch_ref(inp: dict, topk, rows=None, variant: str = "B"):
+def pqhsa_batch_ref(inp: dict, topk, rows=None, variant: str = "B", force_T=None):
     """Run the row oracle over (batch element, query head) pairs.
 
     inp holds numpy-convertible arrays with the ABI's layouts:
@@ -294,10 +294,13 @@ def pqhsa_batch_ref(inp: dict, topk, rows=None, variant: str = "B"):
     codebooks [B, Hkv, M, ksub, d/M]; list_means [B, Hkv, n_list, d];
     seq_lens [B]; n_sink, n_local (ints). topk: int per batch element.
     Query head h reads KV head h // G with G = Hq / Hkv (Section 3.3).
-    rows: iterable of (b, h); default all. Returns {(b, h): RowResult}.
+    rows: iterable of (b, h); default all. force_T: optional {(b, h): token ids}.
+    Arrays may be numpy arrays or torch tensors on any device (read-only).
+    Returns {(b, h): RowResult}.
     """
     q = inp["q"]
     B, Hq, _ = q.shape
+    seq_lens = _np(inp["seq_lens"])
     Hkv = inp["k_cache"].shape[1]
     G = Hq // Hkv
     if rows is None:
@@ -309,11 +312,11 @@ def pqhsa_batch_ref(inp: dict, topk, rows=None, variant: str = "B"):
         key = (b, g)
         if key not in cache:
             cache.clear()
-            n = int(inp["seq_lens"][b])
+            n = int(seq_lens[b])
             cache[key] = dict(
                 K=_f64(inp["k_cache"][b, g, :n]), V=_f64(inp["v_cache"][b, g, :n]),
-                list_ids=np.asarray(inp["list_ids"][b, g, :n]),
-                codes=np.asarray(inp["codes"][b, g, :n]),
+                list_ids=_np(inp["list_ids"][b, g, :n]),
+                codes=_np(inp["codes"][b, g, :n]),
                 norms=_f64(inp["norms"][b, g, :n]),
                 centroids=_f64(inp["centroids"][b, g]),
                 codebooks=_f64(inp["codebooks"][b, g]),
@@ -322,13 +325,20 @@ def pqhsa_batch_ref(inp: dict, topk, rows=None, variant: str = "B"):
         out[(b, h)] = pqhsa_row_ref(
             _f64(q[b, h]), c["K"], c["V"], c["list_ids"], c["codes"], c["norms"],
             c["centroids"], c["codebooks"], c["list_means"], c["n"],
-            int(inp["n_sink"]), int(inp["n_local"]), int(np.asarray(topk)[b]),
-            variant=variant)
+            int(inp["n_sink"]), int(inp["n_local"]), int(_np(topk)[b]),
+            variant=variant, force_T=None if force_T is None else force_T.get((b, h)))
     return out
 
 
 def _f64(x):
-    """Exact upcast of a numpy array or a CPU torch tensor (bf16 included)."""
+    """Exact upcast of a numpy array or a torch tensor (bf16 included)."""
     if hasattr(x, "detach"):
         return x.detach().to("cpu").double().numpy()
     return np.asarray(x, np.float64)
+
+
+def _np(x):
+    """A numpy copy of a numpy array or a torch tensor on any device."""
+    if hasattr(x, "detach"):
+        return x.detach().to("cpu").numpy()
+    return np.asarray(x)

@@ -1,0 +1,511 @@
+// Host side of libpqhsa: argument validation, context and workspace
+// management, index preparation and the stream-ordered launch sequence of a
+// decode step. Every numeric step of the operator runs in the HIP kernels of
+// this library; the host only validates, reorders index metadata at prepare
+// time and enqueues work.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "pqhsa.h"
+#include "pqhsa_internal.h"
+
+using namespace pqhsa;
+
+namespace {
+
+thread_local std::string g_create_error;
+
+constexpr int kStages = 6;
+
+}  // namespace
+
+struct pqhsa_ctx {
+    pqhsa_shape shape{};
+    Dims D{};
+    int device = 0;
+    std::string err;
+    std::vector<void*> allocs;
+
+    // prepared index (device)
+    bool prepared = false;
+    std::vector<int32_t> seq_lens, n_r;
+    uint8_t* codes = nullptr;
+    float* norms = nullptr;
+    int32_t* perm = nullptr;
+    int32_t* pos_list = nullptr;
+    int32_t* loff = nullptr;
+    int32_t* seg0 = nullptr;
+    float* centroids = nullptr;
+    float* codebooks = nullptr;
+    float* means = nullptr;
+    int32_t* n_seq_dev = nullptr;
+    int32_t* n_r_dev = nullptr;
+    int2* scan_table = nullptr;
+    int n_scan_wg = 0;
+
+    // workspace
+    Work w{};
+    int nsplit_max = 0;
+    float* dense_partial = nullptr;
+    int dense_nsplit = 0;
+
+    // options
+    int force_fallback = 0;
+    int timing = 0;
+    float bias = 0.0f;
+    hipEvent_t ev[kStages + 1]{};
+    bool events_made = false;
+    bool timed_valid = false;
+
+    Index index() const {
+        Index ix;
+        ix.codes = codes;
+        ix.norms = norms;
+        ix.perm = perm;
+        ix.pos_list = pos_list;
+        ix.loff = loff;
+        ix.seg0 = seg0;
+        ix.centroids = centroids;
+        ix.codebooks = codebooks;
+        ix.means = means;
+        ix.n_seq = n_seq_dev;
+        ix.n_r = n_r_dev;
+        return ix;
+    }
+};
+
+namespace {
+
+pqhsa_status fail(pqhsa_ctx* c, pqhsa_status st, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    if (c) c->err = buf;
+    else g_create_error = buf;
+    return st;
+}
+
+pqhsa_status hip_fail(pqhsa_ctx* c, hipError_t e, const char* what) {
+    return fail(c, PQHSA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+template <typename T>
+hipError_t dev_alloc(pqhsa_ctx* c, T** p, size_t count) {
+    void* raw = nullptr;
+    const size_t bytes = std::max<size_t>(count * sizeof(T), 256);
+    hipError_t e = hipMalloc(&raw, bytes);
+    if (e != hipSuccess) return e;
+    c->allocs.push_back(raw);
+    *p = static_cast<T*>(raw);
+    return hipSuccess;
+}
+
+pqhsa_status check_shape(const pqhsa_shape* s) {
+    if (!s) return fail(nullptr, PQHSA_ERR_INVALID_ARGUMENT, "shape is NULL");
+    if (s->batch < 1 || s->n_q_heads < 1 || s->n_kv_heads < 1 || s->max_seq < 1)
+        return fail(nullptr, PQHSA_ERR_INVALID_ARGUMENT,
+                    "batch, n_q_heads, n_kv_heads and max_seq must be positive");
+    if (s->n_q_heads % s->n_kv_heads)
+        return fail(nullptr, PQHSA_ERR_INVALID_ARGUMENT, "n_q_heads must be a multiple of n_kv_heads");
+    if (s->n_sink < 0 || s->n_local < 0 || s->n_sink + s->n_local > s->max_seq)
+        return fail(nullptr, PQHSA_ERR_INVALID_ARGUMENT, "need 0 <= n_sink, n_local and n_sink + n_local <= max_seq");
+    if (s->max_topk < 0 || s->max_topk > s->max_seq)
+        return fail(nullptr, PQHSA_ERR_INVALID_ARGUMENT, "need 0 <= max_topk <= max_seq");
+    if (s->n_list < 1) return fail(nullptr, PQHSA_ERR_INVALID_ARGUMENT, "n_list must be positive");
+    if (s->kv_dtype != PQHSA_F32 && s->kv_dtype != PQHSA_BF16)
+        return fail(nullptr, PQHSA_ERR_UNSUPPORTED, "kv_dtype must be PQHSA_F32 or PQHSA_BF16");
+    if (s->head_dim != kHeadDim) return fail(nullptr, PQHSA_ERR_UNSUPPORTED, "head_dim must be 128");
+    if (s->pq_m != kPqM || s->pq_ksub != kKsub)
+        return fail(nullptr, PQHSA_ERR_UNSUPPORTED, "only pq_m = 16 and pq_ksub = 256 are supported");
+    const int G = s->n_q_heads / s->n_kv_heads;
+    if (G != 1 && G != 2 && G != 4 && G != 8)
+        return fail(nullptr, PQHSA_ERR_UNSUPPORTED, "GQA group size must be 1, 2, 4 or 8");
+    if (s->batch > kMaxBatch) return fail(nullptr, PQHSA_ERR_UNSUPPORTED, "batch must be <= 256");
+    if (s->n_list > kMaxLists) return fail(nullptr, PQHSA_ERR_UNSUPPORTED, "n_list must be <= 4096");
+    return PQHSA_OK;
+}
+
+pqhsa_status check_device(pqhsa_ctx* c) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(c, e, "hipGetDevice");
+    if (dev != c->device)
+        return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "current device %d is not the context's device %d", dev,
+                    c->device);
+    return PQHSA_OK;
+}
+
+pqhsa_status check_kv(pqhsa_ctx* c, const void* q, const void* k, const void* v,
+                      const int64_t* strides, const void* out, KV* kv) {
+    if (!q || !k || !v || !out || !strides)
+        return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "q, k_cache, v_cache, kv_strides and out must be non-NULL");
+    const int64_t sb = strides[0], sh = strides[1], sn = strides[2];
+    if (sb < 0 || sh < 0 || sn < kHeadDim)
+        return fail(c, PQHSA_ERR_INVALID_ARGUMENT,
+                    "kv_strides must be non-negative with a token stride >= head_dim");
+    const int esz = c->shape.kv_dtype == PQHSA_BF16 ? 2 : 4;
+    if ((sb * esz) % 16 || (sh * esz) % 16 || (sn * esz) % 16 ||
+        reinterpret_cast<uintptr_t>(k) % 16 || reinterpret_cast<uintptr_t>(v) % 16 ||
+        reinterpret_cast<uintptr_t>(q) % 16)
+        return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "q, k_cache, v_cache and their strides must be 16-byte aligned");
+    kv->q = q;
+    kv->k = k;
+    kv->v = v;
+    kv->sb = sb;
+    kv->sh = sh;
+    kv->sn = sn;
+    kv->bf16 = c->shape.kv_dtype == PQHSA_BF16;
+    return PQHSA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* pqhsa_status_string(pqhsa_status st) {
+    switch (st) {
+        case PQHSA_OK: return "ok";
+        case PQHSA_ERR_INVALID_ARGUMENT: return "invalid argument";
+        case PQHSA_ERR_UNSUPPORTED: return "unsupported";
+        case PQHSA_ERR_HIP: return "HIP runtime error";
+        case PQHSA_ERR_OUT_OF_MEMORY: return "out of memory";
+        case PQHSA_ERR_NOT_PREPARED: return "index not prepared";
+        default: return "unknown status";
+    }
+}
+
+const char* pqhsa_last_error(const pqhsa_ctx* ctx) {
+    return ctx ? ctx->err.c_str() : g_create_error.c_str();
+}
+
+void pqhsa_destroy(pqhsa_ctx* ctx) {
+    if (!ctx) return;
+    if (ctx->events_made)
+        for (auto& e : ctx->ev) (void)hipEventDestroy(e);
+    for (void* p : ctx->allocs) (void)hipFree(p);
+    delete ctx;
+}
+
+pqhsa_status pqhsa_create(const pqhsa_shape* shape, pqhsa_ctx** out) {
+    g_create_error.clear();
+    if (!out) return fail(nullptr, PQHSA_ERR_INVALID_ARGUMENT, "out is NULL");
+    *out = nullptr;
+    pqhsa_status st = check_shape(shape);
+    if (st != PQHSA_OK) return st;
+
+    pqhsa_ctx* c = new (std::nothrow) pqhsa_ctx();
+    if (!c) return fail(nullptr, PQHSA_ERR_OUT_OF_MEMORY, "host allocation failed");
+    c->shape = *shape;
+    hipError_t e = hipGetDevice(&c->device);
+    if (e != hipSuccess) {
+        delete c;
+        return fail(nullptr, PQHSA_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+    }
+    Dims& D = c->D;
+    D.B = shape->batch;
+    D.Hq = shape->n_q_heads;
+    D.Hkv = shape->n_kv_heads;
+    D.G = D.Hq / D.Hkv;
+    D.n_list = shape->n_list;
+    D.n_sink = shape->n_sink;
+    D.n_local = shape->n_local;
+    D.rcap = shape->max_seq;
+    D.nsub_cap = (D.rcap + kSub - 1) / kSub;
+    D.nseg_cap = D.n_list + D.nsub_cap;
+    D.max_topk = std::max(shape->max_topk, 1);
+    D.inv_sqrt_d = static_cast<float>(1.0 / std::sqrt(static_cast<double>(kHeadDim)));
+
+    const size_t B = D.B, Hq = D.Hq, Hkv = D.Hkv, G = D.G, L = D.n_list, rc = D.rcap;
+    const size_t BG = B * Hkv, BQ = B * Hq;
+    c->nsplit_max = (D.n_sink + D.n_local + shape->max_topk + kAttnRows - 1) / kAttnRows;
+    if (c->nsplit_max < 1) c->nsplit_max = 1;
+    const int n_bgc = (D.n_list + kBgLists - 1) / kBgLists;
+    c->dense_nsplit = (D.rcap + kDenseRows - 1) / kDenseRows;
+    const size_t max_scan_wg = BG * ((D.nsub_cap + kScanWaves - 1) / kScanWaves);
+
+    Work& w = c->w;
+    hipError_t ea = hipSuccess;
+    auto A = [&](hipError_t r) { if (ea == hipSuccess) ea = r; };
+    A(dev_alloc(c, &c->codes, BG * rc * kPqM));
+    A(dev_alloc(c, &c->norms, BG * rc));
+    A(dev_alloc(c, &c->perm, BG * rc));
+    A(dev_alloc(c, &c->pos_list, BG * rc));
+    A(dev_alloc(c, &c->loff, BG * (L + 1)));
+    A(dev_alloc(c, &c->seg0, BG * (L + 1)));
+    A(dev_alloc(c, &c->centroids, BG * L * kHeadDim));
+    A(dev_alloc(c, &c->codebooks, BG * kPqM * kKsub * kDsub));
+    A(dev_alloc(c, &c->means, BG * L * kHeadDim));
+    A(dev_alloc(c, &c->n_seq_dev, B));
+    A(dev_alloc(c, &c->n_r_dev, B));
+    A(dev_alloc(c, &c->scan_table, max_scan_wg));
+    A(dev_alloc(c, &w.lut, BG * kLutRow * G));
+    A(dev_alloc(c, &w.coarse, BG * L * G));
+    A(dev_alloc(c, &w.tau_lo, BQ));
+    A(dev_alloc(c, &w.cand_score, BQ * rc));
+    A(dev_alloc(c, &w.cand_pos, BQ * rc));
+    A(dev_alloc(c, &w.cand_cnt, BQ * D.nsub_cap));
+    A(dev_alloc(c, &w.seg_sum, BG * D.nseg_cap * G));
+    A(dev_alloc(c, &w.comp_key, BQ * rc));
+    A(dev_alloc(c, &w.comp_pos, BQ * rc));
+    A(dev_alloc(c, &w.sel_tok, BQ * D.max_topk));
+    A(dev_alloc(c, &w.sel_pos, BQ * D.max_topk));
+    A(dev_alloc(c, &w.cand_mass, BQ * L));
+    A(dev_alloc(c, &w.row_shift, BQ));
+    A(dev_alloc(c, &w.row_flag, BQ));
+    A(dev_alloc(c, &w.partial, BQ * (c->nsplit_max + n_bgc) * kPartStride));
+    A(dev_alloc(c, &c->dense_partial, BQ * c->dense_nsplit * kPartStride));
+    if (ea != hipSuccess) {
+        const bool oom = ea == hipErrorOutOfMemory || ea == hipErrorMemoryAllocation;
+        char msg[256];
+        snprintf(msg, sizeof(msg), "device allocation failed: %s", hipGetErrorString(ea));
+        pqhsa_destroy(c);
+        return fail(nullptr, oom ? PQHSA_ERR_OUT_OF_MEMORY : PQHSA_ERR_HIP, "%s", msg);
+    }
+    *out = c;
+    return PQHSA_OK;
+}
+
+pqhsa_status pqhsa_index_prepare(pqhsa_ctx* c, const int32_t* seq_lens, const int32_t* list_ids,
+                                 const uint8_t* codes, const float* norms, const float* centroids,
+                                 const float* codebooks, const float* list_means,
+                                 hipStream_t stream) {
+    if (!c) return fail(nullptr, PQHSA_ERR_INVALID_ARGUMENT, "ctx is NULL");
+    c->err.clear();
+    if (!seq_lens || !list_ids || !codes || !norms || !centroids || !codebooks || !list_means)
+        return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "every index argument must be non-NULL");
+    pqhsa_status st = check_device(c);
+    if (st != PQHSA_OK) return st;
+    const Dims& D = c->D;
+    const int B = D.B, Hkv = D.Hkv, L = D.n_list;
+    const size_t rc = D.rcap;
+    std::vector<int32_t> lens(seq_lens, seq_lens + B), nr(B);
+    for (int b = 0; b < B; ++b) {
+        if (lens[b] < D.n_sink + D.n_local || lens[b] > D.rcap)
+            return fail(c, PQHSA_ERR_INVALID_ARGUMENT,
+                        "seq_lens[%d] = %d outside [n_sink + n_local, max_seq] = [%d, %d]", b, lens[b],
+                        D.n_sink + D.n_local, D.rcap);
+        nr[b] = lens[b] - D.n_sink - D.n_local;
+    }
+    c->prepared = false;
+
+    const size_t BG = static_cast<size_t>(B) * Hkv;
+    std::vector<int32_t> ids(BG * rc);
+    hipError_t e = hipMemcpyAsync(ids.data(), list_ids, ids.size() * sizeof(int32_t),
+                                  hipMemcpyDeviceToHost, stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) return hip_fail(c, e, "copying list ids to the host");
+
+    // stable counting sort of R_b by list id, per (b, kv head)
+    std::vector<int32_t> perm(BG * rc, -1), pos_list(BG * rc, 0), loff(BG * (L + 1)),
+        seg0(BG * (L + 1));
+    std::vector<int2> table;
+    std::vector<int32_t> cnt(L);
+    for (int b = 0; b < B; ++b) {
+        for (int g = 0; g < Hkv; ++g) {
+            const size_t bg = static_cast<size_t>(b) * Hkv + g;
+            const int32_t* a = ids.data() + bg * rc;
+            std::fill(cnt.begin(), cnt.end(), 0);
+            for (int i = D.n_sink; i < D.n_sink + nr[b]; ++i) {
+                if (a[i] < 0 || a[i] >= L)
+                    return fail(c, PQHSA_ERR_INVALID_ARGUMENT,
+                                "list_ids[%d][%d][%d] = %d outside [0, n_list = %d)", b, g, i, a[i], L);
+                ++cnt[a[i]];
+            }
+            int32_t* lo = loff.data() + bg * (L + 1);
+            int32_t* sg = seg0.data() + bg * (L + 1);
+            lo[0] = 0;
+            sg[0] = 0;
+            for (int j = 0; j < L; ++j) {
+                lo[j + 1] = lo[j] + cnt[j];
+                const int nseg = cnt[j] ? (lo[j + 1] - 1) / kSub - lo[j] / kSub + 1 : 0;
+                sg[j + 1] = sg[j] + nseg;
+            }
+            std::vector<int32_t> fillp(lo, lo + L);
+            int32_t* pm = perm.data() + bg * rc;
+            int32_t* pl = pos_list.data() + bg * rc;
+            for (int i = D.n_sink; i < D.n_sink + nr[b]; ++i) {
+                const int p = fillp[a[i]]++;
+                pm[p] = i;
+                pl[p] = a[i];
+            }
+            const int nsub = (nr[b] + kSub - 1) / kSub;
+            for (int s0 = 0; s0 < nsub; s0 += kScanWaves) table.push_back(make_int2(static_cast<int>(bg), s0));
+        }
+    }
+
+    auto H2D = [&](void* dst, const void* src, size_t bytes) {
+        if (e == hipSuccess) e = hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, stream);
+    };
+    auto D2D = [&](void* dst, const void* src, size_t bytes) {
+        if (e == hipSuccess) e = hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDevice, stream);
+    };
+    H2D(c->perm, perm.data(), perm.size() * 4);
+    H2D(c->pos_list, pos_list.data(), pos_list.size() * 4);
+    H2D(c->loff, loff.data(), loff.size() * 4);
+    H2D(c->seg0, seg0.data(), seg0.size() * 4);
+    H2D(c->n_seq_dev, lens.data(), B * 4);
+    H2D(c->n_r_dev, nr.data(), B * 4);
+    if (!table.empty()) H2D(c->scan_table, table.data(), table.size() * sizeof(int2));
+    D2D(c->centroids, centroids, BG * L * kHeadDim * 4);
+    D2D(c->codebooks, codebooks, BG * kPqM * kKsub * kDsub * 4);
+    D2D(c->means, list_means, BG * L * kHeadDim * 4);
+    if (e != hipSuccess) return hip_fail(c, e, "uploading the prepared index");
+    e = launch_prepare_gather(D, codes, norms, c->index(), c->codes, c->norms, stream);
+    if (e != hipSuccess) return hip_fail(c, e, "launching the index gather");
+    e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) return hip_fail(c, e, "preparing the index");
+    c->seq_lens = lens;
+    c->n_r = nr;
+    c->n_scan_wg = static_cast<int>(table.size());
+    c->prepared = true;
+    return PQHSA_OK;
+}
+
+static pqhsa_status decode_impl(pqhsa_ctx* c, const void* q, const void* k, const void* v,
+                                const int64_t* strides, const int32_t* topk, float* out,
+                                hipStream_t stream, BatchInts* tk_out) {
+    if (!c) return fail(nullptr, PQHSA_ERR_INVALID_ARGUMENT, "ctx is NULL");
+    c->err.clear();
+    if (!c->prepared) return fail(c, PQHSA_ERR_NOT_PREPARED, "pqhsa_index_prepare has not succeeded");
+    KV kv;
+    pqhsa_status st = check_kv(c, q, k, v, strides, out, &kv);
+    if (st != PQHSA_OK) return st;
+    if (!topk) return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "topk is NULL");
+    st = check_device(c);
+    if (st != PQHSA_OK) return st;
+    const Dims& D = c->D;
+    BatchInts tk;
+    for (int b = 0; b < D.B; ++b) {
+        if (topk[b] < 0 || topk[b] > c->n_r[b] || topk[b] > c->shape.max_topk)
+            return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "topk[%d] = %d outside [0, min(|R_b| = %d, max_topk = %d)]",
+                        b, topk[b], c->n_r[b], c->shape.max_topk);
+        tk.v[b] = topk[b];
+    }
+    const Index ix = c->index();
+    const bool timed = c->timing != 0;
+    hipError_t e = hipSuccess;
+    if (timed && !c->events_made) {
+        for (auto& ev : c->ev)
+            if (e == hipSuccess) e = hipEventCreate(&ev);
+        if (e != hipSuccess) return hip_fail(c, e, "hipEventCreate");
+        c->events_made = true;
+    }
+    c->timed_valid = false;
+    auto mark = [&](int i) {
+        if (timed && e == hipSuccess) e = hipEventRecord(c->ev[i], stream);
+    };
+    mark(0);
+    if (e == hipSuccess) e = launch_lut(D, kv, ix, c->w, stream);
+    mark(1);
+    if (e == hipSuccess) e = launch_sample(D, tk, ix, c->w, c->bias, stream);
+    mark(2);
+    if (e == hipSuccess) e = launch_scan(D, ix, c->w, c->scan_table, c->n_scan_wg, stream);
+    mark(3);
+    if (e == hipSuccess) e = launch_select(D, tk, ix, c->w, c->force_fallback, stream);
+    mark(4);
+    if (e == hipSuccess) e = launch_attend(D, tk, kv, ix, c->w, c->nsplit_max, stream);
+    mark(5);
+    if (e == hipSuccess) e = launch_merge(D, tk, c->w, out, c->nsplit_max, stream);
+    mark(6);
+    if (e != hipSuccess) return hip_fail(c, e, "enqueueing the decode kernels");
+    c->timed_valid = timed;
+    if (tk_out) *tk_out = tk;
+    return PQHSA_OK;
+}
+
+pqhsa_status pqhsa_decode(pqhsa_ctx* c, const void* q, const void* k, const void* v,
+                          const int64_t* kv_strides, const int32_t* topk, float* out,
+                          hipStream_t stream) {
+    return decode_impl(c, q, k, v, kv_strides, topk, out, stream, nullptr);
+}
+
+pqhsa_status pqhsa_decode_debug(pqhsa_ctx* c, const void* q, const void* k, const void* v,
+                                const int64_t* kv_strides, const int32_t* topk, float* out,
+                                int32_t* selected, int32_t* unselected_per_list, float* scores,
+                                hipStream_t stream) {
+    if (c && selected && topk) {
+        for (int b = 0; b < c->D.B; ++b)
+            if (topk[b] > 8192)
+                return fail(c, PQHSA_ERR_UNSUPPORTED, "the debug call sorts at most 8192 selected tokens per row");
+    }
+    BatchInts tk;
+    pqhsa_status st = decode_impl(c, q, k, v, kv_strides, topk, out, stream, &tk);
+    if (st != PQHSA_OK) return st;
+    hipError_t e = launch_debug(c->D, tk, c->index(), c->w, selected, unselected_per_list, scores, stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) return hip_fail(c, e, "running the debug kernels");
+    return PQHSA_OK;
+}
+
+pqhsa_status pqhsa_dense_decode(pqhsa_ctx* c, const void* q, const void* k, const void* v,
+                                const int64_t* kv_strides, const int32_t* seq_lens, float* out,
+                                hipStream_t stream) {
+    if (!c) return fail(nullptr, PQHSA_ERR_INVALID_ARGUMENT, "ctx is NULL");
+    c->err.clear();
+    KV kv;
+    pqhsa_status st = check_kv(c, q, k, v, kv_strides, out, &kv);
+    if (st != PQHSA_OK) return st;
+    if (!seq_lens) return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "seq_lens is NULL");
+    st = check_device(c);
+    if (st != PQHSA_OK) return st;
+    BatchInts lens;
+    for (int b = 0; b < c->D.B; ++b) {
+        if (seq_lens[b] < 1 || seq_lens[b] > c->D.rcap)
+            return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "seq_lens[%d] = %d outside [1, max_seq]", b, seq_lens[b]);
+        lens.v[b] = seq_lens[b];
+    }
+    hipError_t e = launch_dense(c->D, kv, lens, c->dense_partial, out, c->dense_nsplit, stream);
+    if (e != hipSuccess) return hip_fail(c, e, "enqueueing the dense decode kernels");
+    return PQHSA_OK;
+}
+
+pqhsa_status pqhsa_index_export(pqhsa_ctx* c, int32_t* perm, int32_t* offsets, hipStream_t stream) {
+    if (!c) return fail(nullptr, PQHSA_ERR_INVALID_ARGUMENT, "ctx is NULL");
+    c->err.clear();
+    if (!c->prepared) return fail(c, PQHSA_ERR_NOT_PREPARED, "pqhsa_index_prepare has not succeeded");
+    const size_t BG = static_cast<size_t>(c->D.B) * c->D.Hkv;
+    hipError_t e = hipSuccess;
+    if (perm) e = hipMemcpyAsync(perm, c->perm, BG * c->D.rcap * 4, hipMemcpyDeviceToDevice, stream);
+    if (e == hipSuccess && offsets)
+        e = hipMemcpyAsync(offsets, c->loff, BG * (c->D.n_list + 1) * 4, hipMemcpyDeviceToDevice, stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) return hip_fail(c, e, "exporting the index");
+    return PQHSA_OK;
+}
+
+pqhsa_status pqhsa_set_option(pqhsa_ctx* c, int32_t option, int64_t value) {
+    if (!c) return fail(nullptr, PQHSA_ERR_INVALID_ARGUMENT, "ctx is NULL");
+    switch (option) {
+        case PQHSA_OPT_FORCE_FALLBACK: c->force_fallback = value != 0; return PQHSA_OK;
+        case PQHSA_OPT_STAGE_TIMING: c->timing = value != 0; return PQHSA_OK;
+        case PQHSA_OPT_THRESHOLD_BIAS: c->bias = static_cast<float>(value) / 1000.0f; return PQHSA_OK;
+        default: return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "unknown option %d", option);
+    }
+}
+
+pqhsa_status pqhsa_stage_times(pqhsa_ctx* c, float* ms, int32_t n, int32_t* n_out) {
+    if (!c) return fail(nullptr, PQHSA_ERR_INVALID_ARGUMENT, "ctx is NULL");
+    if (!ms || !n_out) return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "ms and n_out must be non-NULL");
+    if (!c->timed_valid) return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "no decode call was timed");
+    hipError_t e = hipEventSynchronize(c->ev[kStages]);
+    if (e != hipSuccess) return hip_fail(c, e, "hipEventSynchronize");
+    for (int i = 0; i < kStages && i < n; ++i) {
+        float t = 0.0f;
+        e = hipEventElapsedTime(&t, c->ev[i], c->ev[i + 1]);
+        if (e != hipSuccess) return hip_fail(c, e, "hipEventElapsedTime");
+        ms[i] = t;
+    }
+    *n_out = kStages;
+    return PQHSA_OK;
+}
+
+}  // extern "C"

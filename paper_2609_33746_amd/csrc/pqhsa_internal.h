@@ -1,0 +1,107 @@
+// Internal types and kernel launchers of libpqhsa (not part of the C ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace pqhsa {
+
+// --- tiling constants ------------------------------------------------------
+constexpr int kHeadDim = 128;      // d
+constexpr int kPqM = 16;           // subspaces
+constexpr int kKsub = 256;         // codewords per subspace (uint8 codes)
+constexpr int kDsub = 8;           // d / M
+constexpr int kLutRow = kPqM * kKsub;  // LUT entries per query head
+constexpr int kMaxBatch = 256;
+constexpr int kMaxLists = 4096;
+
+constexpr int kSub = 256;          // list-major positions per wave sub-chunk
+constexpr int kScanWaves = 8;      // waves (sub-chunks) per scan workgroup
+constexpr int kSampleStride = 32;  // one sampled position in 32 for the threshold
+constexpr int kMaxSamples = 4096;  // LDS capacity of the sample kernel
+constexpr int kSelThreads = 256;
+constexpr int kAttnRows = 128;     // exact-set rows per split
+constexpr int kBgLists = 64;       // lists per background workgroup
+constexpr int kDenseRows = 512;    // cache rows per dense split
+constexpr int kPartStride = 132;   // floats per partial: m, Z, pad, pad, N[128]
+
+// --- kernel arguments ----------------------------------------------------
+struct Dims {
+    int B, Hq, Hkv, G, n_list, n_sink, n_local;
+    int rcap;       // per-(b, kv head) capacity of list-major arrays (= max_seq)
+    int nsub_cap;   // ceil(rcap / kSub)
+    int nseg_cap;   // n_list + nsub_cap
+    int max_topk;
+    float inv_sqrt_d;
+};
+
+// One int per batch element, passed by value (top-k budgets, lengths).
+struct BatchInts {
+    int32_t v[kMaxBatch];
+};
+
+// Prepared index (list-major), owned by the context.
+struct Index {
+    const uint8_t* codes;      // [B, Hkv, rcap, M]
+    const float* norms;        // [B, Hkv, rcap]
+    const int32_t* perm;       // [B, Hkv, rcap] token id of each position
+    const int32_t* pos_list;   // [B, Hkv, rcap] list id of each position
+    const int32_t* loff;       // [B, Hkv, n_list + 1] list starts
+    const int32_t* seg0;       // [B, Hkv, n_list + 1] first segment of each list
+    const float* centroids;    // [B, Hkv, n_list, d]
+    const float* codebooks;    // [B, Hkv, M, K, d/M]
+    const float* means;        // [B, Hkv, n_list, d]
+    const int32_t* n_seq;      // [B]
+    const int32_t* n_r;        // [B] |R_b|
+};
+
+// Decode workspace, owned by the context.
+struct Work {
+    float* lut;          // [B, Hkv, M, K, G]   (q^(m) . p_{m,z}) / sqrt(d)
+    float* coarse;       // [B, Hkv, n_list, G] (q . c_j) / sqrt(d)
+    float* tau_lo;       // [B, Hq] candidate threshold
+    float* cand_score;   // [B, Hq, rcap] per sub-chunk compacted candidates
+    int32_t* cand_pos;   // [B, Hq, rcap]
+    int32_t* cand_cnt;   // [B, Hq, nsub_cap]
+    float* seg_sum;      // [B, Hkv, nseg_cap, G] below-threshold masses
+    uint32_t* comp_key;  // [B, Hq, rcap] contiguous candidates (order keys)
+    int32_t* comp_pos;   // [B, Hq, rcap]
+    int32_t* sel_tok;    // [B, Hq, max_topk] selected token ids
+    int32_t* sel_pos;    // [B, Hq, max_topk] their list-major positions
+    float* cand_mass;    // [B, Hq, n_list] unselected-candidate masses
+    float* row_shift;    // [B, Hq] shift of the background masses
+    int32_t* row_flag;   // [B, Hq] 1 when the row took the re-scan path
+    float* partial;      // [B, Hq, nsplit_max + n_bgc, kPartStride]
+};
+
+struct KV {
+    const void* q;
+    const void* k;
+    const void* v;
+    int64_t sb, sh, sn;   // element strides of (b, kv head, token)
+    int bf16;
+};
+
+// --- launchers (each returns the launch status) -----------------------
+hipError_t launch_lut(const Dims& D, const KV& kv, const Index& ix, const Work& w,
+                      hipStream_t s);
+hipError_t launch_sample(const Dims& D, const BatchInts& tk, const Index& ix, const Work& w,
+                         float bias, hipStream_t s);
+hipError_t launch_scan(const Dims& D, const Index& ix, const Work& w, const int2* wg_table,
+                       int n_wg, hipStream_t s);
+hipError_t launch_select(const Dims& D, const BatchInts& tk, const Index& ix, const Work& w,
+                         int force_fallback, hipStream_t s);
+hipError_t launch_attend(const Dims& D, const BatchInts& tk, const KV& kv, const Index& ix,
+                         const Work& w, int nsplit_max, hipStream_t s);
+hipError_t launch_merge(const Dims& D, const BatchInts& tk, const Work& w, float* out,
+                        int nsplit_max, hipStream_t s);
+hipError_t launch_dense(const Dims& D, const KV& kv, const BatchInts& lens, float* partial,
+                        float* out, int nsplit_max, hipStream_t s);
+hipError_t launch_prepare_gather(const Dims& D, const uint8_t* codes_in, const float* norms_in,
+                                 const Index& ix, uint8_t* codes_out, float* norms_out,
+                                 hipStream_t s);
+hipError_t launch_debug(const Dims& D, const BatchInts& tk, const Index& ix, const Work& w,
+                        int32_t* selected, int32_t* unselected, float* scores,
+                        hipStream_t s);
+
+}  // namespace pqhsa

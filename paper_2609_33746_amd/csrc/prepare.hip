@@ -1,0 +1,143 @@
+// Index preparation (list-major reorder of codes and norms) and the
+// diagnostics of pqhsa_decode_debug.
+#include "device_common.h"
+#include "pq_score.h"
+#include "pqhsa_internal.h"
+
+namespace pqhsa {
+
+// codes_out[bg][pos] = codes_in[bg][perm[pos]] (16 bytes), same for norms.
+__global__ __launch_bounds__(256) void gather_index_kernel(Dims D, const uint4* __restrict__ codes_in,
+                                                           const float* __restrict__ norms_in,
+                                                           Index ix, uint4* __restrict__ codes_out,
+                                                           float* __restrict__ norms_out) {
+    const int bg = blockIdx.y;
+    const int b = bg / D.Hkv;
+    const int pos = blockIdx.x * 256 + threadIdx.x;
+    if (pos >= ix.n_r[b]) return;
+    const int64_t base = static_cast<int64_t>(bg) * D.rcap;
+    const int tok = ix.perm[base + pos];
+    codes_out[base + pos] = codes_in[base + tok];
+    norms_out[base + pos] = norms_in[base + tok];
+}
+
+hipError_t launch_prepare_gather(const Dims& D, const uint8_t* codes_in, const float* norms_in,
+                                 const Index& ix, uint8_t* codes_out, float* norms_out,
+                                 hipStream_t s) {
+    dim3 grid((D.rcap + 255) / 256, D.B * D.Hkv);
+    hipLaunchKernelGGL(gather_index_kernel, grid, dim3(256), 0, s, D,
+                       reinterpret_cast<const uint4*>(codes_in), norms_in, ix,
+                       reinterpret_cast<uint4*>(codes_out), norms_out);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// diagnostics
+// ---------------------------------------------------------------------------
+constexpr int kDbgThreads = 256;
+constexpr int kSortCap = 8192;   // largest k whose selected set the debug call can sort
+
+__global__ void fill_f32_kernel(float* p, int64_t n, float v) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    if (i < n) p[i] = v;
+}
+
+// Approximate logit of every indexed token, scattered by token id.
+__global__ __launch_bounds__(kDbgThreads) void score_dump_kernel(Dims D, Index ix, Work w,
+                                                                 float* __restrict__ scores,
+                                                                 int64_t out_stride) {
+    __shared__ float lut_s[kLutRow];
+    const int row = blockIdx.y;
+    const int b = row / D.Hq;
+    const int h = row % D.Hq;
+    const int g = h / D.G;
+    const int hh = h % D.G;
+    const int bg = b * D.Hkv + g;
+    stage_head_lut<kDbgThreads>(lut_s, w.lut + static_cast<int64_t>(bg) * kLutRow * D.G, D.G, hh);
+    __syncthreads();
+    const int n_r = ix.n_r[b];
+    const int64_t base = static_cast<int64_t>(bg) * D.rcap;
+    const uint4* codes = reinterpret_cast<const uint4*>(ix.codes) + base;
+    const float* coarse = w.coarse + static_cast<int64_t>(bg) * D.n_list * D.G;
+    for (int pos = blockIdx.x * kDbgThreads + threadIdx.x; pos < n_r;
+         pos += gridDim.x * kDbgThreads) {
+        float fs[1];
+        fine_sum<1>(lut_s, codes[pos], fs);
+        const float s = pq_logit(ix.norms[base + pos], coarse[ix.pos_list[base + pos] * D.G + hh], fs[0]);
+        scores[row * out_stride + ix.perm[base + pos]] = s;
+    }
+}
+
+// Sort the selected token ids of each row ascending (bitonic, in LDS), pad with -1,
+// and count |B n R_j| = |R_j| - |T n R_j| per list.
+__global__ __launch_bounds__(kDbgThreads) void sel_debug_kernel(Dims D, BatchInts tk, Index ix,
+                                                                Work w, int32_t* __restrict__ selected,
+                                                                int32_t* __restrict__ unselected) {
+    __shared__ int keys[kSortCap];
+    __shared__ int counts[kMaxLists];
+    const int row = blockIdx.x;
+    const int b = row / D.Hq;
+    const int g = (row % D.Hq) / D.G;
+    const int bg = b * D.Hkv + g;
+    const int k = tk.v[b];
+    const int32_t* st = w.sel_tok + static_cast<int64_t>(row) * D.max_topk;
+    const int32_t* sp = w.sel_pos + static_cast<int64_t>(row) * D.max_topk;
+    if (selected) {
+        int n2 = 1;
+        while (n2 < k) n2 <<= 1;
+        for (int i = threadIdx.x; i < n2; i += kDbgThreads) keys[i] = i < k ? st[i] : 0x7fffffff;
+        __syncthreads();
+        for (int size = 2; size <= n2; size <<= 1) {
+            for (int stride = size >> 1; stride > 0; stride >>= 1) {
+                for (int i = threadIdx.x; i < n2; i += kDbgThreads) {
+                    const int j = i ^ stride;
+                    if (j > i) {
+                        const bool up = (i & size) == 0;
+                        const int a = keys[i], c = keys[j];
+                        if ((a > c) == up) {
+                            keys[i] = c;
+                            keys[j] = a;
+                        }
+                    }
+                }
+                __syncthreads();
+            }
+        }
+        int32_t* out = selected + static_cast<int64_t>(row) * D.max_topk;
+        for (int i = threadIdx.x; i < D.max_topk; i += kDbgThreads) out[i] = i < k ? keys[i] : -1;
+    }
+    if (unselected) {
+        const int32_t* loff = ix.loff + static_cast<int64_t>(bg) * (D.n_list + 1);
+        for (int j = threadIdx.x; j < D.n_list; j += kDbgThreads) counts[j] = loff[j + 1] - loff[j];
+        __syncthreads();
+        const int64_t base = static_cast<int64_t>(bg) * D.rcap;
+        for (int i = threadIdx.x; i < k; i += kDbgThreads) atomicSub(&counts[ix.pos_list[base + sp[i]]], 1);
+        __syncthreads();
+        int32_t* out = unselected + static_cast<int64_t>(row) * D.n_list;
+        for (int j = threadIdx.x; j < D.n_list; j += kDbgThreads) out[j] = counts[j];
+    }
+}
+
+hipError_t launch_debug(const Dims& D, const BatchInts& tk, const Index& ix, const Work& w,
+                        int32_t* selected, int32_t* unselected, float* scores, hipStream_t s) {
+    if (scores) {
+        const int64_t n = static_cast<int64_t>(D.B) * D.Hq * D.rcap;
+        hipLaunchKernelGGL(fill_f32_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0,
+                           s, scores, n, __builtin_nanf(""));
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        dim3 grid(64, D.B * D.Hq);
+        hipLaunchKernelGGL(score_dump_kernel, grid, dim3(kDbgThreads), 0, s, D, ix, w, scores,
+                           static_cast<int64_t>(D.rcap));
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    if (selected || unselected) {
+        hipLaunchKernelGGL(sel_debug_kernel, dim3(D.B * D.Hq), dim3(kDbgThreads), 0, s, D, tk, ix, w,
+                           selected, unselected);
+        return hipGetLastError();
+    }
+    return hipSuccess;
+}
+
+}  // namespace pqhsa

@@ -18,14 +18,14 @@ Recipe, per (batch element b, KV head g), from one SeedSequence per workload:
   stored (rounded) values, accumulated in float64 and stored as float32
   query of head h: q_h = t_h * k_{j_h}, j_h uniform over the indexed region of
   its own KV head, rounded to the cache dtype.
+Draws use torch generators on the target device, so the largest workloads
+(8.6 GB of K/V) are generated in place in device memory.
 """
 
 from __future__ import annotations
 
 import math
-import os
 import zlib
-from concurrent.futures import ThreadPoolExecutor
 from dataclasses import dataclass, replace
 
 import numpy as np
@@ -76,23 +76,27 @@ def ratio_topk(rho: float, n: int) -> int:
     return int(math.floor(rho * n + 0.5))
 
 
-def _bits_to_dtype(x: np.ndarray, kv_dtype: str) -> torch.Tensor:
-    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32))
-    return t.to(torch.bfloat16) if kv_dtype == "bf16" else t
+def _pair_seeds(root: np.random.SeedSequence, n: int) -> list[int]:
+    return [int(c.generate_state(1, dtype=np.uint64)[0] >> 1) for c in root.spawn(n)]
 
 
-def make_inputs(wl: Workload, seed: int = 0, *, noise: float = 0.05,
-                norm_variant: bool = False, list_constant_values: bool = False,
-                threads: int | None = None, seq_lens=None) -> dict:
-    """Draw one workload's inputs (CPU torch tensors; see module docstring).
+def make_inputs(wl: Workload, seed: int = 0, *, device: str | torch.device = "cpu",
+                noise: float = 0.05, norm_variant: bool = False,
+                list_constant_values: bool = False, seq_lens=None) -> dict:
+    """Draw one workload's inputs as torch tensors on `device`.
+
+    The draws are a function of (seed, workload name, device type): torch's
+    CPU and GPU generators differ, so the same seed gives different data on
+    the two; within one device type the result is deterministic.
 
     Returns a dict with the ABI's token-major layouts:
       q [B, Hq, d]; k_cache, v_cache [B, Hkv, Nmax, d] (kv dtype);
       list_ids int32 [B, Hkv, Nmax]; codes uint8 [B, Hkv, Nmax, M];
       norms float32 [B, Hkv, Nmax]; centroids float32 [B, Hkv, n_list, d];
       codebooks float32 [B, Hkv, M, ksub, d/M]; list_means float32
-      [B, Hkv, n_list, d]; seq_lens int32 [B]; topk int32 [B]; n_sink, n_local.
+      [B, Hkv, n_list, d]; seq_lens, topk int32 [B] (CPU); n_sink, n_local.
     """
+    device = torch.device(device)
     B, Hq, Hkv, d = wl.batch, wl.n_q_heads, wl.n_kv_heads, wl.head_dim
     M, ksub, n_list, Nmax = wl.pq_m, wl.pq_ksub, wl.n_list, wl.max_seq
     if d % M:
@@ -100,7 +104,7 @@ def make_inputs(wl: Workload, seed: int = 0, *, noise: float = 0.05,
     G = Hq // Hkv
     dsub = d // M
     root = np.random.SeedSequence([seed, zlib.crc32(wl.name.encode())])
-    seq_ss, *pair_ss = root.spawn(1 + B * Hkv)
+    seq_ss, pair_root = root.spawn(2)
     g0 = np.random.Generator(np.random.PCG64(seq_ss))
     if seq_lens is not None:
         lens = np.asarray(seq_lens, dtype=np.int64)
@@ -116,92 +120,88 @@ def make_inputs(wl: Workload, seed: int = 0, *, noise: float = 0.05,
         temps = 1.0 + 3.0 * np.arange(Hq) / max(Hq - 1, 1)
     else:
         temps = np.full(Hq, float(wl.temp))
+    seeds = _pair_seeds(pair_root, B * Hkv)
 
     kvt = torch.bfloat16 if wl.kv_dtype == "bf16" else torch.float32
-    k_cache = torch.zeros((B, Hkv, Nmax, d), dtype=kvt)
-    v_cache = torch.zeros((B, Hkv, Nmax, d), dtype=kvt)
-    q = torch.zeros((B, Hq, d), dtype=kvt)
-    list_ids = np.zeros((B, Hkv, Nmax), dtype=np.int32)
-    codes = np.zeros((B, Hkv, Nmax, M), dtype=np.uint8)
-    norms = np.ones((B, Hkv, Nmax), dtype=np.float32)
-    centroids = np.zeros((B, Hkv, n_list, d), dtype=np.float32)
-    codebooks = np.zeros((B, Hkv, M, ksub, dsub), dtype=np.float32)
-    list_means = np.zeros((B, Hkv, n_list, d), dtype=np.float32)
+    f32 = dict(dtype=torch.float32, device=device)
+    k_cache = torch.zeros((B, Hkv, Nmax, d), dtype=kvt, device=device)
+    v_cache = torch.zeros((B, Hkv, Nmax, d), dtype=kvt, device=device)
+    q = torch.zeros((B, Hq, d), dtype=kvt, device=device)
+    list_ids = torch.zeros((B, Hkv, Nmax), dtype=torch.int32, device=device)
+    codes = torch.zeros((B, Hkv, Nmax, M), dtype=torch.uint8, device=device)
+    norms = torch.ones((B, Hkv, Nmax), **f32)
+    centroids = torch.zeros((B, Hkv, n_list, d), **f32)
+    codebooks = torch.zeros((B, Hkv, M, ksub, dsub), **f32)
+    list_means = torch.zeros((B, Hkv, n_list, d), **f32)
+    m_idx = torch.arange(M, device=device)
 
-    def one(pair: int):
+    for pair in range(B * Hkv):
         b, g = divmod(pair, Hkv)
         n = int(lens[b])
-        rng = np.random.Generator(np.random.PCG64(pair_ss[pair]))
-        cen = rng.standard_normal((n_list, d))
-        cb = 0.3 * rng.standard_normal((M, ksub, dsub))
-        a = rng.integers(0, n_list, size=n)
-        z = rng.integers(0, ksub, size=(n, M))
-        recon = cen[a].astype(np.float32)
-        recon += cb[np.arange(M)[None, :], z].reshape(n, d).astype(np.float32)
+        gen = torch.Generator(device=device)
+        gen.manual_seed(seeds[pair])
+        cen = torch.randn((n_list, d), generator=gen, **f32)
+        cb = 0.3 * torch.randn((M, ksub, dsub), generator=gen, **f32)
+        a = torch.randint(0, n_list, (n,), generator=gen, device=device)
+        z = torch.randint(0, ksub, (n, M), generator=gen, device=device)
+        key = cen[a] + cb[m_idx[None, :], z].reshape(n, d)
         if noise:
-            recon += np.float32(noise) * rng.standard_normal((n, d), dtype=np.float32)
+            key += noise * torch.randn((n, d), generator=gen, **f32)
         if norm_variant:
-            s = np.exp(rng.uniform(math.log(0.5), math.log(2.0), size=n)).astype(np.float32)
-            recon *= s[:, None]
-        else:
-            s = np.ones(n, dtype=np.float32)
-        kt = _bits_to_dtype(recon, wl.kv_dtype)
-        del recon
-        off = rng.standard_normal((n_list, d)).astype(np.float32)
+            lo_s, hi_s = math.log(0.5), math.log(2.0)
+            s = torch.exp(lo_s + (hi_s - lo_s) * torch.rand((n,), generator=gen, **f32))
+            key *= s[:, None]
+            norms[b, g, :n] = s
+        kt = key.to(kvt)
+        del key
+        off = torch.randn((n_list, d), generator=gen, **f32)
         if list_constant_values:
             vals = 0.5 * off[a]
         else:
-            vals = rng.standard_normal((n, d), dtype=np.float32)
-            vals += 0.5 * off[a]
-        vt = _bits_to_dtype(vals, wl.kv_dtype)
+            vals = torch.randn((n, d), generator=gen, **f32) + 0.5 * off[a]
+        vt = vals.to(kvt)
         del vals
         k_cache[b, g, :n] = kt
         v_cache[b, g, :n] = vt
-        list_ids[b, g, :n] = a
-        codes[b, g, :n] = z
-        norms[b, g, :n] = s
+        list_ids[b, g, :n] = a.to(torch.int32)
+        codes[b, g, :n] = z.to(torch.uint8)
         centroids[b, g] = cen
         codebooks[b, g] = cb
         # list value means over the indexed region R_j of the stored values
         lo, hi = wl.n_sink, n - wl.n_local
-        vr = vt[lo:hi].double().numpy()
-        ar = a[lo:hi]
-        sums = np.zeros((n_list, d))
-        _segment_add(sums, ar, vr)
-        cnt = np.bincount(ar, minlength=n_list)
-        nz = cnt > 0
-        means = np.zeros((n_list, d))
-        means[nz] = sums[nz] / cnt[nz, None]
-        list_means[b, g] = means
+        list_means[b, g] = _list_means(vt[lo:hi], a[lo:hi], n_list)
         # queries of the G heads that share this KV head
+        if hi > lo:
+            js = torch.randint(lo, hi, (G,), generator=gen, device=device)
+        else:
+            js = torch.zeros(G, dtype=torch.long, device=device)
         for hh in range(G):
             h = g * G + hh
-            j = int(rng.integers(lo, hi)) if hi > lo else 0
-            q[b, h] = (kt[j].float() * float(temps[h])).to(kvt)
-
-    nthreads = threads or min(8, os.cpu_count() or 1)
-    if B * Hkv == 1 or nthreads == 1:
-        for p in range(B * Hkv):
-            one(p)
-    else:
-        with ThreadPoolExecutor(nthreads) as ex:
-            list(ex.map(one, range(B * Hkv)))
+            q[b, h] = (kt[js[hh]].float() * float(temps[h])).to(kvt)
 
     return dict(
-        q=q, k_cache=k_cache, v_cache=v_cache,
-        list_ids=torch.from_numpy(list_ids), codes=torch.from_numpy(codes),
-        norms=torch.from_numpy(norms), centroids=torch.from_numpy(centroids),
-        codebooks=torch.from_numpy(codebooks), list_means=torch.from_numpy(list_means),
+        q=q, k_cache=k_cache, v_cache=v_cache, list_ids=list_ids, codes=codes, norms=norms,
+        centroids=centroids, codebooks=codebooks, list_means=list_means,
         seq_lens=torch.from_numpy(lens.astype(np.int32)),
         topk=torch.from_numpy(topk.astype(np.int32)),
         n_sink=wl.n_sink, n_local=wl.n_local, workload=wl)
 
 
-def _segment_add(sums: np.ndarray, ids: np.ndarray, rows: np.ndarray) -> None:
-    """sums[j] += sum of rows with ids == j (sort + reduceat, float64)."""
-    if ids.shape[0] == 0:
-        return
-    order = np.argsort(ids, kind="stable")
-    ids_s = ids[order]
-    starts = np.flatnonzero(np.r_[True, ids_s[1:] != ids_s[:-1]])
-    sums[ids_s[starts]] += np.add.reduceat(rows[order], starts, axis=0)
+def _list_means(v: torch.Tensor, a: torch.Tensor, n_list: int) -> torch.Tensor:
+    """Float64 mean of the rows of v per list id (0 for an empty list), as float32.
+
+    Sort-and-difference of a float64 prefix sum: deterministic on every device.
+    """
+    d = v.shape[1]
+    if a.numel() == 0:
+        return torch.zeros((n_list, d), dtype=torch.float32, device=v.device)
+    order = torch.argsort(a, stable=True)
+    cs = torch.cumsum(v[order].double(), dim=0)
+    counts = torch.bincount(a, minlength=n_list)
+    ends = torch.cumsum(counts, 0)
+    starts = ends - counts
+    zero = torch.zeros((1, d), dtype=torch.float64, device=v.device)
+    csz = torch.cat([zero, cs], dim=0)
+    tot = csz[ends] - csz[starts]
+    means = tot / counts.clamp(min=1)[:, None].double()
+    return means.float()

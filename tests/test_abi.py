@@ -1,0 +1,68 @@
+"""The C-ABI library loads and exports every declared symbol; shape and
+argument validation that happens before any HIP call (CPU only)."""
+
+import ctypes
+
+import pytest
+
+from paper_2609_33746_amd import pqhsa
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return pqhsa.load_library()
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = pqhsa.declared_functions()
+    assert len(names) >= 11
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def shape(**kw):
+    base = dict(batch=1, n_q_heads=32, n_kv_heads=8, head_dim=128, max_seq=4096, n_list=16,
+                pq_m=16, pq_ksub=256, n_sink=4, n_local=128, max_topk=64, kv_dtype=pqhsa.BF16)
+    base.update(kw)
+    return pqhsa.Shape(**base)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(head_dim=64), pqhsa.ERR_UNSUPPORTED),
+    (dict(pq_m=8), pqhsa.ERR_UNSUPPORTED),
+    (dict(pq_ksub=16), pqhsa.ERR_UNSUPPORTED),
+    (dict(n_q_heads=24, n_kv_heads=2), pqhsa.ERR_UNSUPPORTED),      # G = 12
+    (dict(n_kv_heads=7), pqhsa.ERR_INVALID_ARGUMENT),               # 32 % 7
+    (dict(batch=0), pqhsa.ERR_INVALID_ARGUMENT),
+    (dict(batch=257), pqhsa.ERR_UNSUPPORTED),
+    (dict(n_list=0), pqhsa.ERR_INVALID_ARGUMENT),
+    (dict(n_list=4097), pqhsa.ERR_UNSUPPORTED),
+    (dict(max_topk=-1), pqhsa.ERR_INVALID_ARGUMENT),
+    (dict(max_topk=5000), pqhsa.ERR_INVALID_ARGUMENT),
+    (dict(n_sink=4000, n_local=128), pqhsa.ERR_INVALID_ARGUMENT),
+    (dict(n_local=-1), pqhsa.ERR_INVALID_ARGUMENT),
+    (dict(kv_dtype=7), pqhsa.ERR_UNSUPPORTED),
+])
+def test_create_rejects_bad_shapes_before_touching_the_device(lib, kw, status):
+    ctx = ctypes.c_void_p(1234)
+    s = shape(**kw)
+    assert lib.pqhsa_create(ctypes.byref(s), ctypes.byref(ctx)) == status
+    assert ctx.value is None
+    assert lib.pqhsa_last_error(None)
+
+
+def test_null_arguments(lib):
+    assert lib.pqhsa_create(None, None) == pqhsa.ERR_INVALID_ARGUMENT
+    ctx = ctypes.c_void_p()
+    assert lib.pqhsa_create(None, ctypes.byref(ctx)) == pqhsa.ERR_INVALID_ARGUMENT
+    for fn, nargs in (("pqhsa_decode", 8), ("pqhsa_dense_decode", 8), ("pqhsa_index_export", 4)):
+        assert getattr(lib, fn)(*([None] * nargs)) == pqhsa.ERR_INVALID_ARGUMENT
+    assert lib.pqhsa_index_prepare(*([None] * 9)) == pqhsa.ERR_INVALID_ARGUMENT
+    assert lib.pqhsa_set_option(None, 1, 1) == pqhsa.ERR_INVALID_ARGUMENT
+    lib.pqhsa_destroy(None)
+
+
+def test_status_strings(lib):
+    for st in range(6):
+        assert lib.pqhsa_status_string(st)
+    assert lib.pqhsa_status_string(99) == b"unknown status"

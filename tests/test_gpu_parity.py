@@ -1,0 +1,264 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Element-by-element at sizes the oracle finishes in seconds (several scan
+tiles and a ragged tail), on every query row of the 32K workload, and on
+sampled rows of the 128K workloads at full size in the launch configuration
+the benchmark times.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import check_rows, context, make, run, say
+from oracle import pqhsa_ref as R
+from paper_2609_33746_amd import pqhsa, synth
+
+pytestmark = pytest.mark.gpu
+
+
+def small(idx, **kw):
+    return synth.workload(idx, **kw)
+
+
+# ---------------------------------------------------------------------------
+# index preparation: list-major layout, bit-exact
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("wl", [
+    small(0),
+    small(4, max_seq=6000, ragged_min=3000, batch=3, n_q_heads=8, n_kv_heads=2, n_list=37),
+], ids=["tiny", "ragged"])
+def test_prepare_layout_is_stable_list_major_sort(wl):
+    inp = make(wl, seed=1)
+    ctx = context(inp)
+    perm, offs = ctx.index_export()
+    perm, offs = perm.cpu().numpy(), offs.cpu().numpy()
+    ids = inp["list_ids"].cpu().numpy()
+    for b in range(wl.batch):
+        n = int(inp["seq_lens"][b])
+        Rr = np.arange(wl.n_sink, n - wl.n_local)
+        for g in range(wl.n_kv_heads):
+            a = ids[b, g, Rr]
+            order = np.argsort(a, kind="stable")
+            np.testing.assert_array_equal(perm[b, g, :Rr.size], Rr[order])
+            assert np.all(perm[b, g, Rr.size:] == -1)
+            cnt = np.bincount(a, minlength=wl.n_list)
+            np.testing.assert_array_equal(offs[b, g], np.concatenate([[0], np.cumsum(cnt)]))
+
+
+# ---------------------------------------------------------------------------
+# end to end, every row
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("idx", [0, 1])
+def test_workload_every_row(idx):
+    wl = synth.workload(idx)
+    inp = make(wl)
+    ctx = context(inp)
+    topk, out, sel, unsel, sc = run(ctx, inp, scores=True)
+    rows = [(b, h) for b in range(wl.batch) for h in range(wl.n_q_heads)]
+    check_rows(inp, topk, rows, out, sel, unsel, sc)
+
+
+@pytest.mark.parametrize("idx", [0, 1])
+def test_norm_variant(idx):
+    """Key norms outside the quantizer (r_i != 1)."""
+    wl = synth.workload(idx)
+    inp = make(wl, seed=3, norm_variant=True)
+    ctx = context(inp)
+    topk, out, sel, unsel, sc = run(ctx, inp, scores=True)
+    rows = [(b, h) for b in range(wl.batch) for h in range(0, wl.n_q_heads, 3)]
+    check_rows(inp, topk, rows, out, sel, unsel, sc)
+
+
+# ---------------------------------------------------------------------------
+# full-size workloads (the benchmark's launch configuration), sampled rows
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("idx,rows_per_b", [(2, 32), (3, 6), (4, 2)])
+def test_full_size_workloads(idx, rows_per_b):
+    wl = synth.workload(idx)
+    inp = make(wl)
+    ctx = context(inp)
+    topk, out, sel, unsel, sc = run(ctx, inp, scores=idx == 2)
+    rng = np.random.default_rng(idx)
+    rows = []
+    for b in range(wl.batch):
+        hs = range(wl.n_q_heads) if rows_per_b >= wl.n_q_heads else \
+            sorted(rng.choice(wl.n_q_heads, rows_per_b, replace=False).tolist())
+        rows += [(b, int(h)) for h in hs]
+    check_rows(inp, topk, rows, out, sel, unsel, sc)
+    # properties that hold on every row
+    assert torch.isfinite(out).all()
+    for b in range(wl.batch):
+        k = topk[b]
+        s = sel[b, :, :k]
+        assert bool((s[:, 1:] > s[:, :-1]).all()) if k > 1 else True
+        n = int(inp["seq_lens"][b])
+        assert int(s.min()) >= wl.n_sink and int(s.max()) < n - wl.n_local
+        u = unsel[b].sum(dim=1)
+        assert bool((u == n - wl.n_sink - wl.n_local - k).all())
+
+
+# ---------------------------------------------------------------------------
+# edge cases of the method
+# ---------------------------------------------------------------------------
+EDGE = {
+    # several scan tiles and a ragged tail: |R| = 4868 = 19 x 256 + 4
+    "ragged-tail-g4": (small(1, max_seq=5000, n_list=64, topk=97), {}),
+    "g1-f32": (small(0, max_seq=3000, n_list=8, topk=30), {}),
+    "g2": (small(1, max_seq=3000, n_q_heads=4, n_kv_heads=2, n_list=16, topk=50), {}),
+    "g8": (small(3, batch=2, max_seq=3000, n_q_heads=16, n_kv_heads=2, n_list=16, topk=60), {}),
+    "k0": (small(1, max_seq=3000, n_list=16, topk=0), {}),
+    "k-all": (small(1, max_seq=2000, n_list=16, topk=2000 - 132), {}),
+    "no-sink-no-window": (small(1, max_seq=3000, n_list=16, topk=40, n_sink=0, n_local=0), {}),
+    "k0-no-window": (small(0, max_seq=3000, n_list=16, topk=0, n_sink=0, n_local=0), {}),
+    "one-list": (small(1, max_seq=3000, n_list=1, topk=40), {}),
+    "many-empty-lists": (small(1, max_seq=2000, n_list=4096, topk=40), {}),
+    "tiny-lists": (small(1, max_seq=3000, n_list=1500, topk=40), {}),
+    "diffuse-query": (small(1, max_seq=6000, n_list=64, topk=60, temp="0.3"), {}),
+    "ragged-batch": (small(4, batch=5, max_seq=6000, ragged_min=2500, n_list=40), {}),
+    "window-only": (small(1, max_seq=132, n_list=4, topk=0), {}),
+    "list-constant-values": (small(0, max_seq=3000, n_list=8, topk=30), dict(list_constant_values=True, noise=0.0)),
+}
+
+
+@pytest.mark.parametrize("name", list(EDGE))
+def test_edge_cases(name):
+    wl, kw = EDGE[name]
+    inp = make(wl, seed=7, **kw)
+    ctx = context(inp)
+    topk, out, sel, unsel, sc = run(ctx, inp, scores=True)
+    rows = [(b, h) for b in range(wl.batch) for h in range(wl.n_q_heads)]
+    check_rows(inp, topk, rows, out, sel, unsel, sc)
+
+
+def test_k_all_is_dense_attention():
+    """rho = 1: the background is empty and the output is dense attention."""
+    wl = small(1, max_seq=2000, n_list=16, topk=2000 - 132)
+    inp = make(wl, seed=2)
+    ctx = context(inp)
+    topk, out, *_ = run(ctx, inp)
+    for h in range(wl.n_q_heads):
+        y = R.dense_attention_ref(inp["q"][0, h].double().cpu().numpy(),
+                                  inp["k_cache"][0, h // 4].double().cpu().numpy(),
+                                  inp["v_cache"][0, h // 4].double().cpu().numpy())
+        got = out[0, h].double().cpu().numpy()
+        assert np.max(np.abs(got - y)) / np.max(np.abs(y)) <= 2e-3
+
+
+# ---------------------------------------------------------------------------
+# the exact re-scan path of the top-k stage
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("mode", ["forced", "starved-threshold"])
+@pytest.mark.parametrize("topk", [0, 37])
+def test_rescan_path(mode, topk):
+    wl = small(1, max_seq=5000, n_list=64, topk=topk)
+    inp = make(wl, seed=11)
+    ctx = context(inp)
+    if mode == "forced":
+        ctx.set_option(pqhsa.OPT_FORCE_FALLBACK, 1)
+    else:
+        ctx.set_option(pqhsa.OPT_THRESHOLD_BIAS, 1_000_000)   # +1000 on every threshold
+    topk_l, out, sel, unsel, sc = run(ctx, inp, scores=True)
+    rows = [(0, h) for h in range(wl.n_q_heads)]
+    check_rows(inp, topk_l, rows, out, sel, unsel, sc)
+    ctx.set_option(pqhsa.OPT_FORCE_FALLBACK, 0)
+    ctx.set_option(pqhsa.OPT_THRESHOLD_BIAS, 0)
+    _, out2, sel2, *_ = run(ctx, inp)
+    assert torch.equal(sel2, sel)
+    assert float((out2 - out).abs().max()) <= 1e-4 * float(out.abs().max())
+
+
+# ---------------------------------------------------------------------------
+# repeatability and the plain decode entry point
+# ---------------------------------------------------------------------------
+def test_repeatable_and_plain_decode_matches_debug():
+    wl = small(1, max_seq=8192, n_list=64, topk=160)
+    inp = make(wl, seed=5)
+    ctx = context(inp)
+    topk, out, sel, unsel, _ = run(ctx, inp)
+    _, out_b, sel_b, unsel_b, _ = run(ctx, inp)
+    assert torch.equal(sel, sel_b) and torch.equal(unsel, unsel_b)
+    assert float((out - out_b).abs().max()) <= 1e-6 * float(out.abs().max())
+    plain = ctx.decode(inp["q"], inp["k_cache"], inp["v_cache"], topk)
+    torch.cuda.synchronize()
+    assert float((plain - out).abs().max()) <= 1e-6 * float(out.abs().max())
+
+
+def test_strided_cache_view():
+    """A cache viewed through larger strides (padded token rows) is read in place."""
+    wl = small(1, max_seq=3000, n_list=16, topk=40)
+    inp = make(wl, seed=4)
+    ctx = context(inp)
+    topk, ref_out, *_ = run(ctx, inp)
+    big_k = torch.zeros((1, 8, 3000, 256), dtype=torch.bfloat16, device="cuda")
+    big_v = torch.zeros_like(big_k)
+    big_k[..., 64:192] = inp["k_cache"]
+    big_v[..., 64:192] = inp["v_cache"]
+    out = ctx.decode(inp["q"], big_k[..., 64:192], big_v[..., 64:192], topk)
+    torch.cuda.synchronize()
+    assert float((out - ref_out).abs().max()) <= 1e-6 * float(ref_out.abs().max())
+
+
+# ---------------------------------------------------------------------------
+# dense baseline
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("wl", [small(0), small(1, max_seq=5000), small(4, batch=3, max_seq=6000,
+                                                                         ragged_min=1000, n_list=8),
+                                small(3, batch=1, max_seq=3000, n_list=8, topk=10)],
+                         ids=["f32", "bf16", "ragged", "g8"])
+def test_dense_decode(wl):
+    inp = make(wl, seed=9)
+    ctx = pqhsa.context_for(inp)
+    lens = inp["seq_lens"].tolist()
+    say(f"[dense] lens={lens}")
+    out = ctx.dense_decode(inp["q"], inp["k_cache"], inp["v_cache"], lens)
+    torch.cuda.synchronize()
+    G = wl.n_q_heads // wl.n_kv_heads
+    for b in range(wl.batch):
+        n = lens[b]
+        for h in range(wl.n_q_heads):
+            y = R.dense_attention_ref(inp["q"][b, h].double().cpu().numpy(),
+                                      inp["k_cache"][b, h // G, :n].double().cpu().numpy(),
+                                      inp["v_cache"][b, h // G, :n].double().cpu().numpy())
+            got = out[b, h].double().cpu().numpy()
+            assert np.max(np.abs(got - y)) / np.max(np.abs(y)) <= 2e-3, (b, h)
+    # cross-check against torch's attention in float32 for the first sequence
+    b = 0
+    n = lens[b]
+    qf = inp["q"][b].float()[None, :, None, :]
+    kf = inp["k_cache"][b, :, :n].float().repeat_interleave(G, dim=0)[None].contiguous()
+    vf = inp["v_cache"][b, :, :n].float().repeat_interleave(G, dim=0)[None].contiguous()
+    ref = torch.nn.functional.scaled_dot_product_attention(qf, kf, vf)[0, :, 0]
+    assert float((ref - out[b]).abs().max()) <= 2e-3 * float(ref.abs().max())
+
+
+# ---------------------------------------------------------------------------
+# argument checks that need a device
+# ---------------------------------------------------------------------------
+def test_abi_errors_on_gpu():
+    wl = small(1, max_seq=3000, n_list=16, topk=40)
+    inp = make(wl, seed=1)
+    ctx = pqhsa.context_for(inp)
+    with pytest.raises(pqhsa.PQHSAError) as e:
+        ctx.decode(inp["q"], inp["k_cache"], inp["v_cache"], [40])
+    assert e.value.status == pqhsa.ERR_NOT_PREPARED
+    bad = inp["list_ids"].clone()
+    bad[0, 3, 500] = 16
+    with pytest.raises(pqhsa.PQHSAError) as e:
+        ctx.index_prepare([3000], bad, inp["codes"], inp["norms"], inp["centroids"],
+                          inp["codebooks"], inp["list_means"])
+    assert e.value.status == pqhsa.ERR_INVALID_ARGUMENT
+    with pytest.raises(pqhsa.PQHSAError) as e:
+        ctx.index_prepare([100], inp["list_ids"], inp["codes"], inp["norms"], inp["centroids"],
+                          inp["codebooks"], inp["list_means"])
+    assert e.value.status == pqhsa.ERR_INVALID_ARGUMENT
+    pqhsa.prepare_from(ctx, inp)
+    for k in (-1, 41, 3000):
+        with pytest.raises(pqhsa.PQHSAError) as e:
+            ctx.decode(inp["q"], inp["k_cache"], inp["v_cache"], [k])
+        assert e.value.status == pqhsa.ERR_INVALID_ARGUMENT
+    with pytest.raises(pqhsa.PQHSAError):
+        ctx.dense_decode(inp["q"], inp["k_cache"], inp["v_cache"], [0])
+    out = ctx.decode(inp["q"], inp["k_cache"], inp["v_cache"], [40])
+    torch.cuda.synchronize()
+    assert torch.isfinite(out).all()
