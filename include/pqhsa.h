@@ -51,7 +51,7 @@ typedef enum {
 typedef enum { PQHSA_F32 = 0, PQHSA_BF16 = 1 } pqhsa_dtype;
 
 /* Problem shape, fixed for the life of a context.
- * Supported: head_dim = 128, pq_m = 16 (8-dimensional subspaces),
+ * Supported: head_dim = 128, pq_m = 16 (8-dimensional subspaces), max_seq <= 2^20,
  * pq_ksub = 256 (one uint8 code per subspace), 1 <= n_list <= 4096,
  * G in {1, 2, 4, 8}, 1 <= batch <= 256, kv_dtype F32 or BF16 (the query has
  * the same dtype as the cache), 0 <= max_topk <= max_seq. */

@@ -47,7 +47,7 @@ struct pqhsa_ctx {
     float* means = nullptr;
     int32_t* n_seq_dev = nullptr;
     int32_t* n_r_dev = nullptr;
-    int2* scan_table = nullptr;
+    ScanWG* scan_table = nullptr;
     int n_scan_wg = 0;
 
     // workspace
@@ -131,6 +131,7 @@ pqhsa_status check_shape(const pqhsa_shape* s) {
         return fail(nullptr, PQHSA_ERR_UNSUPPORTED, "GQA group size must be 1, 2, 4 or 8");
     if (s->batch > kMaxBatch) return fail(nullptr, PQHSA_ERR_UNSUPPORTED, "batch must be <= 256");
     if (s->n_list > kMaxLists) return fail(nullptr, PQHSA_ERR_UNSUPPORTED, "n_list must be <= 4096");
+    if (s->max_seq > kMaxSeq) return fail(nullptr, PQHSA_ERR_UNSUPPORTED, "max_seq must be <= 2^20");
     return PQHSA_OK;
 }
 
@@ -206,9 +207,11 @@ pqhsa_status pqhsa_create(const pqhsa_shape* shape, pqhsa_ctx** out) {
     if (!c) return fail(nullptr, PQHSA_ERR_OUT_OF_MEMORY, "host allocation failed");
     c->shape = *shape;
     hipError_t e = hipGetDevice(&c->device);
+    if (e == hipSuccess) e = configure_scan();
+    if (e == hipSuccess) e = configure_select();
     if (e != hipSuccess) {
         delete c;
-        return fail(nullptr, PQHSA_ERR_HIP, "hipGetDevice: %s", hipGetErrorString(e));
+        return fail(nullptr, PQHSA_ERR_HIP, "device set-up: %s", hipGetErrorString(e));
     }
     Dims& D = c->D;
     D.B = shape->batch;
@@ -256,7 +259,6 @@ pqhsa_status pqhsa_create(const pqhsa_shape* shape, pqhsa_ctx** out) {
     A(dev_alloc(c, &w.seg_sum, BG * D.nseg_cap * G));
     A(dev_alloc(c, &w.comp_key, BQ * rc));
     A(dev_alloc(c, &w.comp_pos, BQ * rc));
-    A(dev_alloc(c, &w.sel_tok, BQ * D.max_topk));
     A(dev_alloc(c, &w.sel_pos, BQ * D.max_topk));
     A(dev_alloc(c, &w.cand_mass, BQ * L));
     A(dev_alloc(c, &w.row_shift, BQ));
@@ -307,7 +309,7 @@ pqhsa_status pqhsa_index_prepare(pqhsa_ctx* c, const int32_t* seq_lens, const in
     // stable counting sort of R_b by list id, per (b, kv head)
     std::vector<int32_t> perm(BG * rc, -1), pos_list(BG * rc, 0), loff(BG * (L + 1)),
         seg0(BG * (L + 1));
-    std::vector<int2> table;
+    std::vector<ScanWG> table;
     std::vector<int32_t> cnt(L);
     for (int b = 0; b < B; ++b) {
         for (int g = 0; g < Hkv; ++g) {
@@ -338,7 +340,14 @@ pqhsa_status pqhsa_index_prepare(pqhsa_ctx* c, const int32_t* seq_lens, const in
                 pl[p] = a[i];
             }
             const int nsub = (nr[b] + kSub - 1) / kSub;
-            for (int s0 = 0; s0 < nsub; s0 += kScanWaves) table.push_back(make_int2(static_cast<int>(bg), s0));
+            for (int s0 = 0; s0 < nsub; s0 += kScanWaves) {
+                ScanWG e{};
+                e.bg = static_cast<int>(bg);
+                e.sub0 = s0;
+                for (int wv = 0; wv < kScanWaves; ++wv)
+                    e.list0[wv] = s0 + wv < nsub ? pl[(s0 + wv) * kSub] : 0;
+                table.push_back(e);
+            }
         }
     }
 
@@ -354,7 +363,7 @@ pqhsa_status pqhsa_index_prepare(pqhsa_ctx* c, const int32_t* seq_lens, const in
     H2D(c->seg0, seg0.data(), seg0.size() * 4);
     H2D(c->n_seq_dev, lens.data(), B * 4);
     H2D(c->n_r_dev, nr.data(), B * 4);
-    if (!table.empty()) H2D(c->scan_table, table.data(), table.size() * sizeof(int2));
+    if (!table.empty()) H2D(c->scan_table, table.data(), table.size() * sizeof(ScanWG));
     D2D(c->centroids, centroids, BG * L * kHeadDim * 4);
     D2D(c->codebooks, codebooks, BG * kPqM * kKsub * kDsub * 4);
     D2D(c->means, list_means, BG * L * kHeadDim * 4);

@@ -7,12 +7,14 @@
 // be known in advance.
 //
 //  * attend_kernel, exact role: one workgroup per (row, split of kAttnRows
-//    rows of E). 16 lanes hold one K/V row (8 elements each); a wave keeps 4
-//    rows in flight and runs an online softmax per 16-lane group.
+//    rows of E). 16 lanes hold one K/V row (8 elements each); each 16-lane
+//    group owns kAttnRows / 16 rows and issues all of their token-id, K and V
+//    loads before any arithmetic, so a workgroup keeps its whole split in
+//    flight.
 //  * attend_kernel, background role: one workgroup per (batch element, KV
 //    head, kBgLists lists). For each list j and each of the G query heads:
 //    M_j = (below-threshold mass of the scan segments) * exp(tau_lo - shift)
-//          + (unselected-candidate mass of the top-k stage),
+//          + (weights of the list's unselected candidates from the top-k stage),
 //    then Z_B += M_j and N_B += M_j * v_bar_j (Eq. 4), reading each list mean
 //    once for the whole group.
 //  * merge_kernel: log-sum-exp of all partials of a row, y = N / Z (Eq. 5).
@@ -23,6 +25,12 @@ namespace pqhsa {
 
 constexpr int kAttnThreads = 256;    // 4 waves x 4 groups of 16 lanes = 16 row streams
 constexpr int kStreams = kAttnThreads / 16;
+constexpr int kRowsPerStream = kAttnRows / kStreams;
+// rows per stream in flight in the dense kernel (fewer for large groups, which
+// hold G accumulators per lane)
+template <int G>
+struct DenseBatch { static constexpr int value = G <= 2 ? 8 : (G == 4 ? 4 : 2); };
+constexpr int kMergeThreads = kHeadDim;
 
 struct Online {
     float m, z, acc[8];
@@ -35,13 +43,27 @@ __device__ __forceinline__ void online_init(Online& o) {
     for (int t = 0; t < 8; ++t) o.acc[t] = 0.0f;
 }
 
-__device__ __forceinline__ void online_push(Online& o, float logit, const float (&v)[8]) {
-    const float m_new = fmaxf(o.m, logit);
-    const float a = __expf(o.m - m_new);   // 0 when o.m = -inf
-    const float p = __expf(logit - m_new);
-    o.z = o.z * a + p;
+// Fold R rows (logits l[i], -inf for absent rows; values v[i]) into o.
+template <int R, typename T>
+__device__ __forceinline__ void online_push_batch(Online& o, const float (&l)[R],
+                                                  const Raw8<T> (&v)[R]) {
+    float m_new = o.m;
 #pragma unroll
-    for (int t = 0; t < 8; ++t) o.acc[t] = o.acc[t] * a + p * v[t];
+    for (int i = 0; i < R; ++i) m_new = fmaxf(m_new, l[i]);
+    if (m_new == -__builtin_huge_valf()) return;   // nothing present yet
+    const float a = __expf(o.m - m_new);            // 0 when o.m = -inf
+    o.z *= a;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) o.acc[t] *= a;
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+        const float p = __expf(l[i] - m_new);       // 0 for absent rows
+        float x[8];
+        v[i].to(x);
+        o.z += p;
+#pragma unroll
+        for (int t = 0; t < 8; ++t) o.acc[t] = fmaf(p, x[t], o.acc[t]);
+    }
     o.m = m_new;
 }
 
@@ -61,13 +83,15 @@ __device__ __forceinline__ void block_combine(const Online& o, float* sm, float*
     if (threadIdx.x < kHeadDim) {
         const int t = threadIdx.x;
         float M = -__builtin_huge_valf();
+#pragma unroll
         for (int s = 0; s < kStreams; ++s) M = fmaxf(M, sm[s]);
         float Z = 0.0f, N = 0.0f;
         if (M != -__builtin_huge_valf()) {
+#pragma unroll
             for (int s = 0; s < kStreams; ++s) {
                 const float f = __expf(sm[s] - M);
-                Z += sz[s] * f;
-                N += sacc[s * kHeadDim + t] * f;
+                Z = fmaf(sz[s], f, Z);
+                N = fmaf(sacc[s * kHeadDim + t], f, N);
             }
         }
         if (t == 0) {
@@ -86,10 +110,12 @@ __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchInts 
     __shared__ float sm[kStreams], sz[kStreams];
     // [16 streams][d] for the exact role, [4 waves][G][d] for the background role
     __shared__ float sacc[(kStreams > 4 * G ? kStreams : 4 * G) * kHeadDim];
+    __shared__ float bz[4][G];
     const int n_exact_wg = D.B * D.Hq * nsplit_max;
     const int P = nsplit_max + n_bgc;
     const int lane16 = threadIdx.x & 15;
     const int stream = threadIdx.x >> 4;
+    const float neg_inf = -__builtin_huge_valf();
 
     if (static_cast<int>(blockIdx.x) < n_exact_wg) {
         // ---------------- exact attention over a split of E ----------------
@@ -104,37 +130,63 @@ __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchInts 
         const int e0 = split * kAttnRows;
         if (e0 >= nE) return;   // the merge reads only the splits that exist
         const int e1 = min(e0 + kAttnRows, nE);
-        const T* qp = static_cast<const T*>(kv.q) + static_cast<int64_t>(row) * kHeadDim + lane16 * 8;
-        float qv[8];
-        Load8<T>::run(qp, qv);
+        const int32_t* sel = w.sel_pos + static_cast<int64_t>(row) * D.max_topk;
+        const int32_t* perm = ix.perm + static_cast<int64_t>(b * D.Hkv + g) * D.rcap;
+        const int n_r = ix.n_r[b];
+        const int local0 = n_seq - D.n_local;
+        int pos[kRowsPerStream];
+#pragma unroll
+        for (int i = 0; i < kRowsPerStream; ++i) {
+            const int e = e0 + stream + i * kStreams - D.n_sink - D.n_local;
+            pos[i] = (e >= 0 && e + D.n_sink + D.n_local < e1) ? sel[e] : -1;
+        }
+        int tok[kRowsPerStream];
+#pragma unroll
+        for (int i = 0; i < kRowsPerStream; ++i) {
+            const int e = e0 + stream + i * kStreams;
+            int t = -1;
+            if (e < e1) {
+                if (e < D.n_sink) t = e;
+                else if (e < D.n_sink + D.n_local) t = local0 + (e - D.n_sink);
+                else t = perm[min(max(pos[i], 0), n_r - 1)];   // never outside R
+            }
+            tok[i] = t;
+        }
         const T* kb = static_cast<const T*>(kv.k) + b * kv.sb + g * kv.sh + lane16 * 8;
         const T* vb = static_cast<const T*>(kv.v) + b * kv.sb + g * kv.sh + lane16 * 8;
-        const int32_t* sel = w.sel_tok + static_cast<int64_t>(row) * D.max_topk;
-        const int local0 = n_seq - D.n_local;
-        Online o;
-        online_init(o);
-        for (int e = e0 + stream; e < e1; e += kStreams) {
-            int tok;
-            if (e < D.n_sink) tok = e;
-            else if (e < D.n_sink + D.n_local) tok = local0 + (e - D.n_sink);
-            else tok = sel[e - D.n_sink - D.n_local];
-            tok = min(max(tok, 0), n_seq - 1);   // never read outside the sequence
-            float kf[8], vf[8];
-            Load8<T>::run(kb + tok * kv.sn, kf);
-            Load8<T>::run(vb + tok * kv.sn, vf);
+        Raw8<T> kr[kRowsPerStream], vr[kRowsPerStream];
+#pragma unroll
+        for (int i = 0; i < kRowsPerStream; ++i) {
+            if (tok[i] >= 0) {
+                kr[i].load(kb + tok[i] * kv.sn);
+                vr[i].load(vb + tok[i] * kv.sn);
+            } else {
+                kr[i].zero();
+                vr[i].zero();
+            }
+        }
+        float qv[8];
+        Load8<T>::run(static_cast<const T*>(kv.q) + static_cast<int64_t>(row) * kHeadDim + lane16 * 8, qv);
+        float l[kRowsPerStream];
+#pragma unroll
+        for (int i = 0; i < kRowsPerStream; ++i) {
+            float kf[8];
+            kr[i].to(kf);
             float dot = 0.0f;
 #pragma unroll
             for (int t = 0; t < 8; ++t) dot = fmaf(qv[t], kf[t], dot);
             dot = sum16(dot);
-            online_push(o, dot * D.inv_sqrt_d, vf);
+            l[i] = tok[i] >= 0 ? dot * D.inv_sqrt_d : neg_inf;
         }
+        Online o;
+        online_init(o);
+        online_push_batch<kRowsPerStream>(o, l, vr);
         block_combine(o, sm, sz, sacc,
                       w.partial + (static_cast<int64_t>(row) * P + split) * kPartStride);
         return;
     }
 
     // ---------------- per-list background (Eq. 4) ----------------
-    __shared__ float bz[4][G];
     const int idx = blockIdx.x - n_exact_wg;
     const int bg = idx / n_bgc;
     const int lc = idx % n_bgc;
@@ -143,7 +195,8 @@ __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchInts 
     const int row0 = b * D.Hq + g * G;
     const int wave = threadIdx.x / kWave;
     const int lane = lane_id();
-    const float neg_inf = -__builtin_huge_valf();
+    constexpr int kWaves = kAttnThreads / kWave;
+    constexpr int kListsPerWave = kBgLists / kWaves;   // 16
 
     float shift[G], below_scale[G];
     bool live[G];
@@ -155,28 +208,46 @@ __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchInts 
         const bool use_below = live[hh] && tlo != neg_inf && w.row_flag[row0 + hh] == 0;
         below_scale[hh] = use_below ? __expf(tlo - shift[hh]) : 0.0f;
     }
-    float Z[G], N[G][2];
-#pragma unroll
-    for (int hh = 0; hh < G; ++hh) { Z[hh] = 0.0f; N[hh][0] = 0.0f; N[hh][1] = 0.0f; }
-
-    const int j0 = lc * kBgLists;
-    const int j1 = min(j0 + kBgLists, D.n_list);
-    const int32_t* seg0 = ix.seg0 + static_cast<int64_t>(bg) * (D.n_list + 1);
-    const float* segs = w.seg_sum + static_cast<int64_t>(bg) * D.nseg_cap * G;
-    for (int j = j0 + wave; j < j1; j += kAttnThreads / kWave) {
-        const int s0 = seg0[j], s1 = seg0[j + 1];
-        const float2 vbar = *reinterpret_cast<const float2*>(
-            ix.means + (static_cast<int64_t>(bg) * D.n_list + j) * kHeadDim + 2 * lane);
+    // lanes 0..15 each compute the masses M_j of one list of this wave:
+    // M_j = (scan segments below tau_lo) * exp(tau_lo - shift)
+    //       + (unselected candidates of list j, already relative to shift)
+    const int my_j = lc * kBgLists + wave + (lane & (kListsPerWave - 1)) * kWaves;
+    float mj[G];
+    {
+        const bool ok = lane < kListsPerWave && my_j < D.n_list;
+        const int jj = ok ? my_j : 0;
+        const int32_t* seg0 = ix.seg0 + static_cast<int64_t>(bg) * (D.n_list + 1);
+        const int s0 = seg0[jj];
+        const int s1 = ok ? seg0[jj + 1] : s0;
+        const float* segs = w.seg_sum + static_cast<int64_t>(bg) * D.nseg_cap * G;
 #pragma unroll
         for (int hh = 0; hh < G; ++hh) {
             float below = 0.0f;
             for (int s = s0; s < s1; ++s) below += segs[s * G + hh];
-            float Mj = below * below_scale[hh] +
-                       w.cand_mass[static_cast<int64_t>(row0 + hh) * D.n_list + j];
-            if (!live[hh]) Mj = 0.0f;
+            const float cand = ok ? w.cand_mass[static_cast<int64_t>(row0 + hh) * D.n_list + jj] : 0.0f;
+            mj[hh] = (ok && live[hh]) ? below * below_scale[hh] + cand : 0.0f;
+        }
+    }
+    float2 vbar[kListsPerWave];
+#pragma unroll
+    for (int i = 0; i < kListsPerWave; ++i) {
+        const int j = lc * kBgLists + wave + i * kWaves;
+        vbar[i] = j < D.n_list
+                      ? *reinterpret_cast<const float2*>(
+                            ix.means + (static_cast<int64_t>(bg) * D.n_list + j) * kHeadDim + 2 * lane)
+                      : make_float2(0.f, 0.f);
+    }
+    float Z[G], N[G][2];
+#pragma unroll
+    for (int hh = 0; hh < G; ++hh) { Z[hh] = 0.0f; N[hh][0] = 0.0f; N[hh][1] = 0.0f; }
+#pragma unroll
+    for (int i = 0; i < kListsPerWave; ++i) {
+#pragma unroll
+        for (int hh = 0; hh < G; ++hh) {
+            const float Mj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(mj[hh]), i));
             Z[hh] += Mj;
-            N[hh][0] = fmaf(Mj, vbar.x, N[hh][0]);
-            N[hh][1] = fmaf(Mj, vbar.y, N[hh][1]);
+            N[hh][0] = fmaf(Mj, vbar[i].x, N[hh][0]);
+            N[hh][1] = fmaf(Mj, vbar[i].y, N[hh][1]);
         }
     }
     // combine the 4 waves (sacc reused as [4][G][128])
@@ -208,37 +279,69 @@ __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchInts 
 }
 
 // y = (sum of partials' N) / (sum of partials' Z) under one shift (Eq. 5).
-__global__ __launch_bounds__(kHeadDim) void merge_kernel(Dims D, BatchInts n_exact_parts,
-                                                         const float* __restrict__ partial,
-                                                         int P, int first_bg, int n_bg,
-                                                         float* __restrict__ out) {
+// Partials [0, n_exact(b)) and [first_bg, first_bg + n_bg) of each row are used;
+// partials with Z = 0 are skipped.
+__global__ __launch_bounds__(kMergeThreads) void merge_kernel(Dims D, BatchInts n_exact_parts,
+                                                              const float* __restrict__ partial,
+                                                              int P, int first_bg, int n_bg,
+                                                              float* __restrict__ out) {
+    extern __shared__ float wgt[];   // [P]
+    __shared__ float red[kMergeThreads / kWave];
     const int row = blockIdx.x;
     const int b = row / D.Hq;
     const int t = threadIdx.x;
     const float* pr = partial + static_cast<int64_t>(row) * P * kPartStride;
     const int ne = n_exact_parts.v[b];
-    float M = -__builtin_huge_valf();
-    for (int p = 0; p < ne; ++p) M = fmaxf(M, pr[p * kPartStride]);
-    for (int p = 0; p < n_bg; ++p) {
-        const float* q = pr + (first_bg + p) * kPartStride;
-        if (q[1] > 0.0f) M = fmaxf(M, q[0]);
+    const float neg_inf = -__builtin_huge_valf();
+
+    float m_loc = neg_inf;
+    for (int p = t; p < P; p += kMergeThreads) {
+        const bool used = p < ne || (p >= first_bg && p < first_bg + n_bg);
+        const float2 mz = *reinterpret_cast<const float2*>(pr + p * kPartStride);
+        const float m = (used && mz.y > 0.0f) ? mz.x : neg_inf;
+        wgt[p] = m;
+        m_loc = fmaxf(m_loc, m);
     }
-    float Z = 0.0f, N = 0.0f;
-    for (int p = 0; p < ne; ++p) {
-        const float* q = pr + p * kPartStride;
-        const float f = __expf(q[0] - M);
-        Z += q[1] * f;
-        N += q[4 + t] * f;
+    m_loc = wave_max(m_loc);
+    if (lane_id() == 0) red[t / kWave] = m_loc;
+    __syncthreads();
+    float M = neg_inf;
+#pragma unroll
+    for (int i = 0; i < kMergeThreads / kWave; ++i) M = fmaxf(M, red[i]);
+    __syncthreads();
+    float z_loc = 0.0f;
+    for (int p = t; p < P; p += kMergeThreads) {
+        const float m = wgt[p];
+        const float f = m == neg_inf ? 0.0f : __expf(m - M);
+        wgt[p] = f;
+        const float z = pr[p * kPartStride + 1];   // unused partials may hold garbage
+        z_loc = f != 0.0f ? fmaf(z, f, z_loc) : z_loc;
     }
-    for (int p = 0; p < n_bg; ++p) {
-        const float* q = pr + (first_bg + p) * kPartStride;
-        if (q[1] > 0.0f) {
-            const float f = __expf(q[0] - M);
-            Z += q[1] * f;
-            N += q[4 + t] * f;
+    z_loc = wave_sum(z_loc);
+    if (lane_id() == 0) red[t / kWave] = z_loc;
+    __syncthreads();
+    float Z = 0.0f;
+#pragma unroll
+    for (int i = 0; i < kMergeThreads / kWave; ++i) Z += red[i];
+    // unconditional loads (all issued before use), weights select the used ones
+    constexpr int U = 8;
+    float N[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) N[u] = 0.0f;
+    for (int p0 = 0; p0 < P; p0 += U) {
+        float v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) v[u] = p0 + u < P ? pr[(p0 + u) * kPartStride + 4 + t] : 0.0f;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const float f = p0 + u < P ? wgt[p0 + u] : 0.0f;
+            N[u] = f != 0.0f ? fmaf(v[u], f, N[u]) : N[u];
         }
     }
-    out[static_cast<int64_t>(row) * kHeadDim + t] = N / Z;
+    float n = 0.0f;
+#pragma unroll
+    for (int u = 0; u < U; ++u) n += N[u];
+    out[static_cast<int64_t>(row) * kHeadDim + t] = n / Z;
 }
 
 template <typename T, int G>
@@ -269,6 +372,15 @@ hipError_t launch_attend(const Dims& D, const BatchInts& tk, const KV& kv, const
                    : launch_attend_g<float>(D, tk, kv, ix, w, nsplit_max, s);
 }
 
+static hipError_t launch_merge_parts(const Dims& D, const BatchInts& ne, const float* partial,
+                                     int P, int first_bg, int n_bg, float* out, hipStream_t s) {
+    const size_t lds = static_cast<size_t>(P) * sizeof(float);
+    if (lds > 64 * 1024) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(merge_kernel, dim3(D.B * D.Hq), dim3(kMergeThreads), lds, s, D, ne, partial,
+                       P, first_bg, n_bg, out);
+    return hipGetLastError();
+}
+
 hipError_t launch_merge(const Dims& D, const BatchInts& tk, const Work& w, float* out,
                         int nsplit_max, hipStream_t s) {
     BatchInts ne;
@@ -277,9 +389,7 @@ hipError_t launch_merge(const Dims& D, const BatchInts& tk, const Work& w, float
         ne.v[b] = (nE + kAttnRows - 1) / kAttnRows;
     }
     const int n_bgc = (D.n_list + kBgLists - 1) / kBgLists;
-    hipLaunchKernelGGL(merge_kernel, dim3(D.B * D.Hq), dim3(kHeadDim), 0, s, D, ne, w.partial,
-                       nsplit_max + n_bgc, nsplit_max, n_bgc, out);
-    return hipGetLastError();
+    return launch_merge_parts(D, ne, w.partial, nsplit_max + n_bgc, nsplit_max, n_bgc, out, s);
 }
 
 // ---------------------------------------------------------------------------
@@ -301,6 +411,7 @@ __global__ __launch_bounds__(kAttnThreads) void dense_kernel(Dims D, KV kv, Batc
     const int t1 = min(t0 + kDenseRows, n);
     const int lane16 = threadIdx.x & 15;
     const int stream = threadIdx.x >> 4;
+    const float neg_inf = -__builtin_huge_valf();
     float qv[G][8];
 #pragma unroll
     for (int hh = 0; hh < G; ++hh)
@@ -312,17 +423,34 @@ __global__ __launch_bounds__(kAttnThreads) void dense_kernel(Dims D, KV kv, Batc
     Online o[G];
 #pragma unroll
     for (int hh = 0; hh < G; ++hh) online_init(o[hh]);
-    for (int t = t0 + stream; t < t1; t += kStreams) {
-        float kf[8], vf[8];
-        Load8<T>::run(kb + t * kv.sn, kf);
-        Load8<T>::run(vb + t * kv.sn, vf);
+    constexpr int kDenseBatch = DenseBatch<G>::value;
+    for (int base = t0 + stream; base < t1; base += kStreams * kDenseBatch) {
+        Raw8<T> kr[kDenseBatch], vr[kDenseBatch];
+#pragma unroll
+        for (int i = 0; i < kDenseBatch; ++i) {
+            const int t = base + i * kStreams;
+            if (t < t1) {
+                kr[i].load(kb + t * kv.sn);
+                vr[i].load(vb + t * kv.sn);
+            } else {
+                kr[i].zero();
+                vr[i].zero();
+            }
+        }
 #pragma unroll
         for (int hh = 0; hh < G; ++hh) {
-            float dot = 0.0f;
+            float l[kDenseBatch];
 #pragma unroll
-            for (int i = 0; i < 8; ++i) dot = fmaf(qv[hh][i], kf[i], dot);
-            dot = sum16(dot);
-            online_push(o[hh], dot * D.inv_sqrt_d, vf);
+            for (int i = 0; i < kDenseBatch; ++i) {
+                float kf[8];
+                kr[i].to(kf);
+                float dot = 0.0f;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) dot = fmaf(qv[hh][e], kf[e], dot);
+                dot = sum16(dot);
+                l[i] = base + i * kStreams < t1 ? dot * D.inv_sqrt_d : neg_inf;
+            }
+            online_push_batch<kDenseBatch>(o[hh], l, vr);
         }
     }
 #pragma unroll
@@ -359,9 +487,7 @@ hipError_t launch_dense(const Dims& D, const KV& kv, const BatchInts& lens, floa
     if (e != hipSuccess) return e;
     BatchInts ne;
     for (int b = 0; b < D.B; ++b) ne.v[b] = (lens.v[b] + kDenseRows - 1) / kDenseRows;
-    hipLaunchKernelGGL(merge_kernel, dim3(D.B * D.Hq), dim3(kHeadDim), 0, s, D, ne, partial,
-                       nsplit_max, 0, 0, out);
-    return hipGetLastError();
+    return launch_merge_parts(D, ne, partial, nsplit_max, 0, 0, out, s);
 }
 
 }  // namespace pqhsa

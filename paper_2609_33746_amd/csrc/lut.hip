@@ -62,20 +62,28 @@ __global__ __launch_bounds__(kLutThreads) void lut_kernel(Dims D, const T* __res
 #pragma unroll
         for (int t = 0; t < 8; ++t)
             qc[hh][t] = load1(qg + hh * kHeadDim + lane16 * 8 + t) * D.inv_sqrt_d;
-    for (int jj = group; jj < kCoarseLists; jj += kLutThreads / 16) {
-        const int j = c * kCoarseLists + jj;
+    // all centroid slices of this thread first, then the dot products
+    constexpr int kPer = kCoarseLists / (kLutThreads / 16);
+    float4 cv[kPer][2];
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+        const int j = c * kCoarseLists + group + u * (kLutThreads / 16);
         const int jc = j < D.n_list ? j : D.n_list - 1;   // keep all lanes active
-        const float* cp = centroids + (static_cast<int64_t>(bg) * D.n_list + jc) * kHeadDim +
-                          lane16 * 8;
-        const float4 c0 = *reinterpret_cast<const float4*>(cp);
-        const float4 c1 = *reinterpret_cast<const float4*>(cp + 4);
-        const float cv[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+        const float* cp = centroids + (static_cast<int64_t>(bg) * D.n_list + jc) * kHeadDim + lane16 * 8;
+        cv[u][0] = *reinterpret_cast<const float4*>(cp);
+        cv[u][1] = *reinterpret_cast<const float4*>(cp + 4);
+    }
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+        const int j = c * kCoarseLists + group + u * (kLutThreads / 16);
+        const float cf[8] = {cv[u][0].x, cv[u][0].y, cv[u][0].z, cv[u][0].w,
+                             cv[u][1].x, cv[u][1].y, cv[u][1].z, cv[u][1].w};
         float mine = 0.0f;
 #pragma unroll
         for (int hh = 0; hh < G; ++hh) {
             float acc = 0.0f;
 #pragma unroll
-            for (int t = 0; t < 8; ++t) acc = fmaf(qc[hh][t], cv[t], acc);
+            for (int t = 0; t < 8; ++t) acc = fmaf(qc[hh][t], cf[t], acc);
             acc = sum16(acc);
             if (lane16 == hh) mine = acc;
         }

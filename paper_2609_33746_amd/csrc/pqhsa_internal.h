@@ -17,9 +17,13 @@ constexpr int kMaxLists = 4096;
 
 constexpr int kSub = 256;          // list-major positions per wave sub-chunk
 constexpr int kScanWaves = 8;      // waves (sub-chunks) per scan workgroup
-constexpr int kSampleStride = 32;  // one sampled position in 32 for the threshold
-constexpr int kMaxSamples = 4096;  // LDS capacity of the sample kernel
-constexpr int kSelThreads = 256;
+constexpr int kMaxSamples = 2048;  // sampled positions per row for the threshold
+constexpr int kSelThreads = 1024;
+constexpr int kSelCap = 12288;     // candidates of one row held in LDS by the select kernel
+constexpr int kSelMaxSub = 1024;   // sub-chunks per row on the select kernel's fast path
+constexpr int kSampleRun = 8;      // contiguous positions per sampled run
+constexpr int kPosBits = 20;       // candidate word: list id << kPosBits | position
+constexpr int kMaxSeq = 1 << kPosBits;
 constexpr int kAttnRows = 128;     // exact-set rows per split
 constexpr int kBgLists = 64;       // lists per background workgroup
 constexpr int kDenseRows = 512;    // cache rows per dense split
@@ -61,17 +65,25 @@ struct Work {
     float* coarse;       // [B, Hkv, n_list, G] (q . c_j) / sqrt(d)
     float* tau_lo;       // [B, Hq] candidate threshold
     float* cand_score;   // [B, Hq, rcap] per sub-chunk compacted candidates
-    int32_t* cand_pos;   // [B, Hq, rcap]
+    int32_t* cand_pos;   // [B, Hq, rcap] list id << kPosBits | list-major position
     int32_t* cand_cnt;   // [B, Hq, nsub_cap]
     float* seg_sum;      // [B, Hkv, nseg_cap, G] below-threshold masses
     uint32_t* comp_key;  // [B, Hq, rcap] contiguous candidates (order keys)
-    int32_t* comp_pos;   // [B, Hq, rcap]
-    int32_t* sel_tok;    // [B, Hq, max_topk] selected token ids
-    int32_t* sel_pos;    // [B, Hq, max_topk] their list-major positions
-    float* cand_mass;    // [B, Hq, n_list] unselected-candidate masses
+    int32_t* comp_pos;   // [B, Hq, rcap] (same packing as cand_pos)
+    int32_t* sel_pos;    // [B, Hq, max_topk] list-major positions of T
+    float* cand_mass;    // [B, Hq, n_list] sum over the list's unselected candidates of
+                         //   exp(l~ - shift)
     float* row_shift;    // [B, Hq] shift of the background masses
     int32_t* row_flag;   // [B, Hq] 1 when the row took the re-scan path
     float* partial;      // [B, Hq, nsplit_max + n_bgc, kPartStride]
+};
+
+// One scan workgroup: kScanWaves consecutive sub-chunks of one (b, kv head),
+// with the list id of each sub-chunk's first position.
+struct ScanWG {
+    int bg;
+    int sub0;
+    int list0[kScanWaves];
 };
 
 struct KV {
@@ -83,11 +95,16 @@ struct KV {
 };
 
 // --- launchers (each returns the launch status) -----------------------
+// Kernel attributes (large dynamic LDS) for the current device; called once
+// per context creation.
+hipError_t configure_scan();
+hipError_t configure_select();
+
 hipError_t launch_lut(const Dims& D, const KV& kv, const Index& ix, const Work& w,
                       hipStream_t s);
 hipError_t launch_sample(const Dims& D, const BatchInts& tk, const Index& ix, const Work& w,
                          float bias, hipStream_t s);
-hipError_t launch_scan(const Dims& D, const Index& ix, const Work& w, const int2* wg_table,
+hipError_t launch_scan(const Dims& D, const Index& ix, const Work& w, const ScanWG* wg_table,
                        int n_wg, hipStream_t s);
 hipError_t launch_select(const Dims& D, const BatchInts& tk, const Index& ix, const Work& w,
                          int force_fallback, hipStream_t s);

@@ -80,12 +80,13 @@ __global__ __launch_bounds__(kDbgThreads) void sel_debug_kernel(Dims D, BatchInt
     const int g = (row % D.Hq) / D.G;
     const int bg = b * D.Hkv + g;
     const int k = tk.v[b];
-    const int32_t* st = w.sel_tok + static_cast<int64_t>(row) * D.max_topk;
     const int32_t* sp = w.sel_pos + static_cast<int64_t>(row) * D.max_topk;
+    const int64_t base = static_cast<int64_t>(bg) * D.rcap;
     if (selected) {
         int n2 = 1;
         while (n2 < k) n2 <<= 1;
-        for (int i = threadIdx.x; i < n2; i += kDbgThreads) keys[i] = i < k ? st[i] : 0x7fffffff;
+        for (int i = threadIdx.x; i < n2; i += kDbgThreads)
+            keys[i] = i < k ? ix.perm[base + sp[i]] : 0x7fffffff;
         __syncthreads();
         for (int size = 2; size <= n2; size <<= 1) {
             for (int stride = size >> 1; stride > 0; stride >>= 1) {
@@ -110,7 +111,6 @@ __global__ __launch_bounds__(kDbgThreads) void sel_debug_kernel(Dims D, BatchInt
         const int32_t* loff = ix.loff + static_cast<int64_t>(bg) * (D.n_list + 1);
         for (int j = threadIdx.x; j < D.n_list; j += kDbgThreads) counts[j] = loff[j + 1] - loff[j];
         __syncthreads();
-        const int64_t base = static_cast<int64_t>(bg) * D.rcap;
         for (int i = threadIdx.x; i < k; i += kDbgThreads) atomicSub(&counts[ix.pos_list[base + sp[i]]], 1);
         __syncthreads();
         int32_t* out = unselected + static_cast<int64_t>(row) * D.n_list;

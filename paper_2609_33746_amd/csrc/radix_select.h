@@ -20,6 +20,25 @@ struct SelectScratch {
     int wave_tot[16];
 };
 
+// hist[digit] += 1 for every active lane. Lanes that share a digit are
+// counted with one atomic (scores cluster, so the high digits of a pass are
+// concentrated in a few bins and per-lane atomics would serialise on one LDS
+// address); after two such rounds the remaining lanes add individually.
+// Must be called by every lane of the wave.
+__device__ __forceinline__ void hist_add(int* hist, uint32_t digit, bool active) {
+    uint64_t todo = __ballot(active);
+#pragma unroll
+    for (int round = 0; round < 2; ++round) {
+        if (todo == 0) return;
+        const int leader = __ffsll(static_cast<long long>(todo)) - 1;
+        const uint32_t d = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(digit), leader));
+        const uint64_t same = __ballot(active && digit == d) & todo;
+        if (lane_id() == leader) atomicAdd(&hist[d], __popcll(same));
+        todo &= ~same;
+    }
+    if ((todo >> lane_id()) & 1ull) atomicAdd(&hist[digit], 1);
+}
+
 // All NT threads of the workgroup must call this with the same n and c,
 // 1 <= c <= n.
 template <int NT, typename KeyAt, typename Keep>
@@ -34,10 +53,16 @@ __device__ SelectResult block_select_desc(KeyAt key_at, Keep keep, int n, int c,
     for (int shift = 24; shift >= 0; shift -= 8) {
         for (int i = tid; i < 256; i += NT) sh.hist[i] = 0;
         __syncthreads();
-        for (int i = tid; i < n; i += NT) {
-            if (!keep(i)) continue;
-            const uint32_t k = key_at(i);
-            if ((k & pmask) == prefix) atomicAdd(&sh.hist[(k >> shift) & 0xffu], 1);
+        for (int i0 = 0; i0 < n; i0 += NT) {
+            const int i = i0 + tid;
+            bool act = false;
+            uint32_t digit = 0u;
+            if (i < n && keep(i)) {
+                const uint32_t k = key_at(i);
+                act = (k & pmask) == prefix;
+                digit = (k >> shift) & 0xffu;
+            }
+            hist_add(sh.hist, digit, act);
         }
         __syncthreads();
         if (tid < kWave) {
@@ -47,12 +72,7 @@ __device__ SelectResult block_select_desc(KeyAt key_at, Keep keep, int n, int c,
 #pragma unroll
             for (int j = 0; j < 4; ++j) hv[j] = sh.hist[255 - 4 * l - j];
             const int mine = hv[0] + hv[1] + hv[2] + hv[3];
-            int incl = mine;
-#pragma unroll
-            for (int off = 1; off < kWave; off <<= 1) {
-                const int t = __shfl_up(incl, off);
-                if (l >= off) incl += t;
-            }
+            const int incl = wave_incl_scan_i32(mine);
             int before = incl - mine;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
@@ -82,21 +102,15 @@ __device__ SelectResult block_select_desc(KeyAt key_at, Keep keep, int n, int c,
 template <int NT>
 __device__ int block_excl_scan(int v, int& total, SelectScratch& sh) {
     constexpr int NW = NT / kWave;
-    const int lane = lane_id();
     const int wave = threadIdx.x / kWave;
-    int incl = v;
-#pragma unroll
-    for (int off = 1; off < kWave; off <<= 1) {
-        const int t = __shfl_up(incl, off);
-        if (lane >= off) incl += t;
-    }
-    if (lane == kWave - 1) sh.wave_tot[wave] = incl;
+    const int incl = wave_incl_scan_i32(v);
+    if (lane_id() == kWave - 1) sh.wave_tot[wave] = incl;
     __syncthreads();
     int wbase = 0, tot = 0;
 #pragma unroll
     for (int i = 0; i < NW; ++i) {
         const int t = sh.wave_tot[i];
-        if (i < wave) wbase += t;
+        wbase += i < wave ? t : 0;
         tot += t;
     }
     __syncthreads();

@@ -5,12 +5,16 @@
 // Work decomposition: the list-major positions of each (batch element, KV
 // head) are cut into sub-chunks of kSub positions; one wave owns one
 // sub-chunk, and a workgroup holds kScanWaves consecutive sub-chunks of the
-// same KV head so that they share one copy of the group LUT in LDS.
+// same KV head so that they share one copy of the group LUT in LDS. Each wave
+// keeps the metadata of the lists it walks (start offsets, first segment,
+// coarse terms) in a 64-lane register window, so the inner loop issues no
+// dependent global loads.
 //
 // Per token and head the wave computes l~ and then either
-//   * emits (l~, position) as a top-k candidate when l~ >= tau_lo (the
-//     sampled threshold of its row), compacted in position order at the
-//     start of the sub-chunk's own region of the row's candidate buffer, or
+//   * emits (l~, list id and position) as a top-k candidate when
+//     l~ >= tau_lo (the sampled threshold of its row), compacted in position
+//     order at the start of the sub-chunk's own region of the row's candidate
+//     buffer, or
 //   * adds exp(l~ - tau_lo) (< 1) to the running mass of its inverted list.
 // Tokens below tau_lo can never be in the top-k (tau_lo <= the k-th largest
 // score whenever at least k candidates exist), so these masses are exactly
@@ -24,11 +28,36 @@
 
 namespace pqhsa {
 
+// Metadata of lists [base, base + 63) held one list per lane; lane l also
+// holds the start of list base + l, so list base + i spans
+// [start(i), start(i + 1)).
 template <int G>
-__device__ __forceinline__ void flush_segment(const Dims& D, const Index& ix, const Work& w,
-                                              int bg, int sc, int list, int list_start,
+struct ListWindow {
+    int base;
+    int start;
+    int seg;
+    float cf[G];
+
+    __device__ __forceinline__ void load(const int32_t* loff, const int32_t* seg0,
+                                         const float* coarse, int n_list, int first) {
+        base = first;
+        const int j = first + lane_id();
+        start = j <= n_list ? loff[j] : 0x7fffffff;
+        seg = j < n_list ? seg0[j] : 0;
+#pragma unroll
+        for (int hh = 0; hh < G; ++hh) cf[hh] = j < n_list ? coarse[j * G + hh] : 0.0f;
+    }
+    __device__ __forceinline__ int start_of(int i) const { return __builtin_amdgcn_readlane(start, i); }
+    __device__ __forceinline__ int seg_of(int i) const { return __builtin_amdgcn_readlane(seg, i); }
+    __device__ __forceinline__ float cf_of(int hh, int i) const {
+        return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(cf[hh]), i));
+    }
+};
+constexpr int kWindowLists = kWave - 1;
+
+template <int G>
+__device__ __forceinline__ void flush_segment(const Dims& D, const Work& w, int bg, int seg,
                                               float (&acc)[G]) {
-    const int seg = ix.seg0[static_cast<int64_t>(bg) * (D.n_list + 1) + list] + (sc - list_start / kSub);
     float mine = 0.0f;
 #pragma unroll
     for (int hh = 0; hh < G; ++hh) {
@@ -41,78 +70,97 @@ __device__ __forceinline__ void flush_segment(const Dims& D, const Index& ix, co
 
 template <int G>
 __global__ __launch_bounds__(kScanWaves * kWave) void scan_kernel(Dims D, Index ix, Work w,
-                                                                  const int2* __restrict__ table) {
+                                                                  const ScanWG* __restrict__ table) {
     extern __shared__ float lut_s[];   // [M][K][G]
-    const int2 entry = table[blockIdx.x];
-    const int bg = entry.x;
+    const ScanWG& entry = table[blockIdx.x];
+    const int bg = entry.bg;
     const int b = bg / D.Hkv;
     const int g = bg % D.Hkv;
 
+    const int n_r = ix.n_r[b];
+    const int wave = threadIdx.x / kWave;
+    const int lane = lane_id();
+    const int sc = entry.sub0 + wave;
+    const bool active = sc * kSub < n_r;
+    const int p_begin = sc * kSub;
+    const int p_end = min(p_begin + kSub, n_r);
+    const int64_t base = static_cast<int64_t>(bg) * D.rcap;
+    const uint4* codes = reinterpret_cast<const uint4*>(ix.codes) + base;
+    const int32_t* loff = ix.loff + static_cast<int64_t>(bg) * (D.n_list + 1);
+    const int32_t* seg0 = ix.seg0 + static_cast<int64_t>(bg) * (D.n_list + 1);
+    const float* coarse = w.coarse + static_cast<int64_t>(bg) * D.n_list * G;
+    const int row0 = b * D.Hq + g * G;
+
+    // issue this wave's code, norm and list-metadata loads before staging the LUT
+    constexpr int kIters = kSub / kWave;
+    uint4 c_pre[kIters];
+    float r_pre[kIters];
+#pragma unroll
+    for (int it = 0; it < kIters; ++it) {
+        const int p = p_begin + it * kWave + lane;
+        c_pre[it] = make_uint4(0u, 0u, 0u, 0u);
+        r_pre[it] = 0.0f;
+        if (active && p < p_end) {
+            c_pre[it] = codes[p];
+            r_pre[it] = ix.norms[base + p];
+        }
+    }
+    ListWindow<G> win;
+    win.load(loff, seg0, coarse, D.n_list, active ? entry.list0[wave] : 0);
+    float tlo[G];
+#pragma unroll
+    for (int hh = 0; hh < G; ++hh) tlo[hh] = w.tau_lo[row0 + hh];
     {
         const float4* src = reinterpret_cast<const float4*>(w.lut + static_cast<int64_t>(bg) * kLutRow * G);
         float4* dst = reinterpret_cast<float4*>(lut_s);
         for (int i = threadIdx.x; i < kLutRow * G / 4; i += kScanWaves * kWave) dst[i] = src[i];
     }
     __syncthreads();
+    if (!active) return;
 
-    const int n_r = ix.n_r[b];
-    const int wave = threadIdx.x / kWave;
-    const int sc = entry.y + wave;
-    if (sc * kSub >= n_r) return;
-    const int lane = lane_id();
-    const int p_begin = sc * kSub;
-    const int p_end = min(p_begin + kSub, n_r);
-    const int64_t base = static_cast<int64_t>(bg) * D.rcap;
-    const int row0 = b * D.Hq + g * G;
-
-    float tlo[G];
-#pragma unroll
-    for (int hh = 0; hh < G; ++hh) tlo[hh] = w.tau_lo[row0 + hh];
-
-    const int32_t* loff = ix.loff + static_cast<int64_t>(bg) * (D.n_list + 1);
-    const float* coarse = w.coarse + static_cast<int64_t>(bg) * D.n_list * G;
-    const uint4* codes = reinterpret_cast<const uint4*>(ix.codes) + base;
-
-    int cur = ix.pos_list[base + p_begin];
-    int cur_start = loff[cur];
-    int cur_end = loff[cur + 1];
+    int ci = 0;   // window index of the current list
+    int cur_start = win.start_of(0);
+    int cur_end = win.start_of(1);
     float acc[G];
     int cbase[G];
 #pragma unroll
     for (int hh = 0; hh < G; ++hh) { acc[hh] = 0.0f; cbase[hh] = 0; }
 
-    for (int p_first = p_begin; p_first < p_end; p_first += kWave) {
+#pragma unroll
+    for (int it = 0; it < kIters; ++it) {
+        const int p_first = p_begin + it * kWave;
+        if (p_first >= p_end) break;
         const int p = p_first + lane;
         const bool valid = p < p_end;
         const int p_last = min(p_first + kWave - 1, p_end - 1);
-        uint4 c = make_uint4(0u, 0u, 0u, 0u);
-        float r = 0.0f;
-        if (valid) {
-            c = codes[p];
-            r = ix.norms[base + p];
-        }
         float fs[G];
-        fine_sum<G>(lut_s, c, fs);
+        fine_sum<G>(lut_s, c_pre[it], fs);
+        const float r = r_pre[it];
         float s[G];
 #pragma unroll
         for (int hh = 0; hh < G; ++hh) s[hh] = 0.0f;
+        int my_list = 0;
 
         // walk the lists that cover [p_first, p_last] (wave-uniform)
         while (true) {
             const bool in = valid && p >= cur_start && p < cur_end;
-            const float* cf = coarse + static_cast<int64_t>(cur) * G;
+            if (in) my_list = win.base + ci;
 #pragma unroll
             for (int hh = 0; hh < G; ++hh) {
-                const float sc_h = pq_logit(r, cf[hh], fs[hh]);
+                const float sc_h = pq_logit(r, win.cf_of(hh, ci), fs[hh]);
                 if (in) s[hh] = sc_h;
                 acc[hh] += (in && sc_h < tlo[hh]) ? __expf(sc_h - tlo[hh]) : 0.0f;
             }
             if (cur_end > p_last) break;
-            flush_segment<G>(D, ix, w, bg, sc, cur, cur_start, acc);
+            flush_segment<G>(D, w, bg, win.seg_of(ci) + (sc - cur_start / kSub), acc);
             do {
-                ++cur;
+                ++ci;
+                if (ci == kWindowLists) {
+                    win.load(loff, seg0, coarse, D.n_list, win.base + kWindowLists);
+                    ci = 0;
+                }
                 cur_start = cur_end;
-                cur_end = loff[cur + 1];
+                cur_end = win.start_of(ci + 1);
             } while (cur_end == cur_start);
         }
 
@@ -125,12 +173,13 @@ __global__ __launch_bounds__(kScanWaves * kWave) void scan_kernel(Dims D, Index 
                 const int64_t o = static_cast<int64_t>(row0 + hh) * D.rcap + p_begin + cbase[hh] +
                                   lanes_below(mask);
                 w.cand_score[o] = s[hh];
-                w.cand_pos[o] = p;
+                w.cand_pos[o] = static_cast<int32_t>((static_cast<uint32_t>(my_list) << kPosBits) |
+                                                     static_cast<uint32_t>(p));
             }
             cbase[hh] += __popcll(mask);
         }
     }
-    flush_segment<G>(D, ix, w, bg, sc, cur, cur_start, acc);
+    flush_segment<G>(D, w, bg, win.seg_of(ci) + (sc - cur_start / kSub), acc);
     int mine = 0;
 #pragma unroll
     for (int hh = 0; hh < G; ++hh)
@@ -139,21 +188,22 @@ __global__ __launch_bounds__(kScanWaves * kWave) void scan_kernel(Dims D, Index 
 }
 
 template <int G>
-static hipError_t launch_scan_t(const Dims& D, const Index& ix, const Work& w, const int2* table,
+static hipError_t launch_scan_t(const Dims& D, const Index& ix, const Work& w, const ScanWG* table,
                                 int n_wg, hipStream_t s) {
     const size_t lds = static_cast<size_t>(kLutRow) * G * sizeof(float);
-    if (lds > 64 * 1024) {
-        hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&scan_kernel<G>),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize,
-                                           static_cast<int>(lds));
-        if (e != hipSuccess) return e;
-    }
     hipLaunchKernelGGL((scan_kernel<G>), dim3(n_wg), dim3(kScanWaves * kWave), lds, s, D, ix, w,
                        table);
     return hipGetLastError();
 }
 
-hipError_t launch_scan(const Dims& D, const Index& ix, const Work& w, const int2* table, int n_wg,
+hipError_t configure_scan() {
+    // the G = 8 group LUT (128 KB) exceeds the default dynamic LDS limit
+    return hipFuncSetAttribute(reinterpret_cast<const void*>(&scan_kernel<8>),
+                               hipFuncAttributeMaxDynamicSharedMemorySize,
+                               static_cast<int>(kLutRow * 8 * sizeof(float)));
+}
+
+hipError_t launch_scan(const Dims& D, const Index& ix, const Work& w, const ScanWG* table, int n_wg,
                        hipStream_t s) {
     if (n_wg == 0) return hipSuccess;
     switch (D.G) {

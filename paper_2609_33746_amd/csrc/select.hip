@@ -3,36 +3,110 @@
 // smaller token id.
 //
 // Two kernels:
-//  * sample_kernel (before the scan): scores a strided, list-stratified sample
-//    of the row's list-major positions and takes a sample order statistic as
-//    the candidate threshold tau_lo, chosen so that about twice k tokens of
-//    the full row score at or above it.
+//  * sample_kernel (before the scan): scores a list-stratified sample of the
+//    row's list-major positions (contiguous runs of kSampleRun positions,
+//    evenly spread) and takes a sample order statistic as the candidate
+//    threshold tau_lo, chosen so that about twice k tokens of the full row
+//    score at or above it. Any threshold gives the same final result; it only
+//    decides how many candidates the scan emits.
 //  * select_kernel (after the scan): gathers the candidates of the row (in
-//    list-major position order), finds the exact k-th largest score by radix
-//    select over order-preserving keys, breaks ties on token id with a second
-//    radix select, writes T, and adds the unselected candidates to the
-//    per-list background masses. If the threshold left fewer than k
-//    candidates (or none at all), the row is re-scanned in full from the LUT
-//    and every indexed token becomes a candidate; the below-threshold masses
-//    of the scan are then ignored for that row. The result is exact either
-//    way; only the cost differs.
+//    list-major position order) into LDS, locates the k-th largest score with
+//    one histogram pass over monotone bins of the order keys, ranks the few
+//    candidates of the boundary bin exactly (score, then token id), writes T,
+//    and sums exp(l~ - shift) of the unselected candidates per list (in
+//    64-bit fixed point, so the sums do not depend on the order of the
+//    atomic additions). If the threshold left fewer than k candidates (or none
+//    at all), the row is re-scanned in full from the LUT and every indexed
+//    token becomes a candidate; the below-threshold masses of the scan are
+//    then ignored for that row. Rows with more candidates than the LDS holds,
+//    or a very dense boundary bin, use a radix select instead. Every path
+//    gives the exact top-k.
+//
+// Both kernels keep their dependency chains short: each wave loads the
+// counts of its own sub-chunks and scans them with DPP, candidate loads are
+// issued in batches, and every workgroup-wide step is one scan or reduction.
 #include "device_common.h"
+#include "hist_select.h"
 #include "pq_score.h"
 #include "pqhsa_internal.h"
 #include "radix_select.h"
 
 namespace pqhsa {
 
-__device__ __forceinline__ int sample_stride(int n_r) {
-    const int need = (n_r + kMaxSamples - 1) / kMaxSamples;
-    return need > kSampleStride ? need : kSampleStride;
+constexpr int kNW = kSelThreads / kWave;
+constexpr int kSampleUnroll = kMaxSamples / kSelThreads;   // samples per thread
+constexpr int kRankCap = 512;          // boundary-bin keys ranked exactly
+constexpr int kLoadBatch = 16;         // sub-chunks whose candidates a wave loads at once
+constexpr uint32_t kPosMask = (1u << kPosBits) - 1u;
+constexpr float kMassScale = 1099511627776.0f;       // 2^40: fixed-point weights
+constexpr float kMassUnscale = 1.0f / 1099511627776.0f;
+
+// Rank the keys of one histogram bin exactly: key desc, then token id asc
+// (tok_at is read only when two keys of the bin are equal). Marks the `need`
+// largest in the `chosen` bitmap (if given) and returns the smallest chosen
+// key. Returns false without marking anything when the bin holds more than
+// kRankCap keys. Must be called by the whole workgroup.
+template <typename KeyAt, typename ValidAt, typename TokAt>
+__device__ __forceinline__ bool rank_boundary_bin(KeyAt key_at, ValidAt valid_at, TokAt tok_at,
+                                                  int n, uint32_t kmin, int sh, int bin, int m,
+                                                  int need, uint32_t* r_key, int* r_idx,
+                                                  int* r_tok, int* counter, uint32_t* chosen,
+                                                  uint32_t& kth, BlockScratch& bs) {
+    if (m > kRankCap) return false;
+    const int tid = threadIdx.x;
+    for (int i0 = 0; i0 < n; i0 += kSelThreads) {
+        const int i = i0 + tid;
+        if (i < n && valid_at(i)) {
+            const uint32_t kk = key_at(i);
+            if (static_cast<int>((kk - kmin) >> sh) == bin) {
+                const int slot = atomicAdd(counter, 1);
+                r_key[slot] = kk;
+                r_idx[slot] = i;
+            }
+        }
+    }
+    __syncthreads();
+    int dup = 0;
+    if (tid < m) {
+        const uint32_t mk = r_key[tid];
+        for (int j = 0; j < m; ++j) dup |= (j != tid && r_key[j] == mk) ? 1 : 0;
+    }
+    const bool ties = __syncthreads_or(dup) != 0;
+    if (ties && tid < m) r_tok[tid] = tok_at(r_idx[tid]);
+    __syncthreads();
+    uint32_t mine = 0xffffffffu;
+    if (tid < m) {
+        const uint32_t mk = r_key[tid];
+        const int mt = ties ? r_tok[tid] : 0;
+        int rank = 0;
+        for (int j = 0; j < m; ++j) {
+            const uint32_t ok = r_key[j];
+            rank += (ok > mk || (ties && ok == mk && r_tok[j] < mt)) ? 1 : 0;
+        }
+        if (rank < need) {
+            const int idx = r_idx[tid];
+            if (chosen) atomicOr(&chosen[idx >> 5], 1u << (idx & 31));
+            mine = mk;
+        }
+    }
+    uint32_t dmx = 0u, dcnt = 0u;
+    block_min_max_count<kSelThreads>(mine, dmx, dcnt, bs);
+    kth = mine;
+    return true;
 }
 
 __global__ __launch_bounds__(kSelThreads) void sample_kernel(Dims D, BatchInts tk, Index ix,
                                                              Work w, float bias) {
     __shared__ float lut_s[kLutRow];
     __shared__ uint32_t keys[kMaxSamples];
-    __shared__ SelectScratch sh;
+    __shared__ int hist[kHistBins];
+    __shared__ uint32_t r_key[kRankCap];
+    __shared__ int r_idx[kRankCap];
+    __shared__ int r_tok[kRankCap];
+    __shared__ int counter[1];
+    __shared__ SelectScratch ss;
+    __shared__ BlockScratch bs;
+    const int tid = threadIdx.x;
     const int row = blockIdx.x;
     const int b = row / D.Hq;
     const int h = row % D.Hq;
@@ -43,42 +117,160 @@ __global__ __launch_bounds__(kSelThreads) void sample_kernel(Dims D, BatchInts t
     const int k = tk.v[b];
     const float neg_inf = -__builtin_huge_valf();
     if (n_r == 0) {
-        if (threadIdx.x == 0) w.tau_lo[row] = neg_inf;
+        if (tid == 0) w.tau_lo[row] = neg_inf;
         return;
     }
-    const int stride = sample_stride(n_r);
-    const int ns = (n_r + stride - 1) / stride;
+    // runs of kSampleRun positions, rs apart (rs >= 1), clipped at the next run
+    const int nrun = min(kMaxSamples / kSampleRun, (n_r + kSampleRun - 1) / kSampleRun);
+    const int rs = n_r / nrun;
+    const int run_len = min(kSampleRun, rs);
+    const int64_t base = static_cast<int64_t>(bg) * D.rcap;
+    const uint4* codes = reinterpret_cast<const uint4*>(ix.codes) + base;
+    uint4 cv[kSampleUnroll];
+    float rv[kSampleUnroll];
+    int jv[kSampleUnroll];
+    bool ok[kSampleUnroll];
+#pragma unroll
+    for (int u = 0; u < kSampleUnroll; ++u) {
+        const int s = u * kSelThreads + tid;
+        const int run = s / kSampleRun;
+        const int pos = run * rs + s % kSampleRun;
+        ok[u] = run < nrun && s % kSampleRun < run_len && pos < n_r;
+        const int p = ok[u] ? pos : 0;
+        cv[u] = codes[p];
+        rv[u] = ix.norms[base + p];
+        jv[u] = ix.pos_list[base + p];
+    }
+    const float* coarse = w.coarse + static_cast<int64_t>(bg) * D.n_list * D.G;
+    float cf[kSampleUnroll];
+#pragma unroll
+    for (int u = 0; u < kSampleUnroll; ++u) cf[u] = coarse[jv[u] * D.G + hh];
+    stage_head_lut<kSelThreads>(lut_s, w.lut + static_cast<int64_t>(bg) * kLutRow * D.G, D.G, hh);
+    for (int i = tid; i < kHistBins; i += kSelThreads) hist[i] = 0;
+    if (tid == 0) counter[0] = 0;
+    __syncthreads();
+    uint32_t mn = 0xffffffffu, mx = 0u, cnt = 0u;
+#pragma unroll
+    for (int u = 0; u < kSampleUnroll; ++u) {
+        float fs[1];
+        fine_sum<1>(lut_s, cv[u], fs);
+        const uint32_t kk = float_key(pq_logit(rv[u], cf[u], fs[0]));
+        keys[u * kSelThreads + tid] = kk;
+        if (ok[u]) {
+            mn = min(mn, kk);
+            mx = max(mx, kk);
+            ++cnt;
+        }
+    }
+    block_min_max_count<kSelThreads>(mn, mx, cnt, bs);
+    const int ns = static_cast<int>(cnt);
     // order statistic: about 2k * ns / |R| sampled tokens above, plus a margin
     const int c = (k == 0) ? 1 : static_cast<int>(ceilf(2.0f * k * ns / n_r)) + 8;
     if (c > ns) {   // the budget is a large share of R: every token is a candidate
-        if (threadIdx.x == 0) w.tau_lo[row] = neg_inf;
+        if (tid == 0) w.tau_lo[row] = neg_inf;
         return;
     }
-    stage_head_lut<kSelThreads>(lut_s, w.lut + static_cast<int64_t>(bg) * kLutRow * D.G, D.G, hh);
+    const int sh = bin_shift(mn, mx);
+#pragma unroll
+    for (int u = 0; u < kSampleUnroll; ++u)
+        hist_add(hist, (keys[u * kSelThreads + tid] - mn) >> sh, ok[u]);
     __syncthreads();
-    const int64_t base = static_cast<int64_t>(bg) * D.rcap;
-    const uint4* codes = reinterpret_cast<const uint4*>(ix.codes) + base;
-    const float* coarse = w.coarse + static_cast<int64_t>(bg) * D.n_list * D.G;
-    for (int s = threadIdx.x; s < ns; s += kSelThreads) {
-        const int pos = s * stride;
-        const int j = ix.pos_list[base + pos];
-        float fs[1];
-        fine_sum<1>(lut_s, codes[pos], fs);
-        const float score = pq_logit(ix.norms[base + pos], coarse[j * D.G + hh], fs[0]);
-        keys[s] = float_key(score);
+    int above = 0;
+    const int bin = block_find_bin_desc<kSelThreads>(hist, c, above, ss, bs);
+    uint32_t tau_key = 0u;
+    auto valid_at = [&](int i) {
+        const int run = i / kSampleRun;
+        return run < nrun && i % kSampleRun < run_len && run * rs + i % kSampleRun < n_r;
+    };
+    const bool exact = rank_boundary_bin([&](int i) { return keys[i]; }, valid_at,
+                                         [](int i) { return i; }, kMaxSamples, mn, sh, bin,
+                                         hist[bin], c - above, r_key, r_idx, r_tok, counter,
+                                         nullptr, tau_key, bs);
+    if (!exact) {
+        // very dense bin: its smallest key (<= the c-th largest)
+        uint32_t lo = 0xffffffffu, dmx = 0u, dcnt = 0u;
+#pragma unroll
+        for (int u = 0; u < kSampleUnroll; ++u) {
+            const uint32_t kk = keys[u * kSelThreads + tid];
+            if (ok[u] && static_cast<int>((kk - mn) >> sh) == bin) lo = min(lo, kk);
+        }
+        block_min_max_count<kSelThreads>(lo, dmx, dcnt, bs);
+        tau_key = lo;
     }
+    if (tid == 0) w.tau_lo[row] = key_float(tau_key) + bias;
+}
+
+// LDS layout of select_kernel (dynamic, 4-byte words):
+//   keys [kSelCap] | cand [kSelCap] | mass (uint64) [kMaxLists] | hist [kHistBins] |
+//   rank_key [kRankCap] | rank_idx [kRankCap] | rank_tok [kRankCap] |
+//   chosen bitmap [kSelCap / 32] | counter [4]
+constexpr int kOffCand = kSelCap;
+constexpr int kOffMass = 2 * kSelCap;   // 8-byte aligned
+constexpr int kOffHist = kOffMass + 2 * kMaxLists;
+constexpr int kOffRKey = kOffHist + kHistBins;
+constexpr int kOffRIdx = kOffRKey + kRankCap;
+constexpr int kOffRTok = kOffRIdx + kRankCap;
+constexpr int kOffBits = kOffRTok + kRankCap;
+constexpr int kOffCounter = kOffBits + kSelCap / 32;
+constexpr size_t kSelLdsWords = kOffCounter + 4;
+constexpr size_t kSelLdsBytes = kSelLdsWords * 4;
+
+// Emit T in candidate order (each thread owns a contiguous range of candidate
+// indices) and the per-list sums of exp(l~ - shift) over the unselected
+// candidates (candidates are in list-major order, so a thread adds one
+// partial per run of equal list ids).
+template <typename KeyAt, typename CandAt, typename IsSel>
+__device__ __forceinline__ void emit_selection(KeyAt key_at, CandAt cand_at, IsSel is_sel, int total,
+                                               int k, int n_list, float shift,
+                                               unsigned long long* mass, int32_t* sel_pos,
+                                               float* cand_mass, SelectScratch& ss) {
+    const int tid = threadIdx.x;
+    const int eper = (total + kSelThreads - 1) / kSelThreads;
+    const int e0 = min(tid * eper, total);
+    const int e1 = min(e0 + eper, total);
+    int nsel = 0;
+    for (int i = e0; i < e1; ++i) nsel += is_sel(i, key_at(i), cand_at(i)) ? 1 : 0;
+    int tot = 0;
+    int o = block_excl_scan<kSelThreads>(nsel, tot, ss);
+    int run_list = -1;
+    unsigned long long run = 0ull;
+    for (int i = e0; i < e1; ++i) {
+        const uint32_t key = key_at(i);
+        const uint32_t cand = cand_at(i);
+        const int lst = static_cast<int>(cand >> kPosBits);
+        if (lst != run_list) {
+            if (run) atomicAdd(&mass[run_list], run);
+            run = 0ull;
+            run_list = lst;
+        }
+        if (is_sel(i, key, cand)) {
+            if (o < k) sel_pos[o] = static_cast<int32_t>(cand & kPosMask);
+            ++o;
+        } else {
+            run += static_cast<unsigned long long>(__expf(key_float(key) - shift) * kMassScale);
+        }
+    }
+    if (run) atomicAdd(&mass[run_list], run);
     __syncthreads();
-    const SelectResult r = block_select_desc<kSelThreads>(
-        [&](int i) { return keys[i]; }, [](int) { return true; }, ns, c, sh);
-    if (threadIdx.x == 0) w.tau_lo[row] = key_float(r.key) + bias;
+    for (int j = tid; j < n_list; j += kSelThreads)
+        cand_mass[j] = static_cast<float>(mass[j]) * kMassUnscale;
 }
 
 __global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchInts tk, Index ix,
                                                              Work w, int force_fallback) {
-    __shared__ float mass[kMaxLists];
-    __shared__ float lut_s[kLutRow];
-    __shared__ SelectScratch sh;
+    extern __shared__ uint32_t lds[];
+    unsigned long long* mass = reinterpret_cast<unsigned long long*>(lds + kOffMass);
+    int* hist = reinterpret_cast<int*>(lds + kOffHist);
+    uint32_t* r_key = lds + kOffRKey;
+    int* r_idx = reinterpret_cast<int*>(lds + kOffRIdx);
+    int* r_tok = reinterpret_cast<int*>(lds + kOffRTok);
+    uint32_t* chosen = lds + kOffBits;
+    int* counter = reinterpret_cast<int*>(lds + kOffCounter);
+    __shared__ SelectScratch ss;
+    __shared__ BlockScratch bs;
     const int tid = threadIdx.x;
+    const int lane = lane_id();
+    const int wave = tid / kWave;
     const int row = blockIdx.x;
     const int b = row / D.Hq;
     const int h = row % D.Hq;
@@ -90,108 +282,208 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchInts t
     const int nsub = (n_r + kSub - 1) / kSub;
     const int64_t rbase = static_cast<int64_t>(row) * D.rcap;
     const int64_t base = static_cast<int64_t>(bg) * D.rcap;
+    const int32_t* perm = ix.perm + base;
+    int32_t* sel_pos = w.sel_pos + static_cast<int64_t>(row) * D.max_topk;
+    float* cand_mass = w.cand_mass + static_cast<int64_t>(row) * D.n_list;
     const float neg_inf = -__builtin_huge_valf();
 
-    // 1) candidate count; each thread owns a contiguous range of sub-chunks
-    const int per = (nsub + kSelThreads - 1) / kSelThreads;
-    const int sc0 = min(tid * per, nsub);
-    const int sc1 = min(sc0 + per, nsub);
-    const int32_t* cnt = w.cand_cnt + static_cast<int64_t>(row) * D.nsub_cap;
-    int mine = 0;
-    for (int sc = sc0; sc < sc1; ++sc) mine += cnt[sc];
-    int total = 0;
-    const int off = block_excl_scan<kSelThreads>(mine, total, sh);
-    const bool fallback = force_fallback || (n_r > 0 && total < (k > 0 ? k : 1));
+    for (int j = tid; j < D.n_list; j += kSelThreads) mass[j] = 0ull;
+    for (int i = tid; i < kHistBins; i += kSelThreads) hist[i] = 0;
+    for (int i = tid; i < kSelCap / 32; i += kSelThreads) chosen[i] = 0u;
+    if (tid == 0) counter[0] = 0;
 
-    if (!fallback) {
-        // 2a) compact the row's candidates, position order
-        int o = off;
-        for (int sc = sc0; sc < sc1; ++sc) {
-            const int c = cnt[sc];
-            const int64_t src = rbase + static_cast<int64_t>(sc) * kSub;
-            for (int i = 0; i < c; ++i, ++o) {
-                w.comp_key[rbase + o] = float_key(w.cand_score[src + i]);
-                w.comp_pos[rbase + o] = w.cand_pos[src + i];
+    // 1) candidate counts: wave w owns sub-chunks [w * spw, (w + 1) * spw)
+    const bool small_nsub = nsub <= kSelMaxSub;
+    const int spw = small_nsub ? (nsub + kNW - 1) / kNW : 0;
+    const int32_t* cnt = w.cand_cnt + static_cast<int64_t>(row) * D.nsub_cap;
+    int c_l = 0, incl = 0;
+    int total = 0;
+    if (small_nsub) {
+        const int sc = wave * spw + lane;
+        c_l = (lane < spw && sc < nsub) ? cnt[sc] : 0;
+        incl = wave_incl_scan_i32(c_l);
+        if (lane == kWave - 1) ss.wave_tot[wave] = incl;
+        __syncthreads();
+        int wbase = 0;
+#pragma unroll
+        for (int i = 0; i < kNW; ++i) {
+            const int t = ss.wave_tot[i];
+            wbase += i < wave ? t : 0;
+            total += t;
+        }
+        incl += wbase;   // row-wide inclusive offset of this lane's sub-chunk
+        __syncthreads();
+    } else {
+        int mine = 0;
+        const int per = (nsub + kSelThreads - 1) / kSelThreads;
+        const int sc0 = min(tid * per, nsub), sc1 = min(sc0 + per, nsub);
+        for (int sc = sc0; sc < sc1; ++sc) mine += cnt[sc];
+        block_excl_scan<kSelThreads>(mine, total, ss);
+    }
+    const bool fallback = force_fallback || (n_r > 0 && total < (k > 0 ? k : 1));
+    float shift = neg_inf;
+
+    if (!fallback && small_nsub && total <= kSelCap) {
+        // ---- fast path: candidates in LDS, position order ----
+        auto KEY = [&](int i) { return lds[i]; };
+        auto CAND = [&](int i) { return lds[kOffCand + i]; };
+        uint32_t kmin = 0xffffffffu, kmax = 0u, kcount = 0u;
+        for (int j0 = 0; j0 < spw; j0 += kLoadBatch) {
+            float sv[kLoadBatch];
+            uint32_t pv[kLoadBatch];
+#pragma unroll
+            for (int u = 0; u < kLoadBatch; ++u) {
+                const int j = min(j0 + u, kWave - 1);
+                const int cj = j0 + u < spw ? __builtin_amdgcn_readlane(c_l, j) : 0;
+                const int64_t src = rbase + static_cast<int64_t>(wave * spw + j) * kSub + lane;
+                if (lane < cj) {
+                    sv[u] = w.cand_score[src];
+                    pv[u] = static_cast<uint32_t>(w.cand_pos[src]);
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < kLoadBatch; ++u) {
+                const int j = min(j0 + u, kWave - 1);
+                const int cj = j0 + u < spw ? __builtin_amdgcn_readlane(c_l, j) : 0;
+                const int o = __builtin_amdgcn_readlane(incl, j) - cj + lane;
+                if (lane < cj) {
+                    const uint32_t kk = float_key(sv[u]);
+                    lds[o] = kk;
+                    lds[kOffCand + o] = pv[u];
+                    kmin = min(kmin, kk);
+                    kmax = max(kmax, kk);
+                }
+            }
+        }
+        // sub-chunks with more than one wave of candidates
+        for (int j = 0; j < spw; ++j) {
+            const int cj = __builtin_amdgcn_readlane(c_l, j);
+            if (cj <= kWave) continue;
+            const int o0 = __builtin_amdgcn_readlane(incl, j) - cj;
+            const int64_t src0 = rbase + static_cast<int64_t>(wave * spw + j) * kSub;
+            for (int i = kWave + lane; i < cj; i += kWave) {
+                const uint32_t kk = float_key(w.cand_score[src0 + i]);
+                lds[o0 + i] = kk;
+                lds[kOffCand + o0 + i] = static_cast<uint32_t>(w.cand_pos[src0 + i]);
+                kmin = min(kmin, kk);
+                kmax = max(kmax, kk);
+            }
+        }
+        block_min_max_count<kSelThreads>(kmin, kmax, kcount, bs);
+        if (k == 0) {
+            shift = total > 0 ? key_float(kmax) : neg_inf;
+            emit_selection(KEY, CAND, [](int, uint32_t, uint32_t) { return false; }, total, 0,
+                           D.n_list, shift, mass, sel_pos, cand_mass, ss);
+        } else {
+            const int sh = bin_shift(kmin, kmax);
+            for (int i0 = 0; i0 < total; i0 += kSelThreads) {
+                const int i = i0 + tid;
+                const bool act = i < total;
+                hist_add(hist, act ? (KEY(i) - kmin) >> sh : 0u, act);
+            }
+            __syncthreads();
+            int above = 0;
+            const int bstar = block_find_bin_desc<kSelThreads>(hist, k, above, ss, bs);
+            uint32_t kth = 0u;
+            const bool by_rank = rank_boundary_bin(
+                KEY, [](int) { return true; }, [&](int i) { return perm[CAND(i) & kPosMask]; },
+                total, kmin, sh, bstar, hist[bstar], k - above, r_key, r_idx, r_tok, counter,
+                chosen, kth, bs);
+            if (by_rank) {
+                shift = key_float(kth);   // the k-th largest score
+                emit_selection(
+                    KEY, CAND,
+                    [&](int i, uint32_t key, uint32_t) {
+                        const int bn = static_cast<int>((key - kmin) >> sh);
+                        return bn > bstar || (bn == bstar && ((chosen[i >> 5] >> (i & 31)) & 1u));
+                    },
+                    total, k, D.n_list, shift, mass, sel_pos, cand_mass, ss);
+            } else {
+                // very dense boundary bin: radix select
+                const SelectResult r = block_select_desc<kSelThreads>(
+                    KEY, [](int) { return true; }, total, k, ss);
+                const uint32_t kk = r.key;
+                const int need_r = k - r.count_above;
+                int tok_cut = 0x7fffffff;
+                if (r.count_equal > need_r) {
+                    const SelectResult t = block_select_desc<kSelThreads>(
+                        [&](int i) { return ~static_cast<uint32_t>(perm[CAND(i) & kPosMask]); },
+                        [&](int i) { return KEY(i) == kk; }, total, need_r, ss);
+                    tok_cut = static_cast<int>(~t.key);
+                }
+                shift = key_float(kk);
+                emit_selection(
+                    KEY, CAND,
+                    [&](int, uint32_t key, uint32_t cand) {
+                        return key > kk || (key == kk && perm[cand & kPosMask] <= tok_cut);
+                    },
+                    total, k, D.n_list, shift, mass, sel_pos, cand_mass, ss);
             }
         }
     } else {
-        // 2b) re-scan: every indexed token of the row is a candidate
-        stage_head_lut<kSelThreads>(lut_s, w.lut + static_cast<int64_t>(bg) * kLutRow * D.G, D.G,
-                                    hh);
-        __syncthreads();
-        const uint4* codes = reinterpret_cast<const uint4*>(ix.codes) + base;
-        const float* coarse = w.coarse + static_cast<int64_t>(bg) * D.n_list * D.G;
-        for (int pos = tid; pos < n_r; pos += kSelThreads) {
-            const int j = ix.pos_list[base + pos];
-            float fs[1];
-            fine_sum<1>(lut_s, codes[pos], fs);
-            const float s = pq_logit(ix.norms[base + pos], coarse[j * D.G + hh], fs[0]);
-            w.comp_key[rbase + pos] = float_key(s);
-            w.comp_pos[rbase + pos] = pos;
-        }
-        total = n_r;
-    }
-    __syncthreads();
-
-    const uint32_t* ckey = w.comp_key + rbase;
-    const int32_t* cpos = w.comp_pos + rbase;
-    const int32_t* perm = ix.perm + base;
-
-    // 3) the k-th largest key, and the token-id cut among equal keys
-    uint32_t kth = 0xffffffffu;
-    int tok_cut = 0x7fffffff;
-    float shift = neg_inf;
-    if (total > 0) {
-        const SelectResult r = block_select_desc<kSelThreads>(
-            [&](int i) { return ckey[i]; }, [](int) { return true; }, total, k > 0 ? k : 1, sh);
-        shift = key_float(r.key);
-        if (k > 0) {
-            kth = r.key;
-            const int need = k - r.count_above;
-            if (r.count_equal > need) {
-                const SelectResult t = block_select_desc<kSelThreads>(
-                    [&](int i) { return ~static_cast<uint32_t>(perm[cpos[i]]); },
-                    [&](int i) { return ckey[i] == kth; }, total, need, sh);
-                tok_cut = static_cast<int>(~t.key);
-            }
-        }
-    }
-
-    // 4) emit T (candidate order) and the unselected-candidate masses per list
-    for (int j = tid; j < D.n_list; j += kSelThreads) mass[j] = 0.0f;
-    __syncthreads();
-    int written = 0;
-    int32_t* sel_tok = w.sel_tok + static_cast<int64_t>(row) * D.max_topk;
-    int32_t* sel_pos = w.sel_pos + static_cast<int64_t>(row) * D.max_topk;
-    for (int t0 = 0; t0 < total; t0 += kSelThreads) {
-        const int i = t0 + tid;
-        bool sel = false;
-        int pos = 0, tok = -1;
-        if (i < total) {
-            const uint32_t key = ckey[i];
-            pos = cpos[i];
-            if (k > 0) {
-                if (key > kth) {
-                    sel = true;
-                } else if (key == kth) {
-                    tok = perm[pos];
-                    sel = tok <= tok_cut;
+        // ---- slow path: candidates in global memory (many, or the re-scan) ----
+        if (!fallback) {
+            const int per = (nsub + kSelThreads - 1) / kSelThreads;
+            const int sc0 = min(tid * per, nsub), sc1 = min(sc0 + per, nsub);
+            int mine = 0;
+            for (int sc = sc0; sc < sc1; ++sc) mine += cnt[sc];
+            int tot = 0;
+            int o = block_excl_scan<kSelThreads>(mine, tot, ss);
+            for (int sc = sc0; sc < sc1; ++sc) {
+                const int c = cnt[sc];
+                const int64_t src = rbase + static_cast<int64_t>(sc) * kSub;
+                for (int i = 0; i < c; ++i, ++o) {
+                    w.comp_key[rbase + o] = float_key(w.cand_score[src + i]);
+                    w.comp_pos[rbase + o] = w.cand_pos[src + i];
                 }
             }
-            if (!sel) atomicAdd(&mass[ix.pos_list[base + pos]], __expf(key_float(key) - shift));
+        } else {
+            float* lut_s = reinterpret_cast<float*>(lds);   // 16 KB of the key area
+            stage_head_lut<kSelThreads>(lut_s, w.lut + static_cast<int64_t>(bg) * kLutRow * D.G,
+                                        D.G, hh);
+            __syncthreads();
+            const uint4* codes = reinterpret_cast<const uint4*>(ix.codes) + base;
+            const float* coarse = w.coarse + static_cast<int64_t>(bg) * D.n_list * D.G;
+            for (int pos = tid; pos < n_r; pos += kSelThreads) {
+                const int j = ix.pos_list[base + pos];
+                float fs[1];
+                fine_sum<1>(lut_s, codes[pos], fs);
+                const float sc = pq_logit(ix.norms[base + pos], coarse[j * D.G + hh], fs[0]);
+                w.comp_key[rbase + pos] = float_key(sc);
+                w.comp_pos[rbase + pos] = static_cast<int32_t>(
+                    (static_cast<uint32_t>(j) << kPosBits) | static_cast<uint32_t>(pos));
+            }
+            total = n_r;
         }
-        int tot = 0;
-        const int o = block_excl_scan<kSelThreads>(sel ? 1 : 0, tot, sh);
-        if (sel && written + o < k) {
-            if (tok < 0) tok = perm[pos];
-            sel_tok[written + o] = tok;
-            sel_pos[written + o] = pos;
+        __syncthreads();
+        const uint32_t* ckey = w.comp_key + rbase;
+        const uint32_t* ccand = reinterpret_cast<const uint32_t*>(w.comp_pos + rbase);
+        auto KEY = [&](int i) { return ckey[i]; };
+        auto CAND = [&](int i) { return ccand[i]; };
+        if (total == 0) {
+            shift = neg_inf;
+            emit_selection(KEY, CAND, [](int, uint32_t, uint32_t) { return false; }, 0, 0,
+                           D.n_list, shift, mass, sel_pos, cand_mass, ss);
+        } else {
+            const SelectResult r = block_select_desc<kSelThreads>(
+                KEY, [](int) { return true; }, total, k > 0 ? k : 1, ss);
+            const uint32_t kth = k > 0 ? r.key : 0xffffffffu;
+            int tok_cut = 0x7fffffff;
+            if (k > 0 && r.count_equal > k - r.count_above) {
+                const SelectResult t = block_select_desc<kSelThreads>(
+                    [&](int i) { return ~static_cast<uint32_t>(perm[ccand[i] & kPosMask]); },
+                    [&](int i) { return ckey[i] == kth; }, total, k - r.count_above, ss);
+                tok_cut = static_cast<int>(~t.key);
+            }
+            shift = key_float(r.key);   // k-th largest, or the maximum when k = 0
+            emit_selection(
+                KEY, CAND,
+                [&](int, uint32_t key, uint32_t cand) {
+                    return k > 0 && (key > kth || (key == kth && perm[cand & kPosMask] <= tok_cut));
+                },
+                total, k, D.n_list, shift, mass, sel_pos, cand_mass, ss);
         }
-        written += tot;
     }
-    __syncthreads();
-    float* cm = w.cand_mass + static_cast<int64_t>(row) * D.n_list;
-    for (int j = tid; j < D.n_list; j += kSelThreads) cm[j] = mass[j];
     if (tid == 0) {
         w.row_shift[row] = shift;
         w.row_flag[row] = fallback ? 1 : 0;
@@ -207,9 +499,15 @@ hipError_t launch_sample(const Dims& D, const BatchInts& tk, const Index& ix, co
 
 hipError_t launch_select(const Dims& D, const BatchInts& tk, const Index& ix, const Work& w,
                          int force_fallback, hipStream_t s) {
-    hipLaunchKernelGGL(select_kernel, dim3(D.B * D.Hq), dim3(kSelThreads), 0, s, D, tk, ix, w,
-                       force_fallback);
+    hipLaunchKernelGGL(select_kernel, dim3(D.B * D.Hq), dim3(kSelThreads), kSelLdsBytes, s, D, tk,
+                       ix, w, force_fallback);
     return hipGetLastError();
+}
+
+hipError_t configure_select() {
+    return hipFuncSetAttribute(reinterpret_cast<const void*>(&select_kernel),
+                               hipFuncAttributeMaxDynamicSharedMemorySize,
+                               static_cast<int>(kSelLdsBytes));
 }
 
 }  // namespace pqhsa

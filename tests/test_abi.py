@@ -42,6 +42,7 @@ def shape(**kw):
     (dict(n_sink=4000, n_local=128), pqhsa.ERR_INVALID_ARGUMENT),
     (dict(n_local=-1), pqhsa.ERR_INVALID_ARGUMENT),
     (dict(kv_dtype=7), pqhsa.ERR_UNSUPPORTED),
+    (dict(max_seq=(1 << 20) + 16, max_topk=64), pqhsa.ERR_UNSUPPORTED),
 ])
 def test_create_rejects_bad_shapes_before_touching_the_device(lib, kw, status):
     ctx = ctypes.c_void_p(1234)
