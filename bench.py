@@ -30,6 +30,7 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBPS = 8000.0
 FLUSH_BYTES = 512 << 20
+COPY_CAL_BYTES = 256 << 20
 WORKLOAD = 2
 
 
@@ -75,7 +76,21 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--profile-only", action="store_true",
                     help="run the warm-up and timed decode calls only (for rocprofv3)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="with --profile-only: also run a 256 MiB fp32 elementwise copy "
+                         "(torch.neg) 5 times, whose FETCH_SIZE / WRITE_SIZE counters scale "
+                         "the operator's counters to bytes")
+    ap.add_argument("--summarize-trace", nargs=2, metavar=("STATS_CSV", "COMMAND"),
+                    help="print a summary of a rocprofv3 kernel_stats.csv and exit")
+    ap.add_argument("--summarize-pmc", nargs=4, metavar=("STAGE", "FETCH_CSV", "WRITE_CSV", "COMMANDS"),
+                    help="print the counter summary of one stage's kernel and exit")
     args = ap.parse_args()
+    if args.summarize_trace:
+        sys.stdout.write(summarize_trace(*args.summarize_trace))
+        return 0
+    if args.summarize_pmc:
+        sys.stdout.write(summarize_pmc(*args.summarize_pmc))
+        return 0
     if args.gpus != 1:
         print("bench.py measures one GPU: the operator is a single-GPU kernel path and this "
               "build has no multi-GPU mode (run with --gpus 1)", file=sys.stderr)
@@ -139,6 +154,14 @@ def main() -> int:
     t_pq, wall_pq = timed(pq_call, args.steps)
     if args.profile_only:
         log(f"PQ-HSA mean {t_pq.mean() * 1e3:.2f} us")
+        if args.copy_calibration:
+            n = COPY_CAL_BYTES // 4
+            src = torch.ones(n, dtype=torch.float32, device=dev)
+            dst = torch.empty_like(src)
+            for _ in range(5):
+                torch.neg(src, out=dst)
+            torch.cuda.synchronize()
+            log(f"copy calibration: 5 x {COPY_CAL_BYTES >> 20} MiB read + written")
         return 0
 
     # per-stage durations, HIP events around each kernel on the same stream
@@ -238,7 +261,7 @@ def main() -> int:
         "roofline": {"kernel": dom, "bound": "hbm", "achieved": round(dom_gbps, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(dom_gbps / HBM_PEAK_GBPS, 4),
-                     "algorithmic_bytes": stage_bytes[dom], "traffic": None},
+                     "algorithmic_bytes": stage_bytes[dom], "traffic": pmc_traffic(dom)},
         "stage_roofline_frac": stage_roofline,
         "dense_us_per_call": round(dense_us, 3),
         "dense_hbm_gbps": round(sum(n * wl.n_kv_heads * 2 * wl.head_dim * 2 for n in lens)
@@ -250,6 +273,104 @@ def main() -> int:
     print(json.dumps(rec), flush=True)
     ctx.close()
     return 0
+
+
+# Kernel sources whose text decides each stage's memory traffic: a counter
+# summary taken on other sources no longer describes the kernel.
+STAGE_KERNEL = dict(lut="lut_kernel", sample="sample_kernel", scan="scan_kernel",
+                    select="select_kernel", attend="attend_kernel", merge="merge_kernel")
+STAGE_SOURCES = dict(
+    lut=["lut.hip"], sample=["select.hip", "hist_select.h", "radix_select.h", "pq_score.h"],
+    scan=["scan.hip", "pq_score.h"], select=["select.hip", "hist_select.h", "radix_select.h"],
+    attend=["attend.hip"], merge=["attend.hip"])
+COMMON_SOURCES = ["device_common.h", "pqhsa_internal.h"]
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def source_hash(stage: str) -> str:
+    import hashlib
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2609_33746_amd", "csrc")
+    for f in STAGE_SOURCES[stage] + COMMON_SOURCES:
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
+    return h.hexdigest()[:16]
+
+
+def pmc_file(stage: str) -> str:
+    return os.path.join(PROFILES, f"{STAGE_KERNEL[stage]}_llama8b_n128k_pmc.txt")
+
+
+def pmc_traffic(stage: str):
+    """HBM bytes per launch of `stage` from its committed counter summary, or
+    None when there is none or it was taken on other kernel sources."""
+    path = pmc_file(stage)
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as fh:
+        for line in fh:
+            if ":" in line and not line.startswith(" "):
+                k_, v_ = line.split(":", 1)
+                vals[k_.strip()] = v_.strip()
+    if vals.get("source_hash") != source_hash(stage):
+        log(f"{os.path.basename(path)} was taken on other sources: traffic unknown")
+        return None
+    return int(float(vals["traffic_bytes_per_launch"]))
+
+
+def _csv_rows(path):
+    import csv
+    with open(path) as fh:
+        return list(csv.DictReader(fh))
+
+
+def summarize_trace(stats_csv: str, command: str) -> str:
+    """Text summary of a rocprofv3 --kernel-trace --stats run (kernel_stats.csv)."""
+    out = [f"command: {command}", "kernel  calls  avg_us  min_us  max_us"]
+    for r in _csv_rows(stats_csv):
+        if "pqhsa" in r["Name"]:
+            out.append(f"{r['Name'].split('(')[0]}  {r['Calls']}  {float(r['AverageNs']) / 1e3:.2f}  "
+                       f"{float(r['MinNs']) / 1e3:.2f}  {float(r['MaxNs']) / 1e3:.2f}")
+    return "\n".join(out) + "\n"
+
+
+def summarize_pmc(stage: str, fetch_csv: str, write_csv: str, commands: str) -> str:
+    """Counter summary of one stage's kernel: FETCH_SIZE and WRITE_SIZE (KiB
+    per dispatch) from two runs, each scaled by what the same counter reads
+    for the calibration copy (COPY_CAL_BYTES read and written)."""
+    def per_kernel(path, counter):
+        acc = {}
+        for r in _csv_rows(path):
+            if r["Counter_Name"] == counter:
+                acc.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+        return {k_: sum(v_) / len(v_) for k_, v_ in acc.items()}
+    fetch = per_kernel(fetch_csv, "FETCH_SIZE")
+    write = per_kernel(write_csv, "WRITE_SIZE")
+    cal_f = [v_ for k_, v_ in fetch.items() if "neg_kernel" in k_]
+    cal_w = [v_ for k_, v_ in write.items() if "neg_kernel" in k_]
+    kib = COPY_CAL_BYTES / 1024
+    f_scale = kib / cal_f[0]
+    w_scale = kib / cal_w[0]
+    name = STAGE_KERNEL[stage]
+    kf = [v_ for k_, v_ in fetch.items() if f"pqhsa::{name}" in k_]
+    kw = [v_ for k_, v_ in write.items() if f"pqhsa::{name}" in k_]
+    traffic = (kf[0] * f_scale + kw[0] * w_scale) * 1024
+    lines = [
+        f"commands: {commands}",
+        f"kernel: {name}",
+        f"source_hash: {source_hash(stage)}",
+        f"copy_fetch_kib_per_dispatch: {cal_f[0]:.1f} (expected {kib:.0f}; scale {f_scale:.4f})",
+        f"copy_write_kib_per_dispatch: {cal_w[0]:.1f} (expected {kib:.0f}; scale {w_scale:.4f})",
+        f"fetch_kib_per_dispatch: {kf[0]:.1f}",
+        f"write_kib_per_dispatch: {kw[0]:.1f}",
+        f"traffic_bytes_per_launch: {traffic:.0f}",
+        "all pqhsa kernels (fetch KiB, write KiB per dispatch, unscaled):",
+    ]
+    for k_ in fetch:
+        if "pqhsa" in k_:
+            lines.append(f"  {k_.split('(')[0]}  {fetch[k_]:.1f}  {write.get(k_, float('nan')):.1f}")
+    return "\n".join(lines) + "\n"
 
 
 def cpu_baseline(inp, topk, budget_s: float):

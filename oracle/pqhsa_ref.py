@@ -22,7 +22,7 @@ Everything is written from the paper's statement of the method:
   (no background), C (token-weighted global value mean) and Bx (mean of the
   unselected members of each list).
 
-Readings where the paper is silent (all listed in the design doc):
+Readings where the paper is silent:
 * the top-k tie-break is the smaller token id;
 * r_q = 0 gives a score of 0 for every indexed token;
 * an empty list, or a list whose members are all selected, contributes 0.
