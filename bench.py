@@ -1,6 +1,6 @@
 """Benchmark of one PQ-HSA decode-attention call on one MI355X.
 
-A step is one pqhsa_decode call (LUT build, threshold sample, code scan,
+A step is one pqhsa_decode call (LUT build + threshold sample, code scan,
 top-k select, exact attention + per-list background, merge) over the
 Llama-3.1-8B-shaped 128K workload: batch 1, 32 query / 8 KV heads, d = 128,
 N = 131072 bf16 K/V, 1024 lists, 16 x 8-bit PQ codes, k = 1311 (1%).
@@ -215,12 +215,12 @@ def main() -> int:
     us_med = float(np.median(t_pq)) * 1e3
     dense_us = float(np.mean(t_dense)) * 1e3
     n_scanned = sum((n - wl.n_sink - wl.n_local) * wl.n_kv_heads for n in lens)
-    stage_bytes = dict(lut=by["lut"], sample=0, scan=by["scan"], select=by["select"],
+    stage_bytes = dict(prologue=by["lut"], scan=by["scan"], select=by["select"],
                        attend=by["attend"] + by["background"], merge=by["out"])
     # the dominant kernel: the longest one among those whose time is set by the
-    # bytes they must read (sample and select read only the workspace and
-    # write a few KB of selected ids)
-    dom = max((s_ for s_ in stage_us if s_ not in ("sample", "select")), key=stage_us.get)
+    # bytes they must read (select reads only the workspace and writes a few
+    # KB of selected ids)
+    dom = max((s_ for s_ in stage_us if s_ != "select"), key=stage_us.get)
     dom_gbps = stage_bytes[dom] / (stage_us[dom] * 1e-6) / 1e9
     stage_roofline = {s_: round(stage_bytes[s_] / (stage_us[s_] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)
                       for s_ in stage_us if stage_bytes.get(s_, 0) > 0}
@@ -277,10 +277,10 @@ def main() -> int:
 
 # Kernel sources whose text decides each stage's memory traffic: a counter
 # summary taken on other sources no longer describes the kernel.
-STAGE_KERNEL = dict(lut="lut_kernel", sample="sample_kernel", scan="scan_kernel",
-                    select="select_kernel", attend="attend_kernel", merge="merge_kernel")
+STAGE_KERNEL = dict(prologue="prologue_kernel", scan="scan_kernel", select="select_kernel",
+                    attend="attend_kernel", merge="merge_kernel")
 STAGE_SOURCES = dict(
-    lut=["lut.hip"], sample=["select.hip", "hist_select.h", "radix_select.h", "pq_score.h"],
+    prologue=["prologue.hip", "hist_select.h", "radix_select.h", "pq_score.h"],
     scan=["scan.hip", "pq_score.h"], select=["select.hip", "hist_select.h", "radix_select.h"],
     attend=["attend.hip"], merge=["attend.hip"])
 COMMON_SOURCES = ["device_common.h", "pqhsa_internal.h"]

@@ -166,8 +166,8 @@ enum {
 pqhsa_status pqhsa_set_option(pqhsa_ctx* ctx, int32_t option, int64_t value);
 
 /* Stage durations (ms) of the last decode call made with stage timing on, in
- * launch order: [0] LUT build, [1] threshold sample, [2] code scan,
- * [3] top-k select, [4] exact attention + background, [5] merge.
+ * launch order: [0] LUT build + threshold sample, [1] code scan,
+ * [2] top-k select, [3] exact attention + background, [4] merge.
  * `n` is the capacity of `ms`; *n_out receives the number of stages.
  * Synchronises on the recorded events. */
 pqhsa_status pqhsa_stage_times(pqhsa_ctx* ctx, float* ms, int32_t n, int32_t* n_out);

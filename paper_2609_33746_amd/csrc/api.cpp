@@ -22,7 +22,7 @@ namespace {
 
 thread_local std::string g_create_error;
 
-constexpr int kStages = 6;
+constexpr int kStages = 5;
 
 }  // namespace
 
@@ -41,14 +41,12 @@ struct pqhsa_ctx {
     int32_t* perm = nullptr;
     int32_t* pos_list = nullptr;
     int32_t* loff = nullptr;
-    int32_t* seg0 = nullptr;
     float* centroids = nullptr;
     float* codebooks = nullptr;
     float* means = nullptr;
     int32_t* n_seq_dev = nullptr;
     int32_t* n_r_dev = nullptr;
-    ScanWG* scan_table = nullptr;
-    int n_scan_wg = 0;
+    int scan_nwg = 0;   // scan workgroups per (b, kv head)
 
     // workspace
     Work w{};
@@ -71,7 +69,6 @@ struct pqhsa_ctx {
         ix.perm = perm;
         ix.pos_list = pos_list;
         ix.loff = loff;
-        ix.seg0 = seg0;
         ix.centroids = centroids;
         ix.codebooks = codebooks;
         ix.means = means;
@@ -233,7 +230,6 @@ pqhsa_status pqhsa_create(const pqhsa_shape* shape, pqhsa_ctx** out) {
     if (c->nsplit_max < 1) c->nsplit_max = 1;
     const int n_bgc = (D.n_list + kBgLists - 1) / kBgLists;
     c->dense_nsplit = (D.rcap + kDenseRows - 1) / kDenseRows;
-    const size_t max_scan_wg = BG * ((D.nsub_cap + kScanWaves - 1) / kScanWaves);
 
     Work& w = c->w;
     hipError_t ea = hipSuccess;
@@ -243,18 +239,15 @@ pqhsa_status pqhsa_create(const pqhsa_shape* shape, pqhsa_ctx** out) {
     A(dev_alloc(c, &c->perm, BG * rc));
     A(dev_alloc(c, &c->pos_list, BG * rc));
     A(dev_alloc(c, &c->loff, BG * (L + 1)));
-    A(dev_alloc(c, &c->seg0, BG * (L + 1)));
     A(dev_alloc(c, &c->centroids, BG * L * kHeadDim));
     A(dev_alloc(c, &c->codebooks, BG * kPqM * kKsub * kDsub));
     A(dev_alloc(c, &c->means, BG * L * kHeadDim));
     A(dev_alloc(c, &c->n_seq_dev, B));
     A(dev_alloc(c, &c->n_r_dev, B));
-    A(dev_alloc(c, &c->scan_table, max_scan_wg));
     A(dev_alloc(c, &w.lut, BG * kLutRow * G));
     A(dev_alloc(c, &w.coarse, BG * L * G));
     A(dev_alloc(c, &w.tau_lo, BQ));
-    A(dev_alloc(c, &w.cand_score, BQ * rc));
-    A(dev_alloc(c, &w.cand_pos, BQ * rc));
+    A(dev_alloc(c, &w.cand, BQ * rc));
     A(dev_alloc(c, &w.cand_cnt, BQ * D.nsub_cap));
     A(dev_alloc(c, &w.seg_sum, BG * D.nseg_cap * G));
     A(dev_alloc(c, &w.comp_key, BQ * rc));
@@ -307,9 +300,7 @@ pqhsa_status pqhsa_index_prepare(pqhsa_ctx* c, const int32_t* seq_lens, const in
     if (e != hipSuccess) return hip_fail(c, e, "copying list ids to the host");
 
     // stable counting sort of R_b by list id, per (b, kv head)
-    std::vector<int32_t> perm(BG * rc, -1), pos_list(BG * rc, 0), loff(BG * (L + 1)),
-        seg0(BG * (L + 1));
-    std::vector<ScanWG> table;
+    std::vector<int32_t> perm(BG * rc, -1), pos_list(BG * rc, 0), loff(BG * (L + 1));
     std::vector<int32_t> cnt(L);
     for (int b = 0; b < B; ++b) {
         for (int g = 0; g < Hkv; ++g) {
@@ -323,14 +314,8 @@ pqhsa_status pqhsa_index_prepare(pqhsa_ctx* c, const int32_t* seq_lens, const in
                 ++cnt[a[i]];
             }
             int32_t* lo = loff.data() + bg * (L + 1);
-            int32_t* sg = seg0.data() + bg * (L + 1);
             lo[0] = 0;
-            sg[0] = 0;
-            for (int j = 0; j < L; ++j) {
-                lo[j + 1] = lo[j] + cnt[j];
-                const int nseg = cnt[j] ? (lo[j + 1] - 1) / kSub - lo[j] / kSub + 1 : 0;
-                sg[j + 1] = sg[j] + nseg;
-            }
+            for (int j = 0; j < L; ++j) lo[j + 1] = lo[j] + cnt[j];
             std::vector<int32_t> fillp(lo, lo + L);
             int32_t* pm = perm.data() + bg * rc;
             int32_t* pl = pos_list.data() + bg * rc;
@@ -338,15 +323,6 @@ pqhsa_status pqhsa_index_prepare(pqhsa_ctx* c, const int32_t* seq_lens, const in
                 const int p = fillp[a[i]]++;
                 pm[p] = i;
                 pl[p] = a[i];
-            }
-            const int nsub = (nr[b] + kSub - 1) / kSub;
-            for (int s0 = 0; s0 < nsub; s0 += kScanWaves) {
-                ScanWG e{};
-                e.bg = static_cast<int>(bg);
-                e.sub0 = s0;
-                for (int wv = 0; wv < kScanWaves; ++wv)
-                    e.list0[wv] = s0 + wv < nsub ? pl[(s0 + wv) * kSub] : 0;
-                table.push_back(e);
             }
         }
     }
@@ -360,10 +336,8 @@ pqhsa_status pqhsa_index_prepare(pqhsa_ctx* c, const int32_t* seq_lens, const in
     H2D(c->perm, perm.data(), perm.size() * 4);
     H2D(c->pos_list, pos_list.data(), pos_list.size() * 4);
     H2D(c->loff, loff.data(), loff.size() * 4);
-    H2D(c->seg0, seg0.data(), seg0.size() * 4);
     H2D(c->n_seq_dev, lens.data(), B * 4);
     H2D(c->n_r_dev, nr.data(), B * 4);
-    if (!table.empty()) H2D(c->scan_table, table.data(), table.size() * sizeof(ScanWG));
     D2D(c->centroids, centroids, BG * L * kHeadDim * 4);
     D2D(c->codebooks, codebooks, BG * kPqM * kKsub * kDsub * 4);
     D2D(c->means, list_means, BG * L * kHeadDim * 4);
@@ -374,14 +348,16 @@ pqhsa_status pqhsa_index_prepare(pqhsa_ctx* c, const int32_t* seq_lens, const in
     if (e != hipSuccess) return hip_fail(c, e, "preparing the index");
     c->seq_lens = lens;
     c->n_r = nr;
-    c->n_scan_wg = static_cast<int>(table.size());
+    int nr_max = 0;
+    for (int b = 0; b < B; ++b) nr_max = std::max(nr_max, nr[b]);
+    c->scan_nwg = (nr_max + kScanWaves * kSub - 1) / (kScanWaves * kSub);
     c->prepared = true;
     return PQHSA_OK;
 }
 
 static pqhsa_status decode_impl(pqhsa_ctx* c, const void* q, const void* k, const void* v,
                                 const int64_t* strides, const int32_t* topk, float* out,
-                                hipStream_t stream, BatchInts* tk_out) {
+                                hipStream_t stream, BatchArgs* ba_out) {
     if (!c) return fail(nullptr, PQHSA_ERR_INVALID_ARGUMENT, "ctx is NULL");
     c->err.clear();
     if (!c->prepared) return fail(c, PQHSA_ERR_NOT_PREPARED, "pqhsa_index_prepare has not succeeded");
@@ -392,12 +368,13 @@ static pqhsa_status decode_impl(pqhsa_ctx* c, const void* q, const void* k, cons
     st = check_device(c);
     if (st != PQHSA_OK) return st;
     const Dims& D = c->D;
-    BatchInts tk;
+    BatchArgs ba{};
     for (int b = 0; b < D.B; ++b) {
         if (topk[b] < 0 || topk[b] > c->n_r[b] || topk[b] > c->shape.max_topk)
             return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "topk[%d] = %d outside [0, min(|R_b| = %d, max_topk = %d)]",
                         b, topk[b], c->n_r[b], c->shape.max_topk);
-        tk.v[b] = topk[b];
+        ba.topk[b] = topk[b];
+        ba.n_r[b] = c->n_r[b];
     }
     const Index ix = c->index();
     const bool timed = c->timing != 0;
@@ -413,21 +390,19 @@ static pqhsa_status decode_impl(pqhsa_ctx* c, const void* q, const void* k, cons
         if (timed && e == hipSuccess) e = hipEventRecord(c->ev[i], stream);
     };
     mark(0);
-    if (e == hipSuccess) e = launch_lut(D, kv, ix, c->w, stream);
+    if (e == hipSuccess) e = launch_prologue(D, ba, kv, ix, c->w, c->bias, stream);
     mark(1);
-    if (e == hipSuccess) e = launch_sample(D, tk, ix, c->w, c->bias, stream);
+    if (e == hipSuccess) e = launch_scan(D, ba, ix, c->w, c->scan_nwg, stream);
     mark(2);
-    if (e == hipSuccess) e = launch_scan(D, ix, c->w, c->scan_table, c->n_scan_wg, stream);
+    if (e == hipSuccess) e = launch_select(D, ba, ix, c->w, c->force_fallback, stream);
     mark(3);
-    if (e == hipSuccess) e = launch_select(D, tk, ix, c->w, c->force_fallback, stream);
+    if (e == hipSuccess) e = launch_attend(D, ba, kv, ix, c->w, c->nsplit_max, stream);
     mark(4);
-    if (e == hipSuccess) e = launch_attend(D, tk, kv, ix, c->w, c->nsplit_max, stream);
+    if (e == hipSuccess) e = launch_merge(D, ba, c->w, out, c->nsplit_max, stream);
     mark(5);
-    if (e == hipSuccess) e = launch_merge(D, tk, c->w, out, c->nsplit_max, stream);
-    mark(6);
     if (e != hipSuccess) return hip_fail(c, e, "enqueueing the decode kernels");
     c->timed_valid = timed;
-    if (tk_out) *tk_out = tk;
+    if (ba_out) *ba_out = ba;
     return PQHSA_OK;
 }
 
@@ -446,10 +421,10 @@ pqhsa_status pqhsa_decode_debug(pqhsa_ctx* c, const void* q, const void* k, cons
             if (topk[b] > 8192)
                 return fail(c, PQHSA_ERR_UNSUPPORTED, "the debug call sorts at most 8192 selected tokens per row");
     }
-    BatchInts tk;
-    pqhsa_status st = decode_impl(c, q, k, v, kv_strides, topk, out, stream, &tk);
+    BatchArgs ba{};
+    pqhsa_status st = decode_impl(c, q, k, v, kv_strides, topk, out, stream, &ba);
     if (st != PQHSA_OK) return st;
-    hipError_t e = launch_debug(c->D, tk, c->index(), c->w, selected, unselected_per_list, scores, stream);
+    hipError_t e = launch_debug(c->D, ba, c->index(), c->w, selected, unselected_per_list, scores, stream);
     if (e == hipSuccess) e = hipStreamSynchronize(stream);
     if (e != hipSuccess) return hip_fail(c, e, "running the debug kernels");
     return PQHSA_OK;

@@ -104,7 +104,7 @@ __device__ __forceinline__ void block_combine(const Online& o, float* sm, float*
 }
 
 template <typename T, int G>
-__global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchInts tk, KV kv,
+__global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchArgs ba, KV kv,
                                                               Index ix, Work w, int nsplit_max,
                                                               int n_bgc) {
     __shared__ float sm[kStreams], sz[kStreams];
@@ -124,15 +124,15 @@ __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchInts 
         const int b = row / D.Hq;
         const int h = row % D.Hq;
         const int g = h / G;
-        const int k = tk.v[b];
-        const int n_seq = ix.n_seq[b];
+        const int k = ba.topk[b];
+        const int n_r = ba.n_r[b];
+        const int n_seq = n_r + D.n_sink + D.n_local;
         const int nE = D.n_sink + D.n_local + k;
         const int e0 = split * kAttnRows;
         if (e0 >= nE) return;   // the merge reads only the splits that exist
         const int e1 = min(e0 + kAttnRows, nE);
         const int32_t* sel = w.sel_pos + static_cast<int64_t>(row) * D.max_topk;
         const int32_t* perm = ix.perm + static_cast<int64_t>(b * D.Hkv + g) * D.rcap;
-        const int n_r = ix.n_r[b];
         const int local0 = n_seq - D.n_local;
         int pos[kRowsPerStream];
 #pragma unroll
@@ -216,9 +216,13 @@ __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchInts 
     {
         const bool ok = lane < kListsPerWave && my_j < D.n_list;
         const int jj = ok ? my_j : 0;
-        const int32_t* seg0 = ix.seg0 + static_cast<int64_t>(bg) * (D.n_list + 1);
-        const int s0 = seg0[jj];
-        const int s1 = ok ? seg0[jj + 1] : s0;
+        // list j's positions [lo, hi) span sub-chunks lo / kSub .. (hi - 1) / kSub,
+        // whose masses sit at segments j + s
+        const int32_t* loff = ix.loff + static_cast<int64_t>(bg) * (D.n_list + 1);
+        const int lo = loff[jj];
+        const int hi = ok ? loff[jj + 1] : lo;
+        const int s0 = jj + lo / kSub;
+        const int s1 = hi > lo ? jj + (hi - 1) / kSub + 1 : s0;
         const float* segs = w.seg_sum + static_cast<int64_t>(bg) * D.nseg_cap * G;
 #pragma unroll
         for (int hh = 0; hh < G; ++hh) {
@@ -345,31 +349,31 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(Dims D, BatchInts 
 }
 
 template <typename T, int G>
-static hipError_t launch_attend_t(const Dims& D, const BatchInts& tk, const KV& kv,
+static hipError_t launch_attend_t(const Dims& D, const BatchArgs& ba, const KV& kv,
                                   const Index& ix, const Work& w, int nsplit_max, hipStream_t s) {
     const int n_bgc = (D.n_list + kBgLists - 1) / kBgLists;
     const int grid = D.B * D.Hq * nsplit_max + D.B * D.Hkv * n_bgc;
-    hipLaunchKernelGGL((attend_kernel<T, G>), dim3(grid), dim3(kAttnThreads), 0, s, D, tk, kv,
+    hipLaunchKernelGGL((attend_kernel<T, G>), dim3(grid), dim3(kAttnThreads), 0, s, D, ba, kv,
                        ix, w, nsplit_max, n_bgc);
     return hipGetLastError();
 }
 
 template <typename T>
-static hipError_t launch_attend_g(const Dims& D, const BatchInts& tk, const KV& kv,
+static hipError_t launch_attend_g(const Dims& D, const BatchArgs& ba, const KV& kv,
                                   const Index& ix, const Work& w, int nsplit_max, hipStream_t s) {
     switch (D.G) {
-        case 1: return launch_attend_t<T, 1>(D, tk, kv, ix, w, nsplit_max, s);
-        case 2: return launch_attend_t<T, 2>(D, tk, kv, ix, w, nsplit_max, s);
-        case 4: return launch_attend_t<T, 4>(D, tk, kv, ix, w, nsplit_max, s);
-        case 8: return launch_attend_t<T, 8>(D, tk, kv, ix, w, nsplit_max, s);
+        case 1: return launch_attend_t<T, 1>(D, ba, kv, ix, w, nsplit_max, s);
+        case 2: return launch_attend_t<T, 2>(D, ba, kv, ix, w, nsplit_max, s);
+        case 4: return launch_attend_t<T, 4>(D, ba, kv, ix, w, nsplit_max, s);
+        case 8: return launch_attend_t<T, 8>(D, ba, kv, ix, w, nsplit_max, s);
         default: return hipErrorInvalidValue;
     }
 }
 
-hipError_t launch_attend(const Dims& D, const BatchInts& tk, const KV& kv, const Index& ix,
+hipError_t launch_attend(const Dims& D, const BatchArgs& ba, const KV& kv, const Index& ix,
                          const Work& w, int nsplit_max, hipStream_t s) {
-    return kv.bf16 ? launch_attend_g<bf16_t>(D, tk, kv, ix, w, nsplit_max, s)
-                   : launch_attend_g<float>(D, tk, kv, ix, w, nsplit_max, s);
+    return kv.bf16 ? launch_attend_g<bf16_t>(D, ba, kv, ix, w, nsplit_max, s)
+                   : launch_attend_g<float>(D, ba, kv, ix, w, nsplit_max, s);
 }
 
 static hipError_t launch_merge_parts(const Dims& D, const BatchInts& ne, const float* partial,
@@ -381,11 +385,11 @@ static hipError_t launch_merge_parts(const Dims& D, const BatchInts& ne, const f
     return hipGetLastError();
 }
 
-hipError_t launch_merge(const Dims& D, const BatchInts& tk, const Work& w, float* out,
+hipError_t launch_merge(const Dims& D, const BatchArgs& ba, const Work& w, float* out,
                         int nsplit_max, hipStream_t s) {
     BatchInts ne;
     for (int b = 0; b < D.B; ++b) {
-        const int nE = D.n_sink + D.n_local + tk.v[b];
+        const int nE = D.n_sink + D.n_local + ba.topk[b];
         ne.v[b] = (nE + kAttnRows - 1) / kAttnRows;
     }
     const int n_bgc = (D.n_list + kBgLists - 1) / kBgLists;

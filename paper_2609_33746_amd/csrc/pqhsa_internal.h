@@ -44,6 +44,14 @@ struct BatchInts {
     int32_t v[kMaxBatch];
 };
 
+// The per-sequence integers every decode kernel needs, passed by value so
+// that no kernel starts with a dependent load: k_b and |R_b|
+// (N_b = |R_b| + n_sink + n_local).
+struct BatchArgs {
+    int32_t topk[kMaxBatch];
+    int32_t n_r[kMaxBatch];
+};
+
 // Prepared index (list-major), owned by the context.
 struct Index {
     const uint8_t* codes;      // [B, Hkv, rcap, M]
@@ -51,7 +59,6 @@ struct Index {
     const int32_t* perm;       // [B, Hkv, rcap] token id of each position
     const int32_t* pos_list;   // [B, Hkv, rcap] list id of each position
     const int32_t* loff;       // [B, Hkv, n_list + 1] list starts
-    const int32_t* seg0;       // [B, Hkv, n_list + 1] first segment of each list
     const float* centroids;    // [B, Hkv, n_list, d]
     const float* codebooks;    // [B, Hkv, M, K, d/M]
     const float* means;        // [B, Hkv, n_list, d]
@@ -64,26 +71,19 @@ struct Work {
     float* lut;          // [B, Hkv, M, K, G]   (q^(m) . p_{m,z}) / sqrt(d)
     float* coarse;       // [B, Hkv, n_list, G] (q . c_j) / sqrt(d)
     float* tau_lo;       // [B, Hq] candidate threshold
-    float* cand_score;   // [B, Hq, rcap] per sub-chunk compacted candidates
-    int32_t* cand_pos;   // [B, Hq, rcap] list id << kPosBits | list-major position
+    uint2* cand;         // [B, Hq, rcap] candidates compacted per sub-chunk: (score bits,
+                         //   list id << kPosBits | list-major position)
     int32_t* cand_cnt;   // [B, Hq, nsub_cap]
-    float* seg_sum;      // [B, Hkv, nseg_cap, G] below-threshold masses
+    float* seg_sum;      // [B, Hkv, nseg_cap, G] below-threshold masses; the pair
+                         //   (list j, sub-chunk s) uses segment j + s
     uint32_t* comp_key;  // [B, Hq, rcap] contiguous candidates (order keys)
-    int32_t* comp_pos;   // [B, Hq, rcap] (same packing as cand_pos)
+    int32_t* comp_pos;   // [B, Hq, rcap] (same packing as the candidate word)
     int32_t* sel_pos;    // [B, Hq, max_topk] list-major positions of T
     float* cand_mass;    // [B, Hq, n_list] sum over the list's unselected candidates of
                          //   exp(l~ - shift)
     float* row_shift;    // [B, Hq] shift of the background masses
     int32_t* row_flag;   // [B, Hq] 1 when the row took the re-scan path
     float* partial;      // [B, Hq, nsplit_max + n_bgc, kPartStride]
-};
-
-// One scan workgroup: kScanWaves consecutive sub-chunks of one (b, kv head),
-// with the list id of each sub-chunk's first position.
-struct ScanWG {
-    int bg;
-    int sub0;
-    int list0[kScanWaves];
 };
 
 struct KV {
@@ -100,24 +100,23 @@ struct KV {
 hipError_t configure_scan();
 hipError_t configure_select();
 
-hipError_t launch_lut(const Dims& D, const KV& kv, const Index& ix, const Work& w,
-                      hipStream_t s);
-hipError_t launch_sample(const Dims& D, const BatchInts& tk, const Index& ix, const Work& w,
-                         float bias, hipStream_t s);
-hipError_t launch_scan(const Dims& D, const Index& ix, const Work& w, const ScanWG* wg_table,
-                       int n_wg, hipStream_t s);
-hipError_t launch_select(const Dims& D, const BatchInts& tk, const Index& ix, const Work& w,
+hipError_t launch_prologue(const Dims& D, const BatchArgs& ba, const KV& kv, const Index& ix,
+                           const Work& w, float bias, hipStream_t s);
+// nwg = scan workgroups per (batch element, KV head): enough for the longest R_b
+hipError_t launch_scan(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w, int nwg,
+                       hipStream_t s);
+hipError_t launch_select(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w,
                          int force_fallback, hipStream_t s);
-hipError_t launch_attend(const Dims& D, const BatchInts& tk, const KV& kv, const Index& ix,
+hipError_t launch_attend(const Dims& D, const BatchArgs& ba, const KV& kv, const Index& ix,
                          const Work& w, int nsplit_max, hipStream_t s);
-hipError_t launch_merge(const Dims& D, const BatchInts& tk, const Work& w, float* out,
+hipError_t launch_merge(const Dims& D, const BatchArgs& ba, const Work& w, float* out,
                         int nsplit_max, hipStream_t s);
 hipError_t launch_dense(const Dims& D, const KV& kv, const BatchInts& lens, float* partial,
                         float* out, int nsplit_max, hipStream_t s);
 hipError_t launch_prepare_gather(const Dims& D, const uint8_t* codes_in, const float* norms_in,
                                  const Index& ix, uint8_t* codes_out, float* norms_out,
                                  hipStream_t s);
-hipError_t launch_debug(const Dims& D, const BatchInts& tk, const Index& ix, const Work& w,
+hipError_t launch_debug(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w,
                         int32_t* selected, int32_t* unselected, float* scores,
                         hipStream_t s);
 

@@ -70,7 +70,7 @@ __global__ __launch_bounds__(kDbgThreads) void score_dump_kernel(Dims D, Index i
 
 // Sort the selected token ids of each row ascending (bitonic, in LDS), pad with -1,
 // and count |B n R_j| = |R_j| - |T n R_j| per list.
-__global__ __launch_bounds__(kDbgThreads) void sel_debug_kernel(Dims D, BatchInts tk, Index ix,
+__global__ __launch_bounds__(kDbgThreads) void sel_debug_kernel(Dims D, BatchArgs ba, Index ix,
                                                                 Work w, int32_t* __restrict__ selected,
                                                                 int32_t* __restrict__ unselected) {
     __shared__ int keys[kSortCap];
@@ -79,7 +79,7 @@ __global__ __launch_bounds__(kDbgThreads) void sel_debug_kernel(Dims D, BatchInt
     const int b = row / D.Hq;
     const int g = (row % D.Hq) / D.G;
     const int bg = b * D.Hkv + g;
-    const int k = tk.v[b];
+    const int k = ba.topk[b];
     const int32_t* sp = w.sel_pos + static_cast<int64_t>(row) * D.max_topk;
     const int64_t base = static_cast<int64_t>(bg) * D.rcap;
     if (selected) {
@@ -118,7 +118,7 @@ __global__ __launch_bounds__(kDbgThreads) void sel_debug_kernel(Dims D, BatchInt
     }
 }
 
-hipError_t launch_debug(const Dims& D, const BatchInts& tk, const Index& ix, const Work& w,
+hipError_t launch_debug(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w,
                         int32_t* selected, int32_t* unselected, float* scores, hipStream_t s) {
     if (scores) {
         const int64_t n = static_cast<int64_t>(D.B) * D.Hq * D.rcap;
@@ -133,7 +133,7 @@ hipError_t launch_debug(const Dims& D, const BatchInts& tk, const Index& ix, con
         if (e != hipSuccess) return e;
     }
     if (selected || unselected) {
-        hipLaunchKernelGGL(sel_debug_kernel, dim3(D.B * D.Hq), dim3(kDbgThreads), 0, s, D, tk, ix, w,
+        hipLaunchKernelGGL(sel_debug_kernel, dim3(D.B * D.Hq), dim3(kDbgThreads), 0, s, D, ba, ix, w,
                            selected, unselected);
         return hipGetLastError();
     }

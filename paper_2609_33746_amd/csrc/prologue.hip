@@ -1,0 +1,340 @@
+// Decode prologue: the LUT build (Section 3.1, Eq. 2) and the candidate
+// threshold sample, in one launch with two workgroup roles that do not wait
+// for each other.
+//
+// LUT role, per (batch element, KV head): the fine table
+// F[m][z][hh] = (q_hh^(m) . p_{m,z}) / sqrt(d) for the G query heads of the
+// group, and the coarse table C[j][hh] = (q_hh . c_j) / sqrt(d).
+// Folding r_q / sqrt(d) into the tables: (r_q / sqrt(d)) u_q . x = q . x / sqrt(d),
+// so the tables are built from q / sqrt(d) directly and no normalisation of q
+// is needed (a zero query gives all-zero tables, hence zero scores).
+//
+// Sample role, per (batch element, query head) row: scores a stratified
+// sample of the row's list-major positions (contiguous runs of kSampleRun
+// positions, evenly spread) and takes a sample order statistic as the
+// candidate threshold tau_lo, chosen so that about twice k tokens of the
+// whole row score at or above it. The role builds the table entries it needs
+// itself (the head's fine table and the coarse terms of the lists its
+// samples fall in), with the same arithmetic as the LUT role, so it needs no
+// result of the LUT role. Any threshold gives the same final output: it only
+// decides how many candidates the scan emits (the top-k stage falls back to
+// an exact re-scan when fewer than k tokens reach it).
+#include "device_common.h"
+#include "hist_select.h"
+#include "pq_score.h"
+#include "pqhsa_internal.h"
+#include "radix_select.h"
+
+namespace pqhsa {
+
+constexpr int kProThreads = 512;
+constexpr int kFineWg = kProThreads / kKsub;              // subspaces per fine workgroup: 2
+static_assert(kFineWg * kKsub == kProThreads && kPqM % kFineWg == 0, "fine tiling");
+constexpr int kCoarseLists = 128;                          // lists per coarse workgroup
+constexpr int kCoarseGroups = kProThreads / 16;            // 16-lane groups
+constexpr int kCoarsePer = kCoarseLists / kCoarseGroups;   // lists per group: 4
+constexpr int kSamplesPer = kMaxSamples / kProThreads;     // samples per thread: 4
+constexpr int kSampleListsPer = 12;                        // sampled lists per 16-lane group and batch
+constexpr int kFinePer = kLutRow / kProThreads;            // fine entries per thread: 8
+static_assert(kPqM * (kKsub / kFinePer) == kProThreads, "the sample role builds every fine entry once");
+static_assert(kCoarsePer * kCoarseGroups == kCoarseLists, "coarse tiling");
+static_assert(kSamplesPer * kProThreads == kMaxSamples && kSampleRun % kSamplesPer == 0, "samples");
+
+// (q^(m) / sqrt(d)) . p_{m,z}: 8 products summed in order t = 0..7
+__device__ __forceinline__ float fine_entry(const float (&qs)[kDsub], const float4 p0,
+                                           const float4 p1) {
+    const float pv[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+    float acc = 0.0f;
+#pragma unroll
+    for (int t = 0; t < kDsub; ++t) acc = fmaf(qs[t], pv[t], acc);
+    return acc;
+}
+
+// (q / sqrt(d)) . c over 16 lanes of 8 dimensions each; every lane of the
+// 16-lane group receives the same sum.
+__device__ __forceinline__ float coarse_entry(const float (&qc)[8], const float4 c0,
+                                             const float4 c1) {
+    const float cf[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+    float acc = 0.0f;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) acc = fmaf(qc[t], cf[t], acc);
+    return sum16(acc);
+}
+
+template <typename T, int G>
+__device__ __forceinline__ void lut_role(const Dims& D, const T* __restrict__ q,
+                                         const float* __restrict__ codebooks,
+                                         const float* __restrict__ centroids, const Work& w,
+                                         int bg, int part) {
+    const int b = bg / D.Hkv;
+    const int g = bg % D.Hkv;
+    const T* qg = q + (static_cast<int64_t>(b) * D.Hq + g * G) * kHeadDim;
+    const int tid = threadIdx.x;
+    if (part < kPqM / kFineWg) {
+        // fine table: one (subspace, codeword) per thread
+        const int m = part * kFineWg + tid / kKsub;
+        const int z = tid % kKsub;
+        const float* p = codebooks + ((static_cast<int64_t>(bg) * kPqM + m) * kKsub + z) * kDsub;
+        const float4 p0 = *reinterpret_cast<const float4*>(p);
+        const float4 p1 = *reinterpret_cast<const float4*>(p + 4);
+        float* o = w.lut + ((static_cast<int64_t>(bg) * kPqM + m) * kKsub + z) * G;
+#pragma unroll
+        for (int hh = 0; hh < G; ++hh) {
+            float qs[kDsub];
+            Load8<T>::run(qg + hh * kHeadDim + m * kDsub, qs);
+#pragma unroll
+            for (int t = 0; t < kDsub; ++t) qs[t] *= D.inv_sqrt_d;
+            o[hh] = fine_entry(qs, p0, p1);
+        }
+        return;
+    }
+    // coarse table: 16 lanes per list, 8 dimensions per lane
+    const int c = part - kPqM / kFineWg;
+    const int lane16 = tid & 15;
+    const int group = tid >> 4;
+    float4 cv[kCoarsePer][2];
+#pragma unroll
+    for (int u = 0; u < kCoarsePer; ++u) {
+        const int j = c * kCoarseLists + group + u * kCoarseGroups;
+        const int jc = j < D.n_list ? j : D.n_list - 1;   // keep all lanes active
+        const float* cp = centroids + (static_cast<int64_t>(bg) * D.n_list + jc) * kHeadDim + lane16 * 8;
+        cv[u][0] = *reinterpret_cast<const float4*>(cp);
+        cv[u][1] = *reinterpret_cast<const float4*>(cp + 4);
+    }
+    float qc[G][8];
+#pragma unroll
+    for (int hh = 0; hh < G; ++hh) {
+        Load8<T>::run(qg + hh * kHeadDim + lane16 * 8, qc[hh]);
+#pragma unroll
+        for (int t = 0; t < 8; ++t) qc[hh][t] *= D.inv_sqrt_d;
+    }
+#pragma unroll
+    for (int u = 0; u < kCoarsePer; ++u) {
+        const int j = c * kCoarseLists + group + u * kCoarseGroups;
+        float mine = 0.0f;
+#pragma unroll
+        for (int hh = 0; hh < G; ++hh) {
+            const float acc = coarse_entry(qc[hh], cv[u][0], cv[u][1]);
+            if (lane16 == hh) mine = acc;
+        }
+        if (j < D.n_list && lane16 < G)
+            w.coarse[(static_cast<int64_t>(bg) * D.n_list + j) * G + lane16] = mine;
+    }
+}
+
+struct SampleLds {
+    float lut[kLutRow];          // the head's fine table [M][K]
+    int uniq[kMaxSamples];       // distinct list ids of the samples, in sample order
+    float cf[kMaxSamples];       // coarse term of each distinct list
+    int hist[kHistBins];
+    int prev_last[kProThreads];  // list id of each thread's last sample
+    SelectScratch ss;
+    BlockScratch bs;
+};
+
+template <typename T, int G>
+__device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, const Index& ix,
+                                            const T* __restrict__ q, const Work& w, float bias,
+                                            int row, SampleLds& sm) {
+    const int tid = threadIdx.x;
+    const int b = row / D.Hq;
+    const int h = row % D.Hq;
+    const int g = h / G;
+    const int bg = b * D.Hkv + g;
+    const int n_r = ba.n_r[b];
+    const int k = ba.topk[b];
+    const float neg_inf = -__builtin_huge_valf();
+    if (n_r == 0) {
+        if (tid == 0) w.tau_lo[row] = neg_inf;
+        return;
+    }
+    // runs of kSampleRun positions, rs apart (rs >= 1), clipped at the next run;
+    // thread tid owns samples 4 tid .. 4 tid + 3 (half a run)
+    const int nrun = min(kMaxSamples / kSampleRun, (n_r + kSampleRun - 1) / kSampleRun);
+    const int rs = n_r / nrun;
+    const int run_len = min(kSampleRun, rs);
+    const int64_t base = static_cast<int64_t>(bg) * D.rcap;
+    const uint4* codes = reinterpret_cast<const uint4*>(ix.codes) + base;
+    uint4 cv[kSamplesPer];
+    float rv[kSamplesPer];
+    int jv[kSamplesPer];
+    bool ok[kSamplesPer];
+#pragma unroll
+    for (int u = 0; u < kSamplesPer; ++u) {
+        const int s = tid * kSamplesPer + u;
+        const int run = s / kSampleRun;
+        const int within = s % kSampleRun;
+        const int pos = run * rs + within;
+        ok[u] = run < nrun && within < run_len && pos < n_r;
+        const int p = ok[u] ? pos : 0;
+        cv[u] = codes[p];
+        rv[u] = ix.norms[base + p];
+        jv[u] = ix.pos_list[base + p];
+    }
+    // this head's fine table: thread tid builds the entries (m, z) of subspace
+    // m = tid / 32 for z = tid % 32 + 32 i, so it needs one slice of q
+    const T* qh = q + static_cast<int64_t>(row) * kHeadDim;
+    const float* cbk = ix.codebooks + static_cast<int64_t>(bg) * kPqM * kKsub * kDsub;
+    constexpr int kZStride = kKsub / kFinePer;   // 32
+    const int m = tid / kZStride;
+    const int z0 = tid % kZStride;
+    float4 pv[kFinePer][2];
+#pragma unroll
+    for (int i = 0; i < kFinePer; ++i) {
+        const float* p = cbk + (m * kKsub + z0 + i * kZStride) * kDsub;
+        pv[i][0] = *reinterpret_cast<const float4*>(p);
+        pv[i][1] = *reinterpret_cast<const float4*>(p + 4);
+    }
+    float qs[kDsub];
+    Load8<T>::run(qh + m * kDsub, qs);
+    __builtin_amdgcn_sched_barrier(0);   // every load above is in flight before any use
+#pragma unroll
+    for (int t = 0; t < kDsub; ++t) qs[t] *= D.inv_sqrt_d;
+#pragma unroll
+    for (int i = 0; i < kFinePer; ++i)
+        sm.lut[m * kKsub + z0 + i * kZStride] = fine_entry(qs, pv[i][0], pv[i][1]);
+#pragma unroll
+    for (int u = 0; u < kSamplesPer; ++u) jv[u] = ok[u] ? jv[u] : -1;
+    sm.prev_last[tid] = jv[kSamplesPer - 1];
+    for (int i = tid; i < kHistBins; i += kProThreads) sm.hist[i] = 0;
+    __syncthreads();
+
+    // distinct lists of the (list-major, hence list-sorted) samples
+    int nf = 0;
+    bool first[kSamplesPer];
+#pragma unroll
+    for (int u = 0; u < kSamplesPer; ++u) {
+        const int prev = u > 0 ? jv[u - 1] : (tid > 0 ? sm.prev_last[tid - 1] : -1);
+        first[u] = jv[u] >= 0 && jv[u] != prev;
+        nf += first[u] ? 1 : 0;
+    }
+    int n_uniq = 0;
+    int idx = block_excl_scan<kProThreads>(nf, n_uniq, sm.ss) - 1;
+    int dv[kSamplesPer];
+#pragma unroll
+    for (int u = 0; u < kSamplesPer; ++u) {
+        if (first[u]) sm.uniq[++idx] = jv[u];
+        dv[u] = max(idx, 0);
+    }
+    __syncthreads();
+
+    // coarse terms of the distinct lists: 16 lanes per list
+    {
+        const int lane16 = tid & 15;
+        const int group = tid >> 4;
+        float qc[8];
+        Load8<T>::run(qh + lane16 * 8, qc);
+#pragma unroll
+        for (int t = 0; t < 8; ++t) qc[t] *= D.inv_sqrt_d;
+        const float* cen = ix.centroids + static_cast<int64_t>(bg) * D.n_list * kHeadDim + lane16 * 8;
+        // one batch of loads covers kSampleLists lists (the usual case)
+        for (int d0 = 0; d0 < n_uniq; d0 += kCoarseGroups * kSampleListsPer) {
+            float4 c4[kSampleListsPer][2];
+#pragma unroll
+            for (int u = 0; u < kSampleListsPer; ++u) {
+                const int d = min(d0 + group + u * kCoarseGroups, n_uniq - 1);
+                const float* cp = cen + static_cast<int64_t>(sm.uniq[d]) * kHeadDim;
+                c4[u][0] = *reinterpret_cast<const float4*>(cp);
+                c4[u][1] = *reinterpret_cast<const float4*>(cp + 4);
+            }
+#pragma unroll
+            for (int u = 0; u < kSampleListsPer; ++u) {
+                const int d = d0 + group + u * kCoarseGroups;
+                const float acc = coarse_entry(qc, c4[u][0], c4[u][1]);
+                if (lane16 == 0 && d < n_uniq) sm.cf[d] = acc;
+            }
+        }
+    }
+    __syncthreads();
+
+    // scores of the samples
+    float sc[kSamplesPer];
+    uint32_t mn = 0xffffffffu, mx = 0u, cnt = 0u;
+#pragma unroll
+    for (int u = 0; u < kSamplesPer; ++u) {
+        float fs[1];
+        fine_sum<1>(sm.lut, cv[u], fs);
+        sc[u] = pq_logit(rv[u], sm.cf[dv[u]], fs[0]);
+        if (ok[u]) {
+            const uint32_t kk = float_key(sc[u]);
+            mn = min(mn, kk);
+            mx = max(mx, kk);
+            ++cnt;
+        }
+    }
+    block_min_max_count<kProThreads>(mn, mx, cnt, sm.bs);
+    const int ns = static_cast<int>(cnt);
+    // order statistic: about 2k * ns / |R| sampled tokens above, plus a margin
+    const int c = (k == 0) ? 1 : static_cast<int>(ceilf(2.0f * k * ns / n_r)) + 8;
+    if (c > ns) {   // the budget is a large share of R: every token is a candidate
+        if (tid == 0) w.tau_lo[row] = neg_inf;
+        return;
+    }
+    // bins of equal width in score (monotone: rounded subtraction and
+    // multiplication by a positive constant never reorder two scores)
+    const float fmn = key_float(mn);
+    const float range = key_float(mx) - fmn;
+    const float scale = (range > 0.0f && range < __builtin_huge_valf()) ? kHistBins / range : 0.0f;
+    int bin[kSamplesPer];
+#pragma unroll
+    for (int u = 0; u < kSamplesPer; ++u) {
+        bin[u] = min(static_cast<int>((sc[u] - fmn) * scale), kHistBins - 1);
+        hist_add(sm.hist, static_cast<uint32_t>(ok[u] ? bin[u] : 0), ok[u]);
+    }
+    __syncthreads();
+    int above = 0;
+    const int bstar = block_find_bin_desc<kProThreads>(sm.hist, c, above, sm.ss, sm.bs);
+    // the smallest sample of the boundary bin: at least c samples are >= it
+    uint32_t lo = 0xffffffffu, dmx = 0u, dcnt = 0u;
+#pragma unroll
+    for (int u = 0; u < kSamplesPer; ++u)
+        if (ok[u] && bin[u] == bstar) lo = min(lo, float_key(sc[u]));
+    block_min_max_count<kProThreads>(lo, dmx, dcnt, sm.bs);
+    if (tid == 0) w.tau_lo[row] = key_float(lo) + bias;
+}
+
+template <typename T, int G>
+__global__ __launch_bounds__(kProThreads) __attribute__((amdgpu_waves_per_eu(1, 2))) void prologue_kernel(Dims D, BatchArgs ba, Index ix,
+                                                               const T* __restrict__ q, Work w,
+                                                               float bias, int n_lut_wg) {
+    __shared__ SampleLds sm;
+    const int n_coarse = (D.n_list + kCoarseLists - 1) / kCoarseLists;
+    const int per_bg = kPqM / kFineWg + n_coarse;
+    if (static_cast<int>(blockIdx.x) < n_lut_wg) {
+        lut_role<T, G>(D, q, ix.codebooks, ix.centroids, w, blockIdx.x / per_bg,
+                       blockIdx.x % per_bg);
+        return;
+    }
+    sample_role<T, G>(D, ba, ix, q, w, bias, blockIdx.x - n_lut_wg, sm);
+}
+
+template <typename T, int G>
+static hipError_t launch_prologue_t(const Dims& D, const BatchArgs& ba, const KV& kv,
+                                    const Index& ix, const Work& w, float bias, hipStream_t s) {
+    const int n_coarse = (D.n_list + kCoarseLists - 1) / kCoarseLists;
+    const int n_lut_wg = D.B * D.Hkv * (kPqM / kFineWg + n_coarse);
+    const int grid = n_lut_wg + D.B * D.Hq;
+    hipLaunchKernelGGL((prologue_kernel<T, G>), dim3(grid), dim3(kProThreads), 0, s, D, ba, ix,
+                       static_cast<const T*>(kv.q), w, bias, n_lut_wg);
+    return hipGetLastError();
+}
+
+template <typename T>
+static hipError_t launch_prologue_g(const Dims& D, const BatchArgs& ba, const KV& kv,
+                                    const Index& ix, const Work& w, float bias, hipStream_t s) {
+    switch (D.G) {
+        case 1: return launch_prologue_t<T, 1>(D, ba, kv, ix, w, bias, s);
+        case 2: return launch_prologue_t<T, 2>(D, ba, kv, ix, w, bias, s);
+        case 4: return launch_prologue_t<T, 4>(D, ba, kv, ix, w, bias, s);
+        case 8: return launch_prologue_t<T, 8>(D, ba, kv, ix, w, bias, s);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_prologue(const Dims& D, const BatchArgs& ba, const KV& kv, const Index& ix,
+                           const Work& w, float bias, hipStream_t s) {
+    return kv.bf16 ? launch_prologue_g<bf16_t>(D, ba, kv, ix, w, bias, s)
+                   : launch_prologue_g<float>(D, ba, kv, ix, w, bias, s);
+}
+
+}  // namespace pqhsa

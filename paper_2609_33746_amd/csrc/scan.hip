@@ -5,10 +5,14 @@
 // Work decomposition: the list-major positions of each (batch element, KV
 // head) are cut into sub-chunks of kSub positions; one wave owns one
 // sub-chunk, and a workgroup holds kScanWaves consecutive sub-chunks of the
-// same KV head so that they share one copy of the group LUT in LDS. Each wave
-// keeps the metadata of the lists it walks (start offsets, first segment,
-// coarse terms) in a 64-lane register window, so the inner loop issues no
-// dependent global loads.
+// same KV head so that they share one copy of the group LUT in LDS. Every
+// batch element gets the workgroup count of the longest R_b; the surplus
+// workgroups of shorter sequences exit at once.
+//
+// Every load of a wave is issued before its arithmetic starts: each lane's
+// list ids, codes and norms, the group LUT (staged through registers into
+// LDS) and, once the list ids have arrived, the coarse terms of the lanes'
+// lists, so a wave waits for about two memory round trips in all.
 //
 // Per token and head the wave computes l~ and then either
 //   * emits (l~, list id and position) as a top-k candidate when
@@ -19,45 +23,44 @@
 // Tokens below tau_lo can never be in the top-k (tau_lo <= the k-th largest
 // score whenever at least k candidates exist), so these masses are exactly
 // the "below threshold" part of M_j in Eq. 4; the unselected candidates are
-// added by the top-k stage. Masses are written per (list, sub-chunk)
-// segment, so no atomics are used and the result does not depend on
-// scheduling.
+// added by the top-k stage.
+//
+// Masses are stored per (list j, sub-chunk s) pair at segment j + s of the KV
+// head's segment array: along the list-major order neither j nor s decreases
+// and each new pair increases at least one of them, so distinct pairs get
+// distinct segments (some segment indices stay unused). No atomics are used
+// and the result does not depend on scheduling.
 #include "device_common.h"
 #include "pq_score.h"
 #include "pqhsa_internal.h"
 
 namespace pqhsa {
 
-// Metadata of lists [base, base + 63) held one list per lane; lane l also
-// holds the start of list base + l, so list base + i spans
-// [start(i), start(i + 1)).
-template <int G>
-struct ListWindow {
-    int base;
-    int start;
-    int seg;
-    float cf[G];
+constexpr int kScanThreads = kScanWaves * kWave;
+constexpr int kIters = kSub / kWave;   // 64-position steps per sub-chunk
 
-    __device__ __forceinline__ void load(const int32_t* loff, const int32_t* seg0,
-                                         const float* coarse, int n_list, int first) {
-        base = first;
-        const int j = first + lane_id();
-        start = j <= n_list ? loff[j] : 0x7fffffff;
-        seg = j < n_list ? seg0[j] : 0;
-#pragma unroll
-        for (int hh = 0; hh < G; ++hh) cf[hh] = j < n_list ? coarse[j * G + hh] : 0.0f;
-    }
-    __device__ __forceinline__ int start_of(int i) const { return __builtin_amdgcn_readlane(start, i); }
-    __device__ __forceinline__ int seg_of(int i) const { return __builtin_amdgcn_readlane(seg, i); }
-    __device__ __forceinline__ float cf_of(int hh, int i) const {
-        return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(cf[hh]), i));
-    }
-};
-constexpr int kWindowLists = kWave - 1;
-
+// The G coarse terms of one list, [n_list][G] layout.
 template <int G>
-__device__ __forceinline__ void flush_segment(const Dims& D, const Work& w, int bg, int seg,
-                                              float (&acc)[G]) {
+__device__ __forceinline__ void load_coarse(const float* p, float (&v)[G]) {
+    if constexpr (G == 8) {
+        const float4 a = reinterpret_cast<const float4*>(p)[0];
+        const float4 c = reinterpret_cast<const float4*>(p)[1];
+        v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+        v[4] = c.x; v[5] = c.y; v[6] = c.z; v[7] = c.w;
+    } else if constexpr (G == 4) {
+        const float4 a = *reinterpret_cast<const float4*>(p);
+        v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+    } else if constexpr (G == 2) {
+        const float2 a = *reinterpret_cast<const float2*>(p);
+        v[0] = a.x; v[1] = a.y;
+    } else {
+        v[0] = *p;
+    }
+}
+
+// Store the wave's masses of one list segment and clear them.
+template <int G>
+__device__ __forceinline__ void flush_segment(float* seg_row, float (&acc)[G]) {
     float mine = 0.0f;
 #pragma unroll
     for (int hh = 0; hh < G; ++hh) {
@@ -65,62 +68,68 @@ __device__ __forceinline__ void flush_segment(const Dims& D, const Work& w, int 
         if (lane_id() == hh) mine = tot;
         acc[hh] = 0.0f;
     }
-    if (lane_id() < G) w.seg_sum[(static_cast<int64_t>(bg) * D.nseg_cap + seg) * G + lane_id()] = mine;
+    if (lane_id() < G) seg_row[lane_id()] = mine;
 }
 
 template <int G>
-__global__ __launch_bounds__(kScanWaves * kWave) void scan_kernel(Dims D, Index ix, Work w,
-                                                                  const ScanWG* __restrict__ table) {
+__global__ __launch_bounds__(kScanThreads) void scan_kernel(Dims D, BatchArgs ba, Index ix, Work w,
+                                                            int nwg) {
     extern __shared__ float lut_s[];   // [M][K][G]
-    const ScanWG& entry = table[blockIdx.x];
-    const int bg = entry.bg;
+    const int bg = blockIdx.x / nwg;
     const int b = bg / D.Hkv;
     const int g = bg % D.Hkv;
+    const int n_r = ba.n_r[b];
+    const int sc0 = (blockIdx.x % nwg) * kScanWaves;
+    if (sc0 * kSub >= n_r) return;   // surplus workgroup of a shorter sequence
 
-    const int n_r = ix.n_r[b];
-    const int wave = threadIdx.x / kWave;
+    const int tid = threadIdx.x;
+    const int wave = tid / kWave;
     const int lane = lane_id();
-    const int sc = entry.sub0 + wave;
-    const bool active = sc * kSub < n_r;
+    const int sc = sc0 + wave;
     const int p_begin = sc * kSub;
     const int p_end = min(p_begin + kSub, n_r);
+    const bool active = p_begin < n_r;
     const int64_t base = static_cast<int64_t>(bg) * D.rcap;
-    const uint4* codes = reinterpret_cast<const uint4*>(ix.codes) + base;
-    const int32_t* loff = ix.loff + static_cast<int64_t>(bg) * (D.n_list + 1);
-    const int32_t* seg0 = ix.seg0 + static_cast<int64_t>(bg) * (D.n_list + 1);
-    const float* coarse = w.coarse + static_cast<int64_t>(bg) * D.n_list * G;
     const int row0 = b * D.Hq + g * G;
 
-    // issue this wave's code, norm and list-metadata loads before staging the LUT
-    constexpr int kIters = kSub / kWave;
-    uint4 c_pre[kIters];
-    float r_pre[kIters];
+    // 1) list ids (addresses clamped into R_b: every load is in bounds)
+    int jl[kIters];
 #pragma unroll
-    for (int it = 0; it < kIters; ++it) {
-        const int p = p_begin + it * kWave + lane;
-        c_pre[it] = make_uint4(0u, 0u, 0u, 0u);
-        r_pre[it] = 0.0f;
-        if (active && p < p_end) {
-            c_pre[it] = codes[p];
-            r_pre[it] = ix.norms[base + p];
-        }
-    }
-    ListWindow<G> win;
-    win.load(loff, seg0, coarse, D.n_list, active ? entry.list0[wave] : 0);
+    for (int it = 0; it < kIters; ++it)
+        jl[it] = ix.pos_list[base + min(p_begin + it * kWave + lane, n_r - 1)];
+    // 2) the group LUT and the thresholds
+    constexpr int kStage = kLutRow * G / 4 / kScanThreads;
+    static_assert(kStage * kScanThreads * 4 == kLutRow * G, "LUT staging tiling");
+    const float4* lsrc = reinterpret_cast<const float4*>(w.lut + static_cast<int64_t>(bg) * kLutRow * G);
+    float4 st[kStage];
+#pragma unroll
+    for (int i = 0; i < kStage; ++i) st[i] = lsrc[i * kScanThreads + tid];
     float tlo[G];
 #pragma unroll
     for (int hh = 0; hh < G; ++hh) tlo[hh] = w.tau_lo[row0 + hh];
-    {
-        const float4* src = reinterpret_cast<const float4*>(w.lut + static_cast<int64_t>(bg) * kLutRow * G);
-        float4* dst = reinterpret_cast<float4*>(lut_s);
-        for (int i = threadIdx.x; i < kLutRow * G / 4; i += kScanWaves * kWave) dst[i] = src[i];
+    // 3) codes and norms
+    const uint4* codes = reinterpret_cast<const uint4*>(ix.codes) + base;
+    uint4 cv[kIters];
+    float rv[kIters];
+#pragma unroll
+    for (int it = 0; it < kIters; ++it) {
+        const int p = min(p_begin + it * kWave + lane, n_r - 1);
+        cv[it] = codes[p];
+        rv[it] = ix.norms[base + p];
     }
+    // 4) coarse terms of the lanes' lists
+    const float* coarse = w.coarse + static_cast<int64_t>(bg) * D.n_list * G;
+    float cf[kIters][G];
+#pragma unroll
+    for (int it = 0; it < kIters; ++it) load_coarse<G>(coarse + jl[it] * G, cf[it]);
+    float4* ldst = reinterpret_cast<float4*>(lut_s);
+#pragma unroll
+    for (int i = 0; i < kStage; ++i) ldst[i * kScanThreads + tid] = st[i];
     __syncthreads();
     if (!active) return;
 
-    int ci = 0;   // window index of the current list
-    int cur_start = win.start_of(0);
-    int cur_end = win.start_of(1);
+    float* segs = w.seg_sum + (static_cast<int64_t>(bg) * D.nseg_cap + sc) * G;   // + j * G
+    int cur = __builtin_amdgcn_readfirstlane(jl[0]);   // list of the open segment
     float acc[G];
     int cbase[G];
 #pragma unroll
@@ -129,57 +138,51 @@ __global__ __launch_bounds__(kScanWaves * kWave) void scan_kernel(Dims D, Index 
 #pragma unroll
     for (int it = 0; it < kIters; ++it) {
         const int p_first = p_begin + it * kWave;
-        if (p_first >= p_end) break;
+        if (p_first >= p_end) continue;   // uniform: past the end of a short last sub-chunk
         const int p = p_first + lane;
         const bool valid = p < p_end;
-        const int p_last = min(p_first + kWave - 1, p_end - 1);
         float fs[G];
-        fine_sum<G>(lut_s, c_pre[it], fs);
-        const float r = r_pre[it];
-        float s[G];
+        fine_sum<G>(lut_s, cv[it], fs);
+        float s[G], e[G];
 #pragma unroll
-        for (int hh = 0; hh < G; ++hh) s[hh] = 0.0f;
-        int my_list = 0;
-
-        // walk the lists that cover [p_first, p_last] (wave-uniform)
-        while (true) {
-            const bool in = valid && p >= cur_start && p < cur_end;
-            if (in) my_list = win.base + ci;
-#pragma unroll
-            for (int hh = 0; hh < G; ++hh) {
-                const float sc_h = pq_logit(r, win.cf_of(hh, ci), fs[hh]);
-                if (in) s[hh] = sc_h;
-                acc[hh] += (in && sc_h < tlo[hh]) ? __expf(sc_h - tlo[hh]) : 0.0f;
-            }
-            if (cur_end > p_last) break;
-            flush_segment<G>(D, w, bg, win.seg_of(ci) + (sc - cur_start / kSub), acc);
-            do {
-                ++ci;
-                if (ci == kWindowLists) {
-                    win.load(loff, seg0, coarse, D.n_list, win.base + kWindowLists);
-                    ci = 0;
-                }
-                cur_start = cur_end;
-                cur_end = win.start_of(ci + 1);
-            } while (cur_end == cur_start);
+        for (int hh = 0; hh < G; ++hh) {
+            s[hh] = pq_logit(rv[it], cf[it][hh], fs[hh]);
+            e[hh] = (valid && s[hh] < tlo[hh]) ? __expf(s[hh] - tlo[hh]) : 0.0f;
         }
-
+        // close the lists that end inside this step (lists are contiguous and
+        // ascending along the lanes)
+        const int j = jl[it];
+        const int j_last = __builtin_amdgcn_readlane(j, min(p_end - p_first, kWave) - 1);
+        while (cur != j_last) {
+            const bool in = valid && j == cur;
+#pragma unroll
+            for (int hh = 0; hh < G; ++hh) acc[hh] += in ? e[hh] : 0.0f;
+            flush_segment<G>(segs + cur * G, acc);
+            const int nxt = __popcll(__ballot(valid && j <= cur));
+            cur = __builtin_amdgcn_readlane(j, nxt);
+        }
+        {
+            const bool in = valid && j == cur;
+#pragma unroll
+            for (int hh = 0; hh < G; ++hh) acc[hh] += in ? e[hh] : 0.0f;
+        }
         // candidates >= tau_lo, compacted in position order
 #pragma unroll
         for (int hh = 0; hh < G; ++hh) {
-            const bool pred = valid && s[hh] >= tlo[hh];
-            const uint64_t mask = __ballot(pred);
-            if (pred) {
-                const int64_t o = static_cast<int64_t>(row0 + hh) * D.rcap + p_begin + cbase[hh] +
-                                  lanes_below(mask);
-                w.cand_score[o] = s[hh];
-                w.cand_pos[o] = static_cast<int32_t>((static_cast<uint32_t>(my_list) << kPosBits) |
-                                                     static_cast<uint32_t>(p));
+            const uint64_t mask = __ballot(valid && s[hh] >= tlo[hh]);
+            if (mask) {
+                if ((mask >> lane) & 1ull) {
+                    const int64_t o = static_cast<int64_t>(row0 + hh) * D.rcap + p_begin +
+                                      cbase[hh] + lanes_below(mask);
+                    w.cand[o] = make_uint2(__float_as_uint(s[hh]),
+                                           (static_cast<uint32_t>(j) << kPosBits) |
+                                               static_cast<uint32_t>(p));
+                }
+                cbase[hh] += __popcll(mask);
             }
-            cbase[hh] += __popcll(mask);
         }
     }
-    flush_segment<G>(D, w, bg, win.seg_of(ci) + (sc - cur_start / kSub), acc);
+    flush_segment<G>(segs + cur * G, acc);
     int mine = 0;
 #pragma unroll
     for (int hh = 0; hh < G; ++hh)
@@ -188,11 +191,11 @@ __global__ __launch_bounds__(kScanWaves * kWave) void scan_kernel(Dims D, Index 
 }
 
 template <int G>
-static hipError_t launch_scan_t(const Dims& D, const Index& ix, const Work& w, const ScanWG* table,
-                                int n_wg, hipStream_t s) {
+static hipError_t launch_scan_t(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w,
+                                int nwg, hipStream_t s) {
     const size_t lds = static_cast<size_t>(kLutRow) * G * sizeof(float);
-    hipLaunchKernelGGL((scan_kernel<G>), dim3(n_wg), dim3(kScanWaves * kWave), lds, s, D, ix, w,
-                       table);
+    hipLaunchKernelGGL((scan_kernel<G>), dim3(D.B * D.Hkv * nwg), dim3(kScanThreads), lds, s, D,
+                       ba, ix, w, nwg);
     return hipGetLastError();
 }
 
@@ -203,14 +206,14 @@ hipError_t configure_scan() {
                                static_cast<int>(kLutRow * 8 * sizeof(float)));
 }
 
-hipError_t launch_scan(const Dims& D, const Index& ix, const Work& w, const ScanWG* table, int n_wg,
+hipError_t launch_scan(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w, int nwg,
                        hipStream_t s) {
-    if (n_wg == 0) return hipSuccess;
+    if (nwg == 0) return hipSuccess;
     switch (D.G) {
-        case 1: return launch_scan_t<1>(D, ix, w, table, n_wg, s);
-        case 2: return launch_scan_t<2>(D, ix, w, table, n_wg, s);
-        case 4: return launch_scan_t<4>(D, ix, w, table, n_wg, s);
-        case 8: return launch_scan_t<8>(D, ix, w, table, n_wg, s);
+        case 1: return launch_scan_t<1>(D, ba, ix, w, nwg, s);
+        case 2: return launch_scan_t<2>(D, ba, ix, w, nwg, s);
+        case 4: return launch_scan_t<4>(D, ba, ix, w, nwg, s);
+        case 8: return launch_scan_t<8>(D, ba, ix, w, nwg, s);
         default: return hipErrorInvalidValue;
     }
 }

@@ -2,29 +2,22 @@
 // largest approximate logits, per (batch element, query head) row, ties to the
 // smaller token id.
 //
-// Two kernels:
-//  * sample_kernel (before the scan): scores a list-stratified sample of the
-//    row's list-major positions (contiguous runs of kSampleRun positions,
-//    evenly spread) and takes a sample order statistic as the candidate
-//    threshold tau_lo, chosen so that about twice k tokens of the full row
-//    score at or above it. Any threshold gives the same final result; it only
-//    decides how many candidates the scan emits.
-//  * select_kernel (after the scan): gathers the candidates of the row (in
-//    list-major position order) into LDS, locates the k-th largest score with
-//    one histogram pass over monotone bins of the order keys, ranks the few
-//    candidates of the boundary bin exactly (score, then token id), writes T,
-//    and sums exp(l~ - shift) of the unselected candidates per list (in
-//    64-bit fixed point, so the sums do not depend on the order of the
-//    atomic additions). If the threshold left fewer than k candidates (or none
-//    at all), the row is re-scanned in full from the LUT and every indexed
-//    token becomes a candidate; the below-threshold masses of the scan are
-//    then ignored for that row. Rows with more candidates than the LDS holds,
-//    or a very dense boundary bin, use a radix select instead. Every path
-//    gives the exact top-k.
+// One workgroup per row gathers the row's candidates (the tokens the scan
+// found at or above the sampled threshold tau_lo, in list-major position
+// order) into LDS, locates the k-th largest score with one histogram pass
+// over monotone bins of the order keys, ranks the few candidates of the
+// boundary bin exactly (score, then token id), writes T, and sums
+// exp(l~ - shift) of the unselected candidates per list (in 64-bit fixed
+// point, so the sums do not depend on the order of the atomic additions).
+// If the threshold left fewer than k candidates (or none at all), the row is
+// re-scanned in full from the LUT and every indexed token becomes a
+// candidate; the below-threshold masses of the scan are then ignored for that
+// row. Rows with more candidates than the LDS holds, or a very dense boundary
+// bin, use a radix select instead. Every path gives the exact top-k.
 //
-// Both kernels keep their dependency chains short: each wave loads the
-// counts of its own sub-chunks and scans them with DPP, candidate loads are
-// issued in batches, and every workgroup-wide step is one scan or reduction.
+// Each wave loads the counts of its own sub-chunks and scans them with DPP,
+// candidate loads are issued in batches, and every workgroup-wide step is one
+// scan or reduction, so the dependency chain stays short.
 #include "device_common.h"
 #include "hist_select.h"
 #include "pq_score.h"
@@ -34,29 +27,32 @@
 namespace pqhsa {
 
 constexpr int kNW = kSelThreads / kWave;
-constexpr int kSampleUnroll = kMaxSamples / kSelThreads;   // samples per thread
 constexpr int kRankCap = 512;          // boundary-bin keys ranked exactly
-constexpr int kLoadBatch = 16;         // sub-chunks whose candidates a wave loads at once
+constexpr int kCopyPer = 4;            // candidates a thread loads at once
 constexpr uint32_t kPosMask = (1u << kPosBits) - 1u;
 constexpr float kMassScale = 1099511627776.0f;       // 2^40: fixed-point weights
 constexpr float kMassUnscale = 1.0f / 1099511627776.0f;
 
-// Rank the keys of one histogram bin exactly: key desc, then token id asc
-// (tok_at is read only when two keys of the bin are equal). Marks the `need`
-// largest in the `chosen` bitmap (if given) and returns the smallest chosen
-// key. Returns false without marking anything when the bin holds more than
-// kRankCap keys. Must be called by the whole workgroup.
-template <typename KeyAt, typename ValidAt, typename TokAt>
-__device__ __forceinline__ bool rank_boundary_bin(KeyAt key_at, ValidAt valid_at, TokAt tok_at,
-                                                  int n, uint32_t kmin, int sh, int bin, int m,
-                                                  int need, uint32_t* r_key, int* r_idx,
-                                                  int* r_tok, int* counter, uint32_t* chosen,
-                                                  uint32_t& kth, BlockScratch& bs) {
+// Rank the keys of one histogram bin exactly: key desc, then token id asc.
+// The bin's keys are gathered into r_key / r_idx, then each wave ranks some of
+// them against all the others with one ballot per 64 keys; token ids
+// (tok_at) are read only when two keys of the bin are equal. Marks the `need`
+// largest in the `chosen` bitmap and returns the need-th largest key in kth.
+// Returns false without marking anything when the bin holds more than
+// kRankCap keys. Must be called by the whole workgroup; flags[0] must be 0.
+template <typename KeyAt, typename TokAt>
+__device__ __forceinline__ bool rank_boundary_bin(KeyAt key_at, TokAt tok_at, int n, uint32_t kmin,
+                                                  int sh, int bin, int m, int need, uint32_t* r_key,
+                                                  int* r_idx, int* r_tok, int* counter, int* flags,
+                                                  uint32_t* chosen, uint32_t& kth,
+                                                  BlockScratch& bs) {
     if (m > kRankCap) return false;
     const int tid = threadIdx.x;
+    const int wave = tid / kWave;
+    const int lane = lane_id();
     for (int i0 = 0; i0 < n; i0 += kSelThreads) {
         const int i = i0 + tid;
-        if (i < n && valid_at(i)) {
+        if (i < n) {
             const uint32_t kk = key_at(i);
             if (static_cast<int>((kk - kmin) >> sh) == bin) {
                 const int slot = atomicAdd(counter, 1);
@@ -66,144 +62,60 @@ __device__ __forceinline__ bool rank_boundary_bin(KeyAt key_at, ValidAt valid_at
         }
     }
     __syncthreads();
-    int dup = 0;
-    if (tid < m) {
-        const uint32_t mk = r_key[tid];
-        for (int j = 0; j < m; ++j) dup |= (j != tid && r_key[j] == mk) ? 1 : 0;
-    }
-    const bool ties = __syncthreads_or(dup) != 0;
-    if (ties && tid < m) r_tok[tid] = tok_at(r_idx[tid]);
-    __syncthreads();
-    uint32_t mine = 0xffffffffu;
-    if (tid < m) {
-        const uint32_t mk = r_key[tid];
-        const int mt = ties ? r_tok[tid] : 0;
+    // pass 1: rank by key alone, and look for equal keys
+    for (int i = wave; i < m; i += kNW) {
+        const uint32_t ki = r_key[i];
         int rank = 0;
-        for (int j = 0; j < m; ++j) {
-            const uint32_t ok = r_key[j];
-            rank += (ok > mk || (ties && ok == mk && r_tok[j] < mt)) ? 1 : 0;
+        bool dup = false;
+        for (int j0 = 0; j0 < m; j0 += kWave) {
+            const int j = j0 + lane;
+            const uint32_t kj = j < m ? r_key[j] : 0u;
+            rank += __popcll(__ballot(j < m && kj > ki));
+            dup |= __ballot(j < m && j != i && kj == ki) != 0ull;
         }
-        if (rank < need) {
-            const int idx = r_idx[tid];
-            if (chosen) atomicOr(&chosen[idx >> 5], 1u << (idx & 31));
-            mine = mk;
+        if (dup) {
+            if (lane == 0) flags[0] = 1;
+        } else if (lane == 0 && rank < need) {
+            const int idx = r_idx[i];
+            atomicOr(&chosen[idx >> 5], 1u << (idx & 31));
+            if (rank == need - 1) bs.bcast[2] = static_cast<int>(ki);
         }
     }
-    uint32_t dmx = 0u, dcnt = 0u;
-    block_min_max_count<kSelThreads>(mine, dmx, dcnt, bs);
-    kth = mine;
+    __syncthreads();
+    if (flags[0]) {
+        // equal keys in the bin: rank again with the token ids
+        if (tid < m) r_tok[tid] = tok_at(r_idx[tid]);
+        __syncthreads();
+        for (int i = wave; i < m; i += kNW) {
+            const uint32_t ki = r_key[i];
+            const int ti = r_tok[i];
+            int rank = 0;
+            bool dup = false;
+            for (int j0 = 0; j0 < m; j0 += kWave) {
+                const int j = j0 + lane;
+                const uint32_t kj = j < m ? r_key[j] : 0u;
+                const int tj = j < m ? r_tok[j] : 0;
+                rank += __popcll(__ballot(j < m && (kj > ki || (kj == ki && tj < ti))));
+                dup |= __ballot(j < m && j != i && kj == ki) != 0ull;
+            }
+            // keys that had no equal were marked by pass 1 already
+            if (dup && lane == 0 && rank < need) {
+                const int idx = r_idx[i];
+                atomicOr(&chosen[idx >> 5], 1u << (idx & 31));
+            }
+            if (lane == 0 && rank == need - 1) bs.bcast[2] = static_cast<int>(ki);
+        }
+        __syncthreads();
+    }
+    kth = static_cast<uint32_t>(bs.bcast[2]);
+    __syncthreads();
     return true;
-}
-
-__global__ __launch_bounds__(kSelThreads) void sample_kernel(Dims D, BatchInts tk, Index ix,
-                                                             Work w, float bias) {
-    __shared__ float lut_s[kLutRow];
-    __shared__ uint32_t keys[kMaxSamples];
-    __shared__ int hist[kHistBins];
-    __shared__ uint32_t r_key[kRankCap];
-    __shared__ int r_idx[kRankCap];
-    __shared__ int r_tok[kRankCap];
-    __shared__ int counter[1];
-    __shared__ SelectScratch ss;
-    __shared__ BlockScratch bs;
-    const int tid = threadIdx.x;
-    const int row = blockIdx.x;
-    const int b = row / D.Hq;
-    const int h = row % D.Hq;
-    const int g = h / D.G;
-    const int hh = h % D.G;
-    const int bg = b * D.Hkv + g;
-    const int n_r = ix.n_r[b];
-    const int k = tk.v[b];
-    const float neg_inf = -__builtin_huge_valf();
-    if (n_r == 0) {
-        if (tid == 0) w.tau_lo[row] = neg_inf;
-        return;
-    }
-    // runs of kSampleRun positions, rs apart (rs >= 1), clipped at the next run
-    const int nrun = min(kMaxSamples / kSampleRun, (n_r + kSampleRun - 1) / kSampleRun);
-    const int rs = n_r / nrun;
-    const int run_len = min(kSampleRun, rs);
-    const int64_t base = static_cast<int64_t>(bg) * D.rcap;
-    const uint4* codes = reinterpret_cast<const uint4*>(ix.codes) + base;
-    uint4 cv[kSampleUnroll];
-    float rv[kSampleUnroll];
-    int jv[kSampleUnroll];
-    bool ok[kSampleUnroll];
-#pragma unroll
-    for (int u = 0; u < kSampleUnroll; ++u) {
-        const int s = u * kSelThreads + tid;
-        const int run = s / kSampleRun;
-        const int pos = run * rs + s % kSampleRun;
-        ok[u] = run < nrun && s % kSampleRun < run_len && pos < n_r;
-        const int p = ok[u] ? pos : 0;
-        cv[u] = codes[p];
-        rv[u] = ix.norms[base + p];
-        jv[u] = ix.pos_list[base + p];
-    }
-    const float* coarse = w.coarse + static_cast<int64_t>(bg) * D.n_list * D.G;
-    float cf[kSampleUnroll];
-#pragma unroll
-    for (int u = 0; u < kSampleUnroll; ++u) cf[u] = coarse[jv[u] * D.G + hh];
-    stage_head_lut<kSelThreads>(lut_s, w.lut + static_cast<int64_t>(bg) * kLutRow * D.G, D.G, hh);
-    for (int i = tid; i < kHistBins; i += kSelThreads) hist[i] = 0;
-    if (tid == 0) counter[0] = 0;
-    __syncthreads();
-    uint32_t mn = 0xffffffffu, mx = 0u, cnt = 0u;
-#pragma unroll
-    for (int u = 0; u < kSampleUnroll; ++u) {
-        float fs[1];
-        fine_sum<1>(lut_s, cv[u], fs);
-        const uint32_t kk = float_key(pq_logit(rv[u], cf[u], fs[0]));
-        keys[u * kSelThreads + tid] = kk;
-        if (ok[u]) {
-            mn = min(mn, kk);
-            mx = max(mx, kk);
-            ++cnt;
-        }
-    }
-    block_min_max_count<kSelThreads>(mn, mx, cnt, bs);
-    const int ns = static_cast<int>(cnt);
-    // order statistic: about 2k * ns / |R| sampled tokens above, plus a margin
-    const int c = (k == 0) ? 1 : static_cast<int>(ceilf(2.0f * k * ns / n_r)) + 8;
-    if (c > ns) {   // the budget is a large share of R: every token is a candidate
-        if (tid == 0) w.tau_lo[row] = neg_inf;
-        return;
-    }
-    const int sh = bin_shift(mn, mx);
-#pragma unroll
-    for (int u = 0; u < kSampleUnroll; ++u)
-        hist_add(hist, (keys[u * kSelThreads + tid] - mn) >> sh, ok[u]);
-    __syncthreads();
-    int above = 0;
-    const int bin = block_find_bin_desc<kSelThreads>(hist, c, above, ss, bs);
-    uint32_t tau_key = 0u;
-    auto valid_at = [&](int i) {
-        const int run = i / kSampleRun;
-        return run < nrun && i % kSampleRun < run_len && run * rs + i % kSampleRun < n_r;
-    };
-    const bool exact = rank_boundary_bin([&](int i) { return keys[i]; }, valid_at,
-                                         [](int i) { return i; }, kMaxSamples, mn, sh, bin,
-                                         hist[bin], c - above, r_key, r_idx, r_tok, counter,
-                                         nullptr, tau_key, bs);
-    if (!exact) {
-        // very dense bin: its smallest key (<= the c-th largest)
-        uint32_t lo = 0xffffffffu, dmx = 0u, dcnt = 0u;
-#pragma unroll
-        for (int u = 0; u < kSampleUnroll; ++u) {
-            const uint32_t kk = keys[u * kSelThreads + tid];
-            if (ok[u] && static_cast<int>((kk - mn) >> sh) == bin) lo = min(lo, kk);
-        }
-        block_min_max_count<kSelThreads>(lo, dmx, dcnt, bs);
-        tau_key = lo;
-    }
-    if (tid == 0) w.tau_lo[row] = key_float(tau_key) + bias;
 }
 
 // LDS layout of select_kernel (dynamic, 4-byte words):
 //   keys [kSelCap] | cand [kSelCap] | mass (uint64) [kMaxLists] | hist [kHistBins] |
 //   rank_key [kRankCap] | rank_idx [kRankCap] | rank_tok [kRankCap] |
-//   chosen bitmap [kSelCap / 32] | counter [4]
+//   chosen bitmap [kSelCap / 32] | counter, flags [4] | sub-chunk offsets [kSelMaxSub]
 constexpr int kOffCand = kSelCap;
 constexpr int kOffMass = 2 * kSelCap;   // 8-byte aligned
 constexpr int kOffHist = kOffMass + 2 * kMaxLists;
@@ -212,7 +124,8 @@ constexpr int kOffRIdx = kOffRKey + kRankCap;
 constexpr int kOffRTok = kOffRIdx + kRankCap;
 constexpr int kOffBits = kOffRTok + kRankCap;
 constexpr int kOffCounter = kOffBits + kSelCap / 32;
-constexpr size_t kSelLdsWords = kOffCounter + 4;
+constexpr int kOffPre = kOffCounter + 4;
+constexpr size_t kSelLdsWords = kOffPre + kSelMaxSub;
 constexpr size_t kSelLdsBytes = kSelLdsWords * 4;
 
 // Emit T in candidate order (each thread owns a contiguous range of candidate
@@ -256,7 +169,7 @@ __device__ __forceinline__ void emit_selection(KeyAt key_at, CandAt cand_at, IsS
         cand_mass[j] = static_cast<float>(mass[j]) * kMassUnscale;
 }
 
-__global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchInts tk, Index ix,
+__global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchArgs ba, Index ix,
                                                              Work w, int force_fallback) {
     extern __shared__ uint32_t lds[];
     unsigned long long* mass = reinterpret_cast<unsigned long long*>(lds + kOffMass);
@@ -266,6 +179,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchInts t
     int* r_tok = reinterpret_cast<int*>(lds + kOffRTok);
     uint32_t* chosen = lds + kOffBits;
     int* counter = reinterpret_cast<int*>(lds + kOffCounter);
+    int* pre = reinterpret_cast<int*>(lds + kOffPre);
     __shared__ SelectScratch ss;
     __shared__ BlockScratch bs;
     const int tid = threadIdx.x;
@@ -277,8 +191,8 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchInts t
     const int g = h / D.G;
     const int hh = h % D.G;
     const int bg = b * D.Hkv + g;
-    const int n_r = ix.n_r[b];
-    const int k = tk.v[b];
+    const int n_r = ba.n_r[b];
+    const int k = ba.topk[b];
     const int nsub = (n_r + kSub - 1) / kSub;
     const int64_t rbase = static_cast<int64_t>(row) * D.rcap;
     const int64_t base = static_cast<int64_t>(bg) * D.rcap;
@@ -290,7 +204,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchInts t
     for (int j = tid; j < D.n_list; j += kSelThreads) mass[j] = 0ull;
     for (int i = tid; i < kHistBins; i += kSelThreads) hist[i] = 0;
     for (int i = tid; i < kSelCap / 32; i += kSelThreads) chosen[i] = 0u;
-    if (tid == 0) counter[0] = 0;
+    if (tid < 4) counter[tid] = 0;   // counter[1] is the equal-key flag of the rank
 
     // 1) candidate counts: wave w owns sub-chunks [w * spw, (w + 1) * spw)
     const bool small_nsub = nsub <= kSelMaxSub;
@@ -312,6 +226,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchInts t
             total += t;
         }
         incl += wbase;   // row-wide inclusive offset of this lane's sub-chunk
+        if (lane < spw && sc < nsub) pre[sc] = incl - c_l;
         __syncthreads();
     } else {
         int mine = 0;
@@ -328,45 +243,40 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchInts t
         auto KEY = [&](int i) { return lds[i]; };
         auto CAND = [&](int i) { return lds[kOffCand + i]; };
         uint32_t kmin = 0xffffffffu, kmax = 0u, kcount = 0u;
-        for (int j0 = 0; j0 < spw; j0 += kLoadBatch) {
-            float sv[kLoadBatch];
-            uint32_t pv[kLoadBatch];
+        // candidate i lives in the sub-chunk sc with pre[sc] <= i < pre[sc + 1]
+        // (the last of equal offsets: empty sub-chunks never match); every
+        // thread loads a few candidates, all loads issued before any is used
+        const uint2* cand = w.cand + rbase;
+        for (int i0 = 0; i0 < total; i0 += kCopyPer * kSelThreads) {
+            int ci[kCopyPer], cs[kCopyPer];
 #pragma unroll
-            for (int u = 0; u < kLoadBatch; ++u) {
-                const int j = min(j0 + u, kWave - 1);
-                const int cj = j0 + u < spw ? __builtin_amdgcn_readlane(c_l, j) : 0;
-                const int64_t src = rbase + static_cast<int64_t>(wave * spw + j) * kSub + lane;
-                if (lane < cj) {
-                    sv[u] = w.cand_score[src];
-                    pv[u] = static_cast<uint32_t>(w.cand_pos[src]);
-                }
+            for (int u = 0; u < kCopyPer; ++u) {
+                ci[u] = i0 + u * kSelThreads + tid;
+                cs[u] = 0;
             }
 #pragma unroll
-            for (int u = 0; u < kLoadBatch; ++u) {
-                const int j = min(j0 + u, kWave - 1);
-                const int cj = j0 + u < spw ? __builtin_amdgcn_readlane(c_l, j) : 0;
-                const int o = __builtin_amdgcn_readlane(incl, j) - cj + lane;
-                if (lane < cj) {
-                    const uint32_t kk = float_key(sv[u]);
-                    lds[o] = kk;
-                    lds[kOffCand + o] = pv[u];
+            for (int step = kSelMaxSub / 2; step > 0; step >>= 1) {
+#pragma unroll
+                for (int u = 0; u < kCopyPer; ++u) {
+                    const int t = cs[u] + step;
+                    if (t < nsub && pre[t] <= ci[u]) cs[u] = t;
+                }
+            }
+            uint2 rec[kCopyPer];
+#pragma unroll
+            for (int u = 0; u < kCopyPer; ++u) {
+                const int slot = min(ci[u], total - 1) - pre[cs[u]];
+                rec[u] = cand[static_cast<int64_t>(cs[u]) * kSub + slot];
+            }
+#pragma unroll
+            for (int u = 0; u < kCopyPer; ++u) {
+                if (ci[u] < total) {
+                    const uint32_t kk = float_key(__uint_as_float(rec[u].x));
+                    lds[ci[u]] = kk;
+                    lds[kOffCand + ci[u]] = rec[u].y;
                     kmin = min(kmin, kk);
                     kmax = max(kmax, kk);
                 }
-            }
-        }
-        // sub-chunks with more than one wave of candidates
-        for (int j = 0; j < spw; ++j) {
-            const int cj = __builtin_amdgcn_readlane(c_l, j);
-            if (cj <= kWave) continue;
-            const int o0 = __builtin_amdgcn_readlane(incl, j) - cj;
-            const int64_t src0 = rbase + static_cast<int64_t>(wave * spw + j) * kSub;
-            for (int i = kWave + lane; i < cj; i += kWave) {
-                const uint32_t kk = float_key(w.cand_score[src0 + i]);
-                lds[o0 + i] = kk;
-                lds[kOffCand + o0 + i] = static_cast<uint32_t>(w.cand_pos[src0 + i]);
-                kmin = min(kmin, kk);
-                kmax = max(kmax, kk);
             }
         }
         block_min_max_count<kSelThreads>(kmin, kmax, kcount, bs);
@@ -386,9 +296,8 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchInts t
             const int bstar = block_find_bin_desc<kSelThreads>(hist, k, above, ss, bs);
             uint32_t kth = 0u;
             const bool by_rank = rank_boundary_bin(
-                KEY, [](int) { return true; }, [&](int i) { return perm[CAND(i) & kPosMask]; },
-                total, kmin, sh, bstar, hist[bstar], k - above, r_key, r_idx, r_tok, counter,
-                chosen, kth, bs);
+                KEY, [&](int i) { return perm[CAND(i) & kPosMask]; }, total, kmin, sh, bstar,
+                hist[bstar], k - above, r_key, r_idx, r_tok, counter, counter + 1, chosen, kth, bs);
             if (by_rank) {
                 shift = key_float(kth);   // the k-th largest score
                 emit_selection(
@@ -433,8 +342,9 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchInts t
                 const int c = cnt[sc];
                 const int64_t src = rbase + static_cast<int64_t>(sc) * kSub;
                 for (int i = 0; i < c; ++i, ++o) {
-                    w.comp_key[rbase + o] = float_key(w.cand_score[src + i]);
-                    w.comp_pos[rbase + o] = w.cand_pos[src + i];
+                    const uint2 rec = w.cand[src + i];
+                    w.comp_key[rbase + o] = float_key(__uint_as_float(rec.x));
+                    w.comp_pos[rbase + o] = static_cast<int32_t>(rec.y);
                 }
             }
         } else {
@@ -490,16 +400,9 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchInts t
     }
 }
 
-hipError_t launch_sample(const Dims& D, const BatchInts& tk, const Index& ix, const Work& w,
-                         float bias, hipStream_t s) {
-    hipLaunchKernelGGL(sample_kernel, dim3(D.B * D.Hq), dim3(kSelThreads), 0, s, D, tk, ix, w,
-                       bias);
-    return hipGetLastError();
-}
-
-hipError_t launch_select(const Dims& D, const BatchInts& tk, const Index& ix, const Work& w,
+hipError_t launch_select(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w,
                          int force_fallback, hipStream_t s) {
-    hipLaunchKernelGGL(select_kernel, dim3(D.B * D.Hq), dim3(kSelThreads), kSelLdsBytes, s, D, tk,
+    hipLaunchKernelGGL(select_kernel, dim3(D.B * D.Hq), dim3(kSelThreads), kSelLdsBytes, s, D, ba,
                        ix, w, force_fallback);
     return hipGetLastError();
 }
