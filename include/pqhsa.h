@@ -54,7 +54,8 @@ typedef enum { PQHSA_F32 = 0, PQHSA_BF16 = 1 } pqhsa_dtype;
  * Supported: head_dim = 128, pq_m = 16 (8-dimensional subspaces), max_seq <= 2^20,
  * pq_ksub = 256 (one uint8 code per subspace), 1 <= n_list <= 4096,
  * G in {1, 2, 4, 8}, 1 <= batch <= 256, kv_dtype F32 or BF16 (the query has
- * the same dtype as the cache), 0 <= max_topk <= max_seq. */
+ * the same dtype as the cache), 0 <= max_topk <= max_seq, and
+ * ceil((n_sink + n_local + max_topk) / 128) + ceil(n_list / 64) <= 512. */
 typedef struct {
     int32_t batch;
     int32_t n_q_heads;

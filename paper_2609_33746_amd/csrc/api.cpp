@@ -47,6 +47,7 @@ struct pqhsa_ctx {
     int32_t* n_seq_dev = nullptr;
     int32_t* n_r_dev = nullptr;
     int scan_nwg = 0;   // scan workgroups per (b, kv head)
+    uint32_t epoch = 0;  // prologue launches so far (LUT completion counters)
 
     // workspace
     Work w{};
@@ -129,6 +130,15 @@ pqhsa_status check_shape(const pqhsa_shape* s) {
     if (s->batch > kMaxBatch) return fail(nullptr, PQHSA_ERR_UNSUPPORTED, "batch must be <= 256");
     if (s->n_list > kMaxLists) return fail(nullptr, PQHSA_ERR_UNSUPPORTED, "n_list must be <= 4096");
     if (s->max_seq > kMaxSeq) return fail(nullptr, PQHSA_ERR_UNSUPPORTED, "max_seq must be <= 2^20");
+    {
+        // partials per row: splits of the exact set plus background chunks
+        const int nsplit = std::max((s->n_sink + s->n_local + s->max_topk + kAttnRows - 1) / kAttnRows, 1);
+        const int nbgc = (s->n_list + kBgLists - 1) / kBgLists;
+        if (nsplit + nbgc > kMaxRowParts)
+            return fail(nullptr, PQHSA_ERR_UNSUPPORTED,
+                        "n_sink + n_local + max_topk must be <= %d for n_list = %d",
+                        (kMaxRowParts - nbgc) * kAttnRows, s->n_list);
+    }
     return PQHSA_OK;
 }
 
@@ -245,7 +255,10 @@ pqhsa_status pqhsa_create(const pqhsa_shape* shape, pqhsa_ctx** out) {
     A(dev_alloc(c, &c->n_seq_dev, B));
     A(dev_alloc(c, &c->n_r_dev, B));
     A(dev_alloc(c, &w.lut, BG * kLutRow * G));
-    A(dev_alloc(c, &w.coarse, BG * L * G));
+    A(dev_alloc(c, &w.coarse, BG * L * G + 16));   // + 16: whole float4 reads at the end
+    A(dev_alloc(c, &w.lut_head, BQ * kLutRow));
+    A(dev_alloc(c, &w.lut_done, BG));
+    if (ea == hipSuccess) ea = hipMemset(w.lut_done, 0, BG * sizeof(uint32_t));
     A(dev_alloc(c, &w.tau_lo, BQ));
     A(dev_alloc(c, &w.cand, BQ * rc));
     A(dev_alloc(c, &w.cand_cnt, BQ * D.nsub_cap));
@@ -390,7 +403,10 @@ static pqhsa_status decode_impl(pqhsa_ctx* c, const void* q, const void* k, cons
         if (timed && e == hipSuccess) e = hipEventRecord(c->ev[i], stream);
     };
     mark(0);
-    if (e == hipSuccess) e = launch_prologue(D, ba, kv, ix, c->w, c->bias, stream);
+    if (e == hipSuccess) {
+        e = launch_prologue(D, ba, kv, ix, c->w, c->bias, c->epoch + 1, stream);
+        if (e == hipSuccess) ++c->epoch;   // the counters advance only if the launch happened
+    }
     mark(1);
     if (e == hipSuccess) e = launch_scan(D, ba, ix, c->w, c->scan_nwg, stream);
     mark(2);

@@ -200,4 +200,35 @@ __device__ __forceinline__ float key_float(uint32_t k) {
     return __uint_as_float(u);
 }
 
+
+// ---------------------------------------------------------------------------
+// publication between workgroups of one launch
+//
+// A producer writes the data a consumer workgroup will read with device-scope
+// stores (written through to the device's coherence point, so no cache
+// write-back is needed), waits until all of its stores are acknowledged, and
+// only then increments a device-scope counter. A consumer polls the counter,
+// then performs an acquire fence before reading the data.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void store_device(float* p, float v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void store_device(int32_t* p, int32_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void store_device(uint32_t* p, uint32_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// Wait until every vector memory operation of this wave has completed
+// (s_waitcnt vmcnt(0); the expcnt and lgkmcnt fields are left at their
+// no-wait maxima).
+__device__ __forceinline__ void wait_vector_memory() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+__device__ __forceinline__ uint32_t counter_add(uint32_t* c, uint32_t v) {
+    return __hip_atomic_fetch_add(c, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t counter_read(const uint32_t* c) {
+    return __hip_atomic_load(c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void acquire_device() { __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent"); }
+
 }  // namespace pqhsa

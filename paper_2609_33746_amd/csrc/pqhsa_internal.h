@@ -28,6 +28,7 @@ constexpr int kAttnRows = 128;     // exact-set rows per split
 constexpr int kBgLists = 64;       // lists per background workgroup
 constexpr int kDenseRows = 512;    // cache rows per dense split
 constexpr int kPartStride = 132;   // floats per partial: m, Z, pad, pad, N[128]
+constexpr int kMaxRowParts = 512;  // partials per row (exact splits + background chunks)
 
 // --- kernel arguments ----------------------------------------------------
 struct Dims {
@@ -69,6 +70,8 @@ struct Index {
 // Decode workspace, owned by the context.
 struct Work {
     float* lut;          // [B, Hkv, M, K, G]   (q^(m) . p_{m,z}) / sqrt(d)
+    float* lut_head;     // [B, Hq, M, K]       the same entries, head-major
+    uint32_t* lut_done;  // [B, Hkv] LUT workgroups finished, summed over all calls
     float* coarse;       // [B, Hkv, n_list, G] (q . c_j) / sqrt(d)
     float* tau_lo;       // [B, Hq] candidate threshold
     uint2* cand;         // [B, Hq, rcap] candidates compacted per sub-chunk: (score bits,
@@ -100,8 +103,13 @@ struct KV {
 hipError_t configure_scan();
 hipError_t configure_select();
 
+// LUT workgroups per (b, kv head) in the prologue: kPqM / 2 fine parts plus
+// one coarse part per 128 lists. epoch = the number of prologue launches on
+// this workspace so far, this one included: the LUT counters then read
+// epoch * prologue_parts(n_list).
+__host__ __device__ inline int prologue_parts(int n_list) { return kPqM / 2 + (n_list + 127) / 128; }
 hipError_t launch_prologue(const Dims& D, const BatchArgs& ba, const KV& kv, const Index& ix,
-                           const Work& w, float bias, hipStream_t s);
+                           const Work& w, float bias, uint32_t epoch, hipStream_t s);
 // nwg = scan workgroups per (batch element, KV head): enough for the longest R_b
 hipError_t launch_scan(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w, int nwg,
                        hipStream_t s);

@@ -1,24 +1,30 @@
 // Decode prologue: the LUT build (Section 3.1, Eq. 2) and the candidate
-// threshold sample, in one launch with two workgroup roles that do not wait
-// for each other.
+// threshold sample, in one launch with two workgroup roles.
 //
-// LUT role, per (batch element, KV head): the fine table
+// LUT role, per (batch element, KV head) and part: the fine table
 // F[m][z][hh] = (q_hh^(m) . p_{m,z}) / sqrt(d) for the G query heads of the
-// group, and the coarse table C[j][hh] = (q_hh . c_j) / sqrt(d).
+// group (also written head-major for the sample role), and the coarse table
+// C[j][hh] = (q_hh . c_j) / sqrt(d).
 // Folding r_q / sqrt(d) into the tables: (r_q / sqrt(d)) u_q . x = q . x / sqrt(d),
 // so the tables are built from q / sqrt(d) directly and no normalisation of q
 // is needed (a zero query gives all-zero tables, hence zero scores).
+// Each LUT workgroup writes its part with device-scope stores and, once they
+// are acknowledged, increments its KV head's counter.
 //
 // Sample role, per (batch element, query head) row: scores a stratified
 // sample of the row's list-major positions (contiguous runs of kSampleRun
 // positions, evenly spread) and takes a sample order statistic as the
 // candidate threshold tau_lo, chosen so that about twice k tokens of the
-// whole row score at or above it. The role builds the table entries it needs
-// itself (the head's fine table and the coarse terms of the lists its
-// samples fall in), with the same arithmetic as the LUT role, so it needs no
-// result of the LUT role. Any threshold gives the same final output: it only
-// decides how many candidates the scan emits (the top-k stage falls back to
-// an exact re-scan when fewer than k tokens reach it).
+// whole row score at or above it. The role issues its sample loads, then
+// waits for its KV head's LUT parts (every LUT workgroup has a lower
+// workgroup id and waits for nothing, so it is dispatched first and
+// finishes), then reads the head's tables.
+//
+// Any threshold gives the same final output: it only decides how many
+// candidates the scan emits (the top-k stage falls back to an exact re-scan
+// when fewer than k tokens reach it). So the wait is bounded: a sample
+// workgroup that does not see its tables within kSpinLimit polls sets
+// tau_lo = -inf, which makes every token a candidate, and exits.
 #include "device_common.h"
 #include "hist_select.h"
 #include "pq_score.h"
@@ -29,26 +35,19 @@ namespace pqhsa {
 
 constexpr int kProThreads = 512;
 constexpr int kFineWg = kProThreads / kKsub;              // subspaces per fine workgroup: 2
-static_assert(kFineWg * kKsub == kProThreads && kPqM % kFineWg == 0, "fine tiling");
+constexpr int kFineParts = kPqM / kFineWg;                 // fine workgroups per KV head: 8
 constexpr int kCoarseLists = 128;                          // lists per coarse workgroup
 constexpr int kCoarseGroups = kProThreads / 16;            // 16-lane groups
 constexpr int kCoarsePer = kCoarseLists / kCoarseGroups;   // lists per group: 4
 constexpr int kSamplesPer = kMaxSamples / kProThreads;     // samples per thread: 4
-constexpr int kSampleListsPer = 12;                        // sampled lists per 16-lane group and batch
-constexpr int kFinePer = kLutRow / kProThreads;            // fine entries per thread: 8
-static_assert(kPqM * (kKsub / kFinePer) == kProThreads, "the sample role builds every fine entry once");
+constexpr int kLutF4 = kLutRow / 4 / kProThreads;          // float4 of a head table per thread: 2
+constexpr int kSpinLimit = 1 << 18;                        // polls before giving up (~0.3 s)
+static_assert(kFineWg * kKsub == kProThreads && kPqM % kFineWg == 0, "fine tiling");
 static_assert(kCoarsePer * kCoarseGroups == kCoarseLists, "coarse tiling");
 static_assert(kSamplesPer * kProThreads == kMaxSamples && kSampleRun % kSamplesPer == 0, "samples");
+static_assert(kLutF4 * 4 * kProThreads == kLutRow, "head table staging");
 
-// (q^(m) / sqrt(d)) . p_{m,z}: 8 products summed in order t = 0..7
-__device__ __forceinline__ float fine_entry(const float (&qs)[kDsub], const float4 p0,
-                                           const float4 p1) {
-    const float pv[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
-    float acc = 0.0f;
-#pragma unroll
-    for (int t = 0; t < kDsub; ++t) acc = fmaf(qs[t], pv[t], acc);
-    return acc;
-}
+static_assert(kFineParts == kPqM / 2 && kCoarseLists == 128, "prologue_parts() counts these");
 
 // (q / sqrt(d)) . c over 16 lanes of 8 dimensions each; every lane of the
 // 16-lane group receives the same sum.
@@ -68,78 +67,85 @@ __device__ __forceinline__ void lut_role(const Dims& D, const T* __restrict__ q,
                                          int bg, int part) {
     const int b = bg / D.Hkv;
     const int g = bg % D.Hkv;
-    const T* qg = q + (static_cast<int64_t>(b) * D.Hq + g * G) * kHeadDim;
+    const int row0 = b * D.Hq + g * G;
+    const T* qg = q + static_cast<int64_t>(row0) * kHeadDim;
     const int tid = threadIdx.x;
-    if (part < kPqM / kFineWg) {
+    if (part < kFineParts) {
         // fine table: one (subspace, codeword) per thread
         const int m = part * kFineWg + tid / kKsub;
         const int z = tid % kKsub;
         const float* p = codebooks + ((static_cast<int64_t>(bg) * kPqM + m) * kKsub + z) * kDsub;
         const float4 p0 = *reinterpret_cast<const float4*>(p);
         const float4 p1 = *reinterpret_cast<const float4*>(p + 4);
+        const float pv[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
         float* o = w.lut + ((static_cast<int64_t>(bg) * kPqM + m) * kKsub + z) * G;
 #pragma unroll
         for (int hh = 0; hh < G; ++hh) {
             float qs[kDsub];
             Load8<T>::run(qg + hh * kHeadDim + m * kDsub, qs);
+            float acc = 0.0f;
 #pragma unroll
-            for (int t = 0; t < kDsub; ++t) qs[t] *= D.inv_sqrt_d;
-            o[hh] = fine_entry(qs, p0, p1);
+            for (int t = 0; t < kDsub; ++t) acc = fmaf(qs[t] * D.inv_sqrt_d, pv[t], acc);
+            store_device(o + hh, acc);
+            store_device(w.lut_head + static_cast<int64_t>(row0 + hh) * kLutRow + m * kKsub + z, acc);
         }
-        return;
-    }
-    // coarse table: 16 lanes per list, 8 dimensions per lane
-    const int c = part - kPqM / kFineWg;
-    const int lane16 = tid & 15;
-    const int group = tid >> 4;
-    float4 cv[kCoarsePer][2];
+    } else {
+        // coarse table: 16 lanes per list, 8 dimensions per lane
+        const int c = part - kFineParts;
+        const int lane16 = tid & 15;
+        const int group = tid >> 4;
+        float4 cv[kCoarsePer][2];
 #pragma unroll
-    for (int u = 0; u < kCoarsePer; ++u) {
-        const int j = c * kCoarseLists + group + u * kCoarseGroups;
-        const int jc = j < D.n_list ? j : D.n_list - 1;   // keep all lanes active
-        const float* cp = centroids + (static_cast<int64_t>(bg) * D.n_list + jc) * kHeadDim + lane16 * 8;
-        cv[u][0] = *reinterpret_cast<const float4*>(cp);
-        cv[u][1] = *reinterpret_cast<const float4*>(cp + 4);
-    }
-    float qc[G][8];
-#pragma unroll
-    for (int hh = 0; hh < G; ++hh) {
-        Load8<T>::run(qg + hh * kHeadDim + lane16 * 8, qc[hh]);
-#pragma unroll
-        for (int t = 0; t < 8; ++t) qc[hh][t] *= D.inv_sqrt_d;
-    }
-#pragma unroll
-    for (int u = 0; u < kCoarsePer; ++u) {
-        const int j = c * kCoarseLists + group + u * kCoarseGroups;
-        float mine = 0.0f;
+        for (int u = 0; u < kCoarsePer; ++u) {
+            const int j = c * kCoarseLists + group + u * kCoarseGroups;
+            const int jc = j < D.n_list ? j : D.n_list - 1;   // keep all lanes active
+            const float* cp = centroids + (static_cast<int64_t>(bg) * D.n_list + jc) * kHeadDim + lane16 * 8;
+            cv[u][0] = *reinterpret_cast<const float4*>(cp);
+            cv[u][1] = *reinterpret_cast<const float4*>(cp + 4);
+        }
+        float qc[G][8];
 #pragma unroll
         for (int hh = 0; hh < G; ++hh) {
-            const float acc = coarse_entry(qc[hh], cv[u][0], cv[u][1]);
-            if (lane16 == hh) mine = acc;
+            Load8<T>::run(qg + hh * kHeadDim + lane16 * 8, qc[hh]);
+#pragma unroll
+            for (int t = 0; t < 8; ++t) qc[hh][t] *= D.inv_sqrt_d;
         }
-        if (j < D.n_list && lane16 < G)
-            w.coarse[(static_cast<int64_t>(bg) * D.n_list + j) * G + lane16] = mine;
+#pragma unroll
+        for (int u = 0; u < kCoarsePer; ++u) {
+            const int j = c * kCoarseLists + group + u * kCoarseGroups;
+            float mine = 0.0f;
+#pragma unroll
+            for (int hh = 0; hh < G; ++hh) {
+                const float acc = coarse_entry(qc[hh], cv[u][0], cv[u][1]);
+                if (lane16 == hh) mine = acc;
+            }
+            if (j < D.n_list && lane16 < G)
+                store_device(w.coarse + (static_cast<int64_t>(bg) * D.n_list + j) * G + lane16, mine);
+        }
     }
+    // publish: every store acknowledged at device scope, then one increment
+    wait_vector_memory();
+    __syncthreads();
+    if (tid == 0) counter_add(w.lut_done + bg, 1u);
 }
 
 struct SampleLds {
-    float lut[kLutRow];          // the head's fine table [M][K]
-    int uniq[kMaxSamples];       // distinct list ids of the samples, in sample order
-    float cf[kMaxSamples];       // coarse term of each distinct list
+    float lut[kLutRow];   // the head's fine table [M][K]
     int hist[kHistBins];
-    int prev_last[kProThreads];  // list id of each thread's last sample
+    int ready;
     SelectScratch ss;
     BlockScratch bs;
 };
 
 template <typename T, int G>
 __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, const Index& ix,
-                                            const T* __restrict__ q, const Work& w, float bias,
+                                            const Work& w, float bias, uint32_t lut_target,
                                             int row, SampleLds& sm) {
     const int tid = threadIdx.x;
     const int b = row / D.Hq;
     const int h = row % D.Hq;
     const int g = h / G;
+    const int hh = h % G;
     const int bg = b * D.Hkv + g;
     const int n_r = ba.n_r[b];
     const int k = ba.topk[b];
@@ -148,8 +154,8 @@ __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, 
         if (tid == 0) w.tau_lo[row] = neg_inf;
         return;
     }
-    // runs of kSampleRun positions, rs apart (rs >= 1), clipped at the next run;
-    // thread tid owns samples 4 tid .. 4 tid + 3 (half a run)
+    // 1) the samples: runs of kSampleRun positions, rs apart (rs >= 1),
+    //    clipped at the next run; thread tid owns samples 4 tid .. 4 tid + 3
     const int nrun = min(kMaxSamples / kSampleRun, (n_r + kSampleRun - 1) / kSampleRun);
     const int rs = n_r / nrun;
     const int run_len = min(kSampleRun, rs);
@@ -171,90 +177,49 @@ __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, 
         rv[u] = ix.norms[base + p];
         jv[u] = ix.pos_list[base + p];
     }
-    // this head's fine table: thread tid builds the entries (m, z) of subspace
-    // m = tid / 32 for z = tid % 32 + 32 i, so it needs one slice of q
-    const T* qh = q + static_cast<int64_t>(row) * kHeadDim;
-    const float* cbk = ix.codebooks + static_cast<int64_t>(bg) * kPqM * kKsub * kDsub;
-    constexpr int kZStride = kKsub / kFinePer;   // 32
-    const int m = tid / kZStride;
-    const int z0 = tid % kZStride;
-    float4 pv[kFinePer][2];
-#pragma unroll
-    for (int i = 0; i < kFinePer; ++i) {
-        const float* p = cbk + (m * kKsub + z0 + i * kZStride) * kDsub;
-        pv[i][0] = *reinterpret_cast<const float4*>(p);
-        pv[i][1] = *reinterpret_cast<const float4*>(p + 4);
-    }
-    float qs[kDsub];
-    Load8<T>::run(qh + m * kDsub, qs);
-    __builtin_amdgcn_sched_barrier(0);   // every load above is in flight before any use
-#pragma unroll
-    for (int t = 0; t < kDsub; ++t) qs[t] *= D.inv_sqrt_d;
-#pragma unroll
-    for (int i = 0; i < kFinePer; ++i)
-        sm.lut[m * kKsub + z0 + i * kZStride] = fine_entry(qs, pv[i][0], pv[i][1]);
-#pragma unroll
-    for (int u = 0; u < kSamplesPer; ++u) jv[u] = ok[u] ? jv[u] : -1;
-    sm.prev_last[tid] = jv[kSamplesPer - 1];
     for (int i = tid; i < kHistBins; i += kProThreads) sm.hist[i] = 0;
-    __syncthreads();
 
-    // distinct lists of the (list-major, hence list-sorted) samples
-    int nf = 0;
-    bool first[kSamplesPer];
-#pragma unroll
-    for (int u = 0; u < kSamplesPer; ++u) {
-        const int prev = u > 0 ? jv[u - 1] : (tid > 0 ? sm.prev_last[tid - 1] : -1);
-        first[u] = jv[u] >= 0 && jv[u] != prev;
-        nf += first[u] ? 1 : 0;
-    }
-    int n_uniq = 0;
-    int idx = block_excl_scan<kProThreads>(nf, n_uniq, sm.ss) - 1;
-    int dv[kSamplesPer];
-#pragma unroll
-    for (int u = 0; u < kSamplesPer; ++u) {
-        if (first[u]) sm.uniq[++idx] = jv[u];
-        dv[u] = max(idx, 0);
-    }
-    __syncthreads();
-
-    // coarse terms of the distinct lists: 16 lanes per list
-    {
-        const int lane16 = tid & 15;
-        const int group = tid >> 4;
-        float qc[8];
-        Load8<T>::run(qh + lane16 * 8, qc);
-#pragma unroll
-        for (int t = 0; t < 8; ++t) qc[t] *= D.inv_sqrt_d;
-        const float* cen = ix.centroids + static_cast<int64_t>(bg) * D.n_list * kHeadDim + lane16 * 8;
-        // one batch of loads covers kSampleLists lists (the usual case)
-        for (int d0 = 0; d0 < n_uniq; d0 += kCoarseGroups * kSampleListsPer) {
-            float4 c4[kSampleListsPer][2];
-#pragma unroll
-            for (int u = 0; u < kSampleListsPer; ++u) {
-                const int d = min(d0 + group + u * kCoarseGroups, n_uniq - 1);
-                const float* cp = cen + static_cast<int64_t>(sm.uniq[d]) * kHeadDim;
-                c4[u][0] = *reinterpret_cast<const float4*>(cp);
-                c4[u][1] = *reinterpret_cast<const float4*>(cp + 4);
+    // 2) wait for the KV head's tables (bounded)
+    if (tid == 0) {
+        int ready = 0;
+        for (int it = 0; it < kSpinLimit; ++it) {
+            if (static_cast<int32_t>(counter_read(w.lut_done + bg) - lut_target) >= 0) {
+                ready = 1;
+                break;
             }
-#pragma unroll
-            for (int u = 0; u < kSampleListsPer; ++u) {
-                const int d = d0 + group + u * kCoarseGroups;
-                const float acc = coarse_entry(qc, c4[u][0], c4[u][1]);
-                if (lane16 == 0 && d < n_uniq) sm.cf[d] = acc;
-            }
+            __builtin_amdgcn_s_sleep(2);
         }
+        acquire_device();
+        sm.ready = ready;
     }
     __syncthreads();
+    if (!sm.ready) {   // tables not seen in time: every token becomes a candidate
+        if (tid == 0) w.tau_lo[row] = neg_inf;
+        return;
+    }
 
-    // scores of the samples
+    // 3) the head's fine table into LDS, the coarse term of every sample
+    const float4* lsrc = reinterpret_cast<const float4*>(w.lut_head + static_cast<int64_t>(row) * kLutRow);
+    float4 lv[kLutF4];
+#pragma unroll
+    for (int i = 0; i < kLutF4; ++i) lv[i] = lsrc[i * kProThreads + tid];
+    const float* coarse = w.coarse + static_cast<int64_t>(bg) * D.n_list * G + hh;
+    float cf[kSamplesPer];
+#pragma unroll
+    for (int u = 0; u < kSamplesPer; ++u) cf[u] = coarse[jv[u] * G];
+    float4* ldst = reinterpret_cast<float4*>(sm.lut);
+#pragma unroll
+    for (int i = 0; i < kLutF4; ++i) ldst[i * kProThreads + tid] = lv[i];
+    __syncthreads();
+
+    // 4) scores of the samples
     float sc[kSamplesPer];
     uint32_t mn = 0xffffffffu, mx = 0u, cnt = 0u;
 #pragma unroll
     for (int u = 0; u < kSamplesPer; ++u) {
         float fs[1];
         fine_sum<1>(sm.lut, cv[u], fs);
-        sc[u] = pq_logit(rv[u], sm.cf[dv[u]], fs[0]);
+        sc[u] = pq_logit(rv[u], cf[u], fs[0]);
         if (ok[u]) {
             const uint32_t kk = float_key(sc[u]);
             mn = min(mn, kk);
@@ -270,8 +235,8 @@ __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, 
         if (tid == 0) w.tau_lo[row] = neg_inf;
         return;
     }
-    // bins of equal width in score (monotone: rounded subtraction and
-    // multiplication by a positive constant never reorder two scores)
+    // 5) bins of equal width in score (monotone: rounded subtraction and
+    //    multiplication by a positive constant never reorder two scores)
     const float fmn = key_float(mn);
     const float range = key_float(mx) - fmn;
     const float scale = (range > 0.0f && range < __builtin_huge_valf()) ? kHistBins / range : 0.0f;
@@ -294,47 +259,50 @@ __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, 
 }
 
 template <typename T, int G>
-__global__ __launch_bounds__(kProThreads) __attribute__((amdgpu_waves_per_eu(1, 2))) void prologue_kernel(Dims D, BatchArgs ba, Index ix,
+__global__ __launch_bounds__(kProThreads) void prologue_kernel(Dims D, BatchArgs ba, Index ix,
                                                                const T* __restrict__ q, Work w,
-                                                               float bias, int n_lut_wg) {
+                                                               float bias, uint32_t lut_target,
+                                                               int n_lut_wg) {
     __shared__ SampleLds sm;
-    const int n_coarse = (D.n_list + kCoarseLists - 1) / kCoarseLists;
-    const int per_bg = kPqM / kFineWg + n_coarse;
     if (static_cast<int>(blockIdx.x) < n_lut_wg) {
+        const int per_bg = prologue_parts(D.n_list);
         lut_role<T, G>(D, q, ix.codebooks, ix.centroids, w, blockIdx.x / per_bg,
                        blockIdx.x % per_bg);
         return;
     }
-    sample_role<T, G>(D, ba, ix, q, w, bias, blockIdx.x - n_lut_wg, sm);
+    sample_role<T, G>(D, ba, ix, w, bias, lut_target, blockIdx.x - n_lut_wg, sm);
 }
 
 template <typename T, int G>
 static hipError_t launch_prologue_t(const Dims& D, const BatchArgs& ba, const KV& kv,
-                                    const Index& ix, const Work& w, float bias, hipStream_t s) {
-    const int n_coarse = (D.n_list + kCoarseLists - 1) / kCoarseLists;
-    const int n_lut_wg = D.B * D.Hkv * (kPqM / kFineWg + n_coarse);
+                                    const Index& ix, const Work& w, float bias, uint32_t epoch,
+                                    hipStream_t s) {
+    const int per_bg = prologue_parts(D.n_list);
+    const int n_lut_wg = D.B * D.Hkv * per_bg;
     const int grid = n_lut_wg + D.B * D.Hq;
+    const uint32_t target = epoch * static_cast<uint32_t>(per_bg);
     hipLaunchKernelGGL((prologue_kernel<T, G>), dim3(grid), dim3(kProThreads), 0, s, D, ba, ix,
-                       static_cast<const T*>(kv.q), w, bias, n_lut_wg);
+                       static_cast<const T*>(kv.q), w, bias, target, n_lut_wg);
     return hipGetLastError();
 }
 
 template <typename T>
 static hipError_t launch_prologue_g(const Dims& D, const BatchArgs& ba, const KV& kv,
-                                    const Index& ix, const Work& w, float bias, hipStream_t s) {
+                                    const Index& ix, const Work& w, float bias, uint32_t epoch,
+                                    hipStream_t s) {
     switch (D.G) {
-        case 1: return launch_prologue_t<T, 1>(D, ba, kv, ix, w, bias, s);
-        case 2: return launch_prologue_t<T, 2>(D, ba, kv, ix, w, bias, s);
-        case 4: return launch_prologue_t<T, 4>(D, ba, kv, ix, w, bias, s);
-        case 8: return launch_prologue_t<T, 8>(D, ba, kv, ix, w, bias, s);
+        case 1: return launch_prologue_t<T, 1>(D, ba, kv, ix, w, bias, epoch, s);
+        case 2: return launch_prologue_t<T, 2>(D, ba, kv, ix, w, bias, epoch, s);
+        case 4: return launch_prologue_t<T, 4>(D, ba, kv, ix, w, bias, epoch, s);
+        case 8: return launch_prologue_t<T, 8>(D, ba, kv, ix, w, bias, epoch, s);
         default: return hipErrorInvalidValue;
     }
 }
 
 hipError_t launch_prologue(const Dims& D, const BatchArgs& ba, const KV& kv, const Index& ix,
-                           const Work& w, float bias, hipStream_t s) {
-    return kv.bf16 ? launch_prologue_g<bf16_t>(D, ba, kv, ix, w, bias, s)
-                   : launch_prologue_g<float>(D, ba, kv, ix, w, bias, s);
+                           const Work& w, float bias, uint32_t epoch, hipStream_t s) {
+    return kv.bf16 ? launch_prologue_g<bf16_t>(D, ba, kv, ix, w, bias, epoch, s)
+                   : launch_prologue_g<float>(D, ba, kv, ix, w, bias, epoch, s);
 }
 
 }  // namespace pqhsa

@@ -9,10 +9,12 @@
 // batch element gets the workgroup count of the longest R_b; the surplus
 // workgroups of shorter sequences exit at once.
 //
-// Every load of a wave is issued before its arithmetic starts: each lane's
-// list ids, codes and norms, the group LUT (staged through registers into
-// LDS) and, once the list ids have arrived, the coarse terms of the lanes'
-// lists, so a wave waits for about two memory round trips in all.
+// The workgroup first stages the group LUT and the coarse table in LDS
+// (through registers), then each wave issues the loads of all its 64-position
+// steps (list ids, codes, norms) at once, in step order, so the arithmetic of
+// the first steps overlaps the arrival of the later ones. When the coarse
+// table does not fit in LDS beside the LUT, each lane gathers its lists'
+// coarse terms instead.
 //
 // Per token and head the wave computes l~ and then either
 //   * emits (l~, list id and position) as a top-k candidate when
@@ -38,6 +40,12 @@ namespace pqhsa {
 
 constexpr int kScanThreads = kScanWaves * kWave;
 constexpr int kIters = kSub / kWave;   // 64-position steps per sub-chunk
+// float4 of the coarse table each thread stages into LDS: room for 1024 lists
+// at G = 4 and 8 (the LUT and the table then fill 80 KB / 160 KB of LDS)
+template <int G>
+constexpr int kCoarseStage = G >= 4 ? G / 2 : 2;
+template <int G>
+constexpr int kCoarseCapF4 = kCoarseStage<G> * kScanThreads;
 
 // The G coarse terms of one list, [n_list][G] layout.
 template <int G>
@@ -71,10 +79,12 @@ __device__ __forceinline__ void flush_segment(float* seg_row, float (&acc)[G]) {
     if (lane_id() < G) seg_row[lane_id()] = mine;
 }
 
-template <int G>
+template <int G, bool kCoarseLds>
 __global__ __launch_bounds__(kScanThreads) void scan_kernel(Dims D, BatchArgs ba, Index ix, Work w,
                                                             int nwg) {
-    extern __shared__ float lut_s[];   // [M][K][G]
+    // [M][K][G] group LUT, then (when it fits) the [n_list][G] coarse table
+    extern __shared__ float lut_s[];
+    float* coarse_s = lut_s + kLutRow * G;
     const int bg = blockIdx.x / nwg;
     const int b = bg / D.Hkv;
     const int g = bg % D.Hkv;
@@ -91,43 +101,51 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(Dims D, BatchArgs ba
     const bool active = p_begin < n_r;
     const int64_t base = static_cast<int64_t>(bg) * D.rcap;
     const int row0 = b * D.Hq + g * G;
+    const float* coarse = w.coarse + static_cast<int64_t>(bg) * D.n_list * G;
 
-    // 1) list ids (addresses clamped into R_b: every load is in bounds)
-    int jl[kIters];
-#pragma unroll
-    for (int it = 0; it < kIters; ++it)
-        jl[it] = ix.pos_list[base + min(p_begin + it * kWave + lane, n_r - 1)];
-    // 2) the group LUT and the thresholds
+    // 1) the tables shared by the workgroup, and the thresholds
     constexpr int kStage = kLutRow * G / 4 / kScanThreads;
     static_assert(kStage * kScanThreads * 4 == kLutRow * G, "LUT staging tiling");
     const float4* lsrc = reinterpret_cast<const float4*>(w.lut + static_cast<int64_t>(bg) * kLutRow * G);
     float4 st[kStage];
 #pragma unroll
     for (int i = 0; i < kStage; ++i) st[i] = lsrc[i * kScanThreads + tid];
+    // the coarse table, kCoarseStage float4 per thread (addresses clamped, so
+    // every load is in bounds; the LDS region is padded to the full staging size)
+    const int n_cf4 = D.n_list * G / 4;
+    float4 cst[kCoarseStage<G>];
+    if constexpr (kCoarseLds) {
+#pragma unroll
+        for (int i = 0; i < kCoarseStage<G>; ++i)
+            cst[i] = reinterpret_cast<const float4*>(coarse)[min(i * kScanThreads + tid, n_cf4 - 1)];
+    }
     float tlo[G];
 #pragma unroll
     for (int hh = 0; hh < G; ++hh) tlo[hh] = w.tau_lo[row0 + hh];
-    // 3) codes and norms
+    float4* ldst = reinterpret_cast<float4*>(lut_s);
+#pragma unroll
+    for (int i = 0; i < kStage; ++i) ldst[i * kScanThreads + tid] = st[i];
+    if constexpr (kCoarseLds) {
+#pragma unroll
+        for (int i = 0; i < kCoarseStage<G>; ++i)
+            reinterpret_cast<float4*>(coarse_s)[i * kScanThreads + tid] = cst[i];
+    }
+    __syncthreads();
+    if (!active) return;
+    // 2) per 64-position step: list ids, codes and norms (addresses clamped
+    //    into R_b, so every load is in bounds), issued in the order the steps
+    //    use them, after the tables: each step waits only for its own data
     const uint4* codes = reinterpret_cast<const uint4*>(ix.codes) + base;
+    int jl[kIters];
     uint4 cv[kIters];
     float rv[kIters];
 #pragma unroll
     for (int it = 0; it < kIters; ++it) {
         const int p = min(p_begin + it * kWave + lane, n_r - 1);
+        jl[it] = ix.pos_list[base + p];
         cv[it] = codes[p];
         rv[it] = ix.norms[base + p];
     }
-    // 4) coarse terms of the lanes' lists
-    const float* coarse = w.coarse + static_cast<int64_t>(bg) * D.n_list * G;
-    float cf[kIters][G];
-#pragma unroll
-    for (int it = 0; it < kIters; ++it) load_coarse<G>(coarse + jl[it] * G, cf[it]);
-    float4* ldst = reinterpret_cast<float4*>(lut_s);
-#pragma unroll
-    for (int i = 0; i < kStage; ++i) ldst[i * kScanThreads + tid] = st[i];
-    __syncthreads();
-    if (!active) return;
-
     float* segs = w.seg_sum + (static_cast<int64_t>(bg) * D.nseg_cap + sc) * G;   // + j * G
     int cur = __builtin_amdgcn_readfirstlane(jl[0]);   // list of the open segment
     float acc[G];
@@ -141,12 +159,17 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(Dims D, BatchArgs ba
         if (p_first >= p_end) continue;   // uniform: past the end of a short last sub-chunk
         const int p = p_first + lane;
         const bool valid = p < p_end;
+        // coarse terms of the lanes' lists: from LDS, or gathered when the
+        // coarse table does not fit beside the LUT
+        float cf[G];
+        if constexpr (kCoarseLds) load_coarse<G>(coarse_s + jl[it] * G, cf);
+        else load_coarse<G>(coarse + jl[it] * G, cf);
         float fs[G];
         fine_sum<G>(lut_s, cv[it], fs);
         float s[G], e[G];
 #pragma unroll
         for (int hh = 0; hh < G; ++hh) {
-            s[hh] = pq_logit(rv[it], cf[it][hh], fs[hh]);
+            s[hh] = pq_logit(rv[it], cf[hh], fs[hh]);
             e[hh] = (valid && s[hh] < tlo[hh]) ? __expf(s[hh] - tlo[hh]) : 0.0f;
         }
         // close the lists that end inside this step (lists are contiguous and
@@ -190,20 +213,37 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(Dims D, BatchArgs ba
     if (lane < G) w.cand_cnt[static_cast<int64_t>(row0 + lane) * D.nsub_cap + sc] = mine;
 }
 
+constexpr size_t kScanLdsMax = 160 * 1024;   // LDS of one workgroup on gfx950
+
 template <int G>
 static hipError_t launch_scan_t(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w,
                                 int nwg, hipStream_t s) {
-    const size_t lds = static_cast<size_t>(kLutRow) * G * sizeof(float);
-    hipLaunchKernelGGL((scan_kernel<G>), dim3(D.B * D.Hkv * nwg), dim3(kScanThreads), lds, s, D,
-                       ba, ix, w, nwg);
+    const size_t lut = static_cast<size_t>(kLutRow) * G * sizeof(float);
+    const size_t cf = static_cast<size_t>(kCoarseCapF4<G>) * 16;
+    static_assert(kLutRow * G * 4 + kCoarseCapF4<G> * 16 <= kScanLdsMax, "LDS budget");
+    const dim3 grid(D.B * D.Hkv * nwg);
+    if (D.n_list * G % 4 == 0 && D.n_list * G / 4 <= kCoarseCapF4<G>)
+        hipLaunchKernelGGL((scan_kernel<G, true>), grid, dim3(kScanThreads), lut + cf, s, D, ba, ix,
+                           w, nwg);
+    else
+        hipLaunchKernelGGL((scan_kernel<G, false>), grid, dim3(kScanThreads), lut, s, D, ba, ix, w,
+                           nwg);
     return hipGetLastError();
 }
 
 hipError_t configure_scan() {
-    // the G = 8 group LUT (128 KB) exceeds the default dynamic LDS limit
-    return hipFuncSetAttribute(reinterpret_cast<const void*>(&scan_kernel<8>),
-                               hipFuncAttributeMaxDynamicSharedMemorySize,
-                               static_cast<int>(kLutRow * 8 * sizeof(float)));
+    // the group LUT plus the coarse table can exceed the default dynamic LDS limit
+    const void* k[] = {reinterpret_cast<const void*>(&scan_kernel<1, true>),
+                       reinterpret_cast<const void*>(&scan_kernel<2, true>),
+                       reinterpret_cast<const void*>(&scan_kernel<4, true>),
+                       reinterpret_cast<const void*>(&scan_kernel<8, true>),
+                       reinterpret_cast<const void*>(&scan_kernel<8, false>)};
+    for (const void* f : k) {
+        const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                 static_cast<int>(kScanLdsMax));
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 hipError_t launch_scan(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w, int nwg,
