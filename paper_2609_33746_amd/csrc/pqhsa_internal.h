@@ -15,8 +15,8 @@ constexpr int kLutRow = kPqM * kKsub;  // LUT entries per query head
 constexpr int kMaxBatch = 256;
 constexpr int kMaxLists = 4096;
 
-constexpr int kSub = 256;          // list-major positions per wave sub-chunk
-constexpr int kScanWaves = 8;      // waves (sub-chunks) per scan workgroup
+constexpr int kSub = 128;          // list-major positions per wave sub-chunk
+constexpr int kScanWaves = 16;     // waves (sub-chunks) per scan workgroup
 constexpr int kMaxSamples = 2048;  // sampled positions per row for the threshold
 constexpr int kSelThreads = 1024;
 constexpr int kSelCap = 12288;     // candidates of one row held in LDS by the select kernel

@@ -43,7 +43,7 @@ constexpr int kIters = kSub / kWave;   // 64-position steps per sub-chunk
 // float4 of the coarse table each thread stages into LDS: room for 1024 lists
 // at G = 4 and 8 (the LUT and the table then fill 80 KB / 160 KB of LDS)
 template <int G>
-constexpr int kCoarseStage = G >= 4 ? G / 2 : 2;
+constexpr int kCoarseStage = 256 * G / kScanThreads > 1 ? 256 * G / kScanThreads : 1;
 template <int G>
 constexpr int kCoarseCapF4 = kCoarseStage<G> * kScanThreads;
 
