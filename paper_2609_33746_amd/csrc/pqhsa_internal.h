@@ -21,7 +21,7 @@ constexpr int kMaxSamples = 2048;  // sampled positions per row for the threshol
 constexpr int kSelThreads = 1024;
 constexpr int kSelCap = 12288;     // candidates of one row held in LDS by the select kernel
 constexpr int kSelMaxSub = 1024;   // sub-chunks per row on the select kernel's fast path
-constexpr int kSampleRun = 8;      // contiguous positions per sampled run
+constexpr int kSampleRun = 2;      // contiguous positions per sampled run
 constexpr int kPosBits = 20;       // candidate word: list id << kPosBits | position
 constexpr int kMaxSeq = 1 << kPosBits;
 constexpr int kAttnRows = 128;     // exact-set rows per split

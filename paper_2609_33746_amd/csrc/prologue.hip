@@ -44,7 +44,7 @@ constexpr int kLutF4 = kLutRow / 4 / kProThreads;          // float4 of a head t
 constexpr int kSpinLimit = 1 << 18;                        // polls before giving up (~0.3 s)
 static_assert(kFineWg * kKsub == kProThreads && kPqM % kFineWg == 0, "fine tiling");
 static_assert(kCoarsePer * kCoarseGroups == kCoarseLists, "coarse tiling");
-static_assert(kSamplesPer * kProThreads == kMaxSamples && kSampleRun % kSamplesPer == 0, "samples");
+static_assert(kSamplesPer * kProThreads == kMaxSamples && kMaxSamples % kSampleRun == 0, "samples");
 static_assert(kLutF4 * 4 * kProThreads == kLutRow, "head table staging");
 
 static_assert(kFineParts == kPqM / 2 && kCoarseLists == 128, "prologue_parts() counts these");
@@ -155,7 +155,10 @@ __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, 
         return;
     }
     // 1) the samples: runs of kSampleRun positions, rs apart (rs >= 1),
-    //    clipped at the next run; thread tid owns samples 4 tid .. 4 tid + 3
+    //    clipped at the next run; thread tid owns samples u * 512 + tid, so
+    //    neighbouring lanes read neighbouring positions (short runs: scores
+    //    within a list are correlated, so many short runs estimate the
+    //    quantile with far less spread than a few long ones)
     const int nrun = min(kMaxSamples / kSampleRun, (n_r + kSampleRun - 1) / kSampleRun);
     const int rs = n_r / nrun;
     const int run_len = min(kSampleRun, rs);
@@ -167,7 +170,7 @@ __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, 
     bool ok[kSamplesPer];
 #pragma unroll
     for (int u = 0; u < kSamplesPer; ++u) {
-        const int s = tid * kSamplesPer + u;
+        const int s = u * kProThreads + tid;
         const int run = s / kSampleRun;
         const int within = s % kSampleRun;
         const int pos = run * rs + within;
@@ -270,7 +273,12 @@ __global__ __launch_bounds__(kProThreads) void prologue_kernel(Dims D, BatchArgs
                        blockIdx.x % per_bg);
         return;
     }
-    sample_role<T, G>(D, ba, ix, w, bias, lut_target, blockIdx.x - n_lut_wg, sm);
+    // sample workgroup s serves group s % NG, head s / NG: workgroups are
+    // dispatched to the XCDs round-robin by id, so when the group count is a
+    // multiple of 8 the G rows of a group share one L2 and its sample loads
+    const int s_idx = blockIdx.x - n_lut_wg;
+    const int n_grp = D.B * D.Hkv;
+    sample_role<T, G>(D, ba, ix, w, bias, lut_target, (s_idx % n_grp) * G + s_idx / n_grp, sm);
 }
 
 template <typename T, int G>

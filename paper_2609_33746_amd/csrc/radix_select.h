@@ -42,7 +42,7 @@ __device__ __forceinline__ void hist_add(int* hist, uint32_t digit, bool active)
 // All NT threads of the workgroup must call this with the same n and c,
 // 1 <= c <= n.
 template <int NT, typename KeyAt, typename Keep>
-__device__ SelectResult block_select_desc(KeyAt key_at, Keep keep, int n, int c,
+__device__ __forceinline__ SelectResult block_select_desc(KeyAt key_at, Keep keep, int n, int c,
                                           SelectScratch& sh) {
     static_assert(NT >= 64, "needs at least one full wave");
     const int tid = threadIdx.x;
@@ -100,7 +100,7 @@ __device__ SelectResult block_select_desc(KeyAt key_at, Keep keep, int n, int c,
 // Exclusive prefix of a per-thread count over the workgroup (NT threads);
 // returns this thread's offset, writes the total to `total`.
 template <int NT>
-__device__ int block_excl_scan(int v, int& total, SelectScratch& sh) {
+__device__ __forceinline__ int block_excl_scan(int v, int& total, SelectScratch& sh) {
     constexpr int NW = NT / kWave;
     const int wave = threadIdx.x / kWave;
     const int incl = wave_incl_scan_i32(v);

@@ -28,7 +28,6 @@ namespace pqhsa {
 
 constexpr int kNW = kSelThreads / kWave;
 constexpr int kRankCap = 512;          // boundary-bin keys ranked exactly
-constexpr int kCopyPer = 4;            // candidates a thread loads at once
 constexpr uint32_t kPosMask = (1u << kPosBits) - 1u;
 constexpr float kMassScale = 1099511627776.0f;       // 2^40: fixed-point weights
 constexpr float kMassUnscale = 1.0f / 1099511627776.0f;
@@ -127,6 +126,50 @@ constexpr int kOffCounter = kOffBits + kSelCap / 32;
 constexpr int kOffPre = kOffCounter + 4;
 constexpr size_t kSelLdsWords = kOffPre + kSelMaxSub;
 constexpr size_t kSelLdsBytes = kSelLdsWords * 4;
+
+// Copy the row's `total` candidates (total <= N * kSelThreads) from their
+// sub-chunk slots into LDS in position order: keys at lds[i], candidate
+// words at lds[kOffCand + i]. Candidate i lives in the sub-chunk sc with
+// pre[sc] <= i < pre[sc + 1] (the last of equal offsets, so empty sub-chunks
+// never match). Every thread searches all of its N indices together and
+// issues all N loads before using any, so the copy costs one search chain
+// and one memory round trip (indices past the end repeat the last
+// candidate's load). Tracks the min / max key of this thread. total >= 1.
+template <int N>
+__device__ __forceinline__ void copy_candidates(const uint2* __restrict__ cand, const int* pre,
+                                                int nsub, int total, uint32_t* lds,
+                                                uint32_t& kmin, uint32_t& kmax) {
+    const int tid = threadIdx.x;
+    int cs[N];
+#pragma unroll
+    for (int u = 0; u < N; ++u) {
+        const int ci = min(u * kSelThreads + tid, total - 1);
+        int c = 0;
+#pragma unroll
+        for (int step = kSelMaxSub / 2; step > 0; step >>= 1) {
+            const int t = c + step;
+            if (t < nsub && pre[t] <= ci) c = t;
+        }
+        cs[u] = c;
+    }
+    uint2 rec[N];
+#pragma unroll
+    for (int u = 0; u < N; ++u) {
+        const int slot = min(u * kSelThreads + tid, total - 1) - pre[cs[u]];   // in [0, count)
+        rec[u] = cand[static_cast<int64_t>(cs[u]) * kSub + slot];
+    }
+#pragma unroll
+    for (int u = 0; u < N; ++u) {
+        const int ci = u * kSelThreads + tid;
+        if (ci < total) {
+            const uint32_t kk = float_key(__uint_as_float(rec[u].x));
+            lds[ci] = kk;
+            lds[kOffCand + ci] = rec[u].y;
+            kmin = min(kmin, kk);
+            kmax = max(kmax, kk);
+        }
+    }
+}
 
 // Emit T in candidate order (each thread owns a contiguous range of candidate
 // indices) and the per-list sums of exp(l~ - shift) over the unselected
@@ -243,42 +286,13 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchArgs b
         auto KEY = [&](int i) { return lds[i]; };
         auto CAND = [&](int i) { return lds[kOffCand + i]; };
         uint32_t kmin = 0xffffffffu, kmax = 0u, kcount = 0u;
-        // candidate i lives in the sub-chunk sc with pre[sc] <= i < pre[sc + 1]
-        // (the last of equal offsets: empty sub-chunks never match); every
-        // thread loads a few candidates, all loads issued before any is used
         const uint2* cand = w.cand + rbase;
-        for (int i0 = 0; i0 < total; i0 += kCopyPer * kSelThreads) {
-            int ci[kCopyPer], cs[kCopyPer];
-#pragma unroll
-            for (int u = 0; u < kCopyPer; ++u) {
-                ci[u] = i0 + u * kSelThreads + tid;
-                cs[u] = 0;
-            }
-#pragma unroll
-            for (int step = kSelMaxSub / 2; step > 0; step >>= 1) {
-#pragma unroll
-                for (int u = 0; u < kCopyPer; ++u) {
-                    const int t = cs[u] + step;
-                    if (t < nsub && pre[t] <= ci[u]) cs[u] = t;
-                }
-            }
-            uint2 rec[kCopyPer];
-#pragma unroll
-            for (int u = 0; u < kCopyPer; ++u) {
-                const int slot = min(ci[u], total - 1) - pre[cs[u]];
-                rec[u] = cand[static_cast<int64_t>(cs[u]) * kSub + slot];
-            }
-#pragma unroll
-            for (int u = 0; u < kCopyPer; ++u) {
-                if (ci[u] < total) {
-                    const uint32_t kk = float_key(__uint_as_float(rec[u].x));
-                    lds[ci[u]] = kk;
-                    lds[kOffCand + ci[u]] = rec[u].y;
-                    kmin = min(kmin, kk);
-                    kmax = max(kmax, kk);
-                }
-            }
-        }
+        if (total > 8 * kSelThreads)
+            copy_candidates<kSelCap / kSelThreads>(cand, pre, nsub, total, lds, kmin, kmax);
+        else if (total > 4 * kSelThreads)
+            copy_candidates<8>(cand, pre, nsub, total, lds, kmin, kmax);
+        else if (total > 0)
+            copy_candidates<4>(cand, pre, nsub, total, lds, kmin, kmax);
         block_min_max_count<kSelThreads>(kmin, kmax, kcount, bs);
         if (k == 0) {
             shift = total > 0 ? key_float(kmax) : neg_inf;
