@@ -125,7 +125,9 @@ pqhsa_status pqhsa_decode(pqhsa_ctx* ctx, const void* q, const void* k_cache,
  *   scores              float [B, Hq, Nmax] or NULL: the approximate logit of
  *                       Eq. 2 for every token of R_b by token id, NaN
  *                       elsewhere (computed by the same device code as the
- *                       scan) */
+ *                       scan)
+ * Returns PQHSA_ERR_UNSUPPORTED when selected or unselected_per_list is
+ * requested and some k_b exceeds 8192. */
 pqhsa_status pqhsa_decode_debug(pqhsa_ctx* ctx, const void* q, const void* k_cache,
                                 const void* v_cache, const int64_t* kv_strides,
                                 const int32_t* topk, float* out, int32_t* selected,

@@ -39,7 +39,7 @@ struct pqhsa_ctx {
     uint8_t* codes = nullptr;
     float* norms = nullptr;
     int32_t* perm = nullptr;
-    int32_t* pos_list = nullptr;
+    uint32_t* pos_word = nullptr;
     int32_t* loff = nullptr;
     float* centroids = nullptr;
     float* codebooks = nullptr;
@@ -68,7 +68,7 @@ struct pqhsa_ctx {
         ix.codes = codes;
         ix.norms = norms;
         ix.perm = perm;
-        ix.pos_list = pos_list;
+        ix.pos_word = pos_word;
         ix.loff = loff;
         ix.centroids = centroids;
         ix.codebooks = codebooks;
@@ -247,7 +247,7 @@ pqhsa_status pqhsa_create(const pqhsa_shape* shape, pqhsa_ctx** out) {
     A(dev_alloc(c, &c->codes, BG * rc * kPqM));
     A(dev_alloc(c, &c->norms, BG * rc));
     A(dev_alloc(c, &c->perm, BG * rc));
-    A(dev_alloc(c, &c->pos_list, BG * rc));
+    A(dev_alloc(c, &c->pos_word, BG * rc));
     A(dev_alloc(c, &c->loff, BG * (L + 1)));
     A(dev_alloc(c, &c->centroids, BG * L * kHeadDim));
     A(dev_alloc(c, &c->codebooks, BG * kPqM * kKsub * kDsub));
@@ -265,7 +265,7 @@ pqhsa_status pqhsa_create(const pqhsa_shape* shape, pqhsa_ctx** out) {
     A(dev_alloc(c, &w.seg_sum, BG * D.nseg_cap * G));
     A(dev_alloc(c, &w.comp_key, BQ * rc));
     A(dev_alloc(c, &w.comp_pos, BQ * rc));
-    A(dev_alloc(c, &w.sel_pos, BQ * D.max_topk));
+    A(dev_alloc(c, &w.sel_tok, BQ * D.max_topk));
     A(dev_alloc(c, &w.cand_mass, BQ * L));
     A(dev_alloc(c, &w.row_shift, BQ));
     A(dev_alloc(c, &w.row_flag, BQ));
@@ -313,7 +313,8 @@ pqhsa_status pqhsa_index_prepare(pqhsa_ctx* c, const int32_t* seq_lens, const in
     if (e != hipSuccess) return hip_fail(c, e, "copying list ids to the host");
 
     // stable counting sort of R_b by list id, per (b, kv head)
-    std::vector<int32_t> perm(BG * rc, -1), pos_list(BG * rc, 0), loff(BG * (L + 1));
+    std::vector<int32_t> perm(BG * rc, -1), loff(BG * (L + 1));
+    std::vector<uint32_t> pos_word(BG * rc, 0u);
     std::vector<int32_t> cnt(L);
     for (int b = 0; b < B; ++b) {
         for (int g = 0; g < Hkv; ++g) {
@@ -331,11 +332,11 @@ pqhsa_status pqhsa_index_prepare(pqhsa_ctx* c, const int32_t* seq_lens, const in
             for (int j = 0; j < L; ++j) lo[j + 1] = lo[j] + cnt[j];
             std::vector<int32_t> fillp(lo, lo + L);
             int32_t* pm = perm.data() + bg * rc;
-            int32_t* pl = pos_list.data() + bg * rc;
+            uint32_t* pw = pos_word.data() + bg * rc;
             for (int i = D.n_sink; i < D.n_sink + nr[b]; ++i) {
                 const int p = fillp[a[i]]++;
                 pm[p] = i;
-                pl[p] = a[i];
+                pw[p] = (static_cast<uint32_t>(a[i]) << kPosBits) | static_cast<uint32_t>(i);
             }
         }
     }
@@ -347,7 +348,7 @@ pqhsa_status pqhsa_index_prepare(pqhsa_ctx* c, const int32_t* seq_lens, const in
         if (e == hipSuccess) e = hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDevice, stream);
     };
     H2D(c->perm, perm.data(), perm.size() * 4);
-    H2D(c->pos_list, pos_list.data(), pos_list.size() * 4);
+    H2D(c->pos_word, pos_word.data(), pos_word.size() * 4);
     H2D(c->loff, loff.data(), loff.size() * 4);
     H2D(c->n_seq_dev, lens.data(), B * 4);
     H2D(c->n_r_dev, nr.data(), B * 4);
@@ -432,7 +433,7 @@ pqhsa_status pqhsa_decode_debug(pqhsa_ctx* c, const void* q, const void* k, cons
                                 const int64_t* kv_strides, const int32_t* topk, float* out,
                                 int32_t* selected, int32_t* unselected_per_list, float* scores,
                                 hipStream_t stream) {
-    if (c && selected && topk) {
+    if (c && (selected || unselected_per_list) && topk) {
         for (int b = 0; b < c->D.B; ++b)
             if (topk[b] > 8192)
                 return fail(c, PQHSA_ERR_UNSUPPORTED, "the debug call sorts at most 8192 selected tokens per row");

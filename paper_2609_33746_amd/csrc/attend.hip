@@ -131,15 +131,8 @@ __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchArgs 
         const int e0 = split * kAttnRows;
         if (e0 >= nE) return;   // the merge reads only the splits that exist
         const int e1 = min(e0 + kAttnRows, nE);
-        const int32_t* sel = w.sel_pos + static_cast<int64_t>(row) * D.max_topk;
-        const int32_t* perm = ix.perm + static_cast<int64_t>(b * D.Hkv + g) * D.rcap;
+        const int32_t* sel = w.sel_tok + static_cast<int64_t>(row) * D.max_topk;
         const int local0 = n_seq - D.n_local;
-        int pos[kRowsPerStream];
-#pragma unroll
-        for (int i = 0; i < kRowsPerStream; ++i) {
-            const int e = e0 + stream + i * kStreams - D.n_sink - D.n_local;
-            pos[i] = (e >= 0 && e + D.n_sink + D.n_local < e1) ? sel[e] : -1;
-        }
         int tok[kRowsPerStream];
 #pragma unroll
         for (int i = 0; i < kRowsPerStream; ++i) {
@@ -148,7 +141,7 @@ __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchArgs 
             if (e < e1) {
                 if (e < D.n_sink) t = e;
                 else if (e < D.n_sink + D.n_local) t = local0 + (e - D.n_sink);
-                else t = perm[min(max(pos[i], 0), n_r - 1)];   // never outside R
+                else t = min(max(sel[e - D.n_sink - D.n_local], D.n_sink), local0 - 1);   // never outside R
             }
             tok[i] = t;
         }

@@ -22,7 +22,8 @@ constexpr int kSelThreads = 1024;
 constexpr int kSelCap = 12288;     // candidates of one row held in LDS by the select kernel
 constexpr int kSelMaxSub = 1024;   // sub-chunks per row on the select kernel's fast path
 constexpr int kSampleRun = 2;      // contiguous positions per sampled run
-constexpr int kPosBits = 20;       // candidate word: list id << kPosBits | position
+constexpr int kPosBits = 20;       // position / candidate word: list id << kPosBits | token id
+constexpr uint32_t kPosMask = (1u << kPosBits) - 1u;
 constexpr int kMaxSeq = 1 << kPosBits;
 constexpr int kAttnRows = 128;     // exact-set rows per split
 constexpr int kBgLists = 64;       // lists per background workgroup
@@ -58,7 +59,7 @@ struct Index {
     const uint8_t* codes;      // [B, Hkv, rcap, M]
     const float* norms;        // [B, Hkv, rcap]
     const int32_t* perm;       // [B, Hkv, rcap] token id of each position
-    const int32_t* pos_list;   // [B, Hkv, rcap] list id of each position
+    const uint32_t* pos_word;  // [B, Hkv, rcap] list id << kPosBits | token id of each position
     const int32_t* loff;       // [B, Hkv, n_list + 1] list starts
     const float* centroids;    // [B, Hkv, n_list, d]
     const float* codebooks;    // [B, Hkv, M, K, d/M]
@@ -81,7 +82,7 @@ struct Work {
                          //   (list j, sub-chunk s) uses segment j + s
     uint32_t* comp_key;  // [B, Hq, rcap] contiguous candidates (order keys)
     int32_t* comp_pos;   // [B, Hq, rcap] (same packing as the candidate word)
-    int32_t* sel_pos;    // [B, Hq, max_topk] list-major positions of T
+    int32_t* sel_tok;    // [B, Hq, max_topk] token ids of T
     float* cand_mass;    // [B, Hq, n_list] sum over the list's unselected candidates of
                          //   exp(l~ - shift)
     float* row_shift;    // [B, Hq] shift of the background masses

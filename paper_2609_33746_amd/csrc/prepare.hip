@@ -63,8 +63,9 @@ __global__ __launch_bounds__(kDbgThreads) void score_dump_kernel(Dims D, Index i
          pos += gridDim.x * kDbgThreads) {
         float fs[1];
         fine_sum<1>(lut_s, codes[pos], fs);
-        const float s = pq_logit(ix.norms[base + pos], coarse[ix.pos_list[base + pos] * D.G + hh], fs[0]);
-        scores[row * out_stride + ix.perm[base + pos]] = s;
+        const uint32_t wd = ix.pos_word[base + pos];
+        const float s = pq_logit(ix.norms[base + pos], coarse[(wd >> kPosBits) * D.G + hh], fs[0]);
+        scores[row * out_stride + (wd & kPosMask)] = s;
     }
 }
 
@@ -80,38 +81,50 @@ __global__ __launch_bounds__(kDbgThreads) void sel_debug_kernel(Dims D, BatchArg
     const int g = (row % D.Hq) / D.G;
     const int bg = b * D.Hkv + g;
     const int k = ba.topk[b];
-    const int32_t* sp = w.sel_pos + static_cast<int64_t>(row) * D.max_topk;
+    const int32_t* st = w.sel_tok + static_cast<int64_t>(row) * D.max_topk;
     const int64_t base = static_cast<int64_t>(bg) * D.rcap;
-    if (selected) {
-        int n2 = 1;
-        while (n2 < k) n2 <<= 1;
-        for (int i = threadIdx.x; i < n2; i += kDbgThreads)
-            keys[i] = i < k ? ix.perm[base + sp[i]] : 0x7fffffff;
-        __syncthreads();
-        for (int size = 2; size <= n2; size <<= 1) {
-            for (int stride = size >> 1; stride > 0; stride >>= 1) {
-                for (int i = threadIdx.x; i < n2; i += kDbgThreads) {
-                    const int j = i ^ stride;
-                    if (j > i) {
-                        const bool up = (i & size) == 0;
-                        const int a = keys[i], c = keys[j];
-                        if ((a > c) == up) {
-                            keys[i] = c;
-                            keys[j] = a;
-                        }
+    // the selected token ids, sorted (both outputs use them)
+    int n2 = 1;
+    while (n2 < k) n2 <<= 1;
+    for (int i = threadIdx.x; i < n2; i += kDbgThreads) keys[i] = i < k ? st[i] : 0x7fffffff;
+    __syncthreads();
+    for (int size = 2; size <= n2; size <<= 1) {
+        for (int stride = size >> 1; stride > 0; stride >>= 1) {
+            for (int i = threadIdx.x; i < n2; i += kDbgThreads) {
+                const int j = i ^ stride;
+                if (j > i) {
+                    const bool up = (i & size) == 0;
+                    const int a = keys[i], c = keys[j];
+                    if ((a > c) == up) {
+                        keys[i] = c;
+                        keys[j] = a;
                     }
                 }
-                __syncthreads();
             }
+            __syncthreads();
         }
+    }
+    if (selected) {
         int32_t* out = selected + static_cast<int64_t>(row) * D.max_topk;
         for (int i = threadIdx.x; i < D.max_topk; i += kDbgThreads) out[i] = i < k ? keys[i] : -1;
     }
     if (unselected) {
+        // a position is selected when its token id is among the sorted keys
         const int32_t* loff = ix.loff + static_cast<int64_t>(bg) * (D.n_list + 1);
         for (int j = threadIdx.x; j < D.n_list; j += kDbgThreads) counts[j] = loff[j + 1] - loff[j];
         __syncthreads();
-        for (int i = threadIdx.x; i < k; i += kDbgThreads) atomicSub(&counts[ix.pos_list[base + sp[i]]], 1);
+        const int n_r = ba.n_r[b];
+        for (int pos = threadIdx.x; pos < n_r; pos += kDbgThreads) {
+            const uint32_t wd = ix.pos_word[base + pos];
+            const int tok = static_cast<int>(wd & kPosMask);
+            int lo = 0, hi = k;   // first key >= tok
+            while (lo < hi) {
+                const int mid = (lo + hi) >> 1;
+                if (keys[mid] < tok) lo = mid + 1;
+                else hi = mid;
+            }
+            if (lo < k && keys[lo] == tok) atomicSub(&counts[wd >> kPosBits], 1);
+        }
         __syncthreads();
         int32_t* out = unselected + static_cast<int64_t>(row) * D.n_list;
         for (int j = threadIdx.x; j < D.n_list; j += kDbgThreads) out[j] = counts[j];

@@ -178,7 +178,7 @@ __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, 
         const int p = ok[u] ? pos : 0;
         cv[u] = codes[p];
         rv[u] = ix.norms[base + p];
-        jv[u] = ix.pos_list[base + p];
+        jv[u] = static_cast<int>(ix.pos_word[base + p] >> kPosBits);
     }
     for (int i = tid; i < kHistBins; i += kProThreads) sm.hist[i] = 0;
 

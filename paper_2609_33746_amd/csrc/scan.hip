@@ -17,7 +17,7 @@
 // coarse terms instead.
 //
 // Per token and head the wave computes l~ and then either
-//   * emits (l~, list id and position) as a top-k candidate when
+//   * emits (l~, list id and token id) as a top-k candidate when
 //     l~ >= tau_lo (the sampled threshold of its row), compacted in position
 //     order at the start of the sub-chunk's own region of the row's candidate
 //     buffer, or
@@ -136,18 +136,18 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(Dims D, BatchArgs ba
     //    into R_b, so every load is in bounds), issued in the order the steps
     //    use them, after the tables: each step waits only for its own data
     const uint4* codes = reinterpret_cast<const uint4*>(ix.codes) + base;
-    int jl[kIters];
+    uint32_t wl[kIters];   // list id << kPosBits | token id
     uint4 cv[kIters];
     float rv[kIters];
 #pragma unroll
     for (int it = 0; it < kIters; ++it) {
         const int p = min(p_begin + it * kWave + lane, n_r - 1);
-        jl[it] = ix.pos_list[base + p];
+        wl[it] = ix.pos_word[base + p];
         cv[it] = codes[p];
         rv[it] = ix.norms[base + p];
     }
     float* segs = w.seg_sum + (static_cast<int64_t>(bg) * D.nseg_cap + sc) * G;   // + j * G
-    int cur = __builtin_amdgcn_readfirstlane(jl[0]);   // list of the open segment
+    int cur = __builtin_amdgcn_readfirstlane(static_cast<int>(wl[0] >> kPosBits));   // open segment's list
     float acc[G];
     int cbase[G];
 #pragma unroll
@@ -161,9 +161,10 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(Dims D, BatchArgs ba
         const bool valid = p < p_end;
         // coarse terms of the lanes' lists: from LDS, or gathered when the
         // coarse table does not fit beside the LUT
+        const int j = static_cast<int>(wl[it] >> kPosBits);
         float cf[G];
-        if constexpr (kCoarseLds) load_coarse<G>(coarse_s + jl[it] * G, cf);
-        else load_coarse<G>(coarse + jl[it] * G, cf);
+        if constexpr (kCoarseLds) load_coarse<G>(coarse_s + j * G, cf);
+        else load_coarse<G>(coarse + j * G, cf);
         float fs[G];
         fine_sum<G>(lut_s, cv[it], fs);
         float s[G], e[G];
@@ -174,7 +175,6 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(Dims D, BatchArgs ba
         }
         // close the lists that end inside this step (lists are contiguous and
         // ascending along the lanes)
-        const int j = jl[it];
         const int j_last = __builtin_amdgcn_readlane(j, min(p_end - p_first, kWave) - 1);
         while (cur != j_last) {
             const bool in = valid && j == cur;
@@ -197,9 +197,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(Dims D, BatchArgs ba
                 if ((mask >> lane) & 1ull) {
                     const int64_t o = static_cast<int64_t>(row0 + hh) * D.rcap + p_begin +
                                       cbase[hh] + lanes_below(mask);
-                    w.cand[o] = make_uint2(__float_as_uint(s[hh]),
-                                           (static_cast<uint32_t>(j) << kPosBits) |
-                                               static_cast<uint32_t>(p));
+                    w.cand[o] = make_uint2(__float_as_uint(s[hh]), wl[it]);
                 }
                 cbase[hh] += __popcll(mask);
             }

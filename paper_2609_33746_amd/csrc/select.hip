@@ -28,7 +28,6 @@ namespace pqhsa {
 
 constexpr int kNW = kSelThreads / kWave;
 constexpr int kRankCap = 512;          // boundary-bin keys ranked exactly
-constexpr uint32_t kPosMask = (1u << kPosBits) - 1u;
 constexpr float kMassScale = 1099511627776.0f;       // 2^40: fixed-point weights
 constexpr float kMassUnscale = 1.0f / 1099511627776.0f;
 
@@ -127,14 +126,16 @@ constexpr int kOffPre = kOffCounter + 4;
 constexpr size_t kSelLdsWords = kOffPre + kSelMaxSub;
 constexpr size_t kSelLdsBytes = kSelLdsWords * 4;
 
-// Copy the row's `total` candidates (total <= N * kSelThreads) from their
-// sub-chunk slots into LDS in position order: keys at lds[i], candidate
-// words at lds[kOffCand + i]. Candidate i lives in the sub-chunk sc with
-// pre[sc] <= i < pre[sc + 1] (the last of equal offsets, so empty sub-chunks
-// never match). Every thread searches all of its N indices together and
-// issues all N loads before using any, so the copy costs one search chain
-// and one memory round trip (indices past the end repeat the last
-// candidate's load). Tracks the min / max key of this thread. total >= 1.
+// Copy the row's `total` candidates (1 <= total <= N * kSelThreads) from
+// their sub-chunk slots into LDS in position order: keys at lds[i], words
+// (list << kPosBits | token) at lds[kOffCand + i]. Thread t copies the
+// indices u * kSelThreads + t, so neighbouring lanes read neighbouring
+// slots. Candidate i lives in the sub-chunk sc with pre[sc] <= i < pre[sc + 1]
+// (the last of equal offsets, so empty sub-chunks never match). Every thread
+// searches all of its indices together and issues all loads before using
+// any, so the copy costs one search chain and one memory round trip
+// (indices past the end repeat the last candidate's load). Tracks this
+// thread's min / max key.
 template <int N>
 __device__ __forceinline__ void copy_candidates(const uint2* __restrict__ cand, const int* pre,
                                                 int nsub, int total, uint32_t* lds,
@@ -171,15 +172,16 @@ __device__ __forceinline__ void copy_candidates(const uint2* __restrict__ cand, 
     }
 }
 
-// Emit T in candidate order (each thread owns a contiguous range of candidate
-// indices) and the per-list sums of exp(l~ - shift) over the unselected
-// candidates (candidates are in list-major order, so a thread adds one
-// partial per run of equal list ids).
+// Emit T as token ids in candidate order (each thread owns a contiguous
+// range of candidate indices) and the per-list sums of exp(l~ - shift) over
+// the unselected candidates (candidates are in list-major order, so a thread
+// adds one partial per run of equal list ids).
 template <typename KeyAt, typename CandAt, typename IsSel>
-__device__ __forceinline__ void emit_selection(KeyAt key_at, CandAt cand_at, IsSel is_sel, int total,
-                                               int k, int n_list, float shift,
-                                               unsigned long long* mass, int32_t* sel_pos,
-                                               float* cand_mass, SelectScratch& ss) {
+__device__ __forceinline__ void emit_selection(KeyAt key_at, CandAt cand_at, IsSel is_sel,
+                                               int total, int k, int n_list,
+                                               float shift, unsigned long long* mass,
+                                               int32_t* sel_tok, float* cand_mass,
+                                               SelectScratch& ss) {
     const int tid = threadIdx.x;
     const int eper = (total + kSelThreads - 1) / kSelThreads;
     const int e0 = min(tid * eper, total);
@@ -200,7 +202,7 @@ __device__ __forceinline__ void emit_selection(KeyAt key_at, CandAt cand_at, IsS
             run_list = lst;
         }
         if (is_sel(i, key, cand)) {
-            if (o < k) sel_pos[o] = static_cast<int32_t>(cand & kPosMask);
+            if (o < k) sel_tok[o] = static_cast<int32_t>(cand & kPosMask);
             ++o;
         } else {
             run += static_cast<unsigned long long>(__expf(key_float(key) - shift) * kMassScale);
@@ -239,8 +241,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchArgs b
     const int nsub = (n_r + kSub - 1) / kSub;
     const int64_t rbase = static_cast<int64_t>(row) * D.rcap;
     const int64_t base = static_cast<int64_t>(bg) * D.rcap;
-    const int32_t* perm = ix.perm + base;
-    int32_t* sel_pos = w.sel_pos + static_cast<int64_t>(row) * D.max_topk;
+    int32_t* sel_tok = w.sel_tok + static_cast<int64_t>(row) * D.max_topk;
     float* cand_mass = w.cand_mass + static_cast<int64_t>(row) * D.n_list;
     const float neg_inf = -__builtin_huge_valf();
 
@@ -294,10 +295,11 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchArgs b
         else if (total > 0)
             copy_candidates<4>(cand, pre, nsub, total, lds, kmin, kmax);
         block_min_max_count<kSelThreads>(kmin, kmax, kcount, bs);
+        auto TOK = [&](int i) { return static_cast<int>(CAND(i) & kPosMask); };
         if (k == 0) {
             shift = total > 0 ? key_float(kmax) : neg_inf;
             emit_selection(KEY, CAND, [](int, uint32_t, uint32_t) { return false; }, total, 0,
-                           D.n_list, shift, mass, sel_pos, cand_mass, ss);
+                           D.n_list, shift, mass, sel_tok, cand_mass, ss);
         } else {
             const int sh = bin_shift(kmin, kmax);
             for (int i0 = 0; i0 < total; i0 += kSelThreads) {
@@ -309,9 +311,9 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchArgs b
             int above = 0;
             const int bstar = block_find_bin_desc<kSelThreads>(hist, k, above, ss, bs);
             uint32_t kth = 0u;
-            const bool by_rank = rank_boundary_bin(
-                KEY, [&](int i) { return perm[CAND(i) & kPosMask]; }, total, kmin, sh, bstar,
-                hist[bstar], k - above, r_key, r_idx, r_tok, counter, counter + 1, chosen, kth, bs);
+            const bool by_rank = rank_boundary_bin(KEY, TOK, total, kmin, sh, bstar, hist[bstar],
+                                                   k - above, r_key, r_idx, r_tok, counter,
+                                                   counter + 1, chosen, kth, bs);
             if (by_rank) {
                 shift = key_float(kth);   // the k-th largest score
                 emit_selection(
@@ -320,7 +322,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchArgs b
                         const int bn = static_cast<int>((key - kmin) >> sh);
                         return bn > bstar || (bn == bstar && ((chosen[i >> 5] >> (i & 31)) & 1u));
                     },
-                    total, k, D.n_list, shift, mass, sel_pos, cand_mass, ss);
+                    total, k, D.n_list, shift, mass, sel_tok, cand_mass, ss);
             } else {
                 // very dense boundary bin: radix select
                 const SelectResult r = block_select_desc<kSelThreads>(
@@ -330,17 +332,17 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchArgs b
                 int tok_cut = 0x7fffffff;
                 if (r.count_equal > need_r) {
                     const SelectResult t = block_select_desc<kSelThreads>(
-                        [&](int i) { return ~static_cast<uint32_t>(perm[CAND(i) & kPosMask]); },
+                        [&](int i) { return ~static_cast<uint32_t>(TOK(i)); },
                         [&](int i) { return KEY(i) == kk; }, total, need_r, ss);
                     tok_cut = static_cast<int>(~t.key);
                 }
                 shift = key_float(kk);
                 emit_selection(
                     KEY, CAND,
-                    [&](int, uint32_t key, uint32_t cand) {
-                        return key > kk || (key == kk && perm[cand & kPosMask] <= tok_cut);
+                    [&](int, uint32_t key, uint32_t cw) {
+                        return key > kk || (key == kk && static_cast<int>(cw & kPosMask) <= tok_cut);
                     },
-                    total, k, D.n_list, shift, mass, sel_pos, cand_mass, ss);
+                    total, k, D.n_list, shift, mass, sel_tok, cand_mass, ss);
             }
         }
     } else {
@@ -369,13 +371,13 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchArgs b
             const uint4* codes = reinterpret_cast<const uint4*>(ix.codes) + base;
             const float* coarse = w.coarse + static_cast<int64_t>(bg) * D.n_list * D.G;
             for (int pos = tid; pos < n_r; pos += kSelThreads) {
-                const int j = ix.pos_list[base + pos];
+                const uint32_t wd = ix.pos_word[base + pos];
+                const int j = static_cast<int>(wd >> kPosBits);
                 float fs[1];
                 fine_sum<1>(lut_s, codes[pos], fs);
                 const float sc = pq_logit(ix.norms[base + pos], coarse[j * D.G + hh], fs[0]);
                 w.comp_key[rbase + pos] = float_key(sc);
-                w.comp_pos[rbase + pos] = static_cast<int32_t>(
-                    (static_cast<uint32_t>(j) << kPosBits) | static_cast<uint32_t>(pos));
+                w.comp_pos[rbase + pos] = static_cast<int32_t>(wd);
             }
             total = n_r;
         }
@@ -387,7 +389,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchArgs b
         if (total == 0) {
             shift = neg_inf;
             emit_selection(KEY, CAND, [](int, uint32_t, uint32_t) { return false; }, 0, 0,
-                           D.n_list, shift, mass, sel_pos, cand_mass, ss);
+                           D.n_list, shift, mass, sel_tok, cand_mass, ss);
         } else {
             const SelectResult r = block_select_desc<kSelThreads>(
                 KEY, [](int) { return true; }, total, k > 0 ? k : 1, ss);
@@ -395,7 +397,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchArgs b
             int tok_cut = 0x7fffffff;
             if (k > 0 && r.count_equal > k - r.count_above) {
                 const SelectResult t = block_select_desc<kSelThreads>(
-                    [&](int i) { return ~static_cast<uint32_t>(perm[ccand[i] & kPosMask]); },
+                    [&](int i) { return ~(ccand[i] & kPosMask); },
                     [&](int i) { return ckey[i] == kth; }, total, k - r.count_above, ss);
                 tok_cut = static_cast<int>(~t.key);
             }
@@ -403,9 +405,9 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchArgs b
             emit_selection(
                 KEY, CAND,
                 [&](int, uint32_t key, uint32_t cand) {
-                    return k > 0 && (key > kth || (key == kth && perm[cand & kPosMask] <= tok_cut));
+                    return k > 0 && (key > kth || (key == kth && static_cast<int>(cand & kPosMask) <= tok_cut));
                 },
-                total, k, D.n_list, shift, mass, sel_pos, cand_mass, ss);
+                total, k, D.n_list, shift, mass, sel_tok, cand_mass, ss);
         }
     }
     if (tid == 0) {
