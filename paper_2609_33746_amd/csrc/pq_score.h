@@ -12,30 +12,33 @@ namespace pqhsa {
 // LUT layout in LDS: [M][K][G] floats, entry (m, z, hh) = (q_hh^(m) . p_{m,z}) / sqrt(d)
 // for the G query heads of one KV head. `stride` is G for the group LUT or 1 for a
 // single head's slice. fs[hh] = sum over m (in order m = 0..M-1) of the entries.
+// The first entry initialises the sums (no 0 + x). With the table at a
+// compile-time LDS address, each entry address is one byte-select shift.
 template <int G>
 __device__ __forceinline__ void fine_sum(const float* __restrict__ lut, const uint4 c,
                                          float (&fs)[G]) {
-#pragma unroll
-    for (int hh = 0; hh < G; ++hh) fs[hh] = 0.0f;
     const uint32_t w[4] = {c.x, c.y, c.z, c.w};
 #pragma unroll
     for (int m = 0; m < kPqM; ++m) {
         const uint32_t z = (w[m >> 2] >> (8 * (m & 3))) & 0xffu;
         const float* e = lut + (m * kKsub + static_cast<int>(z)) * G;
+        float v[G];
         if constexpr (G == 8) {
             const float4 a = *reinterpret_cast<const float4*>(e);
             const float4 b = *reinterpret_cast<const float4*>(e + 4);
-            fs[0] += a.x; fs[1] += a.y; fs[2] += a.z; fs[3] += a.w;
-            fs[4] += b.x; fs[5] += b.y; fs[6] += b.z; fs[7] += b.w;
+            v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+            v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
         } else if constexpr (G == 4) {
             const float4 a = *reinterpret_cast<const float4*>(e);
-            fs[0] += a.x; fs[1] += a.y; fs[2] += a.z; fs[3] += a.w;
+            v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
         } else if constexpr (G == 2) {
             const float2 a = *reinterpret_cast<const float2*>(e);
-            fs[0] += a.x; fs[1] += a.y;
+            v[0] = a.x; v[1] = a.y;
         } else {
-            fs[0] += e[0];
+            v[0] = e[0];
         }
+#pragma unroll
+        for (int hh = 0; hh < G; ++hh) fs[hh] = m == 0 ? v[hh] : fs[hh] + v[hh];
     }
 }
 

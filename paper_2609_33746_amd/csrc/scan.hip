@@ -82,9 +82,13 @@ __device__ __forceinline__ void flush_segment(float* seg_row, float (&acc)[G]) {
 template <int G, bool kCoarseLds>
 __global__ __launch_bounds__(kScanThreads) void scan_kernel(Dims D, BatchArgs ba, Index ix, Work w,
                                                             int nwg) {
-    // [M][K][G] group LUT, then (when it fits) the [n_list][G] coarse table
-    extern __shared__ float lut_s[];
-    float* coarse_s = lut_s + kLutRow * G;
+    // [M][K][G] group LUT at a compile-time LDS address (so that an entry
+    // address is one shift of a code byte), then, when it fits, the
+    // [n_list][G] coarse table in the dynamic part
+    __shared__ float4 lut4[kLutRow * G / 4];
+    extern __shared__ float4 coarse4[];
+    float* lut_s = reinterpret_cast<float*>(lut4);
+    float* coarse_s = reinterpret_cast<float*>(coarse4);
     const int bg = blockIdx.x / nwg;
     const int b = bg / D.Hkv;
     const int g = bg % D.Hkv;
@@ -216,29 +220,29 @@ constexpr size_t kScanLdsMax = 160 * 1024;   // LDS of one workgroup on gfx950
 template <int G>
 static hipError_t launch_scan_t(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w,
                                 int nwg, hipStream_t s) {
-    const size_t lut = static_cast<size_t>(kLutRow) * G * sizeof(float);
     const size_t cf = static_cast<size_t>(kCoarseCapF4<G>) * 16;
     static_assert(kLutRow * G * 4 + kCoarseCapF4<G> * 16 <= kScanLdsMax, "LDS budget");
     const dim3 grid(D.B * D.Hkv * nwg);
     if (D.n_list * G % 4 == 0 && D.n_list * G / 4 <= kCoarseCapF4<G>)
-        hipLaunchKernelGGL((scan_kernel<G, true>), grid, dim3(kScanThreads), lut + cf, s, D, ba, ix,
-                           w, nwg);
+        hipLaunchKernelGGL((scan_kernel<G, true>), grid, dim3(kScanThreads), cf, s, D, ba, ix, w,
+                           nwg);
     else
-        hipLaunchKernelGGL((scan_kernel<G, false>), grid, dim3(kScanThreads), lut, s, D, ba, ix, w,
+        hipLaunchKernelGGL((scan_kernel<G, false>), grid, dim3(kScanThreads), 0, s, D, ba, ix, w,
                            nwg);
     return hipGetLastError();
 }
 
 hipError_t configure_scan() {
-    // the group LUT plus the coarse table can exceed the default dynamic LDS limit
+    // the coarse table (dynamic) can exceed the default dynamic LDS limit
     const void* k[] = {reinterpret_cast<const void*>(&scan_kernel<1, true>),
                        reinterpret_cast<const void*>(&scan_kernel<2, true>),
                        reinterpret_cast<const void*>(&scan_kernel<4, true>),
-                       reinterpret_cast<const void*>(&scan_kernel<8, true>),
-                       reinterpret_cast<const void*>(&scan_kernel<8, false>)};
-    for (const void* f : k) {
-        const hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                                 static_cast<int>(kScanLdsMax));
+                       reinterpret_cast<const void*>(&scan_kernel<8, true>)};
+    const int cap[] = {kCoarseCapF4<1> * 16, kCoarseCapF4<2> * 16, kCoarseCapF4<4> * 16,
+                       kCoarseCapF4<8> * 16};
+    for (int i = 0; i < 4; ++i) {
+        const hipError_t e =
+            hipFuncSetAttribute(k[i], hipFuncAttributeMaxDynamicSharedMemorySize, cap[i]);
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
