@@ -205,26 +205,9 @@ __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchArgs 
     // M_j = (scan segments below tau_lo) * exp(tau_lo - shift)
     //       + (unselected candidates of list j, already relative to shift)
     const int my_j = lc * kBgLists + wave + (lane & (kListsPerWave - 1)) * kWaves;
-    float mj[G];
-    {
-        const bool ok = lane < kListsPerWave && my_j < D.n_list;
-        const int jj = ok ? my_j : 0;
-        // list j's positions [lo, hi) span sub-chunks lo / kSub .. (hi - 1) / kSub,
-        // whose masses sit at segments j + s
-        const int32_t* loff = ix.loff + static_cast<int64_t>(bg) * (D.n_list + 1);
-        const int lo = loff[jj];
-        const int hi = ok ? loff[jj + 1] : lo;
-        const int s0 = jj + lo / kSub;
-        const int s1 = hi > lo ? jj + (hi - 1) / kSub + 1 : s0;
-        const float* segs = w.seg_sum + static_cast<int64_t>(bg) * D.nseg_cap * G;
-#pragma unroll
-        for (int hh = 0; hh < G; ++hh) {
-            float below = 0.0f;
-            for (int s = s0; s < s1; ++s) below += segs[s * G + hh];
-            const float cand = ok ? w.cand_mass[static_cast<int64_t>(row0 + hh) * D.n_list + jj] : 0.0f;
-            mj[hh] = (ok && live[hh]) ? below * below_scale[hh] + cand : 0.0f;
-        }
-    }
+    // every load that does not depend on another is issued first: the list
+    // means, the candidate weights and the list offsets; then the list's
+    // scan segments (usually one or two) all at once
     float2 vbar[kListsPerWave];
 #pragma unroll
     for (int i = 0; i < kListsPerWave; ++i) {
@@ -233,6 +216,42 @@ __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchArgs 
                       ? *reinterpret_cast<const float2*>(
                             ix.means + (static_cast<int64_t>(bg) * D.n_list + j) * kHeadDim + 2 * lane)
                       : make_float2(0.f, 0.f);
+    }
+    float mj[G];
+    {
+        const bool ok = lane < kListsPerWave && my_j < D.n_list;
+        const int jj = ok ? my_j : 0;
+        float cand[G];
+#pragma unroll
+        for (int hh = 0; hh < G; ++hh)
+            cand[hh] = ok ? w.cand_mass[static_cast<int64_t>(row0 + hh) * D.n_list + jj] : 0.0f;
+        // list j's positions [lo, hi) span sub-chunks lo / kSub .. (hi - 1) / kSub,
+        // whose masses sit at segments j + s
+        const int32_t* loff = ix.loff + static_cast<int64_t>(bg) * (D.n_list + 1);
+        const int lo = loff[jj];
+        const int hi = ok ? loff[jj + 1] : lo;
+        const int s0 = jj + lo / kSub;
+        const int s1 = hi > lo ? jj + (hi - 1) / kSub + 1 : s0;
+        const float* segs = w.seg_sum + static_cast<int64_t>(bg) * D.nseg_cap * G;
+        constexpr int kSegsAtOnce = 4;
+        float sv[kSegsAtOnce][G];
+#pragma unroll
+        for (int u = 0; u < kSegsAtOnce; ++u)
+#pragma unroll
+            for (int hh = 0; hh < G; ++hh) sv[u][hh] = s0 + u < s1 ? segs[(s0 + u) * G + hh] : 0.0f;
+        float below[G];
+#pragma unroll
+        for (int hh = 0; hh < G; ++hh) {
+            below[hh] = sv[0][hh];
+#pragma unroll
+            for (int u = 1; u < kSegsAtOnce; ++u) below[hh] += sv[u][hh];
+        }
+        for (int s = s0 + kSegsAtOnce; s < s1; ++s)   // lists longer than 3 sub-chunks
+#pragma unroll
+            for (int hh = 0; hh < G; ++hh) below[hh] += segs[s * G + hh];
+#pragma unroll
+        for (int hh = 0; hh < G; ++hh)
+            mj[hh] = (ok && live[hh]) ? below[hh] * below_scale[hh] + cand[hh] : 0.0f;
     }
     float Z[G], N[G][2];
 #pragma unroll
