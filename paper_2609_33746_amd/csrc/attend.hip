@@ -296,68 +296,56 @@ __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchArgs 
 
 // y = (sum of partials' N) / (sum of partials' Z) under one shift (Eq. 5).
 // Partials [0, n_exact(b)) and [first_bg, first_bg + n_bg) of each row are used;
-// partials with Z = 0 are skipped.
+// partials with Z = 0 are skipped. Per batch of kMergeBatch used partials,
+// thread u < kMergeBatch loads (m, Z) of partial u and every thread t loads
+// N[t] of all of them, all at once, so a row with at most kMergeBatch
+// partials costs one memory round trip; batches fold by the log-sum-exp rule.
+constexpr int kMergeBatch = 32;
+static_assert(kMergeBatch <= kMergeThreads, "one (m, Z) per thread");
+
 __global__ __launch_bounds__(kMergeThreads) void merge_kernel(Dims D, BatchInts n_exact_parts,
                                                               const float* __restrict__ partial,
                                                               int P, int first_bg, int n_bg,
                                                               float* __restrict__ out) {
-    extern __shared__ float wgt[];   // [P]
-    __shared__ float red[kMergeThreads / kWave];
+    __shared__ float2 smz[kMergeBatch];
     const int row = blockIdx.x;
     const int b = row / D.Hq;
     const int t = threadIdx.x;
     const float* pr = partial + static_cast<int64_t>(row) * P * kPartStride;
     const int ne = n_exact_parts.v[b];
+    const int n_used = ne + n_bg;
     const float neg_inf = -__builtin_huge_valf();
-
-    float m_loc = neg_inf;
-    for (int p = t; p < P; p += kMergeThreads) {
-        const bool used = p < ne || (p >= first_bg && p < first_bg + n_bg);
-        const float2 mz = *reinterpret_cast<const float2*>(pr + p * kPartStride);
-        const float m = (used && mz.y > 0.0f) ? mz.x : neg_inf;
-        wgt[p] = m;
-        m_loc = fmaxf(m_loc, m);
-    }
-    m_loc = wave_max(m_loc);
-    if (lane_id() == 0) red[t / kWave] = m_loc;
-    __syncthreads();
-    float M = neg_inf;
+    auto part = [&](int i) { return i < ne ? i : first_bg + (i - ne); };   // i-th used partial
+    float M = neg_inf, Z = 0.0f, N = 0.0f;
+    for (int i0 = 0; i0 < n_used; i0 += kMergeBatch) {
+        float2 mz = make_float2(neg_inf, 0.0f);
+        if (t < kMergeBatch && i0 + t < n_used)
+            mz = *reinterpret_cast<const float2*>(pr + part(i0 + t) * kPartStride);
+        float n[kMergeBatch];
 #pragma unroll
-    for (int i = 0; i < kMergeThreads / kWave; ++i) M = fmaxf(M, red[i]);
-    __syncthreads();
-    float z_loc = 0.0f;
-    for (int p = t; p < P; p += kMergeThreads) {
-        const float m = wgt[p];
-        const float f = m == neg_inf ? 0.0f : __expf(m - M);
-        wgt[p] = f;
-        const float z = pr[p * kPartStride + 1];   // unused partials may hold garbage
-        z_loc = f != 0.0f ? fmaf(z, f, z_loc) : z_loc;
-    }
-    z_loc = wave_sum(z_loc);
-    if (lane_id() == 0) red[t / kWave] = z_loc;
-    __syncthreads();
-    float Z = 0.0f;
+        for (int u = 0; u < kMergeBatch; ++u)
+            n[u] = i0 + u < n_used ? pr[part(i0 + u) * kPartStride + 4 + t] : 0.0f;
+        if (t < kMergeBatch) smz[t] = mz.y > 0.0f ? mz : make_float2(neg_inf, 0.0f);
+        __syncthreads();
+        float mb = M;
 #pragma unroll
-    for (int i = 0; i < kMergeThreads / kWave; ++i) Z += red[i];
-    // unconditional loads (all issued before use), weights select the used ones
-    constexpr int U = 8;
-    float N[U];
+        for (int u = 0; u < kMergeBatch; ++u) mb = fmaxf(mb, smz[u].x);
+        if (mb != neg_inf) {
+            const float a = __expf(M - mb);   // 0 while M = -inf
+            Z *= a;
+            N *= a;
 #pragma unroll
-    for (int u = 0; u < U; ++u) N[u] = 0.0f;
-    for (int p0 = 0; p0 < P; p0 += U) {
-        float v[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) v[u] = p0 + u < P ? pr[(p0 + u) * kPartStride + 4 + t] : 0.0f;
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const float f = p0 + u < P ? wgt[p0 + u] : 0.0f;
-            N[u] = f != 0.0f ? fmaf(v[u], f, N[u]) : N[u];
+            for (int u = 0; u < kMergeBatch; ++u) {
+                const float2 e = smz[u];
+                const float f = e.x == neg_inf ? 0.0f : __expf(e.x - mb);
+                Z = fmaf(e.y, f, Z);
+                N = f != 0.0f ? fmaf(n[u], f, N) : N;
+            }
+            M = mb;
         }
+        __syncthreads();
     }
-    float n = 0.0f;
-#pragma unroll
-    for (int u = 0; u < U; ++u) n += N[u];
-    out[static_cast<int64_t>(row) * kHeadDim + t] = n / Z;
+    out[static_cast<int64_t>(row) * kHeadDim + t] = N / Z;
 }
 
 template <typename T, int G>
@@ -390,9 +378,7 @@ hipError_t launch_attend(const Dims& D, const BatchArgs& ba, const KV& kv, const
 
 static hipError_t launch_merge_parts(const Dims& D, const BatchInts& ne, const float* partial,
                                      int P, int first_bg, int n_bg, float* out, hipStream_t s) {
-    const size_t lds = static_cast<size_t>(P) * sizeof(float);
-    if (lds > 64 * 1024) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(merge_kernel, dim3(D.B * D.Hq), dim3(kMergeThreads), lds, s, D, ne, partial,
+    hipLaunchKernelGGL(merge_kernel, dim3(D.B * D.Hq), dim3(kMergeThreads), 0, s, D, ne, partial,
                        P, first_bg, n_bg, out);
     return hipGetLastError();
 }
