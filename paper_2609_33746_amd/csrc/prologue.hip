@@ -3,13 +3,13 @@
 //
 // LUT role, per (batch element, KV head) and part: the fine table
 // F[m][z][hh] = (q_hh^(m) . p_{m,z}) / sqrt(d) for the G query heads of the
-// group (also written head-major for the sample role), and the coarse table
-// C[j][hh] = (q_hh . c_j) / sqrt(d).
+// group (read by the scan, the next launch; also written head-major for the
+// sample role), and the coarse table C[j][hh] = (q_hh . c_j) / sqrt(d).
 // Folding r_q / sqrt(d) into the tables: (r_q / sqrt(d)) u_q . x = q . x / sqrt(d),
 // so the tables are built from q / sqrt(d) directly and no normalisation of q
 // is needed (a zero query gives all-zero tables, hence zero scores).
-// Each LUT workgroup writes its part with device-scope stores and, once they
-// are acknowledged, increments its KV head's counter.
+// Each LUT workgroup writes what the sample role reads with device-scope
+// stores and, once they are acknowledged, increments its KV head's counter.
 //
 // Sample role, per (batch element, query head) row: scores a stratified
 // sample of the row's list-major positions (contiguous runs of kSampleRun
@@ -18,7 +18,8 @@
 // whole row score at or above it. The role issues its sample loads, then
 // waits for its KV head's LUT parts (every LUT workgroup has a lower
 // workgroup id and waits for nothing, so it is dispatched first and
-// finishes), then reads the head's tables.
+// finishes), then reads its head's fine table and the coarse terms of its
+// samples.
 //
 // Any threshold gives the same final output: it only decides how many
 // candidates the scan emits (the top-k stage falls back to an exact re-scan
@@ -41,7 +42,8 @@ constexpr int kCoarseGroups = kProThreads / 16;            // 16-lane groups
 constexpr int kCoarsePer = kCoarseLists / kCoarseGroups;   // lists per group: 4
 constexpr int kSamplesPer = kMaxSamples / kProThreads;     // samples per thread: 4
 constexpr int kLutF4 = kLutRow / 4 / kProThreads;          // float4 of a head table per thread: 2
-constexpr int kSpinLimit = 1 << 18;                        // polls before giving up (~0.3 s)
+constexpr int kPolls = 4;                                  // counter reads in flight
+constexpr int kSpinLimit = 1 << 16;                        // poll rounds before giving up
 static_assert(kFineWg * kKsub == kProThreads && kPqM % kFineWg == 0, "fine tiling");
 static_assert(kCoarsePer * kCoarseGroups == kCoarseLists, "coarse tiling");
 static_assert(kSamplesPer * kProThreads == kMaxSamples && kMaxSamples % kSampleRun == 0, "samples");
@@ -60,6 +62,40 @@ __device__ __forceinline__ float coarse_entry(const float (&qc)[8], const float4
     return sum16(acc);
 }
 
+// One fine-table entry (q^(m) / sqrt(d)) . p_{m,z} for the 8 dimensions of
+// subspace m (qm points at them); shared by the LUT and sample roles.
+template <typename T>
+__device__ __forceinline__ float fine_entry(const T* qm, const float (&pv)[kDsub], float inv_sqrt_d) {
+    float qs[kDsub];
+    Load8<T>::run(qm, qs);
+    float acc = 0.0f;
+#pragma unroll
+    for (int t = 0; t < kDsub; ++t) acc = fmaf(qs[t] * inv_sqrt_d, pv[t], acc);
+    return acc;
+}
+
+__device__ __forceinline__ void load_codeword(const float* p, float (&pv)[kDsub]) {
+    const float4 p0 = *reinterpret_cast<const float4*>(p);
+    const float4 p1 = *reinterpret_cast<const float4*>(p + 4);
+    pv[0] = p0.x; pv[1] = p0.y; pv[2] = p0.z; pv[3] = p0.w;
+    pv[4] = p1.x; pv[5] = p1.y; pv[6] = p1.z; pv[7] = p1.w;
+}
+
+// Store G consecutive floats.
+template <int G>
+__device__ __forceinline__ void store_g(float* o, const float (&e)[G]) {
+    if constexpr (G == 8) {
+        reinterpret_cast<float4*>(o)[0] = make_float4(e[0], e[1], e[2], e[3]);
+        reinterpret_cast<float4*>(o)[1] = make_float4(e[4], e[5], e[6], e[7]);
+    } else if constexpr (G == 4) {
+        *reinterpret_cast<float4*>(o) = make_float4(e[0], e[1], e[2], e[3]);
+    } else if constexpr (G == 2) {
+        *reinterpret_cast<float2*>(o) = make_float2(e[0], e[1]);
+    } else {
+        o[0] = e[0];
+    }
+}
+
 template <typename T, int G>
 __device__ __forceinline__ void lut_role(const Dims& D, const T* __restrict__ q,
                                          const float* __restrict__ codebooks,
@@ -74,21 +110,16 @@ __device__ __forceinline__ void lut_role(const Dims& D, const T* __restrict__ q,
         // fine table: one (subspace, codeword) per thread
         const int m = part * kFineWg + tid / kKsub;
         const int z = tid % kKsub;
-        const float* p = codebooks + ((static_cast<int64_t>(bg) * kPqM + m) * kKsub + z) * kDsub;
-        const float4 p0 = *reinterpret_cast<const float4*>(p);
-        const float4 p1 = *reinterpret_cast<const float4*>(p + 4);
-        const float pv[8] = {p0.x, p0.y, p0.z, p0.w, p1.x, p1.y, p1.z, p1.w};
+        float pv[kDsub];
+        load_codeword(codebooks + ((static_cast<int64_t>(bg) * kPqM + m) * kKsub + z) * kDsub, pv);
         float* o = w.lut + ((static_cast<int64_t>(bg) * kPqM + m) * kKsub + z) * G;
+        float e[G];
 #pragma unroll
         for (int hh = 0; hh < G; ++hh) {
-            float qs[kDsub];
-            Load8<T>::run(qg + hh * kHeadDim + m * kDsub, qs);
-            float acc = 0.0f;
-#pragma unroll
-            for (int t = 0; t < kDsub; ++t) acc = fmaf(qs[t] * D.inv_sqrt_d, pv[t], acc);
-            store_device(o + hh, acc);
-            store_device(w.lut_head + static_cast<int64_t>(row0 + hh) * kLutRow + m * kKsub + z, acc);
+            e[hh] = fine_entry<T>(qg + hh * kHeadDim + m * kDsub, pv, D.inv_sqrt_d);
+            store_device(w.lut_head + static_cast<int64_t>(row0 + hh) * kLutRow + m * kKsub + z, e[hh]);
         }
+        store_g<G>(o, e);   // read by the next launch only: plain stores
     } else {
         // coarse table: 16 lanes per list, 8 dimensions per lane
         const int c = part - kFineParts;
@@ -182,15 +213,26 @@ __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, 
     }
     for (int i = tid; i < kHistBins; i += kProThreads) sm.hist[i] = 0;
 
-    // 2) wait for the KV head's tables (bounded)
+    // 2) wait for the KV head's LUT parts (bounded), with kPolls reads of
+    //    the counter in flight so that the wait ends about a quarter of a
+    //    memory round trip after the last part is counted
     if (tid == 0) {
         int ready = 0;
-        for (int it = 0; it < kSpinLimit; ++it) {
-            if (static_cast<int32_t>(counter_read(w.lut_done + bg) - lut_target) >= 0) {
-                ready = 1;
-                break;
+        uint32_t v[kPolls];
+#pragma unroll
+        for (int i = 0; i < kPolls; ++i) {
+            v[i] = counter_read(w.lut_done + bg);
+            __builtin_amdgcn_s_sleep(1);
+        }
+        for (int it = 0; it < kSpinLimit && !ready; ++it) {
+#pragma unroll
+            for (int i = 0; i < kPolls; ++i) {
+                if (!ready && static_cast<int32_t>(v[i] - lut_target) >= 0) ready = 1;
+                if (!ready) {
+                    v[i] = counter_read(w.lut_done + bg);
+                    __builtin_amdgcn_s_sleep(1);
+                }
             }
-            __builtin_amdgcn_s_sleep(2);
         }
         acquire_device();
         sm.ready = ready;
@@ -288,6 +330,7 @@ static hipError_t launch_prologue_t(const Dims& D, const BatchArgs& ba, const KV
     const int per_bg = prologue_parts(D.n_list);
     const int n_lut_wg = D.B * D.Hkv * per_bg;
     const int grid = n_lut_wg + D.B * D.Hq;
+    // each call, every LUT workgroup adds 1 to its KV head's counter
     const uint32_t target = epoch * static_cast<uint32_t>(per_bg);
     hipLaunchKernelGGL((prologue_kernel<T, G>), dim3(grid), dim3(kProThreads), 0, s, D, ba, ix,
                        static_cast<const T*>(kv.q), w, bias, target, n_lut_wg);
