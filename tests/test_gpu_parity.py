@@ -169,6 +169,26 @@ def test_rescan_path(mode, topk):
 
 
 # ---------------------------------------------------------------------------
+# every indexed token a candidate: the copy tiers of the top-k stage (up to
+# 4, 8 and 12 candidates per thread) and its global-memory path beyond the
+# LDS capacity (12288 candidates)
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("n_r", [3000, 6000, 10000, 14000])
+def test_candidate_volume(n_r):
+    wl = small(1, max_seq=n_r + 132, n_list=96, topk=n_r // 50)
+    inp = make(wl, seed=13)
+    ctx = context(inp)
+    ctx.set_option(pqhsa.OPT_THRESHOLD_BIAS, -1_000_000)   # -1000 on every threshold
+    topk_l, out, sel, unsel, sc = run(ctx, inp, scores=True)
+    rows = [(0, h) for h in range(0, wl.n_q_heads, 5)]
+    check_rows(inp, topk_l, rows, out, sel, unsel, sc)
+    ctx.set_option(pqhsa.OPT_THRESHOLD_BIAS, 0)
+    _, out2, sel2, *_ = run(ctx, inp)
+    assert torch.equal(sel2, sel)
+    assert float((out2 - out).abs().max()) <= 1e-4 * float(out.abs().max())
+
+
+# ---------------------------------------------------------------------------
 # repeatability and the plain decode entry point
 # ---------------------------------------------------------------------------
 def test_repeatable_and_plain_decode_matches_debug():
