@@ -260,6 +260,7 @@ pqhsa_status pqhsa_create(const pqhsa_shape* shape, pqhsa_ctx** out) {
     A(dev_alloc(c, &w.lut_done, BG));
     if (ea == hipSuccess) ea = hipMemset(w.lut_done, 0, BG * sizeof(uint32_t));
     A(dev_alloc(c, &w.tau_lo, BQ));
+    A(dev_alloc(c, &w.tau_hi, BQ));
     A(dev_alloc(c, &w.cand, BQ * rc));
     A(dev_alloc(c, &w.cand_cnt, BQ * D.nsub_cap));
     A(dev_alloc(c, &w.seg_sum, BG * D.nseg_cap * G));

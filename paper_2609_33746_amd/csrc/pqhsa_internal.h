@@ -75,6 +75,7 @@ struct Work {
     uint32_t* lut_done;  // [B, Hkv] LUT workgroups finished, summed over all calls
     float* coarse;       // [B, Hkv, n_list, G] (q . c_j) / sqrt(d)
     float* tau_lo;       // [B, Hq] candidate threshold
+    float* tau_hi;       // [B, Hq] largest sampled score (-inf when not sampled)
     uint2* cand;         // [B, Hq, rcap] candidates compacted per sub-chunk: (score bits,
                          //   list id << kPosBits | list-major position)
     int32_t* cand_cnt;   // [B, Hq, nsub_cap]

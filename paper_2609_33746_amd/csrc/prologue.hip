@@ -182,7 +182,10 @@ __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, 
     const int k = ba.topk[b];
     const float neg_inf = -__builtin_huge_valf();
     if (n_r == 0) {
-        if (tid == 0) w.tau_lo[row] = neg_inf;
+        if (tid == 0) {
+            w.tau_lo[row] = neg_inf;
+            w.tau_hi[row] = neg_inf;
+        }
         return;
     }
     // 1) the samples: runs of kSampleRun positions, rs apart (rs >= 1),
@@ -239,7 +242,10 @@ __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, 
     }
     __syncthreads();
     if (!sm.ready) {   // tables not seen in time: every token becomes a candidate
-        if (tid == 0) w.tau_lo[row] = neg_inf;
+        if (tid == 0) {
+            w.tau_lo[row] = neg_inf;
+            w.tau_hi[row] = neg_inf;
+        }
         return;
     }
 
@@ -277,7 +283,10 @@ __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, 
     // order statistic: about 2k * ns / |R| sampled tokens above, plus a margin
     const int c = (k == 0) ? 1 : static_cast<int>(ceilf(2.0f * k * ns / n_r)) + 8;
     if (c > ns) {   // the budget is a large share of R: every token is a candidate
-        if (tid == 0) w.tau_lo[row] = neg_inf;
+        if (tid == 0) {
+            w.tau_lo[row] = neg_inf;
+            w.tau_hi[row] = neg_inf;
+        }
         return;
     }
     // 5) bins of equal width in score (monotone: rounded subtraction and
@@ -300,7 +309,10 @@ __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, 
     for (int u = 0; u < kSamplesPer; ++u)
         if (ok[u] && bin[u] == bstar) lo = min(lo, float_key(sc[u]));
     block_min_max_count<kProThreads>(lo, dmx, dcnt, sm.bs);
-    if (tid == 0) w.tau_lo[row] = key_float(lo) + bias;
+    if (tid == 0) {
+        w.tau_lo[row] = key_float(lo) + bias;
+        w.tau_hi[row] = key_float(mx);   // lets the top-k stage fix its bins in advance
+    }
 }
 
 template <typename T, int G>

@@ -31,6 +31,12 @@ constexpr int kRankCap = 512;          // boundary-bin keys ranked exactly
 constexpr float kMassScale = 1099511627776.0f;       // 2^40: fixed-point weights
 constexpr float kMassUnscale = 1.0f / 1099511627776.0f;
 
+// Bin of a key under bins fixed before the candidates are seen: keys from
+// bkmin upward in steps of 2^bsh, everything above the last bin in it.
+__device__ __forceinline__ uint32_t fixed_bin(uint32_t key, uint32_t bkmin, int bsh) {
+    return key >= bkmin ? min((key - bkmin) >> bsh, static_cast<uint32_t>(kHistBins - 1)) : 0u;
+}
+
 // Rank the keys of one histogram bin exactly: key desc, then token id asc.
 // The bin's keys are gathered into r_key / r_idx, then each wave ranks some of
 // them against all the others with one ballot per 64 keys; token ids
@@ -52,7 +58,7 @@ __device__ __forceinline__ bool rank_boundary_bin(KeyAt key_at, TokAt tok_at, in
         const int i = i0 + tid;
         if (i < n) {
             const uint32_t kk = key_at(i);
-            if (static_cast<int>((kk - kmin) >> sh) == bin) {
+            if (static_cast<int>(fixed_bin(kk, kmin, sh)) == bin) {
                 const int slot = atomicAdd(counter, 1);
                 r_key[slot] = kk;
                 r_idx[slot] = i;
@@ -136,10 +142,13 @@ constexpr size_t kSelLdsBytes = kSelLdsWords * 4;
 // any, so the copy costs one search chain and one memory round trip
 // (indices past the end repeat the last candidate's load). Tracks this
 // thread's min / max key.
+// With fixed bins (hist != nullptr), every candidate is also counted in
+// hist at bin min((key - bkmin) >> bsh, kHistBins - 1).
 template <int N>
 __device__ __forceinline__ void copy_candidates(const uint2* __restrict__ cand, const int* pre,
                                                 int nsub, int total, uint32_t* lds,
-                                                uint32_t& kmin, uint32_t& kmax) {
+                                                uint32_t& kmin, uint32_t& kmax, int* hist,
+                                                uint32_t bkmin, int bsh) {
     const int tid = threadIdx.x;
     int cs[N];
 #pragma unroll
@@ -162,13 +171,14 @@ __device__ __forceinline__ void copy_candidates(const uint2* __restrict__ cand, 
 #pragma unroll
     for (int u = 0; u < N; ++u) {
         const int ci = u * kSelThreads + tid;
+        const uint32_t kk = float_key(__uint_as_float(rec[u].x));
         if (ci < total) {
-            const uint32_t kk = float_key(__uint_as_float(rec[u].x));
             lds[ci] = kk;
             lds[kOffCand + ci] = rec[u].y;
             kmin = min(kmin, kk);
             kmax = max(kmax, kk);
         }
+        if (hist) hist_add(hist, fixed_bin(kk, bkmin, bsh), ci < total);
     }
 }
 
@@ -288,30 +298,43 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchArgs b
         auto CAND = [&](int i) { return lds[kOffCand + i]; };
         uint32_t kmin = 0xffffffffu, kmax = 0u, kcount = 0u;
         const uint2* cand = w.cand + rbase;
+        // Bins fixed in advance from the sampled range [tau_lo, tau_hi] (every
+        // candidate is >= tau_lo; those above tau_hi share the last bin), so
+        // the histogram is built during the copy; otherwise from the
+        // candidates' own min / max in a second pass.
+        const float tlo = w.tau_lo[row], thi = w.tau_hi[row];
+        const bool fixed = k > 0 && tlo > neg_inf && thi > tlo && thi < -neg_inf;
+        uint32_t bkmin = fixed ? float_key(tlo) : 0u;
+        int bsh = fixed ? bin_shift(bkmin, float_key(thi)) : 0;
+        int* fh = fixed ? hist : nullptr;
         if (total > 8 * kSelThreads)
-            copy_candidates<kSelCap / kSelThreads>(cand, pre, nsub, total, lds, kmin, kmax);
+            copy_candidates<kSelCap / kSelThreads>(cand, pre, nsub, total, lds, kmin, kmax, fh,
+                                                   bkmin, bsh);
         else if (total > 4 * kSelThreads)
-            copy_candidates<8>(cand, pre, nsub, total, lds, kmin, kmax);
+            copy_candidates<8>(cand, pre, nsub, total, lds, kmin, kmax, fh, bkmin, bsh);
         else if (total > 0)
-            copy_candidates<4>(cand, pre, nsub, total, lds, kmin, kmax);
-        block_min_max_count<kSelThreads>(kmin, kmax, kcount, bs);
+            copy_candidates<4>(cand, pre, nsub, total, lds, kmin, kmax, fh, bkmin, bsh);
+        if (!fixed) block_min_max_count<kSelThreads>(kmin, kmax, kcount, bs);
         auto TOK = [&](int i) { return static_cast<int>(CAND(i) & kPosMask); };
         if (k == 0) {
             shift = total > 0 ? key_float(kmax) : neg_inf;
             emit_selection(KEY, CAND, [](int, uint32_t, uint32_t) { return false; }, total, 0,
                            D.n_list, shift, mass, sel_tok, cand_mass, ss);
         } else {
-            const int sh = bin_shift(kmin, kmax);
-            for (int i0 = 0; i0 < total; i0 += kSelThreads) {
-                const int i = i0 + tid;
-                const bool act = i < total;
-                hist_add(hist, act ? (KEY(i) - kmin) >> sh : 0u, act);
+            if (!fixed) {
+                bkmin = kmin;
+                bsh = bin_shift(kmin, kmax);
+                for (int i0 = 0; i0 < total; i0 += kSelThreads) {
+                    const int i = i0 + tid;
+                    const bool act = i < total;
+                    hist_add(hist, act ? fixed_bin(KEY(i), bkmin, bsh) : 0u, act);
+                }
             }
             __syncthreads();
             int above = 0;
             const int bstar = block_find_bin_desc<kSelThreads>(hist, k, above, ss, bs);
             uint32_t kth = 0u;
-            const bool by_rank = rank_boundary_bin(KEY, TOK, total, kmin, sh, bstar, hist[bstar],
+            const bool by_rank = rank_boundary_bin(KEY, TOK, total, bkmin, bsh, bstar, hist[bstar],
                                                    k - above, r_key, r_idx, r_tok, counter,
                                                    counter + 1, chosen, kth, bs);
             if (by_rank) {
@@ -319,7 +342,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchArgs b
                 emit_selection(
                     KEY, CAND,
                     [&](int i, uint32_t key, uint32_t) {
-                        const int bn = static_cast<int>((key - kmin) >> sh);
+                        const int bn = static_cast<int>(fixed_bin(key, bkmin, bsh));
                         return bn > bstar || (bn == bstar && ((chosen[i >> 5] >> (i & 31)) & 1u));
                     },
                     total, k, D.n_list, shift, mass, sel_tok, cand_mass, ss);
