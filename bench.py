@@ -243,10 +243,10 @@ def main() -> int:
     n_scanned = sum((n - wl.n_sink - wl.n_local) * wl.n_kv_heads for n in lens)
     stage_bytes = dict(prologue=by["lut"], scan=by["scan"], select=by["select"],
                        attend=by["attend"] + by["background"], merge=by["out"])
-    # the dominant kernel: the longest one among those whose time is set by the
-    # bytes they must read (select reads only the workspace and writes a few
-    # KB of selected ids)
-    dom = max((s_ for s_ in stage_us if s_ != "select"), key=stage_us.get)
+    # the dominant kernel for the HBM roofline: the one that must move the most
+    # bytes (the four main kernels all take 14-16 us, so the longest one
+    # changes from run to run; select reads only the workspace)
+    dom = max((s_ for s_ in stage_us if s_ != "select"), key=lambda s_: stage_bytes.get(s_, 0))
     dom_gbps = stage_bytes[dom] / (stage_us[dom] * 1e-6) / 1e9
     stage_roofline = {s_: round(stage_bytes[s_] / (stage_us[s_] * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)
                       for s_ in stage_us if stage_bytes.get(s_, 0) > 0}

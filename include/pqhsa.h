@@ -156,8 +156,9 @@ pqhsa_status pqhsa_index_export(pqhsa_ctx* ctx, int32_t* perm, int32_t* offsets,
  *                             top-k stage (normally used only when the
  *                             sampled threshold yields fewer than k
  *                             candidates); for testing that path.
- *   PQHSA_OPT_STAGE_TIMING    1: record HIP events between the stages of each
- *                             decode call (read with pqhsa_stage_times).
+ *   PQHSA_OPT_STAGE_TIMING    1: record HIP events around the kernel of each
+ *                             stage of each decode call (read with
+ *                             pqhsa_stage_times).
  *   PQHSA_OPT_THRESHOLD_BIAS  added (as value / 1000.0) to every sampled
  *                             candidate threshold; a large value starves the
  *                             candidate set and forces the fallback. */
@@ -170,7 +171,9 @@ pqhsa_status pqhsa_set_option(pqhsa_ctx* ctx, int32_t option, int64_t value);
 
 /* Stage durations (ms) of the last decode call made with stage timing on, in
  * launch order: [0] LUT build + threshold sample, [1] code scan,
- * [2] top-k select, [3] exact attention + background, [4] merge.
+ * [2] top-k select, [3] exact attention + background, [4] merge. Each is the
+ * execution time of that stage's kernel (events recorded by the kernel
+ * launch itself), without the gaps between launches.
  * `n` is the capacity of `ms`; *n_out receives the number of stages.
  * Synchronises on the recorded events. */
 pqhsa_status pqhsa_stage_times(pqhsa_ctx* ctx, float* ms, int32_t n, int32_t* n_out);

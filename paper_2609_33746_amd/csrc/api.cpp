@@ -59,7 +59,7 @@ struct pqhsa_ctx {
     int force_fallback = 0;
     int timing = 0;
     float bias = 0.0f;
-    hipEvent_t ev[kStages + 1]{};
+    hipEvent_t ev[2 * kStages]{};   // start and stop of each stage's kernel
     bool events_made = false;
     bool timed_valid = false;
 
@@ -401,23 +401,18 @@ static pqhsa_status decode_impl(pqhsa_ctx* c, const void* q, const void* k, cons
         c->events_made = true;
     }
     c->timed_valid = false;
-    auto mark = [&](int i) {
-        if (timed && e == hipSuccess) e = hipEventRecord(c->ev[i], stream);
+    // with stage timing, each kernel records events around its own execution
+    auto tm = [&](int i) {
+        return timed ? KTiming{c->ev[2 * i], c->ev[2 * i + 1]} : KTiming{};
     };
-    mark(0);
     if (e == hipSuccess) {
-        e = launch_prologue(D, ba, kv, ix, c->w, c->bias, c->epoch + 1, stream);
+        e = launch_prologue(D, ba, kv, ix, c->w, c->bias, c->epoch + 1, stream, tm(0));
         if (e == hipSuccess) ++c->epoch;   // the counters advance only if the launch happened
     }
-    mark(1);
-    if (e == hipSuccess) e = launch_scan(D, ba, ix, c->w, c->scan_nwg, stream);
-    mark(2);
-    if (e == hipSuccess) e = launch_select(D, ba, ix, c->w, c->force_fallback, stream);
-    mark(3);
-    if (e == hipSuccess) e = launch_attend(D, ba, kv, ix, c->w, c->nsplit_max, stream);
-    mark(4);
-    if (e == hipSuccess) e = launch_merge(D, ba, c->w, out, c->nsplit_max, stream);
-    mark(5);
+    if (e == hipSuccess) e = launch_scan(D, ba, ix, c->w, c->scan_nwg, stream, tm(1));
+    if (e == hipSuccess) e = launch_select(D, ba, ix, c->w, c->force_fallback, stream, tm(2));
+    if (e == hipSuccess) e = launch_attend(D, ba, kv, ix, c->w, c->nsplit_max, stream, tm(3));
+    if (e == hipSuccess) e = launch_merge(D, ba, c->w, out, c->nsplit_max, stream, tm(4));
     if (e != hipSuccess) return hip_fail(c, e, "enqueueing the decode kernels");
     c->timed_valid = timed;
     if (ba_out) *ba_out = ba;
@@ -498,11 +493,11 @@ pqhsa_status pqhsa_stage_times(pqhsa_ctx* c, float* ms, int32_t n, int32_t* n_ou
     if (!c) return fail(nullptr, PQHSA_ERR_INVALID_ARGUMENT, "ctx is NULL");
     if (!ms || !n_out) return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "ms and n_out must be non-NULL");
     if (!c->timed_valid) return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "no decode call was timed");
-    hipError_t e = hipEventSynchronize(c->ev[kStages]);
+    hipError_t e = hipEventSynchronize(c->ev[2 * kStages - 1]);
     if (e != hipSuccess) return hip_fail(c, e, "hipEventSynchronize");
     for (int i = 0; i < kStages && i < n; ++i) {
         float t = 0.0f;
-        e = hipEventElapsedTime(&t, c->ev[i], c->ev[i + 1]);
+        e = hipEventElapsedTime(&t, c->ev[2 * i], c->ev[2 * i + 1]);
         if (e != hipSuccess) return hip_fail(c, e, "hipEventElapsedTime");
         ms[i] = t;
     }

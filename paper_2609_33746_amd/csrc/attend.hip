@@ -350,48 +350,51 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(Dims D, BatchInts 
 
 template <typename T, int G>
 static hipError_t launch_attend_t(const Dims& D, const BatchArgs& ba, const KV& kv,
-                                  const Index& ix, const Work& w, int nsplit_max, hipStream_t s) {
+                                  const Index& ix, const Work& w, int nsplit_max, hipStream_t s,
+                                  const KTiming& tm) {
     const int n_bgc = (D.n_list + kBgLists - 1) / kBgLists;
     const int grid = D.B * D.Hq * nsplit_max + D.B * D.Hkv * n_bgc;
-    hipLaunchKernelGGL((attend_kernel<T, G>), dim3(grid), dim3(kAttnThreads), 0, s, D, ba, kv,
-                       ix, w, nsplit_max, n_bgc);
+    hipExtLaunchKernelGGL((attend_kernel<T, G>), dim3(grid), dim3(kAttnThreads), 0, s, tm.start,
+                          tm.stop, 0, D, ba, kv, ix, w, nsplit_max, n_bgc);
     return hipGetLastError();
 }
 
 template <typename T>
 static hipError_t launch_attend_g(const Dims& D, const BatchArgs& ba, const KV& kv,
-                                  const Index& ix, const Work& w, int nsplit_max, hipStream_t s) {
+                                  const Index& ix, const Work& w, int nsplit_max, hipStream_t s,
+                                  const KTiming& tm) {
     switch (D.G) {
-        case 1: return launch_attend_t<T, 1>(D, ba, kv, ix, w, nsplit_max, s);
-        case 2: return launch_attend_t<T, 2>(D, ba, kv, ix, w, nsplit_max, s);
-        case 4: return launch_attend_t<T, 4>(D, ba, kv, ix, w, nsplit_max, s);
-        case 8: return launch_attend_t<T, 8>(D, ba, kv, ix, w, nsplit_max, s);
+        case 1: return launch_attend_t<T, 1>(D, ba, kv, ix, w, nsplit_max, s, tm);
+        case 2: return launch_attend_t<T, 2>(D, ba, kv, ix, w, nsplit_max, s, tm);
+        case 4: return launch_attend_t<T, 4>(D, ba, kv, ix, w, nsplit_max, s, tm);
+        case 8: return launch_attend_t<T, 8>(D, ba, kv, ix, w, nsplit_max, s, tm);
         default: return hipErrorInvalidValue;
     }
 }
 
 hipError_t launch_attend(const Dims& D, const BatchArgs& ba, const KV& kv, const Index& ix,
-                         const Work& w, int nsplit_max, hipStream_t s) {
-    return kv.bf16 ? launch_attend_g<bf16_t>(D, ba, kv, ix, w, nsplit_max, s)
-                   : launch_attend_g<float>(D, ba, kv, ix, w, nsplit_max, s);
+                         const Work& w, int nsplit_max, hipStream_t s, const KTiming& tm) {
+    return kv.bf16 ? launch_attend_g<bf16_t>(D, ba, kv, ix, w, nsplit_max, s, tm)
+                   : launch_attend_g<float>(D, ba, kv, ix, w, nsplit_max, s, tm);
 }
 
 static hipError_t launch_merge_parts(const Dims& D, const BatchInts& ne, const float* partial,
-                                     int P, int first_bg, int n_bg, float* out, hipStream_t s) {
-    hipLaunchKernelGGL(merge_kernel, dim3(D.B * D.Hq), dim3(kMergeThreads), 0, s, D, ne, partial,
-                       P, first_bg, n_bg, out);
+                                     int P, int first_bg, int n_bg, float* out, hipStream_t s,
+                                     const KTiming& tm) {
+    hipExtLaunchKernelGGL(merge_kernel, dim3(D.B * D.Hq), dim3(kMergeThreads), 0, s, tm.start,
+                          tm.stop, 0, D, ne, partial, P, first_bg, n_bg, out);
     return hipGetLastError();
 }
 
 hipError_t launch_merge(const Dims& D, const BatchArgs& ba, const Work& w, float* out,
-                        int nsplit_max, hipStream_t s) {
+                        int nsplit_max, hipStream_t s, const KTiming& tm) {
     BatchInts ne;
     for (int b = 0; b < D.B; ++b) {
         const int nE = D.n_sink + D.n_local + ba.topk[b];
         ne.v[b] = (nE + kAttnRows - 1) / kAttnRows;
     }
     const int n_bgc = (D.n_list + kBgLists - 1) / kBgLists;
-    return launch_merge_parts(D, ne, w.partial, nsplit_max + n_bgc, nsplit_max, n_bgc, out, s);
+    return launch_merge_parts(D, ne, w.partial, nsplit_max + n_bgc, nsplit_max, n_bgc, out, s, tm);
 }
 
 // ---------------------------------------------------------------------------
@@ -489,7 +492,7 @@ hipError_t launch_dense(const Dims& D, const KV& kv, const BatchInts& lens, floa
     if (e != hipSuccess) return e;
     BatchInts ne;
     for (int b = 0; b < D.B; ++b) ne.v[b] = (lens.v[b] + kDenseRows - 1) / kDenseRows;
-    return launch_merge_parts(D, ne, partial, nsplit_max, 0, 0, out, s);
+    return launch_merge_parts(D, ne, partial, nsplit_max, 0, 0, out, s, KTiming{});
 }
 
 }  // namespace pqhsa

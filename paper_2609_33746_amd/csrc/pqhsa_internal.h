@@ -1,6 +1,7 @@
 // Internal types and kernel launchers of libpqhsa (not part of the C ABI).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -30,6 +31,12 @@ constexpr int kBgLists = 64;       // lists per background workgroup
 constexpr int kDenseRows = 512;    // cache rows per dense split
 constexpr int kPartStride = 132;   // floats per partial: m, Z, pad, pad, N[128]
 constexpr int kMaxRowParts = 512;  // partials per row (exact splits + background chunks)
+
+// Optional events a launch records around its kernel's own execution
+// (hipExtLaunchKernel), for per-kernel timing; null events record nothing.
+struct KTiming {
+    hipEvent_t start = nullptr, stop = nullptr;
+};
 
 // --- kernel arguments ----------------------------------------------------
 struct Dims {
@@ -111,16 +118,18 @@ hipError_t configure_select();
 // epoch * prologue_parts(n_list).
 __host__ __device__ inline int prologue_parts(int n_list) { return kPqM / 2 + (n_list + 127) / 128; }
 hipError_t launch_prologue(const Dims& D, const BatchArgs& ba, const KV& kv, const Index& ix,
-                           const Work& w, float bias, uint32_t epoch, hipStream_t s);
+                           const Work& w, float bias, uint32_t epoch, hipStream_t s,
+                           const KTiming& tm = KTiming{});
 // nwg = scan workgroups per (batch element, KV head): enough for the longest R_b
 hipError_t launch_scan(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w, int nwg,
-                       hipStream_t s);
+                       hipStream_t s, const KTiming& tm = KTiming{});
 hipError_t launch_select(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w,
-                         int force_fallback, hipStream_t s);
+                         int force_fallback, hipStream_t s, const KTiming& tm = KTiming{});
 hipError_t launch_attend(const Dims& D, const BatchArgs& ba, const KV& kv, const Index& ix,
-                         const Work& w, int nsplit_max, hipStream_t s);
+                         const Work& w, int nsplit_max, hipStream_t s,
+                         const KTiming& tm = KTiming{});
 hipError_t launch_merge(const Dims& D, const BatchArgs& ba, const Work& w, float* out,
-                        int nsplit_max, hipStream_t s);
+                        int nsplit_max, hipStream_t s, const KTiming& tm = KTiming{});
 hipError_t launch_dense(const Dims& D, const KV& kv, const BatchInts& lens, float* partial,
                         float* out, int nsplit_max, hipStream_t s);
 hipError_t launch_prepare_gather(const Dims& D, const uint8_t* codes_in, const float* norms_in,

@@ -338,34 +338,36 @@ __global__ __launch_bounds__(kProThreads) void prologue_kernel(Dims D, BatchArgs
 template <typename T, int G>
 static hipError_t launch_prologue_t(const Dims& D, const BatchArgs& ba, const KV& kv,
                                     const Index& ix, const Work& w, float bias, uint32_t epoch,
-                                    hipStream_t s) {
+                                    hipStream_t s, const KTiming& tm) {
     const int per_bg = prologue_parts(D.n_list);
     const int n_lut_wg = D.B * D.Hkv * per_bg;
     const int grid = n_lut_wg + D.B * D.Hq;
     // each call, every LUT workgroup adds 1 to its KV head's counter
     const uint32_t target = epoch * static_cast<uint32_t>(per_bg);
-    hipLaunchKernelGGL((prologue_kernel<T, G>), dim3(grid), dim3(kProThreads), 0, s, D, ba, ix,
-                       static_cast<const T*>(kv.q), w, bias, target, n_lut_wg);
+    hipExtLaunchKernelGGL((prologue_kernel<T, G>), dim3(grid), dim3(kProThreads), 0, s, tm.start,
+                          tm.stop, 0, D, ba, ix, static_cast<const T*>(kv.q), w, bias, target,
+                          n_lut_wg);
     return hipGetLastError();
 }
 
 template <typename T>
 static hipError_t launch_prologue_g(const Dims& D, const BatchArgs& ba, const KV& kv,
                                     const Index& ix, const Work& w, float bias, uint32_t epoch,
-                                    hipStream_t s) {
+                                    hipStream_t s, const KTiming& tm) {
     switch (D.G) {
-        case 1: return launch_prologue_t<T, 1>(D, ba, kv, ix, w, bias, epoch, s);
-        case 2: return launch_prologue_t<T, 2>(D, ba, kv, ix, w, bias, epoch, s);
-        case 4: return launch_prologue_t<T, 4>(D, ba, kv, ix, w, bias, epoch, s);
-        case 8: return launch_prologue_t<T, 8>(D, ba, kv, ix, w, bias, epoch, s);
+        case 1: return launch_prologue_t<T, 1>(D, ba, kv, ix, w, bias, epoch, s, tm);
+        case 2: return launch_prologue_t<T, 2>(D, ba, kv, ix, w, bias, epoch, s, tm);
+        case 4: return launch_prologue_t<T, 4>(D, ba, kv, ix, w, bias, epoch, s, tm);
+        case 8: return launch_prologue_t<T, 8>(D, ba, kv, ix, w, bias, epoch, s, tm);
         default: return hipErrorInvalidValue;
     }
 }
 
 hipError_t launch_prologue(const Dims& D, const BatchArgs& ba, const KV& kv, const Index& ix,
-                           const Work& w, float bias, uint32_t epoch, hipStream_t s) {
-    return kv.bf16 ? launch_prologue_g<bf16_t>(D, ba, kv, ix, w, bias, epoch, s)
-                   : launch_prologue_g<float>(D, ba, kv, ix, w, bias, epoch, s);
+                           const Work& w, float bias, uint32_t epoch, hipStream_t s,
+                           const KTiming& tm) {
+    return kv.bf16 ? launch_prologue_g<bf16_t>(D, ba, kv, ix, w, bias, epoch, s, tm)
+                   : launch_prologue_g<float>(D, ba, kv, ix, w, bias, epoch, s, tm);
 }
 
 }  // namespace pqhsa

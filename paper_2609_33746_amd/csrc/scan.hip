@@ -219,16 +219,16 @@ constexpr size_t kScanLdsMax = 160 * 1024;   // LDS of one workgroup on gfx950
 
 template <int G>
 static hipError_t launch_scan_t(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w,
-                                int nwg, hipStream_t s) {
+                                int nwg, hipStream_t s, const KTiming& tm) {
     const size_t cf = static_cast<size_t>(kCoarseCapF4<G>) * 16;
     static_assert(kLutRow * G * 4 + kCoarseCapF4<G> * 16 <= kScanLdsMax, "LDS budget");
     const dim3 grid(D.B * D.Hkv * nwg);
     if (D.n_list * G % 4 == 0 && D.n_list * G / 4 <= kCoarseCapF4<G>)
-        hipLaunchKernelGGL((scan_kernel<G, true>), grid, dim3(kScanThreads), cf, s, D, ba, ix, w,
-                           nwg);
+        hipExtLaunchKernelGGL((scan_kernel<G, true>), grid, dim3(kScanThreads), cf, s, tm.start,
+                              tm.stop, 0, D, ba, ix, w, nwg);
     else
-        hipLaunchKernelGGL((scan_kernel<G, false>), grid, dim3(kScanThreads), 0, s, D, ba, ix, w,
-                           nwg);
+        hipExtLaunchKernelGGL((scan_kernel<G, false>), grid, dim3(kScanThreads), 0, s, tm.start,
+                              tm.stop, 0, D, ba, ix, w, nwg);
     return hipGetLastError();
 }
 
@@ -249,13 +249,13 @@ hipError_t configure_scan() {
 }
 
 hipError_t launch_scan(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w, int nwg,
-                       hipStream_t s) {
+                       hipStream_t s, const KTiming& tm) {
     if (nwg == 0) return hipSuccess;
     switch (D.G) {
-        case 1: return launch_scan_t<1>(D, ba, ix, w, nwg, s);
-        case 2: return launch_scan_t<2>(D, ba, ix, w, nwg, s);
-        case 4: return launch_scan_t<4>(D, ba, ix, w, nwg, s);
-        case 8: return launch_scan_t<8>(D, ba, ix, w, nwg, s);
+        case 1: return launch_scan_t<1>(D, ba, ix, w, nwg, s, tm);
+        case 2: return launch_scan_t<2>(D, ba, ix, w, nwg, s, tm);
+        case 4: return launch_scan_t<4>(D, ba, ix, w, nwg, s, tm);
+        case 8: return launch_scan_t<8>(D, ba, ix, w, nwg, s, tm);
         default: return hipErrorInvalidValue;
     }
 }

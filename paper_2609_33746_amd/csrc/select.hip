@@ -440,9 +440,9 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchArgs b
 }
 
 hipError_t launch_select(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w,
-                         int force_fallback, hipStream_t s) {
-    hipLaunchKernelGGL(select_kernel, dim3(D.B * D.Hq), dim3(kSelThreads), kSelLdsBytes, s, D, ba,
-                       ix, w, force_fallback);
+                         int force_fallback, hipStream_t s, const KTiming& tm) {
+    hipExtLaunchKernelGGL(select_kernel, dim3(D.B * D.Hq), dim3(kSelThreads), kSelLdsBytes, s,
+                          tm.start, tm.stop, 0, D, ba, ix, w, force_fallback);
     return hipGetLastError();
 }
 
