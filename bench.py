@@ -42,7 +42,7 @@ def algorithmic_bytes(inp, topk, sel_union):
     """Bytes each stage must read (and the output it must write), per call.
 
     a1 LUT:    q (G d s_q) + centroids (n_list d 4) + codebooks (256 d 4) per (b, g)
-    a2 scan:   codes + norms (M + 4 per indexed token) + list offsets ((n_list+1) 4)
+    a2 scan:   codes + norms (M b / 8 + 4 per indexed token) + list offsets ((n_list+1) 4)
     a3 select: the selected ids (G k 4) per (b, g)
     a4 attend: the distinct gathered K and V rows (U 2 d s_kv) per (b, g)
     a5 bg:     list means (n_list d 4) per (b, g)
@@ -58,7 +58,8 @@ def algorithmic_bytes(inp, topk, sel_union):
         n_r = n - wl.n_sink - wl.n_local
         for g in range(wl.n_kv_heads):
             by["lut"] += G * d * s_kv + wl.n_list * d * 4 + wl.pq_ksub * d * 4
-            by["scan"] += n_r * (wl.pq_m + 4) + (wl.n_list + 1) * 4
+            code_bytes = wl.pq_m * (wl.pq_ksub.bit_length() - 1) // 8
+            by["scan"] += n_r * (code_bytes + 4) + (wl.n_list + 1) * 4
             by["select"] += G * topk[b] * 4
             by["attend"] += sel_union[b][g] * 2 * d * s_kv
             by["background"] += wl.n_list * d * 4
@@ -73,6 +74,8 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-pq4", action="store_true",
+                    help="skip the arm with the paper's 4-bit-code index setting")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--profile-only", action="store_true",
                     help="run the warm-up and timed decode calls only (for rocprofv3)")
@@ -215,6 +218,40 @@ def main() -> int:
     except Exception as exc:  # noqa: BLE001 - reported, not fatal
         log(f"library dense reference unavailable: {exc}")
 
+    # the paper's own index setting on the same 128K shapes (8 subspaces of
+    # 4-bit codes, 512 lists): a second PQ-HSA arm, reported beside the value
+    pq4 = None
+    if not args.no_pq4:
+        log("timing the 4-bit-code index arm")
+        wl4 = synth.pq4(WORKLOAD)
+        inp4 = synth.make_inputs(wl4, seed=args.seed, device=dev)
+        ctx4 = pqhsa.context_for(inp4)
+        pqhsa.prepare_from(ctx4, inp4)
+        q4, k4, v4 = inp4["q"], inp4["k_cache"], inp4["v_cache"]
+        topk4 = inp4["topk"].tolist()
+        out4 = torch.empty(q4.shape, dtype=torch.float32, device=dev)
+
+        def pq4_call():
+            ctx4.decode(q4, k4, v4, topk4, out=out4)
+        for _ in range(args.warmup):
+            flush()
+            pq4_call()
+        t_pq4, _ = timed(pq4_call, max(20, args.steps // 2))
+        ctx4.set_option(pqhsa.OPT_STAGE_TIMING, 1)
+        acc4 = {}
+        for _ in range(20):
+            flush()
+            pq4_call()
+            for k_, v_ in ctx4.stage_times().items():
+                acc4.setdefault(k_, []).append(v_)
+        ctx4.set_option(pqhsa.OPT_STAGE_TIMING, 0)
+        us4 = float(np.mean(t_pq4)) * 1e3
+        pq4 = {"workload": wl4.name, "pq_m": wl4.pq_m, "pq_ksub": wl4.pq_ksub,
+               "n_list": wl4.n_list, "topk": topk4[0], "us_per_call": round(us4, 3),
+               "stage_us": {k_: round(float(np.mean(v_)) * 1e3, 3) for k_, v_ in acc4.items()}}
+        ctx4.close()
+        del inp4, q4, k4, v4
+
     # distinct gathered rows per (b, g) for the byte model
     _, sel, _, _ = ctx.decode_debug(q, kc, vc, topk)
     torch.cuda.synchronize()
@@ -297,6 +334,8 @@ def main() -> int:
         "dense_best_arm": best_dense[0],
         "speedup_vs_dense": round(best_dense[1] / us, 3),
         "cpu_baseline": cpu,
+        "paper_index_arm": pq4 if pq4 is None else dict(
+            pq4, speedup_vs_dense=round(best_dense[1] / pq4["us_per_call"], 3)),
     }
     print(json.dumps(rec), flush=True)
     ctx.close()

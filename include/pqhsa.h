@@ -51,8 +51,10 @@ typedef enum {
 typedef enum { PQHSA_F32 = 0, PQHSA_BF16 = 1 } pqhsa_dtype;
 
 /* Problem shape, fixed for the life of a context.
- * Supported: head_dim = 128, pq_m = 16 (8-dimensional subspaces), max_seq <= 2^20,
- * pq_ksub = 256 (one uint8 code per subspace), 1 <= n_list <= 4096,
+ * Supported: head_dim = 128; (pq_m, pq_ksub) = (16, 256), 8-bit codes of
+ * 8-dimensional subspaces, or (8, 16), the paper's own setting of 4-bit codes
+ * of 16-dimensional subspaces (Section 3.1), kept as 4 bytes per token;
+ * max_seq <= 2^20, 1 <= n_list <= 4096,
  * G in {1, 2, 4, 8}, 1 <= batch <= 256, kv_dtype F32 or BF16 (the query has
  * the same dtype as the cache), 0 <= max_topk <= max_seq, and
  * ceil((n_sink + n_local + max_topk) / 128) + ceil(n_list / 64) <= 512. */
@@ -85,7 +87,9 @@ void pqhsa_destroy(pqhsa_ctx* ctx);
 /* Load one prompt's IVF-PQ index into the context (Section 3.1, 3.3).
  *   seq_lens   HOST int32 [B]: N_b, with n_sink + n_local <= N_b <= max_seq.
  *   list_ids   int32 [B, Hkv, Nmax]          a_i, 0 <= a_i < n_list on R_b
- *   codes      uint8 [B, Hkv, Nmax, M]       z_im
+ *   codes      uint8 [B, Hkv, Nmax, M]       z_im, one code per byte
+ *                                             (< K; with K = 16 only the low
+ *                                             four bits are kept)
  *   norms      float [B, Hkv, Nmax]          r_i (the key norm kept outside
  *                                             the quantizer)
  *   centroids  float [B, Hkv, n_list, d]     c_j

@@ -54,6 +54,7 @@ struct pqhsa_ctx {
     int nsplit_max = 0;
     float* dense_partial = nullptr;
     int dense_nsplit = 0;
+    size_t codebook_floats = 0;   // per (b, kv head): K * d
 
     // options
     int force_fallback = 0;
@@ -122,8 +123,9 @@ pqhsa_status check_shape(const pqhsa_shape* s) {
     if (s->kv_dtype != PQHSA_F32 && s->kv_dtype != PQHSA_BF16)
         return fail(nullptr, PQHSA_ERR_UNSUPPORTED, "kv_dtype must be PQHSA_F32 or PQHSA_BF16");
     if (s->head_dim != kHeadDim) return fail(nullptr, PQHSA_ERR_UNSUPPORTED, "head_dim must be 128");
-    if (s->pq_m != kPqM || s->pq_ksub != kKsub)
-        return fail(nullptr, PQHSA_ERR_UNSUPPORTED, "only pq_m = 16 and pq_ksub = 256 are supported");
+    if (!((s->pq_m == Pq8::M && s->pq_ksub == Pq8::K) || (s->pq_m == Pq4::M && s->pq_ksub == Pq4::K)))
+        return fail(nullptr, PQHSA_ERR_UNSUPPORTED,
+                    "(pq_m, pq_ksub) must be (16, 256) or (8, 16)");
     const int G = s->n_q_heads / s->n_kv_heads;
     if (G != 1 && G != 2 && G != 4 && G != 8)
         return fail(nullptr, PQHSA_ERR_UNSUPPORTED, "GQA group size must be 1, 2, 4 or 8");
@@ -232,6 +234,7 @@ pqhsa_status pqhsa_create(const pqhsa_shape* shape, pqhsa_ctx** out) {
     D.nsub_cap = (D.rcap + kSub - 1) / kSub;
     D.nseg_cap = D.n_list + D.nsub_cap;
     D.max_topk = std::max(shape->max_topk, 1);
+    D.pq_bits = shape->pq_m == Pq4::M ? Pq4::BITS : Pq8::BITS;
     D.inv_sqrt_d = static_cast<float>(1.0 / std::sqrt(static_cast<double>(kHeadDim)));
 
     const size_t B = D.B, Hq = D.Hq, Hkv = D.Hkv, G = D.G, L = D.n_list, rc = D.rcap;
@@ -244,19 +247,23 @@ pqhsa_status pqhsa_create(const pqhsa_shape* shape, pqhsa_ctx** out) {
     Work& w = c->w;
     hipError_t ea = hipSuccess;
     auto A = [&](hipError_t r) { if (ea == hipSuccess) ea = r; };
-    A(dev_alloc(c, &c->codes, BG * rc * kPqM));
+    const size_t code_bytes = D.pq_bits == 4 ? Pq4::CODE_BYTES : Pq8::CODE_BYTES;
+    const size_t lut_row = D.pq_bits == 4 ? Pq4::LUT_ROW : Pq8::LUT_ROW;
+    const size_t codebook_floats = (D.pq_bits == 4 ? Pq4::K : Pq8::K) * static_cast<size_t>(kHeadDim);
+    c->codebook_floats = codebook_floats;
+    A(dev_alloc(c, &c->codes, BG * rc * code_bytes));
     A(dev_alloc(c, &c->norms, BG * rc));
     A(dev_alloc(c, &c->perm, BG * rc));
     A(dev_alloc(c, &c->pos_word, BG * rc));
     A(dev_alloc(c, &c->loff, BG * (L + 1)));
     A(dev_alloc(c, &c->centroids, BG * L * kHeadDim));
-    A(dev_alloc(c, &c->codebooks, BG * kPqM * kKsub * kDsub));
+    A(dev_alloc(c, &c->codebooks, BG * codebook_floats));
     A(dev_alloc(c, &c->means, BG * L * kHeadDim));
     A(dev_alloc(c, &c->n_seq_dev, B));
     A(dev_alloc(c, &c->n_r_dev, B));
-    A(dev_alloc(c, &w.lut, BG * kLutRow * G));
+    A(dev_alloc(c, &w.lut, BG * lut_row * G));
     A(dev_alloc(c, &w.coarse, BG * L * G + 16));   // + 16: whole float4 reads at the end
-    A(dev_alloc(c, &w.lut_head, BQ * kLutRow));
+    A(dev_alloc(c, &w.lut_head, BQ * lut_row));
     A(dev_alloc(c, &w.lut_done, BG));
     if (ea == hipSuccess) ea = hipMemset(w.lut_done, 0, BG * sizeof(uint32_t));
     A(dev_alloc(c, &w.tau_lo, BQ));
@@ -354,7 +361,7 @@ pqhsa_status pqhsa_index_prepare(pqhsa_ctx* c, const int32_t* seq_lens, const in
     H2D(c->n_seq_dev, lens.data(), B * 4);
     H2D(c->n_r_dev, nr.data(), B * 4);
     D2D(c->centroids, centroids, BG * L * kHeadDim * 4);
-    D2D(c->codebooks, codebooks, BG * kPqM * kKsub * kDsub * 4);
+    D2D(c->codebooks, codebooks, BG * c->codebook_floats * 4);
     D2D(c->means, list_means, BG * L * kHeadDim * 4);
     if (e != hipSuccess) return hip_fail(c, e, "uploading the prepared index");
     e = launch_prepare_gather(D, codes, norms, c->index(), c->codes, c->norms, stream);

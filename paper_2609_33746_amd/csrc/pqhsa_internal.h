@@ -9,10 +9,23 @@ namespace pqhsa {
 
 // --- tiling constants ------------------------------------------------------
 constexpr int kHeadDim = 128;      // d
-constexpr int kPqM = 16;           // subspaces
-constexpr int kKsub = 256;         // codewords per subspace (uint8 codes)
-constexpr int kDsub = 8;           // d / M
-constexpr int kLutRow = kPqM * kKsub;  // LUT entries per query head
+
+// The two product-quantizer layouts of the index (Section 3.1, Eq. 2).
+// Pq8: 16 subspaces of 8 dimensions, 256 codewords, one byte per code
+// (16 bytes per position). Pq4, the paper's own setting: 8 subspaces of 16
+// dimensions, 16 codewords, two codes per byte (4 bytes per position; code m
+// in bits 4m .. 4m + 3 of the word).
+struct Pq8 {
+    static constexpr int M = 16, K = 256, DSUB = 8, CODE_BYTES = 16, BITS = 8;
+    static constexpr int LUT_ROW = M * K;   // fine-table entries per query head
+    using Code = uint4;
+};
+struct Pq4 {
+    static constexpr int M = 8, K = 16, DSUB = 16, CODE_BYTES = 4, BITS = 4;
+    static constexpr int LUT_ROW = M * K;
+    using Code = uint32_t;
+};
+constexpr int kLutRowMax = Pq8::LUT_ROW;
 constexpr int kMaxBatch = 256;
 constexpr int kMaxLists = 4096;
 
@@ -45,6 +58,7 @@ struct Dims {
     int nsub_cap;   // ceil(rcap / kSub)
     int nseg_cap;   // n_list + nsub_cap
     int max_topk;
+    int pq_bits;    // 8 (Pq8) or 4 (Pq4)
     float inv_sqrt_d;
 };
 
@@ -112,11 +126,14 @@ struct KV {
 hipError_t configure_scan();
 hipError_t configure_select();
 
-// LUT workgroups per (b, kv head) in the prologue: kPqM / 2 fine parts plus
-// one coarse part per 128 lists. epoch = the number of prologue launches on
-// this workspace so far, this one included: the LUT counters then read
-// epoch * prologue_parts(n_list).
-__host__ __device__ inline int prologue_parts(int n_list) { return kPqM / 2 + (n_list + 127) / 128; }
+// LUT workgroups per (b, kv head) in the prologue: fine parts (8 for Pq8,
+// 2 subspaces each; 1 for Pq4) plus one coarse part per 128 lists. epoch =
+// the number of prologue launches on this workspace so far, this one
+// included: the LUT counters then read epoch * prologue_parts(...).
+__host__ __device__ inline int prologue_fine_parts(int pq_bits) { return pq_bits == 4 ? 1 : 8; }
+__host__ __device__ inline int prologue_parts(int n_list, int pq_bits) {
+    return prologue_fine_parts(pq_bits) + (n_list + 127) / 128;
+}
 hipError_t launch_prologue(const Dims& D, const BatchArgs& ba, const KV& kv, const Index& ix,
                            const Work& w, float bias, uint32_t epoch, hipStream_t s,
                            const KTiming& tm = KTiming{});

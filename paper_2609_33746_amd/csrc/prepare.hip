@@ -6,10 +6,29 @@
 
 namespace pqhsa {
 
-// codes_out[bg][pos] = codes_in[bg][perm[pos]] (16 bytes), same for norms.
-__global__ __launch_bounds__(256) void gather_index_kernel(Dims D, const uint4* __restrict__ codes_in,
+// Codes of one position from the caller's one-byte-per-code layout: Pq8 as
+// is (16 bytes), Pq4 packed two per byte (code m in bits 4m .. 4m + 3; the
+// caller's codes are < 16, only their low four bits are kept).
+__device__ __forceinline__ uint4 prepared_code(const uint8_t* p, Pq8) {
+    return *reinterpret_cast<const uint4*>(p);
+}
+__device__ __forceinline__ uint32_t prepared_code(const uint8_t* p, Pq4) {
+    const uint2 v = *reinterpret_cast<const uint2*>(p);
+    uint32_t out = 0u;
+#pragma unroll
+    for (int m = 0; m < 8; ++m) {
+        const uint32_t byte = ((m < 4 ? v.x : v.y) >> (8 * (m & 3))) & 0xfu;
+        out |= byte << (4 * m);
+    }
+    return out;
+}
+
+// codes_out[bg][pos] = codes_in[bg][perm[pos]] (prepared layout), same for norms.
+template <typename PQ>
+__global__ __launch_bounds__(256) void gather_index_kernel(Dims D, const uint8_t* __restrict__ codes_in,
                                                            const float* __restrict__ norms_in,
-                                                           Index ix, uint4* __restrict__ codes_out,
+                                                           Index ix,
+                                                           typename PQ::Code* __restrict__ codes_out,
                                                            float* __restrict__ norms_out) {
     const int bg = blockIdx.y;
     const int b = bg / D.Hkv;
@@ -17,7 +36,7 @@ __global__ __launch_bounds__(256) void gather_index_kernel(Dims D, const uint4* 
     if (pos >= ix.n_r[b]) return;
     const int64_t base = static_cast<int64_t>(bg) * D.rcap;
     const int tok = ix.perm[base + pos];
-    codes_out[base + pos] = codes_in[base + tok];
+    codes_out[base + pos] = prepared_code(codes_in + (base + tok) * PQ::M, PQ{});
     norms_out[base + pos] = norms_in[base + tok];
 }
 
@@ -25,9 +44,12 @@ hipError_t launch_prepare_gather(const Dims& D, const uint8_t* codes_in, const f
                                  const Index& ix, uint8_t* codes_out, float* norms_out,
                                  hipStream_t s) {
     dim3 grid((D.rcap + 255) / 256, D.B * D.Hkv);
-    hipLaunchKernelGGL(gather_index_kernel, grid, dim3(256), 0, s, D,
-                       reinterpret_cast<const uint4*>(codes_in), norms_in, ix,
-                       reinterpret_cast<uint4*>(codes_out), norms_out);
+    if (D.pq_bits == 4)
+        hipLaunchKernelGGL(gather_index_kernel<Pq4>, grid, dim3(256), 0, s, D, codes_in, norms_in,
+                           ix, reinterpret_cast<uint32_t*>(codes_out), norms_out);
+    else
+        hipLaunchKernelGGL(gather_index_kernel<Pq8>, grid, dim3(256), 0, s, D, codes_in, norms_in,
+                           ix, reinterpret_cast<uint4*>(codes_out), norms_out);
     return hipGetLastError();
 }
 
@@ -43,26 +65,28 @@ __global__ void fill_f32_kernel(float* p, int64_t n, float v) {
 }
 
 // Approximate logit of every indexed token, scattered by token id.
+template <typename PQ>
 __global__ __launch_bounds__(kDbgThreads) void score_dump_kernel(Dims D, Index ix, Work w,
                                                                  float* __restrict__ scores,
                                                                  int64_t out_stride) {
-    __shared__ float lut_s[kLutRow];
+    __shared__ float lut_s[PQ::LUT_ROW];
     const int row = blockIdx.y;
     const int b = row / D.Hq;
     const int h = row % D.Hq;
     const int g = h / D.G;
     const int hh = h % D.G;
     const int bg = b * D.Hkv + g;
-    stage_head_lut<kDbgThreads>(lut_s, w.lut + static_cast<int64_t>(bg) * kLutRow * D.G, D.G, hh);
+    stage_head_lut<PQ, kDbgThreads>(lut_s, w.lut + static_cast<int64_t>(bg) * PQ::LUT_ROW * D.G,
+                                    D.G, hh);
     __syncthreads();
     const int n_r = ix.n_r[b];
     const int64_t base = static_cast<int64_t>(bg) * D.rcap;
-    const uint4* codes = reinterpret_cast<const uint4*>(ix.codes) + base;
+    const typename PQ::Code* codes = reinterpret_cast<const typename PQ::Code*>(ix.codes) + base;
     const float* coarse = w.coarse + static_cast<int64_t>(bg) * D.n_list * D.G;
     for (int pos = blockIdx.x * kDbgThreads + threadIdx.x; pos < n_r;
          pos += gridDim.x * kDbgThreads) {
         float fs[1];
-        fine_sum<1>(lut_s, codes[pos], fs);
+        fine_sum<PQ, 1>(lut_s, codes[pos], fs);
         const uint32_t wd = ix.pos_word[base + pos];
         const float s = pq_logit(ix.norms[base + pos], coarse[(wd >> kPosBits) * D.G + hh], fs[0]);
         scores[row * out_stride + (wd & kPosMask)] = s;
@@ -140,8 +164,12 @@ hipError_t launch_debug(const Dims& D, const BatchArgs& ba, const Index& ix, con
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
         dim3 grid(64, D.B * D.Hq);
-        hipLaunchKernelGGL(score_dump_kernel, grid, dim3(kDbgThreads), 0, s, D, ix, w, scores,
-                           static_cast<int64_t>(D.rcap));
+        if (D.pq_bits == 4)
+            hipLaunchKernelGGL(score_dump_kernel<Pq4>, grid, dim3(kDbgThreads), 0, s, D, ix, w,
+                               scores, static_cast<int64_t>(D.rcap));
+        else
+            hipLaunchKernelGGL(score_dump_kernel<Pq8>, grid, dim3(kDbgThreads), 0, s, D, ix, w,
+                               scores, static_cast<int64_t>(D.rcap));
         e = hipGetLastError();
         if (e != hipSuccess) return e;
     }

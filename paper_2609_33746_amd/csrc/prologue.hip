@@ -26,6 +26,8 @@
 // when fewer than k tokens reach it). So the wait is bounded: a sample
 // workgroup that does not see its tables within kSpinLimit polls sets
 // tau_lo = -inf, which makes every token a candidate, and exits.
+#include <type_traits>
+
 #include "device_common.h"
 #include "hist_select.h"
 #include "pq_score.h"
@@ -35,21 +37,18 @@
 namespace pqhsa {
 
 constexpr int kProThreads = 512;
-constexpr int kFineWg = kProThreads / kKsub;              // subspaces per fine workgroup: 2
-constexpr int kFineParts = kPqM / kFineWg;                 // fine workgroups per KV head: 8
+constexpr int kFineWg = kProThreads / Pq8::K;              // Pq8 subspaces per fine workgroup: 2
 constexpr int kCoarseLists = 128;                          // lists per coarse workgroup
 constexpr int kCoarseGroups = kProThreads / 16;            // 16-lane groups
 constexpr int kCoarsePer = kCoarseLists / kCoarseGroups;   // lists per group: 4
 constexpr int kSamplesPer = kMaxSamples / kProThreads;     // samples per thread: 4
-constexpr int kLutF4 = kLutRow / 4 / kProThreads;          // float4 of a head table per thread: 2
 constexpr int kPolls = 4;                                  // counter reads in flight
 constexpr int kSpinLimit = 1 << 16;                        // poll rounds before giving up
-static_assert(kFineWg * kKsub == kProThreads && kPqM % kFineWg == 0, "fine tiling");
+static_assert(kFineWg * Pq8::K == kProThreads && Pq8::M / kFineWg == 8, "Pq8 fine tiling");
+static_assert(Pq4::LUT_ROW <= kProThreads, "Pq4 fine table: one codeword per thread");
 static_assert(kCoarsePer * kCoarseGroups == kCoarseLists, "coarse tiling");
 static_assert(kSamplesPer * kProThreads == kMaxSamples && kMaxSamples % kSampleRun == 0, "samples");
-static_assert(kLutF4 * 4 * kProThreads == kLutRow, "head table staging");
-
-static_assert(kFineParts == kPqM / 2 && kCoarseLists == 128, "prologue_parts() counts these");
+static_assert(kCoarseLists == 128, "prologue_parts() counts these");
 
 // (q / sqrt(d)) . c over 16 lanes of 8 dimensions each; every lane of the
 // 16-lane group receives the same sum.
@@ -62,23 +61,28 @@ __device__ __forceinline__ float coarse_entry(const float (&qc)[8], const float4
     return sum16(acc);
 }
 
-// One fine-table entry (q^(m) / sqrt(d)) . p_{m,z} for the 8 dimensions of
-// subspace m (qm points at them); shared by the LUT and sample roles.
-template <typename T>
-__device__ __forceinline__ float fine_entry(const T* qm, const float (&pv)[kDsub], float inv_sqrt_d) {
-    float qs[kDsub];
-    Load8<T>::run(qm, qs);
+// One fine-table entry (q^(m) / sqrt(d)) . p_{m,z} over the DSUB dimensions of
+// subspace m (qm points at them).
+template <typename T, int DSUB>
+__device__ __forceinline__ float fine_entry(const T* qm, const float (&pv)[DSUB], float inv_sqrt_d) {
     float acc = 0.0f;
 #pragma unroll
-    for (int t = 0; t < kDsub; ++t) acc = fmaf(qs[t] * inv_sqrt_d, pv[t], acc);
+    for (int t0 = 0; t0 < DSUB; t0 += 8) {
+        float qs[8];
+        Load8<T>::run(qm + t0, qs);
+#pragma unroll
+        for (int t = 0; t < 8; ++t) acc = fmaf(qs[t] * inv_sqrt_d, pv[t0 + t], acc);
+    }
     return acc;
 }
 
-__device__ __forceinline__ void load_codeword(const float* p, float (&pv)[kDsub]) {
-    const float4 p0 = *reinterpret_cast<const float4*>(p);
-    const float4 p1 = *reinterpret_cast<const float4*>(p + 4);
-    pv[0] = p0.x; pv[1] = p0.y; pv[2] = p0.z; pv[3] = p0.w;
-    pv[4] = p1.x; pv[5] = p1.y; pv[6] = p1.z; pv[7] = p1.w;
+template <int DSUB>
+__device__ __forceinline__ void load_codeword(const float* p, float (&pv)[DSUB]) {
+#pragma unroll
+    for (int t = 0; t < DSUB; t += 4) {
+        const float4 v = *reinterpret_cast<const float4*>(p + t);
+        pv[t] = v.x; pv[t + 1] = v.y; pv[t + 2] = v.z; pv[t + 3] = v.w;
+    }
 }
 
 // Store G consecutive floats.
@@ -96,7 +100,7 @@ __device__ __forceinline__ void store_g(float* o, const float (&e)[G]) {
     }
 }
 
-template <typename T, int G>
+template <typename T, int G, typename PQ>
 __device__ __forceinline__ void lut_role(const Dims& D, const T* __restrict__ q,
                                          const float* __restrict__ codebooks,
                                          const float* __restrict__ centroids, const Work& w,
@@ -106,23 +110,29 @@ __device__ __forceinline__ void lut_role(const Dims& D, const T* __restrict__ q,
     const int row0 = b * D.Hq + g * G;
     const T* qg = q + static_cast<int64_t>(row0) * kHeadDim;
     const int tid = threadIdx.x;
-    if (part < kFineParts) {
-        // fine table: one (subspace, codeword) per thread
-        const int m = part * kFineWg + tid / kKsub;
-        const int z = tid % kKsub;
-        float pv[kDsub];
-        load_codeword(codebooks + ((static_cast<int64_t>(bg) * kPqM + m) * kKsub + z) * kDsub, pv);
-        float* o = w.lut + ((static_cast<int64_t>(bg) * kPqM + m) * kKsub + z) * G;
-        float e[G];
+    const int fine_parts = prologue_fine_parts(PQ::BITS);
+    if (part < fine_parts) {
+        // fine table: one (subspace, codeword) per thread (Pq8: 2 subspaces
+        // per part; Pq4: the whole table, 128 codewords, in one part)
+        const int e_id = std::is_same<PQ, Pq8>::value ? part * kProThreads + tid : tid;
+        if (e_id < PQ::LUT_ROW) {
+            const int m = e_id / PQ::K;
+            const int z = e_id % PQ::K;
+            float pv[PQ::DSUB];
+            load_codeword<PQ::DSUB>(codebooks + (static_cast<int64_t>(bg) * PQ::LUT_ROW + e_id) * PQ::DSUB, pv);
+            float* o = w.lut + (static_cast<int64_t>(bg) * PQ::LUT_ROW + e_id) * G;
+            float e[G];
 #pragma unroll
-        for (int hh = 0; hh < G; ++hh) {
-            e[hh] = fine_entry<T>(qg + hh * kHeadDim + m * kDsub, pv, D.inv_sqrt_d);
-            store_device(w.lut_head + static_cast<int64_t>(row0 + hh) * kLutRow + m * kKsub + z, e[hh]);
+            for (int hh = 0; hh < G; ++hh) {
+                e[hh] = fine_entry<T, PQ::DSUB>(qg + hh * kHeadDim + m * PQ::DSUB, pv, D.inv_sqrt_d);
+                store_device(w.lut_head + static_cast<int64_t>(row0 + hh) * PQ::LUT_ROW + m * PQ::K + z,
+                             e[hh]);
+            }
+            store_g<G>(o, e);   // read by the next launch only: plain stores
         }
-        store_g<G>(o, e);   // read by the next launch only: plain stores
     } else {
         // coarse table: 16 lanes per list, 8 dimensions per lane
-        const int c = part - kFineParts;
+        const int c = part - fine_parts;
         const int lane16 = tid & 15;
         const int group = tid >> 4;
         float4 cv[kCoarsePer][2];
@@ -161,14 +171,14 @@ __device__ __forceinline__ void lut_role(const Dims& D, const T* __restrict__ q,
 }
 
 struct SampleLds {
-    float lut[kLutRow];   // the head's fine table [M][K]
+    float lut[kLutRowMax];   // the head's fine table [M][K]
     int hist[kHistBins];
     int ready;
     SelectScratch ss;
     BlockScratch bs;
 };
 
-template <typename T, int G>
+template <typename T, int G, typename PQ>
 __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, const Index& ix,
                                             const Work& w, float bias, uint32_t lut_target,
                                             int row, SampleLds& sm) {
@@ -197,8 +207,8 @@ __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, 
     const int rs = n_r / nrun;
     const int run_len = min(kSampleRun, rs);
     const int64_t base = static_cast<int64_t>(bg) * D.rcap;
-    const uint4* codes = reinterpret_cast<const uint4*>(ix.codes) + base;
-    uint4 cv[kSamplesPer];
+    const typename PQ::Code* codes = reinterpret_cast<const typename PQ::Code*>(ix.codes) + base;
+    typename PQ::Code cv[kSamplesPer];
     float rv[kSamplesPer];
     int jv[kSamplesPer];
     bool ok[kSamplesPer];
@@ -250,17 +260,20 @@ __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, 
     }
 
     // 3) the head's fine table into LDS, the coarse term of every sample
-    const float4* lsrc = reinterpret_cast<const float4*>(w.lut_head + static_cast<int64_t>(row) * kLutRow);
+    constexpr int kLutF4 = (PQ::LUT_ROW / 4 + kProThreads - 1) / kProThreads;   // float4 per thread
+    const float4* lsrc = reinterpret_cast<const float4*>(w.lut_head + static_cast<int64_t>(row) * PQ::LUT_ROW);
     float4 lv[kLutF4];
 #pragma unroll
-    for (int i = 0; i < kLutF4; ++i) lv[i] = lsrc[i * kProThreads + tid];
+    for (int i = 0; i < kLutF4; ++i)
+        lv[i] = lsrc[min(i * kProThreads + tid, PQ::LUT_ROW / 4 - 1)];
     const float* coarse = w.coarse + static_cast<int64_t>(bg) * D.n_list * G + hh;
     float cf[kSamplesPer];
 #pragma unroll
     for (int u = 0; u < kSamplesPer; ++u) cf[u] = coarse[jv[u] * G];
     float4* ldst = reinterpret_cast<float4*>(sm.lut);
 #pragma unroll
-    for (int i = 0; i < kLutF4; ++i) ldst[i * kProThreads + tid] = lv[i];
+    for (int i = 0; i < kLutF4; ++i)
+        if (i * kProThreads + tid < PQ::LUT_ROW / 4) ldst[i * kProThreads + tid] = lv[i];
     __syncthreads();
 
     // 4) scores of the samples
@@ -269,7 +282,7 @@ __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, 
 #pragma unroll
     for (int u = 0; u < kSamplesPer; ++u) {
         float fs[1];
-        fine_sum<1>(sm.lut, cv[u], fs);
+        fine_sum<PQ, 1>(sm.lut, cv[u], fs);
         sc[u] = pq_logit(rv[u], cf[u], fs[0]);
         if (ok[u]) {
             const uint32_t kk = float_key(sc[u]);
@@ -315,16 +328,16 @@ __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, 
     }
 }
 
-template <typename T, int G>
+template <typename T, int G, typename PQ>
 __global__ __launch_bounds__(kProThreads) void prologue_kernel(Dims D, BatchArgs ba, Index ix,
                                                                const T* __restrict__ q, Work w,
                                                                float bias, uint32_t lut_target,
                                                                int n_lut_wg) {
     __shared__ SampleLds sm;
     if (static_cast<int>(blockIdx.x) < n_lut_wg) {
-        const int per_bg = prologue_parts(D.n_list);
-        lut_role<T, G>(D, q, ix.codebooks, ix.centroids, w, blockIdx.x / per_bg,
-                       blockIdx.x % per_bg);
+        const int per_bg = prologue_parts(D.n_list, PQ::BITS);
+        lut_role<T, G, PQ>(D, q, ix.codebooks, ix.centroids, w, blockIdx.x / per_bg,
+                           blockIdx.x % per_bg);
         return;
     }
     // sample workgroup s serves group s % NG, head s / NG: workgroups are
@@ -332,42 +345,50 @@ __global__ __launch_bounds__(kProThreads) void prologue_kernel(Dims D, BatchArgs
     // multiple of 8 the G rows of a group share one L2 and its sample loads
     const int s_idx = blockIdx.x - n_lut_wg;
     const int n_grp = D.B * D.Hkv;
-    sample_role<T, G>(D, ba, ix, w, bias, lut_target, (s_idx % n_grp) * G + s_idx / n_grp, sm);
+    sample_role<T, G, PQ>(D, ba, ix, w, bias, lut_target, (s_idx % n_grp) * G + s_idx / n_grp, sm);
 }
 
-template <typename T, int G>
+template <typename T, int G, typename PQ>
 static hipError_t launch_prologue_t(const Dims& D, const BatchArgs& ba, const KV& kv,
                                     const Index& ix, const Work& w, float bias, uint32_t epoch,
                                     hipStream_t s, const KTiming& tm) {
-    const int per_bg = prologue_parts(D.n_list);
+    const int per_bg = prologue_parts(D.n_list, PQ::BITS);
     const int n_lut_wg = D.B * D.Hkv * per_bg;
     const int grid = n_lut_wg + D.B * D.Hq;
     // each call, every LUT workgroup adds 1 to its KV head's counter
     const uint32_t target = epoch * static_cast<uint32_t>(per_bg);
-    hipExtLaunchKernelGGL((prologue_kernel<T, G>), dim3(grid), dim3(kProThreads), 0, s, tm.start,
+    hipExtLaunchKernelGGL((prologue_kernel<T, G, PQ>), dim3(grid), dim3(kProThreads), 0, s, tm.start,
                           tm.stop, 0, D, ba, ix, static_cast<const T*>(kv.q), w, bias, target,
                           n_lut_wg);
     return hipGetLastError();
 }
 
-template <typename T>
+template <typename T, typename PQ>
 static hipError_t launch_prologue_g(const Dims& D, const BatchArgs& ba, const KV& kv,
                                     const Index& ix, const Work& w, float bias, uint32_t epoch,
                                     hipStream_t s, const KTiming& tm) {
     switch (D.G) {
-        case 1: return launch_prologue_t<T, 1>(D, ba, kv, ix, w, bias, epoch, s, tm);
-        case 2: return launch_prologue_t<T, 2>(D, ba, kv, ix, w, bias, epoch, s, tm);
-        case 4: return launch_prologue_t<T, 4>(D, ba, kv, ix, w, bias, epoch, s, tm);
-        case 8: return launch_prologue_t<T, 8>(D, ba, kv, ix, w, bias, epoch, s, tm);
+        case 1: return launch_prologue_t<T, 1, PQ>(D, ba, kv, ix, w, bias, epoch, s, tm);
+        case 2: return launch_prologue_t<T, 2, PQ>(D, ba, kv, ix, w, bias, epoch, s, tm);
+        case 4: return launch_prologue_t<T, 4, PQ>(D, ba, kv, ix, w, bias, epoch, s, tm);
+        case 8: return launch_prologue_t<T, 8, PQ>(D, ba, kv, ix, w, bias, epoch, s, tm);
         default: return hipErrorInvalidValue;
     }
+}
+
+template <typename PQ>
+static hipError_t launch_prologue_pq(const Dims& D, const BatchArgs& ba, const KV& kv,
+                                     const Index& ix, const Work& w, float bias, uint32_t epoch,
+                                     hipStream_t s, const KTiming& tm) {
+    return kv.bf16 ? launch_prologue_g<bf16_t, PQ>(D, ba, kv, ix, w, bias, epoch, s, tm)
+                   : launch_prologue_g<float, PQ>(D, ba, kv, ix, w, bias, epoch, s, tm);
 }
 
 hipError_t launch_prologue(const Dims& D, const BatchArgs& ba, const KV& kv, const Index& ix,
                            const Work& w, float bias, uint32_t epoch, hipStream_t s,
                            const KTiming& tm) {
-    return kv.bf16 ? launch_prologue_g<bf16_t>(D, ba, kv, ix, w, bias, epoch, s, tm)
-                   : launch_prologue_g<float>(D, ba, kv, ix, w, bias, epoch, s, tm);
+    return D.pq_bits == 4 ? launch_prologue_pq<Pq4>(D, ba, kv, ix, w, bias, epoch, s, tm)
+                          : launch_prologue_pq<Pq8>(D, ba, kv, ix, w, bias, epoch, s, tm);
 }
 
 }  // namespace pqhsa

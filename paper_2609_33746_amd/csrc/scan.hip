@@ -32,6 +32,8 @@
 // and each new pair increases at least one of them, so distinct pairs get
 // distinct segments (some segment indices stay unused). No atomics are used
 // and the result does not depend on scheduling.
+#include <type_traits>
+
 #include "device_common.h"
 #include "pq_score.h"
 #include "pqhsa_internal.h"
@@ -79,13 +81,18 @@ __device__ __forceinline__ void flush_segment(float* seg_row, float (&acc)[G]) {
     if (lane_id() < G) seg_row[lane_id()] = mine;
 }
 
-template <int G, bool kCoarseLds>
+// Floats of the group LUT as staged in LDS: Pq8 [M][K][G]; Pq4 replicated
+// (kRep4 interleaved copies, conflict-free lookups).
+template <typename PQ, int G>
+constexpr int kScanLutFloats = std::is_same<PQ, Pq4>::value ? kRep4Floats : PQ::LUT_ROW * G;
+
+template <int G, bool kCoarseLds, typename PQ>
 __global__ __launch_bounds__(kScanThreads) void scan_kernel(Dims D, BatchArgs ba, Index ix, Work w,
                                                             int nwg) {
-    // [M][K][G] group LUT at a compile-time LDS address (so that an entry
-    // address is one shift of a code byte), then, when it fits, the
-    // [n_list][G] coarse table in the dynamic part
-    __shared__ float4 lut4[kLutRow * G / 4];
+    // the group LUT at a compile-time LDS address (so that an entry address
+    // is one shift of a code), then, when it fits, the [n_list][G] coarse
+    // table in the dynamic part
+    __shared__ float4 lut4[kScanLutFloats<PQ, G> / 4];
     extern __shared__ float4 coarse4[];
     float* lut_s = reinterpret_cast<float*>(lut4);
     float* coarse_s = reinterpret_cast<float*>(coarse4);
@@ -108,12 +115,23 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(Dims D, BatchArgs ba
     const float* coarse = w.coarse + static_cast<int64_t>(bg) * D.n_list * G;
 
     // 1) the tables shared by the workgroup, and the thresholds
-    constexpr int kStage = kLutRow * G / 4 / kScanThreads;
-    static_assert(kStage * kScanThreads * 4 == kLutRow * G, "LUT staging tiling");
-    const float4* lsrc = reinterpret_cast<const float4*>(w.lut + static_cast<int64_t>(bg) * kLutRow * G);
+    constexpr int kStage = kScanLutFloats<PQ, G> / 4 / kScanThreads;
+    static_assert(kStage * kScanThreads * 4 == kScanLutFloats<PQ, G>, "LUT staging tiling");
+    const float* glut = w.lut + static_cast<int64_t>(bg) * PQ::LUT_ROW * G;
     float4 st[kStage];
 #pragma unroll
-    for (int i = 0; i < kStage; ++i) st[i] = lsrc[i * kScanThreads + tid];
+    for (int i = 0; i < kStage; ++i) {
+        const int f4 = i * kScanThreads + tid;
+        if constexpr (std::is_same<PQ, Pq4>::value) {
+            // float t of replicated row `entry` is component (f mod G) of the entry
+            const int entry = f4 / 16;
+            const int f = (f4 % 16) * 4;
+            const float* src = glut + entry * G;
+            st[i] = make_float4(src[f % G], src[(f + 1) % G], src[(f + 2) % G], src[(f + 3) % G]);
+        } else {
+            st[i] = reinterpret_cast<const float4*>(glut)[f4];
+        }
+    }
     // the coarse table, kCoarseStage float4 per thread (addresses clamped, so
     // every load is in bounds; the LDS region is padded to the full staging size)
     const int n_cf4 = D.n_list * G / 4;
@@ -139,9 +157,9 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(Dims D, BatchArgs ba
     // 2) per 64-position step: list ids, codes and norms (addresses clamped
     //    into R_b, so every load is in bounds), issued in the order the steps
     //    use them, after the tables: each step waits only for its own data
-    const uint4* codes = reinterpret_cast<const uint4*>(ix.codes) + base;
+    const typename PQ::Code* codes = reinterpret_cast<const typename PQ::Code*>(ix.codes) + base;
     uint32_t wl[kIters];   // list id << kPosBits | token id
-    uint4 cv[kIters];
+    typename PQ::Code cv[kIters];
     float rv[kIters];
 #pragma unroll
     for (int it = 0; it < kIters; ++it) {
@@ -170,7 +188,8 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(Dims D, BatchArgs ba
         if constexpr (kCoarseLds) load_coarse<G>(coarse_s + j * G, cf);
         else load_coarse<G>(coarse + j * G, cf);
         float fs[G];
-        fine_sum<G>(lut_s, cv[it], fs);
+        if constexpr (std::is_same<PQ, Pq4>::value) fine_sum_rep4<G>(lut_s, cv[it], fs);
+        else fine_sum<PQ, G>(lut_s, cv[it], fs);
         float s[G], e[G];
 #pragma unroll
         for (int hh = 0; hh < G; ++hh) {
@@ -217,27 +236,28 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(Dims D, BatchArgs ba
 
 constexpr size_t kScanLdsMax = 160 * 1024;   // LDS of one workgroup on gfx950
 
-template <int G>
+template <int G, typename PQ>
 static hipError_t launch_scan_t(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w,
                                 int nwg, hipStream_t s, const KTiming& tm) {
     const size_t cf = static_cast<size_t>(kCoarseCapF4<G>) * 16;
-    static_assert(kLutRow * G * 4 + kCoarseCapF4<G> * 16 <= kScanLdsMax, "LDS budget");
+    static_assert(kScanLutFloats<PQ, G> * 4 + kCoarseCapF4<G> * 16 <= kScanLdsMax, "LDS budget");
     const dim3 grid(D.B * D.Hkv * nwg);
     if (D.n_list * G % 4 == 0 && D.n_list * G / 4 <= kCoarseCapF4<G>)
-        hipExtLaunchKernelGGL((scan_kernel<G, true>), grid, dim3(kScanThreads), cf, s, tm.start,
+        hipExtLaunchKernelGGL((scan_kernel<G, true, PQ>), grid, dim3(kScanThreads), cf, s, tm.start,
                               tm.stop, 0, D, ba, ix, w, nwg);
     else
-        hipExtLaunchKernelGGL((scan_kernel<G, false>), grid, dim3(kScanThreads), 0, s, tm.start,
+        hipExtLaunchKernelGGL((scan_kernel<G, false, PQ>), grid, dim3(kScanThreads), 0, s, tm.start,
                               tm.stop, 0, D, ba, ix, w, nwg);
     return hipGetLastError();
 }
 
-hipError_t configure_scan() {
+template <typename PQ>
+static hipError_t configure_scan_pq() {
     // the coarse table (dynamic) can exceed the default dynamic LDS limit
-    const void* k[] = {reinterpret_cast<const void*>(&scan_kernel<1, true>),
-                       reinterpret_cast<const void*>(&scan_kernel<2, true>),
-                       reinterpret_cast<const void*>(&scan_kernel<4, true>),
-                       reinterpret_cast<const void*>(&scan_kernel<8, true>)};
+    const void* k[] = {reinterpret_cast<const void*>(&scan_kernel<1, true, PQ>),
+                       reinterpret_cast<const void*>(&scan_kernel<2, true, PQ>),
+                       reinterpret_cast<const void*>(&scan_kernel<4, true, PQ>),
+                       reinterpret_cast<const void*>(&scan_kernel<8, true, PQ>)};
     const int cap[] = {kCoarseCapF4<1> * 16, kCoarseCapF4<2> * 16, kCoarseCapF4<4> * 16,
                        kCoarseCapF4<8> * 16};
     for (int i = 0; i < 4; ++i) {
@@ -248,16 +268,28 @@ hipError_t configure_scan() {
     return hipSuccess;
 }
 
+hipError_t configure_scan() {
+    const hipError_t e = configure_scan_pq<Pq8>();
+    return e != hipSuccess ? e : configure_scan_pq<Pq4>();
+}
+
+template <typename PQ>
+static hipError_t launch_scan_pq(const Dims& D, const BatchArgs& ba, const Index& ix,
+                                 const Work& w, int nwg, hipStream_t s, const KTiming& tm) {
+    switch (D.G) {
+        case 1: return launch_scan_t<1, PQ>(D, ba, ix, w, nwg, s, tm);
+        case 2: return launch_scan_t<2, PQ>(D, ba, ix, w, nwg, s, tm);
+        case 4: return launch_scan_t<4, PQ>(D, ba, ix, w, nwg, s, tm);
+        case 8: return launch_scan_t<8, PQ>(D, ba, ix, w, nwg, s, tm);
+        default: return hipErrorInvalidValue;
+    }
+}
+
 hipError_t launch_scan(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w, int nwg,
                        hipStream_t s, const KTiming& tm) {
     if (nwg == 0) return hipSuccess;
-    switch (D.G) {
-        case 1: return launch_scan_t<1>(D, ba, ix, w, nwg, s, tm);
-        case 2: return launch_scan_t<2>(D, ba, ix, w, nwg, s, tm);
-        case 4: return launch_scan_t<4>(D, ba, ix, w, nwg, s, tm);
-        case 8: return launch_scan_t<8>(D, ba, ix, w, nwg, s, tm);
-        default: return hipErrorInvalidValue;
-    }
+    return D.pq_bits == 4 ? launch_scan_pq<Pq4>(D, ba, ix, w, nwg, s, tm)
+                          : launch_scan_pq<Pq8>(D, ba, ix, w, nwg, s, tm);
 }
 
 }  // namespace pqhsa

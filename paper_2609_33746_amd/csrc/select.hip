@@ -224,6 +224,28 @@ __device__ __forceinline__ void emit_selection(KeyAt key_at, CandAt cand_at, IsS
         cand_mass[j] = static_cast<float>(mass[j]) * kMassUnscale;
 }
 
+// Score every indexed token of a row again from its head's LUT (the re-scan
+// path): keys and words into comp_key / comp_pos in position order.
+template <typename PQ>
+__device__ __forceinline__ void rescan_row(const Dims& D, const Index& ix, const Work& w,
+                                           float* lut_s, int bg, int hh, int n_r, int64_t base,
+                                           int64_t rbase) {
+    stage_head_lut<PQ, kSelThreads>(lut_s, w.lut + static_cast<int64_t>(bg) * PQ::LUT_ROW * D.G,
+                                    D.G, hh);
+    __syncthreads();
+    const typename PQ::Code* codes = reinterpret_cast<const typename PQ::Code*>(ix.codes) + base;
+    const float* coarse = w.coarse + static_cast<int64_t>(bg) * D.n_list * D.G;
+    for (int pos = threadIdx.x; pos < n_r; pos += kSelThreads) {
+        const uint32_t wd = ix.pos_word[base + pos];
+        const int j = static_cast<int>(wd >> kPosBits);
+        float fs[1];
+        fine_sum<PQ, 1>(lut_s, codes[pos], fs);
+        const float sc = pq_logit(ix.norms[base + pos], coarse[j * D.G + hh], fs[0]);
+        w.comp_key[rbase + pos] = float_key(sc);
+        w.comp_pos[rbase + pos] = static_cast<int32_t>(wd);
+    }
+}
+
 __global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchArgs ba, Index ix,
                                                              Work w, int force_fallback) {
     extern __shared__ uint32_t lds[];
@@ -387,21 +409,11 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchArgs b
                 }
             }
         } else {
-            float* lut_s = reinterpret_cast<float*>(lds);   // 16 KB of the key area
-            stage_head_lut<kSelThreads>(lut_s, w.lut + static_cast<int64_t>(bg) * kLutRow * D.G,
-                                        D.G, hh);
-            __syncthreads();
-            const uint4* codes = reinterpret_cast<const uint4*>(ix.codes) + base;
-            const float* coarse = w.coarse + static_cast<int64_t>(bg) * D.n_list * D.G;
-            for (int pos = tid; pos < n_r; pos += kSelThreads) {
-                const uint32_t wd = ix.pos_word[base + pos];
-                const int j = static_cast<int>(wd >> kPosBits);
-                float fs[1];
-                fine_sum<1>(lut_s, codes[pos], fs);
-                const float sc = pq_logit(ix.norms[base + pos], coarse[j * D.G + hh], fs[0]);
-                w.comp_key[rbase + pos] = float_key(sc);
-                w.comp_pos[rbase + pos] = static_cast<int32_t>(wd);
-            }
+            float* lut_s = reinterpret_cast<float*>(lds);   // at most 16 KB of the key area
+            if (D.pq_bits == 4)
+                rescan_row<Pq4>(D, ix, w, lut_s, bg, hh, n_r, base, rbase);
+            else
+                rescan_row<Pq8>(D, ix, w, lut_s, bg, hh, n_r, base, rbase);
             total = n_r;
         }
         __syncthreads();

@@ -31,7 +31,7 @@ from dataclasses import dataclass, replace
 import numpy as np
 import torch
 
-__all__ = ["Workload", "WORKLOADS", "workload", "make_inputs", "ratio_topk"]
+__all__ = ["Workload", "WORKLOADS", "workload", "pq4", "make_inputs", "ratio_topk"]
 
 
 @dataclass(frozen=True)
@@ -69,6 +69,16 @@ WORKLOADS = {
 
 def workload(idx: int, **overrides) -> Workload:
     return replace(WORKLOADS[idx], **overrides)
+
+
+def pq4(idx: int, **overrides) -> Workload:
+    """Workload idx with the paper's own index setting (Section 3.1): 8
+    subspaces of 4-bit codes (16 codewords of 16 dimensions) and at most 512
+    lists. The name changes too, so the draws differ from workload idx."""
+    wl = WORKLOADS[idx]
+    kw = dict(name=wl.name + "-pq4", pq_m=8, pq_ksub=16, n_list=min(wl.n_list, 512))
+    kw.update(overrides)
+    return replace(wl, **kw)
 
 
 def ratio_topk(rho: float, n: int) -> int:

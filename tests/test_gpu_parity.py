@@ -189,6 +189,53 @@ def test_candidate_volume(n_r):
 
 
 # ---------------------------------------------------------------------------
+# the paper's own index setting: 8 subspaces of 4-bit codes (Section 3.1)
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("idx", [0, 1])
+def test_pq4_every_row(idx):
+    wl = synth.pq4(idx)
+    inp = make(wl, seed=2)
+    ctx = context(inp)
+    topk, out, sel, unsel, sc = run(ctx, inp, scores=True)
+    rows = [(b, h) for b in range(wl.batch) for h in range(wl.n_q_heads)]
+    check_rows(inp, topk, rows, out, sel, unsel, sc)
+
+
+@pytest.mark.parametrize("idx,rows_per_b", [(2, 8), (3, 3)])
+def test_pq4_full_size(idx, rows_per_b):
+    """128K with 512 lists of 4-bit codes (the paper's index), sampled rows."""
+    wl = synth.pq4(idx)
+    inp = make(wl)
+    ctx = context(inp)
+    topk, out, sel, unsel, sc = run(ctx, inp, scores=True)
+    rng = np.random.default_rng(idx)
+    rows = [(b, int(h)) for b in range(wl.batch)
+            for h in rng.choice(wl.n_q_heads, rows_per_b, replace=False)]
+    check_rows(inp, topk, rows, out, sel, unsel, sc)
+
+
+@pytest.mark.parametrize("case", ["g1-f32", "g8", "k0", "rescan", "all-candidates"])
+def test_pq4_edge_cases(case):
+    if case == "g1-f32":
+        wl = synth.pq4(0, max_seq=3000, topk=50)
+    elif case == "g8":
+        wl = synth.pq4(3, batch=1, max_seq=6000, topk=120, n_list=64)
+    elif case == "k0":
+        wl = synth.pq4(1, max_seq=5000, n_list=64, topk=0)
+    else:
+        wl = synth.pq4(1, max_seq=9000, n_list=96, topk=150)
+    inp = make(wl, seed=21)
+    ctx = context(inp)
+    if case == "rescan":
+        ctx.set_option(pqhsa.OPT_FORCE_FALLBACK, 1)
+    if case == "all-candidates":
+        ctx.set_option(pqhsa.OPT_THRESHOLD_BIAS, -1_000_000)
+    topk, out, sel, unsel, sc = run(ctx, inp, scores=True)
+    rows = [(b, h) for b in range(wl.batch) for h in range(0, wl.n_q_heads, 3)]
+    check_rows(inp, topk, rows, out, sel, unsel, sc)
+
+
+# ---------------------------------------------------------------------------
 # repeatability and the plain decode entry point
 # ---------------------------------------------------------------------------
 def test_repeatable_and_plain_decode_matches_debug():

@@ -76,3 +76,12 @@ def test_keys_follow_the_index_recipe():
     recon = cen[a] + torch.cat([cb[m][z[:, m]] for m in range(16)], dim=1)
     recon = recon * inp["norms"][0, 0].double()[:, None]
     torch.testing.assert_close(inp["k_cache"][0, 0].double(), recon, rtol=1e-5, atol=1e-5)
+
+
+def test_pq4_workloads_use_the_papers_index_setting():
+    wl = synth.pq4(2)
+    assert (wl.pq_m, wl.pq_ksub, wl.n_list) == (8, 16, 512)
+    small = synth.pq4(0, max_seq=600, topk=8)
+    inp = synth.make_inputs(small, seed=0)
+    assert inp["codes"].shape[-1] == 8 and int(inp["codes"].max()) < 16
+    assert tuple(inp["codebooks"].shape[-3:]) == (8, 16, 16)
