@@ -5,9 +5,13 @@ top-k select, exact attention + per-list background, merge) over the
 Llama-3.1-8B-shaped 128K workload: batch 1, 32 query / 8 KV heads, d = 128,
 N = 131072 bf16 K/V, 1024 lists, 16 x 8-bit PQ codes, k = 1311 (1%).
 Inputs are synthetic and resident in HBM before timing. Between timed calls
-a 512 MB buffer is overwritten so that neither the 256 MB Infinity Cache nor
-L2 holds the operator's data (a decode step of a real model runs the other
-layers in between); each call is bracketed by HIP events on its stream.
+a 1 GB buffer is read so that neither the 256 MB Infinity Cache nor L2 holds
+the operator's data (a decode step of a real model runs the other layers in
+between, whose traffic is mostly weight and KV reads); each call is
+bracketed by HIP events on its stream. Overwriting the buffer instead would
+leave the Infinity Cache full of dirty lines whose write-back competes with
+the call's reads (a plain streaming read drops from 6.4 to 4.1 TB/s on
+MI355X); that number is reported too, as us_per_call_write_flush.
 
 Prints one JSON line (rank 0) with the per-call time, throughput forms, the
 roofline of the dominant kernel, the same-chip dense decode and the CPU
@@ -29,7 +33,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
-FLUSH_BYTES = 512 << 20
+FLUSH_BYTES = 1 << 30
 COPY_CAL_BYTES = 256 << 20
 WORKLOAD = 2
 
@@ -122,10 +126,18 @@ def main() -> int:
     flush_buf = torch.empty(FLUSH_BYTES // 4, dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream()
 
+    flush_buf.fill_(1.0)
+
     def flush():
+        # a read of 4x the Infinity Cache: evicts the operator's data and
+        # leaves clean lines behind
+        torch.sum(flush_buf)
+
+    def write_flush():
         flush_buf.fill_(1.0)
 
-    def timed(fn, steps, do_flush=True):
+    def timed(fn, steps, do_flush=True, flush_fn=None):
+        flush_fn = flush_fn or flush
         times = []
         ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
               for _ in range(steps)]
@@ -133,7 +145,7 @@ def main() -> int:
         t0 = time.perf_counter()
         for i in range(steps):
             if do_flush:
-                flush()
+                flush_fn()
             ev[i][0].record(stream)
             fn()
             ev[i][1].record(stream)
@@ -181,10 +193,13 @@ def main() -> int:
 
     log("timing hot (unflushed) calls")
     t_hot, _ = timed(pq_call, args.steps, do_flush=False)
+    log("timing calls after a write flush (dirty Infinity Cache)")
+    t_pq_wf, _ = timed(pq_call, max(20, args.steps // 4), flush_fn=write_flush)
     log("timing dense decode")
     for _ in range(5):
         dense_call()
     t_dense, _ = timed(dense_call, max(20, args.steps // 4))
+    t_dense_wf, _ = timed(dense_call, 20, flush_fn=write_flush)
     # torch's own attention as a second dense reference (GQA-expanded bf16)
     sdpa_us = None
     try:
@@ -313,6 +328,7 @@ def main() -> int:
                    "n_sink": wl.n_sink, "n_local": wl.n_local, "parallelism": "single GPU"},
         "us_per_call_median": round(us_med, 3),
         "us_per_call_hot": round(float(np.mean(t_hot)) * 1e3, 3),
+        "us_per_call_write_flush": round(float(np.mean(t_pq_wf)) * 1e3, 3),
         "timed_region_wall_s": round(wall_pq, 4),
         "tokens_scanned_per_s": n_scanned / (us * 1e-6),
         "score_evals_per_s": n_scanned * G / (us * 1e-6),
@@ -327,6 +343,7 @@ def main() -> int:
                      "algorithmic_bytes": stage_bytes[dom], "traffic": pmc_traffic(dom)},
         "stage_roofline_frac": stage_roofline,
         "dense_us_per_call": round(dense_us, 3),
+        "dense_us_per_call_write_flush": round(float(np.mean(t_dense_wf)) * 1e3, 3),
         "dense_hbm_gbps": round(sum(n * wl.n_kv_heads * 2 * wl.head_dim * 2 for n in lens)
                                 / (dense_us * 1e-6) / 1e9, 1),
         "torch_sdpa_us_per_call": None if sdpa_us is None else round(sdpa_us, 3),
