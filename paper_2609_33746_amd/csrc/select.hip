@@ -150,17 +150,24 @@ __device__ __forceinline__ void copy_candidates(const uint2* __restrict__ cand, 
                                                 uint32_t& kmin, uint32_t& kmax, int* hist,
                                                 uint32_t bkmin, int bsh) {
     const int tid = threadIdx.x;
-    int cs[N];
+    // the N searches advance together, one step at a time, so their LDS
+    // reads overlap instead of forming one long dependent chain
+    int cs[N], ci[N];
 #pragma unroll
     for (int u = 0; u < N; ++u) {
-        const int ci = min(u * kSelThreads + tid, total - 1);
-        int c = 0;
+        ci[u] = min(u * kSelThreads + tid, total - 1);
+        cs[u] = 0;
+    }
 #pragma unroll
-        for (int step = kSelMaxSub / 2; step > 0; step >>= 1) {
-            const int t = c + step;
-            if (t < nsub && pre[t] <= ci) c = t;
+    for (int step = kSelMaxSub / 2; step > 0; step >>= 1) {
+        int pv[N];
+#pragma unroll
+        for (int u = 0; u < N; ++u) pv[u] = pre[min(cs[u] + step, kSelMaxSub - 1)];
+#pragma unroll
+        for (int u = 0; u < N; ++u) {
+            const int t = cs[u] + step;
+            if (t < nsub && pv[u] <= ci[u]) cs[u] = t;
         }
-        cs[u] = c;
     }
     uint2 rec[N];
 #pragma unroll
