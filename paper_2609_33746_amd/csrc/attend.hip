@@ -29,7 +29,7 @@ constexpr int kRowsPerStream = kAttnRows / kStreams;
 // rows per stream in flight in the dense kernel (fewer for large groups, which
 // hold G accumulators per lane)
 template <int G>
-struct DenseBatch { static constexpr int value = G <= 2 ? 8 : (G == 4 ? 4 : 2); };
+struct DenseBatch { static constexpr int value = G <= 2 ? 4 : 2; };
 constexpr int kMergeThreads = kHeadDim;
 
 struct Online {
@@ -399,7 +399,81 @@ hipError_t launch_merge(const Dims& D, const BatchArgs& ba, const Work& w, float
 
 // ---------------------------------------------------------------------------
 // Dense decode baseline: every cached row, all G heads of a group per K/V load.
+// Each 16-lane stream walks rows stream, stream + 16, ... of its split; the
+// loads of the next batch of rows are issued before the current batch is
+// used, so every stream keeps two batches in flight. bf16 queries stay packed
+// and the q.k products use the two-way bf16 dot instruction (fp32 sums).
 // ---------------------------------------------------------------------------
+template <typename T, int G>
+struct DenseQ;
+
+template <int G>
+struct DenseQ<bf16_t, G> {
+    uint32_t q[G][4];
+    __device__ __forceinline__ void load(const bf16_t* p, int64_t head_stride) {
+#pragma unroll
+        for (int hh = 0; hh < G; ++hh) {
+            const uint4 w = *reinterpret_cast<const uint4*>(p + hh * head_stride);
+            q[hh][0] = w.x; q[hh][1] = w.y; q[hh][2] = w.z; q[hh][3] = w.w;
+        }
+    }
+    __device__ __forceinline__ float dot(int hh, const Raw8<bf16_t>& k) const {
+        const uint32_t kw[4] = {k.w.x, k.w.y, k.w.z, k.w.w};
+        float d = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) d = dot2_bf16(q[hh][i], kw[i], d);
+        return d;
+    }
+};
+
+template <int G>
+struct DenseQ<float, G> {
+    float q[G][8];
+    __device__ __forceinline__ void load(const float* p, int64_t head_stride) {
+#pragma unroll
+        for (int hh = 0; hh < G; ++hh) Load8<float>::run(p + hh * head_stride, q[hh]);
+    }
+    __device__ __forceinline__ float dot(int hh, const Raw8<float>& k) const {
+        float kf[8];
+        k.to(kf);
+        float d = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) d = fmaf(q[hh][e], kf[e], d);
+        return d;
+    }
+};
+
+template <typename T, int R>
+__device__ __forceinline__ void dense_load(Raw8<T> (&kr)[R], Raw8<T> (&vr)[R], const T* kb,
+                                           const T* vb, int64_t sn, int base, int t1) {
+    // rows past t1 re-read row t1 - 1 (their logits are masked to -inf, so
+    // their weights are exactly 0): no branch around the loads
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+        const int64_t t = min(base + i * kStreams, t1 - 1);
+        kr[i].load(kb + t * sn);
+        vr[i].load(vb + t * sn);
+    }
+}
+
+// Fold rows base, base + 16, ... (R of them; those at or past t1 are absent)
+// into the G heads' online states.
+template <typename T, int G, int R>
+__device__ __forceinline__ void dense_rows(const DenseQ<T, G>& qv, Online (&o)[G],
+                                           const Raw8<T> (&kr)[R], const Raw8<T> (&vr)[R],
+                                           int base, int t1, float inv_sqrt_d) {
+#pragma unroll
+    for (int hh = 0; hh < G; ++hh) {
+        float l[R];
+#pragma unroll
+        for (int i = 0; i < R; ++i) {
+            const float dot = sum16(qv.dot(hh, kr[i]));
+            l[i] = base + i * kStreams < t1 ? dot * inv_sqrt_d : -__builtin_huge_valf();
+        }
+        online_push_batch<R>(o[hh], l, vr);
+    }
+}
+
 template <typename T, int G>
 __global__ __launch_bounds__(kAttnThreads) void dense_kernel(Dims D, KV kv, BatchInts lens,
                                                              float* __restrict__ partial,
@@ -417,46 +491,26 @@ __global__ __launch_bounds__(kAttnThreads) void dense_kernel(Dims D, KV kv, Batc
     const int lane16 = threadIdx.x & 15;
     const int stream = threadIdx.x >> 4;
     const float neg_inf = -__builtin_huge_valf();
-    float qv[G][8];
-#pragma unroll
-    for (int hh = 0; hh < G; ++hh)
-        Load8<T>::run(static_cast<const T*>(kv.q) +
-                          (static_cast<int64_t>(b) * D.Hq + g * G + hh) * kHeadDim + lane16 * 8,
-                      qv[hh]);
+    DenseQ<T, G> qv;
+    qv.load(static_cast<const T*>(kv.q) + (static_cast<int64_t>(b) * D.Hq + g * G) * kHeadDim +
+                lane16 * 8,
+            kHeadDim);
     const T* kb = static_cast<const T*>(kv.k) + b * kv.sb + g * kv.sh + lane16 * 8;
     const T* vb = static_cast<const T*>(kv.v) + b * kv.sb + g * kv.sh + lane16 * 8;
     Online o[G];
 #pragma unroll
     for (int hh = 0; hh < G; ++hh) online_init(o[hh]);
-    constexpr int kDenseBatch = DenseBatch<G>::value;
-    for (int base = t0 + stream; base < t1; base += kStreams * kDenseBatch) {
-        Raw8<T> kr[kDenseBatch], vr[kDenseBatch];
-#pragma unroll
-        for (int i = 0; i < kDenseBatch; ++i) {
-            const int t = base + i * kStreams;
-            if (t < t1) {
-                kr[i].load(kb + t * kv.sn);
-                vr[i].load(vb + t * kv.sn);
-            } else {
-                kr[i].zero();
-                vr[i].zero();
-            }
-        }
-#pragma unroll
-        for (int hh = 0; hh < G; ++hh) {
-            float l[kDenseBatch];
-#pragma unroll
-            for (int i = 0; i < kDenseBatch; ++i) {
-                float kf[8];
-                kr[i].to(kf);
-                float dot = 0.0f;
-#pragma unroll
-                for (int e = 0; e < 8; ++e) dot = fmaf(qv[hh][e], kf[e], dot);
-                dot = sum16(dot);
-                l[i] = base + i * kStreams < t1 ? dot * D.inv_sqrt_d : neg_inf;
-            }
-            online_push_batch<kDenseBatch>(o[hh], l, vr);
-        }
+    constexpr int R = DenseBatch<G>::value;
+    constexpr int kStep = kStreams * R;
+    // two register sets take turns: one is being loaded while the other is used
+    Raw8<T> ka[R], va[R], kc[R], vc[R];
+    dense_load<T, R>(ka, va, kb, vb, kv.sn, t0 + stream, t1);
+    for (int base = t0 + stream; base < t1; base += 2 * kStep) {
+        dense_load<T, R>(kc, vc, kb, vb, kv.sn, base + kStep, t1);
+        dense_rows<T, G, R>(qv, o, ka, va, base, t1, D.inv_sqrt_d);
+        if (base + kStep >= t1) break;
+        dense_load<T, R>(ka, va, kb, vb, kv.sn, base + 2 * kStep, t1);
+        dense_rows<T, G, R>(qv, o, kc, vc, base + kStep, t1, D.inv_sqrt_d);
     }
 #pragma unroll
     for (int hh = 0; hh < G; ++hh)
