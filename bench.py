@@ -83,6 +83,8 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--profile-only", action="store_true",
                     help="run the warm-up and timed decode calls only (for rocprofv3)")
+    ap.add_argument("--profile-dense", action="store_true",
+                    help="with --profile-only: time the dense decode instead of PQ-HSA")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="with --profile-only: also run a 256 MiB fp32 elementwise copy "
                          "(torch.neg) 5 times, whose FETCH_SIZE / WRITE_SIZE counters scale "
@@ -160,6 +162,24 @@ def main() -> int:
     def dense_call():
         ctx.dense_decode(q, kc, vc, lens, out=out_dense)
 
+    def copy_calibration():
+        n = COPY_CAL_BYTES // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        log(f"copy calibration: 5 x {COPY_CAL_BYTES >> 20} MiB read + written")
+
+    if args.profile_only and args.profile_dense:
+        for _ in range(args.warmup):
+            flush()
+            dense_call()
+        t_d, _ = timed(dense_call, args.steps)
+        log(f"dense mean {t_d.mean() * 1e3:.2f} us")
+        if args.copy_calibration:
+            copy_calibration()
+        return 0
     log(f"warmup {args.warmup}")
     for _ in range(args.warmup):
         flush()
@@ -170,13 +190,7 @@ def main() -> int:
     if args.profile_only:
         log(f"PQ-HSA mean {t_pq.mean() * 1e3:.2f} us")
         if args.copy_calibration:
-            n = COPY_CAL_BYTES // 4
-            src = torch.ones(n, dtype=torch.float32, device=dev)
-            dst = torch.empty_like(src)
-            for _ in range(5):
-                torch.neg(src, out=dst)
-            torch.cuda.synchronize()
-            log(f"copy calibration: 5 x {COPY_CAL_BYTES >> 20} MiB read + written")
+            copy_calibration()
         return 0
 
     # per-stage durations, HIP events around each kernel on the same stream
@@ -362,11 +376,11 @@ def main() -> int:
 # Kernel sources whose text decides each stage's memory traffic: a counter
 # summary taken on other sources no longer describes the kernel.
 STAGE_KERNEL = dict(prologue="prologue_kernel", scan="scan_kernel", select="select_kernel",
-                    attend="attend_kernel", merge="merge_kernel")
+                    attend="attend_kernel", merge="merge_kernel", dense="dense_kernel")
 STAGE_SOURCES = dict(
     prologue=["prologue.hip", "hist_select.h", "radix_select.h", "pq_score.h"],
     scan=["scan.hip", "pq_score.h"], select=["select.hip", "hist_select.h", "radix_select.h"],
-    attend=["attend.hip"], merge=["attend.hip"])
+    attend=["attend.hip"], merge=["attend.hip"], dense=["attend.hip"])
 COMMON_SOURCES = ["device_common.h", "pqhsa_internal.h"]
 PROFILES = os.path.join(ROOT, "profiles")
 
