@@ -303,21 +303,29 @@ __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchArgs 
 constexpr int kMergeBatch = 32;
 static_assert(kMergeBatch <= kMergeThreads, "one (m, Z) per thread");
 
-__global__ __launch_bounds__(kMergeThreads) void merge_kernel(Dims D, BatchInts n_exact_parts,
-                                                              const float* __restrict__ partial,
-                                                              int P, int first_bg, int n_bg,
-                                                              float* __restrict__ out) {
-    __shared__ float2 smz[kMergeBatch];
+// kGroups groups of kMergeThreads threads: group gi folds batches gi,
+// gi + kGroups, ... of the row's partials, then the groups' results fold in
+// LDS. One group serves the PQ-HSA rows (a few dozen partials); the dense
+// decode's hundreds of splits per row take 8.
+template <int kGroups>
+__global__ __launch_bounds__(kMergeThreads * kGroups) void merge_kernel(
+    Dims D, BatchInts n_exact_parts, const float* __restrict__ partial, int P, int first_bg,
+    int n_bg, float* __restrict__ out) {
+    __shared__ float2 smz[kGroups][kMergeBatch];
+    __shared__ float gm[kGroups], gz[kGroups];
+    __shared__ float gn[kGroups > 1 ? kGroups : 1][kMergeThreads];
     const int row = blockIdx.x;
     const int b = row / D.Hq;
-    const int t = threadIdx.x;
+    const int gi = kGroups > 1 ? static_cast<int>(threadIdx.x) / kMergeThreads : 0;
+    const int t = kGroups > 1 ? static_cast<int>(threadIdx.x) % kMergeThreads : static_cast<int>(threadIdx.x);
     const float* pr = partial + static_cast<int64_t>(row) * P * kPartStride;
     const int ne = n_exact_parts.v[b];
     const int n_used = ne + n_bg;
     const float neg_inf = -__builtin_huge_valf();
     auto part = [&](int i) { return i < ne ? i : first_bg + (i - ne); };   // i-th used partial
     float M = neg_inf, Z = 0.0f, N = 0.0f;
-    for (int i0 = 0; i0 < n_used; i0 += kMergeBatch) {
+    for (int r0 = 0; r0 < n_used; r0 += kGroups * kMergeBatch) {   // the same trip count in every group
+        const int i0 = r0 + gi * kMergeBatch;
         float2 mz = make_float2(neg_inf, 0.0f);
         if (t < kMergeBatch && i0 + t < n_used)
             mz = *reinterpret_cast<const float2*>(pr + part(i0 + t) * kPartStride);
@@ -325,18 +333,18 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(Dims D, BatchInts 
 #pragma unroll
         for (int u = 0; u < kMergeBatch; ++u)
             n[u] = i0 + u < n_used ? pr[part(i0 + u) * kPartStride + 4 + t] : 0.0f;
-        if (t < kMergeBatch) smz[t] = mz.y > 0.0f ? mz : make_float2(neg_inf, 0.0f);
+        if (t < kMergeBatch) smz[gi][t] = mz.y > 0.0f ? mz : make_float2(neg_inf, 0.0f);
         __syncthreads();
         float mb = M;
 #pragma unroll
-        for (int u = 0; u < kMergeBatch; ++u) mb = fmaxf(mb, smz[u].x);
+        for (int u = 0; u < kMergeBatch; ++u) mb = fmaxf(mb, smz[gi][u].x);
         if (mb != neg_inf) {
             const float a = __expf(M - mb);   // 0 while M = -inf
             Z *= a;
             N *= a;
 #pragma unroll
             for (int u = 0; u < kMergeBatch; ++u) {
-                const float2 e = smz[u];
+                const float2 e = smz[gi][u];
                 const float f = e.x == neg_inf ? 0.0f : __expf(e.x - mb);
                 Z = fmaf(e.y, f, Z);
                 N = f != 0.0f ? fmaf(n[u], f, N) : N;
@@ -344,6 +352,26 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(Dims D, BatchInts 
             M = mb;
         }
         __syncthreads();
+    }
+    if constexpr (kGroups > 1) {
+        if (t == 0) {
+            gm[gi] = M;
+            gz[gi] = Z;
+        }
+        gn[gi][t] = N;
+        __syncthreads();
+        if (gi != 0) return;
+        float mt = neg_inf;
+#pragma unroll
+        for (int g = 0; g < kGroups; ++g) mt = fmaxf(mt, gm[g]);
+        Z = 0.0f;
+        N = 0.0f;
+#pragma unroll
+        for (int g = 0; g < kGroups; ++g) {
+            const float f = gm[g] == neg_inf ? 0.0f : __expf(gm[g] - mt);
+            Z = fmaf(gz[g], f, Z);
+            N = fmaf(gn[g][t], f, N);
+        }
     }
     out[static_cast<int64_t>(row) * kHeadDim + t] = N / Z;
 }
@@ -381,8 +409,14 @@ hipError_t launch_attend(const Dims& D, const BatchArgs& ba, const KV& kv, const
 static hipError_t launch_merge_parts(const Dims& D, const BatchInts& ne, const float* partial,
                                      int P, int first_bg, int n_bg, float* out, hipStream_t s,
                                      const KTiming& tm) {
-    hipExtLaunchKernelGGL(merge_kernel, dim3(D.B * D.Hq), dim3(kMergeThreads), 0, s, tm.start,
-                          tm.stop, 0, D, ne, partial, P, first_bg, n_bg, out);
+    int most = 0;   // the most partials of a row
+    for (int b = 0; b < D.B; ++b) most = ne.v[b] + n_bg > most ? ne.v[b] + n_bg : most;
+    if (most <= 2 * kMergeBatch)
+        hipExtLaunchKernelGGL(merge_kernel<1>, dim3(D.B * D.Hq), dim3(kMergeThreads), 0, s, tm.start,
+                              tm.stop, 0, D, ne, partial, P, first_bg, n_bg, out);
+    else
+        hipExtLaunchKernelGGL(merge_kernel<8>, dim3(D.B * D.Hq), dim3(8 * kMergeThreads), 0, s,
+                              tm.start, tm.stop, 0, D, ne, partial, P, first_bg, n_bg, out);
     return hipGetLastError();
 }
 
