@@ -490,6 +490,37 @@ __device__ __forceinline__ void dense_load(Raw8<T> (&kr)[R], Raw8<T> (&vr)[R], c
     }
 }
 
+// Fold R rows into o with a lazily moved shift: o.m changes only when a row's
+// logit exceeds it by more than kLazyShift, so the weights exp(l - o.m) stay
+// below e^kLazyShift (far from fp32 overflow) and the rescaling of the
+// accumulators, the costliest part of a fold, is skipped for almost every
+// batch. The result equals the eager fold up to rounding.
+constexpr float kLazyShift = 8.0f;
+template <int R, typename T>
+__device__ __forceinline__ void online_push_lazy(Online& o, const float (&l)[R],
+                                                 const Raw8<T> (&v)[R]) {
+    float m_new = l[0];
+#pragma unroll
+    for (int i = 1; i < R; ++i) m_new = fmaxf(m_new, l[i]);
+    if (m_new > o.m + kLazyShift) {   // also the first present row (o.m = -inf)
+        const float a = __expf(o.m - m_new);   // 0 when o.m = -inf
+        o.z *= a;
+#pragma unroll
+        for (int t = 0; t < 8; ++t) o.acc[t] *= a;
+        o.m = m_new;
+    }
+    if (o.m == -__builtin_huge_valf()) return;   // nothing present yet
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+        const float p = __expf(l[i] - o.m);   // 0 for absent rows
+        float x[8];
+        v[i].to(x);
+        o.z += p;
+#pragma unroll
+        for (int t = 0; t < 8; ++t) o.acc[t] = fmaf(p, x[t], o.acc[t]);
+    }
+}
+
 // Fold rows base, base + 16, ... (R of them; those at or past t1 are absent)
 // into the G heads' online states.
 template <typename T, int G, int R>
@@ -504,7 +535,7 @@ __device__ __forceinline__ void dense_rows(const DenseQ<T, G>& qv, Online (&o)[G
             const float dot = sum16(qv.dot(hh, kr[i]));
             l[i] = base + i * kStreams < t1 ? dot * inv_sqrt_d : -__builtin_huge_valf();
         }
-        online_push_batch<R>(o[hh], l, vr);
+        online_push_lazy<R>(o[hh], l, vr);
     }
 }
 

@@ -41,7 +41,7 @@ constexpr uint32_t kPosMask = (1u << kPosBits) - 1u;
 constexpr int kMaxSeq = 1 << kPosBits;
 constexpr int kAttnRows = 128;     // exact-set rows per split
 constexpr int kBgLists = 64;       // lists per background workgroup
-constexpr int kDenseRows = 512;    // cache rows per dense split
+constexpr int kDenseRows = 2048;   // cache rows per dense split
 constexpr int kPartStride = 132;   // floats per partial: m, Z, pad, pad, N[128]
 constexpr int kMaxRowParts = 512;  // partials per row (exact splits + background chunks)
 
