@@ -71,6 +71,91 @@ def algorithmic_bytes(inp, topk, sel_union):
     return by
 
 
+def config_sweep(args, dev) -> int:
+    """Every synthetic workload (0-4) at its own shape: mean µs per call with
+    the caches flushed between calls (as the bench line), the dense decode of
+    the same cache, and the algorithmic bytes per stage (rooflines against the
+    8 TB/s HBM peak). One JSON line per workload."""
+    import numpy as np
+    import torch
+
+    from paper_2609_33746_amd import pqhsa, synth
+
+    flush_buf = torch.ones(FLUSH_BYTES // 4, dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def timed(fn, steps):
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(steps)]
+        for i in range(steps):
+            torch.sum(flush_buf)
+            ev[i][0].record(stream)
+            fn()
+            ev[i][1].record(stream)
+        torch.cuda.synchronize()
+        return float(np.mean([a.elapsed_time(b) for a, b in ev])) * 1e3
+
+    for idx in range(5):
+        wl = synth.workload(idx)
+        log(f"config {idx}: {wl.name}")
+        inp = synth.make_inputs(wl, seed=args.seed, device=dev)
+        topk = inp["topk"].tolist()
+        lens = inp["seq_lens"].tolist()
+        ctx = pqhsa.context_for(inp)
+        pqhsa.prepare_from(ctx, inp)
+        q, kc, vc = inp["q"], inp["k_cache"], inp["v_cache"]
+        out = torch.empty(q.shape, dtype=torch.float32, device=dev)
+        out_d = torch.empty_like(out)
+        steps = max(20, args.steps // 4)
+        for _ in range(args.warmup):
+            ctx.decode(q, kc, vc, topk, out=out)
+        us = timed(lambda: ctx.decode(q, kc, vc, topk, out=out), steps)
+        ctx.set_option(pqhsa.OPT_STAGE_TIMING, 1)
+        acc = {}
+        for _ in range(20):
+            torch.sum(flush_buf)
+            ctx.decode(q, kc, vc, topk, out=out)
+            for k_, v_ in ctx.stage_times().items():
+                acc.setdefault(k_, []).append(v_)
+        ctx.set_option(pqhsa.OPT_STAGE_TIMING, 0)
+        stage_us = {k_: float(np.mean(v_)) * 1e3 for k_, v_ in acc.items()}
+        for _ in range(3):
+            ctx.dense_decode(q, kc, vc, lens, out=out_d)
+        dense_us = timed(lambda: ctx.dense_decode(q, kc, vc, lens, out=out_d), max(10, steps // 2))
+        _, sel, _, _ = ctx.decode_debug(q, kc, vc, topk)
+        torch.cuda.synchronize()
+        G = wl.n_q_heads // wl.n_kv_heads
+        sel_c = sel.cpu().numpy()
+        union = [[int(np.unique(sel_c[b, g * G:(g + 1) * G, :topk[b]]).size) + wl.n_sink + wl.n_local
+                  for g in range(wl.n_kv_heads)] for b in range(wl.batch)]
+        by = algorithmic_bytes(inp, topk, union)
+        total = sum(by.values())
+        stage_bytes = dict(prologue=by["lut"], scan=by["scan"], select=by["select"],
+                           attend=by["attend"] + by["background"], merge=by["out"])
+        s_kv = 2 if wl.kv_dtype == "bf16" else 4
+        dense_bytes = sum(n * wl.n_kv_heads * 2 * wl.head_dim * s_kv for n in lens)
+        n_scanned = sum((n - wl.n_sink - wl.n_local) * wl.n_kv_heads for n in lens)
+        print(json.dumps({
+            "workload": wl.name, "batch": wl.batch, "n_q_heads": wl.n_q_heads,
+            "n_kv_heads": wl.n_kv_heads, "max_seq": wl.max_seq, "seq_lens": [min(lens), max(lens)],
+            "kv_dtype": wl.kv_dtype, "n_list": wl.n_list, "topk": [min(topk), max(topk)],
+            "us_per_call": round(us, 3),
+            "tokens_scanned_per_s": n_scanned / (us * 1e-6),
+            "hbm_gbps_algorithmic": round(total / (us * 1e-6) / 1e9, 1),
+            "call_roofline_frac": round(total / (us * 1e-6) / 8e12, 4),
+            "stage_us": {k_: round(v_, 3) for k_, v_ in stage_us.items()},
+            "stage_roofline_frac": {k_: round(stage_bytes[k_] / (stage_us[k_] * 1e-6) / 8e12, 4)
+                                    for k_ in stage_us},
+            "dense_us_per_call": round(dense_us, 3),
+            "dense_hbm_gbps": round(dense_bytes / (dense_us * 1e-6) / 1e9, 1),
+            "speedup_vs_dense": round(dense_us / us, 3),
+        }), flush=True)
+        ctx.close()
+        del inp, q, kc, vc, out, out_d, sel
+        torch.cuda.empty_cache()
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -83,6 +168,10 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--profile-only", action="store_true",
                     help="run the warm-up and timed decode calls only (for rocprofv3)")
+    ap.add_argument("--all-configs", action="store_true",
+                    help="instead of the bench line: one JSON line per synthetic workload "
+                         "(µs per call, tokens scanned per second, algorithmic GB/s and "
+                         "roofline fraction per stage, the same-chip dense decode beside it)")
     ap.add_argument("--profile-dense", action="store_true",
                     help="with --profile-only: time the dense decode instead of PQ-HSA")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -115,6 +204,8 @@ def main() -> int:
         return 2
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
+    if args.all_configs:
+        return config_sweep(args, dev)
     wl = synth.workload(WORKLOAD)
     log(f"generating {wl.name}")
     inp = synth.make_inputs(wl, seed=args.seed, device=dev)

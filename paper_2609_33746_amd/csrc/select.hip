@@ -27,7 +27,7 @@
 namespace pqhsa {
 
 constexpr int kNW = kSelThreads / kWave;
-constexpr int kRankCap = 512;          // boundary-bin keys ranked exactly
+constexpr int kRankCap = 128;          // boundary-bin keys ranked exactly (O(m^2 / 64) ballots)
 constexpr float kMassScale = 1099511627776.0f;       // 2^40: fixed-point weights
 constexpr float kMassUnscale = 1.0f / 1099511627776.0f;
 
