@@ -299,6 +299,26 @@ def test_dense_decode(wl):
     assert float((ref - out[b]).abs().max()) <= 2e-3 * float(ref.abs().max())
 
 
+def test_dense_decode_many_splits():
+    """More than 64 splits of 2048 rows: the merge folds the partials in
+    several thread groups at once (sampled rows, fp64 reference)."""
+    wl = small(1, max_seq=135_000, n_q_heads=4, n_kv_heads=2, n_list=32, topk=100)
+    inp = make(wl, seed=11)
+    ctx = pqhsa.context_for(inp)
+    lens = inp["seq_lens"].tolist()
+    say(f"[dense many splits] lens={lens}")
+    out = ctx.dense_decode(inp["q"], inp["k_cache"], inp["v_cache"], lens)
+    torch.cuda.synchronize()
+    G = wl.n_q_heads // wl.n_kv_heads
+    n = lens[0]
+    for h in (0, 3):
+        y = R.dense_attention_ref(inp["q"][0, h].double().cpu().numpy(),
+                                  inp["k_cache"][0, h // G, :n].double().cpu().numpy(),
+                                  inp["v_cache"][0, h // G, :n].double().cpu().numpy())
+        got = out[0, h].double().cpu().numpy()
+        assert np.max(np.abs(got - y)) / np.max(np.abs(y)) <= 2e-3, h
+
+
 # ---------------------------------------------------------------------------
 # argument checks that need a device
 # ---------------------------------------------------------------------------
