@@ -86,7 +86,11 @@ __device__ __forceinline__ void flush_segment(float* seg_row, float (&acc)[G]) {
 template <typename PQ, int G>
 constexpr int kScanLutFloats = std::is_same<PQ, Pq4>::value ? kRep4Floats : PQ::LUT_ROW * G;
 
-template <int G, bool kCoarseLds, typename PQ>
+// G = heads scored per workgroup; GT = heads of the KV head's group (the
+// stride of the group tables, masses and rows). A group of GT = 8 heads is
+// split over two workgroups of G = 4: their tables then take 80 KB of LDS,
+// so two workgroups share a CU instead of one (the codes are read twice).
+template <int G, int GT, bool kCoarseLds, typename PQ>
 __global__ __launch_bounds__(kScanThreads) void scan_kernel(Dims D, BatchArgs ba, Index ix, Work w,
                                                             int nwg) {
     // the group LUT at a compile-time LDS address (so that an entry address
@@ -96,7 +100,10 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(Dims D, BatchArgs ba
     extern __shared__ float4 coarse4[];
     float* lut_s = reinterpret_cast<float*>(lut4);
     float* coarse_s = reinterpret_cast<float*>(coarse4);
-    const int bg = blockIdx.x / nwg;
+    constexpr int kParts = GT / G;   // workgroups per (b, g) and sub-chunk range
+    static_assert(kParts * G == GT, "head split");
+    const int part = (blockIdx.x / nwg) % kParts;
+    const int bg = blockIdx.x / nwg / kParts;
     const int b = bg / D.Hkv;
     const int g = bg % D.Hkv;
     const int n_r = ba.n_r[b];
@@ -111,13 +118,14 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(Dims D, BatchArgs ba
     const int p_end = min(p_begin + kSub, n_r);
     const bool active = p_begin < n_r;
     const int64_t base = static_cast<int64_t>(bg) * D.rcap;
-    const int row0 = b * D.Hq + g * G;
-    const float* coarse = w.coarse + static_cast<int64_t>(bg) * D.n_list * G;
+    const int row0 = b * D.Hq + g * GT + part * G;
+    // this workgroup's G heads within the group tables ([..][GT] layouts)
+    const float* coarse = w.coarse + static_cast<int64_t>(bg) * D.n_list * GT + part * G;
 
     // 1) the tables shared by the workgroup, and the thresholds
     constexpr int kStage = kScanLutFloats<PQ, G> / 4 / kScanThreads;
     static_assert(kStage * kScanThreads * 4 == kScanLutFloats<PQ, G>, "LUT staging tiling");
-    const float* glut = w.lut + static_cast<int64_t>(bg) * PQ::LUT_ROW * G;
+    const float* glut = w.lut + static_cast<int64_t>(bg) * PQ::LUT_ROW * GT + part * G;
     float4 st[kStage];
 #pragma unroll
     for (int i = 0; i < kStage; ++i) {
@@ -126,10 +134,14 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(Dims D, BatchArgs ba
             // float t of replicated row `entry` is component (f mod G) of the entry
             const int entry = f4 / 16;
             const int f = (f4 % 16) * 4;
-            const float* src = glut + entry * G;
+            const float* src = glut + entry * GT;
             st[i] = make_float4(src[f % G], src[(f + 1) % G], src[(f + 2) % G], src[(f + 3) % G]);
-        } else {
+        } else if constexpr (G == GT) {
             st[i] = reinterpret_cast<const float4*>(glut)[f4];
+        } else {
+            // float4 f4 of the [M][K][G] slice: entry f4 * 4 / G, heads from (f4 * 4) mod G
+            const int f = f4 * 4;
+            st[i] = *reinterpret_cast<const float4*>(glut + (f / G) * GT + f % G);
         }
     }
     // the coarse table, kCoarseStage float4 per thread (addresses clamped, so
@@ -138,8 +150,10 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(Dims D, BatchArgs ba
     float4 cst[kCoarseStage<G>];
     if constexpr (kCoarseLds) {
 #pragma unroll
-        for (int i = 0; i < kCoarseStage<G>; ++i)
-            cst[i] = reinterpret_cast<const float4*>(coarse)[min(i * kScanThreads + tid, n_cf4 - 1)];
+        for (int i = 0; i < kCoarseStage<G>; ++i) {
+            const int f = min(i * kScanThreads + tid, n_cf4 - 1) * 4;   // list f / G, heads from f mod G
+            cst[i] = *reinterpret_cast<const float4*>(coarse + (f / G) * GT + f % G);
+        }
     }
     float tlo[G];
 #pragma unroll
@@ -168,7 +182,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(Dims D, BatchArgs ba
         cv[it] = codes[p];
         rv[it] = ix.norms[base + p];
     }
-    float* segs = w.seg_sum + (static_cast<int64_t>(bg) * D.nseg_cap + sc) * G;   // + j * G
+    float* segs = w.seg_sum + (static_cast<int64_t>(bg) * D.nseg_cap + sc) * GT + part * G;   // + j * GT
     int cur = __builtin_amdgcn_readfirstlane(static_cast<int>(wl[0] >> kPosBits));   // open segment's list
     float acc[G];
     int cbase[G];
@@ -186,7 +200,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(Dims D, BatchArgs ba
         const int j = static_cast<int>(wl[it] >> kPosBits);
         float cf[G];
         if constexpr (kCoarseLds) load_coarse<G>(coarse_s + j * G, cf);
-        else load_coarse<G>(coarse + j * G, cf);
+        else load_coarse<G>(coarse + j * GT, cf);
         float fs[G];
         if constexpr (std::is_same<PQ, Pq4>::value) fine_sum_rep4<G>(lut_s, cv[it], fs);
         else fine_sum<PQ, G>(lut_s, cv[it], fs);
@@ -203,7 +217,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(Dims D, BatchArgs ba
             const bool in = valid && j == cur;
 #pragma unroll
             for (int hh = 0; hh < G; ++hh) acc[hh] += in ? e[hh] : 0.0f;
-            flush_segment<G>(segs + cur * G, acc);
+            flush_segment<G>(segs + cur * GT, acc);
             const int nxt = __popcll(__ballot(valid && j <= cur));
             cur = __builtin_amdgcn_readlane(j, nxt);
         }
@@ -226,7 +240,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(Dims D, BatchArgs ba
             }
         }
     }
-    flush_segment<G>(segs + cur * G, acc);
+    flush_segment<G>(segs + cur * GT, acc);
     int mine = 0;
 #pragma unroll
     for (int hh = 0; hh < G; ++hh)
@@ -236,30 +250,30 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(Dims D, BatchArgs ba
 
 constexpr size_t kScanLdsMax = 160 * 1024;   // LDS of one workgroup on gfx950
 
-template <int G, typename PQ>
+template <int G, int GT, typename PQ>
 static hipError_t launch_scan_t(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w,
                                 int nwg, hipStream_t s, const KTiming& tm) {
     const size_t cf = static_cast<size_t>(kCoarseCapF4<G>) * 16;
     static_assert(kScanLutFloats<PQ, G> * 4 + kCoarseCapF4<G> * 16 <= kScanLdsMax, "LDS budget");
-    const dim3 grid(D.B * D.Hkv * nwg);
+    const dim3 grid(D.B * D.Hkv * (GT / G) * nwg);
     if (D.n_list * G % 4 == 0 && D.n_list * G / 4 <= kCoarseCapF4<G>)
-        hipExtLaunchKernelGGL((scan_kernel<G, true, PQ>), grid, dim3(kScanThreads), cf, s, tm.start,
-                              tm.stop, 0, D, ba, ix, w, nwg);
+        hipExtLaunchKernelGGL((scan_kernel<G, GT, true, PQ>), grid, dim3(kScanThreads), cf, s,
+                              tm.start, tm.stop, 0, D, ba, ix, w, nwg);
     else
-        hipExtLaunchKernelGGL((scan_kernel<G, false, PQ>), grid, dim3(kScanThreads), 0, s, tm.start,
-                              tm.stop, 0, D, ba, ix, w, nwg);
+        hipExtLaunchKernelGGL((scan_kernel<G, GT, false, PQ>), grid, dim3(kScanThreads), 0, s,
+                              tm.start, tm.stop, 0, D, ba, ix, w, nwg);
     return hipGetLastError();
 }
 
 template <typename PQ>
 static hipError_t configure_scan_pq() {
     // the coarse table (dynamic) can exceed the default dynamic LDS limit
-    const void* k[] = {reinterpret_cast<const void*>(&scan_kernel<1, true, PQ>),
-                       reinterpret_cast<const void*>(&scan_kernel<2, true, PQ>),
-                       reinterpret_cast<const void*>(&scan_kernel<4, true, PQ>),
-                       reinterpret_cast<const void*>(&scan_kernel<8, true, PQ>)};
+    const void* k[] = {reinterpret_cast<const void*>(&scan_kernel<1, 1, true, PQ>),
+                       reinterpret_cast<const void*>(&scan_kernel<2, 2, true, PQ>),
+                       reinterpret_cast<const void*>(&scan_kernel<4, 4, true, PQ>),
+                       reinterpret_cast<const void*>(&scan_kernel<4, 8, true, PQ>)};
     const int cap[] = {kCoarseCapF4<1> * 16, kCoarseCapF4<2> * 16, kCoarseCapF4<4> * 16,
-                       kCoarseCapF4<8> * 16};
+                       kCoarseCapF4<4> * 16};
     for (int i = 0; i < 4; ++i) {
         const hipError_t e =
             hipFuncSetAttribute(k[i], hipFuncAttributeMaxDynamicSharedMemorySize, cap[i]);
@@ -277,10 +291,10 @@ template <typename PQ>
 static hipError_t launch_scan_pq(const Dims& D, const BatchArgs& ba, const Index& ix,
                                  const Work& w, int nwg, hipStream_t s, const KTiming& tm) {
     switch (D.G) {
-        case 1: return launch_scan_t<1, PQ>(D, ba, ix, w, nwg, s, tm);
-        case 2: return launch_scan_t<2, PQ>(D, ba, ix, w, nwg, s, tm);
-        case 4: return launch_scan_t<4, PQ>(D, ba, ix, w, nwg, s, tm);
-        case 8: return launch_scan_t<8, PQ>(D, ba, ix, w, nwg, s, tm);
+        case 1: return launch_scan_t<1, 1, PQ>(D, ba, ix, w, nwg, s, tm);
+        case 2: return launch_scan_t<2, 2, PQ>(D, ba, ix, w, nwg, s, tm);
+        case 4: return launch_scan_t<4, 4, PQ>(D, ba, ix, w, nwg, s, tm);
+        case 8: return launch_scan_t<4, 8, PQ>(D, ba, ix, w, nwg, s, tm);   // two workgroups of 4 heads
         default: return hipErrorInvalidValue;
     }
 }
