@@ -42,7 +42,7 @@ constexpr int kCoarseLists = 128;                          // lists per coarse w
 constexpr int kCoarseGroups = kProThreads / 16;            // 16-lane groups
 constexpr int kCoarsePer = kCoarseLists / kCoarseGroups;   // lists per group: 4
 constexpr int kSamplesPer = kMaxSamples / kProThreads;     // samples per thread: 4
-constexpr int kPolls = 4;                                  // counter reads in flight
+constexpr int kPolls = 2;                                  // counter reads in flight
 constexpr int kSpinLimit = 1 << 16;                        // poll rounds before giving up
 static_assert(kFineWg * Pq8::K == kProThreads && Pq8::M / kFineWg == 8, "Pq8 fine tiling");
 static_assert(Pq4::LUT_ROW <= kProThreads, "Pq4 fine table: one codeword per thread");
@@ -227,15 +227,16 @@ __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, 
     for (int i = tid; i < kHistBins; i += kProThreads) sm.hist[i] = 0;
 
     // 2) wait for the KV head's LUT parts (bounded), with kPolls reads of
-    //    the counter in flight so that the wait ends about a quarter of a
-    //    memory round trip after the last part is counted
+    //    the counter in flight, spaced out: reads of a line slow the
+    //    increments of it (with G = 8 and four batch elements, four reads in
+    //    flight per row held the last LUT part back by several us)
     if (tid == 0) {
         int ready = 0;
         uint32_t v[kPolls];
 #pragma unroll
         for (int i = 0; i < kPolls; ++i) {
             v[i] = counter_read(w.lut_done + bg);
-            __builtin_amdgcn_s_sleep(1);
+            __builtin_amdgcn_s_sleep(16);
         }
         for (int it = 0; it < kSpinLimit && !ready; ++it) {
 #pragma unroll
@@ -243,7 +244,7 @@ __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, 
                 if (!ready && static_cast<int32_t>(v[i] - lut_target) >= 0) ready = 1;
                 if (!ready) {
                     v[i] = counter_read(w.lut_done + bg);
-                    __builtin_amdgcn_s_sleep(1);
+                    __builtin_amdgcn_s_sleep(16);
                 }
             }
         }
