@@ -26,8 +26,8 @@ namespace pqhsa {
 constexpr int kAttnThreads = 256;    // 4 waves x 4 groups of 16 lanes = 16 row streams
 constexpr int kStreams = kAttnThreads / 16;
 constexpr int kRowsPerStream = kAttnRows / kStreams;
-// rows per stream in flight in the dense kernel (fewer for large groups, which
-// hold G accumulators per lane)
+// rows per stream in one batch of the dense kernel (two batches are in
+// flight; fewer for large groups, which hold G accumulators per lane)
 template <int G>
 struct DenseBatch { static constexpr int value = G <= 2 ? 4 : 2; };
 constexpr int kMergeThreads = kHeadDim;
@@ -305,8 +305,9 @@ static_assert(kMergeBatch <= kMergeThreads, "one (m, Z) per thread");
 
 // kGroups groups of kMergeThreads threads: group gi folds batches gi,
 // gi + kGroups, ... of the row's partials, then the groups' results fold in
-// LDS. One group serves the PQ-HSA rows (a few dozen partials); the dense
-// decode's hundreds of splits per row take 8.
+// LDS. One group serves rows of up to 64 partials (the PQ-HSA rows and the
+// dense decode up to 128K rows); longer dense rows (more than 64 splits of
+// 2048 rows) take 8.
 template <int kGroups>
 __global__ __launch_bounds__(kMergeThreads * kGroups) void merge_kernel(
     Dims D, BatchInts n_exact_parts, const float* __restrict__ partial, int P, int first_bg,
