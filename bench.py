@@ -338,6 +338,18 @@ def main() -> int:
     except Exception as exc:  # noqa: BLE001 - reported, not fatal
         log(f"library dense reference unavailable: {exc}")
 
+    # the mechanism variants of the background term (Appendix B) on the same
+    # context: T drops the background workgroups, C reads one mean per (b, g)
+    variant_us = {}
+    for name, code in (("T", pqhsa.VARIANT_T), ("C", pqhsa.VARIANT_C)):
+        ctx.set_option(pqhsa.OPT_VARIANT, code)
+        for _ in range(3):
+            flush()
+            pq_call()
+        t_v, _ = timed(pq_call, max(20, args.steps // 4))
+        variant_us[name] = round(float(np.mean(t_v)) * 1e3, 3)
+    ctx.set_option(pqhsa.OPT_VARIANT, pqhsa.VARIANT_B)
+
     # the paper's own index setting on the same 128K shapes (8 subspaces of
     # 4-bit codes, 512 lists): a second PQ-HSA arm, reported beside the value
     pq4 = None
@@ -456,6 +468,7 @@ def main() -> int:
         "dense_best_arm": best_dense[0],
         "speedup_vs_dense": round(best_dense[1] / us, 3),
         "cpu_baseline": cpu,
+        "variant_us_per_call": variant_us,
         "paper_index_arm": pq4 if pq4 is None else dict(
             pq4, speedup_vs_dense=round(best_dense[1] / pq4["us_per_call"], 3)),
     }

@@ -165,12 +165,27 @@ pqhsa_status pqhsa_index_export(pqhsa_ctx* ctx, int32_t* perm, int32_t* offsets,
  *                             pqhsa_stage_times).
  *   PQHSA_OPT_THRESHOLD_BIAS  added (as value / 1000.0) to every sampled
  *                             candidate threshold; a large value starves the
- *                             candidate set and forces the fallback. */
+ *                             candidate set and forces the fallback.
+ *   PQHSA_OPT_VARIANT         the background term (the mechanism variants of
+ *                             Appendix B, on the same exact set):
+ *                             PQHSA_VARIANT_B (default) per-list value means,
+ *                             Eq. 4; PQHSA_VARIANT_T no background (softmax
+ *                             over E alone); PQHSA_VARIANT_C every list takes
+ *                             the global value mean over R_b (computed at
+ *                             prepare as sum_j |R_j| v_bar_j / |R_b|, which is
+ *                             the mean of the values over R_b when the list
+ *                             means are the means over R_j). Under
+ *                             PQHSA_VARIANT_T a row whose exact set is empty
+ *                             (no sink, no window, k = 0) has no defined
+ *                             output: its entries are NaN (0 / 0). Any other
+ *                             value is PQHSA_ERR_INVALID_ARGUMENT. */
 enum {
     PQHSA_OPT_FORCE_FALLBACK = 1,
     PQHSA_OPT_STAGE_TIMING = 2,
-    PQHSA_OPT_THRESHOLD_BIAS = 3
+    PQHSA_OPT_THRESHOLD_BIAS = 3,
+    PQHSA_OPT_VARIANT = 4
 };
+enum { PQHSA_VARIANT_B = 0, PQHSA_VARIANT_T = 1, PQHSA_VARIANT_C = 2 };
 pqhsa_status pqhsa_set_option(pqhsa_ctx* ctx, int32_t option, int64_t value);
 
 /* Stage durations (ms) of the last decode call made with stage timing on, in

@@ -44,6 +44,7 @@ struct pqhsa_ctx {
     float* centroids = nullptr;
     float* codebooks = nullptr;
     float* means = nullptr;
+    float* glob_mean = nullptr;   // [B, Hkv, d] for variant C
     int32_t* n_seq_dev = nullptr;
     int32_t* n_r_dev = nullptr;
     int scan_nwg = 0;   // scan workgroups per (b, kv head)
@@ -60,6 +61,7 @@ struct pqhsa_ctx {
     int force_fallback = 0;
     int timing = 0;
     float bias = 0.0f;
+    int variant = PQHSA_VARIANT_B;
     hipEvent_t ev[2 * kStages]{};   // start and stop of each stage's kernel
     bool events_made = false;
     bool timed_valid = false;
@@ -74,6 +76,7 @@ struct pqhsa_ctx {
         ix.centroids = centroids;
         ix.codebooks = codebooks;
         ix.means = means;
+        ix.glob_mean = glob_mean;
         ix.n_seq = n_seq_dev;
         ix.n_r = n_r_dev;
         return ix;
@@ -259,6 +262,7 @@ pqhsa_status pqhsa_create(const pqhsa_shape* shape, pqhsa_ctx** out) {
     A(dev_alloc(c, &c->centroids, BG * L * kHeadDim));
     A(dev_alloc(c, &c->codebooks, BG * codebook_floats));
     A(dev_alloc(c, &c->means, BG * L * kHeadDim));
+    A(dev_alloc(c, &c->glob_mean, BG * kHeadDim));
     A(dev_alloc(c, &c->n_seq_dev, B));
     A(dev_alloc(c, &c->n_r_dev, B));
     A(dev_alloc(c, &w.lut, BG * lut_row * G));
@@ -366,6 +370,8 @@ pqhsa_status pqhsa_index_prepare(pqhsa_ctx* c, const int32_t* seq_lens, const in
     if (e != hipSuccess) return hip_fail(c, e, "uploading the prepared index");
     e = launch_prepare_gather(D, codes, norms, c->index(), c->codes, c->norms, stream);
     if (e != hipSuccess) return hip_fail(c, e, "launching the index gather");
+    e = launch_glob_mean(D, c->index(), c->glob_mean, stream);
+    if (e != hipSuccess) return hip_fail(c, e, "launching the global value mean");
     e = hipStreamSynchronize(stream);
     if (e != hipSuccess) return hip_fail(c, e, "preparing the index");
     c->seq_lens = lens;
@@ -418,8 +424,9 @@ static pqhsa_status decode_impl(pqhsa_ctx* c, const void* q, const void* k, cons
     }
     if (e == hipSuccess) e = launch_scan(D, ba, ix, c->w, c->scan_nwg, stream, tm(1));
     if (e == hipSuccess) e = launch_select(D, ba, ix, c->w, c->force_fallback, stream, tm(2));
-    if (e == hipSuccess) e = launch_attend(D, ba, kv, ix, c->w, c->nsplit_max, stream, tm(3));
-    if (e == hipSuccess) e = launch_merge(D, ba, c->w, out, c->nsplit_max, stream, tm(4));
+    if (e == hipSuccess)
+        e = launch_attend(D, ba, kv, ix, c->w, c->nsplit_max, c->variant, stream, tm(3));
+    if (e == hipSuccess) e = launch_merge(D, ba, c->w, out, c->nsplit_max, c->variant, stream, tm(4));
     if (e != hipSuccess) return hip_fail(c, e, "enqueueing the decode kernels");
     c->timed_valid = timed;
     if (ba_out) *ba_out = ba;
@@ -492,6 +499,12 @@ pqhsa_status pqhsa_set_option(pqhsa_ctx* c, int32_t option, int64_t value) {
         case PQHSA_OPT_FORCE_FALLBACK: c->force_fallback = value != 0; return PQHSA_OK;
         case PQHSA_OPT_STAGE_TIMING: c->timing = value != 0; return PQHSA_OK;
         case PQHSA_OPT_THRESHOLD_BIAS: c->bias = static_cast<float>(value) / 1000.0f; return PQHSA_OK;
+        case PQHSA_OPT_VARIANT:
+            if (value != PQHSA_VARIANT_B && value != PQHSA_VARIANT_T && value != PQHSA_VARIANT_C)
+                return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "variant %lld is not one of B, T, C",
+                            static_cast<long long>(value));
+            c->variant = static_cast<int>(value);
+            return PQHSA_OK;
         default: return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "unknown option %d", option);
     }
 }

@@ -19,6 +19,7 @@
 //    once for the whole group.
 //  * merge_kernel: log-sum-exp of all partials of a row, y = N / Z (Eq. 5).
 #include "device_common.h"
+#include "pqhsa.h"
 #include "pqhsa_internal.h"
 
 namespace pqhsa {
@@ -106,7 +107,7 @@ __device__ __forceinline__ void block_combine(const Online& o, float* sm, float*
 template <typename T, int G>
 __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchArgs ba, KV kv,
                                                               Index ix, Work w, int nsplit_max,
-                                                              int n_bgc) {
+                                                              int n_bgc, int variant) {
     __shared__ float sm[kStreams], sz[kStreams];
     // [16 streams][d] for the exact role, [4 waves][G][d] for the background role
     __shared__ float sacc[(kStreams > 4 * G ? kStreams : 4 * G) * kHeadDim];
@@ -208,14 +209,17 @@ __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchArgs 
     // every load that does not depend on another is issued first: the list
     // means, the candidate weights and the list offsets; then the list's
     // scan segments (usually one or two) all at once
+    // variant C: every list takes the global value mean of R_b
+    const bool global_mean = variant == PQHSA_VARIANT_C;
     float2 vbar[kListsPerWave];
 #pragma unroll
     for (int i = 0; i < kListsPerWave; ++i) {
         const int j = lc * kBgLists + wave + i * kWaves;
-        vbar[i] = j < D.n_list
-                      ? *reinterpret_cast<const float2*>(
-                            ix.means + (static_cast<int64_t>(bg) * D.n_list + j) * kHeadDim + 2 * lane)
-                      : make_float2(0.f, 0.f);
+        const float* src = global_mean
+                               ? ix.glob_mean + static_cast<int64_t>(bg) * kHeadDim
+                               : ix.means + (static_cast<int64_t>(bg) * D.n_list + j) * kHeadDim;
+        vbar[i] = j < D.n_list ? *reinterpret_cast<const float2*>(src + 2 * lane)
+                               : make_float2(0.f, 0.f);
     }
     float mj[G];
     {
@@ -379,32 +383,34 @@ __global__ __launch_bounds__(kMergeThreads * kGroups) void merge_kernel(
 
 template <typename T, int G>
 static hipError_t launch_attend_t(const Dims& D, const BatchArgs& ba, const KV& kv,
-                                  const Index& ix, const Work& w, int nsplit_max, hipStream_t s,
-                                  const KTiming& tm) {
-    const int n_bgc = (D.n_list + kBgLists - 1) / kBgLists;
-    const int grid = D.B * D.Hq * nsplit_max + D.B * D.Hkv * n_bgc;
+                                  const Index& ix, const Work& w, int nsplit_max, int variant,
+                                  hipStream_t s, const KTiming& tm) {
+    const int n_bgc = (D.n_list + kBgLists - 1) / kBgLists;   // the partials' layout
+    // variant T has no background: the background workgroups are not launched
+    const int grid = D.B * D.Hq * nsplit_max + (variant == PQHSA_VARIANT_T ? 0 : D.B * D.Hkv * n_bgc);
     hipExtLaunchKernelGGL((attend_kernel<T, G>), dim3(grid), dim3(kAttnThreads), 0, s, tm.start,
-                          tm.stop, 0, D, ba, kv, ix, w, nsplit_max, n_bgc);
+                          tm.stop, 0, D, ba, kv, ix, w, nsplit_max, n_bgc, variant);
     return hipGetLastError();
 }
 
 template <typename T>
 static hipError_t launch_attend_g(const Dims& D, const BatchArgs& ba, const KV& kv,
-                                  const Index& ix, const Work& w, int nsplit_max, hipStream_t s,
-                                  const KTiming& tm) {
+                                  const Index& ix, const Work& w, int nsplit_max, int variant,
+                                  hipStream_t s, const KTiming& tm) {
     switch (D.G) {
-        case 1: return launch_attend_t<T, 1>(D, ba, kv, ix, w, nsplit_max, s, tm);
-        case 2: return launch_attend_t<T, 2>(D, ba, kv, ix, w, nsplit_max, s, tm);
-        case 4: return launch_attend_t<T, 4>(D, ba, kv, ix, w, nsplit_max, s, tm);
-        case 8: return launch_attend_t<T, 8>(D, ba, kv, ix, w, nsplit_max, s, tm);
+        case 1: return launch_attend_t<T, 1>(D, ba, kv, ix, w, nsplit_max, variant, s, tm);
+        case 2: return launch_attend_t<T, 2>(D, ba, kv, ix, w, nsplit_max, variant, s, tm);
+        case 4: return launch_attend_t<T, 4>(D, ba, kv, ix, w, nsplit_max, variant, s, tm);
+        case 8: return launch_attend_t<T, 8>(D, ba, kv, ix, w, nsplit_max, variant, s, tm);
         default: return hipErrorInvalidValue;
     }
 }
 
 hipError_t launch_attend(const Dims& D, const BatchArgs& ba, const KV& kv, const Index& ix,
-                         const Work& w, int nsplit_max, hipStream_t s, const KTiming& tm) {
-    return kv.bf16 ? launch_attend_g<bf16_t>(D, ba, kv, ix, w, nsplit_max, s, tm)
-                   : launch_attend_g<float>(D, ba, kv, ix, w, nsplit_max, s, tm);
+                         const Work& w, int nsplit_max, int variant, hipStream_t s,
+                         const KTiming& tm) {
+    return kv.bf16 ? launch_attend_g<bf16_t>(D, ba, kv, ix, w, nsplit_max, variant, s, tm)
+                   : launch_attend_g<float>(D, ba, kv, ix, w, nsplit_max, variant, s, tm);
 }
 
 static hipError_t launch_merge_parts(const Dims& D, const BatchInts& ne, const float* partial,
@@ -422,14 +428,16 @@ static hipError_t launch_merge_parts(const Dims& D, const BatchInts& ne, const f
 }
 
 hipError_t launch_merge(const Dims& D, const BatchArgs& ba, const Work& w, float* out,
-                        int nsplit_max, hipStream_t s, const KTiming& tm) {
+                        int nsplit_max, int variant, hipStream_t s, const KTiming& tm) {
     BatchInts ne;
     for (int b = 0; b < D.B; ++b) {
         const int nE = D.n_sink + D.n_local + ba.topk[b];
         ne.v[b] = (nE + kAttnRows - 1) / kAttnRows;
     }
     const int n_bgc = (D.n_list + kBgLists - 1) / kBgLists;
-    return launch_merge_parts(D, ne, w.partial, nsplit_max + n_bgc, nsplit_max, n_bgc, out, s, tm);
+    // variant T: the exact partials alone
+    return launch_merge_parts(D, ne, w.partial, nsplit_max + n_bgc, nsplit_max,
+                              variant == PQHSA_VARIANT_T ? 0 : n_bgc, out, s, tm);
 }
 
 // ---------------------------------------------------------------------------

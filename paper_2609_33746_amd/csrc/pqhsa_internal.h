@@ -85,6 +85,7 @@ struct Index {
     const float* centroids;    // [B, Hkv, n_list, d]
     const float* codebooks;    // [B, Hkv, M, K, d/M]
     const float* means;        // [B, Hkv, n_list, d]
+    const float* glob_mean;    // [B, Hkv, d] sum_j |R_j| v_bar_j / |R_b| (variant C)
     const int32_t* n_seq;      // [B]
     const int32_t* n_r;        // [B] |R_b|
 };
@@ -142,13 +143,17 @@ hipError_t launch_scan(const Dims& D, const BatchArgs& ba, const Index& ix, cons
                        hipStream_t s, const KTiming& tm = KTiming{});
 hipError_t launch_select(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w,
                          int force_fallback, hipStream_t s, const KTiming& tm = KTiming{});
+// variant: the background term, a PQHSA_VARIANT_* value
 hipError_t launch_attend(const Dims& D, const BatchArgs& ba, const KV& kv, const Index& ix,
-                         const Work& w, int nsplit_max, hipStream_t s,
+                         const Work& w, int nsplit_max, int variant, hipStream_t s,
                          const KTiming& tm = KTiming{});
 hipError_t launch_merge(const Dims& D, const BatchArgs& ba, const Work& w, float* out,
-                        int nsplit_max, hipStream_t s, const KTiming& tm = KTiming{});
+                        int nsplit_max, int variant, hipStream_t s, const KTiming& tm = KTiming{});
 hipError_t launch_dense(const Dims& D, const KV& kv, const BatchInts& lens, float* partial,
                         float* out, int nsplit_max, hipStream_t s);
+// the token-weighted mean of the list means per (b, g): the global value
+// mean over R_b of variant C
+hipError_t launch_glob_mean(const Dims& D, const Index& ix, float* glob, hipStream_t s);
 hipError_t launch_prepare_gather(const Dims& D, const uint8_t* codes_in, const float* norms_in,
                                  const Index& ix, uint8_t* codes_out, float* norms_out,
                                  hipStream_t s);

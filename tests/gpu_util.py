@@ -49,10 +49,11 @@ def run(ctx, inp, topk=None, scores=False):
     return topk, out, sel, unsel, sc
 
 
-def check_rows(inp, topk, rows, out, sel, unsel, scores=None, out_tol=OUT_TOL):
-    """Compare the listed (b, h) rows with the oracle; returns worst errors."""
+def check_rows(inp, topk, rows, out, sel, unsel, scores=None, out_tol=OUT_TOL, variant="B"):
+    """Compare the listed (b, h) rows with the oracle's mechanism `variant`;
+    returns worst errors."""
     rows = list(rows)
-    refs = R.pqhsa_batch_ref(inp, topk, rows)
+    refs = R.pqhsa_batch_ref(inp, topk, rows, variant=variant)
     worst = dict(out=0.0, score=0.0, tie_swaps=0)
     out_c = out.double().cpu().numpy()
     sel_c = sel.cpu().numpy()
@@ -82,7 +83,7 @@ def check_rows(inp, topk, rows, out, sel, unsel, scores=None, out_tol=OUT_TOL):
             others = np.setdiff1d(np.arange(sc_c.shape[2]), ref.R)
             assert np.all(np.isnan(sc_c[b, h, others]))
     if force:
-        refs.update(R.pqhsa_batch_ref(inp, topk, list(force), force_T=force))
+        refs.update(R.pqhsa_batch_ref(inp, topk, list(force), variant=variant, force_T=force))
     for (b, h), ref in refs.items():
         y = out_c[b, h]
         err = np.max(np.abs(y - ref.y)) / np.max(np.abs(ref.y))

@@ -236,6 +236,67 @@ def test_pq4_edge_cases(case):
 
 
 # ---------------------------------------------------------------------------
+# mechanism variants of the background term (Appendix B): the same exact set,
+# background dropped (T) or filled with the global value mean (C)
+# ---------------------------------------------------------------------------
+VARIANTS = {"T": pqhsa.VARIANT_T, "C": pqhsa.VARIANT_C}
+
+
+@pytest.mark.parametrize("variant", list(VARIANTS))
+@pytest.mark.parametrize("idx", [0, 1])
+def test_variant_every_row(idx, variant):
+    wl = synth.workload(idx)
+    inp = make(wl, seed=5)
+    ctx = context(inp)
+    ctx.set_option(pqhsa.OPT_VARIANT, VARIANTS[variant])
+    topk, out, sel, unsel, sc = run(ctx, inp, scores=True)
+    rows = [(b, h) for b in range(wl.batch) for h in range(0, wl.n_q_heads, 1 + idx)]
+    check_rows(inp, topk, rows, out, sel, unsel, sc, variant=variant)
+
+
+@pytest.mark.parametrize("variant", list(VARIANTS))
+def test_variant_full_size(variant):
+    """128K tokens, 512 lists, sampled rows; then back to the default."""
+    wl = synth.workload(2)
+    inp = make(wl)
+    ctx = context(inp)
+    ctx.set_option(pqhsa.OPT_VARIANT, VARIANTS[variant])
+    topk, out, sel, unsel, _ = run(ctx, inp)
+    rng = np.random.default_rng(11)
+    rows = [(b, int(h)) for b in range(wl.batch)
+            for h in rng.choice(wl.n_q_heads, 8, replace=False)]
+    check_rows(inp, topk, rows, out, sel, unsel, variant=variant)
+    ctx.set_option(pqhsa.OPT_VARIANT, pqhsa.VARIANT_B)
+    topk, out_b, sel_b, unsel_b, _ = run(ctx, inp)
+    assert torch.equal(sel_b, sel)
+    check_rows(inp, topk, rows[:4], out_b, sel_b, unsel_b)
+
+
+VARIANT_EDGE = {
+    "g8": (small(3, batch=2, max_seq=3000, n_q_heads=16, n_kv_heads=2, n_list=16, topk=60), {}),
+    "k0": (small(1, max_seq=3000, n_list=16, topk=0), {}),
+    "ragged-batch": (small(4, batch=5, max_seq=6000, ragged_min=2500, n_list=40), {}),
+    "many-empty-lists": (small(1, max_seq=2000, n_list=4096, topk=40), {}),
+    "rescan": (small(1, max_seq=5000, n_list=64, topk=97), {}),
+    "pq4": (synth.pq4(1, max_seq=9000, n_list=96, topk=150), {}),
+}
+
+
+@pytest.mark.parametrize("variant", list(VARIANTS))
+@pytest.mark.parametrize("case", list(VARIANT_EDGE))
+def test_variant_edge_cases(case, variant):
+    wl, kw = VARIANT_EDGE[case]
+    inp = make(wl, seed=9, **kw)
+    ctx = context(inp)
+    ctx.set_option(pqhsa.OPT_VARIANT, VARIANTS[variant])
+    if case == "rescan":
+        ctx.set_option(pqhsa.OPT_FORCE_FALLBACK, 1)
+    topk, out, sel, unsel, sc = run(ctx, inp, scores=True)
+    rows = [(b, h) for b in range(wl.batch) for h in range(0, wl.n_q_heads, 2)]
+    check_rows(inp, topk, rows, out, sel, unsel, sc, variant=variant)
+
+
+# ---------------------------------------------------------------------------
 # repeatability and the plain decode entry point
 # ---------------------------------------------------------------------------
 def test_repeatable_and_plain_decode_matches_debug():
@@ -346,6 +407,10 @@ def test_abi_errors_on_gpu():
         assert e.value.status == pqhsa.ERR_INVALID_ARGUMENT
     with pytest.raises(pqhsa.PQHSAError):
         ctx.dense_decode(inp["q"], inp["k_cache"], inp["v_cache"], [0])
+    for v in (-1, 3):
+        with pytest.raises(pqhsa.PQHSAError) as e:
+            ctx.set_option(pqhsa.OPT_VARIANT, v)
+        assert e.value.status == pqhsa.ERR_INVALID_ARGUMENT
     out = ctx.decode(inp["q"], inp["k_cache"], inp["v_cache"], [40])
     torch.cuda.synchronize()
     assert torch.isfinite(out).all()
