@@ -339,9 +339,10 @@ def main() -> int:
         log(f"library dense reference unavailable: {exc}")
 
     # the mechanism variants of the background term (Appendix B) on the same
-    # context: T drops the background workgroups, C reads one mean per (b, g)
+    # context: T drops the background workgroups, C reads one mean per (b, g),
+    # Bx adds a per-row weight kernel and weights the exact rows of T
     variant_us = {}
-    for name, code in (("T", pqhsa.VARIANT_T), ("C", pqhsa.VARIANT_C)):
+    for name, code in (("T", pqhsa.VARIANT_T), ("C", pqhsa.VARIANT_C), ("Bx", pqhsa.VARIANT_BX)):
         ctx.set_option(pqhsa.OPT_VARIANT, code)
         for _ in range(3):
             flush()

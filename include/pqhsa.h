@@ -174,7 +174,11 @@ pqhsa_status pqhsa_index_export(pqhsa_ctx* ctx, int32_t* perm, int32_t* offsets,
  *                             the global value mean over R_b (computed at
  *                             prepare as sum_j |R_j| v_bar_j / |R_b|, which is
  *                             the mean of the values over R_b when the list
- *                             means are the means over R_j). Under
+ *                             means are the means over R_j);
+ *                             PQHSA_VARIANT_BX list j takes the mean of its
+ *                             unselected members, (|R_j| v_bar_j - sum of v_i
+ *                             over T n R_j) / |B n R_j|, one more kernel after
+ *                             the top-k stage. Under
  *                             PQHSA_VARIANT_T a row whose exact set is empty
  *                             (no sink, no window, k = 0) has no defined
  *                             output: its entries are NaN (0 / 0). Any other
@@ -185,7 +189,7 @@ enum {
     PQHSA_OPT_THRESHOLD_BIAS = 3,
     PQHSA_OPT_VARIANT = 4
 };
-enum { PQHSA_VARIANT_B = 0, PQHSA_VARIANT_T = 1, PQHSA_VARIANT_C = 2 };
+enum { PQHSA_VARIANT_B = 0, PQHSA_VARIANT_T = 1, PQHSA_VARIANT_C = 2, PQHSA_VARIANT_BX = 3 };
 pqhsa_status pqhsa_set_option(pqhsa_ctx* ctx, int32_t option, int64_t value);
 
 /* Stage durations (ms) of the last decode call made with stage timing on, in

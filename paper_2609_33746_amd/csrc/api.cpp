@@ -45,6 +45,7 @@ struct pqhsa_ctx {
     float* codebooks = nullptr;
     float* means = nullptr;
     float* glob_mean = nullptr;   // [B, Hkv, d] for variant C
+    uint16_t* tok_list = nullptr; // [B, Hkv, rcap] for variant Bx
     int32_t* n_seq_dev = nullptr;
     int32_t* n_r_dev = nullptr;
     int scan_nwg = 0;   // scan workgroups per (b, kv head)
@@ -77,6 +78,7 @@ struct pqhsa_ctx {
         ix.codebooks = codebooks;
         ix.means = means;
         ix.glob_mean = glob_mean;
+        ix.tok_list = tok_list;
         ix.n_seq = n_seq_dev;
         ix.n_r = n_r_dev;
         return ix;
@@ -263,6 +265,7 @@ pqhsa_status pqhsa_create(const pqhsa_shape* shape, pqhsa_ctx** out) {
     A(dev_alloc(c, &c->codebooks, BG * codebook_floats));
     A(dev_alloc(c, &c->means, BG * L * kHeadDim));
     A(dev_alloc(c, &c->glob_mean, BG * kHeadDim));
+    A(dev_alloc(c, &c->tok_list, BG * rc));
     A(dev_alloc(c, &c->n_seq_dev, B));
     A(dev_alloc(c, &c->n_r_dev, B));
     A(dev_alloc(c, &w.lut, BG * lut_row * G));
@@ -279,6 +282,8 @@ pqhsa_status pqhsa_create(const pqhsa_shape* shape, pqhsa_ctx** out) {
     A(dev_alloc(c, &w.comp_pos, BQ * rc));
     A(dev_alloc(c, &w.sel_tok, BQ * D.max_topk));
     A(dev_alloc(c, &w.cand_mass, BQ * L));
+    A(dev_alloc(c, &w.bx_w, BQ * L));
+    A(dev_alloc(c, &w.bx_wsel, BQ * D.max_topk));
     A(dev_alloc(c, &w.row_shift, BQ));
     A(dev_alloc(c, &w.row_flag, BQ));
     A(dev_alloc(c, &w.partial, BQ * (c->nsplit_max + n_bgc) * kPartStride));
@@ -327,6 +332,7 @@ pqhsa_status pqhsa_index_prepare(pqhsa_ctx* c, const int32_t* seq_lens, const in
     // stable counting sort of R_b by list id, per (b, kv head)
     std::vector<int32_t> perm(BG * rc, -1), loff(BG * (L + 1));
     std::vector<uint32_t> pos_word(BG * rc, 0u);
+    std::vector<uint16_t> tok_list(BG * rc, 0);
     std::vector<int32_t> cnt(L);
     for (int b = 0; b < B; ++b) {
         for (int g = 0; g < Hkv; ++g) {
@@ -345,7 +351,9 @@ pqhsa_status pqhsa_index_prepare(pqhsa_ctx* c, const int32_t* seq_lens, const in
             std::vector<int32_t> fillp(lo, lo + L);
             int32_t* pm = perm.data() + bg * rc;
             uint32_t* pw = pos_word.data() + bg * rc;
+            uint16_t* tl = tok_list.data() + bg * rc;
             for (int i = D.n_sink; i < D.n_sink + nr[b]; ++i) {
+                tl[i] = static_cast<uint16_t>(a[i]);
                 const int p = fillp[a[i]]++;
                 pm[p] = i;
                 pw[p] = (static_cast<uint32_t>(a[i]) << kPosBits) | static_cast<uint32_t>(i);
@@ -361,6 +369,7 @@ pqhsa_status pqhsa_index_prepare(pqhsa_ctx* c, const int32_t* seq_lens, const in
     };
     H2D(c->perm, perm.data(), perm.size() * 4);
     H2D(c->pos_word, pos_word.data(), pos_word.size() * 4);
+    H2D(c->tok_list, tok_list.data(), tok_list.size() * 2);
     H2D(c->loff, loff.data(), loff.size() * 4);
     H2D(c->n_seq_dev, lens.data(), B * 4);
     H2D(c->n_r_dev, nr.data(), B * 4);
@@ -424,6 +433,7 @@ static pqhsa_status decode_impl(pqhsa_ctx* c, const void* q, const void* k, cons
     }
     if (e == hipSuccess) e = launch_scan(D, ba, ix, c->w, c->scan_nwg, stream, tm(1));
     if (e == hipSuccess) e = launch_select(D, ba, ix, c->w, c->force_fallback, stream, tm(2));
+    if (e == hipSuccess && c->variant == PQHSA_VARIANT_BX) e = launch_bx_weights(D, ba, ix, c->w, stream);
     if (e == hipSuccess)
         e = launch_attend(D, ba, kv, ix, c->w, c->nsplit_max, c->variant, stream, tm(3));
     if (e == hipSuccess) e = launch_merge(D, ba, c->w, out, c->nsplit_max, c->variant, stream, tm(4));
@@ -500,8 +510,9 @@ pqhsa_status pqhsa_set_option(pqhsa_ctx* c, int32_t option, int64_t value) {
         case PQHSA_OPT_STAGE_TIMING: c->timing = value != 0; return PQHSA_OK;
         case PQHSA_OPT_THRESHOLD_BIAS: c->bias = static_cast<float>(value) / 1000.0f; return PQHSA_OK;
         case PQHSA_OPT_VARIANT:
-            if (value != PQHSA_VARIANT_B && value != PQHSA_VARIANT_T && value != PQHSA_VARIANT_C)
-                return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "variant %lld is not one of B, T, C",
+            if (value != PQHSA_VARIANT_B && value != PQHSA_VARIANT_T && value != PQHSA_VARIANT_C &&
+                value != PQHSA_VARIANT_BX)
+                return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "variant %lld is not one of B, T, C, Bx",
                             static_cast<long long>(value));
             c->variant = static_cast<int>(value);
             return PQHSA_OK;

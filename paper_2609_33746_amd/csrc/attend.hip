@@ -104,7 +104,10 @@ __device__ __forceinline__ void block_combine(const Online& o, float* sm, float*
     __syncthreads();
 }
 
-template <typename T, int G>
+// kBx: variant Bx. The exact role subtracts, at the background's shift, the
+// selected rows weighted by their lists' W_j = M_j / |B n R_j|; the background
+// role weights list j's mean by W_j |R_j| instead of M_j.
+template <typename T, int G, bool kBx>
 __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchArgs ba, KV kv,
                                                               Index ix, Work w, int nsplit_max,
                                                               int n_bgc, int variant) {
@@ -146,6 +149,17 @@ __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchArgs 
             }
             tok[i] = t;
         }
+        float wx[kRowsPerStream];   // Bx: W of the row's list for rows of T, else 0
+        float bx_shift = neg_inf;
+        if constexpr (kBx) {
+            const float* wsel = w.bx_wsel + static_cast<int64_t>(row) * D.max_topk;
+#pragma unroll
+            for (int i = 0; i < kRowsPerStream; ++i) {
+                const int e = e0 + stream + i * kStreams;
+                wx[i] = e < e1 && e >= D.n_sink + D.n_local ? wsel[e - D.n_sink - D.n_local] : 0.0f;
+            }
+            bx_shift = w.row_shift[row];
+        }
         const T* kb = static_cast<const T*>(kv.k) + b * kv.sb + g * kv.sh + lane16 * 8;
         const T* vb = static_cast<const T*>(kv.v) + b * kv.sb + g * kv.sh + lane16 * 8;
         Raw8<T> kr[kRowsPerStream], vr[kRowsPerStream];
@@ -175,6 +189,27 @@ __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchArgs 
         Online o;
         online_init(o);
         online_push_batch<kRowsPerStream>(o, l, vr);
+        if constexpr (kBx) {
+            // fold -sum_i W_i v_i, which lives at the background's shift, into
+            // the stream's state under m' = max(m, shift) (both factors <= 1)
+            if (bx_shift != neg_inf) {
+                float c[8] = {};
+#pragma unroll
+                for (int i = 0; i < kRowsPerStream; ++i) {
+                    float x[8];
+                    vr[i].to(x);
+#pragma unroll
+                    for (int t = 0; t < 8; ++t) c[t] = fmaf(wx[i], x[t], c[t]);
+                }
+                const float m2 = fmaxf(o.m, bx_shift);
+                const float a = __expf(o.m - m2);   // 0 when o.m = -inf
+                const float f = __expf(bx_shift - m2);
+                o.z *= a;
+#pragma unroll
+                for (int t = 0; t < 8; ++t) o.acc[t] = fmaf(o.acc[t], a, -c[t] * f);
+                o.m = m2;
+            }
+        }
         block_combine(o, sm, sz, sacc,
                       w.partial + (static_cast<int64_t>(row) * P + split) * kPartStride);
         return;
@@ -221,7 +256,7 @@ __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchArgs 
         vbar[i] = j < D.n_list ? *reinterpret_cast<const float2*>(src + 2 * lane)
                                : make_float2(0.f, 0.f);
     }
-    float mj[G];
+    float mj[G], mn[G];   // M_j, and the weight of v_bar_j in N (M_j, or W_j |R_j| for Bx)
     {
         const bool ok = lane < kListsPerWave && my_j < D.n_list;
         const int jj = ok ? my_j : 0;
@@ -254,8 +289,14 @@ __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchArgs 
 #pragma unroll
             for (int hh = 0; hh < G; ++hh) below[hh] += segs[s * G + hh];
 #pragma unroll
-        for (int hh = 0; hh < G; ++hh)
+        for (int hh = 0; hh < G; ++hh) {
             mj[hh] = (ok && live[hh]) ? below[hh] * below_scale[hh] + cand[hh] : 0.0f;
+            mn[hh] = mj[hh];
+            if constexpr (kBx)
+                mn[hh] = (ok && live[hh])
+                             ? w.bx_w[static_cast<int64_t>(row0 + hh) * D.n_list + jj] * static_cast<float>(hi - lo)
+                             : 0.0f;
+        }
     }
     float Z[G], N[G][2];
 #pragma unroll
@@ -265,9 +306,10 @@ __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchArgs 
 #pragma unroll
         for (int hh = 0; hh < G; ++hh) {
             const float Mj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(mj[hh]), i));
+            const float Mn = kBx ? __int_as_float(__builtin_amdgcn_readlane(__float_as_int(mn[hh]), i)) : Mj;
             Z[hh] += Mj;
-            N[hh][0] = fmaf(Mj, vbar[i].x, N[hh][0]);
-            N[hh][1] = fmaf(Mj, vbar[i].y, N[hh][1]);
+            N[hh][0] = fmaf(Mn, vbar[i].x, N[hh][0]);
+            N[hh][1] = fmaf(Mn, vbar[i].y, N[hh][1]);
         }
     }
     // combine the 4 waves (sacc reused as [4][G][128])
@@ -296,6 +338,67 @@ __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchArgs 
             dst[4 + t] = n;
         }
     }
+}
+
+// Variant Bx (Appendix B): the background value of list j is the mean of
+// its unselected members, (|R_j| v_bar_j - sum over T n R_j of v_i) / u_j
+// with u_j = |B n R_j|. Its Eq. 4 term splits into W_j |R_j| v_bar_j minus
+// W_j times the selected rows of the list, W_j = M_j / u_j: the background
+// role takes the first part, the exact role (which gathers those rows
+// anyway) the second. One workgroup per row counts T per list, forms W_j
+// from the same masses as the background role and hands every entry of T
+// its list's W_j.
+constexpr int kBxThreads = 512;
+
+__global__ __launch_bounds__(kBxThreads) void bx_weight_kernel(Dims D, BatchArgs ba, Index ix,
+                                                               Work w) {
+    __shared__ int cnt[kMaxLists];
+    __shared__ float wl[kMaxLists];
+    const int row = blockIdx.x;
+    const int b = row / D.Hq;
+    const int h = row % D.Hq;
+    const int hh = h % D.G;
+    const int bg = b * D.Hkv + h / D.G;
+    const int k = ba.topk[b];
+    const int32_t* sel = w.sel_tok + static_cast<int64_t>(row) * D.max_topk;
+    const uint16_t* tl = ix.tok_list + static_cast<int64_t>(bg) * D.rcap;
+    auto list_of = [&](int e) { return static_cast<int>(tl[min(max(sel[e], 0), D.rcap - 1)]); };
+    for (int j = threadIdx.x; j < D.n_list; j += kBxThreads) cnt[j] = 0;
+    __syncthreads();
+    for (int e = threadIdx.x; e < k; e += kBxThreads) atomicAdd(&cnt[list_of(e)], 1);
+    __syncthreads();
+    const float neg_inf = -__builtin_huge_valf();
+    const float shift = w.row_shift[row];
+    const float tlo = w.tau_lo[row];
+    const bool live = shift != neg_inf;
+    const bool use_below = live && tlo != neg_inf && w.row_flag[row] == 0;
+    const float below_scale = use_below ? __expf(tlo - shift) : 0.0f;
+    const int32_t* loff = ix.loff + static_cast<int64_t>(bg) * (D.n_list + 1);
+    const float* segs = w.seg_sum + static_cast<int64_t>(bg) * D.nseg_cap * D.G + hh;
+    for (int j = threadIdx.x; j < D.n_list; j += kBxThreads) {
+        const int lo = loff[j], hi = loff[j + 1];
+        float Mj = 0.0f;
+        if (live) {
+            float below = 0.0f;
+            if (use_below && hi > lo)
+                for (int sg = j + lo / kSub; sg <= j + (hi - 1) / kSub; ++sg) below += segs[sg * D.G];
+            Mj = below * below_scale + w.cand_mass[static_cast<int64_t>(row) * D.n_list + j];
+        }
+        const int u = hi - lo - cnt[j];
+        const float W = u > 0 ? Mj / static_cast<float>(u) : 0.0f;
+        wl[j] = W;
+        w.bx_w[static_cast<int64_t>(row) * D.n_list + j] = W;
+    }
+    __syncthreads();
+    float* wsel = w.bx_wsel + static_cast<int64_t>(row) * D.max_topk;
+    for (int e = threadIdx.x; e < k; e += kBxThreads) wsel[e] = wl[list_of(e)];
+}
+
+hipError_t launch_bx_weights(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w,
+                             hipStream_t s, const KTiming& tm) {
+    hipExtLaunchKernelGGL(bx_weight_kernel, dim3(D.B * D.Hq), dim3(kBxThreads), 0, s, tm.start,
+                          tm.stop, 0, D, ba, ix, w);
+    return hipGetLastError();
 }
 
 // y = (sum of partials' N) / (sum of partials' Z) under one shift (Eq. 5).
@@ -388,8 +491,12 @@ static hipError_t launch_attend_t(const Dims& D, const BatchArgs& ba, const KV& 
     const int n_bgc = (D.n_list + kBgLists - 1) / kBgLists;   // the partials' layout
     // variant T has no background: the background workgroups are not launched
     const int grid = D.B * D.Hq * nsplit_max + (variant == PQHSA_VARIANT_T ? 0 : D.B * D.Hkv * n_bgc);
-    hipExtLaunchKernelGGL((attend_kernel<T, G>), dim3(grid), dim3(kAttnThreads), 0, s, tm.start,
-                          tm.stop, 0, D, ba, kv, ix, w, nsplit_max, n_bgc, variant);
+    if (variant == PQHSA_VARIANT_BX)
+        hipExtLaunchKernelGGL((attend_kernel<T, G, true>), dim3(grid), dim3(kAttnThreads), 0, s,
+                              tm.start, tm.stop, 0, D, ba, kv, ix, w, nsplit_max, n_bgc, variant);
+    else
+        hipExtLaunchKernelGGL((attend_kernel<T, G, false>), dim3(grid), dim3(kAttnThreads), 0, s,
+                              tm.start, tm.stop, 0, D, ba, kv, ix, w, nsplit_max, n_bgc, variant);
     return hipGetLastError();
 }
 

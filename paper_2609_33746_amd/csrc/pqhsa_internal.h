@@ -86,6 +86,7 @@ struct Index {
     const float* codebooks;    // [B, Hkv, M, K, d/M]
     const float* means;        // [B, Hkv, n_list, d]
     const float* glob_mean;    // [B, Hkv, d] sum_j |R_j| v_bar_j / |R_b| (variant C)
+    const uint16_t* tok_list;  // [B, Hkv, rcap] list id a_i of each token i of R (by token id)
     const int32_t* n_seq;      // [B]
     const int32_t* n_r;        // [B] |R_b|
 };
@@ -111,6 +112,9 @@ struct Work {
     float* row_shift;    // [B, Hq] shift of the background masses
     int32_t* row_flag;   // [B, Hq] 1 when the row took the re-scan path
     float* partial;      // [B, Hq, nsplit_max + n_bgc, kPartStride]
+    float* bx_w;         // [B, Hq, n_list] variant Bx: M_j / |B n R_j| (0 when no member
+                         //   of list j is unselected)
+    float* bx_wsel;      // [B, Hq, max_topk] variant Bx: bx_w of the list of each entry of T
 };
 
 struct KV {
@@ -147,6 +151,10 @@ hipError_t launch_select(const Dims& D, const BatchArgs& ba, const Index& ix, co
 hipError_t launch_attend(const Dims& D, const BatchArgs& ba, const KV& kv, const Index& ix,
                          const Work& w, int nsplit_max, int variant, hipStream_t s,
                          const KTiming& tm = KTiming{});
+// variant Bx, after the select: the per-list weights bx_w and, for every
+// selected entry, the weight of its list (bx_wsel)
+hipError_t launch_bx_weights(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w,
+                             hipStream_t s, const KTiming& tm = KTiming{});
 hipError_t launch_merge(const Dims& D, const BatchArgs& ba, const Work& w, float* out,
                         int nsplit_max, int variant, hipStream_t s, const KTiming& tm = KTiming{});
 hipError_t launch_dense(const Dims& D, const KV& kv, const BatchInts& lens, float* partial,

@@ -21,7 +21,7 @@ HEADER = os.path.join(os.path.dirname(_HERE), "include", "pqhsa.h")
 OK, ERR_INVALID_ARGUMENT, ERR_UNSUPPORTED, ERR_HIP, ERR_OUT_OF_MEMORY, ERR_NOT_PREPARED = range(6)
 F32, BF16 = 0, 1
 OPT_FORCE_FALLBACK, OPT_STAGE_TIMING, OPT_THRESHOLD_BIAS, OPT_VARIANT = 1, 2, 3, 4
-VARIANT_B, VARIANT_T, VARIANT_C = 0, 1, 2
+VARIANT_B, VARIANT_T, VARIANT_C, VARIANT_BX = 0, 1, 2, 3
 STAGES = ("prologue", "scan", "select", "attend", "merge")
 
 

@@ -237,9 +237,10 @@ def test_pq4_edge_cases(case):
 
 # ---------------------------------------------------------------------------
 # mechanism variants of the background term (Appendix B): the same exact set,
-# background dropped (T) or filled with the global value mean (C)
+# background dropped (T), filled with the global value mean (C) or with the
+# mean of each list's unselected members (Bx)
 # ---------------------------------------------------------------------------
-VARIANTS = {"T": pqhsa.VARIANT_T, "C": pqhsa.VARIANT_C}
+VARIANTS = {"T": pqhsa.VARIANT_T, "C": pqhsa.VARIANT_C, "Bx": pqhsa.VARIANT_BX}
 
 
 @pytest.mark.parametrize("variant", list(VARIANTS))
@@ -407,7 +408,7 @@ def test_abi_errors_on_gpu():
         assert e.value.status == pqhsa.ERR_INVALID_ARGUMENT
     with pytest.raises(pqhsa.PQHSAError):
         ctx.dense_decode(inp["q"], inp["k_cache"], inp["v_cache"], [0])
-    for v in (-1, 3):
+    for v in (-1, 4):
         with pytest.raises(pqhsa.PQHSAError) as e:
             ctx.set_option(pqhsa.OPT_VARIANT, v)
         assert e.value.status == pqhsa.ERR_INVALID_ARGUMENT
