@@ -351,6 +351,32 @@ def main() -> int:
         variant_us[name] = round(float(np.mean(t_v)) * 1e3, 3)
     ctx.set_option(pqhsa.OPT_VARIANT, pqhsa.VARIANT_B)
 
+    # the same call on a paged cache (pages of 16 tokens at random page
+    # indices, K and V interleaved in each page as in vLLM's layout)
+    paged_us = None
+    if not args.no_pq4:
+        B_, Hkv_, N_, d_ = kc.shape
+        page = 16
+        nb = -(-N_ // page)
+        gen = torch.Generator().manual_seed(args.seed)
+        table = torch.randperm(B_ * nb + 5, generator=gen)[:B_ * nb].reshape(B_, nb)
+        pages = torch.zeros((B_ * nb + 5, Hkv_, page, 2 * d_), dtype=kc.dtype, device=dev)
+        for lo, src in ((0, kc), (d_, vc)):
+            x = torch.nn.functional.pad(src, (0, 0, 0, nb * page - N_))
+            pages[table.reshape(-1).to(dev), :, :, lo:lo + d_] = \
+                x.reshape(B_, Hkv_, nb, page, d_).permute(0, 2, 1, 3, 4).reshape(B_ * nb, Hkv_, page, d_)
+        table = table.to(torch.int32).to(dev)
+        kp, vp = pages[..., :d_], pages[..., d_:]
+
+        def paged_call():
+            ctx.decode_paged(q, kp, vp, table, page, topk, out=out)
+        for _ in range(3):
+            flush()
+            paged_call()
+        t_pg, _ = timed(paged_call, max(20, args.steps // 4))
+        paged_us = {"page_size": page, "us_per_call": round(float(np.mean(t_pg)) * 1e3, 3)}
+        del pages, kp, vp
+
     # the paper's own index setting on the same 128K shapes (8 subspaces of
     # 4-bit codes, 512 lists): a second PQ-HSA arm, reported beside the value
     pq4 = None
@@ -470,6 +496,7 @@ def main() -> int:
         "speedup_vs_dense": round(best_dense[1] / us, 3),
         "cpu_baseline": cpu,
         "variant_us_per_call": variant_us,
+        "paged_kv_arm": paged_us,
         "paper_index_arm": pq4 if pq4 is None else dict(
             pq4, speedup_vs_dense=round(best_dense[1] / pq4["us_per_call"], 3)),
     }

@@ -122,6 +122,28 @@ pqhsa_status pqhsa_decode(pqhsa_ctx* ctx, const void* q, const void* k_cache,
                           const void* v_cache, const int64_t* kv_strides,
                           const int32_t* topk, float* out, hipStream_t stream);
 
+/* pqhsa_decode reading a paged KV cache in place (the serving setting of
+ * Section 4: vLLM-style pages named by a block table). Token t of sequence b
+ * and KV head g sits at element
+ *   block_table[b * max_blocks + t / page_size] * page_strides[0]
+ *   + g * page_strides[1] + (t % page_size) * page_strides[2]
+ * of k_pages (keys) and of v_pages (values); the last dimension d is
+ * contiguous. An interleaved page layout [pages, Hkv, page_size, 2d] is
+ * passed as k_pages = base, v_pages = base + d with page_strides
+ * (Hkv * page_size * 2d, page_size * 2d, 2d).
+ *   block_table DEVICE int32 [B, max_blocks]: page index of each logical
+ *               block; entries past a sequence's last block are not read.
+ *               The page indices are not validated.
+ *   page_size   a power of two in [1, 2^20]; max_blocks * page_size must
+ *               cover the longest prepared sequence.
+ * Other arguments, and the result, as in pqhsa_decode (bit-identical to it
+ * on the same rows). Asynchronous; allocates nothing. */
+pqhsa_status pqhsa_decode_paged(pqhsa_ctx* ctx, const void* q, const void* k_pages,
+                                const void* v_pages, const int64_t* page_strides,
+                                const int32_t* block_table, int32_t max_blocks,
+                                int32_t page_size, const int32_t* topk, float* out,
+                                hipStream_t stream);
+
 /* pqhsa_decode plus diagnostics for parity checks (synchronises `stream`).
  *   selected            int32 [B, Hq, max_topk] or NULL: the token ids of T,
  *                       ascending, padded with -1

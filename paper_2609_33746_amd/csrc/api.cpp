@@ -182,6 +182,27 @@ pqhsa_status check_kv(pqhsa_ctx* c, const void* q, const void* k, const void* v,
     return PQHSA_OK;
 }
 
+// A paged cache: the strides are those of (page, kv head, token in page);
+// page_size a power of two, and the block table long enough for the longest
+// prepared sequence.
+pqhsa_status check_pages(pqhsa_ctx* c, const int32_t* block_table, int32_t max_blocks,
+                         int32_t page_size, KV* kv) {
+    if (!block_table) return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "block_table is NULL");
+    if (page_size < 1 || page_size > (1 << 20) || (page_size & (page_size - 1)))
+        return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "page_size %d is not a power of two in [1, 2^20]",
+                    page_size);
+    int n_max = 0;
+    for (int n : c->seq_lens) n_max = std::max(n_max, n);
+    if (max_blocks < 1 || static_cast<int64_t>(max_blocks) * page_size < n_max)
+        return fail(c, PQHSA_ERR_INVALID_ARGUMENT,
+                    "max_blocks %d x page_size %d does not cover the longest sequence (%d tokens)",
+                    max_blocks, page_size, n_max);
+    kv->bt = block_table;
+    kv->max_blocks = max_blocks;
+    kv->page_shift = __builtin_ctz(static_cast<unsigned>(page_size));
+    return PQHSA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -392,15 +413,21 @@ pqhsa_status pqhsa_index_prepare(pqhsa_ctx* c, const int32_t* seq_lens, const in
     return PQHSA_OK;
 }
 
+// block_table null: contiguous cache; else paged (see check_pages)
 static pqhsa_status decode_impl(pqhsa_ctx* c, const void* q, const void* k, const void* v,
-                                const int64_t* strides, const int32_t* topk, float* out,
-                                hipStream_t stream, BatchArgs* ba_out) {
+                                const int64_t* strides, const int32_t* block_table,
+                                int32_t max_blocks, int32_t page_size, const int32_t* topk,
+                                float* out, hipStream_t stream, BatchArgs* ba_out) {
     if (!c) return fail(nullptr, PQHSA_ERR_INVALID_ARGUMENT, "ctx is NULL");
     c->err.clear();
     if (!c->prepared) return fail(c, PQHSA_ERR_NOT_PREPARED, "pqhsa_index_prepare has not succeeded");
     KV kv;
     pqhsa_status st = check_kv(c, q, k, v, strides, out, &kv);
     if (st != PQHSA_OK) return st;
+    if (block_table) {
+        st = check_pages(c, block_table, max_blocks, page_size, &kv);
+        if (st != PQHSA_OK) return st;
+    }
     if (!topk) return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "topk is NULL");
     st = check_device(c);
     if (st != PQHSA_OK) return st;
@@ -446,7 +473,16 @@ static pqhsa_status decode_impl(pqhsa_ctx* c, const void* q, const void* k, cons
 pqhsa_status pqhsa_decode(pqhsa_ctx* c, const void* q, const void* k, const void* v,
                           const int64_t* kv_strides, const int32_t* topk, float* out,
                           hipStream_t stream) {
-    return decode_impl(c, q, k, v, kv_strides, topk, out, stream, nullptr);
+    return decode_impl(c, q, k, v, kv_strides, nullptr, 0, 0, topk, out, stream, nullptr);
+}
+
+pqhsa_status pqhsa_decode_paged(pqhsa_ctx* c, const void* q, const void* k_pages,
+                                const void* v_pages, const int64_t* page_strides,
+                                const int32_t* block_table, int32_t max_blocks, int32_t page_size,
+                                const int32_t* topk, float* out, hipStream_t stream) {
+    if (c && !block_table) return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "block_table is NULL");
+    return decode_impl(c, q, k_pages, v_pages, page_strides, block_table, max_blocks, page_size,
+                       topk, out, stream, nullptr);
 }
 
 pqhsa_status pqhsa_decode_debug(pqhsa_ctx* c, const void* q, const void* k, const void* v,
@@ -459,7 +495,7 @@ pqhsa_status pqhsa_decode_debug(pqhsa_ctx* c, const void* q, const void* k, cons
                 return fail(c, PQHSA_ERR_UNSUPPORTED, "the debug call sorts at most 8192 selected tokens per row");
     }
     BatchArgs ba{};
-    pqhsa_status st = decode_impl(c, q, k, v, kv_strides, topk, out, stream, &ba);
+    pqhsa_status st = decode_impl(c, q, k, v, kv_strides, nullptr, 0, 0, topk, out, stream, &ba);
     if (st != PQHSA_OK) return st;
     hipError_t e = launch_debug(c->D, ba, c->index(), c->w, selected, unselected_per_list, scores, stream);
     if (e == hipSuccess) e = hipStreamSynchronize(stream);

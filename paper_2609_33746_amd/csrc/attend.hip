@@ -160,14 +160,17 @@ __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchArgs 
             }
             bx_shift = w.row_shift[row];
         }
-        const T* kb = static_cast<const T*>(kv.k) + b * kv.sb + g * kv.sh + lane16 * 8;
-        const T* vb = static_cast<const T*>(kv.v) + b * kv.sb + g * kv.sh + lane16 * 8;
+        const T* kb = static_cast<const T*>(kv.k) + lane16 * 8;
+        const T* vb = static_cast<const T*>(kv.v) + lane16 * 8;
+        int64_t roff[kRowsPerStream];   // a paged cache adds one block-table read
+#pragma unroll
+        for (int i = 0; i < kRowsPerStream; ++i) roff[i] = tok[i] >= 0 ? kv_row(kv, b, g, tok[i]) : 0;
         Raw8<T> kr[kRowsPerStream], vr[kRowsPerStream];
 #pragma unroll
         for (int i = 0; i < kRowsPerStream; ++i) {
             if (tok[i] >= 0) {
-                kr[i].load(kb + tok[i] * kv.sn);
-                vr[i].load(vb + tok[i] * kv.sn);
+                kr[i].load(kb + roff[i]);
+                vr[i].load(vb + roff[i]);
             } else {
                 kr[i].zero();
                 vr[i].zero();

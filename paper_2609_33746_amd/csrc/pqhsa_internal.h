@@ -117,13 +117,28 @@ struct Work {
     float* bx_wsel;      // [B, Hq, max_topk] variant Bx: bx_w of the list of each entry of T
 };
 
+// The caller's KV cache. Contiguous: token t of (b, g) at b sb + g sh + t sn
+// elements. Paged (bt != null): at bt[b max_blocks + t >> page_shift] sb +
+// g sh + (t & (2^page_shift - 1)) sn, sb then being the page stride.
 struct KV {
     const void* q;
     const void* k;
     const void* v;
-    int64_t sb, sh, sn;   // element strides of (b, kv head, token)
+    int64_t sb, sh, sn;   // element strides of (b or page, kv head, token)
     int bf16;
+    const int32_t* bt = nullptr;   // [B, max_blocks] page of each logical block
+    int max_blocks = 0;
+    int page_shift = 0;
 };
+
+// Element offset of token t of (b, g) in the cache (t >= 0).
+__device__ __forceinline__ int64_t kv_row(const KV& kv, int b, int g, int t) {
+    if (kv.bt) {
+        const int pg = kv.bt[static_cast<int64_t>(b) * kv.max_blocks + (t >> kv.page_shift)];
+        return pg * kv.sb + g * kv.sh + (t & ((1 << kv.page_shift) - 1)) * kv.sn;
+    }
+    return b * kv.sb + g * kv.sh + t * kv.sn;
+}
 
 // --- launchers (each returns the launch status) -----------------------
 // Kernel attributes (large dynamic LDS) for the current device; called once

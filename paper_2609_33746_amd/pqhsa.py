@@ -57,6 +57,7 @@ def load_library(build_if_missing: bool = True) -> ctypes.CDLL:
         "pqhsa_destroy": ([P], None),
         "pqhsa_index_prepare": ([P] + [P] * 7 + [P], I32),
         "pqhsa_decode": ([P, P, P, P, P, P, P, P], I32),
+        "pqhsa_decode_paged": ([P, P, P, P, P, P, I32, I32, P, P, P], I32),
         "pqhsa_decode_debug": ([P, P, P, P, P, P, P, P, P, P, P], I32),
         "pqhsa_dense_decode": ([P, P, P, P, P, P, P, P], I32),
         "pqhsa_index_export": ([P, P, P, P], I32),
@@ -156,6 +157,22 @@ class PQHSA:
         out = self._out(q, out)
         self._check(self.lib.pqhsa_decode(self.ctx, _ptr(q), _ptr(k_cache), _ptr(v_cache), strides,
                                           _host_i32(list(topk)), _ptr(out), _stream()))
+        return out
+
+    def decode_paged(self, q, k_pages, v_pages, block_table, page_size, topk, out=None):
+        """Decode from a paged cache: k_pages / v_pages [n_pages, Hkv, page_size, d]
+        (views of one interleaved tensor allowed), block_table int32 [B, max_blocks]."""
+        strides = self._kv(k_pages, v_pages)
+        if k_pages.shape[2] != page_size:
+            raise ValueError("k_pages.shape[2] must equal page_size")
+        bt = self._dev(block_table, torch.int32, "block_table")
+        if bt.dim() != 2 or bt.shape[0] != self.shape.batch:
+            raise ValueError("block_table must be [batch, max_blocks]")
+        q = self._dev(q, self.dtype, "q")
+        out = self._out(q, out)
+        self._check(self.lib.pqhsa_decode_paged(
+            self.ctx, _ptr(q), _ptr(k_pages), _ptr(v_pages), strides, _ptr(bt), int(bt.shape[1]),
+            int(page_size), _host_i32(list(topk)), _ptr(out), _stream()))
         return out
 
     def decode_debug(self, q, k_cache, v_cache, topk, out=None, want_scores=False):

@@ -298,6 +298,55 @@ def test_variant_edge_cases(case, variant):
 
 
 # ---------------------------------------------------------------------------
+# paged KV cache read in place (block table, interleaved K|V pages)
+# ---------------------------------------------------------------------------
+def paged_copy(k, v, page, seed, spare=5):
+    """Scatter the [B, Hkv, N, d] caches into pages [n_pages, Hkv, page, 2d]
+    (K in the first d, V in the last d) at a random page per logical block."""
+    B, Hkv, N, d = k.shape
+    nb = -(-N // page)
+    gen = torch.Generator().manual_seed(seed)
+    n_pages = B * nb + spare
+    table = torch.randperm(n_pages, generator=gen)[:B * nb].reshape(B, nb)
+    pages = torch.full((n_pages, Hkv, page, 2 * d), float("nan"), dtype=k.dtype, device=k.device)
+    for half, src in ((slice(0, d), k), (slice(d, 2 * d), v)):
+        x = torch.nn.functional.pad(src, (0, 0, 0, nb * page - N))
+        x = x.reshape(B, Hkv, nb, page, d).permute(0, 2, 1, 3, 4).reshape(B * nb, Hkv, page, d)
+        pages[table.reshape(-1).to(k.device), :, :, half] = x
+    return pages[..., :d], pages[..., d:], table.to(torch.int32).to(k.device)
+
+
+PAGED = {
+    "tiny-p16": (small(0), 16, "B"),
+    "32k-p16": (small(1), 16, "B"),
+    "32k-p1": (small(1, max_seq=6000), 1, "B"),
+    "ragged-p64": (small(4, batch=5, max_seq=6000, ragged_min=2500, n_list=40), 64, "B"),
+    "g8-p32-bx": (small(3, batch=2, max_seq=3000, n_q_heads=16, n_kv_heads=2, n_list=16, topk=60), 32, "Bx"),
+    "128k-p16": (small(2), 16, "B"),
+}
+
+
+@pytest.mark.parametrize("case", list(PAGED))
+def test_paged_kv_matches_contiguous(case):
+    wl, page, variant = PAGED[case]
+    inp = make(wl, seed=4)
+    ctx = context(inp)
+    ctx.set_option(pqhsa.OPT_VARIANT, VARIANTS.get(variant, pqhsa.VARIANT_B))
+    topk, out, sel, unsel, _ = run(ctx, inp)
+    kp, vp, table = paged_copy(inp["k_cache"], inp["v_cache"], page, seed=len(case))
+    say(f"[paged] page={page} pages={kp.shape[0]} table={tuple(table.shape)}")
+    out_p = ctx.decode_paged(inp["q"], kp, vp, table, page, topk)
+    torch.cuda.synchronize()
+    assert torch.equal(out_p, out)
+    rows = [(b, h) for b in range(wl.batch) for h in range(0, wl.n_q_heads, 5)][:12]
+    check_rows(inp, topk, rows, out_p, sel, unsel, variant=variant)
+    with pytest.raises(pqhsa.PQHSAError) as e:   # a table too short for the longest sequence
+        n_max = int(inp["seq_lens"].max())
+        ctx.decode_paged(inp["q"], kp, vp, table[:, :(n_max - 1) // page].contiguous(), page, topk)
+    assert e.value.status == pqhsa.ERR_INVALID_ARGUMENT
+
+
+# ---------------------------------------------------------------------------
 # repeatability and the plain decode entry point
 # ---------------------------------------------------------------------------
 def test_repeatable_and_plain_decode_matches_debug():
