@@ -18,6 +18,12 @@ Everything is written from the paper's statement of the method:
   list value means; Eq. (5): the output.
 * Appendix A ("Budgets"): 4 sinks, a 128-token local window, k = ceil(rho |R|)
   and the exact-set size rounded up to whole pages of 16 tokens.
+* Section 3.1 (the index): a key k = r u is stored as its norm r, the list
+  a of the centroid nearest to its direction u, and the codes of the
+  residual u - c_a, the nearest codeword in each of the M subspaces
+  (`encode_ref`). Section 3.3 (execution path): later tokens are encoded
+  into the existing lists without re-clustering, and each update refreshes
+  the list means (`update_ref`).
 * Appendix B (variant definitions, Table "mechanism variants"): variants T
   (no background), C (token-weighted global value mean) and Bx (mean of the
   unselected members of each list).
@@ -25,7 +31,11 @@ Everything is written from the paper's statement of the method:
 Readings where the paper is silent:
 * the top-k tie-break is the smaller token id;
 * r_q = 0 gives a score of 0 for every indexed token;
-* an empty list, or a list whose members are all selected, contributes 0.
+* an empty list, or a list whose members are all selected, contributes 0;
+* "nearest" is the smallest squared Euclidean distance, ties going to the
+  smaller list id or codeword index; a zero key has r = 0 and u = 0;
+* an update from n_old to n_new tokens indexes the tokens that leave the
+  local window, [max(n_sink, n_old - n_local), n_new - n_local).
 
 Parity pins for every function live in tests/test_oracle_pins.py (brute force,
 closed forms, special cases). No function here is "parity unpinned".
@@ -49,6 +59,9 @@ __all__ = [
     "pqhsa_row_ref",
     "pqhsa_batch_ref",
     "RowResult",
+    "Encoding",
+    "encode_ref",
+    "update_ref",
 ]
 
 
@@ -178,6 +191,74 @@ def list_means_ref(V, list_ids, n_list: int, R: np.ndarray):
     nz = cnt > 0
     means[nz] = sums[nz] / cnt[nz, None]
     return means
+
+
+# ---------------------------------------------------------------------------
+# Encoding keys into the existing index (Section 3.1) and the incremental
+# update (Section 3.3).
+# ---------------------------------------------------------------------------
+@dataclass
+class Encoding:
+    a: np.ndarray          # [n] list id
+    z: np.ndarray          # [n, M] code per subspace
+    r: np.ndarray          # [n] key norm
+    coarse_d2: np.ndarray  # [n, n_list] ||u - c_j||^2
+    fine_d2: np.ndarray    # [n, M, K] ||(u - c_a)^(m) - p_{m,z}||^2
+
+
+def encode_ref(keys, centroids, codebooks) -> Encoding:
+    """Direction-norm residual IVF-PQ encoding of keys [n, d] (Section 3.1).
+
+    r = ||k||, u = k / r; a = the list whose centroid is nearest to u; then
+    for each subspace m the codeword nearest to the m-th slice of u - c_a.
+    The distance tables are returned for validity checks of other encoders.
+    """
+    K = np.asarray(keys, np.float64)
+    C = np.asarray(centroids, np.float64)
+    P = np.asarray(codebooks, np.float64)
+    n, d = K.shape
+    M, ksub, dsub = P.shape
+    r = np.sqrt((K * K).sum(axis=1))
+    u = np.zeros_like(K)
+    nz = r > 0
+    u[nz] = K[nz] / r[nz, None]
+    coarse = np.empty((n, C.shape[0]))
+    for s in range(0, n, 256):
+        coarse[s:s + 256] = ((u[s:s + 256, None, :] - C[None]) ** 2).sum(axis=2)
+    a = coarse.argmin(axis=1)            # the first minimum: the smaller id
+    res = (u - C[a]).reshape(n, M, dsub)
+    fine = np.empty((n, M, ksub))
+    for m in range(M):
+        fine[:, m, :] = ((res[:, m, None, :] - P[m][None]) ** 2).sum(axis=2)
+    z = fine.argmin(axis=2)
+    return Encoding(a=a, z=z, r=r, coarse_d2=coarse, fine_d2=fine)
+
+
+def update_ref(list_ids, codes, norms, K, V, n_old: int, n_new: int, n_sink: int,
+               n_local: int, centroids, codebooks):
+    """Grow one (sequence, KV head) index from n_old to n_new cached tokens.
+
+    list_ids [>= n_new], codes [>= n_new, M], norms [>= n_new]: the current
+    token-major index (entries outside R ignored); K, V [>= n_new, d]. The
+    tokens leaving the local window join R, encoded with `encode_ref` against
+    the existing centroids and codebooks; the list means become the means
+    over the grown lists. Returns (list_ids, codes, norms, list_means,
+    Encoding of the new tokens) as new arrays.
+    """
+    if n_new < n_old:
+        raise ValueError("an update cannot shrink the sequence")
+    lo = max(n_sink, n_old - n_local)
+    hi = max(n_sink, n_new - n_local)
+    ids = np.array(list_ids, np.int64, copy=True)
+    cds = np.array(codes, np.int64, copy=True)
+    nrm = np.array(norms, np.float64, copy=True)
+    enc = encode_ref(np.asarray(K, np.float64)[lo:hi], centroids, codebooks)
+    ids[lo:hi] = enc.a
+    cds[lo:hi] = enc.z
+    nrm[lo:hi] = enc.r
+    R = split_positions(n_new, n_sink, n_local)[2]
+    means = list_means_ref(V, ids, np.asarray(centroids).shape[0], R)
+    return ids, cds, nrm, means, enc
 
 
 # ---------------------------------------------------------------------------

@@ -389,3 +389,101 @@ def test_float64_oracle_against_mpmath():
         num = [a + e * b for a, b in zip(num, val)]
     ref = np.array([float(x / den) for x in num])
     assert close(res.y, ref, 1e-13)
+
+
+# ---------------------------------------------------------------------------
+# encoding into the existing index (Section 3.1) and the incremental update
+# (Section 3.3)
+# ---------------------------------------------------------------------------
+def _enc_problem(seed, n=300, d=32, n_m=4, ksub=16, n_list=12):
+    rng = np.random.default_rng(seed)
+    C = rng.standard_normal((n_list, d))
+    C /= np.linalg.norm(C, axis=1, keepdims=True)
+    P = 0.15 * rng.standard_normal((n_m, ksub, d // n_m))
+    K = rng.standard_normal((n, d)) * np.exp(rng.uniform(-1, 1, size=(n, 1)))
+    return K, C, P
+
+
+def test_encode_matches_scipy_vq():
+    """Nearest centroid and nearest codeword against scipy's own vector quantizer."""
+    import scipy.cluster.vq as vq
+    K, C, P = _enc_problem(1)
+    enc = R.encode_ref(K, C, P)
+    u = K / np.linalg.norm(K, axis=1, keepdims=True)
+    a_vq, _ = vq.vq(u, C, check_finite=False)
+    np.testing.assert_array_equal(enc.a, a_vq)
+    np.testing.assert_allclose(enc.r, np.linalg.norm(K, axis=1), rtol=1e-14)
+    res = u - C[a_vq]
+    ds = P.shape[2]
+    for m in range(P.shape[0]):
+        z_vq, _ = vq.vq(res[:, m * ds:(m + 1) * ds], P[m], check_finite=False)
+        np.testing.assert_array_equal(enc.z[:, m], z_vq)
+
+
+def test_encode_recovers_an_exactly_representable_key():
+    """A key whose direction is c_j0 + P(z0) exactly is stored as (j0, z0, ||k||)."""
+    rng = np.random.default_rng(2)
+    d, n_m, ksub, n_list = 32, 4, 8, 6
+    ds = d // n_m
+    u0 = rng.standard_normal(d)
+    u0 /= np.linalg.norm(u0)
+    delta = 0.05 * rng.standard_normal(d)
+    C = 3.0 * rng.standard_normal((n_list, d))   # far from the unit sphere
+    j0 = 4
+    C[j0] = u0 - delta
+    P = 0.5 + rng.standard_normal((n_m, ksub, ds))   # far from delta's slices
+    z0 = rng.integers(0, ksub, size=n_m)
+    for m in range(n_m):
+        P[m, z0[m]] = delta[m * ds:(m + 1) * ds]
+    r = np.array([0.5, 1.0, 1.7])
+    enc = R.encode_ref(r[:, None] * u0[None], C, P)
+    assert np.all(enc.a == j0)
+    assert np.all(enc.z == z0[None])
+    np.testing.assert_allclose(enc.r, r, rtol=1e-14)
+    recon = C[enc.a] + np.concatenate([P[m, enc.z[:, m]] for m in range(n_m)], axis=1)
+    np.testing.assert_allclose(enc.r[:, None] * recon, r[:, None] * u0[None], atol=1e-12)
+
+
+def test_encode_norm_scaling_and_zero_key():
+    K, C, P = _enc_problem(3, n=80)
+    e1 = R.encode_ref(K, C, P)
+    e2 = R.encode_ref(2.5 * K, C, P)
+    np.testing.assert_array_equal(e1.a, e2.a)
+    np.testing.assert_array_equal(e1.z, e2.z)
+    np.testing.assert_allclose(e2.r, 2.5 * e1.r, rtol=1e-14)
+    z0 = R.encode_ref(np.zeros((1, K.shape[1])), C, P)
+    assert z0.r[0] == 0.0
+    assert z0.a[0] == int(np.argmin((C ** 2).sum(axis=1)))   # the centroid nearest the origin
+
+
+def test_update_composes_and_matches_an_encoding_from_scratch():
+    """Two updates equal one; both equal encoding all of R at once, with the
+    list means recomputed by brute force over each list's members."""
+    K, C, P = _enc_problem(4, n=400)
+    V = np.random.default_rng(5).standard_normal(K.shape)
+    n_sink, n_local, n_list = 4, 16, C.shape[0]
+    n0, n1, n2 = 150, 270, 400
+    R0 = np.arange(n_sink, n0 - n_local)
+    e0 = R.encode_ref(K[R0], C, P)
+    ids = np.zeros(400, np.int64)
+    codes = np.zeros((400, P.shape[0]), np.int64)
+    norms = np.zeros(400)
+    ids[R0], codes[R0], norms[R0] = e0.a, e0.z, e0.r
+    a1 = R.update_ref(ids, codes, norms, K, V, n0, n1, n_sink, n_local, C, P)
+    a2 = R.update_ref(*a1[:3], K, V, n1, n2, n_sink, n_local, C, P)
+    b2 = R.update_ref(ids, codes, norms, K, V, n0, n2, n_sink, n_local, C, P)
+    Rn = np.arange(n_sink, n2 - n_local)
+    full = R.encode_ref(K[Rn], C, P)
+    for got in (a2, b2):
+        np.testing.assert_array_equal(got[0][Rn], full.a)
+        np.testing.assert_array_equal(got[1][Rn], full.z)
+        np.testing.assert_allclose(got[2][Rn], full.r, rtol=1e-14)
+        for j in range(n_list):
+            members = [i for i in Rn if full.a[i - n_sink] == j]
+            want = V[members].mean(axis=0) if members else np.zeros(K.shape[1])
+            np.testing.assert_allclose(got[3][j], want, atol=1e-12)
+    same = R.update_ref(*a2[:3], K, V, n2, n2, n_sink, n_local, C, P)
+    np.testing.assert_array_equal(same[0], a2[0])
+    np.testing.assert_allclose(same[3], a2[3], atol=0)
+    with pytest.raises(ValueError):
+        R.update_ref(*a2[:3], K, V, n2, n1, n_sink, n_local, C, P)
