@@ -377,6 +377,25 @@ def main() -> int:
         paged_us = {"page_size": page, "us_per_call": round(float(np.mean(t_pg)) * 1e3, 3)}
         del pages, kp, vp
 
+    # the incremental index update: 256 tokens leave the local window and are
+    # encoded into the lists (wall time of the whole call: encode and means
+    # kernels, the host counting sort, uploads and the list-major gather)
+    update = None
+    if not args.no_pq4:
+        ctxu = pqhsa.context_for(inp)
+        n0 = [int(x) - 5 * 256 for x in inp["seq_lens"]]
+        pqhsa.prepare_from(ctxu, dict(inp, seq_lens=torch.tensor(n0, dtype=torch.int32)))
+        t_up = []
+        for i in range(1, 6):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            ctxu.index_update([n + 256 * i for n in n0], kc, vc)
+            t_up.append(time.perf_counter() - t0)
+        ms_up = 1e3 * float(np.median(t_up))
+        update = {"tokens_per_update": 256, "ms_per_update": round(ms_up, 3),
+                  "us_per_step_amortized_over_256": round(ms_up * 1e3 / 256, 3)}
+        ctxu.close()
+
     # the paper's own index setting on the same 128K shapes (8 subspaces of
     # 4-bit codes, 512 lists): a second PQ-HSA arm, reported beside the value
     pq4 = None
@@ -497,6 +516,7 @@ def main() -> int:
         "cpu_baseline": cpu,
         "variant_us_per_call": variant_us,
         "paged_kv_arm": paged_us,
+        "index_update": update,
         "paper_index_arm": pq4 if pq4 is None else dict(
             pq4, speedup_vs_dense=round(best_dense[1] / pq4["us_per_call"], 3)),
     }

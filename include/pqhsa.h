@@ -23,7 +23,8 @@
  *   - Sequence b has N_b tokens. Its sink prefix is S = [0, n_sink), its local
  *     window L = [N_b - n_local, N_b) and its indexed region
  *     R_b = [n_sink, N_b - n_local) (Section 3.2). Index entries outside R_b
- *     are ignored.
+ *     are ignored. Between index updates the cache may grow past the index
+ *     (pqhsa_set_lengths): L then spans every token after R_b.
  *   - One context serves one stream at a time: calls that overlap on
  *     different streams with the same context race on its workspace.
  */
@@ -57,7 +58,8 @@ typedef enum { PQHSA_F32 = 0, PQHSA_BF16 = 1 } pqhsa_dtype;
  * max_seq <= 2^20, 1 <= n_list <= 4096,
  * G in {1, 2, 4, 8}, 1 <= batch <= 256, kv_dtype F32 or BF16 (the query has
  * the same dtype as the cache), 0 <= max_topk <= max_seq, and
- * ceil((n_sink + n_local + max_topk) / 128) + ceil(n_list / 64) <= 512. */
+ * ceil((n_sink + n_local + 1024 + max_topk) / 128) + ceil(n_list / 64) <= 512
+ * (1024: the growth of L between index updates). */
 typedef struct {
     int32_t batch;
     int32_t n_q_heads;
@@ -105,6 +107,49 @@ pqhsa_status pqhsa_index_prepare(pqhsa_ctx* ctx, const int32_t* seq_lens,
                                  const float* norms, const float* centroids,
                                  const float* codebooks, const float* list_means,
                                  hipStream_t stream);
+
+/* Incremental index update (Section 3.3): the caches now hold
+ * new_seq_lens[b] tokens (HOST int32 [B], each >= the current N_b and
+ * <= max_seq, where N_b is the current length, see pqhsa_set_lengths). The
+ * tokens that leave the local window, [n_sink + |R_b|, new N_b - n_local),
+ * join R_b without re-clustering.
+ *   - Each key k is stored as its norm r = ||k||, the list a of the centroid
+ *     nearest to its direction u = k / r, and, per subspace, the index of
+ *     the codeword nearest to that slice of u - c_a (Section 3.1). Distances
+ *     are squared Euclidean in fp32; ties go to the smaller id; a zero key
+ *     has r = 0.
+ *   - The list means are refreshed over the grown lists (Eq. 4), in
+ *     float64: (n_old v_bar + sum of new v) / (n_old + n_new).
+ *   - The list-major layout is rebuilt as by pqhsa_index_prepare.
+ * k_cache / v_cache / kv_strides as in pqhsa_decode (keys and values of
+ * every token up to new_seq_lens). Equal lengths are a no-op rebuild.
+ * Synchronises `stream`; allocates nothing. INVALID_ARGUMENT for a length
+ * that shrinks or exceeds max_seq. After any other failure the index is
+ * unspecified until the next successful prepare. */
+pqhsa_status pqhsa_index_update(pqhsa_ctx* ctx, const int32_t* new_seq_lens,
+                                const void* k_cache, const void* v_cache,
+                                const int64_t* kv_strides, hipStream_t stream);
+
+/* Set the current cache lengths N_b (HOST int32 [B]) between index updates
+ * (Section 3.3: new tokens stay exact until the next update encodes them).
+ * The tokens past R_b, [n_sink + |R_b|, N_b), form the exact tail L_b of
+ * later decode calls, which grows from n_local to at most n_local + 1024.
+ * Each N_b must lie in [indexed N_b, indexed N_b + 1024] and <= max_seq,
+ * where the indexed N_b is the length of the last prepare or update (which
+ * also reset the current lengths to it); otherwise INVALID_ARGUMENT. No
+ * device work. */
+pqhsa_status pqhsa_set_lengths(pqhsa_ctx* ctx, const int32_t* seq_lens);
+
+/* Copy out the token-major index the context holds (synchronises `stream`);
+ * any pointer may be NULL to skip that array. Entries of tokens outside R_b
+ * are unspecified.
+ *   list_ids   int32 [B, Hkv, max_seq]
+ *   codes      uint8 [B, Hkv, max_seq, M], one code per byte
+ *   norms      float [B, Hkv, max_seq]
+ *   list_means float [B, Hkv, n_list, d] */
+pqhsa_status pqhsa_index_export_tokens(pqhsa_ctx* ctx, int32_t* list_ids, uint8_t* codes,
+                                       float* norms, float* list_means,
+                                       hipStream_t stream);
 
 /* One PQ-HSA decode step (Eqs. 2-5) for every (batch element, query head).
  *   q          [B, Hq, d] in kv_dtype, contiguous

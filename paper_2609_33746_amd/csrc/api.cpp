@@ -35,7 +35,8 @@ struct pqhsa_ctx {
 
     // prepared index (device)
     bool prepared = false;
-    std::vector<int32_t> seq_lens, n_r;
+    std::vector<int32_t> seq_lens, n_r;   // N_b and |R_b| of the index
+    std::vector<int32_t> cur_len;         // current cache lengths (>= seq_lens; the tail is exact)
     uint8_t* codes = nullptr;
     float* norms = nullptr;
     int32_t* perm = nullptr;
@@ -46,6 +47,11 @@ struct pqhsa_ctx {
     float* means = nullptr;
     float* glob_mean = nullptr;   // [B, Hkv, d] for variant C
     uint16_t* tok_list = nullptr; // [B, Hkv, rcap] for variant Bx
+    // token-major copy of the index, the source of every list-major rebuild
+    std::vector<int32_t> ids_host;   // [B, Hkv, rcap] list id of each token
+    int32_t* ids_tm = nullptr;       // the same on the device
+    uint8_t* codes_tm = nullptr;     // [B, Hkv, rcap, M] one code per byte
+    float* norms_tm = nullptr;       // [B, Hkv, rcap]
     int32_t* n_seq_dev = nullptr;
     int32_t* n_r_dev = nullptr;
     int scan_nwg = 0;   // scan workgroups per (b, kv head)
@@ -139,12 +145,13 @@ pqhsa_status check_shape(const pqhsa_shape* s) {
     if (s->max_seq > kMaxSeq) return fail(nullptr, PQHSA_ERR_UNSUPPORTED, "max_seq must be <= 2^20");
     {
         // partials per row: splits of the exact set plus background chunks
-        const int nsplit = std::max((s->n_sink + s->n_local + s->max_topk + kAttnRows - 1) / kAttnRows, 1);
+        const int nsplit = std::max(
+            (s->n_sink + s->n_local + kTailGrowth + s->max_topk + kAttnRows - 1) / kAttnRows, 1);
         const int nbgc = (s->n_list + kBgLists - 1) / kBgLists;
         if (nsplit + nbgc > kMaxRowParts)
             return fail(nullptr, PQHSA_ERR_UNSUPPORTED,
                         "n_sink + n_local + max_topk must be <= %d for n_list = %d",
-                        (kMaxRowParts - nbgc) * kAttnRows, s->n_list);
+                        (kMaxRowParts - nbgc) * kAttnRows - kTailGrowth, s->n_list);
     }
     return PQHSA_OK;
 }
@@ -192,7 +199,7 @@ pqhsa_status check_pages(pqhsa_ctx* c, const int32_t* block_table, int32_t max_b
         return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "page_size %d is not a power of two in [1, 2^20]",
                     page_size);
     int n_max = 0;
-    for (int n : c->seq_lens) n_max = std::max(n_max, n);
+    for (int n : c->cur_len) n_max = std::max(n_max, n);
     if (max_blocks < 1 || static_cast<int64_t>(max_blocks) * page_size < n_max)
         return fail(c, PQHSA_ERR_INVALID_ARGUMENT,
                     "max_blocks %d x page_size %d does not cover the longest sequence (%d tokens)",
@@ -265,7 +272,7 @@ pqhsa_status pqhsa_create(const pqhsa_shape* shape, pqhsa_ctx** out) {
 
     const size_t B = D.B, Hq = D.Hq, Hkv = D.Hkv, G = D.G, L = D.n_list, rc = D.rcap;
     const size_t BG = B * Hkv, BQ = B * Hq;
-    c->nsplit_max = (D.n_sink + D.n_local + shape->max_topk + kAttnRows - 1) / kAttnRows;
+    c->nsplit_max = (D.n_sink + D.n_local + kTailGrowth + shape->max_topk + kAttnRows - 1) / kAttnRows;
     if (c->nsplit_max < 1) c->nsplit_max = 1;
     const int n_bgc = (D.n_list + kBgLists - 1) / kBgLists;
     c->dense_nsplit = (D.rcap + kDenseRows - 1) / kDenseRows;
@@ -287,6 +294,9 @@ pqhsa_status pqhsa_create(const pqhsa_shape* shape, pqhsa_ctx** out) {
     A(dev_alloc(c, &c->means, BG * L * kHeadDim));
     A(dev_alloc(c, &c->glob_mean, BG * kHeadDim));
     A(dev_alloc(c, &c->tok_list, BG * rc));
+    A(dev_alloc(c, &c->ids_tm, BG * rc));
+    A(dev_alloc(c, &c->codes_tm, BG * rc * static_cast<size_t>(shape->pq_m)));
+    A(dev_alloc(c, &c->norms_tm, BG * rc));
     A(dev_alloc(c, &c->n_seq_dev, B));
     A(dev_alloc(c, &c->n_r_dev, B));
     A(dev_alloc(c, &w.lut, BG * lut_row * G));
@@ -320,6 +330,74 @@ pqhsa_status pqhsa_create(const pqhsa_shape* shape, pqhsa_ctx** out) {
     return PQHSA_OK;
 }
 
+// Rebuild the list-major layout of every (b, kv head) from the token-major
+// index (c->ids_host, codes_tm, norms_tm) for sequence lengths `lens`: a
+// stable counting sort of R_b by list id on the host (lists in increasing id,
+// tokens in increasing id within a list), then the device gather of codes and
+// norms and the global value means. Synchronises `stream`.
+static pqhsa_status relayout(pqhsa_ctx* c, const std::vector<int32_t>& lens, hipStream_t stream) {
+    const Dims& D = c->D;
+    const int B = D.B, Hkv = D.Hkv, L = D.n_list;
+    const size_t rc = D.rcap;
+    const size_t BG = static_cast<size_t>(B) * Hkv;
+    std::vector<int32_t> nr(B);
+    for (int b = 0; b < B; ++b) nr[b] = lens[b] - D.n_sink - D.n_local;
+    c->prepared = false;
+    hipError_t e = hipSuccess;
+    // stable counting sort of R_b by list id, per (b, kv head)
+    std::vector<int32_t> perm(BG * rc, -1), loff(BG * (L + 1));
+    std::vector<uint32_t> pos_word(BG * rc, 0u);
+    std::vector<uint16_t> tok_list(BG * rc, 0);
+    std::vector<int32_t> cnt(L);
+    for (int b = 0; b < B; ++b) {
+        for (int g = 0; g < Hkv; ++g) {
+            const size_t bg = static_cast<size_t>(b) * Hkv + g;
+            const int32_t* a = c->ids_host.data() + bg * rc;
+            std::fill(cnt.begin(), cnt.end(), 0);
+            for (int i = D.n_sink; i < D.n_sink + nr[b]; ++i) ++cnt[a[i]];
+            int32_t* lo = loff.data() + bg * (L + 1);
+            lo[0] = 0;
+            for (int j = 0; j < L; ++j) lo[j + 1] = lo[j] + cnt[j];
+            std::vector<int32_t> fillp(lo, lo + L);
+            int32_t* pm = perm.data() + bg * rc;
+            uint32_t* pw = pos_word.data() + bg * rc;
+            uint16_t* tl = tok_list.data() + bg * rc;
+            for (int i = D.n_sink; i < D.n_sink + nr[b]; ++i) {
+                tl[i] = static_cast<uint16_t>(a[i]);
+                const int p = fillp[a[i]]++;
+                pm[p] = i;
+                pw[p] = (static_cast<uint32_t>(a[i]) << kPosBits) | static_cast<uint32_t>(i);
+            }
+        }
+    }
+
+    auto H2D = [&](void* dst, const void* src, size_t bytes) {
+        if (e == hipSuccess) e = hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, stream);
+    };
+    H2D(c->perm, perm.data(), perm.size() * 4);
+    H2D(c->pos_word, pos_word.data(), pos_word.size() * 4);
+    H2D(c->tok_list, tok_list.data(), tok_list.size() * 2);
+    H2D(c->loff, loff.data(), loff.size() * 4);
+    H2D(c->n_seq_dev, lens.data(), B * 4);
+    H2D(c->n_r_dev, nr.data(), B * 4);
+    if (e != hipSuccess) return hip_fail(c, e, "uploading the prepared index");
+    e = launch_prepare_gather(D, c->codes_tm, c->norms_tm, c->index(), c->codes, c->norms, stream);
+    if (e != hipSuccess) return hip_fail(c, e, "launching the index gather");
+    e = launch_glob_mean(D, c->index(), c->glob_mean, stream);
+    if (e != hipSuccess) return hip_fail(c, e, "launching the global value mean");
+    e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) return hip_fail(c, e, "preparing the index");
+    c->seq_lens = lens;
+    c->cur_len = lens;
+    c->n_r = nr;
+    int nr_max = 0;
+    for (int b = 0; b < B; ++b) nr_max = std::max(nr_max, nr[b]);
+    c->scan_nwg = (nr_max + kScanWaves * kSub - 1) / (kScanWaves * kSub);
+    c->prepared = true;
+    return PQHSA_OK;
+}
+
+
 pqhsa_status pqhsa_index_prepare(pqhsa_ctx* c, const int32_t* seq_lens, const int32_t* list_ids,
                                  const uint8_t* codes, const float* norms, const float* centroids,
                                  const float* codebooks, const float* list_means,
@@ -350,66 +428,107 @@ pqhsa_status pqhsa_index_prepare(pqhsa_ctx* c, const int32_t* seq_lens, const in
     if (e == hipSuccess) e = hipStreamSynchronize(stream);
     if (e != hipSuccess) return hip_fail(c, e, "copying list ids to the host");
 
-    // stable counting sort of R_b by list id, per (b, kv head)
-    std::vector<int32_t> perm(BG * rc, -1), loff(BG * (L + 1));
-    std::vector<uint32_t> pos_word(BG * rc, 0u);
-    std::vector<uint16_t> tok_list(BG * rc, 0);
-    std::vector<int32_t> cnt(L);
-    for (int b = 0; b < B; ++b) {
-        for (int g = 0; g < Hkv; ++g) {
-            const size_t bg = static_cast<size_t>(b) * Hkv + g;
-            const int32_t* a = ids.data() + bg * rc;
-            std::fill(cnt.begin(), cnt.end(), 0);
-            for (int i = D.n_sink; i < D.n_sink + nr[b]; ++i) {
-                if (a[i] < 0 || a[i] >= L)
-                    return fail(c, PQHSA_ERR_INVALID_ARGUMENT,
-                                "list_ids[%d][%d][%d] = %d outside [0, n_list = %d)", b, g, i, a[i], L);
-                ++cnt[a[i]];
-            }
-            int32_t* lo = loff.data() + bg * (L + 1);
-            lo[0] = 0;
-            for (int j = 0; j < L; ++j) lo[j + 1] = lo[j] + cnt[j];
-            std::vector<int32_t> fillp(lo, lo + L);
-            int32_t* pm = perm.data() + bg * rc;
-            uint32_t* pw = pos_word.data() + bg * rc;
-            uint16_t* tl = tok_list.data() + bg * rc;
-            for (int i = D.n_sink; i < D.n_sink + nr[b]; ++i) {
-                tl[i] = static_cast<uint16_t>(a[i]);
-                const int p = fillp[a[i]]++;
-                pm[p] = i;
-                pw[p] = (static_cast<uint32_t>(a[i]) << kPosBits) | static_cast<uint32_t>(i);
-            }
-        }
+    for (size_t bg = 0; bg < BG; ++bg) {
+        const int b = static_cast<int>(bg / Hkv), g = static_cast<int>(bg % Hkv);
+        const int32_t* a = ids.data() + bg * rc;
+        for (int i = D.n_sink; i < D.n_sink + nr[b]; ++i)
+            if (a[i] < 0 || a[i] >= L)
+                return fail(c, PQHSA_ERR_INVALID_ARGUMENT,
+                            "list_ids[%d][%d][%d] = %d outside [0, n_list = %d)", b, g, i, a[i], L);
     }
+    e = hipMemcpyAsync(c->ids_tm, list_ids, BG * rc * 4, hipMemcpyDeviceToDevice, stream);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(c->codes_tm, codes, BG * rc * c->shape.pq_m, hipMemcpyDeviceToDevice, stream);
+    if (e == hipSuccess) e = hipMemcpyAsync(c->norms_tm, norms, BG * rc * 4, hipMemcpyDeviceToDevice, stream);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(c->centroids, centroids, BG * L * kHeadDim * 4, hipMemcpyDeviceToDevice, stream);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(c->codebooks, codebooks, BG * c->codebook_floats * 4, hipMemcpyDeviceToDevice, stream);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(c->means, list_means, BG * L * kHeadDim * 4, hipMemcpyDeviceToDevice, stream);
+    if (e != hipSuccess) return hip_fail(c, e, "copying the index");
+    c->ids_host.swap(ids);
+    return relayout(c, lens, stream);
+}
 
-    auto H2D = [&](void* dst, const void* src, size_t bytes) {
-        if (e == hipSuccess) e = hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, stream);
-    };
+pqhsa_status pqhsa_index_update(pqhsa_ctx* c, const int32_t* new_seq_lens, const void* k_cache,
+                                const void* v_cache, const int64_t* kv_strides, hipStream_t stream) {
+    if (!c) return fail(nullptr, PQHSA_ERR_INVALID_ARGUMENT, "ctx is NULL");
+    c->err.clear();
+    if (!c->prepared) return fail(c, PQHSA_ERR_NOT_PREPARED, "pqhsa_index_prepare has not succeeded");
+    if (!new_seq_lens || !k_cache || !v_cache || !kv_strides)
+        return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "new_seq_lens, k_cache, v_cache and kv_strides must be non-NULL");
+    pqhsa_status st = check_device(c);
+    if (st != PQHSA_OK) return st;
+    KV kv;
+    // the update reads no query and writes no output: the cache stands in for both
+    st = check_kv(c, k_cache, k_cache, v_cache, kv_strides, k_cache, &kv);
+    if (st != PQHSA_OK) return st;
+    const Dims& D = c->D;
+    const size_t rc = D.rcap;
+    std::vector<int32_t> lens(new_seq_lens, new_seq_lens + D.B);
+    BatchInts lo{}, hi{};
+    int max_new = 0;
+    for (int b = 0; b < D.B; ++b) {
+        if (lens[b] < c->cur_len[b] || lens[b] > D.rcap)
+            return fail(c, PQHSA_ERR_INVALID_ARGUMENT,
+                        "new_seq_lens[%d] = %d outside [current N_b, max_seq] = [%d, %d]", b, lens[b],
+                        c->cur_len[b], D.rcap);
+        lo.v[b] = c->seq_lens[b] - D.n_local;   // the current end of R_b
+        hi.v[b] = lens[b] - D.n_local;
+        max_new = std::max(max_new, hi.v[b] - lo.v[b]);
+    }
+    hipError_t e = launch_update(D, lo, hi, max_new, kv, c->centroids, c->codebooks, c->loff,
+                                 c->ids_tm, c->codes_tm, c->norms_tm, c->means, stream);
+    if (e != hipSuccess) return hip_fail(c, e, "launching the index update");
+    for (int b = 0; b < D.B && e == hipSuccess; ++b)
+        for (int g = 0; g < D.Hkv && e == hipSuccess; ++g) {
+            const size_t off = (static_cast<size_t>(b) * D.Hkv + g) * rc + lo.v[b];
+            if (hi.v[b] > lo.v[b])
+                e = hipMemcpyAsync(c->ids_host.data() + off, c->ids_tm + off,
+                                   (hi.v[b] - lo.v[b]) * sizeof(int32_t), hipMemcpyDeviceToHost, stream);
+        }
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) return hip_fail(c, e, "encoding the new tokens");
+    return relayout(c, lens, stream);
+}
+
+pqhsa_status pqhsa_set_lengths(pqhsa_ctx* c, const int32_t* seq_lens) {
+    if (!c) return fail(nullptr, PQHSA_ERR_INVALID_ARGUMENT, "ctx is NULL");
+    c->err.clear();
+    if (!c->prepared) return fail(c, PQHSA_ERR_NOT_PREPARED, "pqhsa_index_prepare has not succeeded");
+    if (!seq_lens) return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "seq_lens is NULL");
+    for (int b = 0; b < c->D.B; ++b) {
+        const int lo = c->seq_lens[b];
+        const int hi = std::min(lo + kTailGrowth, c->D.rcap);
+        if (seq_lens[b] < lo || seq_lens[b] > hi)
+            return fail(c, PQHSA_ERR_INVALID_ARGUMENT,
+                        "seq_lens[%d] = %d outside [indexed N_b, indexed N_b + %d] = [%d, %d]", b,
+                        seq_lens[b], kTailGrowth, lo, hi);
+    }
+    c->cur_len.assign(seq_lens, seq_lens + c->D.B);
+    return PQHSA_OK;
+}
+
+pqhsa_status pqhsa_index_export_tokens(pqhsa_ctx* c, int32_t* list_ids, uint8_t* codes,
+                                       float* norms, float* list_means, hipStream_t stream) {
+    if (!c) return fail(nullptr, PQHSA_ERR_INVALID_ARGUMENT, "ctx is NULL");
+    c->err.clear();
+    if (!c->prepared) return fail(c, PQHSA_ERR_NOT_PREPARED, "pqhsa_index_prepare has not succeeded");
+    pqhsa_status st = check_device(c);
+    if (st != PQHSA_OK) return st;
+    const size_t BGR = static_cast<size_t>(c->D.B) * c->D.Hkv * c->D.rcap;
+    const size_t nmean = static_cast<size_t>(c->D.B) * c->D.Hkv * c->D.n_list * kHeadDim;
+    hipError_t e = hipSuccess;
     auto D2D = [&](void* dst, const void* src, size_t bytes) {
-        if (e == hipSuccess) e = hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDevice, stream);
+        if (dst && e == hipSuccess) e = hipMemcpyAsync(dst, src, bytes, hipMemcpyDeviceToDevice, stream);
     };
-    H2D(c->perm, perm.data(), perm.size() * 4);
-    H2D(c->pos_word, pos_word.data(), pos_word.size() * 4);
-    H2D(c->tok_list, tok_list.data(), tok_list.size() * 2);
-    H2D(c->loff, loff.data(), loff.size() * 4);
-    H2D(c->n_seq_dev, lens.data(), B * 4);
-    H2D(c->n_r_dev, nr.data(), B * 4);
-    D2D(c->centroids, centroids, BG * L * kHeadDim * 4);
-    D2D(c->codebooks, codebooks, BG * c->codebook_floats * 4);
-    D2D(c->means, list_means, BG * L * kHeadDim * 4);
-    if (e != hipSuccess) return hip_fail(c, e, "uploading the prepared index");
-    e = launch_prepare_gather(D, codes, norms, c->index(), c->codes, c->norms, stream);
-    if (e != hipSuccess) return hip_fail(c, e, "launching the index gather");
-    e = launch_glob_mean(D, c->index(), c->glob_mean, stream);
-    if (e != hipSuccess) return hip_fail(c, e, "launching the global value mean");
-    e = hipStreamSynchronize(stream);
-    if (e != hipSuccess) return hip_fail(c, e, "preparing the index");
-    c->seq_lens = lens;
-    c->n_r = nr;
-    int nr_max = 0;
-    for (int b = 0; b < B; ++b) nr_max = std::max(nr_max, nr[b]);
-    c->scan_nwg = (nr_max + kScanWaves * kSub - 1) / (kScanWaves * kSub);
-    c->prepared = true;
+    D2D(list_ids, c->ids_tm, BGR * 4);
+    D2D(codes, c->codes_tm, BGR * c->shape.pq_m);
+    D2D(norms, c->norms_tm, BGR * 4);
+    D2D(list_means, c->means, nmean * 4);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) return hip_fail(c, e, "exporting the index");
     return PQHSA_OK;
 }
 
@@ -433,12 +552,15 @@ static pqhsa_status decode_impl(pqhsa_ctx* c, const void* q, const void* k, cons
     if (st != PQHSA_OK) return st;
     const Dims& D = c->D;
     BatchArgs ba{};
+    int nsplit = 1;   // exact-set splits this call needs per row
     for (int b = 0; b < D.B; ++b) {
         if (topk[b] < 0 || topk[b] > c->n_r[b] || topk[b] > c->shape.max_topk)
             return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "topk[%d] = %d outside [0, min(|R_b| = %d, max_topk = %d)]",
                         b, topk[b], c->n_r[b], c->shape.max_topk);
         ba.topk[b] = topk[b];
         ba.n_r[b] = c->n_r[b];
+        ba.n_tail[b] = c->cur_len[b] - D.n_sink - c->n_r[b];
+        nsplit = std::max(nsplit, (D.n_sink + ba.n_tail[b] + topk[b] + kAttnRows - 1) / kAttnRows);
     }
     const Index ix = c->index();
     const bool timed = c->timing != 0;
@@ -462,7 +584,7 @@ static pqhsa_status decode_impl(pqhsa_ctx* c, const void* q, const void* k, cons
     if (e == hipSuccess) e = launch_select(D, ba, ix, c->w, c->force_fallback, stream, tm(2));
     if (e == hipSuccess && c->variant == PQHSA_VARIANT_BX) e = launch_bx_weights(D, ba, ix, c->w, stream);
     if (e == hipSuccess)
-        e = launch_attend(D, ba, kv, ix, c->w, c->nsplit_max, c->variant, stream, tm(3));
+        e = launch_attend(D, ba, kv, ix, c->w, nsplit, c->nsplit_max, c->variant, stream, tm(3));
     if (e == hipSuccess) e = launch_merge(D, ba, c->w, out, c->nsplit_max, c->variant, stream, tm(4));
     if (e != hipSuccess) return hip_fail(c, e, "enqueueing the decode kernels");
     c->timed_valid = timed;

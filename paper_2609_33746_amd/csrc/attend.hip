@@ -109,13 +109,14 @@ __device__ __forceinline__ void block_combine(const Online& o, float* sm, float*
 // role weights list j's mean by W_j |R_j| instead of M_j.
 template <typename T, int G, bool kBx>
 __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchArgs ba, KV kv,
-                                                              Index ix, Work w, int nsplit_max,
-                                                              int n_bgc, int variant) {
+                                                              Index ix, Work w, int nsplit,
+                                                              int nsplit_max, int n_bgc,
+                                                              int variant) {
     __shared__ float sm[kStreams], sz[kStreams];
     // [16 streams][d] for the exact role, [4 waves][G][d] for the background role
     __shared__ float sacc[(kStreams > 4 * G ? kStreams : 4 * G) * kHeadDim];
     __shared__ float bz[4][G];
-    const int n_exact_wg = D.B * D.Hq * nsplit_max;
+    const int n_exact_wg = D.B * D.Hq * nsplit;
     const int P = nsplit_max + n_bgc;
     const int lane16 = threadIdx.x & 15;
     const int stream = threadIdx.x >> 4;
@@ -123,20 +124,20 @@ __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchArgs 
 
     if (static_cast<int>(blockIdx.x) < n_exact_wg) {
         // ---------------- exact attention over a split of E ----------------
-        const int row = blockIdx.x / nsplit_max;
-        const int split = blockIdx.x % nsplit_max;
+        const int row = blockIdx.x / nsplit;
+        const int split = blockIdx.x % nsplit;
         const int b = row / D.Hq;
         const int h = row % D.Hq;
         const int g = h / G;
         const int k = ba.topk[b];
         const int n_r = ba.n_r[b];
-        const int n_seq = n_r + D.n_sink + D.n_local;
-        const int nE = D.n_sink + D.n_local + k;
+        const int n_tail = ba.n_tail[b];   // L_b = [n_sink + |R_b|, N_b)
+        const int nE = D.n_sink + n_tail + k;
         const int e0 = split * kAttnRows;
         if (e0 >= nE) return;   // the merge reads only the splits that exist
         const int e1 = min(e0 + kAttnRows, nE);
         const int32_t* sel = w.sel_tok + static_cast<int64_t>(row) * D.max_topk;
-        const int local0 = n_seq - D.n_local;
+        const int local0 = D.n_sink + n_r;
         int tok[kRowsPerStream];
 #pragma unroll
         for (int i = 0; i < kRowsPerStream; ++i) {
@@ -144,8 +145,8 @@ __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchArgs 
             int t = -1;
             if (e < e1) {
                 if (e < D.n_sink) t = e;
-                else if (e < D.n_sink + D.n_local) t = local0 + (e - D.n_sink);
-                else t = min(max(sel[e - D.n_sink - D.n_local], D.n_sink), local0 - 1);   // never outside R
+                else if (e < D.n_sink + n_tail) t = local0 + (e - D.n_sink);
+                else t = min(max(sel[e - D.n_sink - n_tail], D.n_sink), local0 - 1);   // never outside R
             }
             tok[i] = t;
         }
@@ -156,7 +157,7 @@ __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchArgs 
 #pragma unroll
             for (int i = 0; i < kRowsPerStream; ++i) {
                 const int e = e0 + stream + i * kStreams;
-                wx[i] = e < e1 && e >= D.n_sink + D.n_local ? wsel[e - D.n_sink - D.n_local] : 0.0f;
+                wx[i] = e < e1 && e >= D.n_sink + n_tail ? wsel[e - D.n_sink - n_tail] : 0.0f;
             }
             bx_shift = w.row_shift[row];
         }
@@ -489,38 +490,40 @@ __global__ __launch_bounds__(kMergeThreads * kGroups) void merge_kernel(
 
 template <typename T, int G>
 static hipError_t launch_attend_t(const Dims& D, const BatchArgs& ba, const KV& kv,
-                                  const Index& ix, const Work& w, int nsplit_max, int variant,
-                                  hipStream_t s, const KTiming& tm) {
+                                  const Index& ix, const Work& w, int nsplit, int nsplit_max,
+                                  int variant, hipStream_t s, const KTiming& tm) {
     const int n_bgc = (D.n_list + kBgLists - 1) / kBgLists;   // the partials' layout
     // variant T has no background: the background workgroups are not launched
-    const int grid = D.B * D.Hq * nsplit_max + (variant == PQHSA_VARIANT_T ? 0 : D.B * D.Hkv * n_bgc);
+    const int grid = D.B * D.Hq * nsplit + (variant == PQHSA_VARIANT_T ? 0 : D.B * D.Hkv * n_bgc);
     if (variant == PQHSA_VARIANT_BX)
         hipExtLaunchKernelGGL((attend_kernel<T, G, true>), dim3(grid), dim3(kAttnThreads), 0, s,
-                              tm.start, tm.stop, 0, D, ba, kv, ix, w, nsplit_max, n_bgc, variant);
+                              tm.start, tm.stop, 0, D, ba, kv, ix, w, nsplit, nsplit_max, n_bgc,
+                              variant);
     else
         hipExtLaunchKernelGGL((attend_kernel<T, G, false>), dim3(grid), dim3(kAttnThreads), 0, s,
-                              tm.start, tm.stop, 0, D, ba, kv, ix, w, nsplit_max, n_bgc, variant);
+                              tm.start, tm.stop, 0, D, ba, kv, ix, w, nsplit, nsplit_max, n_bgc,
+                              variant);
     return hipGetLastError();
 }
 
 template <typename T>
 static hipError_t launch_attend_g(const Dims& D, const BatchArgs& ba, const KV& kv,
-                                  const Index& ix, const Work& w, int nsplit_max, int variant,
-                                  hipStream_t s, const KTiming& tm) {
+                                  const Index& ix, const Work& w, int nsplit, int nsplit_max,
+                                  int variant, hipStream_t s, const KTiming& tm) {
     switch (D.G) {
-        case 1: return launch_attend_t<T, 1>(D, ba, kv, ix, w, nsplit_max, variant, s, tm);
-        case 2: return launch_attend_t<T, 2>(D, ba, kv, ix, w, nsplit_max, variant, s, tm);
-        case 4: return launch_attend_t<T, 4>(D, ba, kv, ix, w, nsplit_max, variant, s, tm);
-        case 8: return launch_attend_t<T, 8>(D, ba, kv, ix, w, nsplit_max, variant, s, tm);
+        case 1: return launch_attend_t<T, 1>(D, ba, kv, ix, w, nsplit, nsplit_max, variant, s, tm);
+        case 2: return launch_attend_t<T, 2>(D, ba, kv, ix, w, nsplit, nsplit_max, variant, s, tm);
+        case 4: return launch_attend_t<T, 4>(D, ba, kv, ix, w, nsplit, nsplit_max, variant, s, tm);
+        case 8: return launch_attend_t<T, 8>(D, ba, kv, ix, w, nsplit, nsplit_max, variant, s, tm);
         default: return hipErrorInvalidValue;
     }
 }
 
 hipError_t launch_attend(const Dims& D, const BatchArgs& ba, const KV& kv, const Index& ix,
-                         const Work& w, int nsplit_max, int variant, hipStream_t s,
+                         const Work& w, int nsplit, int nsplit_max, int variant, hipStream_t s,
                          const KTiming& tm) {
-    return kv.bf16 ? launch_attend_g<bf16_t>(D, ba, kv, ix, w, nsplit_max, variant, s, tm)
-                   : launch_attend_g<float>(D, ba, kv, ix, w, nsplit_max, variant, s, tm);
+    return kv.bf16 ? launch_attend_g<bf16_t>(D, ba, kv, ix, w, nsplit, nsplit_max, variant, s, tm)
+                   : launch_attend_g<float>(D, ba, kv, ix, w, nsplit, nsplit_max, variant, s, tm);
 }
 
 static hipError_t launch_merge_parts(const Dims& D, const BatchInts& ne, const float* partial,
@@ -541,7 +544,7 @@ hipError_t launch_merge(const Dims& D, const BatchArgs& ba, const Work& w, float
                         int nsplit_max, int variant, hipStream_t s, const KTiming& tm) {
     BatchInts ne;
     for (int b = 0; b < D.B; ++b) {
-        const int nE = D.n_sink + D.n_local + ba.topk[b];
+        const int nE = D.n_sink + ba.n_tail[b] + ba.topk[b];
         ne.v[b] = (nE + kAttnRows - 1) / kAttnRows;
     }
     const int n_bgc = (D.n_list + kBgLists - 1) / kBgLists;

@@ -44,6 +44,7 @@ constexpr int kBgLists = 64;       // lists per background workgroup
 constexpr int kDenseRows = 2048;   // cache rows per dense split
 constexpr int kPartStride = 132;   // floats per partial: m, Z, pad, pad, N[128]
 constexpr int kMaxRowParts = 512;  // partials per row (exact splits + background chunks)
+constexpr int kTailGrowth = 1024;  // tokens past the local window held exact between updates
 
 // Optional events a launch records around its kernel's own execution
 // (hipExtLaunchKernel), for per-kernel timing; null events record nothing.
@@ -68,11 +69,13 @@ struct BatchInts {
 };
 
 // The per-sequence integers every decode kernel needs, passed by value so
-// that no kernel starts with a dependent load: k_b and |R_b|
-// (N_b = |R_b| + n_sink + n_local).
+// that no kernel starts with a dependent load: k_b, |R_b| and |L_b|, the
+// exact tail after R_b (N_b = n_sink + |R_b| + |L_b|; |L_b| = n_local right
+// after an index prepare or update, up to n_local + kTailGrowth between them).
 struct BatchArgs {
     int32_t topk[kMaxBatch];
     int32_t n_r[kMaxBatch];
+    int32_t n_tail[kMaxBatch];
 };
 
 // Prepared index (list-major), owned by the context.
@@ -162,9 +165,11 @@ hipError_t launch_scan(const Dims& D, const BatchArgs& ba, const Index& ix, cons
                        hipStream_t s, const KTiming& tm = KTiming{});
 hipError_t launch_select(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w,
                          int force_fallback, hipStream_t s, const KTiming& tm = KTiming{});
-// variant: the background term, a PQHSA_VARIANT_* value
+// variant: the background term, a PQHSA_VARIANT_* value. nsplit: exact-set
+// splits launched per row (enough for this call's rows); nsplit_max: the
+// splits per row the partial buffer holds (its layout).
 hipError_t launch_attend(const Dims& D, const BatchArgs& ba, const KV& kv, const Index& ix,
-                         const Work& w, int nsplit_max, int variant, hipStream_t s,
+                         const Work& w, int nsplit, int nsplit_max, int variant, hipStream_t s,
                          const KTiming& tm = KTiming{});
 // variant Bx, after the select: the per-list weights bx_w and, for every
 // selected entry, the weight of its list (bx_wsel)
@@ -177,6 +182,14 @@ hipError_t launch_dense(const Dims& D, const KV& kv, const BatchInts& lens, floa
 // the token-weighted mean of the list means per (b, g): the global value
 // mean over R_b of variant C
 hipError_t launch_glob_mean(const Dims& D, const Index& ix, float* glob, hipStream_t s);
+// incremental update: encode tokens [lo[b], hi[b]) of every (b, kv head) into
+// the token-major ids / codes / norms, then fold their values into the list
+// means (old_loff: the list offsets before the update). max_new = max over b
+// of hi - lo.
+hipError_t launch_update(const Dims& D, const BatchInts& lo, const BatchInts& hi, int max_new,
+                         const KV& kv, const float* centroids, const float* codebooks,
+                         const int32_t* old_loff, int32_t* ids_tm, uint8_t* codes_tm,
+                         float* norms_tm, float* means, hipStream_t s);
 hipError_t launch_prepare_gather(const Dims& D, const uint8_t* codes_in, const float* norms_in,
                                  const Index& ix, uint8_t* codes_out, float* norms_out,
                                  hipStream_t s);

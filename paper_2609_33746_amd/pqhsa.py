@@ -58,6 +58,9 @@ def load_library(build_if_missing: bool = True) -> ctypes.CDLL:
         "pqhsa_index_prepare": ([P] + [P] * 7 + [P], I32),
         "pqhsa_decode": ([P, P, P, P, P, P, P, P], I32),
         "pqhsa_decode_paged": ([P, P, P, P, P, P, I32, I32, P, P, P], I32),
+        "pqhsa_index_update": ([P, P, P, P, P, P], I32),
+        "pqhsa_set_lengths": ([P, P], I32),
+        "pqhsa_index_export_tokens": ([P, P, P, P, P, P], I32),
         "pqhsa_decode_debug": ([P, P, P, P, P, P, P, P, P, P, P], I32),
         "pqhsa_dense_decode": ([P, P, P, P, P, P, P, P], I32),
         "pqhsa_index_export": ([P, P, P, P], I32),
@@ -145,6 +148,31 @@ class PQHSA:
             _ptr(self._dev(centroids, torch.float32, "centroids")),
             _ptr(self._dev(codebooks, torch.float32, "codebooks")),
             _ptr(self._dev(list_means, torch.float32, "list_means")), _stream()))
+
+    def index_update(self, new_seq_lens, k_cache, v_cache):
+        """Encode the tokens leaving the local window into the existing lists."""
+        strides = self._kv(k_cache, v_cache)
+        self._check(self.lib.pqhsa_index_update(self.ctx, _host_i32(list(new_seq_lens)),
+                                                _ptr(k_cache), _ptr(v_cache), strides, _stream()))
+
+    def set_lengths(self, seq_lens):
+        """Current cache lengths: the tokens past the index stay exact."""
+        self._check(self.lib.pqhsa_set_lengths(self.ctx, _host_i32(list(seq_lens))))
+
+    def index_export_tokens(self):
+        """The token-major index: list_ids, codes, norms [B, Hkv, max_seq(, M)] and
+        list_means [B, Hkv, n_list, d] (entries outside R unspecified)."""
+        sh = self.shape
+        dev = torch.device("cuda", torch.cuda.current_device())
+        ids = torch.empty((sh.batch, sh.n_kv_heads, sh.max_seq), dtype=torch.int32, device=dev)
+        codes = torch.empty((sh.batch, sh.n_kv_heads, sh.max_seq, sh.pq_m), dtype=torch.uint8,
+                            device=dev)
+        norms = torch.empty((sh.batch, sh.n_kv_heads, sh.max_seq), dtype=torch.float32, device=dev)
+        means = torch.empty((sh.batch, sh.n_kv_heads, sh.n_list, sh.head_dim), dtype=torch.float32,
+                            device=dev)
+        self._check(self.lib.pqhsa_index_export_tokens(self.ctx, _ptr(ids), _ptr(codes),
+                                                       _ptr(norms), _ptr(means), _stream()))
+        return dict(list_ids=ids, codes=codes, norms=norms, list_means=means)
 
     def _out(self, q, out):
         if out is None:

@@ -1,0 +1,232 @@
+"""GPU parity of the incremental index update (Section 3.3), through the C ABI.
+
+The index is put in the paper's direction-norm form (unit centroids, codebooks
+at the residual scale, norms = ||k||). The tokens that leave the local window
+are encoded by the GPU. Each of its choices must be a nearest centroid and
+nearest codewords by the oracle's float64 distances, within a tie window: the
+encoder decides in fp32, so a near tie may go either way. The list-major
+layout, the list means and the decode output are then checked against the
+oracle on the GPU's choices, and against a fresh prepare of the same index.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import check_rows, make, run, say
+from oracle import pqhsa_ref as R
+from paper_2609_33746_amd import pqhsa, synth
+
+pytestmark = pytest.mark.gpu
+
+DIST_TIE = 1e-5     # squared distances of unit-scale vectors, fp32 against float64
+MEAN_ATOL = 1e-5
+
+
+def paper_form(inp, old_lens):
+    """The generator's index with unit centroids, codebooks scaled to the
+    residual of a unit direction and norms ||k||, at lengths old_lens."""
+    out = dict(inp)
+    cen = inp["centroids"]
+    out["centroids"] = (cen / cen.norm(dim=-1, keepdim=True)).contiguous()
+    kn = inp["k_cache"].float().norm(dim=-1)
+    out["codebooks"] = (inp["codebooks"] / kn.mean()).contiguous()
+    out["norms"] = kn.contiguous()
+    out["seq_lens"] = torch.tensor(old_lens, dtype=torch.int32)
+    out["list_means"] = means_over_R(inp, inp["list_ids"], old_lens)
+    return out
+
+
+def means_over_R(inp, ids, lens):
+    B, Hkv, _, d = inp["v_cache"].shape
+    n_list = inp["centroids"].shape[2]
+    means = torch.zeros((B, Hkv, n_list, d), dtype=torch.float64, device=ids.device)
+    for b in range(B):
+        lo, hi = inp["n_sink"], int(lens[b]) - inp["n_local"]
+        for g in range(Hkv):
+            a = ids[b, g, lo:hi].long()
+            s = torch.zeros((n_list, d), dtype=torch.float64, device=ids.device)
+            s.index_add_(0, a, inp["v_cache"][b, g, lo:hi].double())
+            cnt = torch.bincount(a, minlength=n_list).double()
+            means[b, g] = torch.where(cnt[:, None] > 0, s / cnt.clamp(min=1)[:, None], 0.0)
+    return means.float().contiguous()
+
+
+def new_context(inp):
+    ctx = pqhsa.context_for(inp)
+    pqhsa.prepare_from(ctx, inp)
+    return ctx
+
+
+def check_encoding(idx_inp, ex, old_lens, new_lens):
+    """Every new token's (a, z, r) is a valid nearest choice; R_old is untouched."""
+    n_sink, n_local = idx_inp["n_sink"], idx_inp["n_local"]
+    B, Hkv = ex["list_ids"].shape[:2]
+    ids, codes, norms = (ex[k].cpu().numpy() for k in ("list_ids", "codes", "norms"))
+    ids0 = idx_inp["list_ids"].cpu().numpy()
+    codes0 = idx_inp["codes"].cpu().numpy()
+    flips = 0
+    for b in range(B):
+        lo, hi = int(old_lens[b]) - n_local, int(new_lens[b]) - n_local
+        for g in range(Hkv):
+            np.testing.assert_array_equal(ids[b, g, n_sink:lo], ids0[b, g, n_sink:lo])
+            np.testing.assert_array_equal(codes[b, g, n_sink:lo], codes0[b, g, n_sink:lo])
+            if hi <= lo:
+                continue
+            K = idx_inp["k_cache"][b, g, lo:hi].double().cpu().numpy()
+            C = idx_inp["centroids"][b, g].double().cpu().numpy()
+            P = idx_inp["codebooks"][b, g].double().cpu().numpy()
+            enc = R.encode_ref(K, C, P)
+            a, z, r = ids[b, g, lo:hi], codes[b, g, lo:hi].astype(np.int64), norms[b, g, lo:hi]
+            rows = np.arange(hi - lo)
+            best = enc.coarse_d2.min(axis=1)
+            assert np.all(enc.coarse_d2[rows, a] <= best + DIST_TIE), (b, g)
+            np.testing.assert_allclose(r, enc.r, rtol=2e-6)
+            # fine distances for the GPU's own list (the oracle's table when it agrees)
+            same = a == enc.a
+            flips += int((~same).sum())
+            fine = enc.fine_d2.copy()
+            if not same.all():
+                u = K[~same] / enc.r[~same, None]
+                res = (u - C[a[~same]]).reshape(-1, P.shape[0], P.shape[2])
+                fine[~same] = ((res[:, :, None, :] - P[None]) ** 2).sum(axis=3)
+            got = np.take_along_axis(fine, z[:, :, None], axis=2)[..., 0]
+            assert np.all(got <= fine.min(axis=2) + DIST_TIE), (b, g)
+    say(f"[update] coarse near-tie flips: {flips}")
+    assert flips <= 2
+
+
+def check_layout(ctx, ex, new_lens, n_sink, n_local, n_list):
+    perm, offs = ctx.index_export()
+    perm, offs = perm.cpu().numpy(), offs.cpu().numpy()
+    ids = ex["list_ids"].cpu().numpy()
+    B, Hkv = ids.shape[:2]
+    for b in range(B):
+        Rb = np.arange(n_sink, int(new_lens[b]) - n_local)
+        for g in range(Hkv):
+            a = ids[b, g, Rb]
+            np.testing.assert_array_equal(perm[b, g, :Rb.size], Rb[np.argsort(a, kind="stable")])
+            np.testing.assert_array_equal(offs[b, g], np.concatenate([[0], np.cumsum(np.bincount(a, minlength=n_list))]))
+
+
+def update_case(wl, deltas, rows_every=4, seed=6):
+    inp = make(wl, seed=seed)
+    full = [int(x) for x in inp["seq_lens"]]
+    old = [max(n - dlt, inp["n_sink"] + inp["n_local"]) for n, dlt in zip(full, deltas)]
+    idx_inp = paper_form(inp, old)
+    ctx = new_context(idx_inp)
+    say(f"[update] {old} -> {full}")
+    ctx.index_update(full, inp["k_cache"], inp["v_cache"])
+    ex = ctx.index_export_tokens()
+    check_encoding(idx_inp, ex, old, full)
+    check_layout(ctx, ex, full, inp["n_sink"], inp["n_local"], wl.n_list)
+    ref_means = means_over_R(inp, ex["list_ids"], full)
+    err = float((ex["list_means"] - ref_means).abs().max())
+    say(f"[update] list-mean error {err:.3g}")
+    assert err <= MEAN_ATOL
+    # the updated context decodes exactly as a fresh prepare of the same index
+    after = dict(inp, list_ids=ex["list_ids"], codes=ex["codes"], norms=ex["norms"],
+                 centroids=idx_inp["centroids"], codebooks=idx_inp["codebooks"],
+                 list_means=ex["list_means"], seq_lens=torch.tensor(full, dtype=torch.int32))
+    topk, out, sel, unsel, _ = run(ctx, after)
+    fresh = new_context(after)
+    _, out_f, sel_f, _, _ = run(fresh, after, topk)
+    assert torch.equal(sel, sel_f)
+    assert torch.equal(out, out_f)
+    rows = [(b, h) for b in range(wl.batch) for h in range(0, wl.n_q_heads, rows_every)]
+    check_rows(after, topk, rows, out, sel, unsel)
+    return ctx, inp, after, topk, out
+
+
+CASES = {
+    "tiny-f32": (synth.workload(0), [300]),
+    "32k-shape-8k": (synth.workload(1, max_seq=8000), [256]),
+    "pq4": (synth.pq4(1, max_seq=6000, n_list=64), [256]),
+    "ragged-batch": (synth.workload(4, batch=3, max_seq=6000, ragged_min=3000, n_list=40),
+                     [0, 256, 700]),
+    "g8": (synth.workload(3, batch=2, max_seq=3000, n_q_heads=16, n_kv_heads=2, n_list=16,
+                          topk=60), [256, 100]),
+}
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_index_update(case):
+    wl, deltas = CASES[case]
+    update_case(wl, deltas * wl.batch if len(deltas) == 1 else deltas)
+
+
+def test_index_update_128k():
+    """One 256-step update of the 128K workload; sampled rows."""
+    update_case(synth.workload(2), [256], rows_every=8)
+
+
+def test_update_twice_equals_once_and_noop():
+    wl = synth.workload(1, max_seq=6000)
+    inp = make(wl, seed=8)
+    n = int(inp["seq_lens"][0])
+    idx_inp = paper_form(inp, [n - 600])
+    one = new_context(idx_inp)
+    one.index_update([n], inp["k_cache"], inp["v_cache"])
+    two = new_context(idx_inp)
+    two.index_update([n - 300], inp["k_cache"], inp["v_cache"])
+    two.index_update([n], inp["k_cache"], inp["v_cache"])
+    e1, e2 = one.index_export_tokens(), two.index_export_tokens()
+    Rn = slice(inp["n_sink"], n - inp["n_local"])
+    for k in ("list_ids", "codes", "norms"):
+        assert torch.equal(e1[k][:, :, Rn], e2[k][:, :, Rn]), k
+    assert float((e1["list_means"] - e2["list_means"]).abs().max()) <= 1e-6
+    topk = inp["topk"].tolist()
+    _, out1, sel1, _, _ = run(one, inp, topk)
+    # equal lengths: a no-op rebuild
+    one.index_update([n], inp["k_cache"], inp["v_cache"])
+    _, out1b, sel1b, _, _ = run(one, inp, topk)
+    assert torch.equal(sel1, sel1b) and torch.equal(out1, out1b)
+    for bad in ([n - 1], [wl.max_seq + 1]):
+        with pytest.raises(pqhsa.PQHSAError) as e:
+            one.index_update(bad, inp["k_cache"], inp["v_cache"])
+        assert e.value.status == pqhsa.ERR_INVALID_ARGUMENT
+
+
+TAIL_CASES = {
+    "32k-shape": (synth.workload(1, max_seq=8000), [300], "B"),
+    "ragged": (synth.workload(4, batch=3, max_seq=6000, ragged_min=3500, n_list=40),
+               [0, 1024, 257], "B"),
+    "g8-bx": (synth.workload(3, batch=2, max_seq=3000, n_q_heads=16, n_kv_heads=2, n_list=16,
+                             topk=60), [200, 700], "Bx"),
+}
+
+
+@pytest.mark.parametrize("case", list(TAIL_CASES))
+def test_tail_grows_between_updates(case):
+    """Tokens past the index stay exact: L_b = every token after R_b."""
+    wl, growth, variant = TAIL_CASES[case]
+    inp = make(wl, seed=10)
+    full = [int(x) for x in inp["seq_lens"]]
+    old = [n - gr for n, gr in zip(full, growth)]
+    ctx = new_context(dict(inp, seq_lens=torch.tensor(old, dtype=torch.int32)))
+    ctx.set_option(pqhsa.OPT_VARIANT, {"B": pqhsa.VARIANT_B, "Bx": pqhsa.VARIANT_BX}[variant])
+    ctx.set_lengths(full)
+    topk = inp["topk"].tolist()
+    for b in range(wl.batch):   # the budget is over the indexed region
+        topk[b] = min(topk[b], old[b] - inp["n_sink"] - inp["n_local"])
+    _, out, sel, unsel, _ = run(ctx, inp, topk)
+    for b in range(wl.batch):
+        sub = dict(inp, n_local=inp["n_local"] + growth[b])
+        rows = [(b, h) for h in range(0, wl.n_q_heads, 3)]
+        check_rows(sub, topk, rows, out, sel, unsel, variant=variant)
+    over = list(old)
+    over[0] = old[0] + 1025
+    under = list(full)
+    under[0] = old[0] - 1
+    for bad in (over, under):
+        if bad[0] > wl.max_seq:
+            continue
+        with pytest.raises(pqhsa.PQHSAError) as e:
+            ctx.set_lengths(bad)
+        assert e.value.status == pqhsa.ERR_INVALID_ARGUMENT
+    # an update indexes the tail down to the local window again
+    ctx.index_update(full, inp["k_cache"], inp["v_cache"])
+    _, out2, *_ = run(ctx, inp, topk)
+    assert torch.isfinite(out2).all()
