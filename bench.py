@@ -378,8 +378,8 @@ def main() -> int:
         del pages, kp, vp
 
     # the incremental index update: 256 tokens leave the local window and are
-    # encoded into the lists (wall time of the whole call: encode and means
-    # kernels, the host counting sort, uploads and the list-major gather)
+    # encoded into the lists (wall time of the call and its kernels: encode,
+    # means, the list-major merge, the gather and the global means)
     update = None
     if not args.no_pq4:
         ctxu = pqhsa.context_for(inp)
@@ -390,6 +390,7 @@ def main() -> int:
             torch.cuda.synchronize()
             t0 = time.perf_counter()
             ctxu.index_update([n + 256 * i for n in n0], kc, vc)
+            torch.cuda.synchronize()
             t_up.append(time.perf_counter() - t0)
         ms_up = 1e3 * float(np.median(t_up))
         update = {"tokens_per_update": 256, "ms_per_update": round(ms_up, 3),

@@ -120,12 +120,15 @@ pqhsa_status pqhsa_index_prepare(pqhsa_ctx* ctx, const int32_t* seq_lens,
  *     has r = 0.
  *   - The list means are refreshed over the grown lists (Eq. 4), in
  *     float64: (n_old v_bar + sum of new v) / (n_old + n_new).
- *   - The list-major layout is rebuilt as by pqhsa_index_prepare.
+ *   - The list-major layout becomes that of pqhsa_index_prepare over the
+ *     grown lists (lists in increasing id, tokens in increasing id within a
+ *     list), merged on the device: old members shift right, new ones append.
  * k_cache / v_cache / kv_strides as in pqhsa_decode (keys and values of
  * every token up to new_seq_lens). Equal lengths are a no-op rebuild.
- * Synchronises `stream`; allocates nothing. INVALID_ARGUMENT for a length
- * that shrinks or exceeds max_seq. After any other failure the index is
- * unspecified until the next successful prepare. */
+ * Asynchronous: enqueues kernels on `stream`, allocates nothing. Host
+ * checks first: INVALID_ARGUMENT for a length that shrinks or exceeds
+ * max_seq. After a launch failure the index is unspecified until the next
+ * successful prepare. */
 pqhsa_status pqhsa_index_update(pqhsa_ctx* ctx, const int32_t* new_seq_lens,
                                 const void* k_cache, const void* v_cache,
                                 const int64_t* kv_strides, hipStream_t stream);

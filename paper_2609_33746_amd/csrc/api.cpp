@@ -52,6 +52,12 @@ struct pqhsa_ctx {
     int32_t* ids_tm = nullptr;       // the same on the device
     uint8_t* codes_tm = nullptr;     // [B, Hkv, rcap, M] one code per byte
     float* norms_tm = nullptr;       // [B, Hkv, rcap]
+    // the other half of the double-buffered list-major arrays (an update
+    // builds the new layout there, then the two halves swap)
+    int32_t* perm_alt = nullptr;
+    uint32_t* pos_alt = nullptr;
+    int32_t* loff_alt = nullptr;
+    int32_t* shift = nullptr;        // [B, Hkv, n_list] per-list position shift of an update
     int32_t* n_seq_dev = nullptr;
     int32_t* n_r_dev = nullptr;
     int scan_nwg = 0;   // scan workgroups per (b, kv head)
@@ -297,6 +303,10 @@ pqhsa_status pqhsa_create(const pqhsa_shape* shape, pqhsa_ctx** out) {
     A(dev_alloc(c, &c->ids_tm, BG * rc));
     A(dev_alloc(c, &c->codes_tm, BG * rc * static_cast<size_t>(shape->pq_m)));
     A(dev_alloc(c, &c->norms_tm, BG * rc));
+    A(dev_alloc(c, &c->perm_alt, BG * rc));
+    A(dev_alloc(c, &c->pos_alt, BG * rc));
+    A(dev_alloc(c, &c->loff_alt, BG * (L + 1)));
+    A(dev_alloc(c, &c->shift, BG * L));
     A(dev_alloc(c, &c->n_seq_dev, B));
     A(dev_alloc(c, &c->n_r_dev, B));
     A(dev_alloc(c, &w.lut, BG * lut_row * G));
@@ -478,19 +488,33 @@ pqhsa_status pqhsa_index_update(pqhsa_ctx* c, const int32_t* new_seq_lens, const
         hi.v[b] = lens[b] - D.n_local;
         max_new = std::max(max_new, hi.v[b] - lo.v[b]);
     }
+    // encode and refresh the means (both read the old list offsets), merge
+    // the new tokens into the other half of the list-major arrays, swap the
+    // halves, then gather codes and norms into the new order
+    c->prepared = false;
     hipError_t e = launch_update(D, lo, hi, max_new, kv, c->centroids, c->codebooks, c->loff,
                                  c->ids_tm, c->codes_tm, c->norms_tm, c->means, stream);
+    if (e == hipSuccess)
+        e = launch_update_lists(D, lo, hi, c->ids_tm, c->loff, c->perm, c->pos_word, c->loff_alt,
+                                c->shift, c->perm_alt, c->pos_alt, c->tok_list, c->n_r_dev,
+                                c->n_seq_dev, stream);
     if (e != hipSuccess) return hip_fail(c, e, "launching the index update");
-    for (int b = 0; b < D.B && e == hipSuccess; ++b)
-        for (int g = 0; g < D.Hkv && e == hipSuccess; ++g) {
-            const size_t off = (static_cast<size_t>(b) * D.Hkv + g) * rc + lo.v[b];
-            if (hi.v[b] > lo.v[b])
-                e = hipMemcpyAsync(c->ids_host.data() + off, c->ids_tm + off,
-                                   (hi.v[b] - lo.v[b]) * sizeof(int32_t), hipMemcpyDeviceToHost, stream);
-        }
-    if (e == hipSuccess) e = hipStreamSynchronize(stream);
-    if (e != hipSuccess) return hip_fail(c, e, "encoding the new tokens");
-    return relayout(c, lens, stream);
+    std::swap(c->perm, c->perm_alt);
+    std::swap(c->pos_word, c->pos_alt);
+    std::swap(c->loff, c->loff_alt);
+    e = launch_prepare_gather(D, c->codes_tm, c->norms_tm, c->index(), c->codes, c->norms, stream);
+    if (e == hipSuccess) e = launch_glob_mean(D, c->index(), c->glob_mean, stream);
+    if (e != hipSuccess) return hip_fail(c, e, "launching the index rebuild");
+    int nr_max = 0;
+    for (int b = 0; b < D.B; ++b) {
+        c->n_r[b] = lens[b] - D.n_sink - D.n_local;
+        nr_max = std::max(nr_max, c->n_r[b]);
+    }
+    c->seq_lens = lens;
+    c->cur_len = lens;
+    c->scan_nwg = (nr_max + kScanWaves * kSub - 1) / (kScanWaves * kSub);
+    c->prepared = true;   // ids_host now lags the device; only a prepare reads it, after replacing it
+    return PQHSA_OK;
 }
 
 pqhsa_status pqhsa_set_lengths(pqhsa_ctx* c, const int32_t* seq_lens) {

@@ -190,6 +190,16 @@ hipError_t launch_update(const Dims& D, const BatchInts& lo, const BatchInts& hi
                          const KV& kv, const float* centroids, const float* codebooks,
                          const int32_t* old_loff, int32_t* ids_tm, uint8_t* codes_tm,
                          float* norms_tm, float* means, hipStream_t s);
+// the list-major rebuild after launch_update (lo, hi as there): new list
+// offsets, per-list shifts [B, Hkv, n_list] and the new perm / pos_word in the
+// *_new buffers (which must not alias the old ones); tok_list, n_r and n_seq
+// updated in place
+hipError_t launch_update_lists(const Dims& D, const BatchInts& lo, const BatchInts& hi,
+                               const int32_t* ids_tm, const int32_t* old_loff,
+                               const int32_t* perm_old, const uint32_t* pos_old, int32_t* new_loff,
+                               int32_t* shift, int32_t* perm_new, uint32_t* pos_new,
+                               uint16_t* tok_list, int32_t* n_r_dev, int32_t* n_seq_dev,
+                               hipStream_t s);
 hipError_t launch_prepare_gather(const Dims& D, const uint8_t* codes_in, const float* norms_in,
                                  const Index& ix, uint8_t* codes_out, float* norms_out,
                                  hipStream_t s);

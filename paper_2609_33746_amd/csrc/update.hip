@@ -173,6 +173,135 @@ __global__ __launch_bounds__(kHeadDim) void means_update_kernel(
     *mean = static_cast<float>(v);
 }
 
+// List-major rebuild after an update, on the device. The new tokens of a
+// (b, g) have larger ids than every indexed one, so each list keeps its old
+// members in order and appends its new ones in increasing id: an old position
+// p of list j moves to p + (new members of lists before j), and the r-th new
+// member of list j lands at old_end(j) + (new members of lists before j) + r.
+//
+// update_lists_kernel: one workgroup per (b, g). Counts the new members per
+// list (LDS atomics), scans the counts into the per-list shifts, writes the
+// new list offsets, and places the new tokens chunk by chunk in id order
+// (rank within a chunk = earlier lanes of the chunk with the same list).
+constexpr int kListThreads = 1024;
+constexpr int kScanPer = kMaxLists / kListThreads;   // list counts per thread in the scan
+
+__global__ __launch_bounds__(kListThreads) void update_lists_kernel(
+    Dims D, BatchInts lo, BatchInts hi, const int32_t* __restrict__ ids_tm,
+    const int32_t* __restrict__ old_loff, int32_t* __restrict__ new_loff,
+    int32_t* __restrict__ shift, int32_t* __restrict__ perm_new, uint32_t* __restrict__ pos_new,
+    uint16_t* __restrict__ tok_list, int32_t* __restrict__ n_r_dev, int32_t* __restrict__ n_seq_dev) {
+    __shared__ int cnt[kMaxLists];     // new members per list, then the exclusive scan
+    __shared__ int placed[kMaxLists];  // new members placed so far per list
+    __shared__ int chunk[kListThreads];
+    __shared__ int wtot[kListThreads / kWave];
+    const int bg = blockIdx.x;
+    const int b = bg / D.Hkv;
+    const int tid = threadIdx.x;
+    const int L = D.n_list;
+    const int t0 = lo.v[b], t1 = hi.v[b];
+    if (tid == 0 && bg % D.Hkv == 0) {
+        n_r_dev[b] = t1 - D.n_sink;
+        n_seq_dev[b] = t1 + D.n_local;
+    }
+    for (int j = tid; j < L; j += kListThreads) {
+        cnt[j] = 0;
+        placed[j] = 0;
+    }
+    __syncthreads();
+    const int32_t* ids = ids_tm + static_cast<int64_t>(bg) * D.rcap;
+    for (int t = t0 + tid; t < t1; t += kListThreads) atomicAdd(&cnt[ids[t]], 1);
+    __syncthreads();
+    // exclusive scan of cnt[0, L): kScanPer consecutive entries per thread
+    int v[kScanPer];
+    int mine = 0;
+#pragma unroll
+    for (int u = 0; u < kScanPer; ++u) {
+        const int j = tid * kScanPer + u;
+        v[u] = j < L ? cnt[j] : 0;
+        mine += v[u];
+    }
+    int incl = mine;   // inclusive scan over the wave
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        const int o = __shfl_up(incl, off);
+        if (lane_id() >= off) incl += o;
+    }
+    if (lane_id() == kWave - 1) wtot[tid / kWave] = incl;
+    __syncthreads();
+    int base = incl - mine;
+    for (int w = 0; w < tid / kWave; ++w) base += wtot[w];
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < kScanPer; ++u) {
+        const int j = tid * kScanPer + u;
+        if (j < L) cnt[j] = base;
+        base += v[u];
+    }
+    __syncthreads();
+    const int32_t* ol = old_loff + static_cast<int64_t>(bg) * (L + 1);
+    int32_t* nl = new_loff + static_cast<int64_t>(bg) * (L + 1);
+    for (int j = tid; j <= L; j += kListThreads) nl[j] = ol[j] + (j < L ? cnt[j] : t1 - t0);
+    for (int j = tid; j < L; j += kListThreads) shift[static_cast<int64_t>(bg) * L + j] = cnt[j];
+    const int64_t row = static_cast<int64_t>(bg) * D.rcap;
+    for (int c0 = t0; c0 < t1; c0 += kListThreads) {
+        const int t = c0 + tid;
+        const int j = t < t1 ? ids[t] : -1;
+        chunk[tid] = j;
+        __syncthreads();
+        if (t < t1) {
+            int r = 0;
+            for (int i = 0; i < tid; ++i) r += chunk[i] == j;
+            const int pos = ol[j + 1] + cnt[j] + placed[j] + r;
+            perm_new[row + pos] = t;
+            pos_new[row + pos] = (static_cast<uint32_t>(j) << kPosBits) | static_cast<uint32_t>(t);
+            tok_list[row + t] = static_cast<uint16_t>(j);
+        }
+        __syncthreads();
+        if (t < t1) atomicAdd(&placed[j], 1);
+        __syncthreads();
+    }
+}
+
+// shift_positions_kernel: the old members move right by their list's shift;
+// positions past the new |R_b| are cleared (perm -1).
+__global__ __launch_bounds__(256) void shift_positions_kernel(
+    Dims D, BatchInts lo, BatchInts hi, const int32_t* __restrict__ shift,
+    const int32_t* __restrict__ perm_old, const uint32_t* __restrict__ pos_old,
+    int32_t* __restrict__ perm_new, uint32_t* __restrict__ pos_new) {
+    const int p = blockIdx.x * 256 + threadIdx.x;
+    const int bg = blockIdx.y;
+    if (p >= D.rcap) return;
+    const int b = bg / D.Hkv;
+    const int old_nr = lo.v[b] - D.n_sink, new_nr = hi.v[b] - D.n_sink;
+    const int64_t row = static_cast<int64_t>(bg) * D.rcap;
+    if (p < old_nr) {
+        const uint32_t w = pos_old[row + p];
+        const int q = p + shift[static_cast<int64_t>(bg) * D.n_list + static_cast<int>(w >> kPosBits)];
+        perm_new[row + q] = perm_old[row + p];
+        pos_new[row + q] = w;
+    } else if (p >= new_nr) {
+        perm_new[row + p] = -1;
+        pos_new[row + p] = 0u;
+    }
+}
+
+hipError_t launch_update_lists(const Dims& D, const BatchInts& lo, const BatchInts& hi,
+                               const int32_t* ids_tm, const int32_t* old_loff,
+                               const int32_t* perm_old, const uint32_t* pos_old, int32_t* new_loff,
+                               int32_t* shift, int32_t* perm_new, uint32_t* pos_new,
+                               uint16_t* tok_list, int32_t* n_r_dev, int32_t* n_seq_dev,
+                               hipStream_t s) {
+    hipLaunchKernelGGL(update_lists_kernel, dim3(D.B * D.Hkv), dim3(kListThreads), 0, s, D, lo, hi,
+                       ids_tm, old_loff, new_loff, shift, perm_new, pos_new, tok_list, n_r_dev,
+                       n_seq_dev);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(shift_positions_kernel, dim3((D.rcap + 255) / 256, D.B * D.Hkv), dim3(256), 0,
+                       s, D, lo, hi, shift, perm_old, pos_old, perm_new, pos_new);
+    return hipGetLastError();
+}
+
 template <typename T, typename PQ>
 static hipError_t launch_update_t(const Dims& D, const BatchInts& lo, const BatchInts& hi,
                                   int max_new, const KV& kv, const float* centroids,
