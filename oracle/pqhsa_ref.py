@@ -24,6 +24,11 @@ Everything is written from the paper's statement of the method:
   (`encode_ref`). Section 3.3 (execution path): later tokens are encoded
   into the existing lists without re-clustering, and each update refreshes
   the list means (`update_ref`).
+* Section 3.3 and Appendix "Index build": the index of each KV head is
+  built from its keys' directions by k-means, one coarse problem over the
+  directions and one problem per PQ subspace over the residual slices, with
+  key norms kept apart and empty clusters re-seeded (`kmeans_ref`,
+  `build_ref`; the paper's setting is one coarse and two PQ iterations).
 * Appendix B (variant definitions, Table "mechanism variants"): variants T
   (no background), C (token-weighted global value mean) and Bx (mean of the
   unselected members of each list).
@@ -35,7 +40,17 @@ Readings where the paper is silent:
 * "nearest" is the smallest squared Euclidean distance, ties going to the
   smaller list id or codeword index; a zero key has r = 0 and u = 0;
 * an update from n_old to n_new tokens indexes the tokens that leave the
-  local window, [max(n_sink, n_old - n_local), n_new - n_local).
+  local window, [max(n_sink, n_old - n_local), n_new - n_local);
+* k-means starts from given data points (the caller draws them); one
+  iteration assigns every point to its nearest center, then moves each
+  center to the mean of its points; a center left without points takes the
+  point farthest from its own center in that assignment (the farthest
+  first, ties to the smaller index, one point per empty center in
+  increasing center id);
+* the build trains the coarse centers on the directions of R, assigns,
+  trains each subspace's codewords on the residual slices starting from the
+  residuals of given tokens, and ends with `encode_ref` against the trained
+  model and the list means of the final lists.
 
 Parity pins for every function live in tests/test_oracle_pins.py (brute force,
 closed forms, special cases). No function here is "parity unpinned".
@@ -62,6 +77,8 @@ __all__ = [
     "Encoding",
     "encode_ref",
     "update_ref",
+    "kmeans_ref",
+    "build_ref",
 ]
 
 
@@ -259,6 +276,73 @@ def update_ref(list_ids, codes, norms, K, V, n_old: int, n_new: int, n_sink: int
     R = split_positions(n_new, n_sink, n_local)[2]
     means = list_means_ref(V, ids, np.asarray(centroids).shape[0], R)
     return ids, cds, nrm, means, enc
+
+
+def kmeans_ref(X, init_idx, n_iter: int):
+    """Lloyd's k-means on the rows of X [n, dim] from centers X[init_idx].
+
+    Each iteration: nearest center of every point (squared distance, ties to
+    the smaller center id), then each center becomes the mean of its points;
+    centers without points are re-seeded with the points farthest from their
+    assigned centers. Returns the centers [k, dim].
+    """
+    X = np.asarray(X, np.float64)
+    C = X[np.asarray(init_idx, np.int64)].copy()
+    n, k = X.shape[0], C.shape[0]
+    for _ in range(n_iter):
+        d2 = np.empty((n, k))
+        for s in range(0, n, 512):
+            d2[s:s + 512] = ((X[s:s + 512, None, :] - C[None]) ** 2).sum(axis=2)
+        a = d2.argmin(axis=1)
+        dmin = d2[np.arange(n), a]
+        cnt = np.bincount(a, minlength=k)
+        sums = np.zeros_like(C)
+        np.add.at(sums, a, X)
+        newC = C.copy()
+        nz = cnt > 0
+        newC[nz] = sums[nz] / cnt[nz, None]
+        empty = np.flatnonzero(cnt == 0)
+        if empty.size:
+            far = np.lexsort((np.arange(n), -dmin))   # farthest first, then smaller index
+            for e, j in enumerate(empty):
+                newC[j] = X[far[e]]
+        C = newC
+    return C
+
+
+def build_ref(K, V, R, n_list: int, M: int, ksub: int, init_coarse, init_pq,
+              n_iter_coarse: int = 1, n_iter_pq: int = 2):
+    """Build one (sequence, KV head) index from its keys over R.
+
+    K, V [>= max(R) + 1, d]; R the indexed token ids; init_coarse [n_list] and
+    init_pq [M, ksub] token ids of R whose direction (coarse) or residual
+    slice (subspace m) starts each center. Returns a dict with token-major
+    list_ids, codes, norms (entries outside R zero), centroids [n_list, d],
+    codebooks [M, ksub, d/M] and list_means [n_list, d].
+    """
+    K = np.asarray(K, np.float64)
+    R = np.asarray(R, np.int64)
+    n_tok, d = K.shape
+    ds = d // M
+    r = np.sqrt((K[R] ** 2).sum(axis=1))
+    U = np.zeros((R.size, d))
+    nz = r > 0
+    U[nz] = K[R][nz] / r[nz, None]
+    pos = {int(t): i for i, t in enumerate(R)}
+    C = kmeans_ref(U, [pos[int(t)] for t in init_coarse], n_iter_coarse)
+    a = encode_ref(K[R], C, np.zeros((M, 1, ds))).a
+    res = U - C[a]
+    P = np.stack([kmeans_ref(res[:, m * ds:(m + 1) * ds],
+                             [pos[int(t)] for t in np.asarray(init_pq)[m]], n_iter_pq)
+                  for m in range(M)])
+    enc = encode_ref(K[R], C, P)
+    ids = np.zeros(n_tok, np.int64)
+    codes = np.zeros((n_tok, M), np.int64)
+    norms = np.zeros(n_tok)
+    ids[R], codes[R], norms[R] = enc.a, enc.z, enc.r
+    means = list_means_ref(V, ids, n_list, R)
+    return dict(list_ids=ids, codes=codes, norms=norms, centroids=C, codebooks=P,
+                list_means=means, encoding=enc)
 
 
 # ---------------------------------------------------------------------------

@@ -487,3 +487,74 @@ def test_update_composes_and_matches_an_encoding_from_scratch():
     np.testing.assert_allclose(same[3], a2[3], atol=0)
     with pytest.raises(ValueError):
         R.update_ref(*a2[:3], K, V, n2, n1, n_sink, n_local, C, P)
+
+
+# ---------------------------------------------------------------------------
+# k-means and the index build (Section 3.3, Appendix "Index build")
+# ---------------------------------------------------------------------------
+def _blobs(seed, k=6, per=40, dim=8, spread=0.05):
+    rng = np.random.default_rng(seed)
+    centers = 3.0 * rng.standard_normal((k, dim))
+    X = np.concatenate([c + spread * rng.standard_normal((per, dim)) for c in centers])
+    return X, centers
+
+
+def test_kmeans_matches_scipy_lloyd():
+    """Without empty clusters the iteration is scipy's kmeans2 from given centers."""
+    import scipy.cluster.vq as vq
+    X, _ = _blobs(20)
+    rng = np.random.default_rng(21)
+    init = rng.choice(X.shape[0], 6, replace=False)
+    for n_iter in (1, 2, 5):
+        want, _ = vq.kmeans2(X, X[init].copy(), iter=n_iter, minit="matrix", missing="raise")
+        np.testing.assert_allclose(R.kmeans_ref(X, init, n_iter), want, atol=1e-12)
+    np.testing.assert_array_equal(R.kmeans_ref(X, init, 0), X[init])
+
+
+def test_kmeans_reseeds_empty_clusters_with_the_farthest_points():
+    X, _ = _blobs(22, k=3, per=30)
+    init = [0, 0, 0, 31]          # centers 1 and 2 tie with 0 and lose every point
+    C = R.kmeans_ref(X, init, 1)
+    a = np.array([0 if np.sum((x - X[0]) ** 2) <= np.sum((x - X[31]) ** 2) else 3 for x in X])
+    dist = np.array([np.sum((x - X[init][ai]) ** 2) for x, ai in zip(X, a)])
+    far = sorted(range(len(X)), key=lambda i: (-dist[i], i))
+    np.testing.assert_allclose(C[0], X[a == 0].mean(axis=0), atol=1e-12)
+    np.testing.assert_allclose(C[3], X[a == 3].mean(axis=0), atol=1e-12)
+    np.testing.assert_array_equal(C[1], X[far[0]])
+    np.testing.assert_array_equal(C[2], X[far[1]])
+
+
+def test_build_closed_forms_and_consistency():
+    """Zero iterations keep the drawn points: the coarse centers are the init
+    tokens' directions and each codeword the init token's residual slice; the
+    codes are the encoding against the built model, the means brute force."""
+    rng = np.random.default_rng(23)
+    n, d, M, ksub, n_list = 300, 16, 4, 8, 5
+    K = rng.standard_normal((n, d)) * rng.uniform(0.5, 2.0, size=(n, 1))
+    V = rng.standard_normal((n, d))
+    Rr = np.arange(4, n - 10)
+    init_c = rng.choice(Rr, n_list, replace=False)
+    init_p = np.stack([rng.choice(Rr, ksub, replace=False) for _ in range(M)])
+    b0 = R.build_ref(K, V, Rr, n_list, M, ksub, init_c, init_p, 0, 0)
+    U = K / np.linalg.norm(K, axis=1, keepdims=True)
+    np.testing.assert_allclose(b0["centroids"], U[init_c], atol=1e-15)
+    a = np.array([np.argmin(((U[t] - b0["centroids"]) ** 2).sum(axis=1)) for t in range(n)])
+    ds = d // M
+    for m in range(M):
+        for z in range(ksub):
+            t = init_p[m, z]
+            np.testing.assert_allclose(b0["codebooks"][m, z],
+                                       (U[t] - b0["centroids"][a[t]])[m * ds:(m + 1) * ds], atol=1e-15)
+    for it in ((1, 2), (3, 1)):
+        b = R.build_ref(K, V, Rr, n_list, M, ksub, init_c, init_p, *it)
+        enc = R.encode_ref(K[Rr], b["centroids"], b["codebooks"])
+        np.testing.assert_array_equal(b["list_ids"][Rr], enc.a)
+        np.testing.assert_array_equal(b["codes"][Rr], enc.z)
+        for j in range(n_list):
+            mem = Rr[enc.a == j]
+            want = V[mem].mean(axis=0) if mem.size else np.zeros(d)
+            np.testing.assert_allclose(b["list_means"][j], want, atol=1e-12)
+        # the coarse centers are one more k-means step over the directions of R
+        np.testing.assert_allclose(
+            b["centroids"], R.kmeans_ref(U[Rr], [int(np.flatnonzero(Rr == t)[0]) for t in init_c], it[0]),
+            atol=1e-12)
