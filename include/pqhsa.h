@@ -133,6 +133,37 @@ pqhsa_status pqhsa_index_update(pqhsa_ctx* ctx, const int32_t* new_seq_lens,
                                 const void* k_cache, const void* v_cache,
                                 const int64_t* kv_strides, hipStream_t stream);
 
+/* Build the index from the keys instead of taking one (Section 3.3 and the
+ * appendix on the index build): k-means over every (sequence, KV head) at
+ * once, then the context holds it as after pqhsa_index_prepare.
+ *   - Each key of R_b is split into its norm (fp32) and direction u.
+ *   - The coarse problem runs n_iter_coarse Lloyd iterations over the
+ *     directions. Each iteration assigns every point to its nearest center
+ *     (squared distance in fp32, ties to the smaller id), then moves each
+ *     center to the float64 mean of its points. A center left without points
+ *     takes the point farthest from its assigned center: the farthest first,
+ *     ties to the smaller token id, one point per empty center in increasing
+ *     center id.
+ *   - Every token is then assigned to its list. Each of the M subspace
+ *     problems runs n_iter_pq iterations over the residual slices
+ *     (u - c_a)^(m), by the same rule.
+ *   - Every token is then encoded against the trained model, and the list
+ *     means are taken over the final lists.
+ * The paper's setting is one coarse and two subspace iterations.
+ *   seq_lens    HOST int32 [B]: N_b as in pqhsa_index_prepare
+ *   k_cache, v_cache, kv_strides: as in pqhsa_decode
+ *   init_coarse DEVICE int32 [B, Hkv, n_list]: token ids in R_b whose
+ *               directions start the coarse centers (drawn by the caller)
+ *   init_pq     DEVICE int32 [B, Hkv, M, K]: token ids in R_b whose residual
+ *               slices start the codewords
+ * Allocates and frees its own scratch (about 4 (M + 2) bytes per cache slot)
+ * and synchronises `stream`. INVALID_ARGUMENT for a starting token outside
+ * R_b or an iteration count outside [0, 64]. */
+pqhsa_status pqhsa_index_build(pqhsa_ctx* ctx, const int32_t* seq_lens, const void* k_cache,
+                               const void* v_cache, const int64_t* kv_strides,
+                               const int32_t* init_coarse, const int32_t* init_pq,
+                               int32_t n_iter_coarse, int32_t n_iter_pq, hipStream_t stream);
+
 /* Set the current cache lengths N_b (HOST int32 [B]) between index updates
  * (Section 3.3: new tokens stay exact until the next update encodes them).
  * The tokens past R_b, [n_sink + |R_b|, N_b), form the exact tail L_b of
@@ -149,10 +180,12 @@ pqhsa_status pqhsa_set_lengths(pqhsa_ctx* ctx, const int32_t* seq_lens);
  *   list_ids   int32 [B, Hkv, max_seq]
  *   codes      uint8 [B, Hkv, max_seq, M], one code per byte
  *   norms      float [B, Hkv, max_seq]
- *   list_means float [B, Hkv, n_list, d] */
+ *   list_means float [B, Hkv, n_list, d]
+ *   centroids  float [B, Hkv, n_list, d]
+ *   codebooks  float [B, Hkv, M, K, d / M] */
 pqhsa_status pqhsa_index_export_tokens(pqhsa_ctx* ctx, int32_t* list_ids, uint8_t* codes,
-                                       float* norms, float* list_means,
-                                       hipStream_t stream);
+                                       float* norms, float* list_means, float* centroids,
+                                       float* codebooks, hipStream_t stream);
 
 /* One PQ-HSA decode step (Eqs. 2-5) for every (batch element, query head).
  *   q          [B, Hq, d] in kv_dtype, contiguous

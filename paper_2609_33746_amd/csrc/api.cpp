@@ -517,6 +517,107 @@ pqhsa_status pqhsa_index_update(pqhsa_ctx* c, const int32_t* new_seq_lens, const
     return PQHSA_OK;
 }
 
+pqhsa_status pqhsa_index_build(pqhsa_ctx* c, const int32_t* seq_lens, const void* k_cache,
+                               const void* v_cache, const int64_t* kv_strides,
+                               const int32_t* init_coarse, const int32_t* init_pq,
+                               int32_t n_iter_coarse, int32_t n_iter_pq, hipStream_t stream) {
+    if (!c) return fail(nullptr, PQHSA_ERR_INVALID_ARGUMENT, "ctx is NULL");
+    c->err.clear();
+    if (!seq_lens || !k_cache || !v_cache || !kv_strides || !init_coarse || !init_pq)
+        return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "every build argument must be non-NULL");
+    if (n_iter_coarse < 0 || n_iter_coarse > 64 || n_iter_pq < 0 || n_iter_pq > 64)
+        return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "iteration counts must lie in [0, 64]");
+    pqhsa_status st = check_device(c);
+    if (st != PQHSA_OK) return st;
+    KV kv;
+    st = check_kv(c, k_cache, k_cache, v_cache, kv_strides, k_cache, &kv);
+    if (st != PQHSA_OK) return st;
+    const Dims& D = c->D;
+    const size_t rc = D.rcap, BG = static_cast<size_t>(D.B) * D.Hkv, L = D.n_list;
+    const int M = c->shape.pq_m, Kc = c->shape.pq_ksub;
+    std::vector<int32_t> lens(seq_lens, seq_lens + D.B);
+    BatchInts lo{}, hi{};
+    int max_n = 0;
+    for (int b = 0; b < D.B; ++b) {
+        if (lens[b] < D.n_sink + D.n_local || lens[b] > D.rcap)
+            return fail(c, PQHSA_ERR_INVALID_ARGUMENT,
+                        "seq_lens[%d] = %d outside [n_sink + n_local, max_seq] = [%d, %d]", b, lens[b],
+                        D.n_sink + D.n_local, D.rcap);
+        lo.v[b] = D.n_sink;
+        hi.v[b] = lens[b] - D.n_local;
+        max_n = std::max(max_n, hi.v[b] - lo.v[b]);
+    }
+    // the drawn starting tokens must lie in R_b
+    std::vector<int32_t> ic(BG * L), ip(BG * M * Kc);
+    hipError_t e = hipMemcpyAsync(ic.data(), init_coarse, ic.size() * 4, hipMemcpyDeviceToHost, stream);
+    if (e == hipSuccess) e = hipMemcpyAsync(ip.data(), init_pq, ip.size() * 4, hipMemcpyDeviceToHost, stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) return hip_fail(c, e, "copying the starting tokens to the host");
+    for (size_t i = 0; i < ic.size() + ip.size(); ++i) {
+        const bool coarse = i < ic.size();
+        const size_t bg = coarse ? i / L : (i - ic.size()) / (static_cast<size_t>(M) * Kc);
+        const int t = coarse ? ic[i] : ip[i - ic.size()];
+        const int b = static_cast<int>(bg / D.Hkv);
+        if (t < lo.v[b] || t >= hi.v[b])
+            return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "%s starting token %d of (b %d, kv head %d) outside R_b",
+                        coarse ? "coarse" : "subspace", t, b, static_cast<int>(bg % D.Hkv));
+    }
+    c->prepared = false;
+    BuildBufs bb{};
+    const size_t n_offs = std::max(BG * (L + 1), BG * M * (Kc + 1));
+    e = hipMalloc(&bb.order, BG * M * rc * 4);
+    if (e == hipSuccess) e = hipMalloc(&bb.offs, n_offs * 4);
+    if (e == hipSuccess) e = hipMalloc(&bb.dist_c, BG * rc * 4);
+    if (e == hipSuccess) e = hipMalloc(&bb.dist_f, BG * rc * M * 4);
+    auto release = [&]() {
+        hipFree(bb.order);
+        hipFree(bb.offs);
+        hipFree(bb.dist_c);
+        hipFree(bb.dist_f);
+    };
+    if (e != hipSuccess) {
+        release();
+        return hip_fail(c, e, "allocating the build scratch");
+    }
+    float* C = c->centroids;
+    float* P = c->codebooks;
+    if (e == hipSuccess) e = hipMemsetAsync(C, 0, BG * L * kHeadDim * 4, stream);
+    if (e == hipSuccess) e = hipMemsetAsync(P, 0, BG * c->codebook_floats * 4, stream);
+    auto encode = [&]() {
+        if (e == hipSuccess)
+            e = launch_encode(D, lo, hi, max_n, kv, C, P, c->ids_tm, c->codes_tm, c->norms_tm,
+                              bb.dist_c, bb.dist_f, stream);
+    };
+    encode();   // the norms of R (the assignments against the zero model are discarded)
+    if (e == hipSuccess) e = launch_init_centers(D, 0, kv, init_coarse, c->ids_tm, c->norms_tm, C, C, stream);
+    for (int it = 0; it < n_iter_coarse; ++it) {
+        encode();
+        if (e == hipSuccess) e = launch_group(D, lo, hi, 0, c->ids_tm, c->codes_tm, bb, stream);
+        if (e == hipSuccess) e = launch_centers(D, lo, hi, 0, kv, c->ids_tm, c->norms_tm, C, bb, C, stream);
+        if (e == hipSuccess) e = launch_reseed(D, lo, hi, 0, kv, c->ids_tm, c->norms_tm, C, bb, C, stream);
+    }
+    encode();   // the final lists
+    if (e == hipSuccess) e = launch_init_centers(D, 1, kv, init_pq, c->ids_tm, c->norms_tm, C, P, stream);
+    for (int it = 0; it < n_iter_pq; ++it) {
+        encode();
+        if (e == hipSuccess) e = launch_group(D, lo, hi, 1, c->ids_tm, c->codes_tm, bb, stream);
+        if (e == hipSuccess) e = launch_centers(D, lo, hi, 1, kv, c->ids_tm, c->norms_tm, C, bb, P, stream);
+        if (e == hipSuccess) e = launch_reseed(D, lo, hi, 1, kv, c->ids_tm, c->norms_tm, C, bb, P, stream);
+    }
+    encode();   // the final codes
+    if (e == hipSuccess) e = launch_group(D, lo, hi, 0, c->ids_tm, c->codes_tm, bb, stream);
+    if (e == hipSuccess)
+        e = launch_centers(D, lo, hi, 2, kv, c->ids_tm, c->norms_tm, C, bb, c->means, stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    release();
+    if (e != hipSuccess) return hip_fail(c, e, "building the index");
+    c->ids_host.resize(BG * rc);   // empty when no prepare came first
+    e = hipMemcpyAsync(c->ids_host.data(), c->ids_tm, BG * rc * 4, hipMemcpyDeviceToHost, stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
+    if (e != hipSuccess) return hip_fail(c, e, "copying the built lists to the host");
+    return relayout(c, lens, stream);
+}
+
 pqhsa_status pqhsa_set_lengths(pqhsa_ctx* c, const int32_t* seq_lens) {
     if (!c) return fail(nullptr, PQHSA_ERR_INVALID_ARGUMENT, "ctx is NULL");
     c->err.clear();
@@ -535,7 +636,8 @@ pqhsa_status pqhsa_set_lengths(pqhsa_ctx* c, const int32_t* seq_lens) {
 }
 
 pqhsa_status pqhsa_index_export_tokens(pqhsa_ctx* c, int32_t* list_ids, uint8_t* codes,
-                                       float* norms, float* list_means, hipStream_t stream) {
+                                       float* norms, float* list_means, float* centroids,
+                                       float* codebooks, hipStream_t stream) {
     if (!c) return fail(nullptr, PQHSA_ERR_INVALID_ARGUMENT, "ctx is NULL");
     c->err.clear();
     if (!c->prepared) return fail(c, PQHSA_ERR_NOT_PREPARED, "pqhsa_index_prepare has not succeeded");
@@ -551,6 +653,9 @@ pqhsa_status pqhsa_index_export_tokens(pqhsa_ctx* c, int32_t* list_ids, uint8_t*
     D2D(codes, c->codes_tm, BGR * c->shape.pq_m);
     D2D(norms, c->norms_tm, BGR * 4);
     D2D(list_means, c->means, nmean * 4);
+    D2D(centroids, c->centroids, nmean * 4);
+    D2D(codebooks, c->codebooks,
+        static_cast<size_t>(c->D.B) * c->D.Hkv * c->codebook_floats * 4);
     if (e == hipSuccess) e = hipStreamSynchronize(stream);
     if (e != hipSuccess) return hip_fail(c, e, "exporting the index");
     return PQHSA_OK;

@@ -237,4 +237,38 @@ __device__ __forceinline__ uint32_t counter_read(const uint32_t* c) {
 }
 __device__ __forceinline__ void acquire_device() { __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent"); }
 
+// Exclusive prefix sum of cnt[0, n) in LDS by a workgroup of NT threads
+// (n <= NT * PER; each thread scans PER consecutive entries). wtot: LDS
+// scratch of NT / 64 ints. Must be called by all threads; ends synchronised.
+template <int NT, int PER>
+__device__ __forceinline__ void lds_exclusive_scan(int* cnt, int n, int* wtot) {
+    const int tid = threadIdx.x;
+    int v[PER];
+    int mine = 0;
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+        const int j = tid * PER + u;
+        v[u] = j < n ? cnt[j] : 0;
+        mine += v[u];
+    }
+    int incl = mine;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        const int o = __shfl_up(incl, off);
+        if (lane_id() >= off) incl += o;
+    }
+    if (lane_id() == kWave - 1) wtot[tid / kWave] = incl;
+    __syncthreads();
+    int base = incl - mine;
+    for (int w = 0; w < tid / kWave; ++w) base += wtot[w];
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+        const int j = tid * PER + u;
+        if (j < n) cnt[j] = base;
+        base += v[u];
+    }
+    __syncthreads();
+}
+
 }  // namespace pqhsa

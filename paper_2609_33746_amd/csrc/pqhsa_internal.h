@@ -190,6 +190,36 @@ hipError_t launch_update(const Dims& D, const BatchInts& lo, const BatchInts& hi
                          const KV& kv, const float* centroids, const float* codebooks,
                          const int32_t* old_loff, int32_t* ids_tm, uint8_t* codes_tm,
                          float* norms_tm, float* means, hipStream_t s);
+// encode tokens [lo[b], hi[b]) of every (b, kv head) against the given model
+// (token-major ids / codes / norms); dist_c [B, Hkv, rcap] and dist_f
+// [B, Hkv, rcap, M], when not null, receive the squared distances to the
+// chosen centroid and codewords
+hipError_t launch_encode(const Dims& D, const BatchInts& lo, const BatchInts& hi, int max_new,
+                         const KV& kv, const float* centroids, const float* codebooks,
+                         int32_t* ids_tm, uint8_t* codes_tm, float* norms_tm, float* dist_c,
+                         float* dist_f, hipStream_t s);
+// index build steps (k-means over the tokens [lo[b], hi[b]) of each (b, kv head))
+struct BuildBufs {
+    int32_t* order;      // [problems, rcap] tokens grouped by center, in id order within a center
+    int32_t* offs;       // [problems, n_centers + 1]
+    float* dist_c;       // [B, Hkv, rcap]
+    float* dist_f;       // [B, Hkv, rcap, M]
+};
+// kind: 0 coarse centers over directions, 1 codewords over residual slices,
+// 2 list means over values
+hipError_t launch_group(const Dims& D, const BatchInts& lo, const BatchInts& hi, int kind,
+                        const int32_t* ids_tm, const uint8_t* codes_tm, const BuildBufs& bb,
+                        hipStream_t s);
+hipError_t launch_centers(const Dims& D, const BatchInts& lo, const BatchInts& hi, int kind,
+                          const KV& kv, const int32_t* ids_tm, const float* norms_tm,
+                          const float* centroids, const BuildBufs& bb, float* out, hipStream_t s);
+hipError_t launch_init_centers(const Dims& D, int kind, const KV& kv, const int32_t* init,
+                               const int32_t* ids_tm, const float* norms_tm, const float* centroids,
+                               float* out, hipStream_t s);
+hipError_t launch_reseed(const Dims& D, const BatchInts& lo, const BatchInts& hi, int kind,
+                         const KV& kv, const int32_t* ids_tm, const float* norms_tm,
+                         const float* centroids, const BuildBufs& bb, float* out, hipStream_t s);
+
 // the list-major rebuild after launch_update (lo, hi as there): new list
 // offsets, per-list shifts [B, Hkv, n_list] and the new perm / pos_word in the
 // *_new buffers (which must not alias the old ones); tok_list, n_r and n_seq

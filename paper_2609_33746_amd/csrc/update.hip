@@ -43,7 +43,8 @@ template <typename T, typename PQ>
 __global__ __launch_bounds__(kEncThreads) void encode_kernel(
     Dims D, BatchInts lo, BatchInts hi, const T* __restrict__ kcache, int64_t sb, int64_t sh,
     int64_t sn, const float* __restrict__ centroids, const float* __restrict__ codebooks,
-    int32_t* __restrict__ ids_tm, uint8_t* __restrict__ codes_tm, float* __restrict__ norms_tm) {
+    int32_t* __restrict__ ids_tm, uint8_t* __restrict__ codes_tm, float* __restrict__ norms_tm,
+    float* __restrict__ dist_c, float* __restrict__ dist_f) {
     __shared__ float su[kHeadDim];           // u, then the residual u - c_a
     __shared__ float sdist[kMaxLists];       // coarse distances, then [M][K] fine ones
     __shared__ float wsum[kEncWaves];
@@ -96,7 +97,10 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(
         int bi = 0;   // a valid id even if every distance is NaN
         for (int j = lane; j < D.n_list; j += kWave) argmin_fold(bd, bi, sdist[j], j);
         wave_argmin(bd, bi);
-        if (lane == 0) sa = bi;
+        if (lane == 0) {
+            sa = bi;
+            if (dist_c) dist_c[static_cast<int64_t>(bg) * D.rcap + t] = bd;
+        }
     }
     __syncthreads();
     const int a = sa;
@@ -122,7 +126,10 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(
         int bi = 0;   // a valid id even if every distance is NaN
         for (int z = lane; z < PQ::K; z += kWave) argmin_fold(bd, bi, sdist[m * PQ::K + z], z);
         wave_argmin(bd, bi);
-        if (lane == 0) codes_tm[tok * PQ::M + m] = static_cast<uint8_t>(bi);
+        if (lane == 0) {
+            codes_tm[tok * PQ::M + m] = static_cast<uint8_t>(bi);
+            if (dist_f) dist_f[tok * PQ::M + m] = bd;
+        }
     }
     if (tid == 0) {
         ids_tm[tok] = a;
@@ -212,33 +219,7 @@ __global__ __launch_bounds__(kListThreads) void update_lists_kernel(
     const int32_t* ids = ids_tm + static_cast<int64_t>(bg) * D.rcap;
     for (int t = t0 + tid; t < t1; t += kListThreads) atomicAdd(&cnt[ids[t]], 1);
     __syncthreads();
-    // exclusive scan of cnt[0, L): kScanPer consecutive entries per thread
-    int v[kScanPer];
-    int mine = 0;
-#pragma unroll
-    for (int u = 0; u < kScanPer; ++u) {
-        const int j = tid * kScanPer + u;
-        v[u] = j < L ? cnt[j] : 0;
-        mine += v[u];
-    }
-    int incl = mine;   // inclusive scan over the wave
-#pragma unroll
-    for (int off = 1; off < kWave; off <<= 1) {
-        const int o = __shfl_up(incl, off);
-        if (lane_id() >= off) incl += o;
-    }
-    if (lane_id() == kWave - 1) wtot[tid / kWave] = incl;
-    __syncthreads();
-    int base = incl - mine;
-    for (int w = 0; w < tid / kWave; ++w) base += wtot[w];
-    __syncthreads();
-#pragma unroll
-    for (int u = 0; u < kScanPer; ++u) {
-        const int j = tid * kScanPer + u;
-        if (j < L) cnt[j] = base;
-        base += v[u];
-    }
-    __syncthreads();
+    lds_exclusive_scan<kListThreads, kScanPer>(cnt, L, wtot);
     const int32_t* ol = old_loff + static_cast<int64_t>(bg) * (L + 1);
     int32_t* nl = new_loff + static_cast<int64_t>(bg) * (L + 1);
     for (int j = tid; j <= L; j += kListThreads) nl[j] = ol[j] + (j < L ? cnt[j] : t1 - t0);
@@ -302,15 +283,42 @@ hipError_t launch_update_lists(const Dims& D, const BatchInts& lo, const BatchIn
     return hipGetLastError();
 }
 
-template <typename T, typename PQ>
+hipError_t launch_encode(const Dims& D, const BatchInts& lo, const BatchInts& hi, int max_new,
+                         const KV& kv, const float* centroids, const float* codebooks,
+                         int32_t* ids_tm, uint8_t* codes_tm, float* norms_tm, float* dist_c,
+                         float* dist_f, hipStream_t s) {
+    if (max_new <= 0) return hipSuccess;
+    const dim3 grid(max_new, D.Hkv, D.B);
+    const bool p4 = D.pq_bits == 4;
+    if (kv.bf16) {
+        if (p4)
+            hipLaunchKernelGGL((encode_kernel<bf16_t, Pq4>), grid, dim3(kEncThreads), 0, s, D, lo, hi,
+                               static_cast<const bf16_t*>(kv.k), kv.sb, kv.sh, kv.sn, centroids,
+                               codebooks, ids_tm, codes_tm, norms_tm, dist_c, dist_f);
+        else
+            hipLaunchKernelGGL((encode_kernel<bf16_t, Pq8>), grid, dim3(kEncThreads), 0, s, D, lo, hi,
+                               static_cast<const bf16_t*>(kv.k), kv.sb, kv.sh, kv.sn, centroids,
+                               codebooks, ids_tm, codes_tm, norms_tm, dist_c, dist_f);
+    } else {
+        if (p4)
+            hipLaunchKernelGGL((encode_kernel<float, Pq4>), grid, dim3(kEncThreads), 0, s, D, lo, hi,
+                               static_cast<const float*>(kv.k), kv.sb, kv.sh, kv.sn, centroids,
+                               codebooks, ids_tm, codes_tm, norms_tm, dist_c, dist_f);
+        else
+            hipLaunchKernelGGL((encode_kernel<float, Pq8>), grid, dim3(kEncThreads), 0, s, D, lo, hi,
+                               static_cast<const float*>(kv.k), kv.sb, kv.sh, kv.sn, centroids,
+                               codebooks, ids_tm, codes_tm, norms_tm, dist_c, dist_f);
+    }
+    return hipGetLastError();
+}
+
+template <typename T>
 static hipError_t launch_update_t(const Dims& D, const BatchInts& lo, const BatchInts& hi,
                                   int max_new, const KV& kv, const float* centroids,
                                   const float* codebooks, const int32_t* old_loff, int32_t* ids_tm,
                                   uint8_t* codes_tm, float* norms_tm, float* means, hipStream_t s) {
-    hipLaunchKernelGGL((encode_kernel<T, PQ>), dim3(max_new, D.Hkv, D.B), dim3(kEncThreads), 0, s,
-                       D, lo, hi, static_cast<const T*>(kv.k), kv.sb, kv.sh, kv.sn, centroids,
-                       codebooks, ids_tm, codes_tm, norms_tm);
-    hipError_t e = hipGetLastError();
+    hipError_t e = launch_encode(D, lo, hi, max_new, kv, centroids, codebooks, ids_tm, codes_tm,
+                                 norms_tm, nullptr, nullptr, s);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((means_update_kernel<T>), dim3(D.n_list, D.Hkv, D.B), dim3(kHeadDim), 0, s,
                        D, lo, hi, static_cast<const T*>(kv.v), kv.sb, kv.sh, kv.sn, old_loff,
@@ -323,17 +331,10 @@ hipError_t launch_update(const Dims& D, const BatchInts& lo, const BatchInts& hi
                          const int32_t* old_loff, int32_t* ids_tm, uint8_t* codes_tm,
                          float* norms_tm, float* means, hipStream_t s) {
     if (max_new <= 0) return hipSuccess;
-    if (kv.bf16)
-        return D.pq_bits == 4
-                   ? launch_update_t<bf16_t, Pq4>(D, lo, hi, max_new, kv, centroids, codebooks,
-                                                  old_loff, ids_tm, codes_tm, norms_tm, means, s)
-                   : launch_update_t<bf16_t, Pq8>(D, lo, hi, max_new, kv, centroids, codebooks,
-                                                  old_loff, ids_tm, codes_tm, norms_tm, means, s);
-    return D.pq_bits == 4
-               ? launch_update_t<float, Pq4>(D, lo, hi, max_new, kv, centroids, codebooks, old_loff,
+    return kv.bf16 ? launch_update_t<bf16_t>(D, lo, hi, max_new, kv, centroids, codebooks, old_loff,
                                              ids_tm, codes_tm, norms_tm, means, s)
-               : launch_update_t<float, Pq8>(D, lo, hi, max_new, kv, centroids, codebooks, old_loff,
-                                             ids_tm, codes_tm, norms_tm, means, s);
+                   : launch_update_t<float>(D, lo, hi, max_new, kv, centroids, codebooks, old_loff,
+                                            ids_tm, codes_tm, norms_tm, means, s);
 }
 
 }  // namespace pqhsa

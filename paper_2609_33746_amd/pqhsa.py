@@ -60,7 +60,8 @@ def load_library(build_if_missing: bool = True) -> ctypes.CDLL:
         "pqhsa_decode_paged": ([P, P, P, P, P, P, I32, I32, P, P, P], I32),
         "pqhsa_index_update": ([P, P, P, P, P, P], I32),
         "pqhsa_set_lengths": ([P, P], I32),
-        "pqhsa_index_export_tokens": ([P, P, P, P, P, P], I32),
+        "pqhsa_index_export_tokens": ([P, P, P, P, P, P, P, P], I32),
+        "pqhsa_index_build": ([P, P, P, P, P, P, P, I32, I32, P], I32),
         "pqhsa_decode_debug": ([P, P, P, P, P, P, P, P, P, P, P], I32),
         "pqhsa_dense_decode": ([P, P, P, P, P, P, P, P], I32),
         "pqhsa_index_export": ([P, P, P, P], I32),
@@ -170,9 +171,24 @@ class PQHSA:
         norms = torch.empty((sh.batch, sh.n_kv_heads, sh.max_seq), dtype=torch.float32, device=dev)
         means = torch.empty((sh.batch, sh.n_kv_heads, sh.n_list, sh.head_dim), dtype=torch.float32,
                             device=dev)
+        cen = torch.empty_like(means)
+        cb = torch.empty((sh.batch, sh.n_kv_heads, sh.pq_m, sh.pq_ksub, sh.head_dim // sh.pq_m),
+                         dtype=torch.float32, device=dev)
         self._check(self.lib.pqhsa_index_export_tokens(self.ctx, _ptr(ids), _ptr(codes),
-                                                       _ptr(norms), _ptr(means), _stream()))
-        return dict(list_ids=ids, codes=codes, norms=norms, list_means=means)
+                                                       _ptr(norms), _ptr(means), _ptr(cen),
+                                                       _ptr(cb), _stream()))
+        return dict(list_ids=ids, codes=codes, norms=norms, list_means=means, centroids=cen,
+                    codebooks=cb)
+
+    def index_build(self, seq_lens, k_cache, v_cache, init_coarse, init_pq, n_iter_coarse=1,
+                    n_iter_pq=2):
+        """k-means build of the index from the keys (starting tokens drawn by the caller)."""
+        strides = self._kv(k_cache, v_cache)
+        ic = self._dev(init_coarse, torch.int32, "init_coarse")
+        ip = self._dev(init_pq, torch.int32, "init_pq")
+        self._check(self.lib.pqhsa_index_build(
+            self.ctx, _host_i32(list(seq_lens)), _ptr(k_cache), _ptr(v_cache), strides, _ptr(ic),
+            _ptr(ip), int(n_iter_coarse), int(n_iter_pq), _stream()))
 
     def _out(self, q, out):
         if out is None:
