@@ -583,28 +583,31 @@ pqhsa_status pqhsa_index_build(pqhsa_ctx* c, const int32_t* seq_lens, const void
     float* P = c->codebooks;
     if (e == hipSuccess) e = hipMemsetAsync(C, 0, BG * L * kHeadDim * 4, stream);
     if (e == hipSuccess) e = hipMemsetAsync(P, 0, BG * c->codebook_floats * 4, stream);
-    auto encode = [&]() {
+    // keep_lists: the subspace passes reuse the final lists instead of
+    // searching the (unchanged) centroids again
+    auto encode = [&](int keep_lists) {
         if (e == hipSuccess)
             e = launch_encode(D, lo, hi, max_n, kv, C, P, c->ids_tm, c->codes_tm, c->norms_tm,
-                              bb.dist_c, bb.dist_f, stream);
+                              bb.dist_c, bb.dist_f, keep_lists, stream);
     };
-    encode();   // the norms of R (the assignments against the zero model are discarded)
+    if (e == hipSuccess) e = hipMemsetAsync(c->ids_tm, 0, BG * rc * 4, stream);
+    encode(1);   // the norms of R (codes against the zero model are discarded)
     if (e == hipSuccess) e = launch_init_centers(D, 0, kv, init_coarse, c->ids_tm, c->norms_tm, C, C, stream);
     for (int it = 0; it < n_iter_coarse; ++it) {
-        encode();
+        encode(0);
         if (e == hipSuccess) e = launch_group(D, lo, hi, 0, c->ids_tm, c->codes_tm, bb, stream);
         if (e == hipSuccess) e = launch_centers(D, lo, hi, 0, kv, c->ids_tm, c->norms_tm, C, bb, C, stream);
         if (e == hipSuccess) e = launch_reseed(D, lo, hi, 0, kv, c->ids_tm, c->norms_tm, C, bb, C, stream);
     }
-    encode();   // the final lists
+    encode(0);   // the final lists
     if (e == hipSuccess) e = launch_init_centers(D, 1, kv, init_pq, c->ids_tm, c->norms_tm, C, P, stream);
     for (int it = 0; it < n_iter_pq; ++it) {
-        encode();
+        encode(1);
         if (e == hipSuccess) e = launch_group(D, lo, hi, 1, c->ids_tm, c->codes_tm, bb, stream);
         if (e == hipSuccess) e = launch_centers(D, lo, hi, 1, kv, c->ids_tm, c->norms_tm, C, bb, P, stream);
         if (e == hipSuccess) e = launch_reseed(D, lo, hi, 1, kv, c->ids_tm, c->norms_tm, C, bb, P, stream);
     }
-    encode();   // the final codes
+    encode(1);   // the final codes
     if (e == hipSuccess) e = launch_group(D, lo, hi, 0, c->ids_tm, c->codes_tm, bb, stream);
     if (e == hipSuccess)
         e = launch_centers(D, lo, hi, 2, kv, c->ids_tm, c->norms_tm, C, bb, c->means, stream);

@@ -9,9 +9,9 @@
 //    problem's tokens by their center (LDS histogram, prefix sum, placement
 //    chunk by chunk in token order), so that every mean below adds its
 //    members in a fixed order.
-//  * centers_kernel: one workgroup per (center, problem), one thread per
-//    dimension; the float64 mean of the members' directions, residual slices
-//    or values (the list means).
+//  * centers_kernel: one workgroup per (center, problem), groups of one
+//    thread per dimension over the members; the float64 mean of the
+//    members' directions, residual slices or values (the list means).
 //  * reseed_kernel: one workgroup per problem; a center without members
 //    takes the point farthest from its assigned center (farthest first, ties
 //    to the smaller token id; one point per empty center, in center order).
@@ -107,31 +107,44 @@ __global__ __launch_bounds__(kGroupThreads) void group_kernel(Dims D, BatchInts 
     }
 }
 
+// 1024 threads per center: 1024 / dims groups of one thread per dimension;
+// group gi adds members gi, gi + groups, ... in order, then group 0 adds the
+// group sums in group order (a fixed order: the build is deterministic).
+constexpr int kCenThreads = 1024;
+
 template <typename T>
-__global__ __launch_bounds__(kHeadDim) void centers_kernel(Dims D, int kind, KV kv,
-                                                           const int32_t* ids_tm,
-                                                           const float* norms_tm,
-                                                           const float* centroids,
-                                                           const int32_t* order,
-                                                           const int32_t* offs, float* out) {
+__global__ __launch_bounds__(kCenThreads) void centers_kernel(Dims D, int kind, KV kv,
+                                                              const int32_t* ids_tm,
+                                                              const float* norms_tm,
+                                                              const float* centroids,
+                                                              const int32_t* order,
+                                                              const int32_t* offs, float* out) {
+    __shared__ double part[kCenThreads];
     const int c = blockIdx.x;
     const int p = blockIdx.y;
     const Problem pr = problem_of(D, kind, p);
-    const int x = threadIdx.x;
-    if (c >= pr.nkeys || x >= pr.dims) return;
+    if (c >= pr.nkeys) return;
+    const int groups = kCenThreads / pr.dims;
+    const int gi = threadIdx.x / pr.dims;
+    const int x = threadIdx.x % pr.dims;
     const int32_t* of = offs + static_cast<int64_t>(p) * (pr.nkeys + 1);
     const int o0 = of[c], o1 = of[c + 1];
     if (o1 == o0) {   // empty: the list mean is 0; a center is re-seeded afterwards
-        if (kind == 2) out[center_index(D, kind, pr, c, x)] = 0.0f;
+        if (kind == 2 && gi == 0) out[center_index(D, kind, pr, c, x)] = 0.0f;
         return;
     }
     const int32_t* ord = order + static_cast<int64_t>(p) * D.rcap;
     double acc = 0.0;
-#pragma unroll 8
-    for (int i = o0; i < o1; ++i)
+#pragma unroll 4
+    for (int i = o0 + gi; i < o1; i += groups)
         acc += static_cast<double>(
             token_elem<T>(D, kind, kv, pr.bg, pr.m, pr.dims, ord[i], x, ids_tm, norms_tm, centroids));
-    out[center_index(D, kind, pr, c, x)] = static_cast<float>(acc / (o1 - o0));
+    part[threadIdx.x] = acc;
+    __syncthreads();
+    if (gi != 0) return;
+    double sum = 0.0;
+    for (int w = 0; w < groups; ++w) sum += part[w * pr.dims + x];
+    out[center_index(D, kind, pr, c, x)] = static_cast<float>(sum / (o1 - o0));
 }
 
 template <typename T>
@@ -250,10 +263,10 @@ hipError_t launch_centers(const Dims& D, const BatchInts& lo, const BatchInts& h
     (void)hi;
     const dim3 grid(n_keys(D, kind), n_problems(D, kind));
     if (kv.bf16)
-        hipLaunchKernelGGL(centers_kernel<bf16_t>, grid, dim3(kHeadDim), 0, s, D, kind, kv, ids_tm,
+        hipLaunchKernelGGL(centers_kernel<bf16_t>, grid, dim3(kCenThreads), 0, s, D, kind, kv, ids_tm,
                            norms_tm, centroids, bb.order, bb.offs, out);
     else
-        hipLaunchKernelGGL(centers_kernel<float>, grid, dim3(kHeadDim), 0, s, D, kind, kv, ids_tm,
+        hipLaunchKernelGGL(centers_kernel<float>, grid, dim3(kCenThreads), 0, s, D, kind, kv, ids_tm,
                            norms_tm, centroids, bb.order, bb.offs, out);
     return hipGetLastError();
 }

@@ -193,11 +193,12 @@ hipError_t launch_update(const Dims& D, const BatchInts& lo, const BatchInts& hi
 // encode tokens [lo[b], hi[b]) of every (b, kv head) against the given model
 // (token-major ids / codes / norms); dist_c [B, Hkv, rcap] and dist_f
 // [B, Hkv, rcap, M], when not null, receive the squared distances to the
-// chosen centroid and codewords
+// chosen centroid and codewords; keep_lists: take each token's list from
+// ids_tm instead of searching the centroids
 hipError_t launch_encode(const Dims& D, const BatchInts& lo, const BatchInts& hi, int max_new,
                          const KV& kv, const float* centroids, const float* codebooks,
                          int32_t* ids_tm, uint8_t* codes_tm, float* norms_tm, float* dist_c,
-                         float* dist_f, hipStream_t s);
+                         float* dist_f, int keep_lists, hipStream_t s);
 // index build steps (k-means over the tokens [lo[b], hi[b]) of each (b, kv head))
 struct BuildBufs {
     int32_t* order;      // [problems, rcap] tokens grouped by center, in id order within a center

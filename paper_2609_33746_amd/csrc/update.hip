@@ -2,7 +2,7 @@
 // are encoded into the existing lists, without re-clustering, and the list
 // means are refreshed over the grown lists.
 //
-//  * encode_kernel: one workgroup per new token. The key is split into its
+//  * encode_kernel: one workgroup per 64 new tokens. The key is split into its
 //    norm r and direction u (Section 3.1); u goes to the list with the nearest
 //    centroid, and each M-dimensional slice of the residual u - c_a to its
 //    nearest codeword. Squared Euclidean distances in fp32; ties go to the
@@ -20,7 +20,6 @@
 namespace pqhsa {
 
 constexpr int kEncThreads = 256;
-constexpr int kEncWaves = kEncThreads / kWave;
 
 // (d, i) < (od, oi) lexicographically: the smaller distance, then the smaller index
 __device__ __forceinline__ void argmin_fold(float& d, int& i, float od, int oi) {
@@ -30,110 +29,167 @@ __device__ __forceinline__ void argmin_fold(float& d, int& i, float od, int oi) 
     }
 }
 
-__device__ __forceinline__ void wave_argmin(float& d, int& i) {
-#pragma unroll
-    for (int off = kWave / 2; off > 0; off >>= 1) {
-        const float od = __shfl_xor(d, off);
-        const int oi = __shfl_xor(i, off);
-        argmin_fold(d, i, od, oi);
-    }
-}
+// A workgroup encodes kEncTok tokens: their directions sit in LDS, the
+// centroids stream through LDS kEncCen rows at a time, and each thread keeps
+// the distances of 4 tokens to 4 centers (lane tx of a 16-lane group takes
+// centers tx, tx + 16, ...; the odd row stride puts those rows on distinct
+// banks). Every distance sums its dimensions in order, one fma per
+// dimension. The per-token argmin folds over the 16 lanes by (distance, id).
+constexpr int kEncTok = 64;
+constexpr int kEncCen = 64;
+constexpr int kEncLd = kHeadDim + 1;
 
 template <typename T, typename PQ>
 __global__ __launch_bounds__(kEncThreads) void encode_kernel(
     Dims D, BatchInts lo, BatchInts hi, const T* __restrict__ kcache, int64_t sb, int64_t sh,
     int64_t sn, const float* __restrict__ centroids, const float* __restrict__ codebooks,
     int32_t* __restrict__ ids_tm, uint8_t* __restrict__ codes_tm, float* __restrict__ norms_tm,
-    float* __restrict__ dist_c, float* __restrict__ dist_f) {
-    __shared__ float su[kHeadDim];           // u, then the residual u - c_a
-    __shared__ float sdist[kMaxLists];       // coarse distances, then [M][K] fine ones
-    __shared__ float wsum[kEncWaves];
-    __shared__ int sa;
-    static_assert(PQ::M * PQ::K <= kMaxLists, "fine distances fit the coarse buffer");
+    float* __restrict__ dist_c, float* __restrict__ dist_f, int keep_lists) {
+    constexpr int kSpLd = PQ::DSUB + 1;
+    __shared__ float su[kEncTok * kEncLd];   // directions, then residuals
+    __shared__ float sc[kEncCen * kEncLd];   // a chunk of centroids
+    __shared__ float sp[PQ::K * kSpLd];      // one subspace's codewords
+    __shared__ float sr[kEncTok];
+    __shared__ int sa[kEncTok];
+    static_assert(kEncThreads == 256 && kEncTok == 64 && kEncCen == 64, "4 x 4 per thread");
     const int b = blockIdx.z;
     const int g = blockIdx.y;
-    const int t = lo.v[b] + static_cast<int>(blockIdx.x);
-    if (t >= hi.v[b]) return;
+    const int t_base = lo.v[b] + static_cast<int>(blockIdx.x) * kEncTok;
+    if (t_base >= hi.v[b]) return;
+    const int nt = min(kEncTok, hi.v[b] - t_base);
     const int bg = b * D.Hkv + g;
     const int tid = threadIdx.x;
-    const int wave = tid / kWave;
-    const int lane = lane_id();
+    const int ty = tid / 16, tx = tid % 16;
+    const T* krow = kcache + b * sb + g * sh;
 
-    // r = ||k||, u = k / r (u = 0 for a zero key)
-    float kx = 0.0f;
-    if (tid < kHeadDim) kx = load1<T>(kcache + b * sb + g * sh + t * sn + tid);
-    float ss = kx * kx;
-#pragma unroll
-    for (int off = kWave / 2; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
-    if (lane == 0) wsum[wave] = ss;
+    for (int i = tid; i < kEncTok * kHeadDim; i += kEncThreads) {
+        const int tk = i / kHeadDim, x = i % kHeadDim;
+        su[tk * kEncLd + x] = tk < nt ? load1<T>(krow + (t_base + tk) * sn + x) : 0.0f;
+    }
     __syncthreads();
-    float tot = 0.0f;
-#pragma unroll
-    for (int w = 0; w < kEncWaves; ++w) tot += wsum[w];
-    const float r = sqrtf(tot);
-    if (tid < kHeadDim) su[tid] = r > 0.0f ? kx / r : 0.0f;
+    {   // r = ||k||: 4 lanes per token, 32 dimensions each
+        const int tk = tid / 4, part = tid % 4;
+        float ss = 0.0f;
+        for (int x = part * 32; x < part * 32 + 32; ++x) ss = fmaf(su[tk * kEncLd + x], su[tk * kEncLd + x], ss);
+        ss += __shfl_xor(ss, 1);
+        ss += __shfl_xor(ss, 2);
+        if (part == 0) sr[tk] = sqrtf(ss);
+    }
     __syncthreads();
+    for (int i = tid; i < kEncTok * kHeadDim; i += kEncThreads) {
+        const int tk = i / kHeadDim, x = i % kHeadDim;
+        const float r = sr[tk];
+        su[tk * kEncLd + x] = r > 0.0f ? su[tk * kEncLd + x] / r : 0.0f;
+    }
 
-    // nearest centroid
+    // nearest centroid (or, with keep_lists, the list already in ids_tm)
     const float* cen = centroids + static_cast<int64_t>(bg) * D.n_list * kHeadDim;
-    for (int j = tid; j < D.n_list; j += kEncThreads) {
-        const float4* c4 = reinterpret_cast<const float4*>(cen + static_cast<int64_t>(j) * kHeadDim);
-        float acc = 0.0f;
-#pragma unroll 8
-        for (int x = 0; x < kHeadDim / 4; ++x) {
-            const float4 c = c4[x];
-            const float d0 = su[4 * x] - c.x, d1 = su[4 * x + 1] - c.y;
-            const float d2 = su[4 * x + 2] - c.z, d3 = su[4 * x + 3] - c.w;
-            acc = fmaf(d0, d0, acc);
-            acc = fmaf(d1, d1, acc);
-            acc = fmaf(d2, d2, acc);
-            acc = fmaf(d3, d3, acc);
+    const int64_t row0 = static_cast<int64_t>(bg) * D.rcap + t_base;
+    if (keep_lists) {
+        if (tid < kEncTok) sa[tid] = tid < nt ? ids_tm[row0 + tid] : 0;
+    } else {
+    float bd[4];
+    int bi[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        bd[i] = __builtin_huge_valf();
+        bi[i] = 0;   // a valid id even if every distance is NaN
+    }
+    for (int c0 = 0; c0 < D.n_list; c0 += kEncCen) {
+        const int nc = min(kEncCen, D.n_list - c0);
+        __syncthreads();
+        for (int i = tid; i < kEncCen * kHeadDim; i += kEncThreads) {
+            const int cc = i / kHeadDim, x = i % kHeadDim;
+            sc[cc * kEncLd + x] = cc < nc ? cen[static_cast<int64_t>(c0 + cc) * kHeadDim + x] : 0.0f;
         }
-        sdist[j] = acc;
+        __syncthreads();
+        float acc[4][4] = {};
+        for (int x = 0; x < kHeadDim; ++x) {
+            float uu[4], cv[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) uu[i] = su[(ty * 4 + i) * kEncLd + x];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) cv[j] = sc[(tx + 16 * j) * kEncLd + x];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const float dd = uu[i] - cv[j];
+                    acc[i][j] = fmaf(dd, dd, acc[i][j]);
+                }
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if (tx + 16 * j < nc)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) argmin_fold(bd[i], bi[i], acc[i][j], c0 + tx + 16 * j);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int off = 8; off > 0; off >>= 1) {
+            const float od = __shfl_xor(bd[i], off);
+            const int oi = __shfl_xor(bi[i], off);
+            argmin_fold(bd[i], bi[i], od, oi);
+        }
+    if (tx == 0)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            sa[ty * 4 + i] = bi[i];
+            if (dist_c && ty * 4 + i < nt) dist_c[row0 + ty * 4 + i] = bd[i];
+        }
     }
     __syncthreads();
-    if (wave == 0) {
-        float bd = __builtin_huge_valf();
-        int bi = 0;   // a valid id even if every distance is NaN
-        for (int j = lane; j < D.n_list; j += kWave) argmin_fold(bd, bi, sdist[j], j);
-        wave_argmin(bd, bi);
-        if (lane == 0) {
-            sa = bi;
-            if (dist_c) dist_c[static_cast<int64_t>(bg) * D.rcap + t] = bd;
-        }
+    for (int i = tid; i < kEncTok * kHeadDim; i += kEncThreads) {
+        const int tk = i / kHeadDim, x = i % kHeadDim;
+        su[tk * kEncLd + x] -= cen[static_cast<int64_t>(sa[tk]) * kHeadDim + x];
     }
-    __syncthreads();
-    const int a = sa;
-    if (tid < kHeadDim) su[tid] -= cen[static_cast<int64_t>(a) * kHeadDim + tid];
-    __syncthreads();
 
     // nearest codeword of every subspace slice of the residual
     const float* cb = codebooks + static_cast<int64_t>(bg) * PQ::M * PQ::K * PQ::DSUB;
-    for (int p = tid; p < PQ::M * PQ::K; p += kEncThreads) {
-        const int m = p / PQ::K;
-        float acc = 0.0f;
+    for (int m = 0; m < PQ::M; ++m) {
+        __syncthreads();
+        for (int i = tid; i < PQ::K * PQ::DSUB; i += kEncThreads)
+            sp[(i / PQ::DSUB) * kSpLd + i % PQ::DSUB] = cb[static_cast<int64_t>(m) * PQ::K * PQ::DSUB + i];
+        __syncthreads();
+        float fb[4];
+        int fi[4];
 #pragma unroll
-        for (int x = 0; x < PQ::DSUB; ++x) {
-            const float dx = su[m * PQ::DSUB + x] - cb[static_cast<int64_t>(p) * PQ::DSUB + x];
-            acc = fmaf(dx, dx, acc);
+        for (int i = 0; i < 4; ++i) {
+            fb[i] = __builtin_huge_valf();
+            fi[i] = 0;
         }
-        sdist[p] = acc;
-    }
-    __syncthreads();
-    const int64_t tok = static_cast<int64_t>(bg) * D.rcap + t;
-    for (int m = wave; m < PQ::M; m += kEncWaves) {
-        float bd = __builtin_huge_valf();
-        int bi = 0;   // a valid id even if every distance is NaN
-        for (int z = lane; z < PQ::K; z += kWave) argmin_fold(bd, bi, sdist[m * PQ::K + z], z);
-        wave_argmin(bd, bi);
-        if (lane == 0) {
-            codes_tm[tok * PQ::M + m] = static_cast<uint8_t>(bi);
-            if (dist_f) dist_f[tok * PQ::M + m] = bd;
+        for (int z = tx; z < PQ::K; z += 16) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                float acc = 0.0f;
+#pragma unroll
+                for (int x = 0; x < PQ::DSUB; ++x) {
+                    const float dd = su[(ty * 4 + i) * kEncLd + m * PQ::DSUB + x] - sp[z * kSpLd + x];
+                    acc = fmaf(dd, dd, acc);
+                }
+                argmin_fold(fb[i], fi[i], acc, z);
+            }
         }
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int off = 8; off > 0; off >>= 1) {
+                const float od = __shfl_xor(fb[i], off);
+                const int oi = __shfl_xor(fi[i], off);
+                argmin_fold(fb[i], fi[i], od, oi);
+            }
+        if (tx == 0)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                if (ty * 4 + i < nt) {
+                    codes_tm[(row0 + ty * 4 + i) * PQ::M + m] = static_cast<uint8_t>(fi[i]);
+                    if (dist_f) dist_f[(row0 + ty * 4 + i) * PQ::M + m] = fb[i];
+                }
     }
-    if (tid == 0) {
-        ids_tm[tok] = a;
-        norms_tm[tok] = r;
+    if (tid < nt) {
+        ids_tm[row0 + tid] = sa[tid];
+        norms_tm[row0 + tid] = sr[tid];
     }
 }
 
@@ -286,28 +342,28 @@ hipError_t launch_update_lists(const Dims& D, const BatchInts& lo, const BatchIn
 hipError_t launch_encode(const Dims& D, const BatchInts& lo, const BatchInts& hi, int max_new,
                          const KV& kv, const float* centroids, const float* codebooks,
                          int32_t* ids_tm, uint8_t* codes_tm, float* norms_tm, float* dist_c,
-                         float* dist_f, hipStream_t s) {
+                         float* dist_f, int keep_lists, hipStream_t s) {
     if (max_new <= 0) return hipSuccess;
-    const dim3 grid(max_new, D.Hkv, D.B);
+    const dim3 grid((max_new + kEncTok - 1) / kEncTok, D.Hkv, D.B);
     const bool p4 = D.pq_bits == 4;
     if (kv.bf16) {
         if (p4)
             hipLaunchKernelGGL((encode_kernel<bf16_t, Pq4>), grid, dim3(kEncThreads), 0, s, D, lo, hi,
                                static_cast<const bf16_t*>(kv.k), kv.sb, kv.sh, kv.sn, centroids,
-                               codebooks, ids_tm, codes_tm, norms_tm, dist_c, dist_f);
+                               codebooks, ids_tm, codes_tm, norms_tm, dist_c, dist_f, keep_lists);
         else
             hipLaunchKernelGGL((encode_kernel<bf16_t, Pq8>), grid, dim3(kEncThreads), 0, s, D, lo, hi,
                                static_cast<const bf16_t*>(kv.k), kv.sb, kv.sh, kv.sn, centroids,
-                               codebooks, ids_tm, codes_tm, norms_tm, dist_c, dist_f);
+                               codebooks, ids_tm, codes_tm, norms_tm, dist_c, dist_f, keep_lists);
     } else {
         if (p4)
             hipLaunchKernelGGL((encode_kernel<float, Pq4>), grid, dim3(kEncThreads), 0, s, D, lo, hi,
                                static_cast<const float*>(kv.k), kv.sb, kv.sh, kv.sn, centroids,
-                               codebooks, ids_tm, codes_tm, norms_tm, dist_c, dist_f);
+                               codebooks, ids_tm, codes_tm, norms_tm, dist_c, dist_f, keep_lists);
         else
             hipLaunchKernelGGL((encode_kernel<float, Pq8>), grid, dim3(kEncThreads), 0, s, D, lo, hi,
                                static_cast<const float*>(kv.k), kv.sb, kv.sh, kv.sn, centroids,
-                               codebooks, ids_tm, codes_tm, norms_tm, dist_c, dist_f);
+                               codebooks, ids_tm, codes_tm, norms_tm, dist_c, dist_f, keep_lists);
     }
     return hipGetLastError();
 }
@@ -318,7 +374,7 @@ static hipError_t launch_update_t(const Dims& D, const BatchInts& lo, const Batc
                                   const float* codebooks, const int32_t* old_loff, int32_t* ids_tm,
                                   uint8_t* codes_tm, float* norms_tm, float* means, hipStream_t s) {
     hipError_t e = launch_encode(D, lo, hi, max_new, kv, centroids, codebooks, ids_tm, codes_tm,
-                                 norms_tm, nullptr, nullptr, s);
+                                 norms_tm, nullptr, nullptr, 0, s);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((means_update_kernel<T>), dim3(D.n_list, D.Hkv, D.B), dim3(kHeadDim), 0, s,
                        D, lo, hi, static_cast<const T*>(kv.v), kv.sb, kv.sh, kv.sn, old_loff,
