@@ -2,18 +2,20 @@
 // are encoded into the existing lists, without re-clustering, and the list
 // means are refreshed over the grown lists.
 //
-//  * encode_kernel: one workgroup per 64 new tokens. The key is split into its
-//    norm r and direction u (Section 3.1); u goes to the list with the nearest
-//    centroid, and each M-dimensional slice of the residual u - c_a to its
-//    nearest codeword. Squared Euclidean distances in fp32; ties go to the
-//    smaller list id or codeword index. Writes the token-major list id, codes
-//    (one code per byte) and norm.
+//  * encode_one_kernel (one workgroup per new token, for updates) and
+//    encode_kernel (64 tokens per workgroup, for the build's passes over
+//    all of R): the key is split into its norm r and direction u
+//    (Section 3.1); u goes to the list with the nearest centroid, and each
+//    slice of the residual u - c_a to its nearest codeword. Squared
+//    Euclidean distances in fp32; ties go to the smaller list id or
+//    codeword index. Writes the token-major list id, codes (one code per
+//    byte) and norm.
 //  * means_update_kernel: one workgroup per (list, kv head, sequence); folds
 //    the new members' values into the list mean, in float64:
 //    v_bar' = (n_old v_bar + sum of new v) / (n_old + n_new).
 //
-// The list-major layout is then rebuilt from the token-major arrays by the
-// same counting sort and gather as a fresh prepare.
+// The list-major layout is then merged on the device (update_lists_kernel,
+// shift_positions_kernel below) and codes and norms gathered into it.
 #include "device_common.h"
 #include "pqhsa_internal.h"
 
@@ -190,6 +192,110 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(
     if (tid < nt) {
         ids_tm[row0 + tid] = sa[tid];
         norms_tm[row0 + tid] = sr[tid];
+    }
+}
+
+// argmin over the 64 lanes of a wave by (distance, id)
+__device__ __forceinline__ void wave_argmin64(float& d, int& i) {
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) {
+        const float od = __shfl_xor(d, off);
+        const int oi = __shfl_xor(i, off);
+        argmin_fold(d, i, od, oi);
+    }
+}
+
+// One workgroup per token: for updates of a few hundred tokens, where
+// 64-token tiles would leave most of the chip idle. The same choices as
+// encode_kernel up to fp32 rounding order.
+template <typename T, typename PQ>
+__global__ __launch_bounds__(kEncThreads) void encode_one_kernel(
+    Dims D, BatchInts lo, BatchInts hi, const T* __restrict__ kcache, int64_t sb, int64_t sh,
+    int64_t sn, const float* __restrict__ centroids, const float* __restrict__ codebooks,
+    int32_t* __restrict__ ids_tm, uint8_t* __restrict__ codes_tm, float* __restrict__ norms_tm) {
+    __shared__ float su[kHeadDim];           // u, then the residual u - c_a
+    __shared__ float sdist[kMaxLists];       // coarse distances, then [M][K] fine ones
+    __shared__ float wsum[kEncThreads / kWave];
+    __shared__ int sa;
+    static_assert(PQ::M * PQ::K <= kMaxLists, "fine distances fit the coarse buffer");
+    const int b = blockIdx.z;
+    const int g = blockIdx.y;
+    const int t = lo.v[b] + static_cast<int>(blockIdx.x);
+    if (t >= hi.v[b]) return;
+    const int bg = b * D.Hkv + g;
+    const int tid = threadIdx.x;
+    const int wave = tid / kWave;
+    const int lane = lane_id();
+
+    // r = ||k||, u = k / r (u = 0 for a zero key)
+    float kx = 0.0f;
+    if (tid < kHeadDim) kx = load1<T>(kcache + b * sb + g * sh + t * sn + tid);
+    float ss = kx * kx;
+#pragma unroll
+    for (int off = kWave / 2; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
+    if (lane == 0) wsum[wave] = ss;
+    __syncthreads();
+    float tot = 0.0f;
+#pragma unroll
+    for (int w = 0; w < kEncThreads / kWave; ++w) tot += wsum[w];
+    const float r = sqrtf(tot);
+    if (tid < kHeadDim) su[tid] = r > 0.0f ? kx / r : 0.0f;
+    __syncthreads();
+
+    // nearest centroid
+    const float* cen = centroids + static_cast<int64_t>(bg) * D.n_list * kHeadDim;
+    for (int j = tid; j < D.n_list; j += kEncThreads) {
+        const float4* c4 = reinterpret_cast<const float4*>(cen + static_cast<int64_t>(j) * kHeadDim);
+        float acc = 0.0f;
+#pragma unroll 8
+        for (int x = 0; x < kHeadDim / 4; ++x) {
+            const float4 c = c4[x];
+            const float d0 = su[4 * x] - c.x, d1 = su[4 * x + 1] - c.y;
+            const float d2 = su[4 * x + 2] - c.z, d3 = su[4 * x + 3] - c.w;
+            acc = fmaf(d0, d0, acc);
+            acc = fmaf(d1, d1, acc);
+            acc = fmaf(d2, d2, acc);
+            acc = fmaf(d3, d3, acc);
+        }
+        sdist[j] = acc;
+    }
+    __syncthreads();
+    if (wave == 0) {
+        float bd = __builtin_huge_valf();
+        int bi = 0;   // a valid id even if every distance is NaN
+        for (int j = lane; j < D.n_list; j += kWave) argmin_fold(bd, bi, sdist[j], j);
+        wave_argmin64(bd, bi);
+        if (lane == 0) sa = bi;
+    }
+    __syncthreads();
+    const int a = sa;
+    if (tid < kHeadDim) su[tid] -= cen[static_cast<int64_t>(a) * kHeadDim + tid];
+    __syncthreads();
+
+    // nearest codeword of every subspace slice of the residual
+    const float* cb = codebooks + static_cast<int64_t>(bg) * PQ::M * PQ::K * PQ::DSUB;
+    for (int p = tid; p < PQ::M * PQ::K; p += kEncThreads) {
+        const int m = p / PQ::K;
+        float acc = 0.0f;
+#pragma unroll
+        for (int x = 0; x < PQ::DSUB; ++x) {
+            const float dx = su[m * PQ::DSUB + x] - cb[static_cast<int64_t>(p) * PQ::DSUB + x];
+            acc = fmaf(dx, dx, acc);
+        }
+        sdist[p] = acc;
+    }
+    __syncthreads();
+    const int64_t tok = static_cast<int64_t>(bg) * D.rcap + t;
+    for (int m = wave; m < PQ::M; m += kEncThreads / kWave) {
+        float bd = __builtin_huge_valf();
+        int bi = 0;   // a valid id even if every distance is NaN
+        for (int z = lane; z < PQ::K; z += kWave) argmin_fold(bd, bi, sdist[m * PQ::K + z], z);
+        wave_argmin64(bd, bi);
+        if (lane == 0) codes_tm[tok * PQ::M + m] = static_cast<uint8_t>(bi);
+    }
+    if (tid == 0) {
+        ids_tm[tok] = a;
+        norms_tm[tok] = r;
     }
 }
 
@@ -373,8 +479,16 @@ static hipError_t launch_update_t(const Dims& D, const BatchInts& lo, const Batc
                                   int max_new, const KV& kv, const float* centroids,
                                   const float* codebooks, const int32_t* old_loff, int32_t* ids_tm,
                                   uint8_t* codes_tm, float* norms_tm, float* means, hipStream_t s) {
-    hipError_t e = launch_encode(D, lo, hi, max_new, kv, centroids, codebooks, ids_tm, codes_tm,
-                                 norms_tm, nullptr, nullptr, 0, s);
+    const dim3 grid(max_new, D.Hkv, D.B);
+    if (D.pq_bits == 4)
+        hipLaunchKernelGGL((encode_one_kernel<T, Pq4>), grid, dim3(kEncThreads), 0, s, D, lo, hi,
+                           static_cast<const T*>(kv.k), kv.sb, kv.sh, kv.sn, centroids, codebooks,
+                           ids_tm, codes_tm, norms_tm);
+    else
+        hipLaunchKernelGGL((encode_one_kernel<T, Pq8>), grid, dim3(kEncThreads), 0, s, D, lo, hi,
+                           static_cast<const T*>(kv.k), kv.sb, kv.sh, kv.sn, centroids, codebooks,
+                           ids_tm, codes_tm, norms_tm);
+    hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL((means_update_kernel<T>), dim3(D.n_list, D.Hkv, D.B), dim3(kHeadDim), 0, s,
                        D, lo, hi, static_cast<const T*>(kv.v), kv.sb, kv.sh, kv.sn, old_loff,
