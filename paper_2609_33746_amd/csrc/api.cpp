@@ -488,16 +488,16 @@ pqhsa_status pqhsa_index_update(pqhsa_ctx* c, const int32_t* new_seq_lens, const
         hi.v[b] = lens[b] - D.n_local;
         max_new = std::max(max_new, hi.v[b] - lo.v[b]);
     }
-    // encode and refresh the means (both read the old list offsets), merge
-    // the new tokens into the other half of the list-major arrays, swap the
-    // halves, then gather codes and norms into the new order
+    // encode, merge the new tokens into the other half of the list-major
+    // arrays and refresh the means, swap the halves, then gather codes and
+    // norms into the new order
     c->prepared = false;
-    hipError_t e = launch_update(D, lo, hi, max_new, kv, c->centroids, c->codebooks, c->loff,
-                                 c->ids_tm, c->codes_tm, c->norms_tm, c->means, stream);
+    hipError_t e = launch_encode_update(D, lo, hi, max_new, kv, c->centroids, c->codebooks,
+                                        c->ids_tm, c->codes_tm, c->norms_tm, stream);
     if (e == hipSuccess)
-        e = launch_update_lists(D, lo, hi, c->ids_tm, c->loff, c->perm, c->pos_word, c->loff_alt,
-                                c->shift, c->perm_alt, c->pos_alt, c->tok_list, c->n_r_dev,
-                                c->n_seq_dev, stream);
+        e = launch_update_lists(D, lo, hi, kv, c->ids_tm, c->loff, c->perm, c->pos_word,
+                                c->loff_alt, c->shift, c->perm_alt, c->pos_alt, c->tok_list,
+                                c->n_r_dev, c->n_seq_dev, c->means, stream);
     if (e != hipSuccess) return hip_fail(c, e, "launching the index update");
     std::swap(c->perm, c->perm_alt);
     std::swap(c->pos_word, c->pos_alt);

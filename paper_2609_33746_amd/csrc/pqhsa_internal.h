@@ -182,14 +182,6 @@ hipError_t launch_dense(const Dims& D, const KV& kv, const BatchInts& lens, floa
 // the token-weighted mean of the list means per (b, g): the global value
 // mean over R_b of variant C
 hipError_t launch_glob_mean(const Dims& D, const Index& ix, float* glob, hipStream_t s);
-// incremental update: encode tokens [lo[b], hi[b]) of every (b, kv head) into
-// the token-major ids / codes / norms, then fold their values into the list
-// means (old_loff: the list offsets before the update). max_new = max over b
-// of hi - lo.
-hipError_t launch_update(const Dims& D, const BatchInts& lo, const BatchInts& hi, int max_new,
-                         const KV& kv, const float* centroids, const float* codebooks,
-                         const int32_t* old_loff, int32_t* ids_tm, uint8_t* codes_tm,
-                         float* norms_tm, float* means, hipStream_t s);
 // encode tokens [lo[b], hi[b]) of every (b, kv head) against the given model
 // (token-major ids / codes / norms); dist_c [B, Hkv, rcap] and dist_f
 // [B, Hkv, rcap, M], when not null, receive the squared distances to the
@@ -199,6 +191,11 @@ hipError_t launch_encode(const Dims& D, const BatchInts& lo, const BatchInts& hi
                          const KV& kv, const float* centroids, const float* codebooks,
                          int32_t* ids_tm, uint8_t* codes_tm, float* norms_tm, float* dist_c,
                          float* dist_f, int keep_lists, hipStream_t s);
+// the same encoding with one workgroup per token (for a few hundred tokens)
+hipError_t launch_encode_update(const Dims& D, const BatchInts& lo, const BatchInts& hi,
+                                int max_new, const KV& kv, const float* centroids,
+                                const float* codebooks, int32_t* ids_tm, uint8_t* codes_tm,
+                                float* norms_tm, hipStream_t s);
 // index build steps (k-means over the tokens [lo[b], hi[b]) of each (b, kv head))
 struct BuildBufs {
     int32_t* order;      // [problems, rcap] tokens grouped by center, in id order within a center
@@ -221,16 +218,16 @@ hipError_t launch_reseed(const Dims& D, const BatchInts& lo, const BatchInts& hi
                          const KV& kv, const int32_t* ids_tm, const float* norms_tm,
                          const float* centroids, const BuildBufs& bb, float* out, hipStream_t s);
 
-// the list-major rebuild after launch_update (lo, hi as there): new list
-// offsets, per-list shifts [B, Hkv, n_list] and the new perm / pos_word in the
-// *_new buffers (which must not alias the old ones); tok_list, n_r and n_seq
-// updated in place
+// the list-major rebuild after an update's encode pass (lo, hi as there):
+// new list offsets, per-list shifts [B, Hkv, n_list] and the new perm /
+// pos_word in the *_new buffers (which must not alias the old ones); tok_list,
+// n_r, n_seq and the list means (from the values in kv) updated in place
 hipError_t launch_update_lists(const Dims& D, const BatchInts& lo, const BatchInts& hi,
-                               const int32_t* ids_tm, const int32_t* old_loff,
+                               const KV& kv, const int32_t* ids_tm, const int32_t* old_loff,
                                const int32_t* perm_old, const uint32_t* pos_old, int32_t* new_loff,
                                int32_t* shift, int32_t* perm_new, uint32_t* pos_new,
                                uint16_t* tok_list, int32_t* n_r_dev, int32_t* n_seq_dev,
-                               hipStream_t s);
+                               float* means, hipStream_t s);
 hipError_t launch_prepare_gather(const Dims& D, const uint8_t* codes_in, const float* norms_in,
                                  const Index& ix, uint8_t* codes_out, float* norms_out,
                                  hipStream_t s);

@@ -70,6 +70,7 @@ __global__ __launch_bounds__(kHeadDim * kGlobGroups) void glob_mean_kernel(Dims 
     const int32_t* loff = ix.loff + static_cast<int64_t>(bg) * (D.n_list + 1);
     const float* means = ix.means + static_cast<int64_t>(bg) * D.n_list * kHeadDim + t;
     double acc = 0.0;
+#pragma unroll 8
     for (int j = gi; j < D.n_list; j += kGlobGroups)
         acc += static_cast<double>(loff[j + 1] - loff[j]) * static_cast<double>(means[j * kHeadDim]);
     part[gi][t] = acc;

@@ -2,17 +2,17 @@
 // are encoded into the existing lists, without re-clustering, and the list
 // means are refreshed over the grown lists.
 //
-//  * encode_one_kernel (one workgroup per new token, for updates) and
-//    encode_kernel (64 tokens per workgroup, for the build's passes over
-//    all of R): the key is split into its norm r and direction u
-//    (Section 3.1); u goes to the list with the nearest centroid, and each
-//    slice of the residual u - c_a to its nearest codeword. Squared
-//    Euclidean distances in fp32; ties go to the smaller list id or
-//    codeword index. Writes the token-major list id, codes (one code per
-//    byte) and norm.
-//  * means_update_kernel: one workgroup per (list, kv head, sequence); folds
-//    the new members' values into the list mean, in float64:
-//    v_bar' = (n_old v_bar + sum of new v) / (n_old + n_new).
+//  * encode_one_kernel (one token per workgroup: updates of a few hundred
+//    tokens) and encode_kernel (16 or 64 tokens per workgroup: the build's
+//    passes over all of R): the key is split into
+//    its norm r and direction u (Section 3.1); u goes to the list with the
+//    nearest centroid, and each slice of the residual u - c_a to its nearest
+//    codeword. Squared Euclidean distances in fp32; ties go to the smaller
+//    list id or codeword index. Writes the token-major list id, codes (one
+//    code per byte) and norm.
+//  * means_update_kernel, after the merge below: one workgroup per (list,
+//    kv head, sequence) folds the new members' values into the list mean,
+//    in float64: v_bar' = (n_old v_bar + sum of new v) / (n_old + n_new).
 //
 // The list-major layout is then merged on the device (update_lists_kernel,
 // shift_positions_kernel below) and codes and norms gathered into it.
@@ -31,29 +31,31 @@ __device__ __forceinline__ void argmin_fold(float& d, int& i, float od, int oi) 
     }
 }
 
-// A workgroup encodes kEncTok tokens: their directions sit in LDS, the
+// A workgroup encodes 16 TPT tokens: their directions sit in LDS, the
 // centroids stream through LDS kEncCen rows at a time, and each thread keeps
-// the distances of 4 tokens to 4 centers (lane tx of a 16-lane group takes
+// the distances of TPT tokens to 4 centers (lane tx of a 16-lane group takes
 // centers tx, tx + 16, ...; the odd row stride puts those rows on distinct
 // banks). Every distance sums its dimensions in order, one fma per
 // dimension. The per-token argmin folds over the 16 lanes by (distance, id).
-constexpr int kEncTok = 64;
 constexpr int kEncCen = 64;
 constexpr int kEncLd = kHeadDim + 1;
 
-template <typename T, typename PQ>
+// TPT tokens per thread row: 16 TPT tokens per workgroup (64 for the build's
+// passes over all of R, 16 for updates of a few hundred tokens)
+template <typename T, typename PQ, int TPT>
 __global__ __launch_bounds__(kEncThreads) void encode_kernel(
     Dims D, BatchInts lo, BatchInts hi, const T* __restrict__ kcache, int64_t sb, int64_t sh,
     int64_t sn, const float* __restrict__ centroids, const float* __restrict__ codebooks,
     int32_t* __restrict__ ids_tm, uint8_t* __restrict__ codes_tm, float* __restrict__ norms_tm,
     float* __restrict__ dist_c, float* __restrict__ dist_f, int keep_lists) {
     constexpr int kSpLd = PQ::DSUB + 1;
+    constexpr int kEncTok = 16 * TPT;
     __shared__ float su[kEncTok * kEncLd];   // directions, then residuals
     __shared__ float sc[kEncCen * kEncLd];   // a chunk of centroids
     __shared__ float sp[PQ::K * kSpLd];      // one subspace's codewords
     __shared__ float sr[kEncTok];
     __shared__ int sa[kEncTok];
-    static_assert(kEncThreads == 256 && kEncTok == 64 && kEncCen == 64, "4 x 4 per thread");
+    static_assert(kEncThreads == 256 && kEncCen == 64 && 4 * kEncTok <= kEncThreads, "TPT x 4 per thread");
     const int b = blockIdx.z;
     const int g = blockIdx.y;
     const int t_base = lo.v[b] + static_cast<int>(blockIdx.x) * kEncTok;
@@ -69,7 +71,7 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(
         su[tk * kEncLd + x] = tk < nt ? load1<T>(krow + (t_base + tk) * sn + x) : 0.0f;
     }
     __syncthreads();
-    {   // r = ||k||: 4 lanes per token, 32 dimensions each
+    if (tid < 4 * kEncTok) {   // r = ||k||: 4 lanes per token, 32 dimensions each
         const int tk = tid / 4, part = tid % 4;
         float ss = 0.0f;
         for (int x = part * 32; x < part * 32 + 32; ++x) ss = fmaf(su[tk * kEncLd + x], su[tk * kEncLd + x], ss);
@@ -90,10 +92,10 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(
     if (keep_lists) {
         if (tid < kEncTok) sa[tid] = tid < nt ? ids_tm[row0 + tid] : 0;
     } else {
-    float bd[4];
-    int bi[4];
+    float bd[TPT];
+    int bi[TPT];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < TPT; ++i) {
         bd[i] = __builtin_huge_valf();
         bi[i] = 0;   // a valid id even if every distance is NaN
     }
@@ -105,15 +107,15 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(
             sc[cc * kEncLd + x] = cc < nc ? cen[static_cast<int64_t>(c0 + cc) * kHeadDim + x] : 0.0f;
         }
         __syncthreads();
-        float acc[4][4] = {};
+        float acc[TPT][4] = {};
         for (int x = 0; x < kHeadDim; ++x) {
-            float uu[4], cv[4];
+            float uu[TPT], cv[4];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) uu[i] = su[(ty * 4 + i) * kEncLd + x];
+            for (int i = 0; i < TPT; ++i) uu[i] = su[(ty * TPT + i) * kEncLd + x];
 #pragma unroll
             for (int j = 0; j < 4; ++j) cv[j] = sc[(tx + 16 * j) * kEncLd + x];
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < TPT; ++i)
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
                     const float dd = uu[i] - cv[j];
@@ -124,10 +126,10 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(
         for (int j = 0; j < 4; ++j)
             if (tx + 16 * j < nc)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) argmin_fold(bd[i], bi[i], acc[i][j], c0 + tx + 16 * j);
+                for (int i = 0; i < TPT; ++i) argmin_fold(bd[i], bi[i], acc[i][j], c0 + tx + 16 * j);
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < TPT; ++i)
 #pragma unroll
         for (int off = 8; off > 0; off >>= 1) {
             const float od = __shfl_xor(bd[i], off);
@@ -136,9 +138,9 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(
         }
     if (tx == 0)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            sa[ty * 4 + i] = bi[i];
-            if (dist_c && ty * 4 + i < nt) dist_c[row0 + ty * 4 + i] = bd[i];
+        for (int i = 0; i < TPT; ++i) {
+            sa[ty * TPT + i] = bi[i];
+            if (dist_c && ty * TPT + i < nt) dist_c[row0 + ty * TPT + i] = bd[i];
         }
     }
     __syncthreads();
@@ -154,27 +156,27 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(
         for (int i = tid; i < PQ::K * PQ::DSUB; i += kEncThreads)
             sp[(i / PQ::DSUB) * kSpLd + i % PQ::DSUB] = cb[static_cast<int64_t>(m) * PQ::K * PQ::DSUB + i];
         __syncthreads();
-        float fb[4];
-        int fi[4];
+        float fb[TPT];
+        int fi[TPT];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
+        for (int i = 0; i < TPT; ++i) {
             fb[i] = __builtin_huge_valf();
             fi[i] = 0;
         }
         for (int z = tx; z < PQ::K; z += 16) {
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
+            for (int i = 0; i < TPT; ++i) {
                 float acc = 0.0f;
 #pragma unroll
                 for (int x = 0; x < PQ::DSUB; ++x) {
-                    const float dd = su[(ty * 4 + i) * kEncLd + m * PQ::DSUB + x] - sp[z * kSpLd + x];
+                    const float dd = su[(ty * TPT + i) * kEncLd + m * PQ::DSUB + x] - sp[z * kSpLd + x];
                     acc = fmaf(dd, dd, acc);
                 }
                 argmin_fold(fb[i], fi[i], acc, z);
             }
         }
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < TPT; ++i)
 #pragma unroll
             for (int off = 8; off > 0; off >>= 1) {
                 const float od = __shfl_xor(fb[i], off);
@@ -183,10 +185,10 @@ __global__ __launch_bounds__(kEncThreads) void encode_kernel(
             }
         if (tx == 0)
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-                if (ty * 4 + i < nt) {
-                    codes_tm[(row0 + ty * 4 + i) * PQ::M + m] = static_cast<uint8_t>(fi[i]);
-                    if (dist_f) dist_f[(row0 + ty * 4 + i) * PQ::M + m] = fb[i];
+            for (int i = 0; i < TPT; ++i)
+                if (ty * TPT + i < nt) {
+                    codes_tm[(row0 + ty * TPT + i) * PQ::M + m] = static_cast<uint8_t>(fi[i]);
+                    if (dist_f) dist_f[(row0 + ty * TPT + i) * PQ::M + m] = fb[i];
                 }
     }
     if (tid < nt) {
@@ -299,47 +301,32 @@ __global__ __launch_bounds__(kEncThreads) void encode_one_kernel(
     }
 }
 
-// One workgroup per (list j, kv head g, sequence b), one thread per dimension.
-// The new tokens' list ids are staged through LDS a chunk at a time; only the
-// members of list j load their values.
-constexpr int kMeanChunk = 512;
-
+// One workgroup per (list j, kv head g, sequence b), one thread per dimension,
+// after the merge: the list's new members are the last (new size - old size)
+// positions of its new range, in token order.
 template <typename T>
 __global__ __launch_bounds__(kHeadDim) void means_update_kernel(
-    Dims D, BatchInts lo, BatchInts hi, const T* __restrict__ vcache, int64_t sb, int64_t sh,
-    int64_t sn, const int32_t* __restrict__ old_loff, const int32_t* __restrict__ ids_tm,
-    float* __restrict__ means) {
-    __shared__ int32_t sid[kMeanChunk];
+    Dims D, const T* __restrict__ vcache, int64_t sb, int64_t sh, int64_t sn,
+    const int32_t* __restrict__ old_loff, const int32_t* __restrict__ new_loff,
+    const int32_t* __restrict__ perm_new, float* __restrict__ means) {
     const int j = blockIdx.x;
     const int g = blockIdx.y;
     const int b = blockIdx.z;
     const int bg = b * D.Hkv + g;
-    const int t0 = lo.v[b], t1 = hi.v[b];
-    if (t1 <= t0) return;
+    const int64_t lo = static_cast<int64_t>(bg) * (D.n_list + 1) + j;
+    const int n_old = old_loff[lo + 1] - old_loff[lo];
+    const int end = new_loff[lo + 1];
+    const int n_all = end - new_loff[lo];
+    if (n_all == n_old) return;
     const int x = threadIdx.x;
-    const int32_t* ids = ids_tm + static_cast<int64_t>(bg) * D.rcap;
+    const int32_t* perm = perm_new + static_cast<int64_t>(bg) * D.rcap;
     const T* vb = vcache + b * sb + g * sh + x;
     double s = 0.0;
-    int n_add = 0;
-    for (int c0 = t0; c0 < t1; c0 += kMeanChunk) {
-        const int n = min(kMeanChunk, t1 - c0);
-        __syncthreads();
-        for (int i = x; i < n; i += kHeadDim) sid[i] = ids[c0 + i];
-        __syncthreads();
-        for (int i = 0; i < n; ++i) {
-            if (sid[i] == j) {
-                s += static_cast<double>(load1<T>(vb + (c0 + i) * sn));
-                ++n_add;
-            }
-        }
-    }
-    if (n_add == 0) return;
-    const int32_t* lf = old_loff + static_cast<int64_t>(bg) * (D.n_list + 1);
-    const int n_old = lf[j + 1] - lf[j];
+    for (int p = end - (n_all - n_old); p < end; ++p)
+        s += static_cast<double>(load1<T>(vb + static_cast<int64_t>(perm[p]) * sn));
     float* mean = means + (static_cast<int64_t>(bg) * D.n_list + j) * kHeadDim + x;
-    const double v = (static_cast<double>(n_old) * static_cast<double>(*mean) + s) /
-                     static_cast<double>(n_old + n_add);
-    *mean = static_cast<float>(v);
+    *mean = static_cast<float>((static_cast<double>(n_old) * static_cast<double>(*mean) + s) /
+                               static_cast<double>(n_all));
 }
 
 // List-major rebuild after an update, on the device. The new tokens of a
@@ -430,11 +417,11 @@ __global__ __launch_bounds__(256) void shift_positions_kernel(
 }
 
 hipError_t launch_update_lists(const Dims& D, const BatchInts& lo, const BatchInts& hi,
-                               const int32_t* ids_tm, const int32_t* old_loff,
+                               const KV& kv, const int32_t* ids_tm, const int32_t* old_loff,
                                const int32_t* perm_old, const uint32_t* pos_old, int32_t* new_loff,
                                int32_t* shift, int32_t* perm_new, uint32_t* pos_new,
                                uint16_t* tok_list, int32_t* n_r_dev, int32_t* n_seq_dev,
-                               hipStream_t s) {
+                               float* means, hipStream_t s) {
     hipLaunchKernelGGL(update_lists_kernel, dim3(D.B * D.Hkv), dim3(kListThreads), 0, s, D, lo, hi,
                        ids_tm, old_loff, new_loff, shift, perm_new, pos_new, tok_list, n_r_dev,
                        n_seq_dev);
@@ -442,6 +429,36 @@ hipError_t launch_update_lists(const Dims& D, const BatchInts& lo, const BatchIn
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(shift_positions_kernel, dim3((D.rcap + 255) / 256, D.B * D.Hkv), dim3(256), 0,
                        s, D, lo, hi, shift, perm_old, pos_old, perm_new, pos_new);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const dim3 grid(D.n_list, D.Hkv, D.B);
+    if (kv.bf16)
+        hipLaunchKernelGGL(means_update_kernel<bf16_t>, grid, dim3(kHeadDim), 0, s, D,
+                           static_cast<const bf16_t*>(kv.v), kv.sb, kv.sh, kv.sn, old_loff, new_loff,
+                           perm_new, means);
+    else
+        hipLaunchKernelGGL(means_update_kernel<float>, grid, dim3(kHeadDim), 0, s, D,
+                           static_cast<const float*>(kv.v), kv.sb, kv.sh, kv.sn, old_loff, new_loff,
+                           perm_new, means);
+    return hipGetLastError();
+}
+
+hipError_t launch_encode_update(const Dims& D, const BatchInts& lo, const BatchInts& hi,
+                                int max_new, const KV& kv, const float* centroids,
+                                const float* codebooks, int32_t* ids_tm, uint8_t* codes_tm,
+                                float* norms_tm, hipStream_t s) {
+    if (max_new <= 0) return hipSuccess;
+    const dim3 grid(max_new, D.Hkv, D.B);
+#define PQHSA_ENC1(TT, PQT)                                                                     \
+    hipLaunchKernelGGL((encode_one_kernel<TT, PQT>), grid, dim3(kEncThreads), 0, s, D, lo, hi,    \
+                       static_cast<const TT*>(kv.k), kv.sb, kv.sh, kv.sn, centroids, codebooks,   \
+                       ids_tm, codes_tm, norms_tm)
+    if (kv.bf16) {
+        if (D.pq_bits == 4) PQHSA_ENC1(bf16_t, Pq4); else PQHSA_ENC1(bf16_t, Pq8);
+    } else {
+        if (D.pq_bits == 4) PQHSA_ENC1(float, Pq4); else PQHSA_ENC1(float, Pq8);
+    }
+#undef PQHSA_ENC1
     return hipGetLastError();
 }
 
@@ -450,61 +467,25 @@ hipError_t launch_encode(const Dims& D, const BatchInts& lo, const BatchInts& hi
                          int32_t* ids_tm, uint8_t* codes_tm, float* norms_tm, float* dist_c,
                          float* dist_f, int keep_lists, hipStream_t s) {
     if (max_new <= 0) return hipSuccess;
-    const dim3 grid((max_new + kEncTok - 1) / kEncTok, D.Hkv, D.B);
+    // 64-token tiles reuse each centroid chunk 64 times; below about a
+    // thousand such tiles the chip is better filled by 16-token tiles
+    const bool big = static_cast<int64_t>(max_new) * D.Hkv * D.B >= 64 * 1024;
+    const int tok = big ? 64 : 16;
+    const dim3 grid((max_new + tok - 1) / tok, D.Hkv, D.B);
+#define PQHSA_ENC(TT, PQT, TP)                                                                   \
+    hipLaunchKernelGGL((encode_kernel<TT, PQT, TP>), grid, dim3(kEncThreads), 0, s, D, lo, hi,    \
+                       static_cast<const TT*>(kv.k), kv.sb, kv.sh, kv.sn, centroids, codebooks,   \
+                       ids_tm, codes_tm, norms_tm, dist_c, dist_f, keep_lists)
     const bool p4 = D.pq_bits == 4;
     if (kv.bf16) {
-        if (p4)
-            hipLaunchKernelGGL((encode_kernel<bf16_t, Pq4>), grid, dim3(kEncThreads), 0, s, D, lo, hi,
-                               static_cast<const bf16_t*>(kv.k), kv.sb, kv.sh, kv.sn, centroids,
-                               codebooks, ids_tm, codes_tm, norms_tm, dist_c, dist_f, keep_lists);
-        else
-            hipLaunchKernelGGL((encode_kernel<bf16_t, Pq8>), grid, dim3(kEncThreads), 0, s, D, lo, hi,
-                               static_cast<const bf16_t*>(kv.k), kv.sb, kv.sh, kv.sn, centroids,
-                               codebooks, ids_tm, codes_tm, norms_tm, dist_c, dist_f, keep_lists);
+        if (p4) { if (big) PQHSA_ENC(bf16_t, Pq4, 4); else PQHSA_ENC(bf16_t, Pq4, 1); }
+        else { if (big) PQHSA_ENC(bf16_t, Pq8, 4); else PQHSA_ENC(bf16_t, Pq8, 1); }
     } else {
-        if (p4)
-            hipLaunchKernelGGL((encode_kernel<float, Pq4>), grid, dim3(kEncThreads), 0, s, D, lo, hi,
-                               static_cast<const float*>(kv.k), kv.sb, kv.sh, kv.sn, centroids,
-                               codebooks, ids_tm, codes_tm, norms_tm, dist_c, dist_f, keep_lists);
-        else
-            hipLaunchKernelGGL((encode_kernel<float, Pq8>), grid, dim3(kEncThreads), 0, s, D, lo, hi,
-                               static_cast<const float*>(kv.k), kv.sb, kv.sh, kv.sn, centroids,
-                               codebooks, ids_tm, codes_tm, norms_tm, dist_c, dist_f, keep_lists);
+        if (p4) { if (big) PQHSA_ENC(float, Pq4, 4); else PQHSA_ENC(float, Pq4, 1); }
+        else { if (big) PQHSA_ENC(float, Pq8, 4); else PQHSA_ENC(float, Pq8, 1); }
     }
+#undef PQHSA_ENC
     return hipGetLastError();
-}
-
-template <typename T>
-static hipError_t launch_update_t(const Dims& D, const BatchInts& lo, const BatchInts& hi,
-                                  int max_new, const KV& kv, const float* centroids,
-                                  const float* codebooks, const int32_t* old_loff, int32_t* ids_tm,
-                                  uint8_t* codes_tm, float* norms_tm, float* means, hipStream_t s) {
-    const dim3 grid(max_new, D.Hkv, D.B);
-    if (D.pq_bits == 4)
-        hipLaunchKernelGGL((encode_one_kernel<T, Pq4>), grid, dim3(kEncThreads), 0, s, D, lo, hi,
-                           static_cast<const T*>(kv.k), kv.sb, kv.sh, kv.sn, centroids, codebooks,
-                           ids_tm, codes_tm, norms_tm);
-    else
-        hipLaunchKernelGGL((encode_one_kernel<T, Pq8>), grid, dim3(kEncThreads), 0, s, D, lo, hi,
-                           static_cast<const T*>(kv.k), kv.sb, kv.sh, kv.sn, centroids, codebooks,
-                           ids_tm, codes_tm, norms_tm);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((means_update_kernel<T>), dim3(D.n_list, D.Hkv, D.B), dim3(kHeadDim), 0, s,
-                       D, lo, hi, static_cast<const T*>(kv.v), kv.sb, kv.sh, kv.sn, old_loff,
-                       ids_tm, means);
-    return hipGetLastError();
-}
-
-hipError_t launch_update(const Dims& D, const BatchInts& lo, const BatchInts& hi, int max_new,
-                         const KV& kv, const float* centroids, const float* codebooks,
-                         const int32_t* old_loff, int32_t* ids_tm, uint8_t* codes_tm,
-                         float* norms_tm, float* means, hipStream_t s) {
-    if (max_new <= 0) return hipSuccess;
-    return kv.bf16 ? launch_update_t<bf16_t>(D, lo, hi, max_new, kv, centroids, codebooks, old_loff,
-                                             ids_tm, codes_tm, norms_tm, means, s)
-                   : launch_update_t<float>(D, lo, hi, max_new, kv, centroids, codebooks, old_loff,
-                                            ids_tm, codes_tm, norms_tm, means, s);
 }
 
 }  // namespace pqhsa
