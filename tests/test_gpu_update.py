@@ -230,3 +230,22 @@ def test_tail_grows_between_updates(case):
     ctx.index_update(full, inp["k_cache"], inp["v_cache"])
     _, out2, *_ = run(ctx, inp, topk)
     assert torch.isfinite(out2).all()
+
+
+def test_grown_tail_through_a_paged_cache():
+    """A grown tail read through a block table is the contiguous result, bit for bit."""
+    from test_gpu_parity import paged_copy
+    wl = synth.workload(4, batch=3, max_seq=5000, ragged_min=3000, n_list=40)
+    inp = make(wl, seed=14)
+    full = [int(x) for x in inp["seq_lens"]]
+    old = [n - gr for n, gr in zip(full, [300, 0, 900])]
+    ctx = new_context(dict(inp, seq_lens=torch.tensor(old, dtype=torch.int32)))
+    ctx.set_option(pqhsa.OPT_VARIANT, pqhsa.VARIANT_C)
+    ctx.set_lengths(full)
+    topk = [min(k, o - inp["n_sink"] - inp["n_local"]) for k, o in zip(inp["topk"].tolist(), old)]
+    out = ctx.decode(inp["q"], inp["k_cache"], inp["v_cache"], topk)
+    kp, vp, table = paged_copy(inp["k_cache"], inp["v_cache"], 16, seed=3)
+    out_p = ctx.decode_paged(inp["q"], kp, vp, table, 16, topk)
+    torch.cuda.synchronize()
+    assert torch.equal(out, out_p)
+    assert torch.isfinite(out).all()
