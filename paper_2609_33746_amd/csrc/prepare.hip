@@ -55,35 +55,35 @@ hipError_t launch_prepare_gather(const Dims& D, const uint8_t* codes_in, const f
 
 // Global value mean over R_b per (b, g) for variant C (Appendix B): the list
 // means weighted by the list sizes, sum_j |R_j| v_bar_j / |R_b| (0 for an
-// empty R_b), accumulated in float64. One workgroup per (b, g): kGlobGroups
-// groups of one thread per dimension take every kGlobGroups-th list, then
-// group 0 adds the group sums in a fixed order.
-constexpr int kGlobGroups = 8;
+// empty R_b), accumulated in float64. Workgroup (b g, dimension chunk):
+// kGlobGroups groups of one thread per dimension of the chunk take every
+// kGlobGroups-th list, then group 0 adds the group sums in a fixed order.
+constexpr int kGlobDims = 32;                       // dimensions per workgroup
+constexpr int kGlobGroups = 1024 / kGlobDims;       // list groups per workgroup
 
-__global__ __launch_bounds__(kHeadDim * kGlobGroups) void glob_mean_kernel(Dims D, Index ix,
-                                                                          float* glob) {
-    __shared__ double part[kGlobGroups][kHeadDim];
+__global__ __launch_bounds__(1024) void glob_mean_kernel(Dims D, Index ix, float* glob) {
+    __shared__ double part[kGlobGroups][kGlobDims];
     const int bg = blockIdx.x;
     const int b = bg / D.Hkv;
-    const int t = threadIdx.x % kHeadDim;
-    const int gi = threadIdx.x / kHeadDim;
+    const int t = blockIdx.y * kGlobDims + threadIdx.x % kGlobDims;
+    const int gi = threadIdx.x / kGlobDims;
     const int32_t* loff = ix.loff + static_cast<int64_t>(bg) * (D.n_list + 1);
     const float* means = ix.means + static_cast<int64_t>(bg) * D.n_list * kHeadDim + t;
     double acc = 0.0;
 #pragma unroll 8
     for (int j = gi; j < D.n_list; j += kGlobGroups)
         acc += static_cast<double>(loff[j + 1] - loff[j]) * static_cast<double>(means[j * kHeadDim]);
-    part[gi][t] = acc;
+    part[gi][threadIdx.x % kGlobDims] = acc;
     __syncthreads();
     if (gi != 0) return;
-    for (int g = 1; g < kGlobGroups; ++g) acc += part[g][t];
+    for (int g = 1; g < kGlobGroups; ++g) acc += part[g][threadIdx.x];
     const int n_r = ix.n_r[b];
     glob[static_cast<int64_t>(bg) * kHeadDim + t] = n_r > 0 ? static_cast<float>(acc / n_r) : 0.0f;
 }
 
 hipError_t launch_glob_mean(const Dims& D, const Index& ix, float* glob, hipStream_t s) {
-    hipLaunchKernelGGL(glob_mean_kernel, dim3(D.B * D.Hkv), dim3(kHeadDim * kGlobGroups), 0, s, D,
-                       ix, glob);
+    hipLaunchKernelGGL(glob_mean_kernel, dim3(D.B * D.Hkv, kHeadDim / kGlobDims), dim3(1024), 0, s,
+                       D, ix, glob);
     return hipGetLastError();
 }
 
