@@ -273,6 +273,19 @@ def test_variant_full_size(variant):
     check_rows(inp, topk, rows[:4], out_b, sel_b, unsel_b)
 
 
+def test_variant_bx_batched_full_size():
+    """Bx at 128K with four sequences and groups of 8 query heads; sampled rows."""
+    wl = synth.workload(3)
+    inp = make(wl, seed=2)
+    ctx = context(inp)
+    ctx.set_option(pqhsa.OPT_VARIANT, pqhsa.VARIANT_BX)
+    topk, out, sel, unsel, _ = run(ctx, inp)
+    rng = np.random.default_rng(13)
+    rows = [(b, int(h)) for b in range(wl.batch)
+            for h in rng.choice(wl.n_q_heads, 2, replace=False)]
+    check_rows(inp, topk, rows, out, sel, unsel, variant="Bx")
+
+
 VARIANT_EDGE = {
     "g8": (small(3, batch=2, max_seq=3000, n_q_heads=16, n_kv_heads=2, n_list=16, topk=60), {}),
     "k0": (small(1, max_seq=3000, n_list=16, topk=0), {}),
