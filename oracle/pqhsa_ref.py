@@ -52,8 +52,26 @@ Readings where the paper is silent:
   residuals of given tokens, and ends with `encode_ref` against the trained
   model and the list means of the final lists.
 
-Parity pins for every function live in tests/test_oracle_pins.py (brute force,
-closed forms, special cases). No function here is "parity unpinned".
+Each function is pinned in tests/test_oracle_pins.py to something other
+than itself:
+* budget_paper: the budgets the paper prints (Appendix A);
+* lut_ref, pq_scores_ref: explicit key reconstruction, exact-reconstruction
+  keys, a zero query;
+* topk_ref: brute-force ranking and exhaustive subsets;
+* dense_attention_ref: torch's attention routine in float64, whole and
+  truncated caches;
+* list_means_ref: brute-force means;
+* pqhsa_row_ref: rho = 1 against library attention, closed forms under exact
+  reconstruction, the pseudo-token form of pure background, the variants'
+  special cases, invariances, an mpmath re-evaluation;
+* pqhsa_batch_ref: library attention with grouped query heads over ragged
+  sequences (at rho = 1, and for any k under exact reconstruction with
+  list-constant values);
+* encode_ref, update_ref: scipy's vector quantizer, an exactly representable
+  key, norm scaling, update composition;
+* kmeans_ref: scipy's kmeans2, a brute-force re-seed;
+* build_ref: zero-iteration closed forms, and scipy's kmeans2 for the coarse
+  centers and for the codewords on residual slices the test forms itself.
 """
 
 from __future__ import annotations

@@ -1,6 +1,7 @@
-// Code scan (Section 3.1, Eq. 2; Section 3.3 "code scan with a fused per-list
-// reduction"). Every indexed token of every list is scored for the G query
-// heads that share its KV head, in one pass over the list-major uint8 codes.
+// Code scan (Section 3.1, Eq. 2; Section 3.3, execution path: the scan and
+// the per-list reduction of the background run in one pass). Every indexed
+// token of every list is scored for the G query heads that share its KV
+// head, in one pass over the list-major codes.
 //
 // Work decomposition: the list-major positions of each (batch element, KV
 // head) are cut into sub-chunks of kSub positions; one wave owns one

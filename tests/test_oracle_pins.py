@@ -558,3 +558,144 @@ def test_build_closed_forms_and_consistency():
         np.testing.assert_allclose(
             b["centroids"], R.kmeans_ref(U[Rr], [int(np.flatnonzero(Rr == t)[0]) for t in init_c], it[0]),
             atol=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# dense attention (Section 3, opening paragraph; Eq. 1 with B empty)
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("n_seq", [None, 1, 37, 200])
+def test_dense_attention_matches_library_attention(n_seq):
+    """The dense oracle against torch's attention routine (float64, CPU), on
+    the whole cache and truncated to its first n_seq rows; the rows past
+    n_seq hold large values, so reading them fails the pin."""
+    rng = np.random.default_rng(31)
+    d, n = 32, 200
+    K = rng.standard_normal((n, d))
+    V = rng.standard_normal((n, d))
+    q = 0.5 * K[5] + rng.standard_normal(d)   # a spread softmax: the 1/sqrt(d) matters
+    want = sdpa(q, K if n_seq is None else K[:n_seq], V if n_seq is None else V[:n_seq])
+    if n_seq is not None:
+        K[n_seq:] = 50.0 * rng.standard_normal((n - n_seq, d))
+        V[n_seq:] = 1e3
+    assert close(R.dense_attention_ref(q, K, V, n_seq), want, 1e-12)
+
+
+def _gqa_batch(seed, B=2, Hq=8, Hkv=2, d=16, n_m=4, ksub=8, n_list=5, lens=(150, 97),
+               nmax=160, exact=False, list_constant=False):
+    """A ragged batch in the ABI's layouts, built independently of the
+    product's generator. Each (b, KV head) has its own index; padding rows
+    past seq_lens[b] hold values that would show if they were read. With
+    exact=True every key equals its PQ reconstruction (no noise), and with
+    list_constant=True every value is its list's offset."""
+    rng = np.random.default_rng(seed)
+    ds = d // n_m
+    q = np.zeros((B, Hq, d))
+    Kc = np.zeros((B, Hkv, nmax, d))
+    Vc = np.zeros((B, Hkv, nmax, d))
+    ids = np.zeros((B, Hkv, nmax), np.int64)
+    codes = np.zeros((B, Hkv, nmax, n_m), np.uint8)
+    norms = np.ones((B, Hkv, nmax))
+    cen = rng.standard_normal((B, Hkv, n_list, d))
+    cb = 0.4 * rng.standard_normal((B, Hkv, n_m, ksub, ds))
+    means = np.zeros((B, Hkv, n_list, d))
+    for b in range(B):
+        n = lens[b]
+        for g in range(Hkv):
+            a = rng.integers(0, n_list, size=nmax)
+            z = rng.integers(0, ksub, size=(nmax, n_m))
+            recon = cen[b, g, a] + np.concatenate([cb[b, g, m, z[:, m]] for m in range(n_m)], axis=1)
+            Kc[b, g] = recon + (0.0 if exact else 0.1) * rng.standard_normal((nmax, d))
+            off = rng.standard_normal((n_list, d))
+            Vc[b, g] = off[a] if list_constant else rng.standard_normal((nmax, d)) + 0.5 * off[a]
+            Kc[b, g, n:] = 40.0 * rng.standard_normal((nmax - n, d))
+            Vc[b, g, n:] = 1e3
+            ids[b, g], codes[b, g] = a, z
+            means[b, g] = R.list_means_ref(Vc[b, g], a, n_list, np.arange(4, n - 8))
+        for h in range(Hq):
+            g = h // (Hq // Hkv)
+            q[b, h] = 2.0 * Kc[b, g, rng.integers(4, n - 8)] + 0.3 * rng.standard_normal(d)
+    return dict(q=q, k_cache=Kc, v_cache=Vc, list_ids=ids, codes=codes, norms=norms,
+                centroids=cen, codebooks=cb, list_means=means,
+                seq_lens=np.array(lens, np.int32), n_sink=4, n_local=8)
+
+
+def _sdpa_gqa(inp, b):
+    """Library attention of sequence b over its first seq_lens[b] tokens,
+    with torch's own grouped-query head mapping (float64, CPU)."""
+    n = int(inp["seq_lens"][b])
+    qt = torch.from_numpy(inp["q"][b])[None, :, None, :]
+    kt = torch.from_numpy(inp["k_cache"][b, :, :n])[None]
+    vt = torch.from_numpy(inp["v_cache"][b, :, :n])[None]
+    return torch.nn.functional.scaled_dot_product_attention(qt, kt, vt, enable_gqa=True)[0, :, 0].numpy()
+
+
+def test_batch_oracle_gqa_mapping_and_ragged_lengths_at_rho_one():
+    """k = |R_b| makes every row dense attention (Section 3.2, rho = 1): the
+    batch oracle must then equal library attention with grouped query heads
+    (head h reads KV head h // G, Section 3.3) over each sequence's own
+    length. A head mapped to the wrong KV head, or a sequence read past its
+    length, fails."""
+    inp = _gqa_batch(41)
+    topk = [int(n) - 12 for n in inp["seq_lens"]]
+    refs = R.pqhsa_batch_ref(inp, topk)
+    for b in range(2):
+        want = _sdpa_gqa(inp, b)
+        for h in range(8):
+            assert close(refs[(b, h)].y, want[h], 1e-12), (b, h)
+            assert refs[(b, h)].Z_B == 0.0
+
+
+@pytest.mark.parametrize("k", [0, 3, 40])
+def test_batch_oracle_gqa_index_mapping_closed_form(k):
+    """With exact reconstruction (l~ = l for every token) and list-constant
+    values (v_i = v_bar of its list), the background of Eq. 4 equals the
+    dense contribution of B exactly, so every row is dense attention for any
+    k. The index tensors of the wrong KV head give other scores and fail."""
+    inp = _gqa_batch(43, exact=True, list_constant=True)
+    topk = [k, k]
+    refs = R.pqhsa_batch_ref(inp, topk)
+    for b in range(2):
+        want = _sdpa_gqa(inp, b)
+        for h in range(8):
+            assert close(refs[(b, h)].y, want[h], 1e-10), (b, h)
+            if k == 0:
+                assert refs[(b, h)].Z_B > 0.0
+
+
+# ---------------------------------------------------------------------------
+# index build: the subspace problems at n_iter_pq >= 1 (appendix on the index
+# build; Section 3.1 for the residual slices)
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("it_c,it_p", [(1, 1), (1, 2), (2, 2)])
+def test_build_codebooks_match_scipy_on_residual_slices(it_c, it_p):
+    """The codewords after n_iter_pq iterations equal scipy's Lloyd iteration
+    (kmeans2 from given centers) on the residual slices u - c_a, where the
+    test forms u, the coarse centers (scipy too), the nearest-center lists and
+    the residuals itself."""
+    import scipy.cluster.vq as vq
+    rng = np.random.default_rng(47)
+    n, d, M, ksub, n_list = 400, 16, 4, 6, 4
+    # clustered directions, so that no coarse center or codeword loses all points
+    dirs = rng.standard_normal((n_list, d)) * 3.0
+    lab = rng.integers(0, n_list, size=n)
+    K = (dirs[lab] + rng.standard_normal((n, d))) * rng.uniform(0.5, 2.0, size=(n, 1))
+    V = rng.standard_normal((n, d))
+    Rr = np.arange(4, n - 10)
+    init_c = np.array([Rr[np.flatnonzero(lab[Rr] == j)[0]] for j in range(n_list)])
+    init_p = np.stack([rng.choice(Rr, ksub, replace=False) for _ in range(M)])
+    got = R.build_ref(K, V, Rr, n_list, M, ksub, init_c, init_p, it_c, it_p)
+
+    U = K[Rr] / np.sqrt((K[Rr] ** 2).sum(axis=1, keepdims=True))
+    row = {int(t): i for i, t in enumerate(Rr)}
+    C, _ = vq.kmeans2(U, U[[row[int(t)] for t in init_c]].copy(), iter=it_c, minit="matrix",
+                      missing="raise")
+    a, _ = vq.vq(U, C)
+    res = U - C[a]
+    ds = d // M
+    for m in range(M):
+        sl = res[:, m * ds:(m + 1) * ds]
+        want, _ = vq.kmeans2(sl, sl[[row[int(t)] for t in init_p[m]]].copy(), iter=it_p,
+                             minit="matrix", missing="raise")
+        np.testing.assert_allclose(got["codebooks"][m], want, atol=1e-12)
+    np.testing.assert_allclose(got["centroids"], C, atol=1e-12)
+    np.testing.assert_array_equal(got["list_ids"][Rr], a)
