@@ -232,6 +232,26 @@ def list_means_ref(V, list_ids, n_list: int, R: np.ndarray):
 # Encoding keys into the existing index (Section 3.1) and the incremental
 # update (Section 3.3).
 # ---------------------------------------------------------------------------
+def sq_dists(X, C):
+    """Squared Euclidean distances ||x - c||^2 of every row of X [n, dim] to
+    every row of C [k, dim], as ||x||^2 - 2 x . c + ||c||^2 with one matrix
+    product per block of rows (float64; a negative rounding residue is set
+    to 0)."""
+    X = np.asarray(X, np.float64)
+    C = np.asarray(C, np.float64)
+    cc = (C * C).sum(axis=1)
+    out = np.empty((X.shape[0], C.shape[0]))
+    for s in range(0, X.shape[0], 8192):
+        x = X[s:s + 8192]
+        d2 = out[s:s + 8192]
+        np.matmul(x, C.T, out=d2)
+        d2 *= -2.0
+        d2 += (x * x).sum(axis=1)[:, None]
+        d2 += cc[None, :]
+        np.maximum(d2, 0.0, out=d2)
+    return out
+
+
 @dataclass
 class Encoding:
     a: np.ndarray          # [n] list id
@@ -241,12 +261,13 @@ class Encoding:
     fine_d2: np.ndarray    # [n, M, K] ||(u - c_a)^(m) - p_{m,z}||^2
 
 
-def encode_ref(keys, centroids, codebooks) -> Encoding:
+def encode_ref(keys, centroids, codebooks, tables: bool = True) -> Encoding:
     """Direction-norm residual IVF-PQ encoding of keys [n, d] (Section 3.1).
 
     r = ||k||, u = k / r; a = the list whose centroid is nearest to u; then
     for each subspace m the codeword nearest to the m-th slice of u - c_a.
-    The distance tables are returned for validity checks of other encoders.
+    The distance tables are returned for validity checks of other encoders
+    (None for both when tables=False, which keeps only the choices).
     """
     K = np.asarray(keys, np.float64)
     C = np.asarray(centroids, np.float64)
@@ -257,16 +278,17 @@ def encode_ref(keys, centroids, codebooks) -> Encoding:
     u = np.zeros_like(K)
     nz = r > 0
     u[nz] = K[nz] / r[nz, None]
-    coarse = np.empty((n, C.shape[0]))
-    for s in range(0, n, 256):
-        coarse[s:s + 256] = ((u[s:s + 256, None, :] - C[None]) ** 2).sum(axis=2)
+    coarse = sq_dists(u, C)
     a = coarse.argmin(axis=1)            # the first minimum: the smaller id
     res = (u - C[a]).reshape(n, M, dsub)
-    fine = np.empty((n, M, ksub))
+    fine = np.empty((n, M, ksub)) if tables else None
+    z = np.empty((n, M), np.int64)
     for m in range(M):
-        fine[:, m, :] = ((res[:, m, None, :] - P[m][None]) ** 2).sum(axis=2)
-    z = fine.argmin(axis=2)
-    return Encoding(a=a, z=z, r=r, coarse_d2=coarse, fine_d2=fine)
+        dm = sq_dists(res[:, m, :], P[m])
+        z[:, m] = dm.argmin(axis=1)
+        if tables:
+            fine[:, m, :] = dm
+    return Encoding(a=a, z=z, r=r, coarse_d2=coarse if tables else None, fine_d2=fine)
 
 
 def update_ref(list_ids, codes, norms, K, V, n_old: int, n_new: int, n_sink: int,
@@ -308,9 +330,7 @@ def kmeans_ref(X, init_idx, n_iter: int):
     C = X[np.asarray(init_idx, np.int64)].copy()
     n, k = X.shape[0], C.shape[0]
     for _ in range(n_iter):
-        d2 = np.empty((n, k))
-        for s in range(0, n, 512):
-            d2[s:s + 512] = ((X[s:s + 512, None, :] - C[None]) ** 2).sum(axis=2)
+        d2 = sq_dists(X, C)
         a = d2.argmin(axis=1)
         dmin = d2[np.arange(n), a]
         cnt = np.bincount(a, minlength=k)
@@ -348,12 +368,12 @@ def build_ref(K, V, R, n_list: int, M: int, ksub: int, init_coarse, init_pq,
     U[nz] = K[R][nz] / r[nz, None]
     pos = {int(t): i for i, t in enumerate(R)}
     C = kmeans_ref(U, [pos[int(t)] for t in init_coarse], n_iter_coarse)
-    a = encode_ref(K[R], C, np.zeros((M, 1, ds))).a
+    a = encode_ref(K[R], C, np.zeros((M, 1, ds)), tables=False).a
     res = U - C[a]
     P = np.stack([kmeans_ref(res[:, m * ds:(m + 1) * ds],
                              [pos[int(t)] for t in np.asarray(init_pq)[m]], n_iter_pq)
                   for m in range(M)])
-    enc = encode_ref(K[R], C, P)
+    enc = encode_ref(K[R], C, P, tables=False)
     ids = np.zeros(n_tok, np.int64)
     codes = np.zeros((n_tok, M), np.int64)
     norms = np.zeros(n_tok)
