@@ -52,8 +52,13 @@ def run(ctx, inp, topk=None, scores=False):
 def check_rows(inp, topk, rows, out, sel, unsel, scores=None, out_tol=OUT_TOL, variant="B"):
     """Compare the listed (b, h) rows with the oracle's mechanism `variant`;
     returns worst errors."""
-    rows = list(rows)
-    refs = R.pqhsa_batch_ref(inp, topk, rows, variant=variant)
+    rows = sorted(rows)
+    refs = {}
+    for b in sorted({b for b, _ in rows}):   # one batch element at a time, with progress
+        rows_b = [r for r in rows if r[0] == b]
+        refs.update(R.pqhsa_batch_ref(inp, topk, rows_b, variant=variant))
+        if len(rows) > 64:
+            say(f"[oracle] batch element {b}: {len(rows_b)} rows")
     worst = dict(out=0.0, score=0.0, tie_swaps=0)
     out_c = out.double().cpu().numpy()
     sel_c = sel.cpu().numpy()

@@ -158,8 +158,8 @@ def test_index_update(case):
 
 
 def test_index_update_128k():
-    """One 256-step update of the 128K workload; sampled rows."""
-    update_case(synth.workload(2), [256], rows_every=8)
+    """One 256-step update of the 128K workload; every row."""
+    update_case(synth.workload(2), [256], rows_every=1)
 
 
 def test_update_twice_equals_once_and_noop():
