@@ -250,6 +250,33 @@ pqhsa_status pqhsa_dense_decode(pqhsa_ctx* ctx, const void* q, const void* k_cac
                                 const int32_t* seq_lens, float* out,
                                 hipStream_t stream);
 
+/* Dense decode attention as pqhsa_dense_decode, without a context and
+ * without allocating device memory: for callers that cannot allocate (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc).
+ *   batch, n_q_heads, n_kv_heads  the shape (G = n_q_heads / n_kv_heads in
+ *                                 {1, 2, 4, 8}, batch <= 256)
+ *   head_dim                      128
+ *   kv_dtype                      PQHSA_F32 or PQHSA_BF16 (q, k_cache, v_cache)
+ *   q, k_cache, v_cache, kv_strides, out  as in pqhsa_dense_decode
+ *   seq_lens                      HOST int32 [batch], 1 <= N_b <= 2^20
+ * Scratch: the split partials of every row, batch * n_q_heads *
+ * ceil(max N_b / 2048) of 528 bytes each, live in one fixed 32 MiB device
+ * array of the library (a copy on every GPU it runs on, held until the
+ * process ends; its address is looked up on the first call on each device).
+ * A call that needs more (for example batch * n_q_heads > 992 at
+ * N_b = 131072) returns PQHSA_ERR_INVALID_ARGUMENT before any device work.
+ * Nothing in the array needs to start at zero: every partial a call reads it
+ * writes first. Every call on one GPU shares that GPU's array, so calls that
+ * overlap on one GPU (other streams, other threads) race on it.
+ * Asynchronous; enqueues two kernels on `stream`. Errors are reported by
+ * pqhsa_last_error(NULL) on the calling thread. */
+pqhsa_status pqhsa_dense_decode_noalloc(int32_t batch, int32_t n_q_heads, int32_t n_kv_heads,
+                                        int32_t head_dim, int32_t kv_dtype, const void* q,
+                                        const void* k_cache, const void* v_cache,
+                                        const int64_t* kv_strides, const int32_t* seq_lens,
+                                        float* out, hipStream_t stream);
+
 /* Copy out the prepared list-major layout (synchronises `stream`):
  *   perm    int32 [B, Hkv, Nmax]: token id at each list-major position of R_b
  *           (lists in increasing id, tokens in increasing id within a list),
@@ -308,7 +335,8 @@ pqhsa_status pqhsa_stage_times(pqhsa_ctx* ctx, float* ms, int32_t n, int32_t* n_
 const char* pqhsa_status_string(pqhsa_status status);
 
 /* Message of the last failed call on this context ("" if none; NULL ctx gives
- * the message of the last failed pqhsa_create in this process). */
+ * the message of the last failed call made without a context on this thread:
+ * pqhsa_create or pqhsa_dense_decode_noalloc). */
 const char* pqhsa_last_error(const pqhsa_ctx* ctx);
 
 #ifdef __cplusplus

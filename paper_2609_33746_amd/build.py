@@ -19,7 +19,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB_DIR = os.path.join(PKG, "_lib")
 LIB = os.path.join(LIB_DIR, "libpqhsa.so")
 
-SOURCES = ["api.cpp", "prologue.hip", "scan.hip", "select.hip", "attend.hip", "prepare.hip", "update.hip", "build.hip"]
+SOURCES = ["api.cpp", "prologue.hip", "scan.hip", "select.hip", "attend.hip", "prepare.hip", "update.hip", "build.hip", "noalloc.hip"]
 ARCH = "gfx950"
 
 

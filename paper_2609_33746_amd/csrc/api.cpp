@@ -172,15 +172,17 @@ pqhsa_status check_device(pqhsa_ctx* c) {
     return PQHSA_OK;
 }
 
-pqhsa_status check_kv(pqhsa_ctx* c, const void* q, const void* k, const void* v,
-                      const int64_t* strides, const void* out, KV* kv) {
+// The cache pointers and strides of a call; errors go to c (or, with c null,
+// to the thread's context-free message).
+pqhsa_status check_kv_dtype(pqhsa_ctx* c, int kv_dtype, const void* q, const void* k,
+                            const void* v, const int64_t* strides, const void* out, KV* kv) {
     if (!q || !k || !v || !out || !strides)
         return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "q, k_cache, v_cache, kv_strides and out must be non-NULL");
     const int64_t sb = strides[0], sh = strides[1], sn = strides[2];
     if (sb < 0 || sh < 0 || sn < kHeadDim)
         return fail(c, PQHSA_ERR_INVALID_ARGUMENT,
                     "kv_strides must be non-negative with a token stride >= head_dim");
-    const int esz = c->shape.kv_dtype == PQHSA_BF16 ? 2 : 4;
+    const int esz = kv_dtype == PQHSA_BF16 ? 2 : 4;
     if ((sb * esz) % 16 || (sh * esz) % 16 || (sn * esz) % 16 ||
         reinterpret_cast<uintptr_t>(k) % 16 || reinterpret_cast<uintptr_t>(v) % 16 ||
         reinterpret_cast<uintptr_t>(q) % 16)
@@ -191,8 +193,13 @@ pqhsa_status check_kv(pqhsa_ctx* c, const void* q, const void* k, const void* v,
     kv->sb = sb;
     kv->sh = sh;
     kv->sn = sn;
-    kv->bf16 = c->shape.kv_dtype == PQHSA_BF16;
+    kv->bf16 = kv_dtype == PQHSA_BF16;
     return PQHSA_OK;
+}
+
+pqhsa_status check_kv(pqhsa_ctx* c, const void* q, const void* k, const void* v,
+                      const int64_t* strides, const void* out, KV* kv) {
+    return check_kv_dtype(c, c->shape.kv_dtype, q, k, v, strides, out, kv);
 }
 
 // A paged cache: the strides are those of (page, kv head, token in page);
@@ -776,6 +783,59 @@ pqhsa_status pqhsa_dense_decode(pqhsa_ctx* c, const void* q, const void* k, cons
     }
     hipError_t e = launch_dense(c->D, kv, lens, c->dense_partial, out, c->dense_nsplit, stream);
     if (e != hipSuccess) return hip_fail(c, e, "enqueueing the dense decode kernels");
+    return PQHSA_OK;
+}
+
+pqhsa_status pqhsa_dense_decode_noalloc(int32_t batch, int32_t n_q_heads, int32_t n_kv_heads,
+                                        int32_t head_dim, int32_t kv_dtype, const void* q,
+                                        const void* k, const void* v, const int64_t* kv_strides,
+                                        const int32_t* seq_lens, float* out, hipStream_t stream) {
+    g_create_error.clear();
+    // every check on the host first: nothing below touches the device until
+    // the call is known to fit the scratch array
+    if (batch < 1 || n_q_heads < 1 || n_kv_heads < 1 || n_q_heads % n_kv_heads)
+        return fail(nullptr, PQHSA_ERR_INVALID_ARGUMENT,
+                    "need batch, n_q_heads, n_kv_heads >= 1 and n_kv_heads dividing n_q_heads");
+    const int G = n_q_heads / n_kv_heads;
+    if (G != 1 && G != 2 && G != 4 && G != 8)
+        return fail(nullptr, PQHSA_ERR_UNSUPPORTED, "GQA group size must be 1, 2, 4 or 8");
+    if (head_dim != kHeadDim) return fail(nullptr, PQHSA_ERR_UNSUPPORTED, "head_dim must be 128");
+    if (kv_dtype != PQHSA_F32 && kv_dtype != PQHSA_BF16)
+        return fail(nullptr, PQHSA_ERR_UNSUPPORTED, "kv_dtype must be PQHSA_F32 or PQHSA_BF16");
+    if (batch > kMaxBatch) return fail(nullptr, PQHSA_ERR_UNSUPPORTED, "batch must be <= 256");
+    KV kv;
+    pqhsa_status st = check_kv_dtype(nullptr, kv_dtype, q, k, v, kv_strides, out, &kv);
+    if (st != PQHSA_OK) return st;
+    if (!seq_lens) return fail(nullptr, PQHSA_ERR_INVALID_ARGUMENT, "seq_lens is NULL");
+    BatchInts lens;
+    int n_max = 0;
+    for (int b = 0; b < batch; ++b) {
+        if (seq_lens[b] < 1 || seq_lens[b] > kMaxSeq)
+            return fail(nullptr, PQHSA_ERR_INVALID_ARGUMENT, "seq_lens[%d] = %d outside [1, 2^20]", b,
+                        seq_lens[b]);
+        lens.v[b] = seq_lens[b];
+        n_max = std::max(n_max, seq_lens[b]);
+    }
+    // the split partials of every row, in the fixed scratch array
+    const int nsplit = (n_max + kDenseRows - 1) / kDenseRows;
+    const size_t need = static_cast<size_t>(batch) * n_q_heads * nsplit * kPartStride * sizeof(float);
+    if (need > static_scratch_bytes())
+        return fail(nullptr, PQHSA_ERR_INVALID_ARGUMENT,
+                    "batch %d x %d query heads x %d splits of %d tokens need %zu bytes of scratch; "
+                    "the fixed scratch holds %zu",
+                    batch, n_q_heads, nsplit, kDenseRows, need, static_scratch_bytes());
+    void* scratch = nullptr;
+    hipError_t e = static_scratch(&scratch);
+    if (e != hipSuccess) return fail(nullptr, PQHSA_ERR_HIP, "scratch address: %s", hipGetErrorString(e));
+    Dims D{};
+    D.B = batch;
+    D.Hq = n_q_heads;
+    D.Hkv = n_kv_heads;
+    D.G = G;
+    D.inv_sqrt_d = static_cast<float>(1.0 / std::sqrt(static_cast<double>(kHeadDim)));
+    e = launch_dense(D, kv, lens, static_cast<float*>(scratch), out, nsplit, stream);
+    if (e != hipSuccess)
+        return fail(nullptr, PQHSA_ERR_HIP, "enqueueing the dense decode kernels: %s", hipGetErrorString(e));
     return PQHSA_OK;
 }
 

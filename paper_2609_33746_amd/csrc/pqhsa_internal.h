@@ -179,6 +179,11 @@ hipError_t launch_merge(const Dims& D, const BatchArgs& ba, const Work& w, float
                         int nsplit_max, int variant, hipStream_t s, const KTiming& tm = KTiming{});
 hipError_t launch_dense(const Dims& D, const KV& kv, const BatchInts& lens, float* partial,
                         float* out, int nsplit_max, hipStream_t s);
+// The fixed scratch array of the entry point that allocates nothing: its size,
+// and its device address on the current device (looked up on the first call
+// per device, then kept).
+size_t static_scratch_bytes();
+hipError_t static_scratch(void** ptr);
 // the token-weighted mean of the list means per (b, g): the global value
 // mean over R_b of variant C
 hipError_t launch_glob_mean(const Dims& D, const Index& ix, float* glob, hipStream_t s);

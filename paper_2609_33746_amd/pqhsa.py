@@ -64,6 +64,7 @@ def load_library(build_if_missing: bool = True) -> ctypes.CDLL:
         "pqhsa_index_build": ([P, P, P, P, P, P, P, I32, I32, P], I32),
         "pqhsa_decode_debug": ([P, P, P, P, P, P, P, P, P, P, P], I32),
         "pqhsa_dense_decode": ([P, P, P, P, P, P, P, P], I32),
+        "pqhsa_dense_decode_noalloc": ([I32, I32, I32, I32, I32, P, P, P, P, P, P, P], I32),
         "pqhsa_index_export": ([P, P, P, P], I32),
         "pqhsa_set_option": ([P, I32, I64], I32),
         "pqhsa_stage_times": ([P, P, I32, P], I32),
@@ -270,6 +271,36 @@ class PQHSA:
             self.close()
         except Exception:
             pass
+
+
+def dense_decode_noalloc(q, k_cache, v_cache, seq_lens, out=None):
+    """Dense decode without a context: the library's fixed scratch array holds
+    the split partials, and the call allocates no device memory (apart from
+    `out` when it is not given). q [B, Hq, d]; k_cache, v_cache [B, Hkv, N, d]
+    with equal strides and a contiguous last dimension; seq_lens: B ints."""
+    lib = load_library()
+    if q.device.type != "cuda" or k_cache.device.type != "cuda" or v_cache.device.type != "cuda":
+        raise ValueError("q, k_cache and v_cache must be GPU tensors")
+    if not q.is_contiguous() or k_cache.stride() != v_cache.stride() or k_cache.stride(3) != 1:
+        raise ValueError("q must be contiguous; k_cache and v_cache need equal strides and a "
+                         "contiguous last dimension")
+    if q.dtype != k_cache.dtype or v_cache.dtype != k_cache.dtype:
+        raise ValueError("q, k_cache and v_cache must share one dtype")
+    dtype = {torch.bfloat16: BF16, torch.float32: F32}.get(k_cache.dtype)
+    if dtype is None:
+        raise ValueError("dtype must be bfloat16 or float32")
+    if out is None:
+        out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+    if out.dtype != torch.float32 or not out.is_contiguous():
+        raise ValueError("out must be a contiguous float32 tensor")
+    st = k_cache.stride()
+    strides = (ctypes.c_int64 * 3)(st[0], st[1], st[2])
+    status = lib.pqhsa_dense_decode_noalloc(
+        int(q.shape[0]), int(q.shape[1]), int(k_cache.shape[1]), int(q.shape[2]), dtype, _ptr(q),
+        _ptr(k_cache), _ptr(v_cache), strides, _host_i32(list(seq_lens)), _ptr(out), _stream())
+    if status != OK:
+        raise PQHSAError(status, lib.pqhsa_last_error(None).decode())
+    return out
 
 
 def context_for(inp: dict, max_topk: int | None = None) -> "PQHSA":

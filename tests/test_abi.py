@@ -67,3 +67,28 @@ def test_status_strings(lib):
     for st in range(6):
         assert lib.pqhsa_status_string(st)
     assert lib.pqhsa_status_string(99) == b"unknown status"
+
+
+def test_noalloc_dense_rejects_before_touching_the_device(lib):
+    """Argument and scratch-size checks of the entry point that allocates
+    nothing all happen on the host: the pointers below are never read."""
+    I64x3 = ctypes.c_int64 * 3
+    fake = ctypes.c_void_p(1 << 20)   # 16-byte aligned, never dereferenced
+    strides = I64x3(8 * 131072 * 128, 131072 * 128, 128)
+
+    def call(batch, hq, hkv, lens, head_dim=128, dtype=pqhsa.BF16, st=strides, q=fake):
+        arr = (ctypes.c_int32 * len(lens))(*lens)
+        return lib.pqhsa_dense_decode_noalloc(batch, hq, hkv, head_dim, dtype, q, fake, fake, st,
+                                              arr, fake, None)
+    # 16 x 64 query heads x 64 splits of 2048 tokens: 34.6 MB > 32 MiB of scratch
+    assert call(16, 64, 8, [131072] * 16) == pqhsa.ERR_INVALID_ARGUMENT
+    assert b"scratch" in lib.pqhsa_last_error(None)
+    assert call(1, 32, 8, [0]) == pqhsa.ERR_INVALID_ARGUMENT
+    assert call(1, 32, 8, [(1 << 20) + 1]) == pqhsa.ERR_INVALID_ARGUMENT
+    assert call(1, 32, 8, [100], head_dim=64) == pqhsa.ERR_UNSUPPORTED
+    assert call(1, 24, 2, [100]) == pqhsa.ERR_UNSUPPORTED            # G = 12
+    assert call(1, 32, 7, [100]) == pqhsa.ERR_INVALID_ARGUMENT       # 32 % 7
+    assert call(1, 32, 8, [100], dtype=5) == pqhsa.ERR_UNSUPPORTED
+    assert call(257, 32, 8, [100] * 257) == pqhsa.ERR_UNSUPPORTED
+    assert call(1, 32, 8, [100], q=None) == pqhsa.ERR_INVALID_ARGUMENT
+    assert call(1, 32, 8, [100], st=I64x3(0, 0, 64)) == pqhsa.ERR_INVALID_ARGUMENT
