@@ -8,7 +8,9 @@
 // sub-chunk, and a workgroup holds kScanWaves consecutive sub-chunks of the
 // same KV head so that they share one copy of the group LUT in LDS. Every
 // batch element gets the workgroup count of the longest R_b; the surplus
-// workgroups of shorter sequences exit at once.
+// workgroups of shorter sequences exit at once. The workgroups of one KV head
+// are spaced by the number of (batch element, KV head) units in the grid, so
+// that they share an XCD.
 //
 // The workgroup first stages the group LUT and the coarse table in LDS
 // (through registers), then each wave issues the loads of all its 64-position
@@ -103,12 +105,18 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(Dims D, BatchArgs ba
     float* coarse_s = reinterpret_cast<float*>(coarse4);
     constexpr int kParts = GT / G;   // workgroups per (b, g) and sub-chunk range
     static_assert(kParts * G == GT, "head split");
-    const int part = (blockIdx.x / nwg) % kParts;
-    const int bg = blockIdx.x / nwg / kParts;
+    // workgroup i serves unit i mod U of the U = B Hkv kParts (b, g, part)
+    // units, chunk i / U: workgroups run on XCD i mod 8, so when U is a
+    // multiple of 8 every workgroup of a unit shares one XCD and its L2, and
+    // the unit's tables come from HBM once instead of once per XCD
+    const int n_units = D.B * D.Hkv * kParts;
+    const int unit = blockIdx.x % n_units;
+    const int part = unit % kParts;
+    const int bg = unit / kParts;
     const int b = bg / D.Hkv;
     const int g = bg % D.Hkv;
     const int n_r = ba.n_r[b];
-    const int sc0 = (blockIdx.x % nwg) * kScanWaves;
+    const int sc0 = (blockIdx.x / n_units) * kScanWaves;
     if (sc0 * kSub >= n_r) return;   // surplus workgroup of a shorter sequence
 
     const int tid = threadIdx.x;
