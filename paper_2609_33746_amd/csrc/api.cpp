@@ -61,7 +61,6 @@ struct pqhsa_ctx {
     int32_t* n_seq_dev = nullptr;
     int32_t* n_r_dev = nullptr;
     int scan_nwg = 0;   // scan workgroups per (b, kv head)
-    uint32_t epoch = 0;  // prologue launches so far (LUT completion counters)
 
     // workspace
     Work w{};
@@ -319,8 +318,11 @@ pqhsa_status pqhsa_create(const pqhsa_shape* shape, pqhsa_ctx** out) {
     A(dev_alloc(c, &w.lut, BG * lut_row * G));
     A(dev_alloc(c, &w.coarse, BG * L * G + 16));   // + 16: whole float4 reads at the end
     A(dev_alloc(c, &w.lut_head, BQ * lut_row));
-    A(dev_alloc(c, &w.lut_done, BG));
-    if (ea == hipSuccess) ea = hipMemset(w.lut_done, 0, BG * sizeof(uint32_t));
+    const size_t lut_parts = BG * prologue_parts(D.n_list, D.pq_bits);
+    A(dev_alloc(c, &w.lut_flag, lut_parts));
+    A(dev_alloc(c, &w.epoch, BG));
+    if (ea == hipSuccess) ea = hipMemset(w.lut_flag, 0, lut_parts * sizeof(uint32_t));
+    if (ea == hipSuccess) ea = hipMemset(w.epoch, 0, BG * sizeof(uint32_t));
     A(dev_alloc(c, &w.tau_lo, BQ));
     A(dev_alloc(c, &w.tau_hi, BQ));
     A(dev_alloc(c, &w.cand, BQ * rc));
@@ -715,10 +717,7 @@ static pqhsa_status decode_impl(pqhsa_ctx* c, const void* q, const void* k, cons
     auto tm = [&](int i) {
         return timed ? KTiming{c->ev[2 * i], c->ev[2 * i + 1]} : KTiming{};
     };
-    if (e == hipSuccess) {
-        e = launch_prologue(D, ba, kv, ix, c->w, c->bias, c->epoch + 1, stream, tm(0));
-        if (e == hipSuccess) ++c->epoch;   // the counters advance only if the launch happened
-    }
+    if (e == hipSuccess) e = launch_prologue(D, ba, kv, ix, c->w, c->bias, stream, tm(0));
     if (e == hipSuccess) e = launch_scan(D, ba, ix, c->w, c->scan_nwg, stream, tm(1));
     if (e == hipSuccess) e = launch_select(D, ba, ix, c->w, c->force_fallback, stream, tm(2));
     if (e == hipSuccess && c->variant == PQHSA_VARIANT_BX) e = launch_bx_weights(D, ba, ix, c->w, stream);

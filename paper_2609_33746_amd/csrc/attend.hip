@@ -422,7 +422,12 @@ static_assert(kMergeBatch <= kMergeThreads, "one (m, Z) per thread");
 template <int kGroups>
 __global__ __launch_bounds__(kMergeThreads * kGroups) void merge_kernel(
     Dims D, BatchInts n_exact_parts, const float* __restrict__ partial, int P, int first_bg,
-    int n_bg, float* __restrict__ out) {
+    int n_bg, float* __restrict__ out, uint32_t* epoch) {
+    // the decode call is complete once this launch is: the first row of each
+    // (batch element, KV head) advances the epoch the next call's prologue
+    // reads for it (the dense decode passes none)
+    if (epoch && threadIdx.x == 0 && (blockIdx.x % D.Hq) % D.G == 0)
+        counter_add(epoch + blockIdx.x / D.Hq * D.Hkv + (blockIdx.x % D.Hq) / D.G, 1u);
     __shared__ float2 smz[kGroups][kMergeBatch];
     __shared__ float gm[kGroups], gz[kGroups];
     __shared__ float gn[kGroups > 1 ? kGroups : 1][kMergeThreads];
@@ -527,16 +532,16 @@ hipError_t launch_attend(const Dims& D, const BatchArgs& ba, const KV& kv, const
 }
 
 static hipError_t launch_merge_parts(const Dims& D, const BatchInts& ne, const float* partial,
-                                     int P, int first_bg, int n_bg, float* out, hipStream_t s,
-                                     const KTiming& tm) {
+                                     int P, int first_bg, int n_bg, float* out, uint32_t* epoch,
+                                     hipStream_t s, const KTiming& tm) {
     int most = 0;   // the most partials of a row
     for (int b = 0; b < D.B; ++b) most = ne.v[b] + n_bg > most ? ne.v[b] + n_bg : most;
     if (most <= 2 * kMergeBatch)
         hipExtLaunchKernelGGL(merge_kernel<1>, dim3(D.B * D.Hq), dim3(kMergeThreads), 0, s, tm.start,
-                              tm.stop, 0, D, ne, partial, P, first_bg, n_bg, out);
+                              tm.stop, 0, D, ne, partial, P, first_bg, n_bg, out, epoch);
     else
         hipExtLaunchKernelGGL(merge_kernel<8>, dim3(D.B * D.Hq), dim3(8 * kMergeThreads), 0, s,
-                              tm.start, tm.stop, 0, D, ne, partial, P, first_bg, n_bg, out);
+                              tm.start, tm.stop, 0, D, ne, partial, P, first_bg, n_bg, out, epoch);
     return hipGetLastError();
 }
 
@@ -550,7 +555,7 @@ hipError_t launch_merge(const Dims& D, const BatchArgs& ba, const Work& w, float
     const int n_bgc = (D.n_list + kBgLists - 1) / kBgLists;
     // variant T: the exact partials alone
     return launch_merge_parts(D, ne, w.partial, nsplit_max + n_bgc, nsplit_max,
-                              variant == PQHSA_VARIANT_T ? 0 : n_bgc, out, s, tm);
+                              variant == PQHSA_VARIANT_T ? 0 : n_bgc, out, w.epoch, s, tm);
 }
 
 // ---------------------------------------------------------------------------
@@ -733,7 +738,7 @@ hipError_t launch_dense(const Dims& D, const KV& kv, const BatchInts& lens, floa
     if (e != hipSuccess) return e;
     BatchInts ne;
     for (int b = 0; b < D.B; ++b) ne.v[b] = (lens.v[b] + kDenseRows - 1) / kDenseRows;
-    return launch_merge_parts(D, ne, partial, nsplit_max, 0, 0, out, s, KTiming{});
+    return launch_merge_parts(D, ne, partial, nsplit_max, 0, 0, out, nullptr, s, KTiming{});
 }
 
 }  // namespace pqhsa

@@ -98,7 +98,8 @@ struct Index {
 struct Work {
     float* lut;          // [B, Hkv, M, K, G]   (q^(m) . p_{m,z}) / sqrt(d)
     float* lut_head;     // [B, Hq, M, K]       the same entries, head-major
-    uint32_t* lut_done;  // [B, Hkv] LUT workgroups finished, summed over all calls
+    uint32_t* lut_flag;  // [B, Hkv, prologue_parts] epoch of the last call each LUT part finished
+    uint32_t* epoch;     // [B, Hkv] decode calls completed on this workspace (advanced by the merge)
     float* coarse;       // [B, Hkv, n_list, G] (q . c_j) / sqrt(d)
     float* tau_lo;       // [B, Hq] candidate threshold
     float* tau_hi;       // [B, Hq] largest sampled score (-inf when not sampled)
@@ -150,15 +151,14 @@ hipError_t configure_scan();
 hipError_t configure_select();
 
 // LUT workgroups per (b, kv head) in the prologue: fine parts (8 for Pq8,
-// 2 subspaces each; 1 for Pq4) plus one coarse part per 128 lists. epoch =
-// the number of prologue launches on this workspace so far, this one
-// included: the LUT counters then read epoch * prologue_parts(...).
+// 2 subspaces each; 1 for Pq4) plus one coarse part per kCoarseLists lists.
 __host__ __device__ inline int prologue_fine_parts(int pq_bits) { return pq_bits == 4 ? 1 : 8; }
+constexpr int kCoarseLists = 64;   // lists per coarse LUT workgroup of the prologue
 __host__ __device__ inline int prologue_parts(int n_list, int pq_bits) {
-    return prologue_fine_parts(pq_bits) + (n_list + 127) / 128;
+    return prologue_fine_parts(pq_bits) + (n_list + kCoarseLists - 1) / kCoarseLists;
 }
 hipError_t launch_prologue(const Dims& D, const BatchArgs& ba, const KV& kv, const Index& ix,
-                           const Work& w, float bias, uint32_t epoch, hipStream_t s,
+                           const Work& w, float bias, hipStream_t s,
                            const KTiming& tm = KTiming{});
 // nwg = scan workgroups per (batch element, KV head): enough for the longest R_b
 hipError_t launch_scan(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w, int nwg,

@@ -9,7 +9,9 @@
 // so the tables are built from q / sqrt(d) directly and no normalisation of q
 // is needed (a zero query gives all-zero tables, hence zero scores).
 // Each LUT workgroup writes what the sample role reads with device-scope
-// stores and, once they are acknowledged, increments its KV head's counter.
+// stores and, once they are acknowledged, sets its own flag to the call's
+// epoch (read at kernel start from a device counter that the call's last
+// kernel advances).
 //
 // Sample role, per (batch element, query head) row: scores a stratified
 // sample of the row's list-major positions (contiguous runs of kSampleRun
@@ -38,17 +40,18 @@ namespace pqhsa {
 
 constexpr int kProThreads = 512;
 constexpr int kFineWg = kProThreads / Pq8::K;              // Pq8 subspaces per fine workgroup: 2
-constexpr int kCoarseLists = 128;                          // lists per coarse workgroup
 constexpr int kCoarseGroups = kProThreads / 16;            // 16-lane groups
-constexpr int kCoarsePer = kCoarseLists / kCoarseGroups;   // lists per group: 4
+constexpr int kCoarsePer = kCoarseLists / kCoarseGroups;   // lists per group: 2
 constexpr int kSamplesPer = kMaxSamples / kProThreads;     // samples per thread: 4
 constexpr int kPolls = 2;                                  // counter reads in flight
+constexpr int kPollSleep = 8;                              // between reads: 8 x 64 clocks
+constexpr int kFlagsPerLane = 3;                           // LUT part flags per lane of the poll
+static_assert(8 + kMaxLists / kCoarseLists <= kFlagsPerLane * kWave, "LUT parts per KV head");
 constexpr int kSpinLimit = 1 << 16;                        // poll rounds before giving up
 static_assert(kFineWg * Pq8::K == kProThreads && Pq8::M / kFineWg == 8, "Pq8 fine tiling");
 static_assert(Pq4::LUT_ROW <= kProThreads, "Pq4 fine table: one codeword per thread");
 static_assert(kCoarsePer * kCoarseGroups == kCoarseLists, "coarse tiling");
 static_assert(kSamplesPer * kProThreads == kMaxSamples && kMaxSamples % kSampleRun == 0, "samples");
-static_assert(kCoarseLists == 128, "prologue_parts() counts these");
 
 // (q / sqrt(d)) . c over 16 lanes of 8 dimensions each; every lane of the
 // 16-lane group receives the same sum.
@@ -110,6 +113,8 @@ __device__ __forceinline__ void lut_role(const Dims& D, const T* __restrict__ q,
     const int row0 = b * D.Hq + g * G;
     const T* qg = q + static_cast<int64_t>(row0) * kHeadDim;
     const int tid = threadIdx.x;
+    // this call's epoch for the KV head (see sample_role), needed at the end
+    const uint32_t ep = tid == 0 ? counter_read(w.epoch + bg) + 1u : 0u;
     const int fine_parts = prologue_fine_parts(PQ::BITS);
     if (part < fine_parts) {
         // fine table: one (subspace, codeword) per thread (Pq8: 2 subspaces
@@ -164,15 +169,41 @@ __device__ __forceinline__ void lut_role(const Dims& D, const T* __restrict__ q,
                 store_device(w.coarse + (static_cast<int64_t>(bg) * D.n_list + j) * G + lane16, mine);
         }
     }
-    // publish: every store acknowledged at device scope, then one increment
+    // publish: every store acknowledged at device scope, then this part's
+    // flag takes the call's epoch (a plain device-scope store: the parts of a
+    // KV head never contend on one address)
     wait_vector_memory();
     __syncthreads();
-    if (tid == 0) counter_add(w.lut_done + bg, 1u);
+    if (tid == 0) store_device(w.lut_flag + bg * prologue_parts(D.n_list, PQ::BITS) + part, ep);
+}
+
+// The histogram bin holding the c-th largest entry (1 <= c <= the count in
+// hist), found by one wave: lane l sums the 32 bins of rank 32 l .. 32 l + 31
+// from the top (read in a lane-rotated order, so the lanes of one read hit
+// distinct LDS banks), a wave scan finds the lane whose bins reach c, and a
+// second scan over that lane's 32 bins, one per lane, finds the bin.
+__device__ __forceinline__ int wave_find_bin_desc(const int* hist, int c) {
+    constexpr int PER = kHistBins / kWave;
+    static_assert(PER == 32, "two scans of 32 bins");
+    const int lane = lane_id();
+    int sum = 0;
+#pragma unroll
+    for (int q = 0; q < PER; ++q) sum += hist[kHistBins - 1 - (PER * lane + ((q + lane) & (PER - 1)))];
+    const int incl = wave_incl_scan_i32(sum);
+    const uint64_t r1 = __ballot(incl >= c);
+    const int L = r1 ? __ffsll(static_cast<long long>(r1)) - 1 : kWave - 1;
+    const int before = __builtin_amdgcn_readlane(incl - sum, L);
+    const int v = lane < PER ? hist[kHistBins - 1 - (PER * L + lane)] : 0;
+    const int incl2 = wave_incl_scan_i32(v);
+    const uint64_t r2 = __ballot(lane < PER && before + incl2 >= c);
+    const int M = r2 ? __ffsll(static_cast<long long>(r2)) - 1 : PER - 1;
+    return kHistBins - 1 - (PER * L + M);
 }
 
 struct SampleLds {
     float lut[kLutRowMax];   // the head's fine table [M][K]
     int hist[kHistBins];
+    uint32_t binmin[kHistBins];   // smallest sample key of each bin
     int ready;
     SelectScratch ss;
     BlockScratch bs;
@@ -180,8 +211,8 @@ struct SampleLds {
 
 template <typename T, int G, typename PQ>
 __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, const Index& ix,
-                                            const Work& w, float bias, uint32_t lut_target,
-                                            int row, SampleLds& sm) {
+                                            const Work& w, float bias, int row,
+                                            SampleLds& sm) {
     const int tid = threadIdx.x;
     const int b = row / D.Hq;
     const int h = row % D.Hq;
@@ -198,6 +229,11 @@ __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, 
         }
         return;
     }
+    // this call's epoch for the KV head: one more than the decode calls
+    // completed on this workspace (the last kernel of every call advances the
+    // device counter), so that a replayed graph of the call still tells the
+    // LUT parts' fresh flags from stale ones
+    const uint32_t ep = tid < kWave ? counter_read(w.epoch + bg) + 1u : 0u;
     // 1) the samples: runs of kSampleRun positions, rs apart (rs >= 1),
     //    clipped at the next run; thread tid owns samples u * 512 + tid, so
     //    neighbouring lanes read neighbouring positions (short runs: scores
@@ -224,32 +260,47 @@ __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, 
         rv[u] = ix.norms[base + p];
         jv[u] = static_cast<int>(ix.pos_word[base + p] >> kPosBits);
     }
-    for (int i = tid; i < kHistBins; i += kProThreads) sm.hist[i] = 0;
+    for (int i = tid; i < kHistBins; i += kProThreads) {
+        sm.hist[i] = 0;
+        sm.binmin[i] = 0xffffffffu;
+    }
 
-    // 2) wait for the KV head's LUT parts (bounded), with kPolls reads of
-    //    the counter in flight, spaced out: reads of a line slow the
-    //    increments of it (with G = 8 and four batch elements, four reads in
-    //    flight per row held the last LUT part back by several us)
-    if (tid == 0) {
+    // 2) wait for the KV head's LUT parts (bounded): the first wave reads
+    //    every part's flag (one per lane, a few cache lines), with two such
+    //    reads in flight, spaced out, until all hold this call's epoch
+    if (tid < kWave) {
+        const int parts = prologue_parts(D.n_list, PQ::BITS);
+        const uint32_t* flags = w.lut_flag + bg * parts;
+        uint32_t fv[kPolls][kFlagsPerLane];
+        auto issue = [&](uint32_t (&f)[kFlagsPerLane]) {
+#pragma unroll
+            for (int i = 0; i < kFlagsPerLane; ++i)
+                f[i] = i * kWave + tid < parts ? counter_read(flags + i * kWave + tid) : ep;
+        };
+        auto seen = [&](const uint32_t (&f)[kFlagsPerLane]) {
+            bool mine = true;
+#pragma unroll
+            for (int i = 0; i < kFlagsPerLane; ++i) mine = mine && f[i] == ep;
+            return __ballot(!mine) == 0ull;
+        };
         int ready = 0;
-        uint32_t v[kPolls];
 #pragma unroll
         for (int i = 0; i < kPolls; ++i) {
-            v[i] = counter_read(w.lut_done + bg);
-            __builtin_amdgcn_s_sleep(16);
+            issue(fv[i]);
+            __builtin_amdgcn_s_sleep(kPollSleep);
         }
         for (int it = 0; it < kSpinLimit && !ready; ++it) {
 #pragma unroll
             for (int i = 0; i < kPolls; ++i) {
-                if (!ready && static_cast<int32_t>(v[i] - lut_target) >= 0) ready = 1;
+                if (!ready && seen(fv[i])) ready = 1;
                 if (!ready) {
-                    v[i] = counter_read(w.lut_done + bg);
-                    __builtin_amdgcn_s_sleep(16);
+                    issue(fv[i]);
+                    __builtin_amdgcn_s_sleep(kPollSleep);
                 }
             }
         }
         acquire_device();
-        sm.ready = ready;
+        if (tid == 0) sm.ready = ready;
     }
     __syncthreads();
     if (!sm.ready) {   // tables not seen in time: every token becomes a candidate
@@ -308,32 +359,28 @@ __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, 
     const float fmn = key_float(mn);
     const float range = key_float(mx) - fmn;
     const float scale = (range > 0.0f && range < __builtin_huge_valf()) ? kHistBins / range : 0.0f;
-    int bin[kSamplesPer];
 #pragma unroll
     for (int u = 0; u < kSamplesPer; ++u) {
-        bin[u] = min(static_cast<int>((sc[u] - fmn) * scale), kHistBins - 1);
-        hist_add(sm.hist, static_cast<uint32_t>(ok[u] ? bin[u] : 0), ok[u]);
+        const int bin = min(static_cast<int>((sc[u] - fmn) * scale), kHistBins - 1);
+        hist_add(sm.hist, static_cast<uint32_t>(ok[u] ? bin : 0), ok[u]);
+        if (ok[u]) atomicMin(&sm.binmin[bin], float_key(sc[u]));
     }
     __syncthreads();
-    int above = 0;
-    const int bstar = block_find_bin_desc<kProThreads>(sm.hist, c, above, sm.ss, sm.bs);
-    // the smallest sample of the boundary bin: at least c samples are >= it
-    uint32_t lo = 0xffffffffu, dmx = 0u, dcnt = 0u;
-#pragma unroll
-    for (int u = 0; u < kSamplesPer; ++u)
-        if (ok[u] && bin[u] == bstar) lo = min(lo, float_key(sc[u]));
-    block_min_max_count<kProThreads>(lo, dmx, dcnt, sm.bs);
-    if (tid == 0) {
-        w.tau_lo[row] = key_float(lo) + bias;
-        w.tau_hi[row] = key_float(mx);   // lets the top-k stage fix its bins in advance
+    // 6) one wave: the bin holding the c-th largest sample; tau_lo is that
+    //    bin's smallest sample, so at least c samples are >= it
+    if (tid < kWave) {
+        const int bstar = wave_find_bin_desc(sm.hist, c);
+        if (tid == 0) {
+            w.tau_lo[row] = key_float(sm.binmin[bstar]) + bias;
+            w.tau_hi[row] = key_float(mx);   // lets the top-k stage fix its bins in advance
+        }
     }
 }
 
 template <typename T, int G, typename PQ>
 __global__ __launch_bounds__(kProThreads) void prologue_kernel(Dims D, BatchArgs ba, Index ix,
                                                                const T* __restrict__ q, Work w,
-                                                               float bias, uint32_t lut_target,
-                                                               int n_lut_wg) {
+                                                               float bias, int n_lut_wg) {
     __shared__ SampleLds sm;
     if (static_cast<int>(blockIdx.x) < n_lut_wg) {
         const int per_bg = prologue_parts(D.n_list, PQ::BITS);
@@ -346,50 +393,47 @@ __global__ __launch_bounds__(kProThreads) void prologue_kernel(Dims D, BatchArgs
     // multiple of 8 the G rows of a group share one L2 and its sample loads
     const int s_idx = blockIdx.x - n_lut_wg;
     const int n_grp = D.B * D.Hkv;
-    sample_role<T, G, PQ>(D, ba, ix, w, bias, lut_target, (s_idx % n_grp) * G + s_idx / n_grp, sm);
+    sample_role<T, G, PQ>(D, ba, ix, w, bias, (s_idx % n_grp) * G + s_idx / n_grp, sm);
 }
 
 template <typename T, int G, typename PQ>
 static hipError_t launch_prologue_t(const Dims& D, const BatchArgs& ba, const KV& kv,
-                                    const Index& ix, const Work& w, float bias, uint32_t epoch,
+                                    const Index& ix, const Work& w, float bias,
                                     hipStream_t s, const KTiming& tm) {
     const int per_bg = prologue_parts(D.n_list, PQ::BITS);
     const int n_lut_wg = D.B * D.Hkv * per_bg;
     const int grid = n_lut_wg + D.B * D.Hq;
-    // each call, every LUT workgroup adds 1 to its KV head's counter
-    const uint32_t target = epoch * static_cast<uint32_t>(per_bg);
     hipExtLaunchKernelGGL((prologue_kernel<T, G, PQ>), dim3(grid), dim3(kProThreads), 0, s, tm.start,
-                          tm.stop, 0, D, ba, ix, static_cast<const T*>(kv.q), w, bias, target,
-                          n_lut_wg);
+                          tm.stop, 0, D, ba, ix, static_cast<const T*>(kv.q), w, bias, n_lut_wg);
     return hipGetLastError();
 }
 
 template <typename T, typename PQ>
 static hipError_t launch_prologue_g(const Dims& D, const BatchArgs& ba, const KV& kv,
-                                    const Index& ix, const Work& w, float bias, uint32_t epoch,
+                                    const Index& ix, const Work& w, float bias,
                                     hipStream_t s, const KTiming& tm) {
     switch (D.G) {
-        case 1: return launch_prologue_t<T, 1, PQ>(D, ba, kv, ix, w, bias, epoch, s, tm);
-        case 2: return launch_prologue_t<T, 2, PQ>(D, ba, kv, ix, w, bias, epoch, s, tm);
-        case 4: return launch_prologue_t<T, 4, PQ>(D, ba, kv, ix, w, bias, epoch, s, tm);
-        case 8: return launch_prologue_t<T, 8, PQ>(D, ba, kv, ix, w, bias, epoch, s, tm);
+        case 1: return launch_prologue_t<T, 1, PQ>(D, ba, kv, ix, w, bias, s, tm);
+        case 2: return launch_prologue_t<T, 2, PQ>(D, ba, kv, ix, w, bias, s, tm);
+        case 4: return launch_prologue_t<T, 4, PQ>(D, ba, kv, ix, w, bias, s, tm);
+        case 8: return launch_prologue_t<T, 8, PQ>(D, ba, kv, ix, w, bias, s, tm);
         default: return hipErrorInvalidValue;
     }
 }
 
 template <typename PQ>
 static hipError_t launch_prologue_pq(const Dims& D, const BatchArgs& ba, const KV& kv,
-                                     const Index& ix, const Work& w, float bias, uint32_t epoch,
+                                     const Index& ix, const Work& w, float bias,
                                      hipStream_t s, const KTiming& tm) {
-    return kv.bf16 ? launch_prologue_g<bf16_t, PQ>(D, ba, kv, ix, w, bias, epoch, s, tm)
-                   : launch_prologue_g<float, PQ>(D, ba, kv, ix, w, bias, epoch, s, tm);
+    return kv.bf16 ? launch_prologue_g<bf16_t, PQ>(D, ba, kv, ix, w, bias, s, tm)
+                   : launch_prologue_g<float, PQ>(D, ba, kv, ix, w, bias, s, tm);
 }
 
 hipError_t launch_prologue(const Dims& D, const BatchArgs& ba, const KV& kv, const Index& ix,
-                           const Work& w, float bias, uint32_t epoch, hipStream_t s,
+                           const Work& w, float bias, hipStream_t s,
                            const KTiming& tm) {
-    return D.pq_bits == 4 ? launch_prologue_pq<Pq4>(D, ba, kv, ix, w, bias, epoch, s, tm)
-                          : launch_prologue_pq<Pq8>(D, ba, kv, ix, w, bias, epoch, s, tm);
+    return D.pq_bits == 4 ? launch_prologue_pq<Pq4>(D, ba, kv, ix, w, bias, s, tm)
+                          : launch_prologue_pq<Pq8>(D, ba, kv, ix, w, bias, s, tm);
 }
 
 }  // namespace pqhsa
