@@ -118,8 +118,11 @@ pqhsa_status pqhsa_index_prepare(pqhsa_ctx* ctx, const int32_t* seq_lens,
  *     the codeword nearest to that slice of u - c_a (Section 3.1). Distances
  *     are squared Euclidean in fp32; ties go to the smaller id; a zero key
  *     has r = 0.
- *   - The list means are refreshed over the grown lists (Eq. 4), in
- *     float64: (n_old v_bar + sum of new v) / (n_old + n_new).
+ *   - The list means are refreshed over the grown lists (Eq. 4): the
+ *     context keeps a float64 value sum per list, |R_j| v_bar_j from the
+ *     last prepare or build plus every value added since, and each update
+ *     writes sum / (n_old + n_new) in fp32 (the fp32 means never feed back,
+ *     so many updates do not accumulate rounding).
  *   - The list-major layout becomes that of pqhsa_index_prepare over the
  *     grown lists (lists in increasing id, tokens in increasing id within a
  *     list), merged on the device: old members shift right, new ones append.

@@ -46,6 +46,7 @@ struct pqhsa_ctx {
     float* codebooks = nullptr;
     float* means = nullptr;
     float* glob_mean = nullptr;   // [B, Hkv, d] for variant C
+    double* mean_sums = nullptr;  // [B, Hkv, n_list, d] float64 value sums of the lists (updates)
     uint16_t* tok_list = nullptr; // [B, Hkv, rcap] for variant Bx
     // token-major copy of the index, the source of every list-major rebuild
     std::vector<int32_t> ids_host;   // [B, Hkv, rcap] list id of each token
@@ -305,6 +306,7 @@ pqhsa_status pqhsa_create(const pqhsa_shape* shape, pqhsa_ctx** out) {
     A(dev_alloc(c, &c->codebooks, BG * codebook_floats));
     A(dev_alloc(c, &c->means, BG * L * kHeadDim));
     A(dev_alloc(c, &c->glob_mean, BG * kHeadDim));
+    A(dev_alloc(c, &c->mean_sums, BG * L * kHeadDim));
     A(dev_alloc(c, &c->tok_list, BG * rc));
     A(dev_alloc(c, &c->ids_tm, BG * rc));
     A(dev_alloc(c, &c->codes_tm, BG * rc * static_cast<size_t>(shape->pq_m)));
@@ -403,7 +405,8 @@ static pqhsa_status relayout(pqhsa_ctx* c, const std::vector<int32_t>& lens, hip
     e = launch_prepare_gather(D, c->codes_tm, c->norms_tm, c->index(), c->codes, c->norms, stream);
     if (e != hipSuccess) return hip_fail(c, e, "launching the index gather");
     e = launch_glob_mean(D, c->index(), c->glob_mean, stream);
-    if (e != hipSuccess) return hip_fail(c, e, "launching the global value mean");
+    if (e == hipSuccess) e = launch_init_sums(D, c->loff, c->means, c->mean_sums, stream);
+    if (e != hipSuccess) return hip_fail(c, e, "launching the global value mean and list sums");
     e = hipStreamSynchronize(stream);
     if (e != hipSuccess) return hip_fail(c, e, "preparing the index");
     c->seq_lens = lens;
@@ -506,7 +509,7 @@ pqhsa_status pqhsa_index_update(pqhsa_ctx* c, const int32_t* new_seq_lens, const
     if (e == hipSuccess)
         e = launch_update_lists(D, lo, hi, kv, c->ids_tm, c->loff, c->perm, c->pos_word,
                                 c->loff_alt, c->shift, c->perm_alt, c->pos_alt, c->tok_list,
-                                c->n_r_dev, c->n_seq_dev, c->means, stream);
+                                c->n_r_dev, c->n_seq_dev, c->means, c->mean_sums, stream);
     if (e != hipSuccess) return hip_fail(c, e, "launching the index update");
     std::swap(c->perm, c->perm_alt);
     std::swap(c->pos_word, c->pos_alt);

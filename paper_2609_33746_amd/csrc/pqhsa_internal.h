@@ -226,13 +226,17 @@ hipError_t launch_reseed(const Dims& D, const BatchInts& lo, const BatchInts& hi
 // the list-major rebuild after an update's encode pass (lo, hi as there):
 // new list offsets, per-list shifts [B, Hkv, n_list] and the new perm /
 // pos_word in the *_new buffers (which must not alias the old ones); tok_list,
-// n_r, n_seq and the list means (from the values in kv) updated in place
+// n_r, n_seq, the float64 list value sums and the list means (from the values
+// in kv) updated in place
 hipError_t launch_update_lists(const Dims& D, const BatchInts& lo, const BatchInts& hi,
                                const KV& kv, const int32_t* ids_tm, const int32_t* old_loff,
                                const int32_t* perm_old, const uint32_t* pos_old, int32_t* new_loff,
                                int32_t* shift, int32_t* perm_new, uint32_t* pos_new,
                                uint16_t* tok_list, int32_t* n_r_dev, int32_t* n_seq_dev,
-                               float* means, hipStream_t s);
+                               float* means, double* sums, hipStream_t s);
+// float64 value sums of the lists, |R_j| v_bar_j, for later updates
+hipError_t launch_init_sums(const Dims& D, const int32_t* loff, const float* means, double* sums,
+                            hipStream_t s);
 hipError_t launch_prepare_gather(const Dims& D, const uint8_t* codes_in, const float* norms_in,
                                  const Index& ix, uint8_t* codes_out, float* norms_out,
                                  hipStream_t s);

@@ -11,8 +11,10 @@
 //    list id or codeword index. Writes the token-major list id, codes (one
 //    code per byte) and norm.
 //  * means_update_kernel, after the merge below: one workgroup per (list,
-//    kv head, sequence) folds the new members' values into the list mean,
-//    in float64: v_bar' = (n_old v_bar + sum of new v) / (n_old + n_new).
+//    kv head, sequence) adds the new members' values to the list's float64
+//    value sum and writes the mean v_bar' = sum / (n_old + n_new) in fp32. The
+//    sums start at |R_j| v_bar_j when an index is prepared or built, so the
+//    fp32 means never feed back into later updates and do not drift.
 //
 // The list-major layout is then merged on the device (update_lists_kernel,
 // shift_positions_kernel below) and codes and norms gathered into it.
@@ -308,7 +310,7 @@ template <typename T>
 __global__ __launch_bounds__(kHeadDim) void means_update_kernel(
     Dims D, const T* __restrict__ vcache, int64_t sb, int64_t sh, int64_t sn,
     const int32_t* __restrict__ old_loff, const int32_t* __restrict__ new_loff,
-    const int32_t* __restrict__ perm_new, float* __restrict__ means) {
+    const int32_t* __restrict__ perm_new, float* __restrict__ means, double* __restrict__ sums) {
     const int j = blockIdx.x;
     const int g = blockIdx.y;
     const int b = blockIdx.z;
@@ -321,12 +323,31 @@ __global__ __launch_bounds__(kHeadDim) void means_update_kernel(
     const int x = threadIdx.x;
     const int32_t* perm = perm_new + static_cast<int64_t>(bg) * D.rcap;
     const T* vb = vcache + b * sb + g * sh + x;
-    double s = 0.0;
+    const int64_t at = (static_cast<int64_t>(bg) * D.n_list + j) * kHeadDim + x;
+    double s = sums[at];
     for (int p = end - (n_all - n_old); p < end; ++p)
         s += static_cast<double>(load1<T>(vb + static_cast<int64_t>(perm[p]) * sn));
-    float* mean = means + (static_cast<int64_t>(bg) * D.n_list + j) * kHeadDim + x;
-    *mean = static_cast<float>((static_cast<double>(n_old) * static_cast<double>(*mean) + s) /
-                               static_cast<double>(n_all));
+    sums[at] = s;
+    means[at] = static_cast<float>(s / static_cast<double>(n_all));
+}
+
+// The float64 value sums of the lists from the means of a prepared or built
+// index: sum_j = |R_j| v_bar_j (0 for an empty list).
+__global__ __launch_bounds__(kHeadDim) void init_sums_kernel(Dims D, const int32_t* __restrict__ loff,
+                                                             const float* __restrict__ means,
+                                                             double* __restrict__ sums) {
+    const int j = blockIdx.x;
+    const int bg = blockIdx.y;
+    const int64_t lo = static_cast<int64_t>(bg) * (D.n_list + 1) + j;
+    const int64_t at = (static_cast<int64_t>(bg) * D.n_list + j) * kHeadDim + threadIdx.x;
+    sums[at] = static_cast<double>(loff[lo + 1] - loff[lo]) * static_cast<double>(means[at]);
+}
+
+hipError_t launch_init_sums(const Dims& D, const int32_t* loff, const float* means, double* sums,
+                            hipStream_t s) {
+    hipLaunchKernelGGL(init_sums_kernel, dim3(D.n_list, D.B * D.Hkv), dim3(kHeadDim), 0, s, D, loff,
+                       means, sums);
+    return hipGetLastError();
 }
 
 // List-major rebuild after an update, on the device. The new tokens of a
@@ -421,7 +442,7 @@ hipError_t launch_update_lists(const Dims& D, const BatchInts& lo, const BatchIn
                                const int32_t* perm_old, const uint32_t* pos_old, int32_t* new_loff,
                                int32_t* shift, int32_t* perm_new, uint32_t* pos_new,
                                uint16_t* tok_list, int32_t* n_r_dev, int32_t* n_seq_dev,
-                               float* means, hipStream_t s) {
+                               float* means, double* sums, hipStream_t s) {
     hipLaunchKernelGGL(update_lists_kernel, dim3(D.B * D.Hkv), dim3(kListThreads), 0, s, D, lo, hi,
                        ids_tm, old_loff, new_loff, shift, perm_new, pos_new, tok_list, n_r_dev,
                        n_seq_dev);
@@ -435,11 +456,11 @@ hipError_t launch_update_lists(const Dims& D, const BatchInts& lo, const BatchIn
     if (kv.bf16)
         hipLaunchKernelGGL(means_update_kernel<bf16_t>, grid, dim3(kHeadDim), 0, s, D,
                            static_cast<const bf16_t*>(kv.v), kv.sb, kv.sh, kv.sn, old_loff, new_loff,
-                           perm_new, means);
+                           perm_new, means, sums);
     else
         hipLaunchKernelGGL(means_update_kernel<float>, grid, dim3(kHeadDim), 0, s, D,
                            static_cast<const float*>(kv.v), kv.sb, kv.sh, kv.sn, old_loff, new_loff,
-                           perm_new, means);
+                           perm_new, means, sums);
     return hipGetLastError();
 }
 

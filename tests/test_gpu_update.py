@@ -162,6 +162,31 @@ def test_index_update_128k():
     update_case(synth.workload(2), [256], rows_every=1)
 
 
+def test_many_updates_keep_the_list_means():
+    """64 successive 256-token updates: the list means stay the means over
+    the grown lists (Eq. 4) within 1e-6 (float64 value sums, no drift), and
+    the decode on the grown index meets the operator's bar."""
+    wl = synth.workload(1, max_seq=20000)
+    inp = make(wl, seed=14)
+    n = int(inp["seq_lens"][0])
+    n0 = n - 64 * 256
+    idx_inp = paper_form(inp, [n0])
+    ctx = new_context(idx_inp)
+    for i in range(1, 65):
+        ctx.index_update([n0 + 256 * i], inp["k_cache"], inp["v_cache"])
+    torch.cuda.synchronize()
+    ex = ctx.index_export_tokens()
+    ref = means_over_R(inp, ex["list_ids"], [n])
+    err = float((ex["list_means"] - ref).abs().max())
+    say(f"[update x64] list-mean error {err:.3g}")
+    assert err <= 1e-6
+    after = dict(inp, list_ids=ex["list_ids"], codes=ex["codes"], norms=ex["norms"],
+                 centroids=idx_inp["centroids"], codebooks=idx_inp["codebooks"],
+                 list_means=ex["list_means"], seq_lens=torch.tensor([n], dtype=torch.int32))
+    topk, out, sel, unsel, _ = run(ctx, after)
+    check_rows(after, topk, [(0, h) for h in range(0, wl.n_q_heads, 4)], out, sel, unsel)
+
+
 def test_update_twice_equals_once_and_noop():
     wl = synth.workload(1, max_seq=6000)
     inp = make(wl, seed=8)
