@@ -98,10 +98,12 @@ void pqhsa_destroy(pqhsa_ctx* ctx);
  *   codebooks  float [B, Hkv, M, K, d/M]     p_{m,z}
  *   list_means float [B, Hkv, n_list, d]     v_bar_j, the mean value over
  *                                             all of R_j (Eq. 4); 0 if empty
- * The context copies everything it needs (reordered list-major), so the
- * caller may free these arrays once the call returns: the call synchronises
- * `stream` before returning. Returns INVALID_ARGUMENT for a list id out of
- * range (checked on the host after a device-to-host copy). */
+ * The context copies everything it needs and builds the list-major layout
+ * on the device (a stable counting sort of R_b by list id), so the caller
+ * may free these arrays once the call returns: the call synchronises
+ * `stream` before returning. Returns INVALID_ARGUMENT, naming the first
+ * offending (b, g, i), for a list id of R out of range (checked on the
+ * device); the context is then left unprepared. */
 pqhsa_status pqhsa_index_prepare(pqhsa_ctx* ctx, const int32_t* seq_lens,
                                  const int32_t* list_ids, const uint8_t* codes,
                                  const float* norms, const float* centroids,

@@ -49,8 +49,7 @@ struct pqhsa_ctx {
     double* mean_sums = nullptr;  // [B, Hkv, n_list, d] float64 value sums of the lists (updates)
     uint16_t* tok_list = nullptr; // [B, Hkv, rcap] for variant Bx
     // token-major copy of the index, the source of every list-major rebuild
-    std::vector<int32_t> ids_host;   // [B, Hkv, rcap] list id of each token
-    int32_t* ids_tm = nullptr;       // the same on the device
+    int32_t* ids_tm = nullptr;       // [B, Hkv, rcap] list id of each token
     uint8_t* codes_tm = nullptr;     // [B, Hkv, rcap, M] one code per byte
     float* norms_tm = nullptr;       // [B, Hkv, rcap]
     // the other half of the double-buffered list-major arrays (an update
@@ -61,6 +60,7 @@ struct pqhsa_ctx {
     int32_t* shift = nullptr;        // [B, Hkv, n_list] per-list position shift of an update
     int32_t* n_seq_dev = nullptr;
     int32_t* n_r_dev = nullptr;
+    unsigned long long* bad_id = nullptr;   // first invalid list id found by a prepare
     int scan_nwg = 0;   // scan workgroups per (b, kv head)
 
     // workspace
@@ -317,6 +317,7 @@ pqhsa_status pqhsa_create(const pqhsa_shape* shape, pqhsa_ctx** out) {
     A(dev_alloc(c, &c->shift, BG * L));
     A(dev_alloc(c, &c->n_seq_dev, B));
     A(dev_alloc(c, &c->n_r_dev, B));
+    A(dev_alloc(c, &c->bad_id, 1));
     A(dev_alloc(c, &w.lut, BG * lut_row * G));
     A(dev_alloc(c, &w.coarse, BG * L * G + 16));   // + 16: whole float4 reads at the end
     A(dev_alloc(c, &w.lut_head, BQ * lut_row));
@@ -352,63 +353,53 @@ pqhsa_status pqhsa_create(const pqhsa_shape* shape, pqhsa_ctx** out) {
 }
 
 // Rebuild the list-major layout of every (b, kv head) from the token-major
-// index (c->ids_host, codes_tm, norms_tm) for sequence lengths `lens`: a
-// stable counting sort of R_b by list id on the host (lists in increasing id,
-// tokens in increasing id within a list), then the device gather of codes and
-// norms and the global value means. Synchronises `stream`.
+// index (ids_tm, codes_tm, norms_tm) for sequence lengths `lens`, on the
+// device: a check of the list ids, a stable counting sort of R_b by list id
+// (lists in increasing id, tokens in increasing id within a list), the
+// gather of codes and norms, the global value means and the list sums.
+// Synchronises `stream`; fails (and leaves the context unprepared) when a
+// list id of R lies outside [0, n_list).
 static pqhsa_status relayout(pqhsa_ctx* c, const std::vector<int32_t>& lens, hipStream_t stream) {
     const Dims& D = c->D;
     const int B = D.B, Hkv = D.Hkv, L = D.n_list;
     const size_t rc = D.rcap;
     const size_t BG = static_cast<size_t>(B) * Hkv;
     std::vector<int32_t> nr(B);
-    for (int b = 0; b < B; ++b) nr[b] = lens[b] - D.n_sink - D.n_local;
-    c->prepared = false;
-    hipError_t e = hipSuccess;
-    // stable counting sort of R_b by list id, per (b, kv head)
-    std::vector<int32_t> perm(BG * rc, -1), loff(BG * (L + 1));
-    std::vector<uint32_t> pos_word(BG * rc, 0u);
-    std::vector<uint16_t> tok_list(BG * rc, 0);
-    std::vector<int32_t> cnt(L);
+    BatchInts lo{}, hi{};
+    int max_n = 0;
     for (int b = 0; b < B; ++b) {
-        for (int g = 0; g < Hkv; ++g) {
-            const size_t bg = static_cast<size_t>(b) * Hkv + g;
-            const int32_t* a = c->ids_host.data() + bg * rc;
-            std::fill(cnt.begin(), cnt.end(), 0);
-            for (int i = D.n_sink; i < D.n_sink + nr[b]; ++i) ++cnt[a[i]];
-            int32_t* lo = loff.data() + bg * (L + 1);
-            lo[0] = 0;
-            for (int j = 0; j < L; ++j) lo[j + 1] = lo[j] + cnt[j];
-            std::vector<int32_t> fillp(lo, lo + L);
-            int32_t* pm = perm.data() + bg * rc;
-            uint32_t* pw = pos_word.data() + bg * rc;
-            uint16_t* tl = tok_list.data() + bg * rc;
-            for (int i = D.n_sink; i < D.n_sink + nr[b]; ++i) {
-                tl[i] = static_cast<uint16_t>(a[i]);
-                const int p = fillp[a[i]]++;
-                pm[p] = i;
-                pw[p] = (static_cast<uint32_t>(a[i]) << kPosBits) | static_cast<uint32_t>(i);
-            }
-        }
+        nr[b] = lens[b] - D.n_sink - D.n_local;
+        lo.v[b] = D.n_sink;
+        hi.v[b] = D.n_sink + nr[b];
+        max_n = std::max(max_n, nr[b]);
     }
-
-    auto H2D = [&](void* dst, const void* src, size_t bytes) {
-        if (e == hipSuccess) e = hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, stream);
-    };
-    H2D(c->perm, perm.data(), perm.size() * 4);
-    H2D(c->pos_word, pos_word.data(), pos_word.size() * 4);
-    H2D(c->tok_list, tok_list.data(), tok_list.size() * 2);
-    H2D(c->loff, loff.data(), loff.size() * 4);
-    H2D(c->n_seq_dev, lens.data(), B * 4);
-    H2D(c->n_r_dev, nr.data(), B * 4);
-    if (e != hipSuccess) return hip_fail(c, e, "uploading the prepared index");
+    c->prepared = false;
+    // the empty index the sort merges R into, and a clean Bx list table
+    hipError_t e = hipMemsetAsync(c->loff_alt, 0, BG * (L + 1) * sizeof(int32_t), stream);
+    if (e == hipSuccess) e = hipMemsetAsync(c->tok_list, 0, BG * rc * sizeof(uint16_t), stream);
+    if (e == hipSuccess) e = hipMemsetAsync(c->bad_id, 0xff, sizeof(unsigned long long), stream);
+    if (e == hipSuccess)
+        e = launch_sort_lists(D, lo, hi, max_n, c->ids_tm, c->loff_alt, c->loff, c->shift, c->perm,
+                              c->pos_word, c->tok_list, c->n_r_dev, c->n_seq_dev, c->bad_id, stream);
+    if (e != hipSuccess) return hip_fail(c, e, "launching the list-major sort");
     e = launch_prepare_gather(D, c->codes_tm, c->norms_tm, c->index(), c->codes, c->norms, stream);
     if (e != hipSuccess) return hip_fail(c, e, "launching the index gather");
     e = launch_glob_mean(D, c->index(), c->glob_mean, stream);
     if (e == hipSuccess) e = launch_init_sums(D, c->loff, c->means, c->mean_sums, stream);
     if (e != hipSuccess) return hip_fail(c, e, "launching the global value mean and list sums");
-    e = hipStreamSynchronize(stream);
+    unsigned long long bad = 0;
+    e = hipMemcpyAsync(&bad, c->bad_id, sizeof(bad), hipMemcpyDeviceToHost, stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(stream);
     if (e != hipSuccess) return hip_fail(c, e, "preparing the index");
+    if (bad != ~0ull) {
+        int32_t value = 0;
+        e = hipMemcpy(&value, c->ids_tm + bad, sizeof(value), hipMemcpyDeviceToHost);
+        if (e != hipSuccess) return hip_fail(c, e, "reading an invalid list id");
+        const size_t bg = bad / rc;
+        return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "list_ids[%d][%d][%d] = %d outside [0, n_list = %d)",
+                    static_cast<int>(bg / Hkv), static_cast<int>(bg % Hkv), static_cast<int>(bad % rc),
+                    value, L);
+    }
     c->seq_lens = lens;
     c->cur_len = lens;
     c->n_r = nr;
@@ -433,32 +424,16 @@ pqhsa_status pqhsa_index_prepare(pqhsa_ctx* c, const int32_t* seq_lens, const in
     const Dims& D = c->D;
     const int B = D.B, Hkv = D.Hkv, L = D.n_list;
     const size_t rc = D.rcap;
-    std::vector<int32_t> lens(seq_lens, seq_lens + B), nr(B);
-    for (int b = 0; b < B; ++b) {
+    std::vector<int32_t> lens(seq_lens, seq_lens + B);
+    for (int b = 0; b < B; ++b)
         if (lens[b] < D.n_sink + D.n_local || lens[b] > D.rcap)
             return fail(c, PQHSA_ERR_INVALID_ARGUMENT,
                         "seq_lens[%d] = %d outside [n_sink + n_local, max_seq] = [%d, %d]", b, lens[b],
                         D.n_sink + D.n_local, D.rcap);
-        nr[b] = lens[b] - D.n_sink - D.n_local;
-    }
     c->prepared = false;
 
     const size_t BG = static_cast<size_t>(B) * Hkv;
-    std::vector<int32_t> ids(BG * rc);
-    hipError_t e = hipMemcpyAsync(ids.data(), list_ids, ids.size() * sizeof(int32_t),
-                                  hipMemcpyDeviceToHost, stream);
-    if (e == hipSuccess) e = hipStreamSynchronize(stream);
-    if (e != hipSuccess) return hip_fail(c, e, "copying list ids to the host");
-
-    for (size_t bg = 0; bg < BG; ++bg) {
-        const int b = static_cast<int>(bg / Hkv), g = static_cast<int>(bg % Hkv);
-        const int32_t* a = ids.data() + bg * rc;
-        for (int i = D.n_sink; i < D.n_sink + nr[b]; ++i)
-            if (a[i] < 0 || a[i] >= L)
-                return fail(c, PQHSA_ERR_INVALID_ARGUMENT,
-                            "list_ids[%d][%d][%d] = %d outside [0, n_list = %d)", b, g, i, a[i], L);
-    }
-    e = hipMemcpyAsync(c->ids_tm, list_ids, BG * rc * 4, hipMemcpyDeviceToDevice, stream);
+    hipError_t e = hipMemcpyAsync(c->ids_tm, list_ids, BG * rc * 4, hipMemcpyDeviceToDevice, stream);
     if (e == hipSuccess)
         e = hipMemcpyAsync(c->codes_tm, codes, BG * rc * c->shape.pq_m, hipMemcpyDeviceToDevice, stream);
     if (e == hipSuccess) e = hipMemcpyAsync(c->norms_tm, norms, BG * rc * 4, hipMemcpyDeviceToDevice, stream);
@@ -469,7 +444,6 @@ pqhsa_status pqhsa_index_prepare(pqhsa_ctx* c, const int32_t* seq_lens, const in
     if (e == hipSuccess)
         e = hipMemcpyAsync(c->means, list_means, BG * L * kHeadDim * 4, hipMemcpyDeviceToDevice, stream);
     if (e != hipSuccess) return hip_fail(c, e, "copying the index");
-    c->ids_host.swap(ids);
     return relayout(c, lens, stream);
 }
 
@@ -487,7 +461,6 @@ pqhsa_status pqhsa_index_update(pqhsa_ctx* c, const int32_t* new_seq_lens, const
     st = check_kv(c, k_cache, k_cache, v_cache, kv_strides, k_cache, &kv);
     if (st != PQHSA_OK) return st;
     const Dims& D = c->D;
-    const size_t rc = D.rcap;
     std::vector<int32_t> lens(new_seq_lens, new_seq_lens + D.B);
     BatchInts lo{}, hi{};
     int max_new = 0;
@@ -525,7 +498,7 @@ pqhsa_status pqhsa_index_update(pqhsa_ctx* c, const int32_t* new_seq_lens, const
     c->seq_lens = lens;
     c->cur_len = lens;
     c->scan_nwg = (nr_max + kScanWaves * kSub - 1) / (kScanWaves * kSub);
-    c->prepared = true;   // ids_host now lags the device; only a prepare reads it, after replacing it
+    c->prepared = true;
     return PQHSA_OK;
 }
 
@@ -626,10 +599,6 @@ pqhsa_status pqhsa_index_build(pqhsa_ctx* c, const int32_t* seq_lens, const void
     if (e == hipSuccess) e = hipStreamSynchronize(stream);
     release();
     if (e != hipSuccess) return hip_fail(c, e, "building the index");
-    c->ids_host.resize(BG * rc);   // empty when no prepare came first
-    e = hipMemcpyAsync(c->ids_host.data(), c->ids_tm, BG * rc * 4, hipMemcpyDeviceToHost, stream);
-    if (e == hipSuccess) e = hipStreamSynchronize(stream);
-    if (e != hipSuccess) return hip_fail(c, e, "copying the built lists to the host");
     return relayout(c, lens, stream);
 }
 

@@ -682,7 +682,6 @@ __global__ __launch_bounds__(kAttnThreads) void dense_kernel(Dims D, KV kv, Batc
     const int t1 = min(t0 + kDenseRows, n);
     const int lane16 = threadIdx.x & 15;
     const int stream = threadIdx.x >> 4;
-    const float neg_inf = -__builtin_huge_valf();
     DenseQ<T, G> qv;
     qv.load(static_cast<const T*>(kv.q) + (static_cast<int64_t>(b) * D.Hq + g * G) * kHeadDim +
                 lane16 * 8,

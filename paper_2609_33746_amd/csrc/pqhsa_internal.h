@@ -228,6 +228,16 @@ hipError_t launch_reseed(const Dims& D, const BatchInts& lo, const BatchInts& hi
 // pos_word in the *_new buffers (which must not alias the old ones); tok_list,
 // n_r, n_seq, the float64 list value sums and the list means (from the values
 // in kv) updated in place
+// The list-major layout of R_b = tokens [lo_b, hi_b) built from the
+// token-major list ids on the device: a stable counting sort per (b, kv
+// head), lists in increasing id, tokens in increasing id within a list.
+// zero_loff: [B, Hkv, n_list + 1] zeros. bad: one word set to all ones
+// beforehand; receives the smallest flat index of an id outside [0, n_list).
+hipError_t launch_sort_lists(const Dims& D, const BatchInts& lo, const BatchInts& hi, int max_n,
+                             const int32_t* ids_tm, const int32_t* zero_loff, int32_t* loff,
+                             int32_t* shift, int32_t* perm, uint32_t* pos_word, uint16_t* tok_list,
+                             int32_t* n_r_dev, int32_t* n_seq_dev, unsigned long long* bad,
+                             hipStream_t s);
 hipError_t launch_update_lists(const Dims& D, const BatchInts& lo, const BatchInts& hi,
                                const KV& kv, const int32_t* ids_tm, const int32_t* old_loff,
                                const int32_t* perm_old, const uint32_t* pos_old, int32_t* new_loff,

@@ -387,7 +387,10 @@ __global__ __launch_bounds__(kListThreads) void update_lists_kernel(
     }
     __syncthreads();
     const int32_t* ids = ids_tm + static_cast<int64_t>(bg) * D.rcap;
-    for (int t = t0 + tid; t < t1; t += kListThreads) atomicAdd(&cnt[ids[t]], 1);
+    // list ids are clamped into [0, n_list): a prepare checks them separately
+    // (check_ids_kernel) and fails the call, so an invalid id never indexes LDS
+    auto list_of = [&](int t) { return min(max(ids[t], 0), L - 1); };
+    for (int t = t0 + tid; t < t1; t += kListThreads) atomicAdd(&cnt[list_of(t)], 1);
     __syncthreads();
     lds_exclusive_scan<kListThreads, kScanPer>(cnt, L, wtot);
     const int32_t* ol = old_loff + static_cast<int64_t>(bg) * (L + 1);
@@ -397,7 +400,7 @@ __global__ __launch_bounds__(kListThreads) void update_lists_kernel(
     const int64_t row = static_cast<int64_t>(bg) * D.rcap;
     for (int c0 = t0; c0 < t1; c0 += kListThreads) {
         const int t = c0 + tid;
-        const int j = t < t1 ? ids[t] : -1;
+        const int j = t < t1 ? list_of(t) : -1;
         chunk[tid] = j;
         __syncthreads();
         if (t < t1) {
@@ -435,6 +438,44 @@ __global__ __launch_bounds__(256) void shift_positions_kernel(
         perm_new[row + p] = -1;
         pos_new[row + p] = 0u;
     }
+}
+
+// check_ids_kernel: the smallest flat index (b, g, token) of R whose list id
+// lies outside [0, n_list), by atomicMin into `bad` (left at all ones when
+// every id is valid).
+__global__ __launch_bounds__(256) void check_ids_kernel(Dims D, BatchInts lo, BatchInts hi,
+                                                        const int32_t* __restrict__ ids_tm,
+                                                        unsigned long long* bad) {
+    const int bg = blockIdx.y;
+    const int b = bg / D.Hkv;
+    const int t = lo.v[b] + blockIdx.x * 256 + threadIdx.x;
+    if (t >= hi.v[b]) return;
+    const int64_t at = static_cast<int64_t>(bg) * D.rcap + t;
+    const int32_t j = ids_tm[at];
+    if (j < 0 || j >= D.n_list) atomicMin(bad, static_cast<unsigned long long>(at));
+}
+
+hipError_t launch_sort_lists(const Dims& D, const BatchInts& lo, const BatchInts& hi, int max_n,
+                             const int32_t* ids_tm, const int32_t* zero_loff, int32_t* loff,
+                             int32_t* shift, int32_t* perm, uint32_t* pos_word, uint16_t* tok_list,
+                             int32_t* n_r_dev, int32_t* n_seq_dev, unsigned long long* bad,
+                             hipStream_t s) {
+    if (max_n > 0) {
+        hipLaunchKernelGGL(check_ids_kernel, dim3((max_n + 255) / 256, D.B * D.Hkv), dim3(256), 0, s,
+                           D, lo, hi, ids_tm, bad);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    // a merge into an empty index: every token of R is new (old offsets all
+    // zero, no old positions to move)
+    hipLaunchKernelGGL(update_lists_kernel, dim3(D.B * D.Hkv), dim3(kListThreads), 0, s, D, lo, hi,
+                       ids_tm, zero_loff, loff, shift, perm, pos_word, tok_list, n_r_dev, n_seq_dev);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    // positions past |R_b| are cleared
+    hipLaunchKernelGGL(shift_positions_kernel, dim3((D.rcap + 255) / 256, D.B * D.Hkv), dim3(256), 0,
+                       s, D, lo, hi, shift, nullptr, nullptr, perm, pos_word);
+    return hipGetLastError();
 }
 
 hipError_t launch_update_lists(const Dims& D, const BatchInts& lo, const BatchInts& hi,

@@ -447,12 +447,29 @@ def test_abi_errors_on_gpu():
     with pytest.raises(pqhsa.PQHSAError) as e:
         ctx.decode(inp["q"], inp["k_cache"], inp["v_cache"], [40])
     assert e.value.status == pqhsa.ERR_NOT_PREPARED
+    # list ids of R are checked on the device; the first offending (b, g, i) is named
     bad = inp["list_ids"].clone()
     bad[0, 3, 500] = 16
+    bad[0, 5, 7] = -2
     with pytest.raises(pqhsa.PQHSAError) as e:
         ctx.index_prepare([3000], bad, inp["codes"], inp["norms"], inp["centroids"],
                           inp["codebooks"], inp["list_means"])
     assert e.value.status == pqhsa.ERR_INVALID_ARGUMENT
+    assert "list_ids[0][3][500] = 16" in str(e.value), str(e.value)
+    bad[0, 3, 500] = 0
+    with pytest.raises(pqhsa.PQHSAError) as e:
+        ctx.index_prepare([3000], bad, inp["codes"], inp["norms"], inp["centroids"],
+                          inp["codebooks"], inp["list_means"])
+    assert "list_ids[0][5][7] = -2" in str(e.value), str(e.value)
+    with pytest.raises(pqhsa.PQHSAError) as e:   # still unprepared
+        ctx.decode(inp["q"], inp["k_cache"], inp["v_cache"], [40])
+    assert e.value.status == pqhsa.ERR_NOT_PREPARED
+    # ids outside R (sinks, local window, past N) are not part of the index
+    bad = inp["list_ids"].clone()
+    bad[0, :, :4] = 99
+    bad[0, :, 3000 - 128:] = -5
+    ctx.index_prepare([3000], bad, inp["codes"], inp["norms"], inp["centroids"],
+                      inp["codebooks"], inp["list_means"])
     with pytest.raises(pqhsa.PQHSAError) as e:
         ctx.index_prepare([100], inp["list_ids"], inp["codes"], inp["norms"], inp["centroids"],
                           inp["codebooks"], inp["list_means"])
