@@ -178,6 +178,13 @@ def main() -> int:
                     help="with --profile-only: also run a 256 MiB fp32 elementwise copy "
                          "(torch.neg) 5 times, whose FETCH_SIZE / WRITE_SIZE counters scale "
                          "the operator's counters to bytes")
+    ap.add_argument("--profile-build", action="store_true",
+                    help="run only the k-means index build of the bench workload (one coarse "
+                         "and two subspace iterations), --warmup untimed then --steps timed "
+                         "(for rocprofv3)")
+    ap.add_argument("--summarize-build", nargs=2, metavar=("STATS_CSV", "COMMAND"),
+                    help="print the index build's kernel summary (time per kernel, the "
+                         "assignment passes' TFLOP/s against the fp32 peak) and exit")
     ap.add_argument("--summarize-trace", nargs=2, metavar=("STATS_CSV", "COMMAND"),
                     help="print a summary of a rocprofv3 kernel_stats.csv and exit")
     ap.add_argument("--summarize-pmc", nargs=4, metavar=("STAGE", "FETCH_CSV", "WRITE_CSV", "COMMANDS"),
@@ -185,6 +192,9 @@ def main() -> int:
     args = ap.parse_args()
     if args.summarize_trace:
         sys.stdout.write(summarize_trace(*args.summarize_trace))
+        return 0
+    if args.summarize_build:
+        sys.stdout.write(summarize_build(*args.summarize_build))
         return 0
     if args.summarize_pmc:
         sys.stdout.write(summarize_pmc(*args.summarize_pmc))
@@ -206,6 +216,8 @@ def main() -> int:
     torch.cuda.set_device(dev)
     if args.all_configs:
         return config_sweep(args, dev)
+    if args.profile_build:
+        return build_only(args, dev)
     wl = synth.workload(WORKLOAD)
     log(f"generating {wl.name}")
     inp = synth.make_inputs(wl, seed=args.seed, device=dev)
@@ -401,23 +413,14 @@ def main() -> int:
     # iterations, the paper's setting), wall time of one call
     build = None
     if not args.no_pq4:
-        rng = np.random.default_rng(args.seed)
-        n_list, M_, K_ = wl.n_list, wl.pq_m, wl.pq_ksub
-        ic = np.zeros((wl.batch, wl.n_kv_heads, n_list), np.int32)
-        ip = np.zeros((wl.batch, wl.n_kv_heads, M_, K_), np.int32)
-        for b in range(wl.batch):
-            Rb = np.arange(wl.n_sink, int(inp["seq_lens"][b]) - wl.n_local)
-            for g in range(wl.n_kv_heads):
-                ic[b, g] = rng.choice(Rb, n_list, replace=False)
-                for m in range(M_):
-                    ip[b, g, m] = rng.choice(Rb, K_, replace=False)
+        ic_d, ip_d = build_seeds(inp, args.seed, dev)
         ctxb = pqhsa.context_for(inp)
-        ic_d, ip_d = torch.from_numpy(ic).to(dev), torch.from_numpy(ip).to(dev)
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        ctxb.index_build([int(x) for x in inp["seq_lens"]], kc, vc, ic_d, ip_d, 1, 2)
+        ctxb.index_build([int(x) for x in inp["seq_lens"]], kc, vc, ic_d, ip_d, *BUILD_ITERS)
         torch.cuda.synchronize()
-        build = {"n_iter_coarse": 1, "n_iter_pq": 2, "ms": round(1e3 * (time.perf_counter() - t0), 2)}
+        build = {"n_iter_coarse": BUILD_ITERS[0], "n_iter_pq": BUILD_ITERS[1],
+                 "ms": round(1e3 * (time.perf_counter() - t0), 2)}
         log(f"index build {build['ms']} ms")
         ctxb.close()
 
@@ -595,6 +598,100 @@ def pmc_traffic(stage: str):
         log(f"{os.path.basename(path)} was taken on other sources: traffic unknown")
         return None
     return int(float(vals["traffic_bytes_per_launch"]))
+
+
+BUILD_ITERS = (1, 2)   # coarse and subspace k-means iterations of the measured build
+
+
+def build_seeds(inp, seed, dev):
+    """The starting tokens of the index build: distinct tokens of R_b drawn
+    per (b, g) for the coarse centers and per subspace for the codewords."""
+    import numpy as np
+    import torch
+    wl = inp["workload"]
+    rng = np.random.default_rng(seed)
+    ic = np.zeros((wl.batch, wl.n_kv_heads, wl.n_list), np.int32)
+    ip = np.zeros((wl.batch, wl.n_kv_heads, wl.pq_m, wl.pq_ksub), np.int32)
+    for b in range(wl.batch):
+        Rb = np.arange(wl.n_sink, int(inp["seq_lens"][b]) - wl.n_local)
+        for g in range(wl.n_kv_heads):
+            ic[b, g] = rng.choice(Rb, wl.n_list, replace=False)
+            for m in range(wl.pq_m):
+                ip[b, g, m] = rng.choice(Rb, wl.pq_ksub, replace=False)
+    return torch.from_numpy(ic).to(dev), torch.from_numpy(ip).to(dev)
+
+
+def build_only(args, dev) -> int:
+    """The index build of the bench workload alone, for the profiler."""
+    import torch
+
+    from paper_2609_33746_amd import pqhsa, synth
+    wl = synth.workload(WORKLOAD)
+    inp = synth.make_inputs(wl, seed=args.seed, device=dev)
+    ic_d, ip_d = build_seeds(inp, args.seed, dev)
+    ctx = pqhsa.context_for(inp)
+    lens = [int(x) for x in inp["seq_lens"]]
+    for i in range(args.warmup + args.steps):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        ctx.index_build(lens, inp["k_cache"], inp["v_cache"], ic_d, ip_d, *BUILD_ITERS)
+        torch.cuda.synchronize()
+        log(f"index build {i}: {1e3 * (time.perf_counter() - t0):.2f} ms")
+    ctx.close()
+    return 0
+
+
+def build_flops() -> dict:
+    """Distance arithmetic of one build of the bench workload: 3 flops per
+    dimension of a squared distance (a subtraction and a fused multiply-add).
+    Passes: the norm pass (subspace search against the zero model), each
+    coarse iteration and the final lists (coarse + subspace search), each
+    subspace iteration and the final codes (subspace search)."""
+    from paper_2609_33746_amd import synth
+    wl = synth.workload(WORKLOAD)
+    n = wl.batch * wl.n_kv_heads * (wl.max_seq - wl.n_sink - wl.n_local)   # not ragged
+    dsub = wl.head_dim // wl.pq_m
+    coarse = 3.0 * n * wl.n_list * wl.head_dim
+    sub = 3.0 * n * wl.pq_m * wl.pq_ksub * dsub
+    n_coarse = BUILD_ITERS[0] + 1
+    n_sub = 1 + (BUILD_ITERS[0] + 1) + BUILD_ITERS[1] + 1
+    return {"tokens": n, "coarse_passes": n_coarse, "subspace_passes": n_sub,
+            "flops": n_coarse * coarse + n_sub * sub}
+
+
+FP32_PEAK_TFLOPS = 157.3
+
+
+def summarize_build(stats_csv: str, command: str) -> str:
+    """Kernel summary of index builds (rocprofv3 --kernel-trace --stats), with
+    the assignment passes' arithmetic rate against the fp32 peak."""
+    rows = [r for r in _csv_rows(stats_csv) if "pqhsa" in r["Name"]]
+    fl = build_flops()
+    out = [f"command: {command}",
+           f"build: {BUILD_ITERS[0]} coarse and {BUILD_ITERS[1]} subspace iterations, "
+           f"{fl['tokens']} tokens, {fl['coarse_passes']} coarse and {fl['subspace_passes']} "
+           f"subspace assignment passes per build, {fl['flops'] / 1e12:.3f} TFLOP of distances",
+           "kernel  calls  avg_us  total_us"]
+    enc_ns, enc_calls, tot_ns = 0.0, 0, 0.0
+    for r in rows:
+        name = r["Name"].split("(")[0]
+        calls, tot = int(r["Calls"]), float(r["TotalDurationNs"])
+        out.append(f"{name}  {calls}  {float(r['AverageNs']) / 1e3:.2f}  {tot / 1e3:.1f}")
+        tot_ns += tot
+        if "encode_kernel" in name:
+            enc_ns += tot
+            enc_calls += calls
+    # one assignment launch per subspace search (the coarse searches ride in
+    # two of them)
+    builds = enc_calls / fl["subspace_passes"]
+    if builds:
+        per_build_ms = enc_ns / builds / 1e6
+        tflops = fl["flops"] / (enc_ns / builds * 1e-9) / 1e12
+        out.append(f"builds profiled: {builds:g}; kernel time per build {tot_ns / builds / 1e6:.2f} ms, "
+                   f"of which assignment passes {per_build_ms:.2f} ms")
+        out.append(f"assignment passes: {tflops:.1f} TFLOP/s = {tflops / FP32_PEAK_TFLOPS:.3f} of "
+                   f"the {FP32_PEAK_TFLOPS} TFLOP/s fp32 peak")
+    return "\n".join(out) + "\n"
 
 
 def _csv_rows(path):
