@@ -208,6 +208,28 @@ pqhsa_status pqhsa_decode(pqhsa_ctx* ctx, const void* q, const void* k_cache,
                           const void* v_cache, const int64_t* kv_strides,
                           const int32_t* topk, float* out, hipStream_t stream);
 
+/* The same decode step with the budgets and lengths as DEVICE data, for a
+ * caller that captures the step in a graph and replays it with new values
+ * (Section 3.3: one step per generated token; the problem statement's
+ * decode call takes N_b and k_b per step).
+ *   q, k_cache, v_cache, kv_strides, out: as pqhsa_decode
+ *   seq_lens   DEVICE int32 [B]: N_b of this step. The index covers R_b of
+ *              the last prepare or update; tokens n_sink + |R_b| .. N_b - 1
+ *              are the exact tail, at most n_local + 1024 of them.
+ *   topk       DEVICE int32 [B]: k_b, 0 <= k_b <= min(|R_b|, max_topk)
+ * Both arrays are read by the call's first kernel when the step runs, so a
+ * captured graph takes the values present at each replay. Values outside
+ * the ranges above are clamped on the device (not reported). The call
+ * computes what pqhsa_decode computes for the same N_b and k_b (every
+ * exact-set split of the partial buffer is launched; those past a row's
+ * exact set exit at once). Asynchronous, allocates nothing, never
+ * synchronises, records no stage timing. Requires a prior
+ * pqhsa_index_prepare; INVALID_ARGUMENT for NULL arrays. */
+pqhsa_status pqhsa_decode_device_args(pqhsa_ctx* ctx, const void* q, const void* k_cache,
+                                      const void* v_cache, const int64_t* kv_strides,
+                                      const int32_t* seq_lens, const int32_t* topk, float* out,
+                                      hipStream_t stream);
+
 /* pqhsa_decode reading a paged KV cache in place (the serving setting of
  * Section 4: vLLM-style pages named by a block table). Token t of sequence b
  * and KV head g sits at element

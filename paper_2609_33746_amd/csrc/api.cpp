@@ -61,6 +61,7 @@ struct pqhsa_ctx {
     int32_t* n_seq_dev = nullptr;
     int32_t* n_r_dev = nullptr;
     unsigned long long* bad_id = nullptr;   // first invalid list id found by a prepare
+    BatchArgs* ba_dev = nullptr;   // a device-argument decode's per-sequence integers
     int scan_nwg = 0;   // scan workgroups per (b, kv head)
 
     // workspace
@@ -318,6 +319,7 @@ pqhsa_status pqhsa_create(const pqhsa_shape* shape, pqhsa_ctx** out) {
     A(dev_alloc(c, &c->n_seq_dev, B));
     A(dev_alloc(c, &c->n_r_dev, B));
     A(dev_alloc(c, &c->bad_id, 1));
+    A(dev_alloc(c, &c->ba_dev, 1));
     A(dev_alloc(c, &w.lut, BG * lut_row * G));
     A(dev_alloc(c, &w.coarse, BG * L * G + 16));   // + 16: whole float4 reads at the end
     A(dev_alloc(c, &w.lut_head, BQ * lut_row));
@@ -646,10 +648,14 @@ pqhsa_status pqhsa_index_export_tokens(pqhsa_ctx* c, int32_t* list_ids, uint8_t*
 }
 
 // block_table null: contiguous cache; else paged (see check_pages)
+// The decode call. With dev_lens / dev_topk (device arrays) the budgets and
+// lengths are read on the device by the call's first kernel instead of being
+// checked and passed by value; then no stage timing is recorded.
 static pqhsa_status decode_impl(pqhsa_ctx* c, const void* q, const void* k, const void* v,
                                 const int64_t* strides, const int32_t* block_table,
                                 int32_t max_blocks, int32_t page_size, const int32_t* topk,
-                                float* out, hipStream_t stream, BatchArgs* ba_out) {
+                                float* out, hipStream_t stream, BatchArgs* ba_out,
+                                const int32_t* dev_lens = nullptr, const int32_t* dev_topk = nullptr) {
     if (!c) return fail(nullptr, PQHSA_ERR_INVALID_ARGUMENT, "ctx is NULL");
     c->err.clear();
     if (!c->prepared) return fail(c, PQHSA_ERR_NOT_PREPARED, "pqhsa_index_prepare has not succeeded");
@@ -660,13 +666,21 @@ static pqhsa_status decode_impl(pqhsa_ctx* c, const void* q, const void* k, cons
         st = check_pages(c, block_table, max_blocks, page_size, &kv);
         if (st != PQHSA_OK) return st;
     }
-    if (!topk) return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "topk is NULL");
+    const bool dev_args = dev_topk != nullptr;
+    if (!topk && !dev_args) return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "topk is NULL");
     st = check_device(c);
     if (st != PQHSA_OK) return st;
     const Dims& D = c->D;
     BatchArgs ba{};
     int nsplit = 1;   // exact-set splits this call needs per row
-    for (int b = 0; b < D.B; ++b) {
+    Work w = c->w;
+    if (dev_args) {
+        // every split the partial buffer holds: surplus workgroups exit
+        for (int b = 0; b < D.B; ++b) ba.n_r[b] = c->n_r[b];
+        nsplit = c->nsplit_max;
+        w.ba_dev = c->ba_dev;
+    }
+    for (int b = 0; b < D.B && !dev_args; ++b) {
         if (topk[b] < 0 || topk[b] > c->n_r[b] || topk[b] > c->shape.max_topk)
             return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "topk[%d] = %d outside [0, min(|R_b| = %d, max_topk = %d)]",
                         b, topk[b], c->n_r[b], c->shape.max_topk);
@@ -676,7 +690,7 @@ static pqhsa_status decode_impl(pqhsa_ctx* c, const void* q, const void* k, cons
         nsplit = std::max(nsplit, (D.n_sink + ba.n_tail[b] + topk[b] + kAttnRows - 1) / kAttnRows);
     }
     const Index ix = c->index();
-    const bool timed = c->timing != 0;
+    const bool timed = c->timing != 0 && !dev_args;
     hipError_t e = hipSuccess;
     if (timed && !c->events_made) {
         for (auto& ev : c->ev)
@@ -689,13 +703,15 @@ static pqhsa_status decode_impl(pqhsa_ctx* c, const void* q, const void* k, cons
     auto tm = [&](int i) {
         return timed ? KTiming{c->ev[2 * i], c->ev[2 * i + 1]} : KTiming{};
     };
-    if (e == hipSuccess) e = launch_prologue(D, ba, kv, ix, c->w, c->bias, stream, tm(0));
-    if (e == hipSuccess) e = launch_scan(D, ba, ix, c->w, c->scan_nwg, stream, tm(1));
-    if (e == hipSuccess) e = launch_select(D, ba, ix, c->w, c->force_fallback, stream, tm(2));
-    if (e == hipSuccess && c->variant == PQHSA_VARIANT_BX) e = launch_bx_weights(D, ba, ix, c->w, stream);
+    if (dev_args && e == hipSuccess)
+        e = launch_device_args(D, dev_lens, dev_topk, c->n_r_dev, c->ba_dev, stream);
+    if (e == hipSuccess) e = launch_prologue(D, ba, kv, ix, w, c->bias, stream, tm(0));
+    if (e == hipSuccess) e = launch_scan(D, ba, ix, w, c->scan_nwg, stream, tm(1));
+    if (e == hipSuccess) e = launch_select(D, ba, ix, w, c->force_fallback, stream, tm(2));
+    if (e == hipSuccess && c->variant == PQHSA_VARIANT_BX) e = launch_bx_weights(D, ba, ix, w, stream);
     if (e == hipSuccess)
-        e = launch_attend(D, ba, kv, ix, c->w, nsplit, c->nsplit_max, c->variant, stream, tm(3));
-    if (e == hipSuccess) e = launch_merge(D, ba, c->w, out, c->nsplit_max, c->variant, stream, tm(4));
+        e = launch_attend(D, ba, kv, ix, w, nsplit, c->nsplit_max, c->variant, stream, tm(3));
+    if (e == hipSuccess) e = launch_merge(D, ba, w, out, c->nsplit_max, c->variant, stream, tm(4));
     if (e != hipSuccess) return hip_fail(c, e, "enqueueing the decode kernels");
     c->timed_valid = timed;
     if (ba_out) *ba_out = ba;
@@ -706,6 +722,15 @@ pqhsa_status pqhsa_decode(pqhsa_ctx* c, const void* q, const void* k, const void
                           const int64_t* kv_strides, const int32_t* topk, float* out,
                           hipStream_t stream) {
     return decode_impl(c, q, k, v, kv_strides, nullptr, 0, 0, topk, out, stream, nullptr);
+}
+
+pqhsa_status pqhsa_decode_device_args(pqhsa_ctx* c, const void* q, const void* k, const void* v,
+                                      const int64_t* kv_strides, const int32_t* seq_lens,
+                                      const int32_t* topk, float* out, hipStream_t stream) {
+    if (c && (!seq_lens || !topk))
+        return fail(c, PQHSA_ERR_INVALID_ARGUMENT, "seq_lens and topk must be non-NULL device arrays");
+    return decode_impl(c, q, k, v, kv_strides, nullptr, 0, 0, nullptr, out, stream, nullptr, seq_lens,
+                       topk);
 }
 
 pqhsa_status pqhsa_decode_paged(pqhsa_ctx* c, const void* q, const void* k_pages,

@@ -107,7 +107,7 @@ __device__ __forceinline__ void block_combine(const Online& o, float* sm, float*
 // kBx: variant Bx. The exact role subtracts, at the background's shift, the
 // selected rows weighted by their lists' W_j = M_j / |B n R_j|; the background
 // role weights list j's mean by W_j |R_j| instead of M_j.
-template <typename T, int G, bool kBx>
+template <typename T, int G, bool kBx, bool kDev>
 __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchArgs ba, KV kv,
                                                               Index ix, Work w, int nsplit,
                                                               int nsplit_max, int n_bgc,
@@ -129,9 +129,9 @@ __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchArgs 
         const int b = row / D.Hq;
         const int h = row % D.Hq;
         const int g = h / G;
-        const int k = ba.topk[b];
-        const int n_r = ba.n_r[b];
-        const int n_tail = ba.n_tail[b];   // L_b = [n_sink + |R_b|, N_b)
+        const int k = arg_topk<kDev>(ba, w, b);
+        const int n_r = arg_n_r<kDev>(ba, w, b);
+        const int n_tail = arg_n_tail<kDev>(ba, w, b);   // L_b = [n_sink + |R_b|, N_b)
         const int nE = D.n_sink + n_tail + k;
         const int e0 = split * kAttnRows;
         if (e0 >= nE) return;   // the merge reads only the splits that exist
@@ -354,6 +354,7 @@ __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchArgs 
 // its list's W_j.
 constexpr int kBxThreads = 512;
 
+template <bool kDev>
 __global__ __launch_bounds__(kBxThreads) void bx_weight_kernel(Dims D, BatchArgs ba, Index ix,
                                                                Work w) {
     __shared__ int cnt[kMaxLists];
@@ -363,7 +364,7 @@ __global__ __launch_bounds__(kBxThreads) void bx_weight_kernel(Dims D, BatchArgs
     const int h = row % D.Hq;
     const int hh = h % D.G;
     const int bg = b * D.Hkv + h / D.G;
-    const int k = ba.topk[b];
+    const int k = arg_topk<kDev>(ba, w, b);
     const int32_t* sel = w.sel_tok + static_cast<int64_t>(row) * D.max_topk;
     const uint16_t* tl = ix.tok_list + static_cast<int64_t>(bg) * D.rcap;
     auto list_of = [&](int e) { return static_cast<int>(tl[min(max(sel[e], 0), D.rcap - 1)]); };
@@ -400,8 +401,12 @@ __global__ __launch_bounds__(kBxThreads) void bx_weight_kernel(Dims D, BatchArgs
 
 hipError_t launch_bx_weights(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w,
                              hipStream_t s, const KTiming& tm) {
-    hipExtLaunchKernelGGL(bx_weight_kernel, dim3(D.B * D.Hq), dim3(kBxThreads), 0, s, tm.start,
-                          tm.stop, 0, D, ba, ix, w);
+    if (w.ba_dev)
+        hipExtLaunchKernelGGL(bx_weight_kernel<true>, dim3(D.B * D.Hq), dim3(kBxThreads), 0, s,
+                              tm.start, tm.stop, 0, D, ba, ix, w);
+    else
+        hipExtLaunchKernelGGL(bx_weight_kernel<false>, dim3(D.B * D.Hq), dim3(kBxThreads), 0, s,
+                              tm.start, tm.stop, 0, D, ba, ix, w);
     return hipGetLastError();
 }
 
@@ -422,7 +427,7 @@ static_assert(kMergeBatch <= kMergeThreads, "one (m, Z) per thread");
 template <int kGroups>
 __global__ __launch_bounds__(kMergeThreads * kGroups) void merge_kernel(
     Dims D, BatchInts n_exact_parts, const float* __restrict__ partial, int P, int first_bg,
-    int n_bg, float* __restrict__ out, uint32_t* epoch) {
+    int n_bg, float* __restrict__ out, uint32_t* epoch, const BatchArgs* ba_dev) {
     // the decode call is complete once this launch is: the first row of each
     // (batch element, KV head) advances the epoch the next call's prologue
     // reads for it (the dense decode passes none)
@@ -436,7 +441,10 @@ __global__ __launch_bounds__(kMergeThreads * kGroups) void merge_kernel(
     const int gi = kGroups > 1 ? static_cast<int>(threadIdx.x) / kMergeThreads : 0;
     const int t = kGroups > 1 ? static_cast<int>(threadIdx.x) % kMergeThreads : static_cast<int>(threadIdx.x);
     const float* pr = partial + static_cast<int64_t>(row) * P * kPartStride;
-    const int ne = n_exact_parts.v[b];
+    // exact partials of the row: from the host, or from the call's device
+    // budgets and lengths
+    const int ne = ba_dev ? (D.n_sink + ba_dev->n_tail[b] + ba_dev->topk[b] + kAttnRows - 1) / kAttnRows
+                          : n_exact_parts.v[b];
     const int n_used = ne + n_bg;
     const float neg_inf = -__builtin_huge_valf();
     auto part = [&](int i) { return i < ne ? i : first_bg + (i - ne); };   // i-th used partial
@@ -493,22 +501,30 @@ __global__ __launch_bounds__(kMergeThreads * kGroups) void merge_kernel(
     out[static_cast<int64_t>(row) * kHeadDim + t] = N / Z;
 }
 
-template <typename T, int G>
-static hipError_t launch_attend_t(const Dims& D, const BatchArgs& ba, const KV& kv,
+template <typename T, int G, bool kDev>
+static hipError_t launch_attend_d(const Dims& D, const BatchArgs& ba, const KV& kv,
                                   const Index& ix, const Work& w, int nsplit, int nsplit_max,
                                   int variant, hipStream_t s, const KTiming& tm) {
     const int n_bgc = (D.n_list + kBgLists - 1) / kBgLists;   // the partials' layout
     // variant T has no background: the background workgroups are not launched
     const int grid = D.B * D.Hq * nsplit + (variant == PQHSA_VARIANT_T ? 0 : D.B * D.Hkv * n_bgc);
     if (variant == PQHSA_VARIANT_BX)
-        hipExtLaunchKernelGGL((attend_kernel<T, G, true>), dim3(grid), dim3(kAttnThreads), 0, s,
+        hipExtLaunchKernelGGL((attend_kernel<T, G, true, kDev>), dim3(grid), dim3(kAttnThreads), 0, s,
                               tm.start, tm.stop, 0, D, ba, kv, ix, w, nsplit, nsplit_max, n_bgc,
                               variant);
     else
-        hipExtLaunchKernelGGL((attend_kernel<T, G, false>), dim3(grid), dim3(kAttnThreads), 0, s,
-                              tm.start, tm.stop, 0, D, ba, kv, ix, w, nsplit, nsplit_max, n_bgc,
+        hipExtLaunchKernelGGL((attend_kernel<T, G, false, kDev>), dim3(grid), dim3(kAttnThreads), 0,
+                              s, tm.start, tm.stop, 0, D, ba, kv, ix, w, nsplit, nsplit_max, n_bgc,
                               variant);
     return hipGetLastError();
+}
+
+template <typename T, int G>
+static hipError_t launch_attend_t(const Dims& D, const BatchArgs& ba, const KV& kv,
+                                  const Index& ix, const Work& w, int nsplit, int nsplit_max,
+                                  int variant, hipStream_t s, const KTiming& tm) {
+    return w.ba_dev ? launch_attend_d<T, G, true>(D, ba, kv, ix, w, nsplit, nsplit_max, variant, s, tm)
+                    : launch_attend_d<T, G, false>(D, ba, kv, ix, w, nsplit, nsplit_max, variant, s, tm);
 }
 
 template <typename T>
@@ -533,15 +549,15 @@ hipError_t launch_attend(const Dims& D, const BatchArgs& ba, const KV& kv, const
 
 static hipError_t launch_merge_parts(const Dims& D, const BatchInts& ne, const float* partial,
                                      int P, int first_bg, int n_bg, float* out, uint32_t* epoch,
-                                     hipStream_t s, const KTiming& tm) {
+                                     const BatchArgs* ba_dev, hipStream_t s, const KTiming& tm) {
     int most = 0;   // the most partials of a row
     for (int b = 0; b < D.B; ++b) most = ne.v[b] + n_bg > most ? ne.v[b] + n_bg : most;
     if (most <= 2 * kMergeBatch)
         hipExtLaunchKernelGGL(merge_kernel<1>, dim3(D.B * D.Hq), dim3(kMergeThreads), 0, s, tm.start,
-                              tm.stop, 0, D, ne, partial, P, first_bg, n_bg, out, epoch);
+                              tm.stop, 0, D, ne, partial, P, first_bg, n_bg, out, epoch, ba_dev);
     else
         hipExtLaunchKernelGGL(merge_kernel<8>, dim3(D.B * D.Hq), dim3(8 * kMergeThreads), 0, s,
-                              tm.start, tm.stop, 0, D, ne, partial, P, first_bg, n_bg, out, epoch);
+                              tm.start, tm.stop, 0, D, ne, partial, P, first_bg, n_bg, out, epoch, ba_dev);
     return hipGetLastError();
 }
 
@@ -549,13 +565,15 @@ hipError_t launch_merge(const Dims& D, const BatchArgs& ba, const Work& w, float
                         int nsplit_max, int variant, hipStream_t s, const KTiming& tm) {
     BatchInts ne;
     for (int b = 0; b < D.B; ++b) {
+        // with device budgets the kernel counts the partials itself; the
+        // bound here only picks the launch shape
         const int nE = D.n_sink + ba.n_tail[b] + ba.topk[b];
-        ne.v[b] = (nE + kAttnRows - 1) / kAttnRows;
+        ne.v[b] = w.ba_dev ? nsplit_max : (nE + kAttnRows - 1) / kAttnRows;
     }
     const int n_bgc = (D.n_list + kBgLists - 1) / kBgLists;
     // variant T: the exact partials alone
     return launch_merge_parts(D, ne, w.partial, nsplit_max + n_bgc, nsplit_max,
-                              variant == PQHSA_VARIANT_T ? 0 : n_bgc, out, w.epoch, s, tm);
+                              variant == PQHSA_VARIANT_T ? 0 : n_bgc, out, w.epoch, w.ba_dev, s, tm);
 }
 
 // ---------------------------------------------------------------------------
@@ -737,7 +755,7 @@ hipError_t launch_dense(const Dims& D, const KV& kv, const BatchInts& lens, floa
     if (e != hipSuccess) return e;
     BatchInts ne;
     for (int b = 0; b < D.B; ++b) ne.v[b] = (lens.v[b] + kDenseRows - 1) / kDenseRows;
-    return launch_merge_parts(D, ne, partial, nsplit_max, 0, 0, out, nullptr, s, KTiming{});
+    return launch_merge_parts(D, ne, partial, nsplit_max, 0, 0, out, nullptr, nullptr, s, KTiming{});
 }
 
 }  // namespace pqhsa

@@ -119,7 +119,32 @@ struct Work {
     float* bx_w;         // [B, Hq, n_list] variant Bx: M_j / |B n R_j| (0 when no member
                          //   of list j is unselected)
     float* bx_wsel;      // [B, Hq, max_topk] variant Bx: bx_w of the list of each entry of T
+    // the per-sequence integers of a call whose budgets and lengths are
+    // device data (written by the call's first kernel); null when they
+    // travel by value in BatchArgs
+    const BatchArgs* ba_dev;
 };
+
+// k_b, |R_b| and the tail |L_b| of a call: from the kernel argument, or
+// (kDev, a separate instantiation of each kernel) from device memory when the
+// call's budgets and lengths are device data. A runtime choice between the
+// two made the compiler merge them into one generic load that waits for
+// memory at kernel start (1.3 us per call at 128K).
+template <bool kDev>
+__device__ __forceinline__ int arg_topk(const BatchArgs& ba, const Work& w, int b) {
+    if constexpr (kDev) return w.ba_dev->topk[b];
+    else return ba.topk[b];
+}
+template <bool kDev>
+__device__ __forceinline__ int arg_n_r(const BatchArgs& ba, const Work& w, int b) {
+    if constexpr (kDev) return w.ba_dev->n_r[b];
+    else return ba.n_r[b];
+}
+template <bool kDev>
+__device__ __forceinline__ int arg_n_tail(const BatchArgs& ba, const Work& w, int b) {
+    if constexpr (kDev) return w.ba_dev->n_tail[b];
+    else return ba.n_tail[b];
+}
 
 // The caller's KV cache. Contiguous: token t of (b, g) at b sb + g sh + t sn
 // elements. Paged (bt != null): at bt[b max_blocks + t >> page_shift] sb +
@@ -250,6 +275,12 @@ hipError_t launch_init_sums(const Dims& D, const int32_t* loff, const float* mea
 hipError_t launch_prepare_gather(const Dims& D, const uint8_t* codes_in, const float* norms_in,
                                  const Index& ix, uint8_t* codes_out, float* norms_out,
                                  hipStream_t s);
+// The BatchArgs of a call from device budgets and lengths (one small
+// kernel, the call's first): k_b clamped into [0, min(|R_b|, max_topk)],
+// the tail N_b - n_sink - |R_b| clamped into [0, n_local + kTailGrowth] and
+// into the cache. n_r_dev holds |R_b| of the prepared index.
+hipError_t launch_device_args(const Dims& D, const int32_t* seq_lens, const int32_t* topk,
+                              const int32_t* n_r_dev, BatchArgs* out, hipStream_t s);
 hipError_t launch_debug(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w,
                         int32_t* selected, int32_t* unselected, float* scores,
                         hipStream_t s);

@@ -209,7 +209,7 @@ struct SampleLds {
     BlockScratch bs;
 };
 
-template <typename T, int G, typename PQ>
+template <typename T, int G, typename PQ, bool kDev>
 __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, const Index& ix,
                                             const Work& w, float bias, int row,
                                             SampleLds& sm) {
@@ -219,8 +219,8 @@ __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, 
     const int g = h / G;
     const int hh = h % G;
     const int bg = b * D.Hkv + g;
-    const int n_r = ba.n_r[b];
-    const int k = ba.topk[b];
+    const int n_r = arg_n_r<kDev>(ba, w, b);
+    const int k = arg_topk<kDev>(ba, w, b);
     const float neg_inf = -__builtin_huge_valf();
     if (n_r == 0) {
         if (tid == 0) {
@@ -377,7 +377,7 @@ __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, 
     }
 }
 
-template <typename T, int G, typename PQ>
+template <typename T, int G, typename PQ, bool kDev>
 __global__ __launch_bounds__(kProThreads) void prologue_kernel(Dims D, BatchArgs ba, Index ix,
                                                                const T* __restrict__ q, Work w,
                                                                float bias, int n_lut_wg) {
@@ -393,7 +393,7 @@ __global__ __launch_bounds__(kProThreads) void prologue_kernel(Dims D, BatchArgs
     // multiple of 8 the G rows of a group share one L2 and its sample loads
     const int s_idx = blockIdx.x - n_lut_wg;
     const int n_grp = D.B * D.Hkv;
-    sample_role<T, G, PQ>(D, ba, ix, w, bias, (s_idx % n_grp) * G + s_idx / n_grp, sm);
+    sample_role<T, G, PQ, kDev>(D, ba, ix, w, bias, (s_idx % n_grp) * G + s_idx / n_grp, sm);
 }
 
 template <typename T, int G, typename PQ>
@@ -403,8 +403,14 @@ static hipError_t launch_prologue_t(const Dims& D, const BatchArgs& ba, const KV
     const int per_bg = prologue_parts(D.n_list, PQ::BITS);
     const int n_lut_wg = D.B * D.Hkv * per_bg;
     const int grid = n_lut_wg + D.B * D.Hq;
-    hipExtLaunchKernelGGL((prologue_kernel<T, G, PQ>), dim3(grid), dim3(kProThreads), 0, s, tm.start,
-                          tm.stop, 0, D, ba, ix, static_cast<const T*>(kv.q), w, bias, n_lut_wg);
+    if (w.ba_dev)
+        hipExtLaunchKernelGGL((prologue_kernel<T, G, PQ, true>), dim3(grid), dim3(kProThreads), 0, s,
+                              tm.start, tm.stop, 0, D, ba, ix, static_cast<const T*>(kv.q), w, bias,
+                              n_lut_wg);
+    else
+        hipExtLaunchKernelGGL((prologue_kernel<T, G, PQ, false>), dim3(grid), dim3(kProThreads), 0, s,
+                              tm.start, tm.stop, 0, D, ba, ix, static_cast<const T*>(kv.q), w, bias,
+                              n_lut_wg);
     return hipGetLastError();
 }
 

@@ -93,7 +93,7 @@ constexpr int kScanLutFloats = std::is_same<PQ, Pq4>::value ? kRep4Floats : PQ::
 // stride of the group tables, masses and rows). A group of GT = 8 heads is
 // split over two workgroups of G = 4: their tables then take 80 KB of LDS,
 // so two workgroups share a CU instead of one (the codes are read twice).
-template <int G, int GT, bool kCoarseLds, typename PQ>
+template <int G, int GT, bool kCoarseLds, typename PQ, bool kDev>
 __global__ __launch_bounds__(kScanThreads) void scan_kernel(Dims D, BatchArgs ba, Index ix, Work w,
                                                             int nwg) {
     // the group LUT at a compile-time LDS address (so that an entry address
@@ -115,7 +115,7 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(Dims D, BatchArgs ba
     const int bg = unit / kParts;
     const int b = bg / D.Hkv;
     const int g = bg % D.Hkv;
-    const int n_r = ba.n_r[b];
+    const int n_r = arg_n_r<kDev>(ba, w, b);
     const int sc0 = (blockIdx.x / n_units) * kScanWaves;
     if (sc0 * kSub >= n_r) return;   // surplus workgroup of a shorter sequence
 
@@ -259,28 +259,35 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(Dims D, BatchArgs ba
 
 constexpr size_t kScanLdsMax = 160 * 1024;   // LDS of one workgroup on gfx950
 
-template <int G, int GT, typename PQ>
-static hipError_t launch_scan_t(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w,
+template <int G, int GT, typename PQ, bool kDev>
+static hipError_t launch_scan_d(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w,
                                 int nwg, hipStream_t s, const KTiming& tm) {
     const size_t cf = static_cast<size_t>(kCoarseCapF4<G>) * 16;
     static_assert(kScanLutFloats<PQ, G> * 4 + kCoarseCapF4<G> * 16 <= kScanLdsMax, "LDS budget");
     const dim3 grid(D.B * D.Hkv * (GT / G) * nwg);
     if (D.n_list * G % 4 == 0 && D.n_list * G / 4 <= kCoarseCapF4<G>)
-        hipExtLaunchKernelGGL((scan_kernel<G, GT, true, PQ>), grid, dim3(kScanThreads), cf, s,
+        hipExtLaunchKernelGGL((scan_kernel<G, GT, true, PQ, kDev>), grid, dim3(kScanThreads), cf, s,
                               tm.start, tm.stop, 0, D, ba, ix, w, nwg);
     else
-        hipExtLaunchKernelGGL((scan_kernel<G, GT, false, PQ>), grid, dim3(kScanThreads), 0, s,
+        hipExtLaunchKernelGGL((scan_kernel<G, GT, false, PQ, kDev>), grid, dim3(kScanThreads), 0, s,
                               tm.start, tm.stop, 0, D, ba, ix, w, nwg);
     return hipGetLastError();
 }
 
-template <typename PQ>
+template <int G, int GT, typename PQ>
+static hipError_t launch_scan_t(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w,
+                                int nwg, hipStream_t s, const KTiming& tm) {
+    return w.ba_dev ? launch_scan_d<G, GT, PQ, true>(D, ba, ix, w, nwg, s, tm)
+                    : launch_scan_d<G, GT, PQ, false>(D, ba, ix, w, nwg, s, tm);
+}
+
+template <typename PQ, bool kDev>
 static hipError_t configure_scan_pq() {
     // the coarse table (dynamic) can exceed the default dynamic LDS limit
-    const void* k[] = {reinterpret_cast<const void*>(&scan_kernel<1, 1, true, PQ>),
-                       reinterpret_cast<const void*>(&scan_kernel<2, 2, true, PQ>),
-                       reinterpret_cast<const void*>(&scan_kernel<4, 4, true, PQ>),
-                       reinterpret_cast<const void*>(&scan_kernel<4, 8, true, PQ>)};
+    const void* k[] = {reinterpret_cast<const void*>(&scan_kernel<1, 1, true, PQ, kDev>),
+                       reinterpret_cast<const void*>(&scan_kernel<2, 2, true, PQ, kDev>),
+                       reinterpret_cast<const void*>(&scan_kernel<4, 4, true, PQ, kDev>),
+                       reinterpret_cast<const void*>(&scan_kernel<4, 8, true, PQ, kDev>)};
     const int cap[] = {kCoarseCapF4<1> * 16, kCoarseCapF4<2> * 16, kCoarseCapF4<4> * 16,
                        kCoarseCapF4<4> * 16};
     for (int i = 0; i < 4; ++i) {
@@ -292,8 +299,11 @@ static hipError_t configure_scan_pq() {
 }
 
 hipError_t configure_scan() {
-    const hipError_t e = configure_scan_pq<Pq8>();
-    return e != hipSuccess ? e : configure_scan_pq<Pq4>();
+    hipError_t e = configure_scan_pq<Pq8, false>();
+    if (e == hipSuccess) e = configure_scan_pq<Pq4, false>();
+    if (e == hipSuccess) e = configure_scan_pq<Pq8, true>();
+    if (e == hipSuccess) e = configure_scan_pq<Pq4, true>();
+    return e;
 }
 
 template <typename PQ>

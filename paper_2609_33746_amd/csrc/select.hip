@@ -253,6 +253,7 @@ __device__ __forceinline__ void rescan_row(const Dims& D, const Index& ix, const
     }
 }
 
+template <bool kDev>
 __global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchArgs ba, Index ix,
                                                              Work w, int force_fallback) {
     extern __shared__ uint32_t lds[];
@@ -275,8 +276,8 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchArgs b
     const int g = h / D.G;
     const int hh = h % D.G;
     const int bg = b * D.Hkv + g;
-    const int n_r = ba.n_r[b];
-    const int k = ba.topk[b];
+    const int n_r = arg_n_r<kDev>(ba, w, b);
+    const int k = arg_topk<kDev>(ba, w, b);
     const int nsub = (n_r + kSub - 1) / kSub;
     const int64_t rbase = static_cast<int64_t>(row) * D.rcap;
     const int64_t base = static_cast<int64_t>(bg) * D.rcap;
@@ -460,15 +461,24 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchArgs b
 
 hipError_t launch_select(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w,
                          int force_fallback, hipStream_t s, const KTiming& tm) {
-    hipExtLaunchKernelGGL(select_kernel, dim3(D.B * D.Hq), dim3(kSelThreads), kSelLdsBytes, s,
-                          tm.start, tm.stop, 0, D, ba, ix, w, force_fallback);
+    if (w.ba_dev)
+        hipExtLaunchKernelGGL(select_kernel<true>, dim3(D.B * D.Hq), dim3(kSelThreads), kSelLdsBytes,
+                              s, tm.start, tm.stop, 0, D, ba, ix, w, force_fallback);
+    else
+        hipExtLaunchKernelGGL(select_kernel<false>, dim3(D.B * D.Hq), dim3(kSelThreads), kSelLdsBytes,
+                              s, tm.start, tm.stop, 0, D, ba, ix, w, force_fallback);
     return hipGetLastError();
 }
 
 hipError_t configure_select() {
-    return hipFuncSetAttribute(reinterpret_cast<const void*>(&select_kernel),
-                               hipFuncAttributeMaxDynamicSharedMemorySize,
-                               static_cast<int>(kSelLdsBytes));
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&select_kernel<false>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       static_cast<int>(kSelLdsBytes));
+    if (e == hipSuccess)
+        e = hipFuncSetAttribute(reinterpret_cast<const void*>(&select_kernel<true>),
+                                hipFuncAttributeMaxDynamicSharedMemorySize,
+                                static_cast<int>(kSelLdsBytes));
+    return e;
 }
 
 }  // namespace pqhsa

@@ -57,6 +57,7 @@ def load_library(build_if_missing: bool = True) -> ctypes.CDLL:
         "pqhsa_destroy": ([P], None),
         "pqhsa_index_prepare": ([P] + [P] * 7 + [P], I32),
         "pqhsa_decode": ([P, P, P, P, P, P, P, P], I32),
+        "pqhsa_decode_device_args": ([P, P, P, P, P, P, P, P, P], I32),
         "pqhsa_decode_paged": ([P, P, P, P, P, P, I32, I32, P, P, P], I32),
         "pqhsa_index_update": ([P, P, P, P, P, P], I32),
         "pqhsa_set_lengths": ([P, P], I32),
@@ -202,6 +203,22 @@ class PQHSA:
         out = self._out(q, out)
         self._check(self.lib.pqhsa_decode(self.ctx, _ptr(q), _ptr(k_cache), _ptr(v_cache), strides,
                                           _host_i32(list(topk)), _ptr(out), _stream()))
+        return out
+
+    def decode_device_args(self, q, k_cache, v_cache, seq_lens, topk, out=None):
+        """Decode with N_b and k_b read on the device from int32 GPU tensors
+        [B] when the step runs (so a captured graph takes new values on every
+        replay)."""
+        strides = self._kv(k_cache, v_cache)
+        q = self._dev(q, self.dtype, "q")
+        lens = self._dev(seq_lens, torch.int32, "seq_lens")
+        tk = self._dev(topk, torch.int32, "topk")
+        if lens.numel() != self.shape.batch or tk.numel() != self.shape.batch:
+            raise ValueError("seq_lens and topk must hold one entry per sequence")
+        out = self._out(q, out)
+        self._check(self.lib.pqhsa_decode_device_args(self.ctx, _ptr(q), _ptr(k_cache), _ptr(v_cache),
+                                                      strides, _ptr(lens), _ptr(tk), _ptr(out),
+                                                      _stream()))
         return out
 
     def decode_paged(self, q, k_pages, v_pages, block_table, page_size, topk, out=None):
