@@ -363,6 +363,28 @@ def main() -> int:
         variant_us[name] = round(float(np.mean(t_v)) * 1e3, 3)
     ctx.set_option(pqhsa.OPT_VARIANT, pqhsa.VARIANT_B)
 
+    # the step with N_b and k_b as device data, eagerly and as a replayed
+    # graph of the captured call (new values could be written between replays)
+    lens_d = torch.tensor(lens, dtype=torch.int32, device=dev)
+    topk_d = torch.tensor(topk, dtype=torch.int32, device=dev)
+
+    def dev_call():
+        ctx.decode_device_args(q, kc, vc, lens_d, topk_d, out=out)
+    for _ in range(3):
+        flush()
+        dev_call()
+    t_da, _ = timed(dev_call, max(20, args.steps // 4))
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        dev_call()
+    for _ in range(3):
+        flush()
+        graph.replay()
+    t_gr, _ = timed(graph.replay, max(20, args.steps // 4))
+    device_args = {"us_per_call": round(float(np.mean(t_da)) * 1e3, 3),
+                   "graph_replay_us_per_call": round(float(np.mean(t_gr)) * 1e3, 3)}
+    del graph
+
     # the same call on a paged cache (pages of 16 tokens at random page
     # indices, K and V interleaved in each page as in vLLM's layout)
     paged_us = None
@@ -546,6 +568,7 @@ def main() -> int:
         "cpu_baseline": cpu,
         "variant_us_per_call": variant_us,
         "paged_kv_arm": paged_us,
+        "device_args_arm": device_args,
         "index_update": update,
         "index_build": build,
         "paper_index_arm": pq4 if pq4 is None else dict(
@@ -678,17 +701,18 @@ def summarize_build(stats_csv: str, command: str) -> str:
         calls, tot = int(r["Calls"]), float(r["TotalDurationNs"])
         out.append(f"{name}  {calls}  {float(r['AverageNs']) / 1e3:.2f}  {tot / 1e3:.1f}")
         tot_ns += tot
-        if "encode_kernel" in name:
+        if "encode_kernel" in name or "assign_kernel" in name or "subspace_kernel" in name:
             enc_ns += tot
+        if "encode_kernel" in name or "subspace_kernel" in name:
             enc_calls += calls
-    # one assignment launch per subspace search (the coarse searches ride in
-    # two of them)
+    # one subspace-search launch per subspace pass (the coarse searches are
+    # separate launches on the matrix cores)
     builds = enc_calls / fl["subspace_passes"]
     if builds:
         per_build_ms = enc_ns / builds / 1e6
         tflops = fl["flops"] / (enc_ns / builds * 1e-9) / 1e12
         out.append(f"builds profiled: {builds:g}; kernel time per build {tot_ns / builds / 1e6:.2f} ms, "
-                   f"of which assignment passes {per_build_ms:.2f} ms")
+                   f"of which assignment passes (coarse and subspace searches) {per_build_ms:.2f} ms")
         out.append(f"assignment passes: {tflops:.1f} TFLOP/s = {tflops / FP32_PEAK_TFLOPS:.3f} of "
                    f"the {FP32_PEAK_TFLOPS} TFLOP/s fp32 peak")
     return "\n".join(out) + "\n"

@@ -572,10 +572,14 @@ pqhsa_status pqhsa_index_build(pqhsa_ctx* c, const int32_t* seq_lens, const void
     if (e == hipSuccess) e = hipMemsetAsync(P, 0, BG * c->codebook_floats * 4, stream);
     // keep_lists: the subspace passes reuse the final lists instead of
     // searching the (unchanged) centroids again
+    // the coarse search runs on the matrix cores (launch_assign); the encode
+    // pass then takes each token's list from the ids and searches the codewords
     auto encode = [&](int keep_lists) {
+        if (e == hipSuccess && !keep_lists)
+            e = launch_assign(D, lo, hi, max_n, kv, C, c->ids_tm, bb.dist_c, stream);
         if (e == hipSuccess)
             e = launch_encode(D, lo, hi, max_n, kv, C, P, c->ids_tm, c->codes_tm, c->norms_tm,
-                              bb.dist_c, bb.dist_f, keep_lists, stream);
+                              bb.dist_c, bb.dist_f, 1, stream);
     };
     if (e == hipSuccess) e = hipMemsetAsync(c->ids_tm, 0, BG * rc * 4, stream);
     encode(1);   // the norms of R (codes against the zero model are discarded)

@@ -297,4 +297,191 @@ hipError_t launch_init_centers(const Dims& D, int kind, const KV& kv, const int3
     return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// assign_kernel: the coarse assignment of the build on the matrix cores.
+// ||u - c||^2 = ||u||^2 + ||c||^2 - 2 u . c, and the dot products of a tile
+// of tokens with a chunk of centers are one fp32 matrix product: 128 tokens
+// per workgroup (4 waves x 2 tiles of 16), centers in chunks of 64 (4 tiles
+// of 16), K = 128 dimensions as 32 steps of v_mfma_f32_16x16x4f32. In step
+// j, lane group q (lane / 16) contributes dimension 32 q + j, so each lane
+// reads 32 contiguous floats of its row; rows are 132 floats apart in LDS,
+// which puts the 16 rows of a read on distinct 16-byte bank groups. Every
+// lane keeps a running (distance, center) minimum for the 2 token columns
+// it holds, over the 4 centers of each tile it sees; the 4 lane groups are
+// folded at the end, ties going to the smaller center id. The directions,
+// norms and distances are fp32; the distance of the chosen center is
+// written for the re-seeding.
+// ---------------------------------------------------------------------------
+constexpr int kAsgThreads = 256;
+constexpr int kAsgTok = 128;                  // tokens per workgroup
+constexpr int kAsgCen = 64;                   // centers per chunk
+constexpr int kAsgLd = kHeadDim + 4;          // LDS row stride (floats)
+static_assert(kAsgTok * kAsgLd >= 2 * kAsgCen * kAsgLd, "the token rows hold a center chunk");
+
+typedef float asg_v4f __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ void asg_fold(float& d, int& i, float od, int oi) {
+    if (od < d || (od == d && oi < i)) {
+        d = od;
+        i = oi;
+    }
+}
+
+template <typename T>
+__global__ __launch_bounds__(kAsgThreads) void assign_kernel(Dims D, BatchInts lo, BatchInts hi, KV kv,
+                                                             const float* __restrict__ centroids,
+                                                             int32_t* __restrict__ ids_tm,
+                                                             float* __restrict__ dist_c) {
+    __shared__ float4 rows4[kAsgTok * kAsgLd / 4];   // token rows, then center chunks
+    __shared__ float cn[kAsgCen];                    // ||c||^2 of the chunk's centers
+    __shared__ float un[kAsgTok];                    // ||u||^2 of the tokens
+    float* rows = reinterpret_cast<float*>(rows4);
+    const int b = blockIdx.z;
+    const int g = blockIdx.y;
+    const int t_base = lo.v[b] + static_cast<int>(blockIdx.x) * kAsgTok;
+    if (t_base >= hi.v[b]) return;
+    const int nt = min(kAsgTok, hi.v[b] - t_base);
+    const int bg = b * D.Hkv + g;
+    const int tid = threadIdx.x;
+    const int wave = tid / kWave;
+    const int lane = lane_id();
+    const int col = lane % 16;   // the lane's token column (B) / center row (A) in a tile
+    const int q = lane / 16;     // its lane group: dimensions 32 q .. 32 q + 31
+
+    // 1) the directions u = k / ||k|| of the workgroup's tokens into LDS:
+    //    16 threads per token, 8 dimensions each
+    const T* kb = static_cast<const T*>(kv.k) + b * kv.sb + g * kv.sh;
+#pragma unroll
+    for (int it = 0; it < kAsgTok / 16; ++it) {
+        const int tk = it * 16 + tid / 16;
+        const int x0 = (tid % 16) * 8;
+        float x[8];
+        if (tk < nt) {
+            Load8<T>::run(kb + static_cast<int64_t>(t_base + tk) * kv.sn + x0, x);
+        } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) x[e] = 0.0f;
+        }
+        float ss = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) ss = fmaf(x[e], x[e], ss);
+#pragma unroll
+        for (int off = 1; off < 16; off <<= 1) ss += __shfl_xor(ss, off);
+        const float r = sqrtf(ss);
+        float uu = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            x[e] = r > 0.0f ? x[e] / r : 0.0f;
+            uu = fmaf(x[e], x[e], uu);
+        }
+#pragma unroll
+        for (int off = 1; off < 16; off <<= 1) uu += __shfl_xor(uu, off);
+        if (tid % 16 == 0) un[tk] = uu;
+        float4* dst = reinterpret_cast<float4*>(rows + tk * kAsgLd + x0);
+        dst[0] = make_float4(x[0], x[1], x[2], x[3]);
+        dst[1] = make_float4(x[4], x[5], x[6], x[7]);
+    }
+    __syncthreads();
+    // 2) the B operands: token rows (2 tiles of the wave), 32 dimensions each
+    float bv[2][32];
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt) {
+        const float4* src = reinterpret_cast<const float4*>(rows + (wave * 32 + tt * 16 + col) * kAsgLd + 32 * q);
+#pragma unroll
+        for (int v = 0; v < 8; ++v) {
+            const float4 f = src[v];
+            bv[tt][4 * v] = f.x; bv[tt][4 * v + 1] = f.y; bv[tt][4 * v + 2] = f.z; bv[tt][4 * v + 3] = f.w;
+        }
+    }
+    float best_d[2] = {__builtin_huge_valf(), __builtin_huge_valf()};
+    int best_i[2] = {0, 0};   // a valid id even if every distance is NaN
+
+    // 3) the centers, a chunk of 64 at a time
+    const float* cen = centroids + static_cast<int64_t>(bg) * D.n_list * kHeadDim;
+    for (int c0 = 0; c0 < D.n_list; c0 += kAsgCen) {
+        __syncthreads();   // the previous chunk (or the token rows) is no longer read
+#pragma unroll
+        for (int it = 0; it < kAsgCen * kHeadDim / 4 / kAsgThreads; ++it) {
+            const int idx = it * kAsgThreads + tid;
+            const int ci = idx / 32;          // 32 float4 per center row
+            const int p = idx % 32;
+            const bool ok = c0 + ci < D.n_list;
+            const float4 v = ok ? reinterpret_cast<const float4*>(cen + static_cast<int64_t>(c0 + ci) * kHeadDim)[p]
+                                : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+            float ss = v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+#pragma unroll
+            for (int off = 1; off < 32; off <<= 1) ss += __shfl_xor(ss, off);
+            if (p == 0) cn[ci] = ss;
+            reinterpret_cast<float4*>(rows + ci * kAsgLd)[p] = v;
+        }
+        __syncthreads();
+        // dot products: 4 center tiles x 2 token tiles, 8 independent chains
+        asg_v4f acc[4][2];
+#pragma unroll
+        for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+            for (int tt = 0; tt < 2; ++tt) acc[ct][tt] = asg_v4f{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int j4 = 0; j4 < 8; ++j4) {
+            float4 av[4];
+#pragma unroll
+            for (int ct = 0; ct < 4; ++ct)
+                av[ct] = reinterpret_cast<const float4*>(rows + (ct * 16 + col) * kAsgLd + 32 * q)[j4];
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj)
+#pragma unroll
+                for (int ct = 0; ct < 4; ++ct) {
+                    const float a = jj == 0 ? av[ct].x : jj == 1 ? av[ct].y : jj == 2 ? av[ct].z : av[ct].w;
+#pragma unroll
+                    for (int tt = 0; tt < 2; ++tt)
+                        acc[ct][tt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, bv[tt][4 * j4 + jj],
+                                                                        acc[ct][tt], 0, 0, 0);
+                }
+        }
+        // distances up to ||u||^2: row 4 q + i of tile ct is center c0 + 16 ct + 4 q + i
+#pragma unroll
+        for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int cl = ct * 16 + 4 * q + i;
+                if (c0 + cl < D.n_list) {
+                    const float c2 = cn[cl];
+#pragma unroll
+                    for (int tt = 0; tt < 2; ++tt)
+                        asg_fold(best_d[tt], best_i[tt], fmaf(-2.0f, acc[ct][tt][i], c2), c0 + cl);
+                }
+            }
+    }
+    // 4) the 4 lane groups of a token column, then the outputs
+#pragma unroll
+    for (int tt = 0; tt < 2; ++tt) {
+#pragma unroll
+        for (int off = 16; off < kWave; off <<= 1) {
+            const float od = __shfl_xor(best_d[tt], off);
+            const int oi = __shfl_xor(best_i[tt], off);
+            asg_fold(best_d[tt], best_i[tt], od, oi);
+        }
+        const int tk = wave * 32 + tt * 16 + col;
+        if (q == 0 && tk < nt) {
+            const int64_t at = static_cast<int64_t>(bg) * D.rcap + t_base + tk;
+            ids_tm[at] = best_i[tt];
+            if (dist_c) dist_c[at] = fmaxf(best_d[tt] + un[tk], 0.0f);
+        }
+    }
+}
+
+hipError_t launch_assign(const Dims& D, const BatchInts& lo, const BatchInts& hi, int max_n,
+                         const KV& kv, const float* centroids, int32_t* ids_tm, float* dist_c,
+                         hipStream_t s) {
+    if (max_n <= 0) return hipSuccess;
+    const dim3 grid((max_n + kAsgTok - 1) / kAsgTok, D.Hkv, D.B);
+    if (kv.bf16)
+        hipLaunchKernelGGL(assign_kernel<bf16_t>, grid, dim3(kAsgThreads), 0, s, D, lo, hi, kv,
+                           centroids, ids_tm, dist_c);
+    else
+        hipLaunchKernelGGL(assign_kernel<float>, grid, dim3(kAsgThreads), 0, s, D, lo, hi, kv,
+                           centroids, ids_tm, dist_c);
+    return hipGetLastError();
+}
+
 }  // namespace pqhsa

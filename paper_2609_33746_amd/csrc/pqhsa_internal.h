@@ -221,6 +221,11 @@ hipError_t launch_encode(const Dims& D, const BatchInts& lo, const BatchInts& hi
                          const KV& kv, const float* centroids, const float* codebooks,
                          int32_t* ids_tm, uint8_t* codes_tm, float* norms_tm, float* dist_c,
                          float* dist_f, int keep_lists, hipStream_t s);
+// The coarse assignment of the build on the matrix cores: the nearest center
+// of every token of R_b (ids_tm) and its squared distance (dist_c, or null).
+hipError_t launch_assign(const Dims& D, const BatchInts& lo, const BatchInts& hi, int max_n,
+                         const KV& kv, const float* centroids, int32_t* ids_tm, float* dist_c,
+                         hipStream_t s);
 // the same encoding with one workgroup per token (for a few hundred tokens)
 hipError_t launch_encode_update(const Dims& D, const BatchInts& lo, const BatchInts& hi,
                                 int max_new, const KV& kv, const float* centroids,
