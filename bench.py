@@ -694,12 +694,13 @@ def summarize_build(stats_csv: str, command: str) -> str:
            f"build: {BUILD_ITERS[0]} coarse and {BUILD_ITERS[1]} subspace iterations, "
            f"{fl['tokens']} tokens, {fl['coarse_passes']} coarse and {fl['subspace_passes']} "
            f"subspace assignment passes per build, {fl['flops'] / 1e12:.3f} TFLOP of distances",
-           "kernel  calls  avg_us  total_us"]
+           "kernel  calls  avg_us  min_us  max_us  total_us"]
     enc_ns, enc_calls, tot_ns = 0.0, 0, 0.0
     for r in rows:
         name = r["Name"].split("(")[0]
         calls, tot = int(r["Calls"]), float(r["TotalDurationNs"])
-        out.append(f"{name}  {calls}  {float(r['AverageNs']) / 1e3:.2f}  {tot / 1e3:.1f}")
+        out.append(f"{name}  {calls}  {float(r['AverageNs']) / 1e3:.2f}  {float(r['MinNs']) / 1e3:.2f}  "
+                   f"{float(r['MaxNs']) / 1e3:.2f}  {tot / 1e3:.1f}")
         tot_ns += tot
         if "encode_kernel" in name or "assign_kernel" in name or "subspace_kernel" in name:
             enc_ns += tot

@@ -382,7 +382,9 @@ static pqhsa_status relayout(pqhsa_ctx* c, const std::vector<int32_t>& lens, hip
     if (e == hipSuccess) e = hipMemsetAsync(c->bad_id, 0xff, sizeof(unsigned long long), stream);
     if (e == hipSuccess)
         e = launch_sort_lists(D, lo, hi, max_n, c->ids_tm, c->loff_alt, c->loff, c->shift, c->perm,
-                              c->pos_word, c->tok_list, c->n_r_dev, c->n_seq_dev, c->bad_id, stream);
+                              c->pos_word, c->tok_list, c->n_r_dev, c->n_seq_dev, c->bad_id,
+                              reinterpret_cast<int32_t*>(c->w.comp_key),
+                              static_cast<size_t>(D.B) * D.Hq * rc, stream);
     if (e != hipSuccess) return hip_fail(c, e, "launching the list-major sort");
     e = launch_prepare_gather(D, c->codes_tm, c->norms_tm, c->index(), c->codes, c->norms, stream);
     if (e != hipSuccess) return hip_fail(c, e, "launching the index gather");
@@ -556,11 +558,20 @@ pqhsa_status pqhsa_index_build(pqhsa_ctx* c, const int32_t* seq_lens, const void
     if (e == hipSuccess) e = hipMalloc(&bb.offs, n_offs * 4);
     if (e == hipSuccess) e = hipMalloc(&bb.dist_c, BG * rc * 4);
     if (e == hipSuccess) e = hipMalloc(&bb.dist_f, BG * rc * M * 4);
+    {
+        // the grouping's per-segment counts: problems x segments x keys
+        int max_r = 0;
+        for (int b = 0; b < D.B; ++b) max_r = std::max(max_r, hi.v[b] - lo.v[b]);
+        const size_t nseg = (static_cast<size_t>(max_r) + kBuildSegTok - 1) / kBuildSegTok;
+        const size_t n_hist = std::max<size_t>(1, nseg * std::max(BG * L, BG * M * Kc));
+        if (e == hipSuccess) e = hipMalloc(&bb.seg_hist, n_hist * 4);
+    }
     auto release = [&]() {
         hipFree(bb.order);
         hipFree(bb.offs);
         hipFree(bb.dist_c);
         hipFree(bb.dist_f);
+        hipFree(bb.seg_hist);
     };
     if (e != hipSuccess) {
         release();
@@ -572,14 +583,15 @@ pqhsa_status pqhsa_index_build(pqhsa_ctx* c, const int32_t* seq_lens, const void
     if (e == hipSuccess) e = hipMemsetAsync(P, 0, BG * c->codebook_floats * 4, stream);
     // keep_lists: the subspace passes reuse the final lists instead of
     // searching the (unchanged) centroids again
-    // the coarse search runs on the matrix cores (launch_assign); the encode
-    // pass then takes each token's list from the ids and searches the codewords
+    // an assignment pass on the matrix cores: the coarse search (unless the
+    // lists are kept), then the codeword search of every subspace, which
+    // also writes the norms
     auto encode = [&](int keep_lists) {
         if (e == hipSuccess && !keep_lists)
             e = launch_assign(D, lo, hi, max_n, kv, C, c->ids_tm, bb.dist_c, stream);
         if (e == hipSuccess)
-            e = launch_encode(D, lo, hi, max_n, kv, C, P, c->ids_tm, c->codes_tm, c->norms_tm,
-                              bb.dist_c, bb.dist_f, 1, stream);
+            e = launch_subspace(D, lo, hi, max_n, kv, C, P, c->ids_tm, c->codes_tm, c->norms_tm,
+                                bb.dist_f, stream);
     };
     if (e == hipSuccess) e = hipMemsetAsync(c->ids_tm, 0, BG * rc * 4, stream);
     encode(1);   // the norms of R (codes against the zero model are discarded)

@@ -226,6 +226,12 @@ hipError_t launch_encode(const Dims& D, const BatchInts& lo, const BatchInts& hi
 hipError_t launch_assign(const Dims& D, const BatchInts& lo, const BatchInts& hi, int max_n,
                          const KV& kv, const float* centroids, int32_t* ids_tm, float* dist_c,
                          hipStream_t s);
+// The codeword search of the build on the matrix cores, for tokens whose
+// lists are in ids_tm: norms, codes and the chosen distances (dist_f or null).
+hipError_t launch_subspace(const Dims& D, const BatchInts& lo, const BatchInts& hi, int max_n,
+                           const KV& kv, const float* centroids, const float* codebooks,
+                           const int32_t* ids_tm, uint8_t* codes_tm, float* norms_tm, float* dist_f,
+                           hipStream_t s);
 // the same encoding with one workgroup per token (for a few hundred tokens)
 hipError_t launch_encode_update(const Dims& D, const BatchInts& lo, const BatchInts& hi,
                                 int max_new, const KV& kv, const float* centroids,
@@ -237,9 +243,19 @@ struct BuildBufs {
     int32_t* offs;       // [problems, n_centers + 1]
     float* dist_c;       // [B, Hkv, rcap]
     float* dist_f;       // [B, Hkv, rcap, M]
+    int32_t* seg_hist;   // [problems, segments of 4096 tokens, keys] counts, then first positions
+                         //   (problems with at most 1024 keys)
 };
+constexpr int kBuildSegTok = 4096;   // tokens per segment of the build's grouping
 // kind: 0 coarse centers over directions, 1 codewords over residual slices,
 // 2 list means over values
+// The stable grouping of launch_group for problems of at most 1024 keys,
+// over segments of kBuildSegTok tokens: order [problems, rcap] (tokens by key,
+// in id order within a key) and offs [problems, keys + 1]; seg_hist holds
+// problems x ceil(max |R_b| / kBuildSegTok) x keys ints of scratch.
+hipError_t launch_group_segments(const Dims& D, const BatchInts& lo, const BatchInts& hi, int kind,
+                                 const int32_t* ids_tm, const uint8_t* codes_tm, int32_t* seg_hist,
+                                 int32_t* order, int32_t* offs, hipStream_t s);
 hipError_t launch_group(const Dims& D, const BatchInts& lo, const BatchInts& hi, int kind,
                         const int32_t* ids_tm, const uint8_t* codes_tm, const BuildBufs& bb,
                         hipStream_t s);
@@ -263,11 +279,14 @@ hipError_t launch_reseed(const Dims& D, const BatchInts& lo, const BatchInts& hi
 // head), lists in increasing id, tokens in increasing id within a list.
 // zero_loff: [B, Hkv, n_list + 1] zeros. bad: one word set to all ones
 // beforehand; receives the smallest flat index of an id outside [0, n_list).
+// scratch (scratch_ints ints, may be null): with up to 1024 lists and room for
+// the per-segment counts, the sort runs as the build's segmented grouping
+// over many workgroups per (b, g); otherwise one workgroup per (b, g).
 hipError_t launch_sort_lists(const Dims& D, const BatchInts& lo, const BatchInts& hi, int max_n,
                              const int32_t* ids_tm, const int32_t* zero_loff, int32_t* loff,
                              int32_t* shift, int32_t* perm, uint32_t* pos_word, uint16_t* tok_list,
                              int32_t* n_r_dev, int32_t* n_seq_dev, unsigned long long* bad,
-                             hipStream_t s);
+                             int32_t* scratch, size_t scratch_ints, hipStream_t s);
 hipError_t launch_update_lists(const Dims& D, const BatchInts& lo, const BatchInts& hi,
                                const KV& kv, const int32_t* ids_tm, const int32_t* old_loff,
                                const int32_t* perm_old, const uint32_t* pos_old, int32_t* new_loff,

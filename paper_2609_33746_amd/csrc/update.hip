@@ -455,16 +455,56 @@ __global__ __launch_bounds__(256) void check_ids_kernel(Dims D, BatchInts lo, Ba
     if (j < 0 || j >= D.n_list) atomicMin(bad, static_cast<unsigned long long>(at));
 }
 
+// finish_lists_kernel: after the grouping of R_b by list (perm, loff), the
+// list word of every position, the list of every token (tok_list) and the
+// cleared positions past |R_b|.
+__global__ __launch_bounds__(256) void finish_lists_kernel(Dims D, BatchInts lo, BatchInts hi,
+                                                           const int32_t* __restrict__ ids_tm,
+                                                           int32_t* __restrict__ perm,
+                                                           uint32_t* __restrict__ pos_word,
+                                                           uint16_t* __restrict__ tok_list,
+                                                           int32_t* __restrict__ n_r_dev,
+                                                           int32_t* __restrict__ n_seq_dev) {
+    const int p = blockIdx.x * 256 + threadIdx.x;
+    const int bg = blockIdx.y;
+    const int b = bg / D.Hkv;
+    if (p == 0 && bg % D.Hkv == 0) {
+        n_r_dev[b] = hi.v[b] - D.n_sink;
+        n_seq_dev[b] = hi.v[b] + D.n_local;
+    }
+    if (p >= D.rcap) return;
+    const int64_t row = static_cast<int64_t>(bg) * D.rcap;
+    if (p < hi.v[b] - lo.v[b]) {
+        const int t = perm[row + p];
+        const int j = min(max(ids_tm[row + t], 0), D.n_list - 1);
+        pos_word[row + p] = (static_cast<uint32_t>(j) << kPosBits) | static_cast<uint32_t>(t);
+        tok_list[row + t] = static_cast<uint16_t>(j);
+    } else {
+        perm[row + p] = -1;
+        pos_word[row + p] = 0u;
+    }
+}
+
 hipError_t launch_sort_lists(const Dims& D, const BatchInts& lo, const BatchInts& hi, int max_n,
                              const int32_t* ids_tm, const int32_t* zero_loff, int32_t* loff,
                              int32_t* shift, int32_t* perm, uint32_t* pos_word, uint16_t* tok_list,
                              int32_t* n_r_dev, int32_t* n_seq_dev, unsigned long long* bad,
-                             hipStream_t s) {
+                             int32_t* scratch, size_t scratch_ints, hipStream_t s) {
     if (max_n > 0) {
         hipLaunchKernelGGL(check_ids_kernel, dim3((max_n + 255) / 256, D.B * D.Hkv), dim3(256), 0, s,
                            D, lo, hi, ids_tm, bad);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
+    }
+    const size_t nseg = (static_cast<size_t>(max_n) + kBuildSegTok - 1) / kBuildSegTok;
+    if (D.n_list <= 1024 && scratch &&
+        nseg * static_cast<size_t>(D.B) * D.Hkv * D.n_list <= scratch_ints) {
+        // the build's segmented grouping, many workgroups per (b, g)
+        hipError_t e = launch_group_segments(D, lo, hi, 0, ids_tm, nullptr, scratch, perm, loff, s);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(finish_lists_kernel, dim3((D.rcap + 255) / 256, D.B * D.Hkv), dim3(256), 0, s,
+                           D, lo, hi, ids_tm, perm, pos_word, tok_list, n_r_dev, n_seq_dev);
+        return hipGetLastError();
     }
     // a merge into an empty index: every token of R is new (old offsets all
     // zero, no old positions to move)
