@@ -212,15 +212,6 @@ hipError_t static_scratch(void** ptr);
 // the token-weighted mean of the list means per (b, g): the global value
 // mean over R_b of variant C
 hipError_t launch_glob_mean(const Dims& D, const Index& ix, float* glob, hipStream_t s);
-// encode tokens [lo[b], hi[b]) of every (b, kv head) against the given model
-// (token-major ids / codes / norms); dist_c [B, Hkv, rcap] and dist_f
-// [B, Hkv, rcap, M], when not null, receive the squared distances to the
-// chosen centroid and codewords; keep_lists: take each token's list from
-// ids_tm instead of searching the centroids
-hipError_t launch_encode(const Dims& D, const BatchInts& lo, const BatchInts& hi, int max_new,
-                         const KV& kv, const float* centroids, const float* codebooks,
-                         int32_t* ids_tm, uint8_t* codes_tm, float* norms_tm, float* dist_c,
-                         float* dist_f, int keep_lists, hipStream_t s);
 // The coarse assignment of the build on the matrix cores: the nearest center
 // of every token of R_b (ids_tm) and its squared distance (dist_c, or null).
 hipError_t launch_assign(const Dims& D, const BatchInts& lo, const BatchInts& hi, int max_n,
@@ -232,7 +223,7 @@ hipError_t launch_subspace(const Dims& D, const BatchInts& lo, const BatchInts& 
                            const KV& kv, const float* centroids, const float* codebooks,
                            const int32_t* ids_tm, uint8_t* codes_tm, float* norms_tm, float* dist_f,
                            hipStream_t s);
-// the same encoding with one workgroup per token (for a few hundred tokens)
+// the update's encoding of the tokens leaving the window: one workgroup per token
 hipError_t launch_encode_update(const Dims& D, const BatchInts& lo, const BatchInts& hi,
                                 int max_new, const KV& kv, const float* centroids,
                                 const float* codebooks, int32_t* ids_tm, uint8_t* codes_tm,

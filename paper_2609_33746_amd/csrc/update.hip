@@ -2,9 +2,9 @@
 // are encoded into the existing lists, without re-clustering, and the list
 // means are refreshed over the grown lists.
 //
-//  * encode_one_kernel (one token per workgroup: updates of a few hundred
-//    tokens) and encode_kernel (16 or 64 tokens per workgroup: the build's
-//    passes over all of R): the key is split into
+//  * encode_one_kernel, one token per workgroup (updates of a few hundred
+//    tokens; the build's passes over all of R use the matrix-core search in
+//    the build's source): the key is split into
 //    its norm r and direction u (Section 3.1); u goes to the list with the
 //    nearest centroid, and each slice of the residual u - c_a to its nearest
 //    codeword. Squared Euclidean distances in fp32; ties go to the smaller
@@ -33,172 +33,6 @@ __device__ __forceinline__ void argmin_fold(float& d, int& i, float od, int oi) 
     }
 }
 
-// A workgroup encodes 16 TPT tokens: their directions sit in LDS, the
-// centroids stream through LDS kEncCen rows at a time, and each thread keeps
-// the distances of TPT tokens to 4 centers (lane tx of a 16-lane group takes
-// centers tx, tx + 16, ...; the odd row stride puts those rows on distinct
-// banks). Every distance sums its dimensions in order, one fma per
-// dimension. The per-token argmin folds over the 16 lanes by (distance, id).
-constexpr int kEncCen = 64;
-constexpr int kEncLd = kHeadDim + 1;
-
-// TPT tokens per thread row: 16 TPT tokens per workgroup (64 for the build's
-// passes over all of R, 16 for updates of a few hundred tokens)
-template <typename T, typename PQ, int TPT>
-__global__ __launch_bounds__(kEncThreads) void encode_kernel(
-    Dims D, BatchInts lo, BatchInts hi, const T* __restrict__ kcache, int64_t sb, int64_t sh,
-    int64_t sn, const float* __restrict__ centroids, const float* __restrict__ codebooks,
-    int32_t* __restrict__ ids_tm, uint8_t* __restrict__ codes_tm, float* __restrict__ norms_tm,
-    float* __restrict__ dist_c, float* __restrict__ dist_f, int keep_lists) {
-    constexpr int kSpLd = PQ::DSUB + 1;
-    constexpr int kEncTok = 16 * TPT;
-    __shared__ float su[kEncTok * kEncLd];   // directions, then residuals
-    __shared__ float sc[kEncCen * kEncLd];   // a chunk of centroids
-    __shared__ float sp[PQ::K * kSpLd];      // one subspace's codewords
-    __shared__ float sr[kEncTok];
-    __shared__ int sa[kEncTok];
-    static_assert(kEncThreads == 256 && kEncCen == 64 && 4 * kEncTok <= kEncThreads, "TPT x 4 per thread");
-    const int b = blockIdx.z;
-    const int g = blockIdx.y;
-    const int t_base = lo.v[b] + static_cast<int>(blockIdx.x) * kEncTok;
-    if (t_base >= hi.v[b]) return;
-    const int nt = min(kEncTok, hi.v[b] - t_base);
-    const int bg = b * D.Hkv + g;
-    const int tid = threadIdx.x;
-    const int ty = tid / 16, tx = tid % 16;
-    const T* krow = kcache + b * sb + g * sh;
-
-    for (int i = tid; i < kEncTok * kHeadDim; i += kEncThreads) {
-        const int tk = i / kHeadDim, x = i % kHeadDim;
-        su[tk * kEncLd + x] = tk < nt ? load1<T>(krow + (t_base + tk) * sn + x) : 0.0f;
-    }
-    __syncthreads();
-    if (tid < 4 * kEncTok) {   // r = ||k||: 4 lanes per token, 32 dimensions each
-        const int tk = tid / 4, part = tid % 4;
-        float ss = 0.0f;
-        for (int x = part * 32; x < part * 32 + 32; ++x) ss = fmaf(su[tk * kEncLd + x], su[tk * kEncLd + x], ss);
-        ss += __shfl_xor(ss, 1);
-        ss += __shfl_xor(ss, 2);
-        if (part == 0) sr[tk] = sqrtf(ss);
-    }
-    __syncthreads();
-    for (int i = tid; i < kEncTok * kHeadDim; i += kEncThreads) {
-        const int tk = i / kHeadDim, x = i % kHeadDim;
-        const float r = sr[tk];
-        su[tk * kEncLd + x] = r > 0.0f ? su[tk * kEncLd + x] / r : 0.0f;
-    }
-
-    // nearest centroid (or, with keep_lists, the list already in ids_tm)
-    const float* cen = centroids + static_cast<int64_t>(bg) * D.n_list * kHeadDim;
-    const int64_t row0 = static_cast<int64_t>(bg) * D.rcap + t_base;
-    if (keep_lists) {
-        if (tid < kEncTok) sa[tid] = tid < nt ? ids_tm[row0 + tid] : 0;
-    } else {
-    float bd[TPT];
-    int bi[TPT];
-#pragma unroll
-    for (int i = 0; i < TPT; ++i) {
-        bd[i] = __builtin_huge_valf();
-        bi[i] = 0;   // a valid id even if every distance is NaN
-    }
-    for (int c0 = 0; c0 < D.n_list; c0 += kEncCen) {
-        const int nc = min(kEncCen, D.n_list - c0);
-        __syncthreads();
-        for (int i = tid; i < kEncCen * kHeadDim; i += kEncThreads) {
-            const int cc = i / kHeadDim, x = i % kHeadDim;
-            sc[cc * kEncLd + x] = cc < nc ? cen[static_cast<int64_t>(c0 + cc) * kHeadDim + x] : 0.0f;
-        }
-        __syncthreads();
-        float acc[TPT][4] = {};
-        for (int x = 0; x < kHeadDim; ++x) {
-            float uu[TPT], cv[4];
-#pragma unroll
-            for (int i = 0; i < TPT; ++i) uu[i] = su[(ty * TPT + i) * kEncLd + x];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) cv[j] = sc[(tx + 16 * j) * kEncLd + x];
-#pragma unroll
-            for (int i = 0; i < TPT; ++i)
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const float dd = uu[i] - cv[j];
-                    acc[i][j] = fmaf(dd, dd, acc[i][j]);
-                }
-        }
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-            if (tx + 16 * j < nc)
-#pragma unroll
-                for (int i = 0; i < TPT; ++i) argmin_fold(bd[i], bi[i], acc[i][j], c0 + tx + 16 * j);
-    }
-#pragma unroll
-    for (int i = 0; i < TPT; ++i)
-#pragma unroll
-        for (int off = 8; off > 0; off >>= 1) {
-            const float od = __shfl_xor(bd[i], off);
-            const int oi = __shfl_xor(bi[i], off);
-            argmin_fold(bd[i], bi[i], od, oi);
-        }
-    if (tx == 0)
-#pragma unroll
-        for (int i = 0; i < TPT; ++i) {
-            sa[ty * TPT + i] = bi[i];
-            if (dist_c && ty * TPT + i < nt) dist_c[row0 + ty * TPT + i] = bd[i];
-        }
-    }
-    __syncthreads();
-    for (int i = tid; i < kEncTok * kHeadDim; i += kEncThreads) {
-        const int tk = i / kHeadDim, x = i % kHeadDim;
-        su[tk * kEncLd + x] -= cen[static_cast<int64_t>(sa[tk]) * kHeadDim + x];
-    }
-
-    // nearest codeword of every subspace slice of the residual
-    const float* cb = codebooks + static_cast<int64_t>(bg) * PQ::M * PQ::K * PQ::DSUB;
-    for (int m = 0; m < PQ::M; ++m) {
-        __syncthreads();
-        for (int i = tid; i < PQ::K * PQ::DSUB; i += kEncThreads)
-            sp[(i / PQ::DSUB) * kSpLd + i % PQ::DSUB] = cb[static_cast<int64_t>(m) * PQ::K * PQ::DSUB + i];
-        __syncthreads();
-        float fb[TPT];
-        int fi[TPT];
-#pragma unroll
-        for (int i = 0; i < TPT; ++i) {
-            fb[i] = __builtin_huge_valf();
-            fi[i] = 0;
-        }
-        for (int z = tx; z < PQ::K; z += 16) {
-#pragma unroll
-            for (int i = 0; i < TPT; ++i) {
-                float acc = 0.0f;
-#pragma unroll
-                for (int x = 0; x < PQ::DSUB; ++x) {
-                    const float dd = su[(ty * TPT + i) * kEncLd + m * PQ::DSUB + x] - sp[z * kSpLd + x];
-                    acc = fmaf(dd, dd, acc);
-                }
-                argmin_fold(fb[i], fi[i], acc, z);
-            }
-        }
-#pragma unroll
-        for (int i = 0; i < TPT; ++i)
-#pragma unroll
-            for (int off = 8; off > 0; off >>= 1) {
-                const float od = __shfl_xor(fb[i], off);
-                const int oi = __shfl_xor(fi[i], off);
-                argmin_fold(fb[i], fi[i], od, oi);
-            }
-        if (tx == 0)
-#pragma unroll
-            for (int i = 0; i < TPT; ++i)
-                if (ty * TPT + i < nt) {
-                    codes_tm[(row0 + ty * TPT + i) * PQ::M + m] = static_cast<uint8_t>(fi[i]);
-                    if (dist_f) dist_f[(row0 + ty * TPT + i) * PQ::M + m] = fb[i];
-                }
-    }
-    if (tid < nt) {
-        ids_tm[row0 + tid] = sa[tid];
-        norms_tm[row0 + tid] = sr[tid];
-    }
-}
-
 // argmin over the 64 lanes of a wave by (distance, id)
 __device__ __forceinline__ void wave_argmin64(float& d, int& i) {
 #pragma unroll
@@ -211,7 +45,7 @@ __device__ __forceinline__ void wave_argmin64(float& d, int& i) {
 
 // One workgroup per token: for updates of a few hundred tokens, where
 // 64-token tiles would leave most of the chip idle. The same choices as
-// encode_kernel up to fp32 rounding order.
+// the build's search up to fp32 rounding order.
 template <typename T, typename PQ>
 __global__ __launch_bounds__(kEncThreads) void encode_one_kernel(
     Dims D, BatchInts lo, BatchInts hi, const T* __restrict__ kcache, int64_t sb, int64_t sh,
@@ -561,32 +395,6 @@ hipError_t launch_encode_update(const Dims& D, const BatchInts& lo, const BatchI
         if (D.pq_bits == 4) PQHSA_ENC1(float, Pq4); else PQHSA_ENC1(float, Pq8);
     }
 #undef PQHSA_ENC1
-    return hipGetLastError();
-}
-
-hipError_t launch_encode(const Dims& D, const BatchInts& lo, const BatchInts& hi, int max_new,
-                         const KV& kv, const float* centroids, const float* codebooks,
-                         int32_t* ids_tm, uint8_t* codes_tm, float* norms_tm, float* dist_c,
-                         float* dist_f, int keep_lists, hipStream_t s) {
-    if (max_new <= 0) return hipSuccess;
-    // 64-token tiles reuse each centroid chunk 64 times; below about a
-    // thousand such tiles the chip is better filled by 16-token tiles
-    const bool big = static_cast<int64_t>(max_new) * D.Hkv * D.B >= 64 * 1024;
-    const int tok = big ? 64 : 16;
-    const dim3 grid((max_new + tok - 1) / tok, D.Hkv, D.B);
-#define PQHSA_ENC(TT, PQT, TP)                                                                   \
-    hipLaunchKernelGGL((encode_kernel<TT, PQT, TP>), grid, dim3(kEncThreads), 0, s, D, lo, hi,    \
-                       static_cast<const TT*>(kv.k), kv.sb, kv.sh, kv.sn, centroids, codebooks,   \
-                       ids_tm, codes_tm, norms_tm, dist_c, dist_f, keep_lists)
-    const bool p4 = D.pq_bits == 4;
-    if (kv.bf16) {
-        if (p4) { if (big) PQHSA_ENC(bf16_t, Pq4, 4); else PQHSA_ENC(bf16_t, Pq4, 1); }
-        else { if (big) PQHSA_ENC(bf16_t, Pq8, 4); else PQHSA_ENC(bf16_t, Pq8, 1); }
-    } else {
-        if (p4) { if (big) PQHSA_ENC(float, Pq4, 4); else PQHSA_ENC(float, Pq4, 1); }
-        else { if (big) PQHSA_ENC(float, Pq8, 4); else PQHSA_ENC(float, Pq8, 1); }
-    }
-#undef PQHSA_ENC
     return hipGetLastError();
 }
 
