@@ -695,6 +695,8 @@ static pqhsa_status decode_impl(pqhsa_ctx* c, const void* q, const void* k, cons
         for (int b = 0; b < D.B; ++b) ba.n_r[b] = c->n_r[b];
         nsplit = c->nsplit_max;
         w.ba_dev = c->ba_dev;
+        w.dev_lens = dev_lens;
+        w.dev_topk = dev_topk;
     }
     for (int b = 0; b < D.B && !dev_args; ++b) {
         if (topk[b] < 0 || topk[b] > c->n_r[b] || topk[b] > c->shape.max_topk)
@@ -719,8 +721,6 @@ static pqhsa_status decode_impl(pqhsa_ctx* c, const void* q, const void* k, cons
     auto tm = [&](int i) {
         return timed ? KTiming{c->ev[2 * i], c->ev[2 * i + 1]} : KTiming{};
     };
-    if (dev_args && e == hipSuccess)
-        e = launch_device_args(D, dev_lens, dev_topk, c->n_r_dev, c->ba_dev, stream);
     if (e == hipSuccess) e = launch_prologue(D, ba, kv, ix, w, c->bias, stream, tm(0));
     if (e == hipSuccess) e = launch_scan(D, ba, ix, w, c->scan_nwg, stream, tm(1));
     if (e == hipSuccess) e = launch_select(D, ba, ix, w, c->force_fallback, stream, tm(2));

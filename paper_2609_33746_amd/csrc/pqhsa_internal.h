@@ -119,11 +119,28 @@ struct Work {
     float* bx_w;         // [B, Hq, n_list] variant Bx: M_j / |B n R_j| (0 when no member
                          //   of list j is unselected)
     float* bx_wsel;      // [B, Hq, max_topk] variant Bx: bx_w of the list of each entry of T
-    // the per-sequence integers of a call whose budgets and lengths are
-    // device data (written by the call's first kernel); null when they
-    // travel by value in BatchArgs
-    const BatchArgs* ba_dev;
+    // A call whose budgets and lengths are device data: the caller's N_b and
+    // k_b (dev_lens, dev_topk), and the call's clamped per-sequence integers
+    // (ba_dev), written by the prologue for the later kernels. All null when
+    // the integers travel by value in BatchArgs.
+    BatchArgs* ba_dev;
+    const int32_t* dev_lens;
+    const int32_t* dev_topk;
 };
+
+// The integers of batch element b in a device-argument call, from |R_b| of
+// the prepared index and the caller's N_b and k_b: k_b clamped into
+// [0, min(|R_b|, max_topk)], the tail N_b - n_sink - |R_b| into
+// [0, n_local + kTailGrowth] and into the cache. Device data are not
+// validated, so clamping is what keeps every kernel inside its buffers.
+struct SeqArgs {
+    int topk, n_r, n_tail;
+};
+__device__ __forceinline__ SeqArgs clamp_seq_args(const Dims& D, int n_r, int seq_len, int topk) {
+    const int tail_cap = min(D.n_local + kTailGrowth, D.rcap - D.n_sink - n_r);
+    return SeqArgs{min(max(topk, 0), min(n_r, D.max_topk)), n_r,
+                   min(max(seq_len - D.n_sink - n_r, 0), tail_cap)};
+}
 
 // k_b, |R_b| and the tail |L_b| of a call: from the kernel argument, or
 // (kDev, a separate instantiation of each kernel) from device memory when the
@@ -290,12 +307,6 @@ hipError_t launch_init_sums(const Dims& D, const int32_t* loff, const float* mea
 hipError_t launch_prepare_gather(const Dims& D, const uint8_t* codes_in, const float* norms_in,
                                  const Index& ix, uint8_t* codes_out, float* norms_out,
                                  hipStream_t s);
-// The BatchArgs of a call from device budgets and lengths (one small
-// kernel, the call's first): k_b clamped into [0, min(|R_b|, max_topk)],
-// the tail N_b - n_sink - |R_b| clamped into [0, n_local + kTailGrowth] and
-// into the cache. n_r_dev holds |R_b| of the prepared index.
-hipError_t launch_device_args(const Dims& D, const int32_t* seq_lens, const int32_t* topk,
-                              const int32_t* n_r_dev, BatchArgs* out, hipStream_t s);
 hipError_t launch_debug(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w,
                         int32_t* selected, int32_t* unselected, float* scores,
                         hipStream_t s);

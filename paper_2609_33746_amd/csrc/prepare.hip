@@ -215,27 +215,4 @@ hipError_t launch_debug(const Dims& D, const BatchArgs& ba, const Index& ix, con
     return hipSuccess;
 }
 
-// The BatchArgs of a call whose budgets and lengths are device data, so
-// that a captured graph of the call reads new values on every replay. Values
-// out of range are clamped, which keeps every later kernel inside its
-// buffers (device data are not validated).
-__global__ __launch_bounds__(256) void device_args_kernel(Dims D, const int32_t* __restrict__ seq_lens,
-                                                          const int32_t* __restrict__ topk,
-                                                          const int32_t* __restrict__ n_r_dev,
-                                                          BatchArgs* __restrict__ out) {
-    for (int b = threadIdx.x; b < D.B; b += blockDim.x) {
-        const int n_r = n_r_dev[b];
-        const int tail_cap = min(D.n_local + kTailGrowth, D.rcap - D.n_sink - n_r);
-        out->n_r[b] = n_r;
-        out->n_tail[b] = min(max(seq_lens[b] - D.n_sink - n_r, 0), tail_cap);
-        out->topk[b] = min(max(topk[b], 0), min(n_r, D.max_topk));
-    }
-}
-
-hipError_t launch_device_args(const Dims& D, const int32_t* seq_lens, const int32_t* topk,
-                              const int32_t* n_r_dev, BatchArgs* out, hipStream_t s) {
-    hipLaunchKernelGGL(device_args_kernel, dim3(1), dim3(256), 0, s, D, seq_lens, topk, n_r_dev, out);
-    return hipGetLastError();
-}
-
 }  // namespace pqhsa

@@ -23,6 +23,10 @@
 // finishes), then reads its head's fine table and the coarse terms of its
 // samples.
 //
+// When a call's budgets and lengths are device data, the sample role reads
+// them from the caller's arrays, clamps them, and the first query head of
+// each sequence writes them to the workspace for the later kernels.
+//
 // Any threshold gives the same final output: it only decides how many
 // candidates the scan emits (the top-k stage falls back to an exact re-scan
 // when fewer than k tokens reach it). So the wait is bounded: a sample
@@ -219,8 +223,22 @@ __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, 
     const int g = h / G;
     const int hh = h % G;
     const int bg = b * D.Hkv + g;
-    const int n_r = arg_n_r<kDev>(ba, w, b);
-    const int k = arg_topk<kDev>(ba, w, b);
+    int n_r, k;
+    if constexpr (kDev) {
+        // the call's integers from the caller's device arrays, published for
+        // the later kernels by the first query head of each sequence
+        const SeqArgs a = clamp_seq_args(D, ix.n_r[b], w.dev_lens[b], w.dev_topk[b]);
+        n_r = a.n_r;
+        k = a.topk;
+        if (h == 0 && tid == 0) {
+            w.ba_dev->topk[b] = a.topk;
+            w.ba_dev->n_r[b] = a.n_r;
+            w.ba_dev->n_tail[b] = a.n_tail;
+        }
+    } else {
+        n_r = ba.n_r[b];
+        k = ba.topk[b];
+    }
     const float neg_inf = -__builtin_huge_valf();
     if (n_r == 0) {
         if (tid == 0) {
