@@ -116,21 +116,28 @@ __device__ __forceinline__ bool rank_boundary_bin(KeyAt key_at, TokAt tok_at, in
     return true;
 }
 
-// LDS layout of select_kernel (dynamic, 4-byte words):
-//   keys [kSelCap] | cand [kSelCap] | mass (uint64) [kMaxLists] | hist [kHistBins] |
-//   rank_key [kRankCap] | rank_idx [kRankCap] | rank_tok [kRankCap] |
-//   chosen bitmap [kSelCap / 32] | counter, flags [4] | sub-chunk offsets [kSelMaxSub]
-constexpr int kOffCand = kSelCap;
-constexpr int kOffMass = 2 * kSelCap;   // 8-byte aligned
-constexpr int kOffHist = kOffMass + 2 * kMaxLists;
-constexpr int kOffRKey = kOffHist + kHistBins;
-constexpr int kOffRIdx = kOffRKey + kRankCap;
-constexpr int kOffRTok = kOffRIdx + kRankCap;
-constexpr int kOffBits = kOffRTok + kRankCap;
-constexpr int kOffCounter = kOffBits + kSelCap / 32;
-constexpr int kOffPre = kOffCounter + 4;
-constexpr size_t kSelLdsWords = kOffPre + kSelMaxSub;
-constexpr size_t kSelLdsBytes = kSelLdsWords * 4;
+// LDS layout of select_kernel (dynamic, 4-byte words), for kCap candidates:
+//   keys [kCap] | cand [kCap] | hist [kHistBins] | rank_key [kRankCap] |
+//   rank_idx [kRankCap] | rank_tok [kRankCap] | chosen bitmap [kCap / 32] |
+//   counter, flags [4] | sub-chunk offsets [kSelMaxSub] | mass (uint64) [n_list]
+template <int kCap>
+struct SelLayout {
+    static constexpr int kOffCand = kCap;
+    static constexpr int kOffHist = 2 * kCap;
+    static constexpr int kOffRKey = kOffHist + kHistBins;
+    static constexpr int kOffRIdx = kOffRKey + kRankCap;
+    static constexpr int kOffRTok = kOffRIdx + kRankCap;
+    static constexpr int kOffBits = kOffRTok + kRankCap;
+    static constexpr int kOffCounter = kOffBits + kCap / 32;
+    static constexpr int kOffPre = kOffCounter + 4;
+    static constexpr int kOffMass = (kOffPre + kSelMaxSub + 1) & ~1;   // 8-byte aligned
+    static size_t bytes(int n_list) { return static_cast<size_t>(kOffMass + 2 * n_list) * 4; }
+    static_assert(kCap % kSelThreads == 0 && kCap % 32 == 0, "whole copy tiers and bitmap words");
+};
+// Two capacities: every row's candidates of a large budget in LDS (one
+// workgroup per CU), or fewer (two workgroups per CU, for grids of more rows
+// than CUs; rows beyond it take the global-memory path).
+constexpr int kSelCapSmall = 7168;
 
 // Copy the row's `total` candidates (1 <= total <= N * kSelThreads) from
 // their sub-chunk slots into LDS in position order: keys at lds[i], words
@@ -144,7 +151,7 @@ constexpr size_t kSelLdsBytes = kSelLdsWords * 4;
 // thread's min / max key.
 // With fixed bins (hist != nullptr), every candidate is also counted in
 // hist at bin min((key - bkmin) >> bsh, kHistBins - 1).
-template <int N>
+template <int N, int kOffCand>
 __device__ __forceinline__ void copy_candidates(const uint2* __restrict__ cand, const int* pre,
                                                 int nsub, int total, uint32_t* lds,
                                                 uint32_t& kmin, uint32_t& kmax, int* hist,
@@ -253,18 +260,20 @@ __device__ __forceinline__ void rescan_row(const Dims& D, const Index& ix, const
     }
 }
 
-template <bool kDev>
-__global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchArgs ba, Index ix,
-                                                             Work w, int force_fallback) {
+template <bool kDev, int kCap>
+__device__ __forceinline__ void select_row(const Dims& D, const BatchArgs& ba, const Index& ix,
+                                           const Work& w, int force_fallback) {
+    using L = SelLayout<kCap>;
+    constexpr int kOffCand = L::kOffCand;
     extern __shared__ uint32_t lds[];
-    unsigned long long* mass = reinterpret_cast<unsigned long long*>(lds + kOffMass);
-    int* hist = reinterpret_cast<int*>(lds + kOffHist);
-    uint32_t* r_key = lds + kOffRKey;
-    int* r_idx = reinterpret_cast<int*>(lds + kOffRIdx);
-    int* r_tok = reinterpret_cast<int*>(lds + kOffRTok);
-    uint32_t* chosen = lds + kOffBits;
-    int* counter = reinterpret_cast<int*>(lds + kOffCounter);
-    int* pre = reinterpret_cast<int*>(lds + kOffPre);
+    unsigned long long* mass = reinterpret_cast<unsigned long long*>(lds + L::kOffMass);
+    int* hist = reinterpret_cast<int*>(lds + L::kOffHist);
+    uint32_t* r_key = lds + L::kOffRKey;
+    int* r_idx = reinterpret_cast<int*>(lds + L::kOffRIdx);
+    int* r_tok = reinterpret_cast<int*>(lds + L::kOffRTok);
+    uint32_t* chosen = lds + L::kOffBits;
+    int* counter = reinterpret_cast<int*>(lds + L::kOffCounter);
+    int* pre = reinterpret_cast<int*>(lds + L::kOffPre);
     __shared__ SelectScratch ss;
     __shared__ BlockScratch bs;
     const int tid = threadIdx.x;
@@ -287,7 +296,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchArgs b
 
     for (int j = tid; j < D.n_list; j += kSelThreads) mass[j] = 0ull;
     for (int i = tid; i < kHistBins; i += kSelThreads) hist[i] = 0;
-    for (int i = tid; i < kSelCap / 32; i += kSelThreads) chosen[i] = 0u;
+    for (int i = tid; i < kCap / 32; i += kSelThreads) chosen[i] = 0u;
     if (tid < 4) counter[tid] = 0;   // counter[1] is the equal-key flag of the rank
 
     // 1) candidate counts: wave w owns sub-chunks [w * spw, (w + 1) * spw)
@@ -322,7 +331,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchArgs b
     const bool fallback = force_fallback || (n_r > 0 && total < (k > 0 ? k : 1));
     float shift = neg_inf;
 
-    if (!fallback && small_nsub && total <= kSelCap) {
+    if (!fallback && small_nsub && total <= kCap) {
         // ---- fast path: candidates in LDS, position order ----
         auto KEY = [&](int i) { return lds[i]; };
         auto CAND = [&](int i) { return lds[kOffCand + i]; };
@@ -337,13 +346,14 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchArgs b
         uint32_t bkmin = fixed ? float_key(tlo) : 0u;
         int bsh = fixed ? bin_shift(bkmin, float_key(thi)) : 0;
         int* fh = fixed ? hist : nullptr;
-        if (total > 8 * kSelThreads)
-            copy_candidates<kSelCap / kSelThreads>(cand, pre, nsub, total, lds, kmin, kmax, fh,
-                                                   bkmin, bsh);
+        constexpr int kMid = kCap / kSelThreads > 8 ? 8 : kCap / kSelThreads;
+        if (total > kMid * kSelThreads)
+            copy_candidates<kCap / kSelThreads, kOffCand>(cand, pre, nsub, total, lds, kmin, kmax,
+                                                         fh, bkmin, bsh);
         else if (total > 4 * kSelThreads)
-            copy_candidates<8>(cand, pre, nsub, total, lds, kmin, kmax, fh, bkmin, bsh);
+            copy_candidates<kMid, kOffCand>(cand, pre, nsub, total, lds, kmin, kmax, fh, bkmin, bsh);
         else if (total > 0)
-            copy_candidates<4>(cand, pre, nsub, total, lds, kmin, kmax, fh, bkmin, bsh);
+            copy_candidates<4, kOffCand>(cand, pre, nsub, total, lds, kmin, kmax, fh, bkmin, bsh);
         if (!fixed) block_min_max_count<kSelThreads>(kmin, kmax, kcount, bs);
         auto TOK = [&](int i) { return static_cast<int>(CAND(i) & kPosMask); };
         if (k == 0) {
@@ -459,25 +469,70 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchArgs b
     }
 }
 
+template <bool kDev>
+__global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchArgs ba, Index ix, Work w,
+                                                             int force_fallback) {
+    select_row<kDev, kSelCap>(D, ba, ix, w, force_fallback);
+}
+
+// Two of these share a CU only when each wave holds at most 80 SGPRs (the
+// few beyond that spill to VGPR lanes).
+template <bool kDev>
+__global__ __launch_bounds__(kSelThreads) __attribute__((amdgpu_num_sgpr(80))) void select_small_kernel(
+    Dims D, BatchArgs ba, Index ix, Work w, int force_fallback) {
+    select_row<kDev, kSelCapSmall>(D, ba, ix, w, force_fallback);
+}
+
+// The small-capacity select when the rows outnumber the CUs and two of its
+// workgroups fit in one CU's LDS.
+static bool select_small(const Dims& D) {
+    static const int n_cu = [] {
+        int dev = 0, n = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+            return 0;
+        return n;
+    }();
+    constexpr size_t kLdsPerCu = 160 * 1024;
+    constexpr size_t kStatic = sizeof(SelectScratch) + sizeof(BlockScratch);
+    return n_cu > 0 && D.B * D.Hq > n_cu &&
+           2 * (SelLayout<kSelCapSmall>::bytes(D.n_list) + kStatic) <= kLdsPerCu;
+}
+
+template <bool kDev>
+static void launch_select_d(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w,
+                            int force_fallback, hipStream_t s, const KTiming& tm) {
+    if (select_small(D))
+        hipExtLaunchKernelGGL((select_small_kernel<kDev>), dim3(D.B * D.Hq), dim3(kSelThreads),
+                              SelLayout<kSelCapSmall>::bytes(D.n_list), s, tm.start, tm.stop, 0, D, ba,
+                              ix, w, force_fallback);
+    else
+        hipExtLaunchKernelGGL((select_kernel<kDev>), dim3(D.B * D.Hq), dim3(kSelThreads),
+                              SelLayout<kSelCap>::bytes(D.n_list), s, tm.start, tm.stop, 0, D, ba, ix,
+                              w, force_fallback);
+}
+
 hipError_t launch_select(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w,
                          int force_fallback, hipStream_t s, const KTiming& tm) {
     if (w.ba_dev)
-        hipExtLaunchKernelGGL(select_kernel<true>, dim3(D.B * D.Hq), dim3(kSelThreads), kSelLdsBytes,
-                              s, tm.start, tm.stop, 0, D, ba, ix, w, force_fallback);
+        launch_select_d<true>(D, ba, ix, w, force_fallback, s, tm);
     else
-        hipExtLaunchKernelGGL(select_kernel<false>, dim3(D.B * D.Hq), dim3(kSelThreads), kSelLdsBytes,
-                              s, tm.start, tm.stop, 0, D, ba, ix, w, force_fallback);
+        launch_select_d<false>(D, ba, ix, w, force_fallback, s, tm);
     return hipGetLastError();
 }
 
 hipError_t configure_select() {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&select_kernel<false>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize,
-                                       static_cast<int>(kSelLdsBytes));
-    if (e == hipSuccess)
-        e = hipFuncSetAttribute(reinterpret_cast<const void*>(&select_kernel<true>),
-                                hipFuncAttributeMaxDynamicSharedMemorySize,
-                                static_cast<int>(kSelLdsBytes));
+    const void* k[] = {reinterpret_cast<const void*>(&select_kernel<false>),
+                       reinterpret_cast<const void*>(&select_kernel<true>),
+                       reinterpret_cast<const void*>(&select_small_kernel<false>),
+                       reinterpret_cast<const void*>(&select_small_kernel<true>)};
+    const int bytes[] = {static_cast<int>(SelLayout<kSelCap>::bytes(kMaxLists)),
+                         static_cast<int>(SelLayout<kSelCap>::bytes(kMaxLists)),
+                         static_cast<int>(SelLayout<kSelCapSmall>::bytes(kMaxLists)),
+                         static_cast<int>(SelLayout<kSelCapSmall>::bytes(kMaxLists))};
+    hipError_t e = hipSuccess;
+    for (int i = 0; i < 4 && e == hipSuccess; ++i)
+        e = hipFuncSetAttribute(k[i], hipFuncAttributeMaxDynamicSharedMemorySize, bytes[i]);
     return e;
 }
 

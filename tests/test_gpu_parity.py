@@ -186,6 +186,27 @@ def test_candidate_volume(n_r):
     assert float((out2 - out).abs().max()) <= 1e-4 * float(out.abs().max())
 
 
+# more rows than CUs (9 x 32 = 288): the top-k stage runs two workgroups per
+# CU with room for 7168 candidates each; a flood of every token (about 8K per
+# row) takes its global-memory path
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("flood", [False, True], ids=["sampled", "every-token"])
+def test_many_rows_small_select(flood):
+    wl = small(1, batch=9, max_seq=8192 + 132, n_list=96, topk=160)
+    inp = make(wl, seed=17)
+    ctx = context(inp)
+    if flood:
+        ctx.set_option(pqhsa.OPT_THRESHOLD_BIAS, -1_000_000)
+    topk_l, out, sel, unsel, sc = run(ctx, inp, scores=True)
+    rows = [(b, h) for b in range(wl.batch) for h in (0, 13, 31)]
+    check_rows(inp, topk_l, rows, out, sel, unsel, sc)
+    if flood:
+        ctx.set_option(pqhsa.OPT_THRESHOLD_BIAS, 0)
+        _, out2, sel2, *_ = run(ctx, inp)
+        assert torch.equal(sel2, sel)
+        assert float((out2 - out).abs().max()) <= 1e-4 * float(out.abs().max())
+
+
 # ---------------------------------------------------------------------------
 # the paper's own index setting: 8 subspaces of 4-bit codes (Section 3.1)
 # ---------------------------------------------------------------------------
