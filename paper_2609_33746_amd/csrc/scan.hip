@@ -5,8 +5,10 @@
 //
 // Work decomposition: the list-major positions of each (batch element, KV
 // head) are cut into sub-chunks of kSub positions; one wave owns one
-// sub-chunk, and a workgroup holds kScanWaves consecutive sub-chunks of the
-// same KV head so that they share one copy of the group LUT in LDS. Every
+// sub-chunk, and a workgroup holds kScanWaves consecutive sub-chunks (a
+// chunk) of the same KV head so that they share one copy of the group LUT in
+// LDS; when the grid would take several rounds of the device, a workgroup
+// scans up to four chunks of its KV head with one staging of its tables. Every
 // batch element gets the workgroup count of the longest R_b; the surplus
 // workgroups of shorter sequences exit at once. The workgroups of one KV head
 // are spaced by the number of (batch element, KV head) units in the grid, so
@@ -35,6 +37,7 @@
 // and each new pair increases at least one of them, so distinct pairs get
 // distinct segments (some segment indices stay unused). No atomics are used
 // and the result does not depend on scheduling.
+#include <algorithm>
 #include <type_traits>
 
 #include "device_common.h"
@@ -93,9 +96,11 @@ constexpr int kScanLutFloats = std::is_same<PQ, Pq4>::value ? kRep4Floats : PQ::
 // stride of the group tables, masses and rows). A group of GT = 8 heads is
 // split over two workgroups of G = 4: their tables then take 80 KB of LDS,
 // so two workgroups share a CU instead of one (the codes are read twice).
+// At most 80 SGPRs per wave (a few spill to VGPR lanes): with more, a second
+// workgroup does not fit on the CU.
 template <int G, int GT, bool kCoarseLds, typename PQ, bool kDev>
-__global__ __launch_bounds__(kScanThreads) void scan_kernel(Dims D, BatchArgs ba, Index ix, Work w,
-                                                            int nwg) {
+__global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_num_sgpr(80))) void scan_kernel(
+    Dims D, BatchArgs ba, Index ix, Work w, int nwg, int nwg_grid) {
     // the group LUT at a compile-time LDS address (so that an entry address
     // is one shift of a code), then, when it fits, the [n_list][G] coarse
     // table in the dynamic part
@@ -106,9 +111,11 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(Dims D, BatchArgs ba
     constexpr int kParts = GT / G;   // workgroups per (b, g) and sub-chunk range
     static_assert(kParts * G == GT, "head split");
     // workgroup i serves unit i mod U of the U = B Hkv kParts (b, g, part)
-    // units, chunk i / U: workgroups run on XCD i mod 8, so when U is a
-    // multiple of 8 every workgroup of a unit shares one XCD and its L2, and
-    // the unit's tables come from HBM once instead of once per XCD
+    // units, chunks c, c + nwg_grid, c + 2 nwg_grid, ... (c = i / U) of the
+    // unit's nwg chunks, with the tables staged once: workgroups run on XCD
+    // i mod 8, so when U is a multiple of 8 every workgroup of a unit shares
+    // one XCD and its L2, and the unit's tables come from HBM once instead of
+    // once per XCD
     const int n_units = D.B * D.Hkv * kParts;
     const int unit = blockIdx.x % n_units;
     const int part = unit % kParts;
@@ -116,16 +123,12 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(Dims D, BatchArgs ba
     const int b = bg / D.Hkv;
     const int g = bg % D.Hkv;
     const int n_r = arg_n_r<kDev>(ba, w, b);
-    const int sc0 = (blockIdx.x / n_units) * kScanWaves;
-    if (sc0 * kSub >= n_r) return;   // surplus workgroup of a shorter sequence
+    const int chunk0 = blockIdx.x / n_units;
+    if (chunk0 * kScanWaves * kSub >= n_r) return;   // surplus workgroup of a shorter sequence
 
     const int tid = threadIdx.x;
     const int wave = tid / kWave;
     const int lane = lane_id();
-    const int sc = sc0 + wave;
-    const int p_begin = sc * kSub;
-    const int p_end = min(p_begin + kSub, n_r);
-    const bool active = p_begin < n_r;
     const int64_t base = static_cast<int64_t>(bg) * D.rcap;
     const int row0 = b * D.Hq + g * GT + part * G;
     // this workgroup's G heads within the group tables ([..][GT] layouts)
@@ -176,101 +179,123 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(Dims D, BatchArgs ba
             reinterpret_cast<float4*>(coarse_s)[i * kScanThreads + tid] = cst[i];
     }
     __syncthreads();
-    if (!active) return;
-    // 2) per 64-position step: list ids, codes and norms (addresses clamped
-    //    into R_b, so every load is in bounds), issued in the order the steps
-    //    use them, after the tables: each step waits only for its own data
-    const typename PQ::Code* codes = reinterpret_cast<const typename PQ::Code*>(ix.codes) + base;
-    uint32_t wl[kIters];   // list id << kPosBits | token id
-    typename PQ::Code cv[kIters];
-    float rv[kIters];
+    for (int chunk = chunk0; chunk < nwg; chunk += nwg_grid) {
+        const int sc = chunk * kScanWaves + wave;
+        const int p_begin = sc * kSub;
+        const int p_end = min(p_begin + kSub, n_r);
+        if (p_begin >= n_r) break;   // later chunks start later still
+        // 2) per 64-position step: list ids, codes and norms (addresses clamped
+        //    into R_b, so every load is in bounds), issued in the order the steps
+        //    use them, after the tables: each step waits only for its own data
+        const typename PQ::Code* codes = reinterpret_cast<const typename PQ::Code*>(ix.codes) + base;
+        uint32_t wl[kIters];   // list id << kPosBits | token id
+        typename PQ::Code cv[kIters];
+        float rv[kIters];
 #pragma unroll
-    for (int it = 0; it < kIters; ++it) {
-        const int p = min(p_begin + it * kWave + lane, n_r - 1);
-        wl[it] = ix.pos_word[base + p];
-        cv[it] = codes[p];
-        rv[it] = ix.norms[base + p];
-    }
-    float* segs = w.seg_sum + (static_cast<int64_t>(bg) * D.nseg_cap + sc) * GT + part * G;   // + j * GT
-    int cur = __builtin_amdgcn_readfirstlane(static_cast<int>(wl[0] >> kPosBits));   // open segment's list
-    float acc[G];
-    int cbase[G];
+        for (int it = 0; it < kIters; ++it) {
+            const int p = min(p_begin + it * kWave + lane, n_r - 1);
+            wl[it] = ix.pos_word[base + p];
+            cv[it] = codes[p];
+            rv[it] = ix.norms[base + p];
+        }
+        float* segs = w.seg_sum + (static_cast<int64_t>(bg) * D.nseg_cap + sc) * GT + part * G;   // + j * GT
+        int cur = __builtin_amdgcn_readfirstlane(static_cast<int>(wl[0] >> kPosBits));   // open segment's list
+        float acc[G];
+        int cbase[G];
 #pragma unroll
-    for (int hh = 0; hh < G; ++hh) { acc[hh] = 0.0f; cbase[hh] = 0; }
+        for (int hh = 0; hh < G; ++hh) { acc[hh] = 0.0f; cbase[hh] = 0; }
 
 #pragma unroll
-    for (int it = 0; it < kIters; ++it) {
-        const int p_first = p_begin + it * kWave;
-        if (p_first >= p_end) continue;   // uniform: past the end of a short last sub-chunk
-        const int p = p_first + lane;
-        const bool valid = p < p_end;
-        // coarse terms of the lanes' lists: from LDS, or gathered when the
-        // coarse table does not fit beside the LUT
-        const int j = static_cast<int>(wl[it] >> kPosBits);
-        float cf[G];
-        if constexpr (kCoarseLds) load_coarse<G>(coarse_s + j * G, cf);
-        else load_coarse<G>(coarse + j * GT, cf);
-        float fs[G];
-        if constexpr (std::is_same<PQ, Pq4>::value) fine_sum_rep4<G>(lut_s, cv[it], fs);
-        else fine_sum<PQ, G>(lut_s, cv[it], fs);
-        float s[G], e[G];
+        for (int it = 0; it < kIters; ++it) {
+            const int p_first = p_begin + it * kWave;
+            if (p_first >= p_end) continue;   // uniform: past the end of a short last sub-chunk
+            const int p = p_first + lane;
+            const bool valid = p < p_end;
+            // coarse terms of the lanes' lists: from LDS, or gathered when the
+            // coarse table does not fit beside the LUT
+            const int j = static_cast<int>(wl[it] >> kPosBits);
+            float cf[G];
+            if constexpr (kCoarseLds) load_coarse<G>(coarse_s + j * G, cf);
+            else load_coarse<G>(coarse + j * GT, cf);
+            float fs[G];
+            if constexpr (std::is_same<PQ, Pq4>::value) fine_sum_rep4<G>(lut_s, cv[it], fs);
+            else fine_sum<PQ, G>(lut_s, cv[it], fs);
+            float s[G], e[G];
 #pragma unroll
-        for (int hh = 0; hh < G; ++hh) {
-            s[hh] = pq_logit(rv[it], cf[hh], fs[hh]);
-            e[hh] = (valid && s[hh] < tlo[hh]) ? __expf(s[hh] - tlo[hh]) : 0.0f;
-        }
-        // close the lists that end inside this step (lists are contiguous and
-        // ascending along the lanes)
-        const int j_last = __builtin_amdgcn_readlane(j, min(p_end - p_first, kWave) - 1);
-        while (cur != j_last) {
-            const bool in = valid && j == cur;
+            for (int hh = 0; hh < G; ++hh) {
+                s[hh] = pq_logit(rv[it], cf[hh], fs[hh]);
+                e[hh] = (valid && s[hh] < tlo[hh]) ? __expf(s[hh] - tlo[hh]) : 0.0f;
+            }
+            // close the lists that end inside this step (lists are contiguous and
+            // ascending along the lanes)
+            const int j_last = __builtin_amdgcn_readlane(j, min(p_end - p_first, kWave) - 1);
+            while (cur != j_last) {
+                const bool in = valid && j == cur;
 #pragma unroll
-            for (int hh = 0; hh < G; ++hh) acc[hh] += in ? e[hh] : 0.0f;
-            flush_segment<G>(segs + cur * GT, acc);
-            const int nxt = __popcll(__ballot(valid && j <= cur));
-            cur = __builtin_amdgcn_readlane(j, nxt);
-        }
-        {
-            const bool in = valid && j == cur;
+                for (int hh = 0; hh < G; ++hh) acc[hh] += in ? e[hh] : 0.0f;
+                flush_segment<G>(segs + cur * GT, acc);
+                const int nxt = __popcll(__ballot(valid && j <= cur));
+                cur = __builtin_amdgcn_readlane(j, nxt);
+            }
+            {
+                const bool in = valid && j == cur;
 #pragma unroll
-            for (int hh = 0; hh < G; ++hh) acc[hh] += in ? e[hh] : 0.0f;
-        }
-        // candidates >= tau_lo, compacted in position order
+                for (int hh = 0; hh < G; ++hh) acc[hh] += in ? e[hh] : 0.0f;
+            }
+            // candidates >= tau_lo, compacted in position order
 #pragma unroll
-        for (int hh = 0; hh < G; ++hh) {
-            const uint64_t mask = __ballot(valid && s[hh] >= tlo[hh]);
-            if (mask) {
-                if ((mask >> lane) & 1ull) {
-                    const int64_t o = static_cast<int64_t>(row0 + hh) * D.rcap + p_begin +
-                                      cbase[hh] + lanes_below(mask);
-                    w.cand[o] = make_uint2(__float_as_uint(s[hh]), wl[it]);
+            for (int hh = 0; hh < G; ++hh) {
+                const uint64_t mask = __ballot(valid && s[hh] >= tlo[hh]);
+                if (mask) {
+                    if ((mask >> lane) & 1ull) {
+                        const int64_t o = static_cast<int64_t>(row0 + hh) * D.rcap + p_begin +
+                                          cbase[hh] + lanes_below(mask);
+                        w.cand[o] = make_uint2(__float_as_uint(s[hh]), wl[it]);
+                    }
+                    cbase[hh] += __popcll(mask);
                 }
-                cbase[hh] += __popcll(mask);
             }
         }
-    }
-    flush_segment<G>(segs + cur * GT, acc);
-    int mine = 0;
+        flush_segment<G>(segs + cur * GT, acc);
+        int mine = 0;
 #pragma unroll
-    for (int hh = 0; hh < G; ++hh)
-        if (lane == hh) mine = cbase[hh];
-    if (lane < G) w.cand_cnt[static_cast<int64_t>(row0 + lane) * D.nsub_cap + sc] = mine;
+        for (int hh = 0; hh < G; ++hh)
+            if (lane == hh) mine = cbase[hh];
+        if (lane < G) w.cand_cnt[static_cast<int64_t>(row0 + lane) * D.nsub_cap + sc] = mine;
+    }
 }
 
 constexpr size_t kScanLdsMax = 160 * 1024;   // LDS of one workgroup on gfx950
+constexpr int kScanMaxChunks = 4;
 
 template <int G, int GT, typename PQ, bool kDev>
 static hipError_t launch_scan_d(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w,
                                 int nwg, hipStream_t s, const KTiming& tm) {
     const size_t cf = static_cast<size_t>(kCoarseCapF4<G>) * 16;
     static_assert(kScanLutFloats<PQ, G> * 4 + kCoarseCapF4<G> * 16 <= kScanLdsMax, "LDS budget");
-    const dim3 grid(D.B * D.Hkv * (GT / G) * nwg);
+    const int n_units = D.B * D.Hkv * (GT / G);
+    // chunks per workgroup: as many as the grid has rounds of the workgroups
+    // that run at once (two per CU), at most kScanMaxChunks, each workgroup
+    // staging its tables once for all of them (at 4 and 16 sequences 4
+    // chunks per workgroup beat 1, 2, 8 and 16)
+    static const int n_cu = [] {
+        int dev = 0, n = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+            return 0;
+        return n;
+    }();
+    const int64_t resident = static_cast<int64_t>(2) * (n_cu > 0 ? n_cu : 1);
+    const int cpw = static_cast<int>(
+        std::min<int64_t>(kScanMaxChunks, std::max<int64_t>(1, static_cast<int64_t>(n_units) * nwg / resident)));
+    const int nwg_grid = (nwg + cpw - 1) / cpw;
+    const dim3 grid(n_units * nwg_grid);
     if (D.n_list * G % 4 == 0 && D.n_list * G / 4 <= kCoarseCapF4<G>)
         hipExtLaunchKernelGGL((scan_kernel<G, GT, true, PQ, kDev>), grid, dim3(kScanThreads), cf, s,
-                              tm.start, tm.stop, 0, D, ba, ix, w, nwg);
+                              tm.start, tm.stop, 0, D, ba, ix, w, nwg, nwg_grid);
     else
         hipExtLaunchKernelGGL((scan_kernel<G, GT, false, PQ, kDev>), grid, dim3(kScanThreads), 0, s,
-                              tm.start, tm.stop, 0, D, ba, ix, w, nwg);
+                              tm.start, tm.stop, 0, D, ba, ix, w, nwg, nwg_grid);
     return hipGetLastError();
 }
 
