@@ -207,7 +207,6 @@ __device__ __forceinline__ int wave_find_bin_desc(const int* hist, int c) {
 struct SampleLds {
     float lut[kLutRowMax];   // the head's fine table [M][K]
     int hist[kHistBins];
-    uint32_t binmin[kHistBins];   // smallest sample key of each bin
     int ready;
     SelectScratch ss;
     BlockScratch bs;
@@ -278,10 +277,7 @@ __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, 
         rv[u] = ix.norms[base + p];
         jv[u] = static_cast<int>(ix.pos_word[base + p] >> kPosBits);
     }
-    for (int i = tid; i < kHistBins; i += kProThreads) {
-        sm.hist[i] = 0;
-        sm.binmin[i] = 0xffffffffu;
-    }
+    for (int i = tid; i < kHistBins; i += kProThreads) sm.hist[i] = 0;
 
     // 2) wait for the KV head's LUT parts (bounded): the first wave reads
     //    every part's flag (one per lane, a few cache lines), with two such
@@ -348,7 +344,7 @@ __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, 
 
     // 4) scores of the samples
     float sc[kSamplesPer];
-    uint32_t mn = 0xffffffffu, mx = 0u, cnt = 0u;
+    uint32_t mn = 0xffffffffu, mx = 0u;
 #pragma unroll
     for (int u = 0; u < kSamplesPer; ++u) {
         float fs[1];
@@ -358,11 +354,23 @@ __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, 
             const uint32_t kk = float_key(sc[u]);
             mn = min(mn, kk);
             mx = max(mx, kk);
-            ++cnt;
         }
     }
-    block_min_max_count<kProThreads>(mn, mx, cnt, sm.bs);
-    const int ns = static_cast<int>(cnt);
+    // their min and max over the workgroup, with one barrier (the scratch is
+    // not written again); every run is whole, so there are nrun * run_len
+    mn = wave_min_u32(mn);
+    mx = wave_max_u32(mx);
+    if (lane_id() == 0) {
+        sm.bs.v[tid / kWave][0] = mn;
+        sm.bs.v[tid / kWave][1] = mx;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kProThreads / kWave; ++i) {
+        mn = min(mn, sm.bs.v[i][0]);
+        mx = max(mx, sm.bs.v[i][1]);
+    }
+    const int ns = nrun * run_len;
     // order statistic: about 2k * ns / |R| sampled tokens above, plus a margin
     const int c = (k == 0) ? 1 : static_cast<int>(ceilf(2.0f * k * ns / n_r)) + 8;
     if (c > ns) {   // the budget is a large share of R: every token is a candidate
@@ -380,16 +388,23 @@ __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, 
 #pragma unroll
     for (int u = 0; u < kSamplesPer; ++u) {
         const int bin = min(static_cast<int>((sc[u] - fmn) * scale), kHistBins - 1);
-        hist_add(sm.hist, static_cast<uint32_t>(ok[u] ? bin : 0), ok[u]);
-        if (ok[u]) atomicMin(&sm.binmin[bin], float_key(sc[u]));
+        if (ok[u]) atomicAdd(&sm.hist[bin], 1);   // the samples' bins are mostly distinct
     }
     __syncthreads();
-    // 6) one wave: the bin holding the c-th largest sample; tau_lo is that
-    //    bin's smallest sample, so at least c samples are >= it
+    // 6) one wave: the bin holding the c-th largest sample; tau_lo sits just
+    //    below that bin, so at least c samples are >= it
     if (tid < kWave) {
         const int bstar = wave_find_bin_desc(sm.hist, c);
         if (tid == 0) {
-            w.tau_lo[row] = key_float(sm.binmin[bstar]) + bias;
+            // the lower edge of the bin below, nudged down: every sample of
+            // bin bstar and above (at least c of them) scores at or above it
+            // whatever the rounding of the bin computation
+            float tl = fmn;
+            if (bstar > 1 && scale > 0.0f) {
+                tl = fmn + static_cast<float>(bstar - 1) * (range / kHistBins);
+                tl = fmaxf(tl - fabsf(tl) * 0x1p-21f, fmn);
+            }
+            w.tau_lo[row] = tl + bias;
             w.tau_hi[row] = key_float(mx);   // lets the top-k stage fix its bins in advance
         }
     }
