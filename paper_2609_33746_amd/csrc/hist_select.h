@@ -1,6 +1,7 @@
 // Workgroup helpers for order statistics over 32-bit order keys:
 // min / max / count reductions, a shift-based histogram that is monotone in
-// the key, and the search for the histogram bin holding the c-th largest key.
+// the key, and the search (by one wave) for the histogram bin holding the c-th
+// largest key.
 #pragma once
 
 #include "device_common.h"
@@ -50,37 +51,29 @@ __device__ __forceinline__ int bin_shift(uint32_t kmin, uint32_t kmax) {
     return bits > 11 ? bits - 11 : 0;
 }
 
-// Given hist[kHistBins], find the bin holding the c-th largest key (1-based);
-// returns it and writes the number of keys in higher bins to `above`.
-// All NT threads must call this; each owns kHistBins / NT bins.
-template <int NT>
-__device__ __forceinline__ int block_find_bin_desc(const int* hist, int c, int& above,
-                                                   SelectScratch& ss, BlockScratch& bs) {
-    constexpr int PER = kHistBins / NT;
-    static_assert(PER * NT == kHistBins, "bins must divide evenly");
-    const int t = threadIdx.x;
-    int hv[PER];
-    int mine = 0;
+// The histogram bin holding the c-th largest entry (1 <= c <= the count in
+// hist), found by one wave; `above` receives the entries in higher bins.
+// Lane l sums the 32 bins of rank 32 l .. 32 l + 31 from the top (read in a
+// lane-rotated order, so the lanes of one read hit distinct LDS banks), a
+// wave scan finds the lane whose bins reach c, and a second scan over that
+// lane's 32 bins, one per lane, finds the bin.
+__device__ __forceinline__ int wave_find_bin_desc(const int* hist, int c, int& above) {
+    constexpr int PER = kHistBins / kWave;
+    static_assert(PER == 32, "two scans of 32 bins");
+    const int lane = lane_id();
+    int sum = 0;
 #pragma unroll
-    for (int j = 0; j < PER; ++j) {
-        hv[j] = hist[kHistBins - 1 - (PER * t + j)];
-        mine += hv[j];
-    }
-    int total = 0;
-    int before = block_excl_scan<NT>(mine, total, ss);
-#pragma unroll
-    for (int j = 0; j < PER; ++j) {
-        if (before < c && before + hv[j] >= c) {
-            bs.bcast[0] = kHistBins - 1 - (PER * t + j);
-            bs.bcast[1] = before;
-        }
-        before += hv[j];
-    }
-    __syncthreads();
-    const int bin = bs.bcast[0];
-    above = bs.bcast[1];
-    __syncthreads();
-    return bin;
+    for (int q = 0; q < PER; ++q) sum += hist[kHistBins - 1 - (PER * lane + ((q + lane) & (PER - 1)))];
+    const int incl = wave_incl_scan_i32(sum);
+    const uint64_t r1 = __ballot(incl >= c);
+    const int L = r1 ? __ffsll(static_cast<long long>(r1)) - 1 : kWave - 1;
+    const int before = __builtin_amdgcn_readlane(incl - sum, L);
+    const int v = lane < PER ? hist[kHistBins - 1 - (PER * L + lane)] : 0;
+    const int incl2 = wave_incl_scan_i32(v);
+    const uint64_t r2 = __ballot(lane < PER && before + incl2 >= c);
+    const int M = r2 ? __ffsll(static_cast<long long>(r2)) - 1 : PER - 1;
+    above = before + __builtin_amdgcn_readlane(incl2 - v, M);
+    return kHistBins - 1 - (PER * L + M);
 }
 
 }  // namespace pqhsa

@@ -181,29 +181,6 @@ __device__ __forceinline__ void lut_role(const Dims& D, const T* __restrict__ q,
     if (tid == 0) store_device(w.lut_flag + bg * prologue_parts(D.n_list, PQ::BITS) + part, ep);
 }
 
-// The histogram bin holding the c-th largest entry (1 <= c <= the count in
-// hist), found by one wave: lane l sums the 32 bins of rank 32 l .. 32 l + 31
-// from the top (read in a lane-rotated order, so the lanes of one read hit
-// distinct LDS banks), a wave scan finds the lane whose bins reach c, and a
-// second scan over that lane's 32 bins, one per lane, finds the bin.
-__device__ __forceinline__ int wave_find_bin_desc(const int* hist, int c) {
-    constexpr int PER = kHistBins / kWave;
-    static_assert(PER == 32, "two scans of 32 bins");
-    const int lane = lane_id();
-    int sum = 0;
-#pragma unroll
-    for (int q = 0; q < PER; ++q) sum += hist[kHistBins - 1 - (PER * lane + ((q + lane) & (PER - 1)))];
-    const int incl = wave_incl_scan_i32(sum);
-    const uint64_t r1 = __ballot(incl >= c);
-    const int L = r1 ? __ffsll(static_cast<long long>(r1)) - 1 : kWave - 1;
-    const int before = __builtin_amdgcn_readlane(incl - sum, L);
-    const int v = lane < PER ? hist[kHistBins - 1 - (PER * L + lane)] : 0;
-    const int incl2 = wave_incl_scan_i32(v);
-    const uint64_t r2 = __ballot(lane < PER && before + incl2 >= c);
-    const int M = r2 ? __ffsll(static_cast<long long>(r2)) - 1 : PER - 1;
-    return kHistBins - 1 - (PER * L + M);
-}
-
 struct SampleLds {
     float lut[kLutRowMax];   // the head's fine table [M][K]
     int hist[kHistBins];
@@ -394,7 +371,8 @@ __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, 
     // 6) one wave: the bin holding the c-th largest sample; tau_lo sits just
     //    below that bin, so at least c samples are >= it
     if (tid < kWave) {
-        const int bstar = wave_find_bin_desc(sm.hist, c);
+        int above_unused = 0;
+        const int bstar = wave_find_bin_desc(sm.hist, c, above_unused);
         if (tid == 0) {
             // the lower edge of the bin below, nudged down: every sample of
             // bin bstar and above (at least c of them) scores at or above it

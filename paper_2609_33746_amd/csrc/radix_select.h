@@ -99,7 +99,9 @@ __device__ __forceinline__ SelectResult block_select_desc(KeyAt key_at, Keep kee
 
 // Exclusive prefix of a per-thread count over the workgroup (NT threads);
 // returns this thread's offset, writes the total to `total`.
-template <int NT>
+// (kReuse = false: the caller writes sh.wave_tot no more before its next
+// barrier, so the trailing barrier that protects it is left out.)
+template <int NT, bool kReuse = true>
 __device__ __forceinline__ int block_excl_scan(int v, int& total, SelectScratch& sh) {
     constexpr int NW = NT / kWave;
     const int wave = threadIdx.x / kWave;
@@ -113,7 +115,7 @@ __device__ __forceinline__ int block_excl_scan(int v, int& total, SelectScratch&
         wbase += i < wave ? t : 0;
         tot += t;
     }
-    __syncthreads();
+    if constexpr (kReuse) __syncthreads();
     total = tot;
     return wbase + incl - v;
 }

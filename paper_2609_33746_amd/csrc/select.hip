@@ -192,7 +192,8 @@ __device__ __forceinline__ void copy_candidates(const uint2* __restrict__ cand, 
             kmin = min(kmin, kk);
             kmax = max(kmax, kk);
         }
-        if (hist) hist_add(hist, fixed_bin(kk, bkmin, bsh), ci < total);
+        // one LDS atomic per candidate: their bins are mostly distinct
+        if (hist && ci < total) atomicAdd(&hist[fixed_bin(kk, bkmin, bsh)], 1);
     }
 }
 
@@ -213,7 +214,7 @@ __device__ __forceinline__ void emit_selection(KeyAt key_at, CandAt cand_at, IsS
     int nsel = 0;
     for (int i = e0; i < e1; ++i) nsel += is_sel(i, key_at(i), cand_at(i)) ? 1 : 0;
     int tot = 0;
-    int o = block_excl_scan<kSelThreads>(nsel, tot, ss);
+    int o = block_excl_scan<kSelThreads, false>(nsel, tot, ss);   // ss is not written before the barrier below
     int run_list = -1;
     unsigned long long run = 0ull;
     for (int i = e0; i < e1; ++i) {
@@ -358,8 +359,9 @@ __device__ __forceinline__ void select_row(const Dims& D, const BatchArgs& ba, c
         auto TOK = [&](int i) { return static_cast<int>(CAND(i) & kPosMask); };
         if (k == 0) {
             shift = total > 0 ? key_float(kmax) : neg_inf;
-            emit_selection(KEY, CAND, [](int, uint32_t, uint32_t) { return false; }, total, 0,
-                           D.n_list, shift, mass, sel_tok, cand_mass, ss);
+            emit_selection(
+                KEY, CAND, [](int, uint32_t, uint32_t) { return false; }, total, 0, D.n_list, shift,
+                mass, sel_tok, cand_mass, ss);
         } else {
             if (!fixed) {
                 bkmin = kmin;
@@ -367,12 +369,22 @@ __device__ __forceinline__ void select_row(const Dims& D, const BatchArgs& ba, c
                 for (int i0 = 0; i0 < total; i0 += kSelThreads) {
                     const int i = i0 + tid;
                     const bool act = i < total;
-                    hist_add(hist, act ? fixed_bin(KEY(i), bkmin, bsh) : 0u, act);
+                    if (act) atomicAdd(&hist[fixed_bin(KEY(i), bkmin, bsh)], 1);
                 }
             }
             __syncthreads();
-            int above = 0;
-            const int bstar = block_find_bin_desc<kSelThreads>(hist, k, above, ss, bs);
+            // one wave finds the boundary bin and broadcasts it
+            if (tid < kWave) {
+                int ab = 0;
+                const int bin = wave_find_bin_desc(hist, k, ab);
+                if (tid == 0) {
+                    bs.bcast[0] = bin;
+                    bs.bcast[1] = ab;
+                }
+            }
+            __syncthreads();
+            const int bstar = bs.bcast[0];
+            const int above = bs.bcast[1];
             uint32_t kth = 0u;
             const bool by_rank = rank_boundary_bin(KEY, TOK, total, bkmin, bsh, bstar, hist[bstar],
                                                    k - above, r_key, r_idx, r_tok, counter,
