@@ -152,8 +152,8 @@ pqhsa_status check_shape(const pqhsa_shape* s) {
     if (s->max_seq > kMaxSeq) return fail(nullptr, PQHSA_ERR_UNSUPPORTED, "max_seq must be <= 2^20");
     {
         // partials per row: splits of the exact set plus background chunks
-        const int nsplit = std::max(
-            (s->n_sink + s->n_local + kTailGrowth + s->max_topk + kAttnRows - 1) / kAttnRows, 1);
+        const int rows = attn_rows_for(s->n_sink, s->n_local, s->max_topk);
+        const int nsplit = std::max((s->n_sink + s->n_local + kTailGrowth + s->max_topk + rows - 1) / rows, 1);
         const int nbgc = (s->n_list + kBgLists - 1) / kBgLists;
         if (nsplit + nbgc > kMaxRowParts)
             return fail(nullptr, PQHSA_ERR_UNSUPPORTED,
@@ -281,12 +281,13 @@ pqhsa_status pqhsa_create(const pqhsa_shape* shape, pqhsa_ctx** out) {
     D.nsub_cap = (D.rcap + kSub - 1) / kSub;
     D.nseg_cap = D.n_list + D.nsub_cap;
     D.max_topk = std::max(shape->max_topk, 1);
+    D.attn_rows = attn_rows_for(D.n_sink, D.n_local, shape->max_topk);
     D.pq_bits = shape->pq_m == Pq4::M ? Pq4::BITS : Pq8::BITS;
     D.inv_sqrt_d = static_cast<float>(1.0 / std::sqrt(static_cast<double>(kHeadDim)));
 
     const size_t B = D.B, Hq = D.Hq, Hkv = D.Hkv, G = D.G, L = D.n_list, rc = D.rcap;
     const size_t BG = B * Hkv, BQ = B * Hq;
-    c->nsplit_max = (D.n_sink + D.n_local + kTailGrowth + shape->max_topk + kAttnRows - 1) / kAttnRows;
+    c->nsplit_max = (D.n_sink + D.n_local + kTailGrowth + shape->max_topk + D.attn_rows - 1) / D.attn_rows;
     if (c->nsplit_max < 1) c->nsplit_max = 1;
     const int n_bgc = (D.n_list + kBgLists - 1) / kBgLists;
     c->dense_nsplit = (D.rcap + kDenseRows - 1) / kDenseRows;
@@ -705,7 +706,7 @@ static pqhsa_status decode_impl(pqhsa_ctx* c, const void* q, const void* k, cons
         ba.topk[b] = topk[b];
         ba.n_r[b] = c->n_r[b];
         ba.n_tail[b] = c->cur_len[b] - D.n_sink - c->n_r[b];
-        nsplit = std::max(nsplit, (D.n_sink + ba.n_tail[b] + topk[b] + kAttnRows - 1) / kAttnRows);
+        nsplit = std::max(nsplit, (D.n_sink + ba.n_tail[b] + topk[b] + D.attn_rows - 1) / D.attn_rows);
     }
     const Index ix = c->index();
     const bool timed = c->timing != 0 && !dev_args;

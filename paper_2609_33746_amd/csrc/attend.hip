@@ -6,9 +6,10 @@
 // usual log-sum-exp rule, so the common shift m0 of Section 3.2 never has to
 // be known in advance.
 //
-//  * attend_kernel, exact role: one workgroup per (row, split of kAttnRows
-//    rows of E). 16 lanes hold one K/V row (8 elements each); each 16-lane
-//    group owns kAttnRows / 16 rows and issues all of their token-id, K and V
+//  * attend_kernel, exact role: one workgroup per (row, split of kRows rows
+//    of E: 64 or 128 by the context's budget). 16 lanes hold one K/V row (8
+//    elements each); each 16-lane group owns kRows / 16 rows and issues all
+//    of their token-id, K and V
 //    loads before any arithmetic, so a workgroup keeps its whole split in
 //    flight.
 //  * attend_kernel, background role: one workgroup per (batch element, KV
@@ -26,7 +27,6 @@ namespace pqhsa {
 
 constexpr int kAttnThreads = 256;    // 4 waves x 4 groups of 16 lanes = 16 row streams
 constexpr int kStreams = kAttnThreads / 16;
-constexpr int kRowsPerStream = kAttnRows / kStreams;
 // rows per stream in one batch of the dense kernel (two batches are in
 // flight; fewer for large groups, which hold G accumulators per lane)
 template <int G>
@@ -107,11 +107,12 @@ __device__ __forceinline__ void block_combine(const Online& o, float* sm, float*
 // kBx: variant Bx. The exact role subtracts, at the background's shift, the
 // selected rows weighted by their lists' W_j = M_j / |B n R_j|; the background
 // role weights list j's mean by W_j |R_j| instead of M_j.
-template <typename T, int G, bool kBx, bool kDev>
+template <typename T, int G, bool kBx, bool kDev, int kRows>
 __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchArgs ba, KV kv,
                                                               Index ix, Work w, int nsplit,
                                                               int nsplit_max, int n_bgc,
                                                               int variant) {
+    constexpr int kRowsPerStream = kRows / kStreams;
     __shared__ float sm[kStreams], sz[kStreams];
     // [16 streams][d] for the exact role, [4 waves][G][d] for the background role
     __shared__ float sacc[(kStreams > 4 * G ? kStreams : 4 * G) * kHeadDim];
@@ -133,9 +134,9 @@ __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchArgs 
         const int n_r = arg_n_r<kDev>(ba, w, b);
         const int n_tail = arg_n_tail<kDev>(ba, w, b);   // L_b = [n_sink + |R_b|, N_b)
         const int nE = D.n_sink + n_tail + k;
-        const int e0 = split * kAttnRows;
+        const int e0 = split * kRows;
         if (e0 >= nE) return;   // the merge reads only the splits that exist
-        const int e1 = min(e0 + kAttnRows, nE);
+        const int e1 = min(e0 + kRows, nE);
         const int32_t* sel = w.sel_tok + static_cast<int64_t>(row) * D.max_topk;
         const int local0 = D.n_sink + n_r;
         int tok[kRowsPerStream];
@@ -416,14 +417,16 @@ hipError_t launch_bx_weights(const Dims& D, const BatchArgs& ba, const Index& ix
 // thread u < kMergeBatch loads (m, Z) of partial u and every thread t loads
 // N[t] of all of them, all at once, so a row with at most kMergeBatch
 // partials costs one memory round trip; batches fold by the log-sum-exp rule.
-constexpr int kMergeBatch = 32;
+constexpr int kMergeBatch = 40;
 static_assert(kMergeBatch <= kMergeThreads, "one (m, Z) per thread");
 
 // kGroups groups of kMergeThreads threads: group gi folds batches gi,
 // gi + kGroups, ... of the row's partials, then the groups' results fold in
-// LDS. One group serves rows of up to 64 partials (the PQ-HSA rows and the
-// dense decode up to 128K rows); longer dense rows (more than 64 splits of
-// 2048 rows) take 8.
+// LDS. One group serves rows of up to kMergeBatch (40) partials and two
+// groups rows of up to 80, each in one round trip (the PQ-HSA rows and the
+// dense decode up to 128K rows); longer dense rows (more than 80 splits of
+// 2048 rows) take 8. (40 partials per group: a 128K row of 64-row splits has
+// 39; the merge took 4.3 us against 4.8 us with two groups of 32.)
 template <int kGroups>
 __global__ __launch_bounds__(kMergeThreads * kGroups) void merge_kernel(
     Dims D, BatchInts n_exact_parts, const float* __restrict__ partial, int P, int first_bg,
@@ -443,7 +446,7 @@ __global__ __launch_bounds__(kMergeThreads * kGroups) void merge_kernel(
     const float* pr = partial + static_cast<int64_t>(row) * P * kPartStride;
     // exact partials of the row: from the host, or from the call's device
     // budgets and lengths
-    const int ne = ba_dev ? (D.n_sink + ba_dev->n_tail[b] + ba_dev->topk[b] + kAttnRows - 1) / kAttnRows
+    const int ne = ba_dev ? (D.n_sink + ba_dev->n_tail[b] + ba_dev->topk[b] + D.attn_rows - 1) / D.attn_rows
                           : n_exact_parts.v[b];
     const int n_used = ne + n_bg;
     const float neg_inf = -__builtin_huge_valf();
@@ -508,14 +511,13 @@ static hipError_t launch_attend_d(const Dims& D, const BatchArgs& ba, const KV& 
     const int n_bgc = (D.n_list + kBgLists - 1) / kBgLists;   // the partials' layout
     // variant T has no background: the background workgroups are not launched
     const int grid = D.B * D.Hq * nsplit + (variant == PQHSA_VARIANT_T ? 0 : D.B * D.Hkv * n_bgc);
-    if (variant == PQHSA_VARIANT_BX)
-        hipExtLaunchKernelGGL((attend_kernel<T, G, true, kDev>), dim3(grid), dim3(kAttnThreads), 0, s,
-                              tm.start, tm.stop, 0, D, ba, kv, ix, w, nsplit, nsplit_max, n_bgc,
-                              variant);
-    else
-        hipExtLaunchKernelGGL((attend_kernel<T, G, false, kDev>), dim3(grid), dim3(kAttnThreads), 0,
-                              s, tm.start, tm.stop, 0, D, ba, kv, ix, w, nsplit, nsplit_max, n_bgc,
-                              variant);
+    auto kern = variant == PQHSA_VARIANT_BX
+                    ? (D.attn_rows == kAttnRowsSmall ? attend_kernel<T, G, true, kDev, kAttnRowsSmall>
+                                                     : attend_kernel<T, G, true, kDev, kAttnRows>)
+                    : (D.attn_rows == kAttnRowsSmall ? attend_kernel<T, G, false, kDev, kAttnRowsSmall>
+                                                     : attend_kernel<T, G, false, kDev, kAttnRows>);
+    hipExtLaunchKernelGGL(kern, dim3(grid), dim3(kAttnThreads), 0, s, tm.start, tm.stop, 0, D, ba, kv,
+                          ix, w, nsplit, nsplit_max, n_bgc, variant);
     return hipGetLastError();
 }
 
@@ -552,9 +554,14 @@ static hipError_t launch_merge_parts(const Dims& D, const BatchInts& ne, const f
                                      const BatchArgs* ba_dev, hipStream_t s, const KTiming& tm) {
     int most = 0;   // the most partials of a row
     for (int b = 0; b < D.B; ++b) most = ne.v[b] + n_bg > most ? ne.v[b] + n_bg : most;
-    if (most <= 2 * kMergeBatch)
+    // one memory round trip per row: one group of threads per batch of
+    // kMergeBatch partials (up to 2), or 8 groups looping for the dense rows
+    if (most <= kMergeBatch)
         hipExtLaunchKernelGGL(merge_kernel<1>, dim3(D.B * D.Hq), dim3(kMergeThreads), 0, s, tm.start,
                               tm.stop, 0, D, ne, partial, P, first_bg, n_bg, out, epoch, ba_dev);
+    else if (most <= 2 * kMergeBatch)
+        hipExtLaunchKernelGGL(merge_kernel<2>, dim3(D.B * D.Hq), dim3(2 * kMergeThreads), 0, s,
+                              tm.start, tm.stop, 0, D, ne, partial, P, first_bg, n_bg, out, epoch, ba_dev);
     else
         hipExtLaunchKernelGGL(merge_kernel<8>, dim3(D.B * D.Hq), dim3(8 * kMergeThreads), 0, s,
                               tm.start, tm.stop, 0, D, ne, partial, P, first_bg, n_bg, out, epoch, ba_dev);
@@ -568,7 +575,7 @@ hipError_t launch_merge(const Dims& D, const BatchArgs& ba, const Work& w, float
         // with device budgets the kernel counts the partials itself; the
         // bound here only picks the launch shape
         const int nE = D.n_sink + ba.n_tail[b] + ba.topk[b];
-        ne.v[b] = w.ba_dev ? nsplit_max : (nE + kAttnRows - 1) / kAttnRows;
+        ne.v[b] = w.ba_dev ? nsplit_max : (nE + D.attn_rows - 1) / D.attn_rows;
     }
     const int n_bgc = (D.n_list + kBgLists - 1) / kBgLists;
     // variant T: the exact partials alone

@@ -39,7 +39,8 @@ constexpr int kSampleRun = 2;      // contiguous positions per sampled run
 constexpr int kPosBits = 20;       // position / candidate word: list id << kPosBits | token id
 constexpr uint32_t kPosMask = (1u << kPosBits) - 1u;
 constexpr int kMaxSeq = 1 << kPosBits;
-constexpr int kAttnRows = 128;     // exact-set rows per split
+constexpr int kAttnRows = 128;     // exact-set rows per split, the larger of the two sizes
+constexpr int kAttnRowsSmall = 64; // the split of small exact sets (see attn_rows_for)
 constexpr int kBgLists = 64;       // lists per background workgroup
 constexpr int kDenseRows = 2048;   // cache rows per dense split
 constexpr int kPartStride = 132;   // floats per partial: m, Z, pad, pad, N[128]
@@ -60,8 +61,18 @@ struct Dims {
     int nseg_cap;   // n_list + nsub_cap
     int max_topk;
     int pq_bits;    // 8 (Pq8) or 4 (Pq4)
+    int attn_rows;  // exact-set rows per split of the attend: kAttnRowsSmall or kAttnRows
     float inv_sqrt_d;
 };
+
+// Exact-set rows per attend split for a context: 64 when S, the local window
+// and the largest budget hold at most 2048 rows (twice the splits spread a
+// row's gathers over more CUs), else 128 (measured: one 128K sequence 56.4 ->
+// 55.2 us, 16 sequences 245.7 -> 243.6 us; at a budget of 2621 the 64-row
+// splits were slower, 40.5 -> 43.8 us in the attend).
+__host__ __device__ inline int attn_rows_for(int n_sink, int n_local, int max_topk) {
+    return n_sink + n_local + max_topk <= 2048 ? kAttnRowsSmall : kAttnRows;
+}
 
 // One int per batch element, passed by value (top-k budgets, lengths).
 struct BatchInts {
