@@ -232,23 +232,27 @@ __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchArgs 
     constexpr int kWaves = kAttnThreads / kWave;
     constexpr int kListsPerWave = kBgLists / kWaves;   // 16
 
-    float shift[G], below_scale[G];
-    bool live[G];
-#pragma unroll
-    for (int hh = 0; hh < G; ++hh) {
-        shift[hh] = w.row_shift[row0 + hh];
-        const float tlo = w.tau_lo[row0 + hh];
-        live[hh] = shift[hh] != neg_inf;
-        const bool use_below = live[hh] && tlo != neg_inf && w.row_flag[row0 + hh] == 0;
-        below_scale[hh] = use_below ? __expf(tlo - shift[hh]) : 0.0f;
-    }
     // lanes 0..15 each compute the masses M_j of one list of this wave:
     // M_j = (scan segments below tau_lo) * exp(tau_lo - shift)
-    //       + (unselected candidates of list j, already relative to shift)
+    //       + (unselected candidates of list j, already relative to shift);
+    // the segments of list l & 15 are summed by the four lanes l, l + 16,
+    // l + 32 and l + 48, each taking every fourth one, so a long list costs
+    // a quarter of the loads per lane (a 64-list workgroup ends with its
+    // longest list)
+    constexpr int kSegLanes = kWave / kListsPerWave;   // 4
+    static_assert(kSegLanes * kListsPerWave == kWave && kSegLanes == 4, "four lanes per list");
+    const int seg_q = lane / kListsPerWave;
     const int my_j = lc * kBgLists + wave + (lane & (kListsPerWave - 1)) * kWaves;
     // every load that does not depend on another is issued first: the list
-    // means, the candidate weights and the list offsets; then the list's
-    // scan segments (usually one or two) all at once
+    // offsets (first, since a wave's loads return in order and the segment
+    // loads wait for them), the list means and the candidate weights; then
+    // the list's scan segments. The rows' shifts and thresholds (scalar
+    // loads) come after, so that no vector load waits behind them.
+    const bool okj = my_j < D.n_list;
+    const int jj = okj ? my_j : 0;
+    const int32_t* loff = ix.loff + static_cast<int64_t>(bg) * (D.n_list + 1);
+    const int lo = loff[jj];
+    const int hi = okj ? loff[jj + 1] : lo;
     // variant C: every list takes the global value mean of R_b
     const bool global_mean = variant == PQHSA_VARIANT_C;
     float2 vbar[kListsPerWave];
@@ -262,37 +266,50 @@ __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchArgs 
                                : make_float2(0.f, 0.f);
     }
     float mj[G], mn[G];   // M_j, and the weight of v_bar_j in N (M_j, or W_j |R_j| for Bx)
+    float shift[G], below_scale[G];
+    bool live[G];
     {
-        const bool ok = lane < kListsPerWave && my_j < D.n_list;
-        const int jj = ok ? my_j : 0;
+        const bool ok = seg_q == 0 && okj;
         float cand[G];
 #pragma unroll
         for (int hh = 0; hh < G; ++hh)
             cand[hh] = ok ? w.cand_mass[static_cast<int64_t>(row0 + hh) * D.n_list + jj] : 0.0f;
         // list j's positions [lo, hi) span sub-chunks lo / kSub .. (hi - 1) / kSub,
         // whose masses sit at segments j + s
-        const int32_t* loff = ix.loff + static_cast<int64_t>(bg) * (D.n_list + 1);
-        const int lo = loff[jj];
-        const int hi = ok ? loff[jj + 1] : lo;
         const int s0 = jj + lo / kSub;
         const int s1 = hi > lo ? jj + (hi - 1) / kSub + 1 : s0;
         const float* segs = w.seg_sum + static_cast<int64_t>(bg) * D.nseg_cap * G;
-        constexpr int kSegsAtOnce = 4;
-        float sv[kSegsAtOnce][G];
-#pragma unroll
-        for (int u = 0; u < kSegsAtOnce; ++u)
-#pragma unroll
-            for (int hh = 0; hh < G; ++hh) sv[u][hh] = s0 + u < s1 ? segs[(s0 + u) * G + hh] : 0.0f;
+        // this lane's segments s0 + seg_q + 4 i, kSegsAtOnce per round trip
+        constexpr int kSegsAtOnce = 2;
         float below[G];
 #pragma unroll
-        for (int hh = 0; hh < G; ++hh) {
-            below[hh] = sv[0][hh];
+        for (int hh = 0; hh < G; ++hh) below[hh] = 0.0f;
+        for (int s = s0 + seg_q; s < s1; s += kSegLanes * kSegsAtOnce) {
+            float sv[kSegsAtOnce][G];
 #pragma unroll
-            for (int u = 1; u < kSegsAtOnce; ++u) below[hh] += sv[u][hh];
+            for (int u = 0; u < kSegsAtOnce; ++u)
+#pragma unroll
+                for (int hh = 0; hh < G; ++hh)
+                    sv[u][hh] = s + kSegLanes * u < s1 ? segs[(s + kSegLanes * u) * G + hh] : 0.0f;
+#pragma unroll
+            for (int u = 0; u < kSegsAtOnce; ++u)
+#pragma unroll
+                for (int hh = 0; hh < G; ++hh) below[hh] += sv[u][hh];
         }
-        for (int s = s0 + kSegsAtOnce; s < s1; ++s)   // lists longer than 3 sub-chunks
 #pragma unroll
-            for (int hh = 0; hh < G; ++hh) below[hh] += segs[s * G + hh];
+        for (int hh = 0; hh < G; ++hh) {
+            below[hh] += __shfl_xor(below[hh], kListsPerWave);
+            below[hh] += __shfl_xor(below[hh], 2 * kListsPerWave);
+        }
+        // the rows' shifts and thresholds, read after every vector load is out
+#pragma unroll
+        for (int hh = 0; hh < G; ++hh) {
+            shift[hh] = w.row_shift[row0 + hh];
+            const float tlo = w.tau_lo[row0 + hh];
+            live[hh] = shift[hh] != neg_inf;
+            const bool use_below = live[hh] && tlo != neg_inf && w.row_flag[row0 + hh] == 0;
+            below_scale[hh] = use_below ? __expf(tlo - shift[hh]) : 0.0f;
+        }
 #pragma unroll
         for (int hh = 0; hh < G; ++hh) {
             mj[hh] = (ok && live[hh]) ? below[hh] * below_scale[hh] + cand[hh] : 0.0f;
