@@ -263,7 +263,6 @@ pqhsa_status pqhsa_create(const pqhsa_shape* shape, pqhsa_ctx** out) {
     if (!c) return fail(nullptr, PQHSA_ERR_OUT_OF_MEMORY, "host allocation failed");
     c->shape = *shape;
     hipError_t e = hipGetDevice(&c->device);
-    if (e == hipSuccess) e = configure_scan();
     if (e == hipSuccess) e = configure_select();
     if (e != hipSuccess) {
         delete c;

@@ -200,7 +200,6 @@ __device__ __forceinline__ int64_t kv_row(const KV& kv, int b, int g, int t) {
 // --- launchers (each returns the launch status) -----------------------
 // Kernel attributes (large dynamic LDS) for the current device; called once
 // per context creation.
-hipError_t configure_scan();
 hipError_t configure_select();
 
 // LUT workgroups per (b, kv head) in the prologue: fine parts (8 for Pq8,

@@ -14,12 +14,11 @@
 // are spaced by the number of (batch element, KV head) units in the grid, so
 // that they share an XCD.
 //
-// The workgroup first stages the group LUT and the coarse table in LDS
-// (through registers), then each wave issues the loads of all its 64-position
-// steps (list ids, codes, norms) at once, in step order, so the arithmetic of
-// the first steps overlaps the arrival of the later ones. When the coarse
-// table does not fit in LDS beside the LUT, each lane gathers its lists'
-// coarse terms instead.
+// The workgroup first stages the group LUT in LDS (through registers), then
+// each wave issues the loads of all its 64-position steps (list ids, codes,
+// norms) at once, in step order, so the arithmetic of the first steps
+// overlaps the arrival of the later ones; each lane gathers the coarse terms
+// of its list from the group's coarse table.
 //
 // Per token and head the wave computes l~ and then either
 //   * emits (l~, list id and token id) as a top-k candidate when
@@ -48,13 +47,6 @@ namespace pqhsa {
 
 constexpr int kScanThreads = kScanWaves * kWave;
 constexpr int kIters = kSub / kWave;   // 64-position steps per sub-chunk
-// float4 of the coarse table each thread stages into LDS: room for 1024 lists
-// at G = 4 and 8 (the LUT and the table then fill 80 KB / 160 KB of LDS)
-template <int G>
-constexpr int kCoarseStage = 256 * G / kScanThreads > 1 ? 256 * G / kScanThreads : 1;
-template <int G>
-constexpr int kCoarseCapF4 = kCoarseStage<G> * kScanThreads;
-
 // The G coarse terms of one list, [n_list][G] layout.
 template <int G>
 __device__ __forceinline__ void load_coarse(const float* p, float (&v)[G]) {
@@ -98,16 +90,13 @@ constexpr int kScanLutFloats = std::is_same<PQ, Pq4>::value ? kRep4Floats : PQ::
 // so two workgroups share a CU instead of one (the codes are read twice).
 // At most 80 SGPRs per wave (a few spill to VGPR lanes): with more, a second
 // workgroup does not fit on the CU.
-template <int G, int GT, bool kCoarseLds, typename PQ, bool kDev>
+template <int G, int GT, typename PQ, bool kDev>
 __global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_num_sgpr(80))) void scan_kernel(
     Dims D, BatchArgs ba, Index ix, Work w, int nwg, int nwg_grid) {
     // the group LUT at a compile-time LDS address (so that an entry address
-    // is one shift of a code), then, when it fits, the [n_list][G] coarse
-    // table in the dynamic part
+    // is one shift of a code)
     __shared__ float4 lut4[kScanLutFloats<PQ, G> / 4];
-    extern __shared__ float4 coarse4[];
     float* lut_s = reinterpret_cast<float*>(lut4);
-    float* coarse_s = reinterpret_cast<float*>(coarse4);
     constexpr int kParts = GT / G;   // workgroups per (b, g) and sub-chunk range
     static_assert(kParts * G == GT, "head split");
     // workgroup i serves unit i mod U of the U = B Hkv kParts (b, g, part)
@@ -156,28 +145,12 @@ __global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_num_sgpr(80))) 
             st[i] = *reinterpret_cast<const float4*>(glut + (f / G) * GT + f % G);
         }
     }
-    // the coarse table, kCoarseStage float4 per thread (addresses clamped, so
-    // every load is in bounds; the LDS region is padded to the full staging size)
-    const int n_cf4 = D.n_list * G / 4;
-    float4 cst[kCoarseStage<G>];
-    if constexpr (kCoarseLds) {
-#pragma unroll
-        for (int i = 0; i < kCoarseStage<G>; ++i) {
-            const int f = min(i * kScanThreads + tid, n_cf4 - 1) * 4;   // list f / G, heads from f mod G
-            cst[i] = *reinterpret_cast<const float4*>(coarse + (f / G) * GT + f % G);
-        }
-    }
     float tlo[G];
 #pragma unroll
     for (int hh = 0; hh < G; ++hh) tlo[hh] = w.tau_lo[row0 + hh];
     float4* ldst = reinterpret_cast<float4*>(lut_s);
 #pragma unroll
     for (int i = 0; i < kStage; ++i) ldst[i * kScanThreads + tid] = st[i];
-    if constexpr (kCoarseLds) {
-#pragma unroll
-        for (int i = 0; i < kCoarseStage<G>; ++i)
-            reinterpret_cast<float4*>(coarse_s)[i * kScanThreads + tid] = cst[i];
-    }
     __syncthreads();
     for (int chunk = chunk0; chunk < nwg; chunk += nwg_grid) {
         const int sc = chunk * kScanWaves + wave;
@@ -211,12 +184,13 @@ __global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_num_sgpr(80))) 
             if (p_first >= p_end) continue;   // uniform: past the end of a short last sub-chunk
             const int p = p_first + lane;
             const bool valid = p < p_end;
-            // coarse terms of the lanes' lists: from LDS, or gathered when the
-            // coarse table does not fit beside the LUT
+            // coarse terms of the lanes' lists, gathered from the group table
+            // (neighbouring lanes mostly share a list; staging the table in
+            // LDS instead was a little slower, 12.4 against 12.3 us at 128K
+            // and 97.4 against 96.2 us at 16 sequences)
             const int j = static_cast<int>(wl[it] >> kPosBits);
             float cf[G];
-            if constexpr (kCoarseLds) load_coarse<G>(coarse_s + j * G, cf);
-            else load_coarse<G>(coarse + j * GT, cf);
+            load_coarse<G>(coarse + j * GT, cf);
             float fs[G];
             if constexpr (std::is_same<PQ, Pq4>::value) fine_sum_rep4<G>(lut_s, cv[it], fs);
             else fine_sum<PQ, G>(lut_s, cv[it], fs);
@@ -271,8 +245,7 @@ constexpr int kScanMaxChunks = 4;
 template <int G, int GT, typename PQ, bool kDev>
 static hipError_t launch_scan_d(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w,
                                 int nwg, hipStream_t s, const KTiming& tm) {
-    const size_t cf = static_cast<size_t>(kCoarseCapF4<G>) * 16;
-    static_assert(kScanLutFloats<PQ, G> * 4 + kCoarseCapF4<G> * 16 <= kScanLdsMax, "LDS budget");
+    static_assert(kScanLutFloats<PQ, G> * 4 <= kScanLdsMax, "LDS budget");
     const int n_units = D.B * D.Hkv * (GT / G);
     // chunks per workgroup: as many as the grid has rounds of the workgroups
     // that run at once (two per CU), at most kScanMaxChunks, each workgroup
@@ -290,12 +263,8 @@ static hipError_t launch_scan_d(const Dims& D, const BatchArgs& ba, const Index&
         std::min<int64_t>(kScanMaxChunks, std::max<int64_t>(1, static_cast<int64_t>(n_units) * nwg / resident)));
     const int nwg_grid = (nwg + cpw - 1) / cpw;
     const dim3 grid(n_units * nwg_grid);
-    if (D.n_list * G % 4 == 0 && D.n_list * G / 4 <= kCoarseCapF4<G>)
-        hipExtLaunchKernelGGL((scan_kernel<G, GT, true, PQ, kDev>), grid, dim3(kScanThreads), cf, s,
-                              tm.start, tm.stop, 0, D, ba, ix, w, nwg, nwg_grid);
-    else
-        hipExtLaunchKernelGGL((scan_kernel<G, GT, false, PQ, kDev>), grid, dim3(kScanThreads), 0, s,
-                              tm.start, tm.stop, 0, D, ba, ix, w, nwg, nwg_grid);
+    hipExtLaunchKernelGGL((scan_kernel<G, GT, PQ, kDev>), grid, dim3(kScanThreads), 0, s, tm.start,
+                          tm.stop, 0, D, ba, ix, w, nwg, nwg_grid);
     return hipGetLastError();
 }
 
@@ -304,31 +273,6 @@ static hipError_t launch_scan_t(const Dims& D, const BatchArgs& ba, const Index&
                                 int nwg, hipStream_t s, const KTiming& tm) {
     return w.ba_dev ? launch_scan_d<G, GT, PQ, true>(D, ba, ix, w, nwg, s, tm)
                     : launch_scan_d<G, GT, PQ, false>(D, ba, ix, w, nwg, s, tm);
-}
-
-template <typename PQ, bool kDev>
-static hipError_t configure_scan_pq() {
-    // the coarse table (dynamic) can exceed the default dynamic LDS limit
-    const void* k[] = {reinterpret_cast<const void*>(&scan_kernel<1, 1, true, PQ, kDev>),
-                       reinterpret_cast<const void*>(&scan_kernel<2, 2, true, PQ, kDev>),
-                       reinterpret_cast<const void*>(&scan_kernel<4, 4, true, PQ, kDev>),
-                       reinterpret_cast<const void*>(&scan_kernel<4, 8, true, PQ, kDev>)};
-    const int cap[] = {kCoarseCapF4<1> * 16, kCoarseCapF4<2> * 16, kCoarseCapF4<4> * 16,
-                       kCoarseCapF4<4> * 16};
-    for (int i = 0; i < 4; ++i) {
-        const hipError_t e =
-            hipFuncSetAttribute(k[i], hipFuncAttributeMaxDynamicSharedMemorySize, cap[i]);
-        if (e != hipSuccess) return e;
-    }
-    return hipSuccess;
-}
-
-hipError_t configure_scan() {
-    hipError_t e = configure_scan_pq<Pq8, false>();
-    if (e == hipSuccess) e = configure_scan_pq<Pq4, false>();
-    if (e == hipSuccess) e = configure_scan_pq<Pq8, true>();
-    if (e == hipSuccess) e = configure_scan_pq<Pq4, true>();
-    return e;
 }
 
 template <typename PQ>
