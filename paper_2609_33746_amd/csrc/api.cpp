@@ -281,6 +281,12 @@ pqhsa_status pqhsa_create(const pqhsa_shape* shape, pqhsa_ctx** out) {
     D.nseg_cap = D.n_list + D.nsub_cap;
     D.max_topk = std::max(shape->max_topk, 1);
     D.attn_rows = attn_rows_for(D.n_sink, D.n_local, shape->max_topk);
+    // the threshold sample's reads touch a cache line per run and array: many
+    // rows make the prologue bound by those lines, and longer runs halve them
+    // (16 sequences: prologue 46.6 -> 37.8 us; at one 128K sequence the
+    // prologue gained 2.3 us and the select lost 2.5 to the noisier threshold)
+    D.sample_run_log2 = D.B * D.Hq >= kSampleWideRows ? 2 : 1;
+    static_assert(kSampleRun == 2 && kSampleRunWide == 4, "run lengths as log2 1 and 2");
     D.pq_bits = shape->pq_m == Pq4::M ? Pq4::BITS : Pq8::BITS;
     D.inv_sqrt_d = static_cast<float>(1.0 / std::sqrt(static_cast<double>(kHeadDim)));
 

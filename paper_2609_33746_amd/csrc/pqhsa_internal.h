@@ -35,7 +35,9 @@ constexpr int kMaxSamples = 2048;  // sampled positions per row for the threshol
 constexpr int kSelThreads = 1024;
 constexpr int kSelCap = 12288;     // candidates of one row held in LDS by the select kernel
 constexpr int kSelMaxSub = 1024;   // sub-chunks per row on the select kernel's fast path
-constexpr int kSampleRun = 2;      // contiguous positions per sampled run
+constexpr int kSampleRun = 2;      // contiguous positions per sampled run (small grids)
+constexpr int kSampleRunWide = 4;  // the same when a call has at least kSampleWideRows rows
+constexpr int kSampleWideRows = 128;
 constexpr int kPosBits = 20;       // position / candidate word: list id << kPosBits | token id
 constexpr uint32_t kPosMask = (1u << kPosBits) - 1u;
 constexpr int kMaxSeq = 1 << kPosBits;
@@ -62,6 +64,7 @@ struct Dims {
     int max_topk;
     int pq_bits;    // 8 (Pq8) or 4 (Pq4)
     int attn_rows;  // exact-set rows per split of the attend: kAttnRowsSmall or kAttnRows
+    int sample_run_log2;   // log2 of the positions per sampled run of the prologue
     float inv_sqrt_d;
 };
 
