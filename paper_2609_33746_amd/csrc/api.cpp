@@ -39,6 +39,9 @@ struct pqhsa_ctx {
     std::vector<int32_t> cur_len;         // current cache lengths (>= seq_lens; the tail is exact)
     uint8_t* codes = nullptr;
     float* norms = nullptr;
+    uint8_t* samp_codes = nullptr;   // the threshold sample (Index::samp_*)
+    float* samp_norms = nullptr;
+    int32_t* samp_list = nullptr;
     int32_t* perm = nullptr;
     uint32_t* pos_word = nullptr;
     int32_t* loff = nullptr;
@@ -94,6 +97,9 @@ struct pqhsa_ctx {
         ix.tok_list = tok_list;
         ix.n_seq = n_seq_dev;
         ix.n_r = n_r_dev;
+        ix.samp_codes = samp_codes;
+        ix.samp_norms = samp_norms;
+        ix.samp_list = samp_list;
         return ix;
     }
 };
@@ -281,12 +287,6 @@ pqhsa_status pqhsa_create(const pqhsa_shape* shape, pqhsa_ctx** out) {
     D.nseg_cap = D.n_list + D.nsub_cap;
     D.max_topk = std::max(shape->max_topk, 1);
     D.attn_rows = attn_rows_for(D.n_sink, D.n_local, shape->max_topk);
-    // the threshold sample's reads touch a cache line per run and array: many
-    // rows make the prologue bound by those lines, and longer runs halve them
-    // (16 sequences: prologue 46.6 -> 37.8 us; at one 128K sequence the
-    // prologue gained 2.3 us and the select lost 2.5 to the noisier threshold)
-    D.sample_run_log2 = D.B * D.Hq >= kSampleWideRows ? 2 : 1;
-    static_assert(kSampleRun == 2 && kSampleRunWide == 4, "run lengths as log2 1 and 2");
     D.pq_bits = shape->pq_m == Pq4::M ? Pq4::BITS : Pq8::BITS;
     D.inv_sqrt_d = static_cast<float>(1.0 / std::sqrt(static_cast<double>(kHeadDim)));
 
@@ -317,6 +317,9 @@ pqhsa_status pqhsa_create(const pqhsa_shape* shape, pqhsa_ctx** out) {
     A(dev_alloc(c, &c->tok_list, BG * rc));
     A(dev_alloc(c, &c->ids_tm, BG * rc));
     A(dev_alloc(c, &c->codes_tm, BG * rc * static_cast<size_t>(shape->pq_m)));
+    A(dev_alloc(c, &c->samp_codes, BG * kMaxSamples * 16));
+    A(dev_alloc(c, &c->samp_norms, BG * kMaxSamples));
+    A(dev_alloc(c, &c->samp_list, BG * kMaxSamples));
     A(dev_alloc(c, &c->norms_tm, BG * rc));
     A(dev_alloc(c, &c->perm_alt, BG * rc));
     A(dev_alloc(c, &c->pos_alt, BG * rc));
@@ -393,6 +396,8 @@ static pqhsa_status relayout(pqhsa_ctx* c, const std::vector<int32_t>& lens, hip
                               static_cast<size_t>(D.B) * D.Hq * rc, stream);
     if (e != hipSuccess) return hip_fail(c, e, "launching the list-major sort");
     e = launch_prepare_gather(D, c->codes_tm, c->norms_tm, c->index(), c->codes, c->norms, stream);
+    if (e == hipSuccess)
+        e = launch_sample_slab(D, c->index(), c->samp_codes, c->samp_norms, c->samp_list, stream);
     if (e != hipSuccess) return hip_fail(c, e, "launching the index gather");
     e = launch_glob_mean(D, c->index(), c->glob_mean, stream);
     if (e == hipSuccess) e = launch_init_sums(D, c->loff, c->means, c->mean_sums, stream);
@@ -498,6 +503,8 @@ pqhsa_status pqhsa_index_update(pqhsa_ctx* c, const int32_t* new_seq_lens, const
     std::swap(c->pos_word, c->pos_alt);
     std::swap(c->loff, c->loff_alt);
     e = launch_prepare_gather(D, c->codes_tm, c->norms_tm, c->index(), c->codes, c->norms, stream);
+    if (e == hipSuccess)
+        e = launch_sample_slab(D, c->index(), c->samp_codes, c->samp_norms, c->samp_list, stream);
     if (e == hipSuccess) e = launch_glob_mean(D, c->index(), c->glob_mean, stream);
     if (e != hipSuccess) return hip_fail(c, e, "launching the index rebuild");
     int nr_max = 0;

@@ -35,9 +35,7 @@ constexpr int kMaxSamples = 2048;  // sampled positions per row for the threshol
 constexpr int kSelThreads = 1024;
 constexpr int kSelCap = 12288;     // candidates of one row held in LDS by the select kernel
 constexpr int kSelMaxSub = 1024;   // sub-chunks per row on the select kernel's fast path
-constexpr int kSampleRun = 2;      // contiguous positions per sampled run (small grids)
-constexpr int kSampleRunWide = 4;  // the same when a call has at least kSampleWideRows rows
-constexpr int kSampleWideRows = 128;
+constexpr int kSampleRun = 2;      // contiguous positions per sampled run
 constexpr int kPosBits = 20;       // position / candidate word: list id << kPosBits | token id
 constexpr uint32_t kPosMask = (1u << kPosBits) - 1u;
 constexpr int kMaxSeq = 1 << kPosBits;
@@ -64,7 +62,6 @@ struct Dims {
     int max_topk;
     int pq_bits;    // 8 (Pq8) or 4 (Pq4)
     int attn_rows;  // exact-set rows per split of the attend: kAttnRowsSmall or kAttnRows
-    int sample_run_log2;   // log2 of the positions per sampled run of the prologue
     float inv_sqrt_d;
 };
 
@@ -106,7 +103,31 @@ struct Index {
     const uint16_t* tok_list;  // [B, Hkv, rcap] list id a_i of each token i of R (by token id)
     const int32_t* n_seq;      // [B]
     const int32_t* n_r;        // [B] |R_b|
+    // the threshold sample's positions, gathered once per prepare or update
+    // (sample_position) so that the prologue reads them contiguously
+    const uint8_t* samp_codes;  // [B, Hkv, kMaxSamples] codes (16 bytes a slot)
+    const float* samp_norms;    // [B, Hkv, kMaxSamples]
+    const int32_t* samp_list;   // [B, Hkv, kMaxSamples] list id
 };
+
+// The s-th position of the threshold sample of a row with n_r > 0 indexed
+// tokens: runs of kSampleRun positions, rs = n_r / nrun apart, clipped at
+// the next run. Returns false when s lies past the sample (sample count:
+// nrun * run_len).
+struct SampleRuns {
+    int nrun, rs, run_len;
+};
+__host__ __device__ inline SampleRuns sample_runs(int n_r) {
+    const int nrun = min(kMaxSamples / kSampleRun, (n_r + kSampleRun - 1) / kSampleRun);
+    const int rs = n_r / nrun;
+    return SampleRuns{nrun, rs, min(kSampleRun, rs)};
+}
+__host__ __device__ inline bool sample_position(const SampleRuns& sr, int s, int n_r, int& pos) {
+    const int run = s / kSampleRun;
+    const int within = s % kSampleRun;
+    pos = run * sr.rs + within;
+    return run < sr.nrun && within < sr.run_len && pos < n_r;
+}
 
 // Decode workspace, owned by the context.
 struct Work {
@@ -317,6 +338,10 @@ hipError_t launch_update_lists(const Dims& D, const BatchInts& lo, const BatchIn
 // float64 value sums of the lists, |R_j| v_bar_j, for later updates
 hipError_t launch_init_sums(const Dims& D, const int32_t* loff, const float* means, double* sums,
                             hipStream_t s);
+// The threshold sample's codes, norms and list ids per (b, kv head), from the
+// list-major index (after every prepare and update).
+hipError_t launch_sample_slab(const Dims& D, const Index& ix, uint8_t* samp_codes, float* samp_norms,
+                              int32_t* samp_list, hipStream_t s);
 hipError_t launch_prepare_gather(const Dims& D, const uint8_t* codes_in, const float* norms_in,
                                  const Index& ix, uint8_t* codes_out, float* norms_out,
                                  hipStream_t s);

@@ -53,6 +53,41 @@ hipError_t launch_prepare_gather(const Dims& D, const uint8_t* codes_in, const f
     return hipGetLastError();
 }
 
+// The threshold sample of each (b, kv head): sample slot s takes the code,
+// norm and list id of list-major position sample_position(s) (slot data of
+// positions past the sample are those of position 0, never used).
+template <typename PQ>
+__global__ __launch_bounds__(256) void sample_slab_kernel(Dims D, Index ix,
+                                                          typename PQ::Code* __restrict__ codes_out,
+                                                          float* __restrict__ norms_out,
+                                                          int32_t* __restrict__ list_out) {
+    const int bg = blockIdx.x;
+    const int b = bg / D.Hkv;
+    const int n_r = ix.n_r[b];
+    const int64_t base = static_cast<int64_t>(bg) * D.rcap;
+    const typename PQ::Code* codes = reinterpret_cast<const typename PQ::Code*>(ix.codes) + base;
+    const SampleRuns sr = sample_runs(max(n_r, 1));
+    for (int sl = threadIdx.x; sl < kMaxSamples; sl += 256) {
+        int pos = 0;
+        if (n_r == 0 || !sample_position(sr, sl, n_r, pos)) pos = 0;
+        const int64_t o = static_cast<int64_t>(bg) * kMaxSamples + sl;
+        codes_out[o] = codes[pos];
+        norms_out[o] = ix.norms[base + pos];
+        list_out[o] = static_cast<int32_t>(ix.pos_word[base + pos] >> kPosBits);
+    }
+}
+
+hipError_t launch_sample_slab(const Dims& D, const Index& ix, uint8_t* samp_codes, float* samp_norms,
+                              int32_t* samp_list, hipStream_t s) {
+    if (D.pq_bits == 4)
+        hipLaunchKernelGGL(sample_slab_kernel<Pq4>, dim3(D.B * D.Hkv), dim3(256), 0, s, D, ix,
+                           reinterpret_cast<uint32_t*>(samp_codes), samp_norms, samp_list);
+    else
+        hipLaunchKernelGGL(sample_slab_kernel<Pq8>, dim3(D.B * D.Hkv), dim3(256), 0, s, D, ix,
+                           reinterpret_cast<uint4*>(samp_codes), samp_norms, samp_list);
+    return hipGetLastError();
+}
+
 // Global value mean over R_b per (b, g) for variant C (Appendix B): the list
 // means weighted by the list sizes, sum_j |R_j| v_bar_j / |R_b| (0 for an
 // empty R_b), accumulated in float64. Workgroup (b g, dimension chunk):

@@ -14,7 +14,7 @@
 // kernel advances).
 //
 // Sample role, per (batch element, query head) row: scores a stratified
-// sample of the row's list-major positions (contiguous runs of 2 or 4
+// sample of the row's list-major positions (contiguous runs of kSampleRun
 // positions, evenly spread) and takes a sample order statistic as the
 // candidate threshold tau_lo, chosen so that about twice k tokens of the
 // whole row score at or above it. The role issues its sample loads, then
@@ -55,7 +55,7 @@ constexpr int kSpinLimit = 1 << 16;                        // poll rounds before
 static_assert(kFineWg * Pq8::K == kProThreads && Pq8::M / kFineWg == 8, "Pq8 fine tiling");
 static_assert(Pq4::LUT_ROW <= kProThreads, "Pq4 fine table: one codeword per thread");
 static_assert(kCoarsePer * kCoarseGroups == kCoarseLists, "coarse tiling");
-static_assert(kSamplesPer * kProThreads == kMaxSamples && kMaxSamples % kSampleRunWide == 0, "samples");
+static_assert(kSamplesPer * kProThreads == kMaxSamples && kMaxSamples % kSampleRun == 0, "samples");
 
 // (q / sqrt(d)) . c over 16 lanes of 8 dimensions each; every lane of the
 // 16-lane group receives the same sum.
@@ -228,18 +228,18 @@ __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, 
     // device counter), so that a replayed graph of the call still tells the
     // LUT parts' fresh flags from stale ones
     const uint32_t ep = tid < kWave ? counter_read(w.epoch + bg) + 1u : 0u;
-    // 1) the samples: runs of 2 (or 4, for many rows) positions, rs apart (rs >= 1),
-    //    clipped at the next run; thread tid owns samples u * 512 + tid, so
-    //    neighbouring lanes read neighbouring positions (short runs: scores
-    //    within a list are correlated, so many short runs estimate the
-    //    quantile with far less spread than a few long ones)
-    const int run_log2 = D.sample_run_log2;
-    const int run_max = 1 << run_log2;
-    const int nrun = min(kMaxSamples >> run_log2, (n_r + run_max - 1) >> run_log2);
-    const int rs = n_r / nrun;
-    const int run_len = min(run_max, rs);
-    const int64_t base = static_cast<int64_t>(bg) * D.rcap;
-    const typename PQ::Code* codes = reinterpret_cast<const typename PQ::Code*>(ix.codes) + base;
+    // 1) the samples: runs of kSampleRun positions, rs apart (rs >= 1),
+    //    clipped at the next run (short runs: scores within a list
+    //    are correlated, so many short runs estimate the quantile with far
+    //    less spread than a few long ones). Their codes, norms and lists were
+    //    gathered at the index's last prepare or update into one contiguous
+    //    slab per KV head: thread tid reads slots u * 512 + tid, one cache
+    //    line per 128-byte span instead of one per run and array.
+    const SampleRuns sr = sample_runs(n_r);
+    const int nrun = sr.nrun;
+    const int run_len = sr.run_len;
+    const int64_t sbase = static_cast<int64_t>(bg) * kMaxSamples;
+    const typename PQ::Code* scodes = reinterpret_cast<const typename PQ::Code*>(ix.samp_codes) + sbase;
     typename PQ::Code cv[kSamplesPer];
     float rv[kSamplesPer];
     int jv[kSamplesPer];
@@ -247,14 +247,11 @@ __device__ __forceinline__ void sample_role(const Dims& D, const BatchArgs& ba, 
 #pragma unroll
     for (int u = 0; u < kSamplesPer; ++u) {
         const int s = u * kProThreads + tid;
-        const int run = s >> run_log2;
-        const int within = s & (run_max - 1);
-        const int pos = run * rs + within;
-        ok[u] = run < nrun && within < run_len && pos < n_r;
-        const int p = ok[u] ? pos : 0;
-        cv[u] = codes[p];
-        rv[u] = ix.norms[base + p];
-        jv[u] = static_cast<int>(ix.pos_word[base + p] >> kPosBits);
+        int pos;
+        ok[u] = sample_position(sr, s, n_r, pos);
+        cv[u] = scodes[s];
+        rv[u] = ix.samp_norms[sbase + s];
+        jv[u] = ix.samp_list[sbase + s];
     }
     for (int i = tid; i < kHistBins; i += kProThreads) sm.hist[i] = 0;
 
