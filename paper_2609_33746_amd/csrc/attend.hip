@@ -26,6 +26,7 @@
 namespace pqhsa {
 
 constexpr int kAttnThreads = 256;    // 4 waves x 4 groups of 16 lanes = 16 row streams
+constexpr int kAttnBgFirstPerCu = 4; // attend grids above this many workgroups per CU put the background first
 constexpr int kStreams = kAttnThreads / 16;
 // rows per stream in one batch of the dense kernel (two batches are in
 // flight; fewer for large groups, which hold G accumulators per lane)
@@ -111,22 +112,26 @@ template <typename T, int G, bool kBx, bool kDev, int kRows>
 __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchArgs ba, KV kv,
                                                               Index ix, Work w, int nsplit,
                                                               int nsplit_max, int n_bgc,
-                                                              int variant) {
+                                                              int variant, int bg_first) {
     constexpr int kRowsPerStream = kRows / kStreams;
     __shared__ float sm[kStreams], sz[kStreams];
     // [16 streams][d] for the exact role, [4 waves][G][d] for the background role
     __shared__ float sacc[(kStreams > 4 * G ? kStreams : 4 * G) * kHeadDim];
     __shared__ float bz[4][G];
     const int n_exact_wg = D.B * D.Hq * nsplit;
+    const int n_bg_wg = variant == PQHSA_VARIANT_T ? 0 : D.B * D.Hkv * n_bgc;
+    const int first_exact = bg_first ? n_bg_wg : 0;      // grid order of the two roles
+    const int first_bg = bg_first ? 0 : n_exact_wg;
     const int P = nsplit_max + n_bgc;
     const int lane16 = threadIdx.x & 15;
     const int stream = threadIdx.x >> 4;
     const float neg_inf = -__builtin_huge_valf();
 
-    if (static_cast<int>(blockIdx.x) < n_exact_wg) {
+    const int xid = static_cast<int>(blockIdx.x) - first_exact;
+    if (xid >= 0 && xid < n_exact_wg) {
         // ---------------- exact attention over a split of E ----------------
-        const int row = blockIdx.x / nsplit;
-        const int split = blockIdx.x % nsplit;
+        const int row = xid / nsplit;
+        const int split = xid % nsplit;
         const int b = row / D.Hq;
         const int h = row % D.Hq;
         const int g = h / G;
@@ -221,7 +226,7 @@ __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchArgs 
     }
 
     // ---------------- per-list background (Eq. 4) ----------------
-    const int idx = blockIdx.x - n_exact_wg;
+    const int idx = static_cast<int>(blockIdx.x) - first_bg;
     const int bg = idx / n_bgc;
     const int lc = idx % n_bgc;
     const int b = bg / D.Hkv;
@@ -528,13 +533,18 @@ static hipError_t launch_attend_d(const Dims& D, const BatchArgs& ba, const KV& 
     const int n_bgc = (D.n_list + kBgLists - 1) / kBgLists;   // the partials' layout
     // variant T has no background: the background workgroups are not launched
     const int grid = D.B * D.Hq * nsplit + (variant == PQHSA_VARIANT_T ? 0 : D.B * D.Hkv * n_bgc);
+    // Beyond about one round of resident workgroups, the background workgroups
+    // (the longer chain of loads) go first, so that they do not start only
+    // after every exact workgroup: 4 sequences at 128K, 40.7 -> 39.4 us. In a
+    // single round the exact ones go first (0.3 us better at one sequence).
+    const int bg_first = grid > kAttnBgFirstPerCu * device_cu_count() ? 1 : 0;
     auto kern = variant == PQHSA_VARIANT_BX
                     ? (D.attn_rows == kAttnRowsSmall ? attend_kernel<T, G, true, kDev, kAttnRowsSmall>
                                                      : attend_kernel<T, G, true, kDev, kAttnRows>)
                     : (D.attn_rows == kAttnRowsSmall ? attend_kernel<T, G, false, kDev, kAttnRowsSmall>
                                                      : attend_kernel<T, G, false, kDev, kAttnRows>);
     hipExtLaunchKernelGGL(kern, dim3(grid), dim3(kAttnThreads), 0, s, tm.start, tm.stop, 0, D, ba, kv,
-                          ix, w, nsplit, nsplit_max, n_bgc, variant);
+                          ix, w, nsplit, nsplit_max, n_bgc, variant, bg_first);
     return hipGetLastError();
 }
 

@@ -74,6 +74,20 @@ __host__ __device__ inline int attn_rows_for(int n_sink, int n_local, int max_to
     return n_sink + n_local + max_topk <= 2048 ? kAttnRowsSmall : kAttnRows;
 }
 
+// Compute units of the current device (0 if the runtime cannot say), read
+// once per process; launch shapes that depend on how many workgroups run at
+// once use it.
+inline int device_cu_count() {
+    static const int n_cu = [] {
+        int dev = 0, n = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+            return 0;
+        return n;
+    }();
+    return n_cu;
+}
+
 // One int per batch element, passed by value (top-k budgets, lengths).
 struct BatchInts {
     int32_t v[kMaxBatch];

@@ -251,13 +251,7 @@ static hipError_t launch_scan_d(const Dims& D, const BatchArgs& ba, const Index&
     // that run at once (two per CU), at most kScanMaxChunks, each workgroup
     // staging its tables once for all of them (at 4 and 16 sequences 4
     // chunks per workgroup beat 1, 2, 8 and 16)
-    static const int n_cu = [] {
-        int dev = 0, n = 0;
-        if (hipGetDevice(&dev) != hipSuccess ||
-            hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-            return 0;
-        return n;
-    }();
+    const int n_cu = device_cu_count();
     const int64_t resident = static_cast<int64_t>(2) * (n_cu > 0 ? n_cu : 1);
     const int cpw = static_cast<int>(
         std::min<int64_t>(kScanMaxChunks, std::max<int64_t>(1, static_cast<int64_t>(n_units) * nwg / resident)));

@@ -498,13 +498,7 @@ __global__ __launch_bounds__(kSelThreads) __attribute__((amdgpu_num_sgpr(80))) v
 // The small-capacity select when the rows outnumber the CUs and two of its
 // workgroups fit in one CU's LDS.
 static bool select_small(const Dims& D) {
-    static const int n_cu = [] {
-        int dev = 0, n = 0;
-        if (hipGetDevice(&dev) != hipSuccess ||
-            hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-            return 0;
-        return n;
-    }();
+    const int n_cu = device_cu_count();
     constexpr size_t kLdsPerCu = 160 * 1024;
     constexpr size_t kStatic = sizeof(SelectScratch) + sizeof(BlockScratch);
     return n_cu > 0 && D.B * D.Hq > n_cu &&
