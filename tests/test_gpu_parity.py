@@ -290,15 +290,18 @@ def test_variant_full_size(variant):
 
 
 @pytest.mark.timeout(600)
-def test_variant_bx_batched_full_size():
-    """Bx at 128K with four sequences and groups of 8 query heads; every row."""
+@pytest.mark.parametrize("variant", list(VARIANTS))
+def test_variant_batched_full_size(variant):
+    """Each variant at 128K with four sequences and groups of 8 query heads,
+    every row: an attend grid of several rounds, which puts the background
+    workgroups first (none for T)."""
     wl = synth.workload(3)
     inp = make(wl, seed=2)
     ctx = context(inp)
-    ctx.set_option(pqhsa.OPT_VARIANT, pqhsa.VARIANT_BX)
+    ctx.set_option(pqhsa.OPT_VARIANT, VARIANTS[variant])
     topk, out, sel, unsel, _ = run(ctx, inp)
     rows = [(b, h) for b in range(wl.batch) for h in range(wl.n_q_heads)]
-    check_rows(inp, topk, rows, out, sel, unsel, variant="Bx")
+    check_rows(inp, topk, rows, out, sel, unsel, variant=variant)
 
 
 VARIANT_EDGE = {
