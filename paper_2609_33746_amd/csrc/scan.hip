@@ -70,11 +70,33 @@ __device__ __forceinline__ void load_coarse(const float* p, float (&v)[G]) {
 template <int G>
 __device__ __forceinline__ void flush_segment(float* seg_row, float (&acc)[G]) {
     float mine = 0.0f;
+    if constexpr (G == 4) {
+        // the four heads reduced together: two exchanges within each quad
+        // leave lane l with its quad's sum of head l & 3, two row rotations
+        // by 4 and 8 lanes sum the row's quads, and two lane swaps between
+        // rows (16 and 32 apart) sum the rows
+        const int lane = lane_id();
+        const bool b0 = lane & 1, b1 = lane & 2;
+        const float p = (b0 ? acc[1] : acc[0]) + dpp<0xB1>(b0 ? acc[0] : acc[1]);   // quad_perm [1,0,3,2]
+        const float q = (b0 ? acc[3] : acc[2]) + dpp<0xB1>(b0 ? acc[2] : acc[3]);
+        float u = (b1 ? q : p) + dpp<0x4E>(b1 ? p : q);                            // quad_perm [2,3,0,1]
+        u += dpp<0x124>(u);   // row_ror:4
+        u += dpp<0x128>(u);   // row_ror:8
+        const uint32_t ub = __float_as_uint(u);
+        const auto r16 = __builtin_amdgcn_permlane16_swap(ub, ub, false, false);
+        u = __uint_as_float(r16[0]) + __uint_as_float(r16[1]);
+        const uint32_t vb = __float_as_uint(u);
+        const auto r32 = __builtin_amdgcn_permlane32_swap(vb, vb, false, false);
+        mine = __uint_as_float(r32[0]) + __uint_as_float(r32[1]);
 #pragma unroll
-    for (int hh = 0; hh < G; ++hh) {
-        const float tot = wave_sum(acc[hh]);
-        if (lane_id() == hh) mine = tot;
-        acc[hh] = 0.0f;
+        for (int hh = 0; hh < G; ++hh) acc[hh] = 0.0f;
+    } else {
+#pragma unroll
+        for (int hh = 0; hh < G; ++hh) {
+            const float tot = wave_sum(acc[hh]);
+            if (lane_id() == hh) mine = tot;
+            acc[hh] = 0.0f;
+        }
     }
     if (lane_id() < G) seg_row[lane_id()] = mine;
 }
