@@ -206,6 +206,7 @@ __global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_num_sgpr(80))) 
             if (p_first >= p_end) continue;   // uniform: past the end of a short last sub-chunk
             const int p = p_first + lane;
             const bool valid = p < p_end;
+            const uint64_t vmask = __builtin_amdgcn_ballot_w64(valid);
             // coarse terms of the lanes' lists, gathered from the group table
             // (neighbouring lanes mostly share a list; staging the table in
             // LDS instead was a little slower, 12.4 against 12.3 us at 128K
@@ -230,7 +231,7 @@ __global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_num_sgpr(80))) 
 #pragma unroll
                 for (int hh = 0; hh < G; ++hh) acc[hh] += in ? e[hh] : 0.0f;
                 flush_segment<G>(segs + cur * GT, acc);
-                const int nxt = __popcll(__ballot(valid && j <= cur));
+                const int nxt = __popcll(__builtin_amdgcn_ballot_w64(j <= cur) & vmask);
                 cur = __builtin_amdgcn_readlane(j, nxt);
             }
             {
@@ -241,9 +242,11 @@ __global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_num_sgpr(80))) 
             // candidates >= tau_lo, compacted in position order
 #pragma unroll
             for (int hh = 0; hh < G; ++hh) {
-                const uint64_t mask = __ballot(valid && s[hh] >= tlo[hh]);
+                // ballots of bare compares, masked by the valid lanes' ballot,
+                // stay lane masks in scalar registers
+                const uint64_t mask = __builtin_amdgcn_ballot_w64(s[hh] >= tlo[hh]) & vmask;
                 if (mask) {
-                    if ((mask >> lane) & 1ull) {
+                    if (valid && s[hh] >= tlo[hh]) {
                         const int64_t o = static_cast<int64_t>(row0 + hh) * D.rcap + p_begin +
                                           cbase[hh] + lanes_below(mask);
                         w.cand[o] = make_uint2(__float_as_uint(s[hh]), wl[it]);
