@@ -46,6 +46,7 @@
 namespace pqhsa {
 
 constexpr int kScanThreads = kScanWaves * kWave;
+constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kIters = kSub / kWave;   // 64-position steps per sub-chunk
 // The G coarse terms of one list, [n_list][G] layout.
 template <int G>
@@ -89,13 +90,13 @@ __device__ __forceinline__ void flush_segment(float* seg_row, float (&acc)[G]) {
         const auto r32 = __builtin_amdgcn_permlane32_swap(vb, vb, false, false);
         mine = __uint_as_float(r32[0]) + __uint_as_float(r32[1]);
 #pragma unroll
-        for (int hh = 0; hh < G; ++hh) acc[hh] = 0.0f;
+        for (int hh = 0; hh < G; ++hh) acc[hh] = -0.0f;
     } else {
 #pragma unroll
         for (int hh = 0; hh < G; ++hh) {
             const float tot = wave_sum(acc[hh]);
             if (lane_id() == hh) mine = tot;
-            acc[hh] = 0.0f;
+            acc[hh] = -0.0f;
         }
     }
     if (lane_id() < G) seg_row[lane_id()] = mine;
@@ -167,9 +168,12 @@ __global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_num_sgpr(80))) 
             st[i] = *reinterpret_cast<const float4*>(glut + (f / G) * GT + f % G);
         }
     }
-    float tlo[G];
+    float tlo[G], tlo_l2e[G];   // tau_lo, and tau_lo log2(e) for the masses' exp2
 #pragma unroll
-    for (int hh = 0; hh < G; ++hh) tlo[hh] = w.tau_lo[row0 + hh];
+    for (int hh = 0; hh < G; ++hh) {
+        tlo[hh] = w.tau_lo[row0 + hh];
+        tlo_l2e[hh] = tlo[hh] * kLog2e;
+    }
     float4* ldst = reinterpret_cast<float4*>(lut_s);
 #pragma unroll
     for (int i = 0; i < kStage; ++i) ldst[i * kScanThreads + tid] = st[i];
@@ -198,7 +202,7 @@ __global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_num_sgpr(80))) 
         float acc[G];
         int cbase[G];
 #pragma unroll
-        for (int hh = 0; hh < G; ++hh) { acc[hh] = 0.0f; cbase[hh] = 0; }
+        for (int hh = 0; hh < G; ++hh) { acc[hh] = -0.0f; cbase[hh] = 0; }   // -0 + x folds to x
 
 #pragma unroll
         for (int it = 0; it < kIters; ++it) {
@@ -217,11 +221,17 @@ __global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_num_sgpr(80))) 
             float fs[G];
             if constexpr (std::is_same<PQ, Pq4>::value) fine_sum_rep4<G>(lut_s, cv[it], fs);
             else fine_sum<PQ, G>(lut_s, cv[it], fs);
+            // exp(l~ - tau_lo) as exp2(r log2(e) (coarse + fine) - tau_lo log2(e)):
+            // one FMA per head, with r log2(e) shared by the G heads
+            const float r_l2e = rv[it] * kLog2e;
             float s[G], e[G];
 #pragma unroll
             for (int hh = 0; hh < G; ++hh) {
+                const float x = cf[hh] + fs[hh];
                 s[hh] = pq_logit(rv[it], cf[hh], fs[hh]);
-                e[hh] = (valid && s[hh] < tlo[hh]) ? __expf(s[hh] - tlo[hh]) : 0.0f;
+                e[hh] = (valid && s[hh] < tlo[hh])
+                            ? __builtin_amdgcn_exp2f(__builtin_fmaf(r_l2e, x, -tlo_l2e[hh]))
+                            : 0.0f;
             }
             // close the lists that end inside this step (lists are contiguous and
             // ascending along the lanes)
