@@ -18,6 +18,7 @@ struct SelectScratch {
     int hist[256];
     int bcast[4];
     int wave_tot[16];
+    int wave_aux[16];
 };
 
 // hist[digit] += 1 for every active lane. Lanes that share a digit are

@@ -18,6 +18,8 @@
 // Each wave loads the counts of its own sub-chunks and scans them with DPP,
 // candidate loads are issued in batches, and every workgroup-wide step is one
 // scan or reduction, so the dependency chain stays short.
+#include <type_traits>
+
 #include "device_common.h"
 #include "hist_select.h"
 #include "pq_score.h"
@@ -27,7 +29,10 @@
 namespace pqhsa {
 
 constexpr int kNW = kSelThreads / kWave;
-constexpr int kRankCap = 128;          // boundary-bin keys ranked exactly (O(m^2 / 64) ballots)
+constexpr int kRankCap = 128;
+constexpr int kNzSubBits = 10;           // sub-chunk bits of a nonempty-list entry
+static_assert((1 << kNzSubBits) >= kSelMaxSub, "sub-chunk ids");
+static_assert(kSelCap < (1 << (31 - kNzSubBits)), "first-candidate indices");          // boundary-bin keys ranked exactly (O(m^2 / 64) ballots)
 constexpr float kMassScale = 1099511627776.0f;       // 2^40: fixed-point weights
 constexpr float kMassUnscale = 1.0f / 1099511627776.0f;
 
@@ -119,7 +124,8 @@ __device__ __forceinline__ bool rank_boundary_bin(KeyAt key_at, TokAt tok_at, in
 // LDS layout of select_kernel (dynamic, 4-byte words), for kCap candidates:
 //   keys [kCap] | cand [kCap] | hist [kHistBins] | rank_key [kRankCap] |
 //   rank_idx [kRankCap] | rank_tok [kRankCap] | chosen bitmap [kCap / 32] |
-//   counter, flags [4] | sub-chunk offsets [kSelMaxSub] | mass (uint64) [n_list]
+//   counter, flags [4] | sub-chunk offsets, or the nonempty sub-chunks, [kSelMaxSub] |
+//   mass (uint64) [n_list]
 template <int kCap>
 struct SelLayout {
     static constexpr int kOffCand = kCap;
@@ -129,10 +135,11 @@ struct SelLayout {
     static constexpr int kOffRTok = kOffRIdx + kRankCap;
     static constexpr int kOffBits = kOffRTok + kRankCap;
     static constexpr int kOffCounter = kOffBits + kCap / 32;
-    static constexpr int kOffPre = kOffCounter + 4;
-    static constexpr int kOffMass = (kOffPre + kSelMaxSub + 1) & ~1;   // 8-byte aligned
+    static constexpr int kOffSub = kOffCounter + 4;
+    static constexpr int kOffMass = (kOffSub + kSelMaxSub + 1) & ~1;   // 8-byte aligned
     static size_t bytes(int n_list) { return static_cast<size_t>(kOffMass + 2 * n_list) * 4; }
     static_assert(kCap % kSelThreads == 0 && kCap % 32 == 0, "whole copy tiers and bitmap words");
+    static_assert(kOffCand % 4 == 0, "16-byte candidate stores");
 };
 // Two capacities: every row's candidates of a large budget in LDS (one
 // workgroup per CU), or fewer (two workgroups per CU, for grids of more rows
@@ -140,7 +147,7 @@ struct SelLayout {
 constexpr int kSelCapSmall = 7168;
 
 // Copy the row's `total` candidates (1 <= total <= N * kSelThreads) from
-// their sub-chunk slots into LDS in position order: keys at lds[i], words
+// their sub-chunk slots into LDS in position order (one workgroup per CU): keys at lds[i], words
 // (list << kPosBits | token) at lds[kOffCand + i]. Thread t copies the
 // indices u * kSelThreads + t, so neighbouring lanes read neighbouring
 // slots. Candidate i lives in the sub-chunk sc with pre[sc] <= i < pre[sc + 1]
@@ -152,7 +159,7 @@ constexpr int kSelCapSmall = 7168;
 // With fixed bins (hist != nullptr), every candidate is also counted in
 // hist at bin min((key - bkmin) >> bsh, kHistBins - 1).
 template <int N, int kOffCand>
-__device__ __forceinline__ void copy_candidates(const uint2* __restrict__ cand, const int* pre,
+__device__ __forceinline__ void copy_candidates_search(const uint2* __restrict__ cand, const int* pre,
                                                 int nsub, int total, uint32_t* lds,
                                                 uint32_t& kmin, uint32_t& kmax, int* hist,
                                                 uint32_t bkmin, int bsh) {
@@ -194,6 +201,79 @@ __device__ __forceinline__ void copy_candidates(const uint2* __restrict__ cand, 
         }
         // one LDS atomic per candidate: their bins are mostly distinct
         if (hist && ci < total) atomicAdd(&hist[fixed_bin(kk, bkmin, bsh)], 1);
+    }
+}
+
+// The same copy for two workgroups per CU, where the select's VALU work
+// binds: keys at lds[i], words (list << kPosBits | token) at
+// lds[kOffCand + i]. nzl lists the row's n_nz
+// nonempty sub-chunks in position order, each as (index of its first
+// candidate << kNzSubBits | sub-chunk). Thread t copies the N consecutive
+// indices N t .. N t + N - 1: one binary search over nzl finds the entry of
+// the first, and since every listed sub-chunk holds at least one candidate,
+// index N t + u lies at most u entries further, which one batch of N reads
+// settles. All loads are issued before any is used, so the copy costs one
+// search chain and one memory round trip (indices past the end repeat the
+// last candidate's load). Tracks this thread's min / max key.
+// With fixed bins (hist != nullptr), every candidate is also counted in
+// hist at bin min((key - bkmin) >> bsh, kHistBins - 1).
+template <int N, int kOffCand>
+__device__ __forceinline__ void copy_candidates_runs(const uint2* __restrict__ cand, const int* nzl,
+                                                int n_nz, int total, uint32_t* lds,
+                                                uint32_t& kmin, uint32_t& kmax, int* hist,
+                                                uint32_t bkmin, int bsh) {
+    const int tid = threadIdx.x;
+    const int i0 = min(N * tid, total - 1);
+    int k = 0;   // the last entry whose first index is <= i0
+#pragma unroll
+    for (int step = kSelMaxSub / 2; step > 0; step >>= 1) {
+        const int t = k + step;
+        if (t < n_nz && (nzl[min(t, n_nz - 1)] >> kNzSubBits) <= i0) k = t;
+    }
+    int ent[N];   // entries k .. k + N - 1 (the last one repeated past the list)
+#pragma unroll
+    for (int v = 0; v < N; ++v) ent[v] = nzl[min(k + v, n_nz - 1)];
+    uint2 rec[N];
+#pragma unroll
+    for (int u = 0; u < N; ++u) {
+        const int i = min(N * tid + u, total - 1);
+        int e = ent[0];
+#pragma unroll
+        for (int v = 1; v <= u && v < N; ++v)
+            if ((ent[v] >> kNzSubBits) <= i) e = ent[v];
+        const int sc = e & ((1 << kNzSubBits) - 1);
+        rec[u] = cand[static_cast<int64_t>(sc) * kSub + (i - (e >> kNzSubBits))];
+    }
+    uint32_t kk[N], cw[N];
+#pragma unroll
+    for (int u = 0; u < N; ++u) {
+        kk[u] = float_key(__uint_as_float(rec[u].x));
+        cw[u] = rec[u].y;
+    }
+    // the thread's N slots (< N * kSelThreads <= the LDS capacity; slots past
+    // total are never read), 16 bytes per store when N allows
+    if constexpr (N % 4 == 0) {
+#pragma unroll
+        for (int u = 0; u < N; u += 4) {
+            *reinterpret_cast<uint4*>(lds + N * tid + u) = make_uint4(kk[u], kk[u + 1], kk[u + 2], kk[u + 3]);
+            *reinterpret_cast<uint4*>(lds + kOffCand + N * tid + u) =
+                make_uint4(cw[u], cw[u + 1], cw[u + 2], cw[u + 3]);
+        }
+    } else {
+#pragma unroll
+        for (int u = 0; u < N; ++u) {
+            lds[N * tid + u] = kk[u];
+            lds[kOffCand + N * tid + u] = cw[u];
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < N; ++u) {
+        if (N * tid + u < total) {
+            kmin = min(kmin, kk[u]);
+            kmax = max(kmax, kk[u]);
+            // one LDS atomic per candidate: their bins are mostly distinct
+            if (hist) atomicAdd(&hist[fixed_bin(kk[u], bkmin, bsh)], 1);
+        }
     }
 }
 
@@ -274,7 +354,12 @@ __device__ __forceinline__ void select_row(const Dims& D, const BatchArgs& ba, c
     int* r_tok = reinterpret_cast<int*>(lds + L::kOffRTok);
     uint32_t* chosen = lds + L::kOffBits;
     int* counter = reinterpret_cast<int*>(lds + L::kOffCounter);
-    int* pre = reinterpret_cast<int*>(lds + L::kOffPre);
+    // the copy by nonempty sub-chunks where two workgroups share a CU (1.2 us
+    // faster at 512 rows), by a search of every index over the sub-chunk
+    // offsets with one workgroup per CU (0.4 us faster at 32 rows: its loads
+    // of neighbouring lanes touch neighbouring slots)
+    constexpr bool kRunsCopy = kCap == kSelCapSmall;
+    int* subl = reinterpret_cast<int*>(lds + L::kOffSub);
     __shared__ SelectScratch ss;
     __shared__ BlockScratch bs;
     const int tid = threadIdx.x;
@@ -306,21 +391,33 @@ __device__ __forceinline__ void select_row(const Dims& D, const BatchArgs& ba, c
     const int32_t* cnt = w.cand_cnt + static_cast<int64_t>(row) * D.nsub_cap;
     int c_l = 0, incl = 0;
     int total = 0;
+    int n_nz = 0;   // nonempty sub-chunks of the row
     if (small_nsub) {
         const int sc = wave * spw + lane;
         c_l = (lane < spw && sc < nsub) ? cnt[sc] : 0;
         incl = wave_incl_scan_i32(c_l);
-        if (lane == kWave - 1) ss.wave_tot[wave] = incl;
+        const uint64_t nzm = kRunsCopy ? __builtin_amdgcn_ballot_w64(c_l > 0) : 0ull;
+        if (lane == kWave - 1) {
+            ss.wave_tot[wave] = incl;
+            ss.wave_aux[wave] = __popcll(nzm);
+        }
         __syncthreads();
-        int wbase = 0;
+        int wbase = 0, nzbase = 0;
 #pragma unroll
         for (int i = 0; i < kNW; ++i) {
             const int t = ss.wave_tot[i];
+            const int z = ss.wave_aux[i];
             wbase += i < wave ? t : 0;
+            nzbase += i < wave ? z : 0;
             total += t;
+            n_nz += z;
         }
         incl += wbase;   // row-wide inclusive offset of this lane's sub-chunk
-        if (lane < spw && sc < nsub) pre[sc] = incl - c_l;
+        if constexpr (kRunsCopy) {
+            if (c_l > 0) subl[nzbase + lanes_below(nzm)] = ((incl - c_l) << kNzSubBits) | sc;
+        } else {
+            if (lane < spw && sc < nsub) subl[sc] = incl - c_l;
+        }
         __syncthreads();
     } else {
         int mine = 0;
@@ -348,13 +445,19 @@ __device__ __forceinline__ void select_row(const Dims& D, const BatchArgs& ba, c
         int bsh = fixed ? bin_shift(bkmin, float_key(thi)) : 0;
         int* fh = fixed ? hist : nullptr;
         constexpr int kMid = kCap / kSelThreads > 8 ? 8 : kCap / kSelThreads;
+        auto copy = [&](auto tier) {
+            constexpr int N = decltype(tier)::value;
+            if constexpr (kRunsCopy)
+                copy_candidates_runs<N, kOffCand>(cand, subl, n_nz, total, lds, kmin, kmax, fh, bkmin, bsh);
+            else
+                copy_candidates_search<N, kOffCand>(cand, subl, nsub, total, lds, kmin, kmax, fh, bkmin, bsh);
+        };
         if (total > kMid * kSelThreads)
-            copy_candidates<kCap / kSelThreads, kOffCand>(cand, pre, nsub, total, lds, kmin, kmax,
-                                                         fh, bkmin, bsh);
+            copy(std::integral_constant<int, kCap / kSelThreads>{});
         else if (total > 4 * kSelThreads)
-            copy_candidates<kMid, kOffCand>(cand, pre, nsub, total, lds, kmin, kmax, fh, bkmin, bsh);
+            copy(std::integral_constant<int, kMid>{});
         else if (total > 0)
-            copy_candidates<4, kOffCand>(cand, pre, nsub, total, lds, kmin, kmax, fh, bkmin, bsh);
+            copy(std::integral_constant<int, 4>{});
         if (!fixed) block_min_max_count<kSelThreads>(kmin, kmax, kcount, bs);
         auto TOK = [&](int i) { return static_cast<int>(CAND(i) & kPosMask); };
         if (k == 0) {
