@@ -187,12 +187,14 @@ def test_candidate_volume(n_r):
 
 
 # more rows than CUs (9 x 32 = 288): the top-k stage runs two workgroups per
-# CU with room for 7168 candidates each; a flood of every token (about 8K per
-# row) takes its global-memory path
+# CU with room for 7168 candidates each; a flood of every token takes its
+# global-memory path at about 8K tokens per row, and its widest in-LDS copy
+# (4097 to 7168 candidates a row) at about 6K
 # ---------------------------------------------------------------------------
-@pytest.mark.parametrize("flood", [False, True], ids=["sampled", "every-token"])
-def test_many_rows_small_select(flood):
-    wl = small(1, batch=9, max_seq=8192 + 132, n_list=96, topk=160)
+@pytest.mark.parametrize("flood,n_seq", [(False, 8192), (True, 8192), (True, 6144)],
+                         ids=["sampled", "every-token", "every-token-in-lds"])
+def test_many_rows_small_select(flood, n_seq):
+    wl = small(1, batch=9, max_seq=n_seq + 132, n_list=96, topk=160)
     inp = make(wl, seed=17)
     ctx = context(inp)
     if flood:
