@@ -348,6 +348,7 @@ pqhsa_status pqhsa_create(const pqhsa_shape* shape, pqhsa_ctx** out) {
     A(dev_alloc(c, &w.cand_mass, BQ * L));
     A(dev_alloc(c, &w.bx_w, BQ * L));
     A(dev_alloc(c, &w.bx_wsel, BQ * D.max_topk));
+    A(dev_alloc(c, &w.sel_list, BQ * D.max_topk));
     A(dev_alloc(c, &w.row_shift, BQ));
     A(dev_alloc(c, &w.row_flag, BQ));
     A(dev_alloc(c, &w.partial, BQ * (c->nsplit_max + n_bgc) * kPartStride));
@@ -703,6 +704,7 @@ static pqhsa_status decode_impl(pqhsa_ctx* c, const void* q, const void* k, cons
     BatchArgs ba{};
     int nsplit = 1;   // exact-set splits this call needs per row
     Work w = c->w;
+    if (c->variant != PQHSA_VARIANT_BX) w.sel_list = nullptr;   // only Bx reads T's lists
     if (dev_args) {
         // every split the partial buffer holds: surplus workgroups exit
         for (int b = 0; b < D.B; ++b) ba.n_r[b] = c->n_r[b];

@@ -168,6 +168,8 @@ struct Work {
     float* bx_w;         // [B, Hq, n_list] variant Bx: M_j / |B n R_j| (0 when no member
                          //   of list j is unselected)
     float* bx_wsel;      // [B, Hq, max_topk] variant Bx: bx_w of the list of each entry of T
+    int32_t* sel_list;   // [B, Hq, max_topk] variant Bx: list id of each entry of T, written
+                         //   beside sel_tok by the top-k stage (null: not written)
     // A call whose budgets and lengths are device data: the caller's N_b and
     // k_b (dev_lens, dev_topk), and the call's clamped per-sequence integers
     // (ba_dev), written by the prologue for the later kernels. All null when

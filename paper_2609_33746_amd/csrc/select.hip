@@ -285,8 +285,8 @@ template <typename KeyAt, typename CandAt, typename IsSel>
 __device__ __forceinline__ void emit_selection(KeyAt key_at, CandAt cand_at, IsSel is_sel,
                                                int total, int k, int n_list,
                                                float shift, unsigned long long* mass,
-                                               int32_t* sel_tok, float* cand_mass,
-                                               SelectScratch& ss) {
+                                               int32_t* sel_tok, int32_t* sel_list,
+                                               float* cand_mass, SelectScratch& ss) {
     const int tid = threadIdx.x;
     const int eper = (total + kSelThreads - 1) / kSelThreads;
     const int e0 = min(tid * eper, total);
@@ -307,7 +307,10 @@ __device__ __forceinline__ void emit_selection(KeyAt key_at, CandAt cand_at, IsS
             run_list = lst;
         }
         if (is_sel(i, key, cand)) {
-            if (o < k) sel_tok[o] = static_cast<int32_t>(cand & kPosMask);
+            if (o < k) {
+                sel_tok[o] = static_cast<int32_t>(cand & kPosMask);
+                if (sel_list) sel_list[o] = lst;
+            }
             ++o;
         } else {
             run += static_cast<unsigned long long>(__expf(key_float(key) - shift) * kMassScale);
@@ -377,6 +380,7 @@ __device__ __forceinline__ void select_row(const Dims& D, const BatchArgs& ba, c
     const int64_t rbase = static_cast<int64_t>(row) * D.rcap;
     const int64_t base = static_cast<int64_t>(bg) * D.rcap;
     int32_t* sel_tok = w.sel_tok + static_cast<int64_t>(row) * D.max_topk;
+    int32_t* sel_list = w.sel_list ? w.sel_list + static_cast<int64_t>(row) * D.max_topk : nullptr;
     float* cand_mass = w.cand_mass + static_cast<int64_t>(row) * D.n_list;
     const float neg_inf = -__builtin_huge_valf();
 
@@ -464,7 +468,7 @@ __device__ __forceinline__ void select_row(const Dims& D, const BatchArgs& ba, c
             shift = total > 0 ? key_float(kmax) : neg_inf;
             emit_selection(
                 KEY, CAND, [](int, uint32_t, uint32_t) { return false; }, total, 0, D.n_list, shift,
-                mass, sel_tok, cand_mass, ss);
+                mass, sel_tok, sel_list, cand_mass, ss);
         } else {
             if (!fixed) {
                 bkmin = kmin;
@@ -500,7 +504,7 @@ __device__ __forceinline__ void select_row(const Dims& D, const BatchArgs& ba, c
                         const int bn = static_cast<int>(fixed_bin(key, bkmin, bsh));
                         return bn > bstar || (bn == bstar && ((chosen[i >> 5] >> (i & 31)) & 1u));
                     },
-                    total, k, D.n_list, shift, mass, sel_tok, cand_mass, ss);
+                    total, k, D.n_list, shift, mass, sel_tok, sel_list, cand_mass, ss);
             } else {
                 // very dense boundary bin: radix select
                 const SelectResult r = block_select_desc<kSelThreads>(
@@ -520,7 +524,7 @@ __device__ __forceinline__ void select_row(const Dims& D, const BatchArgs& ba, c
                     [&](int, uint32_t key, uint32_t cw) {
                         return key > kk || (key == kk && static_cast<int>(cw & kPosMask) <= tok_cut);
                     },
-                    total, k, D.n_list, shift, mass, sel_tok, cand_mass, ss);
+                    total, k, D.n_list, shift, mass, sel_tok, sel_list, cand_mass, ss);
             }
         }
     } else {
@@ -557,7 +561,7 @@ __device__ __forceinline__ void select_row(const Dims& D, const BatchArgs& ba, c
         if (total == 0) {
             shift = neg_inf;
             emit_selection(KEY, CAND, [](int, uint32_t, uint32_t) { return false; }, 0, 0,
-                           D.n_list, shift, mass, sel_tok, cand_mass, ss);
+                           D.n_list, shift, mass, sel_tok, sel_list, cand_mass, ss);
         } else {
             const SelectResult r = block_select_desc<kSelThreads>(
                 KEY, [](int) { return true; }, total, k > 0 ? k : 1, ss);
@@ -575,7 +579,7 @@ __device__ __forceinline__ void select_row(const Dims& D, const BatchArgs& ba, c
                 [&](int, uint32_t key, uint32_t cand) {
                     return k > 0 && (key > kth || (key == kth && static_cast<int>(cand & kPosMask) <= tok_cut));
                 },
-                total, k, D.n_list, shift, mass, sel_tok, cand_mass, ss);
+                total, k, D.n_list, shift, mass, sel_tok, sel_list, cand_mass, ss);
         }
     }
     if (tid == 0) {
