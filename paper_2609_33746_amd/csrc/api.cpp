@@ -50,7 +50,6 @@ struct pqhsa_ctx {
     float* means = nullptr;
     float* glob_mean = nullptr;   // [B, Hkv, d] for variant C
     double* mean_sums = nullptr;  // [B, Hkv, n_list, d] float64 value sums of the lists (updates)
-    uint16_t* tok_list = nullptr; // [B, Hkv, rcap] for variant Bx
     // token-major copy of the index, the source of every list-major rebuild
     int32_t* ids_tm = nullptr;       // [B, Hkv, rcap] list id of each token
     uint8_t* codes_tm = nullptr;     // [B, Hkv, rcap, M] one code per byte
@@ -94,7 +93,6 @@ struct pqhsa_ctx {
         ix.codebooks = codebooks;
         ix.means = means;
         ix.glob_mean = glob_mean;
-        ix.tok_list = tok_list;
         ix.n_seq = n_seq_dev;
         ix.n_r = n_r_dev;
         ix.samp_codes = samp_codes;
@@ -314,7 +312,6 @@ pqhsa_status pqhsa_create(const pqhsa_shape* shape, pqhsa_ctx** out) {
     A(dev_alloc(c, &c->means, BG * L * kHeadDim));
     A(dev_alloc(c, &c->glob_mean, BG * kHeadDim));
     A(dev_alloc(c, &c->mean_sums, BG * L * kHeadDim));
-    A(dev_alloc(c, &c->tok_list, BG * rc));
     A(dev_alloc(c, &c->ids_tm, BG * rc));
     A(dev_alloc(c, &c->codes_tm, BG * rc * static_cast<size_t>(shape->pq_m)));
     A(dev_alloc(c, &c->samp_codes, BG * kMaxSamples * 16));
@@ -386,13 +383,12 @@ static pqhsa_status relayout(pqhsa_ctx* c, const std::vector<int32_t>& lens, hip
         max_n = std::max(max_n, nr[b]);
     }
     c->prepared = false;
-    // the empty index the sort merges R into, and a clean Bx list table
+    // the empty index the sort merges R into
     hipError_t e = hipMemsetAsync(c->loff_alt, 0, BG * (L + 1) * sizeof(int32_t), stream);
-    if (e == hipSuccess) e = hipMemsetAsync(c->tok_list, 0, BG * rc * sizeof(uint16_t), stream);
     if (e == hipSuccess) e = hipMemsetAsync(c->bad_id, 0xff, sizeof(unsigned long long), stream);
     if (e == hipSuccess)
         e = launch_sort_lists(D, lo, hi, max_n, c->ids_tm, c->loff_alt, c->loff, c->shift, c->perm,
-                              c->pos_word, c->tok_list, c->n_r_dev, c->n_seq_dev, c->bad_id,
+                              c->pos_word, c->n_r_dev, c->n_seq_dev, c->bad_id,
                               reinterpret_cast<int32_t*>(c->w.comp_key),
                               static_cast<size_t>(D.B) * D.Hq * rc, stream);
     if (e != hipSuccess) return hip_fail(c, e, "launching the list-major sort");
@@ -497,8 +493,7 @@ pqhsa_status pqhsa_index_update(pqhsa_ctx* c, const int32_t* new_seq_lens, const
                                         c->ids_tm, c->codes_tm, c->norms_tm, stream);
     if (e == hipSuccess)
         e = launch_update_lists(D, lo, hi, kv, c->ids_tm, c->loff, c->perm, c->pos_word,
-                                c->loff_alt, c->shift, c->perm_alt, c->pos_alt, c->tok_list,
-                                c->n_r_dev, c->n_seq_dev, c->means, c->mean_sums, stream);
+                                c->loff_alt, c->shift, c->perm_alt, c->pos_alt, c->n_r_dev, c->n_seq_dev, c->means, c->mean_sums, stream);
     if (e != hipSuccess) return hip_fail(c, e, "launching the index update");
     std::swap(c->perm, c->perm_alt);
     std::swap(c->pos_word, c->pos_alt);

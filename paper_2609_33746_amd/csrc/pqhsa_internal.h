@@ -114,7 +114,6 @@ struct Index {
     const float* codebooks;    // [B, Hkv, M, K, d/M]
     const float* means;        // [B, Hkv, n_list, d]
     const float* glob_mean;    // [B, Hkv, d] sum_j |R_j| v_bar_j / |R_b| (variant C)
-    const uint16_t* tok_list;  // [B, Hkv, rcap] list id a_i of each token i of R (by token id)
     const int32_t* n_seq;      // [B]
     const int32_t* n_r;        // [B] |R_b|
     // the threshold sample's positions, gathered once per prepare or update
@@ -329,8 +328,8 @@ hipError_t launch_reseed(const Dims& D, const BatchInts& lo, const BatchInts& hi
 
 // the list-major rebuild after an update's encode pass (lo, hi as there):
 // new list offsets, per-list shifts [B, Hkv, n_list] and the new perm /
-// pos_word in the *_new buffers (which must not alias the old ones); tok_list,
-// n_r, n_seq, the float64 list value sums and the list means (from the values
+// pos_word in the *_new buffers (which must not alias the old ones); n_r,
+// n_seq, the float64 list value sums and the list means (from the values
 // in kv) updated in place
 // The list-major layout of R_b = tokens [lo_b, hi_b) built from the
 // token-major list ids on the device: a stable counting sort per (b, kv
@@ -342,14 +341,13 @@ hipError_t launch_reseed(const Dims& D, const BatchInts& lo, const BatchInts& hi
 // over many workgroups per (b, g); otherwise one workgroup per (b, g).
 hipError_t launch_sort_lists(const Dims& D, const BatchInts& lo, const BatchInts& hi, int max_n,
                              const int32_t* ids_tm, const int32_t* zero_loff, int32_t* loff,
-                             int32_t* shift, int32_t* perm, uint32_t* pos_word, uint16_t* tok_list,
-                             int32_t* n_r_dev, int32_t* n_seq_dev, unsigned long long* bad,
+                             int32_t* shift, int32_t* perm, uint32_t* pos_word, int32_t* n_r_dev, int32_t* n_seq_dev, unsigned long long* bad,
                              int32_t* scratch, size_t scratch_ints, hipStream_t s);
 hipError_t launch_update_lists(const Dims& D, const BatchInts& lo, const BatchInts& hi,
                                const KV& kv, const int32_t* ids_tm, const int32_t* old_loff,
                                const int32_t* perm_old, const uint32_t* pos_old, int32_t* new_loff,
                                int32_t* shift, int32_t* perm_new, uint32_t* pos_new,
-                               uint16_t* tok_list, int32_t* n_r_dev, int32_t* n_seq_dev,
+                               int32_t* n_r_dev, int32_t* n_seq_dev,
                                float* means, double* sums, hipStream_t s);
 // float64 value sums of the lists, |R_j| v_bar_j, for later updates
 hipError_t launch_init_sums(const Dims& D, const int32_t* loff, const float* means, double* sums,

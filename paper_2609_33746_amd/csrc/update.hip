@@ -201,7 +201,7 @@ __global__ __launch_bounds__(kListThreads) void update_lists_kernel(
     Dims D, BatchInts lo, BatchInts hi, const int32_t* __restrict__ ids_tm,
     const int32_t* __restrict__ old_loff, int32_t* __restrict__ new_loff,
     int32_t* __restrict__ shift, int32_t* __restrict__ perm_new, uint32_t* __restrict__ pos_new,
-    uint16_t* __restrict__ tok_list, int32_t* __restrict__ n_r_dev, int32_t* __restrict__ n_seq_dev) {
+    int32_t* __restrict__ n_r_dev, int32_t* __restrict__ n_seq_dev) {
     __shared__ int cnt[kMaxLists];     // new members per list, then the exclusive scan
     __shared__ int placed[kMaxLists];  // new members placed so far per list
     __shared__ int chunk[kListThreads];
@@ -243,7 +243,6 @@ __global__ __launch_bounds__(kListThreads) void update_lists_kernel(
             const int pos = ol[j + 1] + cnt[j] + placed[j] + r;
             perm_new[row + pos] = t;
             pos_new[row + pos] = (static_cast<uint32_t>(j) << kPosBits) | static_cast<uint32_t>(t);
-            tok_list[row + t] = static_cast<uint16_t>(j);
         }
         __syncthreads();
         if (t < t1) atomicAdd(&placed[j], 1);
@@ -290,13 +289,11 @@ __global__ __launch_bounds__(256) void check_ids_kernel(Dims D, BatchInts lo, Ba
 }
 
 // finish_lists_kernel: after the grouping of R_b by list (perm, loff), the
-// list word of every position, the list of every token (tok_list) and the
-// cleared positions past |R_b|.
+// list word of every position and the cleared positions past |R_b|.
 __global__ __launch_bounds__(256) void finish_lists_kernel(Dims D, BatchInts lo, BatchInts hi,
                                                            const int32_t* __restrict__ ids_tm,
                                                            int32_t* __restrict__ perm,
                                                            uint32_t* __restrict__ pos_word,
-                                                           uint16_t* __restrict__ tok_list,
                                                            int32_t* __restrict__ n_r_dev,
                                                            int32_t* __restrict__ n_seq_dev) {
     const int p = blockIdx.x * 256 + threadIdx.x;
@@ -312,7 +309,6 @@ __global__ __launch_bounds__(256) void finish_lists_kernel(Dims D, BatchInts lo,
         const int t = perm[row + p];
         const int j = min(max(ids_tm[row + t], 0), D.n_list - 1);
         pos_word[row + p] = (static_cast<uint32_t>(j) << kPosBits) | static_cast<uint32_t>(t);
-        tok_list[row + t] = static_cast<uint16_t>(j);
     } else {
         perm[row + p] = -1;
         pos_word[row + p] = 0u;
@@ -321,7 +317,7 @@ __global__ __launch_bounds__(256) void finish_lists_kernel(Dims D, BatchInts lo,
 
 hipError_t launch_sort_lists(const Dims& D, const BatchInts& lo, const BatchInts& hi, int max_n,
                              const int32_t* ids_tm, const int32_t* zero_loff, int32_t* loff,
-                             int32_t* shift, int32_t* perm, uint32_t* pos_word, uint16_t* tok_list,
+                             int32_t* shift, int32_t* perm, uint32_t* pos_word,
                              int32_t* n_r_dev, int32_t* n_seq_dev, unsigned long long* bad,
                              int32_t* scratch, size_t scratch_ints, hipStream_t s) {
     if (max_n > 0) {
@@ -337,13 +333,13 @@ hipError_t launch_sort_lists(const Dims& D, const BatchInts& lo, const BatchInts
         hipError_t e = launch_group_segments(D, lo, hi, 0, ids_tm, nullptr, scratch, perm, loff, s);
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL(finish_lists_kernel, dim3((D.rcap + 255) / 256, D.B * D.Hkv), dim3(256), 0, s,
-                           D, lo, hi, ids_tm, perm, pos_word, tok_list, n_r_dev, n_seq_dev);
+                           D, lo, hi, ids_tm, perm, pos_word, n_r_dev, n_seq_dev);
         return hipGetLastError();
     }
     // a merge into an empty index: every token of R is new (old offsets all
     // zero, no old positions to move)
     hipLaunchKernelGGL(update_lists_kernel, dim3(D.B * D.Hkv), dim3(kListThreads), 0, s, D, lo, hi,
-                       ids_tm, zero_loff, loff, shift, perm, pos_word, tok_list, n_r_dev, n_seq_dev);
+                       ids_tm, zero_loff, loff, shift, perm, pos_word, n_r_dev, n_seq_dev);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     // positions past |R_b| are cleared
@@ -356,11 +352,10 @@ hipError_t launch_update_lists(const Dims& D, const BatchInts& lo, const BatchIn
                                const KV& kv, const int32_t* ids_tm, const int32_t* old_loff,
                                const int32_t* perm_old, const uint32_t* pos_old, int32_t* new_loff,
                                int32_t* shift, int32_t* perm_new, uint32_t* pos_new,
-                               uint16_t* tok_list, int32_t* n_r_dev, int32_t* n_seq_dev,
+                               int32_t* n_r_dev, int32_t* n_seq_dev,
                                float* means, double* sums, hipStream_t s) {
     hipLaunchKernelGGL(update_lists_kernel, dim3(D.B * D.Hkv), dim3(kListThreads), 0, s, D, lo, hi,
-                       ids_tm, old_loff, new_loff, shift, perm_new, pos_new, tok_list, n_r_dev,
-                       n_seq_dev);
+                       ids_tm, old_loff, new_loff, shift, perm_new, pos_new, n_r_dev, n_seq_dev);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(shift_positions_kernel, dim3((D.rcap + 255) / 256, D.B * D.Hkv), dim3(256), 0,
