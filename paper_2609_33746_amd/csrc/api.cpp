@@ -345,7 +345,6 @@ pqhsa_status pqhsa_create(const pqhsa_shape* shape, pqhsa_ctx** out) {
     A(dev_alloc(c, &w.cand_mass, BQ * L));
     A(dev_alloc(c, &w.bx_w, BQ * L));
     A(dev_alloc(c, &w.bx_wsel, BQ * D.max_topk));
-    A(dev_alloc(c, &w.sel_list, BQ * D.max_topk));
     A(dev_alloc(c, &w.row_shift, BQ));
     A(dev_alloc(c, &w.row_flag, BQ));
     A(dev_alloc(c, &w.partial, BQ * (c->nsplit_max + n_bgc) * kPartStride));
@@ -699,7 +698,6 @@ static pqhsa_status decode_impl(pqhsa_ctx* c, const void* q, const void* k, cons
     BatchArgs ba{};
     int nsplit = 1;   // exact-set splits this call needs per row
     Work w = c->w;
-    if (c->variant != PQHSA_VARIANT_BX) w.sel_list = nullptr;   // only Bx reads T's lists
     if (dev_args) {
         // every split the partial buffer holds: surplus workgroups exit
         for (int b = 0; b < D.B; ++b) ba.n_r[b] = c->n_r[b];
@@ -733,8 +731,8 @@ static pqhsa_status decode_impl(pqhsa_ctx* c, const void* q, const void* k, cons
     };
     if (e == hipSuccess) e = launch_prologue(D, ba, kv, ix, w, c->bias, stream, tm(0));
     if (e == hipSuccess) e = launch_scan(D, ba, ix, w, c->scan_nwg, stream, tm(1));
-    if (e == hipSuccess) e = launch_select(D, ba, ix, w, c->force_fallback, stream, tm(2));
-    if (e == hipSuccess && c->variant == PQHSA_VARIANT_BX) e = launch_bx_weights(D, ba, ix, w, stream);
+    if (e == hipSuccess)
+        e = launch_select(D, ba, ix, w, c->force_fallback, c->variant == PQHSA_VARIANT_BX, stream, tm(2));
     if (e == hipSuccess)
         e = launch_attend(D, ba, kv, ix, w, nsplit, c->nsplit_max, c->variant, stream, tm(3));
     if (e == hipSuccess) e = launch_merge(D, ba, w, out, c->nsplit_max, c->variant, stream, tm(4));

@@ -367,105 +367,6 @@ __global__ __launch_bounds__(kAttnThreads) void attend_kernel(Dims D, BatchArgs 
     }
 }
 
-// Variant Bx (Appendix B): the background value of list j is the mean of
-// its unselected members, (|R_j| v_bar_j - sum over T n R_j of v_i) / u_j
-// with u_j = |B n R_j|. Its Eq. 4 term splits into W_j |R_j| v_bar_j minus
-// W_j times the selected rows of the list, W_j = M_j / u_j: the background
-// role takes the first part, the exact role (which gathers those rows
-// anyway) the second. One workgroup per row counts T per list, forms W_j
-// from the same masses as the background role and hands every entry of T
-// its list's W_j. The lists of T come from the top-k stage (sel_list), and
-// both they and every list's mass M_j are loaded before the count, so the
-// two chains of loads overlap.
-constexpr int kBxThreads = 512;
-constexpr int kBxLists = kMaxLists / kBxThreads;   // lists per thread
-constexpr int kBxHeld = 8;                         // entries of T per thread kept in registers
-static_assert(kMaxLists % kBxThreads == 0, "whole list strides");
-
-template <bool kDev>
-__global__ __launch_bounds__(kBxThreads) void bx_weight_kernel(Dims D, BatchArgs ba, Index ix,
-                                                               Work w) {
-    __shared__ int cnt[kMaxLists];
-    __shared__ float wl[kMaxLists];
-    const int tid = threadIdx.x;
-    const int row = blockIdx.x;
-    const int b = row / D.Hq;
-    const int h = row % D.Hq;
-    const int hh = h % D.G;
-    const int bg = b * D.Hkv + h / D.G;
-    const int k = arg_topk<kDev>(ba, w, b);
-    const int32_t* sl = w.sel_list + static_cast<int64_t>(row) * D.max_topk;
-    auto list_at = [&](int e) { return min(max(static_cast<int>(sl[e]), 0), D.n_list - 1); };
-    int held[kBxHeld];
-#pragma unroll
-    for (int u = 0; u < kBxHeld; ++u) {
-        const int e = tid + u * kBxThreads;
-        held[u] = e < k ? list_at(e) : 0;
-    }
-    const float neg_inf = -__builtin_huge_valf();
-    const float shift = w.row_shift[row];
-    const float tlo = w.tau_lo[row];
-    const bool live = shift != neg_inf;
-    const bool use_below = live && tlo != neg_inf && w.row_flag[row] == 0;
-    const float below_scale = use_below ? __expf(tlo - shift) : 0.0f;
-    const int32_t* loff = ix.loff + static_cast<int64_t>(bg) * (D.n_list + 1);
-    const float* segs = w.seg_sum + static_cast<int64_t>(bg) * D.nseg_cap * D.G + hh;
-    float mj[kBxLists];
-    int sz[kBxLists];
-#pragma unroll
-    for (int u = 0; u < kBxLists; ++u) {
-        const int j = tid + u * kBxThreads;
-        mj[u] = 0.0f;
-        sz[u] = 0;
-        if (j < D.n_list) {
-            cnt[j] = 0;
-            const int lo = loff[j], hi = loff[j + 1];
-            if (live) {
-                float below = 0.0f;
-                if (use_below && hi > lo)
-                    for (int sg = j + lo / kSub; sg <= j + (hi - 1) / kSub; ++sg) below += segs[sg * D.G];
-                mj[u] = below * below_scale + w.cand_mass[static_cast<int64_t>(row) * D.n_list + j];
-            }
-            sz[u] = hi - lo;
-        }
-    }
-    __syncthreads();
-#pragma unroll
-    for (int u = 0; u < kBxHeld; ++u)
-        if (tid + u * kBxThreads < k) atomicAdd(&cnt[held[u]], 1);
-    for (int e = tid + kBxHeld * kBxThreads; e < k; e += kBxThreads) atomicAdd(&cnt[list_at(e)], 1);
-    __syncthreads();
-#pragma unroll
-    for (int u = 0; u < kBxLists; ++u) {
-        const int j = tid + u * kBxThreads;
-        if (j < D.n_list) {
-            const int un = sz[u] - cnt[j];
-            const float W = un > 0 ? mj[u] / static_cast<float>(un) : 0.0f;
-            wl[j] = W;
-            w.bx_w[static_cast<int64_t>(row) * D.n_list + j] = W;
-        }
-    }
-    __syncthreads();
-    float* wsel = w.bx_wsel + static_cast<int64_t>(row) * D.max_topk;
-#pragma unroll
-    for (int u = 0; u < kBxHeld; ++u) {
-        const int e = tid + u * kBxThreads;
-        if (e < k) wsel[e] = wl[held[u]];
-    }
-    for (int e = tid + kBxHeld * kBxThreads; e < k; e += kBxThreads) wsel[e] = wl[list_at(e)];
-}
-
-hipError_t launch_bx_weights(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w,
-                             hipStream_t s, const KTiming& tm) {
-    if (w.ba_dev)
-        hipExtLaunchKernelGGL(bx_weight_kernel<true>, dim3(D.B * D.Hq), dim3(kBxThreads), 0, s,
-                              tm.start, tm.stop, 0, D, ba, ix, w);
-    else
-        hipExtLaunchKernelGGL(bx_weight_kernel<false>, dim3(D.B * D.Hq), dim3(kBxThreads), 0, s,
-                              tm.start, tm.stop, 0, D, ba, ix, w);
-    return hipGetLastError();
-}
-
 // y = (sum of partials' N) / (sum of partials' Z) under one shift (Eq. 5).
 // Partials [0, n_exact(b)) and [first_bg, first_bg + n_bg) of each row are used;
 // partials with Z = 0 are skipped. Per batch of kMergeBatch used partials,

@@ -167,8 +167,6 @@ struct Work {
     float* bx_w;         // [B, Hq, n_list] variant Bx: M_j / |B n R_j| (0 when no member
                          //   of list j is unselected)
     float* bx_wsel;      // [B, Hq, max_topk] variant Bx: bx_w of the list of each entry of T
-    int32_t* sel_list;   // [B, Hq, max_topk] variant Bx: list id of each entry of T, written
-                         //   beside sel_tok by the top-k stage (null: not written)
     // A call whose budgets and lengths are device data: the caller's N_b and
     // k_b (dev_lens, dev_topk), and the call's clamped per-sequence integers
     // (ba_dev), written by the prologue for the later kernels. All null when
@@ -254,18 +252,16 @@ hipError_t launch_prologue(const Dims& D, const BatchArgs& ba, const KV& kv, con
 // nwg = scan workgroups per (batch element, KV head): enough for the longest R_b
 hipError_t launch_scan(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w, int nwg,
                        hipStream_t s, const KTiming& tm = KTiming{});
+// bx: variant Bx, whose per-list weights bx_w and per-entry weights bx_wsel
+// the select forms beside T
 hipError_t launch_select(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w,
-                         int force_fallback, hipStream_t s, const KTiming& tm = KTiming{});
+                         int force_fallback, bool bx, hipStream_t s, const KTiming& tm = KTiming{});
 // variant: the background term, a PQHSA_VARIANT_* value. nsplit: exact-set
 // splits launched per row (enough for this call's rows); nsplit_max: the
 // splits per row the partial buffer holds (its layout).
 hipError_t launch_attend(const Dims& D, const BatchArgs& ba, const KV& kv, const Index& ix,
                          const Work& w, int nsplit, int nsplit_max, int variant, hipStream_t s,
                          const KTiming& tm = KTiming{});
-// variant Bx, after the select: the per-list weights bx_w and, for every
-// selected entry, the weight of its list (bx_wsel)
-hipError_t launch_bx_weights(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w,
-                             hipStream_t s, const KTiming& tm = KTiming{});
 hipError_t launch_merge(const Dims& D, const BatchArgs& ba, const Work& w, float* out,
                         int nsplit_max, int variant, hipStream_t s, const KTiming& tm = KTiming{});
 hipError_t launch_dense(const Dims& D, const KV& kv, const BatchInts& lens, float* partial,

@@ -281,12 +281,35 @@ __device__ __forceinline__ void copy_candidates_runs(const uint2* __restrict__ c
 // range of candidate indices) and the per-list sums of exp(l~ - shift) over
 // the unselected candidates (candidates are in list-major order, so a thread
 // adds one partial per run of equal list ids).
-template <typename KeyAt, typename CandAt, typename IsSel>
+// Variant Bx (Appendix B) in the top-k stage: the background value of list
+// j is the mean of its unselected members, and its Eq. 4 term splits into
+// W_j |R_j| v_bar_j minus W_j times the selected rows of the list, with
+// W_j = M_j / |B n R_j|. The row forms W_j here, from the same masses as the
+// background role (the scan's below-threshold segments of the list, scaled to
+// the row's shift, plus its unselected candidates), and hands every entry of
+// T its list's W_j. Thread t owns lists t + u * kSelThreads; their offsets are
+// loaded when the row starts where one workgroup holds a CU (with two, the
+// registers they would take cost the second workgroup its place), else with
+// the masses.
+constexpr int kBxPer = kMaxLists / kSelThreads;
+static_assert(kMaxLists % kSelThreads == 0, "whole list strides");
+struct BxRow {
+    int lo[kBxPer], hi[kBxPer];   // the thread's lists in the list-major order (preloaded)
+    const int32_t* loff;          // list starts of this head
+    const float* segs;            // below-threshold masses of this head, stride G
+    int seg_stride;
+    float tlo;                    // the row's threshold tau_lo
+    bool rescan;                  // the row took the re-scan path (no below-threshold masses)
+    float* bx_w;                  // [n_list] W_j of the row
+    float* bx_wsel;               // [max_topk] W of the list of each entry of T
+};
+
+template <bool kBx, bool kBxPre, typename KeyAt, typename CandAt, typename IsSel>
 __device__ __forceinline__ void emit_selection(KeyAt key_at, CandAt cand_at, IsSel is_sel,
                                                int total, int k, int n_list,
                                                float shift, unsigned long long* mass,
-                                               int32_t* sel_tok, int32_t* sel_list,
-                                               float* cand_mass, SelectScratch& ss) {
+                                               int32_t* sel_tok, float* cand_mass,
+                                               const BxRow& bx, SelectScratch& ss) {
     const int tid = threadIdx.x;
     const int eper = (total + kSelThreads - 1) / kSelThreads;
     const int e0 = min(tid * eper, total);
@@ -295,6 +318,7 @@ __device__ __forceinline__ void emit_selection(KeyAt key_at, CandAt cand_at, IsS
     for (int i = e0; i < e1; ++i) nsel += is_sel(i, key_at(i), cand_at(i)) ? 1 : 0;
     int tot = 0;
     int o = block_excl_scan<kSelThreads, false>(nsel, tot, ss);   // ss is not written before the barrier below
+    const int o_first = o;
     int run_list = -1;
     unsigned long long run = 0ull;
     for (int i = e0; i < e1; ++i) {
@@ -307,10 +331,7 @@ __device__ __forceinline__ void emit_selection(KeyAt key_at, CandAt cand_at, IsS
             run_list = lst;
         }
         if (is_sel(i, key, cand)) {
-            if (o < k) {
-                sel_tok[o] = static_cast<int32_t>(cand & kPosMask);
-                if (sel_list) sel_list[o] = lst;
-            }
+            if (o < k) sel_tok[o] = static_cast<int32_t>(cand & kPosMask);
             ++o;
         } else {
             run += static_cast<unsigned long long>(__expf(key_float(key) - shift) * kMassScale);
@@ -318,8 +339,69 @@ __device__ __forceinline__ void emit_selection(KeyAt key_at, CandAt cand_at, IsS
     }
     if (run) atomicAdd(&mass[run_list], run);
     __syncthreads();
-    for (int j = tid; j < n_list; j += kSelThreads)
-        cand_mass[j] = static_cast<float>(mass[j]) * kMassUnscale;
+    if constexpr (!kBx) {
+        for (int j = tid; j < n_list; j += kSelThreads)
+            cand_mass[j] = static_cast<float>(mass[j]) * kMassUnscale;
+    } else {
+        const float neg_inf = -__builtin_huge_valf();
+        const bool live = shift != neg_inf;
+        const bool use_below = live && bx.tlo != neg_inf && !bx.rescan;
+        const float below_scale = use_below ? __expf(bx.tlo - shift) : 0.0f;
+        float mj[kBxPer];
+        int sz[kBxPer];
+#pragma unroll
+        for (int u = 0; u < kBxPer; ++u) {
+            const int j = tid + u * kSelThreads;
+            mj[u] = 0.0f;
+            sz[u] = 0;
+            if (j < n_list) {
+                const float cm = static_cast<float>(mass[j]) * kMassUnscale;
+                cand_mass[j] = cm;
+                float below = 0.0f;
+                const int lo = kBxPre ? bx.lo[u] : bx.loff[j];
+                const int hi = kBxPre ? bx.hi[u] : bx.loff[j + 1];
+                sz[u] = hi - lo;
+                if (use_below && hi > lo)
+                    for (int sg = j + lo / kSub; sg <= j + (hi - 1) / kSub; ++sg)
+                        below += bx.segs[sg * bx.seg_stride];
+                mj[u] = live ? below * below_scale + cm : 0.0f;
+            }
+        }
+        // the masses are read: their words now hold |T n R_j| and then W_j
+        __syncthreads();
+        int* cnt = reinterpret_cast<int*>(mass);
+        float* wl = reinterpret_cast<float*>(mass) + n_list;
+        for (int j = tid; j < n_list; j += kSelThreads) cnt[j] = 0;
+        __syncthreads();
+        o = o_first;
+        for (int i = e0; i < e1; ++i) {
+            const uint32_t cand = cand_at(i);
+            if (is_sel(i, key_at(i), cand)) {
+                if (o < k) atomicAdd(&cnt[cand >> kPosBits], 1);
+                ++o;
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int u = 0; u < kBxPer; ++u) {
+            const int j = tid + u * kSelThreads;
+            if (j < n_list) {
+                const int un = sz[u] - cnt[j];
+                const float W = un > 0 ? mj[u] / static_cast<float>(un) : 0.0f;
+                wl[j] = W;
+                bx.bx_w[j] = W;
+            }
+        }
+        __syncthreads();
+        o = o_first;
+        for (int i = e0; i < e1; ++i) {
+            const uint32_t cand = cand_at(i);
+            if (is_sel(i, key_at(i), cand)) {
+                if (o < k) bx.bx_wsel[o] = wl[cand >> kPosBits];
+                ++o;
+            }
+        }
+    }
 }
 
 // Score every indexed token of a row again from its head's LUT (the re-scan
@@ -344,7 +426,7 @@ __device__ __forceinline__ void rescan_row(const Dims& D, const Index& ix, const
     }
 }
 
-template <bool kDev, int kCap>
+template <bool kDev, int kCap, bool kBx>
 __device__ __forceinline__ void select_row(const Dims& D, const BatchArgs& ba, const Index& ix,
                                            const Work& w, int force_fallback) {
     using L = SelLayout<kCap>;
@@ -380,7 +462,6 @@ __device__ __forceinline__ void select_row(const Dims& D, const BatchArgs& ba, c
     const int64_t rbase = static_cast<int64_t>(row) * D.rcap;
     const int64_t base = static_cast<int64_t>(bg) * D.rcap;
     int32_t* sel_tok = w.sel_tok + static_cast<int64_t>(row) * D.max_topk;
-    int32_t* sel_list = w.sel_list ? w.sel_list + static_cast<int64_t>(row) * D.max_topk : nullptr;
     float* cand_mass = w.cand_mass + static_cast<int64_t>(row) * D.n_list;
     const float neg_inf = -__builtin_huge_valf();
 
@@ -388,6 +469,24 @@ __device__ __forceinline__ void select_row(const Dims& D, const BatchArgs& ba, c
     for (int i = tid; i < kHistBins; i += kSelThreads) hist[i] = 0;
     for (int i = tid; i < kCap / 32; i += kSelThreads) chosen[i] = 0u;
     if (tid < 4) counter[tid] = 0;   // counter[1] is the equal-key flag of the rank
+    BxRow bx{};
+    constexpr bool kBxPre = kCap != kSelCapSmall;
+    if constexpr (kBx) {
+        bx.loff = ix.loff + static_cast<int64_t>(bg) * (D.n_list + 1);
+        if constexpr (kBxPre) {
+#pragma unroll
+            for (int u = 0; u < kBxPer; ++u) {
+                const int j = tid + u * kSelThreads;
+                bx.lo[u] = j < D.n_list ? bx.loff[j] : 0;
+                bx.hi[u] = j < D.n_list ? bx.loff[j + 1] : 0;
+            }
+        }
+        bx.segs = w.seg_sum + static_cast<int64_t>(bg) * D.nseg_cap * D.G + hh;
+        bx.seg_stride = D.G;
+        bx.tlo = w.tau_lo[row];
+        bx.bx_w = w.bx_w + static_cast<int64_t>(row) * D.n_list;
+        bx.bx_wsel = w.bx_wsel + static_cast<int64_t>(row) * D.max_topk;
+    }
 
     // 1) candidate counts: wave w owns sub-chunks [w * spw, (w + 1) * spw)
     const bool small_nsub = nsub <= kSelMaxSub;
@@ -431,6 +530,7 @@ __device__ __forceinline__ void select_row(const Dims& D, const BatchArgs& ba, c
         block_excl_scan<kSelThreads>(mine, total, ss);
     }
     const bool fallback = force_fallback || (n_r > 0 && total < (k > 0 ? k : 1));
+    bx.rescan = fallback;
     float shift = neg_inf;
 
     if (!fallback && small_nsub && total <= kCap) {
@@ -466,9 +566,9 @@ __device__ __forceinline__ void select_row(const Dims& D, const BatchArgs& ba, c
         auto TOK = [&](int i) { return static_cast<int>(CAND(i) & kPosMask); };
         if (k == 0) {
             shift = total > 0 ? key_float(kmax) : neg_inf;
-            emit_selection(
+            emit_selection<kBx, kBxPre>(
                 KEY, CAND, [](int, uint32_t, uint32_t) { return false; }, total, 0, D.n_list, shift,
-                mass, sel_tok, sel_list, cand_mass, ss);
+                mass, sel_tok, cand_mass, bx, ss);
         } else {
             if (!fixed) {
                 bkmin = kmin;
@@ -498,13 +598,13 @@ __device__ __forceinline__ void select_row(const Dims& D, const BatchArgs& ba, c
                                                    counter + 1, chosen, kth, bs);
             if (by_rank) {
                 shift = key_float(kth);   // the k-th largest score
-                emit_selection(
+                emit_selection<kBx, kBxPre>(
                     KEY, CAND,
                     [&](int i, uint32_t key, uint32_t) {
                         const int bn = static_cast<int>(fixed_bin(key, bkmin, bsh));
                         return bn > bstar || (bn == bstar && ((chosen[i >> 5] >> (i & 31)) & 1u));
                     },
-                    total, k, D.n_list, shift, mass, sel_tok, sel_list, cand_mass, ss);
+                    total, k, D.n_list, shift, mass, sel_tok, cand_mass, bx, ss);
             } else {
                 // very dense boundary bin: radix select
                 const SelectResult r = block_select_desc<kSelThreads>(
@@ -519,12 +619,12 @@ __device__ __forceinline__ void select_row(const Dims& D, const BatchArgs& ba, c
                     tok_cut = static_cast<int>(~t.key);
                 }
                 shift = key_float(kk);
-                emit_selection(
+                emit_selection<kBx, kBxPre>(
                     KEY, CAND,
                     [&](int, uint32_t key, uint32_t cw) {
                         return key > kk || (key == kk && static_cast<int>(cw & kPosMask) <= tok_cut);
                     },
-                    total, k, D.n_list, shift, mass, sel_tok, sel_list, cand_mass, ss);
+                    total, k, D.n_list, shift, mass, sel_tok, cand_mass, bx, ss);
             }
         }
     } else {
@@ -560,8 +660,8 @@ __device__ __forceinline__ void select_row(const Dims& D, const BatchArgs& ba, c
         auto CAND = [&](int i) { return ccand[i]; };
         if (total == 0) {
             shift = neg_inf;
-            emit_selection(KEY, CAND, [](int, uint32_t, uint32_t) { return false; }, 0, 0,
-                           D.n_list, shift, mass, sel_tok, sel_list, cand_mass, ss);
+            emit_selection<kBx, kBxPre>(KEY, CAND, [](int, uint32_t, uint32_t) { return false; }, 0, 0,
+                           D.n_list, shift, mass, sel_tok, cand_mass, bx, ss);
         } else {
             const SelectResult r = block_select_desc<kSelThreads>(
                 KEY, [](int) { return true; }, total, k > 0 ? k : 1, ss);
@@ -574,12 +674,12 @@ __device__ __forceinline__ void select_row(const Dims& D, const BatchArgs& ba, c
                 tok_cut = static_cast<int>(~t.key);
             }
             shift = key_float(r.key);   // k-th largest, or the maximum when k = 0
-            emit_selection(
+            emit_selection<kBx, kBxPre>(
                 KEY, CAND,
                 [&](int, uint32_t key, uint32_t cand) {
                     return k > 0 && (key > kth || (key == kth && static_cast<int>(cand & kPosMask) <= tok_cut));
                 },
-                total, k, D.n_list, shift, mass, sel_tok, sel_list, cand_mass, ss);
+                total, k, D.n_list, shift, mass, sel_tok, cand_mass, bx, ss);
         }
     }
     if (tid == 0) {
@@ -588,18 +688,18 @@ __device__ __forceinline__ void select_row(const Dims& D, const BatchArgs& ba, c
     }
 }
 
-template <bool kDev>
+template <bool kDev, bool kBx>
 __global__ __launch_bounds__(kSelThreads) void select_kernel(Dims D, BatchArgs ba, Index ix, Work w,
                                                              int force_fallback) {
-    select_row<kDev, kSelCap>(D, ba, ix, w, force_fallback);
+    select_row<kDev, kSelCap, kBx>(D, ba, ix, w, force_fallback);
 }
 
 // Two of these share a CU only when each wave holds at most 80 SGPRs (the
 // few beyond that spill to VGPR lanes).
-template <bool kDev>
+template <bool kDev, bool kBx>
 __global__ __launch_bounds__(kSelThreads) __attribute__((amdgpu_num_sgpr(80))) void select_small_kernel(
     Dims D, BatchArgs ba, Index ix, Work w, int force_fallback) {
-    select_row<kDev, kSelCapSmall>(D, ba, ix, w, force_fallback);
+    select_row<kDev, kSelCapSmall, kBx>(D, ba, ix, w, force_fallback);
 }
 
 // The small-capacity select when the rows outnumber the CUs and two of its
@@ -612,39 +712,46 @@ static bool select_small(const Dims& D) {
            2 * (SelLayout<kSelCapSmall>::bytes(D.n_list) + kStatic) <= kLdsPerCu;
 }
 
-template <bool kDev>
+template <bool kDev, bool kBx>
 static void launch_select_d(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w,
                             int force_fallback, hipStream_t s, const KTiming& tm) {
     if (select_small(D))
-        hipExtLaunchKernelGGL((select_small_kernel<kDev>), dim3(D.B * D.Hq), dim3(kSelThreads),
+        hipExtLaunchKernelGGL((select_small_kernel<kDev, kBx>), dim3(D.B * D.Hq), dim3(kSelThreads),
                               SelLayout<kSelCapSmall>::bytes(D.n_list), s, tm.start, tm.stop, 0, D, ba,
                               ix, w, force_fallback);
     else
-        hipExtLaunchKernelGGL((select_kernel<kDev>), dim3(D.B * D.Hq), dim3(kSelThreads),
+        hipExtLaunchKernelGGL((select_kernel<kDev, kBx>), dim3(D.B * D.Hq), dim3(kSelThreads),
                               SelLayout<kSelCap>::bytes(D.n_list), s, tm.start, tm.stop, 0, D, ba, ix,
                               w, force_fallback);
 }
 
 hipError_t launch_select(const Dims& D, const BatchArgs& ba, const Index& ix, const Work& w,
-                         int force_fallback, hipStream_t s, const KTiming& tm) {
-    if (w.ba_dev)
-        launch_select_d<true>(D, ba, ix, w, force_fallback, s, tm);
+                         int force_fallback, bool bx, hipStream_t s, const KTiming& tm) {
+    if (w.ba_dev && bx)
+        launch_select_d<true, true>(D, ba, ix, w, force_fallback, s, tm);
+    else if (w.ba_dev)
+        launch_select_d<true, false>(D, ba, ix, w, force_fallback, s, tm);
+    else if (bx)
+        launch_select_d<false, true>(D, ba, ix, w, force_fallback, s, tm);
     else
-        launch_select_d<false>(D, ba, ix, w, force_fallback, s, tm);
+        launch_select_d<false, false>(D, ba, ix, w, force_fallback, s, tm);
     return hipGetLastError();
 }
 
 hipError_t configure_select() {
-    const void* k[] = {reinterpret_cast<const void*>(&select_kernel<false>),
-                       reinterpret_cast<const void*>(&select_kernel<true>),
-                       reinterpret_cast<const void*>(&select_small_kernel<false>),
-                       reinterpret_cast<const void*>(&select_small_kernel<true>)};
-    const int bytes[] = {static_cast<int>(SelLayout<kSelCap>::bytes(kMaxLists)),
-                         static_cast<int>(SelLayout<kSelCap>::bytes(kMaxLists)),
-                         static_cast<int>(SelLayout<kSelCapSmall>::bytes(kMaxLists)),
-                         static_cast<int>(SelLayout<kSelCapSmall>::bytes(kMaxLists))};
+    const void* k[] = {reinterpret_cast<const void*>(&select_kernel<false, false>),
+                       reinterpret_cast<const void*>(&select_kernel<true, false>),
+                       reinterpret_cast<const void*>(&select_kernel<false, true>),
+                       reinterpret_cast<const void*>(&select_kernel<true, true>),
+                       reinterpret_cast<const void*>(&select_small_kernel<false, false>),
+                       reinterpret_cast<const void*>(&select_small_kernel<true, false>),
+                       reinterpret_cast<const void*>(&select_small_kernel<false, true>),
+                       reinterpret_cast<const void*>(&select_small_kernel<true, true>)};
+    const int big = static_cast<int>(SelLayout<kSelCap>::bytes(kMaxLists));
+    const int small = static_cast<int>(SelLayout<kSelCapSmall>::bytes(kMaxLists));
+    const int bytes[] = {big, big, big, big, small, small, small, small};
     hipError_t e = hipSuccess;
-    for (int i = 0; i < 4 && e == hipSuccess; ++i)
+    for (int i = 0; i < 8 && e == hipSuccess; ++i)
         e = hipFuncSetAttribute(k[i], hipFuncAttributeMaxDynamicSharedMemorySize, bytes[i]);
     return e;
 }

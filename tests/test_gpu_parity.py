@@ -306,6 +306,22 @@ def test_variant_batched_full_size(variant):
     check_rows(inp, topk, rows, out, sel, unsel, variant=variant)
 
 
+@pytest.mark.parametrize("flood", [False, True], ids=["sampled", "every-token"])
+def test_variant_bx_many_rows(flood):
+    """Bx on more rows than CUs (9 x 32 = 288): the Bx weights of the
+    two-workgroups-per-CU top-k stage, in LDS and, with every token a
+    candidate (about 8K a row), on its global-memory path."""
+    wl = small(1, batch=9, max_seq=8192 + 132, n_list=96, topk=160)
+    inp = make(wl, seed=23)
+    ctx = context(inp)
+    ctx.set_option(pqhsa.OPT_VARIANT, pqhsa.VARIANT_BX)
+    if flood:
+        ctx.set_option(pqhsa.OPT_THRESHOLD_BIAS, -1_000_000)
+    topk, out, sel, unsel, sc = run(ctx, inp, scores=True)
+    rows = [(b, h) for b in range(wl.batch) for h in (0, 13, 31)]
+    check_rows(inp, topk, rows, out, sel, unsel, sc, variant="Bx")
+
+
 VARIANT_EDGE = {
     "g8": (small(3, batch=2, max_seq=3000, n_q_heads=16, n_kv_heads=2, n_list=16, topk=60), {}),
     "k0": (small(1, max_seq=3000, n_list=16, topk=0), {}),
