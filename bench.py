@@ -352,7 +352,7 @@ def main() -> int:
 
     # the mechanism variants of the background term (Appendix B) on the same
     # context: T drops the background workgroups, C reads one mean per (b, g),
-    # Bx adds a per-row weight kernel and weights the exact rows of T
+    # Bx forms per-list weights in the top-k stage and weights the exact rows of T
     variant_us = {}
     for name, code in (("T", pqhsa.VARIANT_T), ("C", pqhsa.VARIANT_C), ("Bx", pqhsa.VARIANT_BX)):
         ctx.set_option(pqhsa.OPT_VARIANT, code)

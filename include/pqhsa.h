@@ -334,8 +334,8 @@ pqhsa_status pqhsa_index_export(pqhsa_ctx* ctx, int32_t* perm, int32_t* offsets,
  *                             means are the means over R_j);
  *                             PQHSA_VARIANT_BX list j takes the mean of its
  *                             unselected members, (|R_j| v_bar_j - sum of v_i
- *                             over T n R_j) / |B n R_j|, one more kernel after
- *                             the top-k stage. Under
+ *                             over T n R_j) / |B n R_j|, its weights formed
+ *                             by the top-k stage. Under
  *                             PQHSA_VARIANT_T a row whose exact set is empty
  *                             (no sink, no window, k = 0) has no defined
  *                             output: its entries are NaN (0 / 0). Any other
